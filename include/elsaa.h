@@ -1,0 +1,142 @@
+/*
+ * elsaa.h -- C ABI of the ELSAA attention operator on AMD Instinct MI355X (gfx950).
+ *
+ * ELSAA ("Efficient Low-Rank and Sparse Approximation of Attention")
+ * replaces dense softmax attention of one head by two branches and a fusion:
+ *   - a sparse branch (sortLSH, Alg. 4; causal divide-and-conquer, Alg. 5):
+ *     queries and keys are hashed with a sign hash, sorted by bucket, cut
+ *     into equal blocks of b keys, and each query takes exact exp-weighted
+ *     sums over its block: O_s = N_s / (d_s + eps), d_s = sum of e^{z};
+ *   - a low-rank branch (RACE, Alg. 2; causal chunked form, Alg. 3): soft
+ *     hypercube-hash features phi(x) of L tables with 2^gamma buckets give
+ *     O_lr = Num / (Den + eps) and the denominator proxy d_lr = Den;
+ *   - the denominator-aware fusion (Eq. m_sparse, Eq. elsaa_fusion_output,
+ *     log-sum-exp form of Alg. 6):
+ *        m = d_s / (d_s + lambda d_lr + eps),
+ *        O = g_s * m * O_s + g_lr * O_lr.
+ * The backward returns dQ, dK, dV (and optionally the gate gradients) with
+ * the selection held fixed; the paper does not write a backward, it is the
+ * exact gradient of the forward above.
+ *
+ * Tensor layout: Q, K, V, O, dO, dQ, dK, dV are [B, H, N, d_h] contiguous
+ * row-major in the storage dtype (float32 or bfloat16); all accumulation is
+ * float32.  Per-row outputs (lse, d_lr) are float32 [B, H, N].  The hash
+ * projections are float32: W_sort [H, sort_bits, d_h] and
+ * W_race [H, L, race_bits, d_h] with L = r / 2^race_bits, shared across the
+ * batch.  gates is float32 [B, H, N, 2] = (g_sparse, g_lr) or NULL (all 1).
+ *
+ * Memory: every pointer except cfg is a device pointer owned by the caller.
+ * The library never allocates, frees or synchronises: it enqueues kernels on
+ * the given stream and returns; results are valid once the stream has
+ * completed.  `saved` (elsaa_saved_bytes) is written by elsaa_fwd and read
+ * by elsaa_bwd; `workspace` (elsaa_workspace_bytes) is scratch for one call
+ * and may be reused by the next call on the same stream.  Calls that share a
+ * workspace on different streams race.
+ *
+ * Errors: every entry point validates all arguments on the host before any
+ * launch, so a rejected call writes nothing and leaves the stream untouched.
+ * It returns a negative elsaa_status; elsaa_last_error() gives a message
+ * (thread-local, valid until the next call on the same thread).
+ */
+#ifndef ELSAA_H
+#define ELSAA_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    ELSAA_OK = 0,
+    ELSAA_ERR_INVALID_ARG = -1,   /* null pointer, out-of-range value */
+    ELSAA_ERR_UNSUPPORTED = -2,   /* valid for the method, not implemented on the GPU path */
+    ELSAA_ERR_WORKSPACE = -3,     /* saved / workspace buffer smaller than required */
+    ELSAA_ERR_HIP = -4            /* a HIP launch or runtime call failed */
+} elsaa_status;
+
+typedef enum { ELSAA_F32 = 0, ELSAA_BF16 = 1 } elsaa_dtype;
+
+typedef struct {
+    int32_t B, H, N, d_h;   /* batch, heads, sequence length, head dim (64 or 128)          */
+    int32_t k;              /* sortLSH block size b: keys per sorted block, 1 <= k           */
+    int32_t r;              /* RACE features L * 2^race_bits (the low-rank rank)             */
+    int32_t race_bits;      /* gamma, hash bits per RACE table (GPU path: 4)                 */
+    int32_t sort_bits;      /* gamma_sort, sign-hash bits of the sortLSH selector (1..8)      */
+    int32_t n0;             /* causal base length N_0 of Alg. 5; <= 0 selects 2k             */
+    int32_t causal;         /* 0: Alg. 1 / 2 / 4;  1: Alg. 6 / 3 / 5                          */
+    int32_t dtype;          /* elsaa_dtype of Q,K,V,O,dO,dQ,dK,dV                             */
+    float beta;             /* RACE temperature beta > 0 (Alg. 2)                            */
+    float lambda;           /* fusion coefficient lambda >= 0 (Eq. m_sparse)                 */
+    float eps;              /* numerical floor eps > 0                                       */
+    float scale;            /* score scale tau; <= 0 selects 1/sqrt(d_h)                     */
+} elsaa_config;
+
+/* Number of causal recursion levels Lv (0 for non-causal): the smallest Lv
+ * with N / 2^Lv <= n0.  Returns a negative status if some segment longer
+ * than n0 would have odd length (Alg. 5 would pad it with a zero token; the
+ * GPU path does not implement that padding). */
+int elsaa_num_levels(const elsaa_config* cfg);
+
+/* Bytes of the `saved` buffer elsaa_fwd fills and elsaa_bwd reads, and of
+ * the per-call scratch `workspace` (pass 0: elsaa_fwd / elsaa_select,
+ * pass 1: elsaa_bwd).  Validates cfg. */
+int elsaa_saved_bytes(const elsaa_config* cfg, size_t* bytes);
+int elsaa_workspace_bytes(const elsaa_config* cfg, int pass, size_t* bytes);
+
+/* Byte offsets inside `saved` (each 256-byte aligned):
+ *   perm_q, perm_k  int32 sorted index lists (layout as elsaa_select);
+ *   m               float32 [B,H,N] denominator-aware multiplier;
+ *   o_sparse        storage dtype [B,H,N,d_h] sparse-branch output O_s;
+ *   o_lowrank       storage dtype [B,H,N,d_h] low-rank output O_lr. */
+typedef struct {
+    size_t perm_q, perm_k, m, o_sparse, o_lowrank, total;
+} elsaa_saved_layout;
+int elsaa_get_saved_layout(const elsaa_config* cfg, elsaa_saved_layout* out);
+
+/* Selection (Alg. 4 steps Hash / Sort / Partition; per level of Alg. 5).
+ * Hash: bit t of a row x is set iff the float32 fused multiply-add chain
+ * p = fma(W_sort[h][t][e], x[e], p) over e = 0..d_h-1 is > 0; the bucket key
+ * is the position of that bit code in the reflected Gray sequence, so
+ * neighbouring buckets differ in one bit ("sorted Hamming LSH", Sec. 3).
+ * Sort: ascending by (key, token index), ties to the lower index.
+ * Output (int32 token indices within one (b,h)):
+ *   non-causal: perm_q, perm_k [B,H,N]; sorted block t = positions
+ *               [t*k, (t+1)*k) and query block t sees key block t;
+ *   causal:     perm_q, perm_k [B,H,Lv,N/2]; level l lists its 2^l segments
+ *               of length N/2^l in order, each giving its future half's
+ *               queries (perm_q) and its past half's keys (perm_k) sorted. */
+int elsaa_select(const elsaa_config* cfg, const void* Q, const void* K, const float* W_sort,
+                 int32_t* perm_q, int32_t* perm_k, void* workspace, size_t workspace_bytes,
+                 hipStream_t stream);
+
+/* Forward (Alg. 1 / Alg. 6 without the projections).  Writes
+ *   O        [B,H,N,d_h] storage dtype, fused output;
+ *   lse      [B,H,N] float32, log d_sparse (log of the sparse denominator);
+ *   d_lr     [B,H,N] float32, RACE denominator proxy Den;
+ *   saved    selection, m, O_s and O_lr for the backward (elsaa_saved_layout). */
+int elsaa_fwd(const elsaa_config* cfg, const void* Q, const void* K, const void* V,
+              const float* W_sort, const float* W_race, const float* gates,
+              void* O, float* lse, float* d_lr, void* saved, size_t saved_bytes,
+              void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Backward.  dO is the upstream gradient of O; lse, d_lr and saved are what
+ * elsaa_fwd wrote for the same inputs.  Writes dQ, dK, dV [B,H,N,d_h]
+ * (storage dtype) and, when dgates is not NULL, dgates [B,H,N,2] float32
+ * (d/dg_sparse, d/dg_lr).  W_sort is not read (the selection comes from
+ * saved) and may be NULL. */
+int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void* V,
+              const float* W_sort, const float* W_race, const float* gates, const void* dO,
+              const float* lse, const float* d_lr, const void* saved, size_t saved_bytes,
+              void* dQ, void* dK, void* dV, float* dgates,
+              void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+const char* elsaa_status_string(int status);
+const char* elsaa_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ELSAA_H */

@@ -1,0 +1,246 @@
+"""ELSAA attention operator on AMD Instinct MI355X (gfx950).
+
+Thin Python binding of the C-ABI library ``libelsaa.so`` (declared in
+``include/elsaa.h``).  The functions below only marshal arguments: they
+allocate the output, ``saved`` and ``workspace`` buffers with torch on the
+tensors' device, pass raw device pointers and torch's current HIP stream,
+and raise if the library reports an error.  Every step of the operator runs
+in the library's HIP kernels; there is no other code path.  If the library
+has not been built, importing works but every call raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import dataclasses
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libelsaa.so")
+_lib = None
+
+F32, BF16 = 0, 1
+_STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported", -3: "buffer too small", -4: "HIP error"}
+
+
+class ElsaaError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"elsaa error {status} ({_STATUS.get(status, '?')}): {msg}")
+        self.status = status
+
+
+class _Config(C.Structure):
+    _fields_ = [("B", C.c_int32), ("H", C.c_int32), ("N", C.c_int32), ("d_h", C.c_int32),
+                ("k", C.c_int32), ("r", C.c_int32), ("race_bits", C.c_int32),
+                ("sort_bits", C.c_int32), ("n0", C.c_int32), ("causal", C.c_int32),
+                ("dtype", C.c_int32), ("beta", C.c_float), ("lam", C.c_float),
+                ("eps", C.c_float), ("scale", C.c_float)]
+
+
+class _SavedLayout(C.Structure):
+    _fields_ = [("perm_q", C.c_size_t), ("perm_k", C.c_size_t), ("m", C.c_size_t),
+                ("o_sparse", C.c_size_t), ("o_lowrank", C.c_size_t), ("total", C.c_size_t)]
+
+
+@dataclasses.dataclass
+class Config:
+    """Operator settings (names follow the paper; see include/elsaa.h)."""
+    B: int
+    H: int
+    N: int
+    d_h: int
+    k: int                  # sortLSH block size b
+    r: int                  # RACE features L * 2^race_bits
+    causal: bool
+    dtype: str = "bf16"     # storage dtype of Q, K, V, O, dO, dQ, dK, dV
+    race_bits: int = 4
+    sort_bits: int = 5
+    n0: int = 0             # <= 0 -> 2k
+    beta: float = 1.0
+    lam: float = 1.0
+    eps: float = 1e-6
+    scale: float = 0.0      # <= 0 -> 1/sqrt(d_h)
+
+    def c(self) -> _Config:
+        return _Config(self.B, self.H, self.N, self.d_h, self.k, self.r, self.race_bits,
+                       self.sort_bits, self.n0, int(self.causal),
+                       BF16 if self.dtype == "bf16" else F32, self.beta, self.lam, self.eps,
+                       self.scale)
+
+    @property
+    def torch_dtype(self):
+        return torch.bfloat16 if self.dtype == "bf16" else torch.float32
+
+
+def load():
+    """Load libelsaa.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ElsaaError(-4, f"{LIB_PATH} not built; run paper_2607_20214_amd/build.py")
+        lib = C.CDLL(LIB_PATH)
+        P, S = C.c_void_p, C.c_size_t
+        lib.elsaa_num_levels.argtypes = [P]
+        lib.elsaa_saved_bytes.argtypes = [P, C.POINTER(C.c_size_t)]
+        lib.elsaa_workspace_bytes.argtypes = [P, C.c_int, C.POINTER(C.c_size_t)]
+        lib.elsaa_get_saved_layout.argtypes = [P, P]
+        lib.elsaa_select.argtypes = [P, P, P, P, P, P, P, S, P]
+        lib.elsaa_fwd.argtypes = [P, P, P, P, P, P, P, P, P, P, P, S, P, S, P]
+        lib.elsaa_bwd.argtypes = [P, P, P, P, P, P, P, P, P, P, P, S, P, P, P, P, P, S, P]
+        lib.elsaa_status_string.restype = C.c_char_p
+        lib.elsaa_status_string.argtypes = [C.c_int]
+        lib.elsaa_last_error.restype = C.c_char_p
+        _lib = lib
+    return _lib
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise ElsaaError(rc, load().elsaa_last_error().decode())
+
+
+def _p(t: Optional[torch.Tensor]):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream(dev) -> C.c_void_p:
+    return C.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+
+
+def num_levels(cfg: Config) -> int:
+    c = cfg.c()
+    rc = load().elsaa_num_levels(C.byref(c))
+    if rc < 0:
+        _check(rc)
+    return rc
+
+
+def saved_bytes(cfg: Config) -> int:
+    c, n = cfg.c(), C.c_size_t()
+    _check(load().elsaa_saved_bytes(C.byref(c), C.byref(n)))
+    return n.value
+
+
+def workspace_bytes(cfg: Config, backward: bool = False) -> int:
+    c, n = cfg.c(), C.c_size_t()
+    _check(load().elsaa_workspace_bytes(C.byref(c), int(backward), C.byref(n)))
+    return n.value
+
+
+def saved_layout(cfg: Config) -> dict:
+    c, L = cfg.c(), _SavedLayout()
+    _check(load().elsaa_get_saved_layout(C.byref(c), C.byref(L)))
+    return {f: getattr(L, f) for f, _ in _SavedLayout._fields_}
+
+
+def _perm_shape(cfg: Config):
+    if cfg.causal:
+        return (cfg.B, cfg.H, num_levels(cfg), cfg.N // 2)
+    return (cfg.B, cfg.H, cfg.N)
+
+
+def saved_views(cfg: Config, saved: torch.Tensor) -> dict:
+    """Typed views into ``saved``: perm_q, perm_k, m, o_sparse, o_lowrank."""
+    L = saved_layout(cfg)
+    es = 2 if cfg.dtype == "bf16" else 4
+    B, H, N, d = cfg.B, cfg.H, cfg.N, cfg.d_h
+    ps = _perm_shape(cfg)
+    npm = 1
+    for x in ps:
+        npm *= x
+
+    def view(off, count, dtype, shape):
+        nbytes = count * (torch.finfo(dtype).bits // 8 if dtype.is_floating_point else torch.iinfo(dtype).bits // 8)
+        return saved[off:off + nbytes].view(dtype).view(*shape)
+
+    return {
+        "perm_q": view(L["perm_q"], npm, torch.int32, ps),
+        "perm_k": view(L["perm_k"], npm, torch.int32, ps),
+        "m": view(L["m"], B * H * N, torch.float32, (B, H, N)),
+        "o_sparse": view(L["o_sparse"], B * H * N * d, cfg.torch_dtype, (B, H, N, d)),
+        "o_lowrank": view(L["o_lowrank"], B * H * N * d, cfg.torch_dtype, (B, H, N, d)),
+    }
+
+
+def _check_tensor(name, t, shape, dtype, dev):
+    if t.shape != torch.Size(shape) or t.dtype != dtype or not t.is_contiguous() or t.device != dev:
+        raise ValueError(f"{name}: expected contiguous {dtype} {tuple(shape)} on {dev}, "
+                         f"got {t.dtype} {tuple(t.shape)} on {t.device}")
+
+
+def _check_inputs(cfg, q, k, v, w_sort, w_race, gates=None, extra=()):
+    dev = q.device
+    shp = (cfg.B, cfg.H, cfg.N, cfg.d_h)
+    for name, t in (("q", q), ("k", k), ("v", v)) + tuple(extra):
+        _check_tensor(name, t, shp, cfg.torch_dtype, dev)
+    if w_sort is not None:
+        _check_tensor("w_sort", w_sort, (cfg.H, cfg.sort_bits, cfg.d_h), torch.float32, dev)
+    if w_race is not None:
+        _check_tensor("w_race", w_race, (cfg.H, cfg.r >> cfg.race_bits, cfg.race_bits, cfg.d_h),
+                      torch.float32, dev)
+    if gates is not None:
+        _check_tensor("gates", gates, (cfg.B, cfg.H, cfg.N, 2), torch.float32, dev)
+    return dev
+
+
+class Buffers:
+    """Preallocated outputs, saved state and workspaces for repeated calls."""
+
+    def __init__(self, cfg: Config, device, backward: bool = True):
+        B, H, N, d = cfg.B, cfg.H, cfg.N, cfg.d_h
+        dt = cfg.torch_dtype
+        self.o = torch.empty(B, H, N, d, dtype=dt, device=device)
+        self.lse = torch.empty(B, H, N, dtype=torch.float32, device=device)
+        self.d_lr = torch.empty(B, H, N, dtype=torch.float32, device=device)
+        self.saved = torch.empty(saved_bytes(cfg), dtype=torch.uint8, device=device)
+        ws = workspace_bytes(cfg, False)
+        if backward:
+            ws = max(ws, workspace_bytes(cfg, True))
+            self.dq = torch.empty(B, H, N, d, dtype=dt, device=device)
+            self.dk = torch.empty(B, H, N, d, dtype=dt, device=device)
+            self.dv = torch.empty(B, H, N, d, dtype=dt, device=device)
+        self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=device)
+
+
+def select(cfg: Config, q, k, w_sort, workspace: Optional[torch.Tensor] = None):
+    """Sorted index lists (perm_q, perm_k) of the sortLSH selection."""
+    dev = _check_inputs(cfg, q, k, k, w_sort, None)
+    ps = _perm_shape(cfg)
+    pq = torch.empty(ps, dtype=torch.int32, device=dev)
+    pk = torch.empty(ps, dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = torch.empty(max(workspace_bytes(cfg), 256), dtype=torch.uint8, device=dev)
+    c = cfg.c()
+    _check(load().elsaa_select(C.byref(c), _p(q), _p(k), _p(w_sort), _p(pq), _p(pk), _p(workspace),
+                               workspace.numel(), _stream(dev)))
+    return pq, pk
+
+
+def fwd(cfg: Config, q, k, v, w_sort, w_race, gates=None, buffers: Optional[Buffers] = None):
+    """Forward; returns (o, lse, d_lr, saved)."""
+    dev = _check_inputs(cfg, q, k, v, w_sort, w_race, gates)
+    bufs = buffers or Buffers(cfg, dev, backward=False)
+    c = cfg.c()
+    _check(load().elsaa_fwd(C.byref(c), _p(q), _p(k), _p(v), _p(w_sort), _p(w_race), _p(gates),
+                            _p(bufs.o), _p(bufs.lse), _p(bufs.d_lr), _p(bufs.saved),
+                            bufs.saved.numel(), _p(bufs.workspace), bufs.workspace.numel(),
+                            _stream(dev)))
+    return bufs.o, bufs.lse, bufs.d_lr, bufs.saved
+
+
+def bwd(cfg: Config, q, k, v, w_race, do, lse, d_lr, saved, gates=None, want_dgates=False,
+        buffers: Optional[Buffers] = None):
+    """Backward; returns (dq, dk, dv) or (dq, dk, dv, dgates)."""
+    dev = _check_inputs(cfg, q, k, v, None, w_race, gates, extra=(("do", do),))
+    bufs = buffers
+    if bufs is None:
+        bufs = Buffers(cfg, dev, backward=True)
+    dg = torch.empty(cfg.B, cfg.H, cfg.N, 2, dtype=torch.float32, device=dev) if want_dgates else None
+    c = cfg.c()
+    _check(load().elsaa_bwd(C.byref(c), _p(q), _p(k), _p(v), None, _p(w_race), _p(gates), _p(do),
+                            _p(lse), _p(d_lr), _p(saved), saved.numel(), _p(bufs.dq), _p(bufs.dk),
+                            _p(bufs.dv), _p(dg), _p(bufs.workspace), bufs.workspace.numel(),
+                            _stream(dev)))
+    return (bufs.dq, bufs.dk, bufs.dv) + ((dg,) if want_dgates else ())

@@ -1,0 +1,294 @@
+// api.hip -- host side of the C ABI (include/elsaa.h): argument validation,
+// buffer layouts and the launch sequence of each entry point.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "elsaa.h"
+#include "internal.hpp"
+
+namespace elsaa {
+int race_padded_features(int r);
+bool race_fits(int bf16, int D, int r);
+size_t race_state_floats(const Shape& s);
+}  // namespace elsaa
+
+using namespace elsaa;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char* what)
+{
+    return fail(ELSAA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Levels of the causal recursion (Alg. 5): smallest Lv with N / 2^Lv <= n0;
+// -1 when a segment longer than n0 would be odd.
+int levels_of(int64_t N, int64_t n0)
+{
+    int lv = 0;
+    while (N > n0) {
+        if (N & 1) return -1;
+        N >>= 1;
+        ++lv;
+    }
+    return lv;
+}
+
+int validate(const elsaa_config* c, Shape* s)
+{
+    if (!c) return fail(ELSAA_ERR_INVALID_ARG, "cfg is NULL");
+    if (c->B < 1 || c->H < 1 || c->N < 1)
+        return fail(ELSAA_ERR_INVALID_ARG, "B, H, N must be >= 1 (got %d, %d, %d)", c->B, c->H, c->N);
+    if (c->d_h < 1) return fail(ELSAA_ERR_INVALID_ARG, "d_h must be >= 1 (got %d)", c->d_h);
+    if (c->k < 1) return fail(ELSAA_ERR_INVALID_ARG, "k (sortLSH block size) must be >= 1 (got %d)", c->k);
+    if (c->race_bits < 1 || c->race_bits > 12)
+        return fail(ELSAA_ERR_INVALID_ARG, "race_bits must be in [1, 12] (got %d)", c->race_bits);
+    if (c->r < (1 << c->race_bits) || c->r % (1 << c->race_bits))
+        return fail(ELSAA_ERR_INVALID_ARG, "r must be a positive multiple of 2^race_bits (got r=%d)", c->r);
+    if (c->sort_bits < 1 || c->sort_bits > 8)
+        return fail(ELSAA_ERR_INVALID_ARG, "sort_bits must be in [1, 8] (got %d)", c->sort_bits);
+    if (c->causal != 0 && c->causal != 1) return fail(ELSAA_ERR_INVALID_ARG, "causal must be 0 or 1");
+    if (c->dtype != ELSAA_F32 && c->dtype != ELSAA_BF16) return fail(ELSAA_ERR_INVALID_ARG, "unknown dtype %d", c->dtype);
+    if (!(c->beta > 0) || !std::isfinite(c->beta)) return fail(ELSAA_ERR_INVALID_ARG, "beta must be finite and > 0");
+    if (!(c->lambda >= 0) || !std::isfinite(c->lambda)) return fail(ELSAA_ERR_INVALID_ARG, "lambda must be finite and >= 0");
+    if (!(c->eps > 0) || !std::isfinite(c->eps)) return fail(ELSAA_ERR_INVALID_ARG, "eps must be finite and > 0");
+    if (!std::isfinite(c->scale)) return fail(ELSAA_ERR_INVALID_ARG, "scale must be finite");
+    // GPU path limits
+    if (c->d_h != 64 && c->d_h != 128) return fail(ELSAA_ERR_UNSUPPORTED, "d_h must be 64 or 128 (got %d)", c->d_h);
+    if (c->race_bits != 4) return fail(ELSAA_ERR_UNSUPPORTED, "the GPU path implements race_bits = 4 only (got %d)", c->race_bits);
+    if (c->r > 256) return fail(ELSAA_ERR_UNSUPPORTED, "r must be <= 256 (got %d)", c->r);
+    if ((int64_t)c->N > (1 << 26)) return fail(ELSAA_ERR_UNSUPPORTED, "N must be <= 2^26");
+    const int bf16 = c->dtype == ELSAA_BF16;
+    if (!race_fits(bf16, c->d_h, c->r))
+        return fail(ELSAA_ERR_UNSUPPORTED, "r = %d with d_h = %d in float32 exceeds the RACE kernel's LDS", c->r, c->d_h);
+    const int n0 = c->n0 > 0 ? c->n0 : 2 * c->k;
+    int lv = 0, n_leaf = c->N;
+    if (c->causal) {
+        lv = levels_of(c->N, n0);
+        if (lv < 0)
+            return fail(ELSAA_ERR_UNSUPPORTED,
+                        "causal N = %d with n0 = %d needs zero-token padding of an odd segment (not on the GPU path)",
+                        c->N, n0);
+        n_leaf = c->N >> lv;
+        if (n_leaf % 64)
+            return fail(ELSAA_ERR_UNSUPPORTED, "causal leaf length N / 2^Lv = %d must be a multiple of 64", n_leaf);
+    }
+    s->B = c->B; s->H = c->H; s->N = c->N; s->D = c->d_h;
+    s->k = c->k;
+    s->r = c->r; s->L = c->r >> c->race_bits;
+    s->Lp = race_padded_features(c->r) / 16;
+    s->sort_bits = c->sort_bits;
+    s->Lv = lv; s->n_leaf = n_leaf;
+    s->causal = c->causal; s->bf16 = bf16;
+    s->beta = c->beta; s->lambda = c->lambda; s->eps = c->eps;
+    s->tau = c->scale > 0 ? c->scale : 1.0f / std::sqrt((float)c->d_h);
+    // RACE segments: enough workgroups to fill the chip, whole 64-token chunks
+    const int64_t chunks = (c->N + 63) / 64;
+    const int64_t bh = (int64_t)c->B * c->H;
+    int64_t nseg = (512 + bh - 1) / bh;
+    if (nseg > chunks) nseg = chunks;
+    if (nseg < 1) nseg = 1;
+    const int64_t per = (chunks + nseg - 1) / nseg;
+    s->seg_len = (int)(per * 64);
+    s->nseg = (int)((c->N + s->seg_len - 1) / s->seg_len);
+    return ELSAA_OK;
+}
+
+struct SavedLayout {
+    size_t perm_q, perm_k, m, o_s, o_lr, total;
+};
+
+SavedLayout saved_layout(const Shape& s)
+{
+    SavedLayout L;
+    const size_t bh = (size_t)s.B * s.H;
+    const size_t es = s.bf16 ? 2 : 4;
+    size_t off = 0;
+    L.perm_q = off; off = align256(off + bh * s.P() * 4);
+    L.perm_k = off; off = align256(off + bh * s.P() * 4);
+    L.m = off; off = align256(off + bh * s.N * 4);
+    L.o_s = off; off = align256(off + bh * s.N * s.D * es);
+    L.o_lr = off; off = align256(off + bh * s.N * s.D * es);
+    L.total = off;
+    return L;
+}
+
+struct FwdWorkspace {
+    size_t keyq, keyk, states, part_o, part_lse, total;
+};
+
+FwdWorkspace fwd_workspace(const Shape& s)
+{
+    FwdWorkspace W;
+    const size_t bh = (size_t)s.B * s.H;
+    size_t off = 0;
+    W.keyq = off; off = align256(off + bh * s.N);
+    W.keyk = off; off = align256(off + bh * s.N);
+    W.states = off; off = align256(off + race_state_floats(s) * 4);
+    const size_t npart = s.causal ? bh * s.Lv * (size_t)(s.N / 2) : 0;
+    W.part_o = off; off = align256(off + npart * s.D * 4);
+    W.part_lse = off; off = align256(off + npart * 4);
+    W.total = off;
+    return W;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+template <class P>
+P* at(void* base, size_t off) { return (P*)((char*)base + off); }
+
+}  // namespace
+
+extern "C" {
+
+int elsaa_num_levels(const elsaa_config* cfg)
+{
+    Shape s;
+    int rc = validate(cfg, &s);
+    if (rc) return rc;
+    return s.Lv;
+}
+
+int elsaa_saved_bytes(const elsaa_config* cfg, size_t* bytes)
+{
+    Shape s;
+    int rc = validate(cfg, &s);
+    if (rc) return rc;
+    if (!bytes) return fail(ELSAA_ERR_INVALID_ARG, "bytes is NULL");
+    *bytes = saved_layout(s).total;
+    return ELSAA_OK;
+}
+
+int elsaa_workspace_bytes(const elsaa_config* cfg, int pass, size_t* bytes)
+{
+    Shape s;
+    int rc = validate(cfg, &s);
+    if (rc) return rc;
+    if (!bytes) return fail(ELSAA_ERR_INVALID_ARG, "bytes is NULL");
+    if (pass == 0) *bytes = fwd_workspace(s).total;
+    else if (pass == 1) *bytes = fwd_workspace(s).total;
+    else return fail(ELSAA_ERR_INVALID_ARG, "pass must be 0 (forward) or 1 (backward)");
+    return ELSAA_OK;
+}
+
+int elsaa_get_saved_layout(const elsaa_config* cfg, elsaa_saved_layout* out)
+{
+    Shape s;
+    int rc = validate(cfg, &s);
+    if (rc) return rc;
+    if (!out) return fail(ELSAA_ERR_INVALID_ARG, "out is NULL");
+    SavedLayout L = saved_layout(s);
+    out->perm_q = L.perm_q;
+    out->perm_k = L.perm_k;
+    out->m = L.m;
+    out->o_sparse = L.o_s;
+    out->o_lowrank = L.o_lr;
+    out->total = L.total;
+    return ELSAA_OK;
+}
+
+int elsaa_select(const elsaa_config* cfg, const void* Q, const void* K, const float* W_sort,
+                 int32_t* perm_q, int32_t* perm_k, void* workspace, size_t workspace_bytes,
+                 hipStream_t stream)
+{
+    Shape s;
+    int rc = validate(cfg, &s);
+    if (rc) return rc;
+    if (!Q || !K || !W_sort || !perm_q || !perm_k || !workspace)
+        return fail(ELSAA_ERR_INVALID_ARG, "a required pointer is NULL");
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(workspace))
+        return fail(ELSAA_ERR_INVALID_ARG, "Q, K and workspace must be 16-byte aligned");
+    FwdWorkspace W = fwd_workspace(s);
+    if (workspace_bytes < W.keyk + (size_t)s.B * s.H * s.N)
+        return fail(ELSAA_ERR_WORKSPACE, "workspace too small");
+    uint8_t* kq = at<uint8_t>(workspace, W.keyq);
+    uint8_t* kk = at<uint8_t>(workspace, W.keyk);
+    hipError_t e;
+    if ((e = launch_hash(s, Q, W_sort, kq, stream)) != hipSuccess) return hip_fail(e, "hash(Q)");
+    if ((e = launch_hash(s, K, W_sort, kk, stream)) != hipSuccess) return hip_fail(e, "hash(K)");
+    if ((e = launch_sort(s, kq, kk, perm_q, perm_k, stream)) != hipSuccess) return hip_fail(e, "sort");
+    return ELSAA_OK;
+}
+
+int elsaa_fwd(const elsaa_config* cfg, const void* Q, const void* K, const void* V,
+              const float* W_sort, const float* W_race, const float* gates,
+              void* O, float* lse, float* d_lr, void* saved, size_t saved_bytes,
+              void* workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    Shape s;
+    int rc = validate(cfg, &s);
+    if (rc) return rc;
+    if (!Q || !K || !V || !W_sort || !W_race || !O || !lse || !d_lr || !saved || !workspace)
+        return fail(ELSAA_ERR_INVALID_ARG, "a required pointer is NULL");
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O) || !aligned16(saved) ||
+        !aligned16(workspace))
+        return fail(ELSAA_ERR_INVALID_ARG, "Q, K, V, O, saved and workspace must be 16-byte aligned");
+    SavedLayout SL = saved_layout(s);
+    FwdWorkspace W = fwd_workspace(s);
+    if (saved_bytes < SL.total)
+        return fail(ELSAA_ERR_WORKSPACE, "saved buffer too small (%zu < %zu bytes)", saved_bytes, SL.total);
+    if (workspace_bytes < W.total)
+        return fail(ELSAA_ERR_WORKSPACE, "workspace too small (%zu < %zu bytes)", workspace_bytes, W.total);
+    uint8_t* kq = at<uint8_t>(workspace, W.keyq);
+    uint8_t* kk = at<uint8_t>(workspace, W.keyk);
+    int32_t* pq = at<int32_t>(saved, SL.perm_q);
+    int32_t* pk = at<int32_t>(saved, SL.perm_k);
+    float* m = at<float>(saved, SL.m);
+    void* o_s = at<char>(saved, SL.o_s);
+    void* o_lr = at<char>(saved, SL.o_lr);
+    hipError_t e;
+    if ((e = launch_hash(s, Q, W_sort, kq, stream)) != hipSuccess) return hip_fail(e, "hash(Q)");
+    if ((e = launch_hash(s, K, W_sort, kk, stream)) != hipSuccess) return hip_fail(e, "hash(K)");
+    if ((e = launch_sort(s, kq, kk, pq, pk, stream)) != hipSuccess) return hip_fail(e, "sort");
+    if ((e = launch_race_fwd(s, Q, K, V, W_race, at<float>(workspace, W.states), o_lr, d_lr, stream)) != hipSuccess)
+        return hip_fail(e, "race forward");
+    if ((e = launch_sparse_fwd(s, Q, K, V, pq, pk, gates, o_lr, d_lr, at<float>(workspace, W.part_o),
+                               at<float>(workspace, W.part_lse), O, lse, m, o_s, stream)) != hipSuccess)
+        return hip_fail(e, "sparse forward");
+    return ELSAA_OK;
+}
+
+int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void* V,
+              const float* W_sort, const float* W_race, const float* gates, const void* dO,
+              const float* lse, const float* d_lr, const void* saved, size_t saved_bytes,
+              void* dQ, void* dK, void* dV, float* dgates,
+              void* workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    Shape s;
+    int rc = validate(cfg, &s);
+    if (rc) return rc;
+    return fail(ELSAA_ERR_UNSUPPORTED, "backward not built yet");
+}
+
+const char* elsaa_status_string(int status)
+{
+    switch (status) {
+        case ELSAA_OK: return "ok";
+        case ELSAA_ERR_INVALID_ARG: return "invalid argument";
+        case ELSAA_ERR_UNSUPPORTED: return "unsupported on the GPU path";
+        case ELSAA_ERR_WORKSPACE: return "buffer too small";
+        case ELSAA_ERR_HIP: return "HIP error";
+        default: return "unknown status";
+    }
+}
+
+const char* elsaa_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,124 @@
+// common.hpp -- device helpers shared by the ELSAA HIP kernels (gfx950 only).
+//
+// Matrix-core convention used by every kernel (v_mfma_f32_16x16x32_bf16 and,
+// for float32 storage, eight v_mfma_f32_16x16x4_f32 per 32-wide k-step):
+//   * a "k-step" contracts 32 values of k; lane l (0..63) holds, for both
+//     operands, the 8 k-slots 8*(l/16) + j (j = 0..7) of row / column l%16;
+//   * the accumulator tile is 16x16 float32: lane l holds rows 4*(l/16)+i
+//     (i = 0..3) of column l%16.
+// Which physical k each slot maps to does not matter as long as A and B use
+// the same slot order, which is how all kernels build their fragments.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace elsaa {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kWave = 64;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// Round to nearest even; inputs here are finite.
+__device__ __forceinline__ uint16_t f32_to_bf16(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// Storage traits: element type in HBM / LDS and the 8-slot operand fragment.
+struct BF16 {
+    using store_t = uint16_t;
+    using frag_t = bf16x8;
+    static constexpr int bytes = 2;
+    __device__ static __forceinline__ float load(store_t v) { return bf16_to_f32(v); }
+    __device__ static __forceinline__ store_t store(float v) { return f32_to_bf16(v); }
+    __device__ static __forceinline__ f32x4 mma(frag_t a, frag_t b, f32x4 c)
+    {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    }
+    // 8 contiguous elements (16-byte aligned)
+    __device__ static __forceinline__ frag_t ld8(const store_t* p) { return *(const frag_t*)p; }
+    // elements p0[0..3] then p1[0..3] (8-byte aligned each)
+    __device__ static __forceinline__ frag_t ld44(const store_t* p0, const store_t* p1)
+    {
+        bf16x4 a = *(const bf16x4*)p0, b = *(const bf16x4*)p1;
+        return frag_t{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    }
+    __device__ static __forceinline__ frag_t pack(const float* v)
+    {
+        frag_t f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) f[j] = __builtin_bit_cast(__bf16, f32_to_bf16(v[j]));
+        return f;
+    }
+};
+
+struct F32 {
+    using store_t = float;
+    using frag_t = f32x8;
+    static constexpr int bytes = 4;
+    __device__ static __forceinline__ float load(store_t v) { return v; }
+    __device__ static __forceinline__ store_t store(float v) { return v; }
+    __device__ static __forceinline__ f32x4 mma(frag_t a, frag_t b, f32x4 c)
+    {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], b[j], c, 0, 0, 0);
+        return c;
+    }
+    __device__ static __forceinline__ frag_t ld8(const store_t* p)
+    {
+        f32x4 a = *(const f32x4*)p, b = *(const f32x4*)(p + 4);
+        return frag_t{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    }
+    __device__ static __forceinline__ frag_t ld44(const store_t* p0, const store_t* p1)
+    {
+        f32x4 a = *(const f32x4*)p0, b = *(const f32x4*)p1;
+        return frag_t{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    }
+    __device__ static __forceinline__ frag_t pack(const float* v)
+    {
+        frag_t f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) f[j] = v[j];
+        return f;
+    }
+};
+
+// 16-byte global load / store of raw bytes.
+__device__ __forceinline__ uint4 ldg16(const void* p) { return *(const uint4*)p; }
+__device__ __forceinline__ void stg16(void* p, uint4 v) { *(uint4*)p = v; }
+
+__device__ __forceinline__ float wave_max16(float v)   // max over lanes l, l^16, l^32, l^48
+{
+    v = fmaxf(v, __shfl_xor(v, 16));
+    v = fmaxf(v, __shfl_xor(v, 32));
+    return v;
+}
+
+__device__ __forceinline__ float wave_sum16(float v)   // sum over lanes l, l^16, l^32, l^48
+{
+    v += __shfl_xor(v, 16);
+    v += __shfl_xor(v, 32);
+    return v;
+}
+
+__device__ __forceinline__ float row_sum16(float v)    // sum over the 16 lanes of a row group
+{
+    v += __shfl_xor(v, 1);
+    v += __shfl_xor(v, 2);
+    v += __shfl_xor(v, 4);
+    v += __shfl_xor(v, 8);
+    return v;
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+}  // namespace elsaa

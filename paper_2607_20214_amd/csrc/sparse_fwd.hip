@@ -1,0 +1,358 @@
+// sparse_fwd.hip -- sortLSH sparse branch forward and the fusion epilogue.
+//
+// One workgroup = 4 waves = 64 queries (16 per wave); keys stream through
+// LDS in tiles of 64 rows gathered by the sorted index lists (K row-major,
+// V transposed so both MFMA operands read 16 contiguous bytes).  Scores are
+// computed transposed (S^T = K Q^T) so each lane owns one query: the running
+// max and denominator of the online softmax are lane-local plus two
+// cross-row shuffles, and P^T feeds O^T = V^T P^T straight from registers.
+//
+// Three modes share the tile loop:
+//   kBlocks  non-causal Alg. 4: the query tile of sorted positions
+//            [64t, 64t+64) sees the keys of its sorted blocks of size
+//            b' = min(b, N); the epilogue fuses with the RACE output.
+//   kLevels  causal Alg. 5, every level at once: SortLSH(Q_future, K_past)
+//            of each segment; writes a normalised partial (O, log d) per
+//            query, stored by natural query index.
+//   kLeaf    causal Alg. 5 leaf (exact causal attention inside segments of
+//            N / 2^Lv tokens), then merges the level partials of the same
+//            queries by log-sum-exp (MergeLSE) and applies the fusion.
+//
+// Fusion (Eq. m_sparse with the log-sum-exp form of Alg. 6, Eq. fusion):
+//   O_s = N_s / (d_s + eps), m = d_s / (d_s + lambda d_lr + eps),
+//   O = g_s m O_s + g_lr O_lr.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace elsaa {
+
+namespace {
+
+constexpr int kQT = 64;       // queries per workgroup
+constexpr int kKT = 64;       // keys per LDS tile
+constexpr int kThreads = 256;
+constexpr int kPad = 8;       // LDS row padding (elements)
+
+enum Mode { kBlocks = 0, kLevels = 1, kLeaf = 2 };
+
+template <class T, int D>
+struct Smem {
+    typename T::store_t k[kKT][D + kPad];
+    typename T::store_t vt[D][kKT + kPad];
+    int32_t kidx[kKT];
+};
+
+struct Args {
+    const void* Q;
+    const void* K;
+    const void* V;
+    const int32_t* perm_q;
+    const int32_t* perm_k;
+    const float* gates;
+    const void* O_lr;
+    const float* d_lr;
+    float* part_o;
+    float* part_lse;
+    void* O;
+    float* lse;
+    float* m;
+    void* O_s;
+    int H, N, k, Lv, n_leaf;
+    float tau2;      // tau * log2(e)
+    float lambda, eps;
+};
+
+// Key row index inside the 64-key tile held by register i of score
+// sub-tile s for lane group g: sub-tiles 2m and 2m+1 together cover keys
+// 32m..32m+31 so that lane group g holds keys 32m + 8g .. 32m + 8g + 7.
+__device__ __forceinline__ int key_of(int s, int g, int i) { return 32 * (s >> 1) + 8 * g + 4 * (s & 1) + i; }
+// K row fed to A-operand row rho of sub-tile s (the inverse of key_of).
+__device__ __forceinline__ int krow_of(int s, int rho) { return 32 * (s >> 1) + 8 * (rho >> 2) + 4 * (s & 1) + (rho & 3); }
+
+template <class T, int D>
+__device__ __forceinline__ void load_kv(Smem<T, D>& sm, const typename T::store_t* K,
+                                        const typename T::store_t* V)
+{
+    using S = typename T::store_t;
+    constexpr int PER = 16 / T::bytes;   // elements per 16-byte chunk
+    constexpr int CH = D / PER;          // chunks per row
+    for (int it = threadIdx.x; it < kKT * CH; it += kThreads) {
+        const int row = it & (kKT - 1), c = it / kKT;
+        const int tok = sm.kidx[row];
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (tok >= 0) v = ldg16(K + (size_t)tok * D + c * PER);
+        *(uint4*)&sm.k[row][c * PER] = v;
+    }
+    for (int it = threadIdx.x; it < (kKT / 2) * CH; it += kThreads) {
+        const int p = it & (kKT / 2 - 1), c = it / (kKT / 2);
+        const int t0 = sm.kidx[2 * p], t1 = sm.kidx[2 * p + 1];
+        uint4 a = make_uint4(0, 0, 0, 0), b = make_uint4(0, 0, 0, 0);
+        if (t0 >= 0) a = ldg16(V + (size_t)t0 * D + c * PER);
+        if (t1 >= 0) b = ldg16(V + (size_t)t1 * D + c * PER);
+        const S* ea = (const S*)&a;
+        const S* eb = (const S*)&b;
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            S* dst = &sm.vt[c * PER + j][2 * p];
+            dst[0] = ea[j];
+            dst[1] = eb[j];
+        }
+    }
+}
+
+template <class T, int D, int MODE>
+__global__ __launch_bounds__(kThreads) void sparse_fwd_kernel(Args a)
+{
+    using S = typename T::store_t;
+    using F = typename T::frag_t;
+    constexpr int KS = D / 32;   // k-steps over the head dim
+    constexpr int DT = D / 16;   // 16-wide tiles of the head dim
+    __shared__ Smem<T, D> sm;
+
+    const int h = blockIdx.y, b = blockIdx.z;
+    const size_t bh = (size_t)b * a.H + h;
+    const int N = a.N;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int g = lane >> 4, qq = lane & 15;
+    const S* Q = (const S*)a.Q + bh * N * D;
+    const S* K = (const S*)a.K + bh * N * D;
+    const S* V = (const S*)a.V + bh * N * D;
+
+    // ---- which queries, which keys -------------------------------------
+    int level = 0, seg = 0, half = N;   // kLevels: level / segment / half length
+    int qpos;                           // position of this lane's query in its sorted list
+    int qtok;                           // token index of this lane's query (-1 = none)
+    int kbeg, kend;                     // key positions [kbeg, kend) scanned by the tile
+    int bq = 1;                         // block size b' (kBlocks / kLevels)
+    const int32_t* klist = nullptr;     // sorted key list (kBlocks / kLevels)
+    const int tile = blockIdx.x;
+    if (MODE == kBlocks) {
+        bq = min(a.k, N);
+        const int p0 = tile * kQT;
+        qpos = p0 + 16 * w + qq;
+        qtok = qpos < N ? a.perm_q[bh * N + qpos] : -1;
+        const int plast = min(p0 + kQT, N) - 1;
+        kbeg = (p0 / bq) * bq;
+        kend = min(N, (plast / bq + 1) * bq);
+        klist = a.perm_k + bh * N;
+    } else if (MODE == kLevels) {
+        const int per_level = (N / 2) / kQT;
+        level = tile / per_level;
+        const int t = tile - level * per_level;
+        half = N >> (level + 1);
+        seg = (t * kQT) / half;
+        const int p0 = t * kQT - seg * half;
+        bq = min(a.k, half);
+        qpos = p0 + 16 * w + qq;
+        const size_t lbase = (bh * a.Lv + level) * (size_t)(N / 2) + (size_t)seg * half;
+        qtok = a.perm_q[lbase + qpos];
+        const int plast = p0 + kQT - 1;
+        kbeg = (p0 / bq) * bq;
+        kend = min(half, (plast / bq + 1) * bq);
+        klist = a.perm_k + lbase;
+    } else {
+        const int q0 = tile * kQT;
+        qtok = q0 + 16 * w + qq;
+        qpos = qtok;
+        kbeg = (q0 / a.n_leaf) * a.n_leaf;
+        kend = q0 + kQT;
+    }
+    const int blk_lo = (MODE == kLeaf) ? 0 : (qpos / bq) * bq;
+    const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), blk_lo + bq);
+
+    // ---- this lane's query fragments (B operand of S^T = K Q^T) ---------
+    F qf[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        if (qtok >= 0) qf[ks] = T::ld8(Q + (size_t)qtok * D + 32 * ks + 8 * g);
+        else {
+            float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+            qf[ks] = T::pack(z);
+        }
+    }
+
+    float m_run = -INFINITY, l_run = 0.f;
+    f32x4 acc[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) acc[dt] = f32x4{0, 0, 0, 0};
+
+    for (int k0 = kbeg; k0 < kend; k0 += kKT) {
+        __syncthreads();
+        if (threadIdx.x < kKT) {
+            const int p = k0 + threadIdx.x;
+            int tok = -1;
+            if (p < kend) tok = (MODE == kLeaf) ? p : klist[p];
+            sm.kidx[threadIdx.x] = tok;
+        }
+        __syncthreads();
+        load_kv<T, D>(sm, K, V);
+        __syncthreads();
+
+        // S^T for the 64 keys of the tile (4 sub-tiles of 16 keys)
+        f32x4 st[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            st[s] = f32x4{0, 0, 0, 0};
+            const int kr = krow_of(s, qq);
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                st[s] = T::mma(T::ld8(&sm.k[kr][32 * ks + 8 * g]), qf[ks], st[s]);
+        }
+        // scale to log2 units and mask
+        float tmax = -INFINITY;
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int p = k0 + key_of(s, g, i);
+                bool ok = p < kend && qtok >= 0;
+                if (MODE == kLeaf) ok = ok && p <= qtok;
+                else ok = ok && p >= blk_lo && p < blk_hi;
+                const float v = ok ? st[s][i] * a.tau2 : -INFINITY;
+                st[s][i] = v;
+                tmax = fmaxf(tmax, v);
+            }
+        tmax = wave_max16(tmax);
+        const float m_new = fmaxf(m_run, tmax);
+        const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+        const float corr = fast_exp2(m_run - m_use);
+        float psum = 0.f;
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float p = fast_exp2(st[s][i] - m_use);
+                st[s][i] = p;
+                psum += p;
+            }
+        psum = wave_sum16(psum);
+        l_run = l_run * corr + psum;
+        m_run = m_new;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) acc[dt] *= corr;
+        // O^T += V^T P^T over two 32-key k-steps
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+            float pv[8];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                pv[j] = st[2 * kk][j];
+                pv[4 + j] = st[2 * kk + 1][j];
+            }
+            const F pf = T::pack(pv);
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+                acc[dt] = T::mma(T::ld8(&sm.vt[16 * dt + qq][32 * kk + 8 * g]), pf, acc[dt]);
+        }
+    }
+
+    if (MODE == kLevels) {
+        if (qtok < 0) return;
+        // compact slot of query qtok among the future halves of this level
+        const int s2 = qtok / (2 * half);
+        const size_t slot = (bh * a.Lv + level) * (size_t)(N / 2) + (size_t)s2 * half +
+                            (qtok - s2 * 2 * half - half);
+        const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+        float* po = a.part_o + slot * D;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+            *(f32x4*)(po + 16 * dt + 4 * g) = acc[dt] * inv;
+        if (g == 0) a.part_lse[slot] = (m_run + __log2f(l_run)) * kLn2;
+        return;
+    }
+
+    if (MODE == kLeaf) {
+        // merge the partial of every level whose future half holds this tile
+        const int q0 = blockIdx.x * kQT;
+        for (int l = 0; l < a.Lv; ++l) {
+            const int hl = N >> (l + 1);
+            if (((q0 / hl) & 1) == 0) continue;
+            const int s2 = qtok / (2 * hl);
+            const size_t slot = (bh * a.Lv + l) * (size_t)(N / 2) + (size_t)s2 * hl +
+                                (qtok - s2 * 2 * hl - hl);
+            const float pl = a.part_lse[slot] * kLog2e;
+            const float m_new = fmaxf(m_run, pl);
+            const float c_old = fast_exp2(m_run - m_new), c_new = fast_exp2(pl - m_new);
+            const float* po = a.part_o + slot * D;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                const f32x4 v = *(const f32x4*)(po + 16 * dt + 4 * g);
+                acc[dt] = acc[dt] * c_old + v * c_new;
+            }
+            l_run = l_run * c_old + c_new;
+            m_run = m_new;
+        }
+    }
+
+    // ---- fusion epilogue (kBlocks, kLeaf) --------------------------------
+    if (qtok < 0) return;
+    const size_t row = bh * N + qtok;
+    const float lse_nat = (m_run + __log2f(l_run)) * kLn2;       // log d_s
+    const float inv_den = 1.f / (l_run + a.eps * fast_exp2(-m_run)); // 1 / (d_s + eps), rescaled
+    const float dl = a.d_lr[row];
+    const float mf = 1.f / (1.f + __expf(__logf(a.lambda * dl + a.eps) - lse_nat));
+    float gs = 1.f, gl = 1.f;
+    if (a.gates) {
+        gs = a.gates[row * 2 + 0];
+        gl = a.gates[row * 2 + 1];
+    }
+    const S* olr = (const S*)a.O_lr + row * D;
+    S* out = (S*)a.O + row * D;
+    S* os = (S*)a.O_s + row * D;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+        const int c0 = 16 * dt + 4 * g;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float o_s = acc[dt][i] * inv_den;
+            const float o = gs * mf * o_s + gl * T::load(olr[c0 + i]);
+            out[c0 + i] = T::store(o);
+            os[c0 + i] = T::store(o_s);
+        }
+    }
+    if (g == 0) {
+        a.lse[row] = lse_nat;
+        a.m[row] = mf;
+    }
+}
+
+template <class T, int D>
+hipError_t launch_t(const Shape& s, const Args& a, hipStream_t st)
+{
+    if (!s.causal) {
+        dim3 grid((s.N + kQT - 1) / kQT, s.H, s.B);
+        hipLaunchKernelGGL((sparse_fwd_kernel<T, D, kBlocks>), grid, dim3(kThreads), 0, st, a);
+        return hipGetLastError();
+    }
+    if (s.Lv > 0) {
+        dim3 grid(s.Lv * (s.N / 2) / kQT, s.H, s.B);
+        hipLaunchKernelGGL((sparse_fwd_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    dim3 grid(s.N / kQT, s.H, s.B);
+    hipLaunchKernelGGL((sparse_fwd_kernel<T, D, kLeaf>), grid, dim3(kThreads), 0, st, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_sparse_fwd(const Shape& s, const void* Q, const void* K, const void* V,
+                             const int32_t* perm_q, const int32_t* perm_k, const float* gates,
+                             const void* O_lr, const float* d_lr, float* part_o, float* part_lse,
+                             void* O, float* lse, float* m, void* O_s, hipStream_t st)
+{
+    Args a;
+    a.Q = Q; a.K = K; a.V = V;
+    a.perm_q = perm_q; a.perm_k = perm_k;
+    a.gates = gates; a.O_lr = O_lr; a.d_lr = d_lr;
+    a.part_o = part_o; a.part_lse = part_lse;
+    a.O = O; a.lse = lse; a.m = m; a.O_s = O_s;
+    a.H = s.H; a.N = s.N; a.k = s.k; a.Lv = s.Lv; a.n_leaf = s.n_leaf;
+    a.tau2 = s.tau * kLog2e;
+    a.lambda = s.lambda; a.eps = s.eps;
+    if (s.bf16) return s.D == 64 ? launch_t<BF16, 64>(s, a, st) : launch_t<BF16, 128>(s, a, st);
+    return s.D == 64 ? launch_t<F32, 64>(s, a, st) : launch_t<F32, 128>(s, a, st);
+}
+
+}  // namespace elsaa

@@ -1,0 +1,75 @@
+"""Helpers of the GPU parity tests: run the HIP library and the CPU oracle
+on the same seeded inputs and compare them.
+
+Tolerances: selected indices bit-exact; floating outputs
+max|gpu - oracle| / max|oracle| per head <= 1e-4 (float32 storage) or
+2e-2 (bfloat16 storage with float32 accumulation)."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+import oracle
+import paper_2607_20214_amd as E
+from paper_2607_20214_amd import workloads as W
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def cfg_of(w: W.Workload, **over) -> E.Config:
+    kw = dict(B=w.B, H=w.H, N=w.N, d_h=w.d, k=w.k, r=w.r, causal=w.causal, dtype=w.dtype,
+              race_bits=w.race_bits, sort_bits=w.sort_bits, n0=w.n0 or 0)
+    kw.update(over)
+    return E.Config(**kw)
+
+
+def head_cfg_of(cfg: E.Config) -> oracle.HeadCfg:
+    return oracle.HeadCfg(N=cfg.N, d=cfg.d_h, k=cfg.k, r=cfg.r, causal=cfg.causal,
+                          race_bits=cfg.race_bits, sort_bits=cfg.sort_bits,
+                          n0=cfg.n0 if cfg.n0 > 0 else None, beta=cfg.beta, lam=cfg.lam,
+                          eps=cfg.eps, scale=cfg.scale)
+
+
+def to_dev(x: np.ndarray, dtype) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(x)).to("cuda").to(dtype).contiguous()
+
+
+def run_gpu_fwd(cfg: E.Config, inp: dict, gates=None):
+    dt = cfg.torch_dtype
+    q, k, v = (to_dev(inp[n], dt) for n in ("Q", "K", "V"))
+    ws = to_dev(inp["W_sort"], torch.float32)
+    wr = to_dev(inp["W_race"], torch.float32)
+    g = None if gates is None else to_dev(gates, torch.float32)
+    o, lse, dlr, saved = E.fwd(cfg, q, k, v, ws, wr, gates=g)
+    torch.cuda.synchronize()
+    sv = E.saved_views(cfg, saved)
+    out = {"O": o, "lse": lse, "d_lr": dlr, "m": sv["m"], "O_s": sv["o_sparse"],
+           "O_lr": sv["o_lowrank"], "perm_q": sv["perm_q"], "perm_k": sv["perm_k"]}
+    return {k_: t.float().cpu().numpy() if t.is_floating_point() else t.cpu().numpy()
+            for k_, t in out.items()}, (q, k, v, ws, wr, g, saved, lse, dlr)
+
+
+def rel_err(a, b) -> float:
+    den = float(np.max(np.abs(b)))
+    return float(np.max(np.abs(a.astype(np.float64) - b))) / (den if den > 0 else 1.0)
+
+
+def compare_heads(name, got, want, tol, heads=None):
+    """max|got - want| / max|want| for each (b, h) slice; returns the worst."""
+    worst = 0.0
+    B, H = got.shape[:2]
+    for b in range(B):
+        for h in range(H):
+            if heads is not None and (b, h) not in heads:
+                continue
+            e = rel_err(got[b, h], want[b, h])
+            worst = max(worst, e)
+            assert e <= tol, f"{name} (b={b}, h={h}): relative error {e:.3e} > {tol:.1e}"
+    return worst

@@ -1,0 +1,106 @@
+"""GPU parity of the forward (selection, both branches, fusion) against the oracle."""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import TOL, cfg_of, compare_heads, head_cfg_of, rel_err, run_gpu_fwd, say
+from paper_2607_20214_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def _w(name, B, H, N, d, k, r, causal, dtype, recipe="iid", seed=50, **kw):
+    qs = d ** -0.25 if recipe == "iid" else 1.0
+    return W.Workload(name, B, H, N, d, k, r, causal, dtype, recipe=recipe, qk_scale=qs, seed=seed,
+                      centres=kw.pop("centres", 16), **kw)
+
+
+SMALL = [
+    _w("nc-f32-512", 1, 1, 512, 64, 32, 32, False, "f32"),
+    _w("nc-bf16-ragged-300", 1, 2, 300, 64, 64, 64, False, "bf16", recipe="clustered"),
+    _w("nc-bf16-d128-1000", 2, 1, 1000, 128, 128, 128, False, "bf16"),
+    _w("nc-bf16-k48-ragged-777", 1, 2, 777, 64, 48, 48, False, "bf16"),
+    _w("nc-bf16-dense-k256-200", 1, 1, 200, 128, 256, 16, False, "bf16"),
+    _w("c-bf16-d128-1024", 1, 2, 1024, 128, 64, 128, True, "bf16"),
+    _w("c-bf16-d64-2048-clustered", 1, 2, 2048, 64, 128, 64, True, "bf16", recipe="clustered"),
+    _w("c-f32-d64-512", 1, 1, 512, 64, 32, 32, True, "f32"),
+    _w("c-f32-d128-512", 1, 1, 512, 128, 32, 64, True, "f32"),
+    _w("c-bf16-leaf-only-256", 2, 1, 256, 64, 128, 48, True, "bf16"),
+    _w("c-bf16-r256-1024", 1, 1, 1024, 128, 128, 256, True, "bf16", recipe="mixed", centres=8),
+    _w("c-bf16-n0-3x-768", 1, 1, 768, 64, 128, 64, True, "bf16"),
+]
+
+
+def _check_case(w, gates=None, lam=1.0, heads=None, row_mask=None):
+    cfg = cfg_of(w, lam=lam)
+    inp = W.make_inputs(w, with_grad=False)
+    say(f"[fwd] {w.name}: B={w.B} H={w.H} N={w.N} d={w.d} k={w.k} r={w.r} causal={w.causal} {w.dtype}")
+    got, _ = run_gpu_fwd(cfg, inp, gates)
+    tol = TOL[w.dtype]
+    hc = head_cfg_of(cfg)
+    errs = {}
+    for b in range(w.B):
+        for h in range(w.H):
+            if heads is not None and (b, h) not in heads:
+                continue
+            args = (inp["Q"][b, h], inp["K"][b, h], inp["V"][b, h], inp["W_sort"][h], inp["W_race"][h])
+            pq, pk = oracle.select(hc, *args[:2], args[3])
+            assert np.array_equal(got["perm_q"][b, h], pq), f"perm_q (b={b}, h={h})"
+            assert np.array_equal(got["perm_k"][b, h], pk), f"perm_k (b={b}, h={h})"
+            ref = oracle.forward(hc, *args, gates=None if gates is None else gates[b, h],
+                                 row_mask=row_mask)
+            rows = slice(None) if row_mask is None else (row_mask > 0)
+            for name in ("O", "O_s", "O_lr", "d_lr", "m"):
+                r_ = rows if name not in ("O_lr", "d_lr") else slice(None)
+                e = rel_err(got[name][b, h][r_], ref[name][r_])
+                errs[name] = max(errs.get(name, 0.0), e)
+                assert e <= tol, f"{name} (b={b}, h={h}): {e:.3e} > {tol}"
+            e = float(np.max(np.abs(got["lse"][b, h][rows] - ref["lse"][rows])))
+            errs["lse(abs)"] = max(errs.get("lse(abs)", 0.0), e)
+            assert e <= tol, f"lse (b={b}, h={h}): {e:.3e}"
+    say("   errors:", {k: f"{v:.2e}" for k, v in errs.items()})
+
+
+@pytest.mark.parametrize("w", SMALL, ids=[w.name for w in SMALL])
+def test_forward_small(w):
+    _check_case(w)
+
+
+def test_forward_gates_and_lambda():
+    w = _w("c-bf16-gates", 1, 2, 1024, 64, 64, 64, True, "bf16", seed=51)
+    _check_case(w, gates=W.make_gates(w), lam=0.37)
+    w2 = _w("nc-f32-gates", 1, 1, 512, 64, 32, 32, False, "f32", seed=52)
+    _check_case(w2, gates=W.make_gates(w2), lam=0.0)
+
+
+def test_forward_tiny_fp32_workload():
+    _check_case(W.TINY_FP32)
+
+
+def test_forward_clustered_4k_workload():
+    _check_case(W.CLUSTERED_4K, heads={(0, 0), (1, 7), (0, 3)})
+
+
+def test_forward_causal_16k_workload_sampled_heads():
+    _check_case(W.CAUSAL_16K, heads={(0, 0), (0, 15)})
+
+
+def test_forward_causal_64k_mixed_workload_sampled_rows():
+    w = W.CAUSAL_64K_MIXED
+    mask = np.zeros(w.N, np.uint8)
+    rng = np.random.default_rng(5)
+    mask[rng.choice(w.N, 300, replace=False)] = 1
+    mask[:64] = 1
+    mask[-64:] = 1
+    _check_case(w, heads={(0, 0), (0, 7)}, row_mask=mask)
+
+
+def test_forward_is_deterministic():
+    w = _w("c-bf16-det", 1, 2, 2048, 128, 128, 128, True, "bf16", seed=53)
+    cfg = cfg_of(w)
+    inp = W.make_inputs(w, with_grad=False)
+    say(f"[fwd-det] {w.name}")
+    a, _ = run_gpu_fwd(cfg, inp)
+    b, _ = run_gpu_fwd(cfg, inp)
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
