@@ -89,10 +89,14 @@ int elsaa_workspace_bytes(const elsaa_config* cfg, int pass, size_t* bytes);
 /* Byte offsets inside `saved` (each 256-byte aligned):
  *   perm_q, perm_k  int32 sorted index lists (layout as elsaa_select);
  *   m               float32 [B,H,N] denominator-aware multiplier;
- *   o_sparse        storage dtype [B,H,N,d_h] sparse-branch output O_s;
- *   o_lowrank       storage dtype [B,H,N,d_h] low-rank output O_lr. */
+ *   o_sparse        float32 [B,H,N,d_h] sparse-branch output O_s;
+ *   o_lowrank       float32 [B,H,N,d_h] low-rank output O_lr (both kept in float32:
+ *                   the backward's <dO, O_s> and <dO, O_lr> cancel against
+ *                   <dO, V_j> terms);
+ *   u_q, u_k        float32 [B,H,N,P] RACE projections u = W_race x of the Q and K
+ *                   rows (P = 4 L rounded up to 8, 16, 32 or 64; padded tables 0). */
 typedef struct {
-    size_t perm_q, perm_k, m, o_sparse, o_lowrank, total;
+    size_t perm_q, perm_k, m, o_sparse, o_lowrank, u_q, u_k, total;
 } elsaa_saved_layout;
 int elsaa_get_saved_layout(const elsaa_config* cfg, elsaa_saved_layout* out);
 
@@ -116,7 +120,8 @@ int elsaa_select(const elsaa_config* cfg, const void* Q, const void* K, const fl
  *   O        [B,H,N,d_h] storage dtype, fused output;
  *   lse      [B,H,N] float32, log d_sparse (log of the sparse denominator);
  *   d_lr     [B,H,N] float32, RACE denominator proxy Den;
- *   saved    selection, m, O_s and O_lr for the backward (elsaa_saved_layout). */
+ *   saved    selection, m, O_s, O_lr and the RACE projections for the backward
+ *            (elsaa_saved_layout). */
 int elsaa_fwd(const elsaa_config* cfg, const void* Q, const void* K, const void* V,
               const float* W_sort, const float* W_race, const float* gates,
               void* O, float* lse, float* d_lr, void* saved, size_t saved_bytes,

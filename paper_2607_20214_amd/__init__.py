@@ -41,7 +41,8 @@ class _Config(C.Structure):
 
 class _SavedLayout(C.Structure):
     _fields_ = [("perm_q", C.c_size_t), ("perm_k", C.c_size_t), ("m", C.c_size_t),
-                ("o_sparse", C.c_size_t), ("o_lowrank", C.c_size_t), ("total", C.c_size_t)]
+                ("o_sparse", C.c_size_t), ("o_lowrank", C.c_size_t), ("u_q", C.c_size_t),
+                ("u_k", C.c_size_t), ("total", C.c_size_t)]
 
 
 @dataclasses.dataclass
@@ -144,7 +145,6 @@ def _perm_shape(cfg: Config):
 def saved_views(cfg: Config, saved: torch.Tensor) -> dict:
     """Typed views into ``saved``: perm_q, perm_k, m, o_sparse, o_lowrank."""
     L = saved_layout(cfg)
-    es = 2 if cfg.dtype == "bf16" else 4
     B, H, N, d = cfg.B, cfg.H, cfg.N, cfg.d_h
     ps = _perm_shape(cfg)
     npm = 1
@@ -159,8 +159,8 @@ def saved_views(cfg: Config, saved: torch.Tensor) -> dict:
         "perm_q": view(L["perm_q"], npm, torch.int32, ps),
         "perm_k": view(L["perm_k"], npm, torch.int32, ps),
         "m": view(L["m"], B * H * N, torch.float32, (B, H, N)),
-        "o_sparse": view(L["o_sparse"], B * H * N * d, cfg.torch_dtype, (B, H, N, d)),
-        "o_lowrank": view(L["o_lowrank"], B * H * N * d, cfg.torch_dtype, (B, H, N, d)),
+        "o_sparse": view(L["o_sparse"], B * H * N * d, torch.float32, (B, H, N, d)),
+        "o_lowrank": view(L["o_lowrank"], B * H * N * d, torch.float32, (B, H, N, d)),
     }
 
 

@@ -8,12 +8,6 @@
 #include "elsaa.h"
 #include "internal.hpp"
 
-namespace elsaa {
-int race_padded_features(int r);
-bool race_fits(int bf16, int D, int r);
-size_t race_state_floats(const Shape& s);
-}  // namespace elsaa
-
 using namespace elsaa;
 
 namespace {
@@ -76,8 +70,6 @@ int validate(const elsaa_config* c, Shape* s)
     if (c->r > 256) return fail(ELSAA_ERR_UNSUPPORTED, "r must be <= 256 (got %d)", c->r);
     if ((int64_t)c->N > (1 << 26)) return fail(ELSAA_ERR_UNSUPPORTED, "N must be <= 2^26");
     const int bf16 = c->dtype == ELSAA_BF16;
-    if (!race_fits(bf16, c->d_h, c->r))
-        return fail(ELSAA_ERR_UNSUPPORTED, "r = %d with d_h = %d in float32 exceeds the RACE kernel's LDS", c->r, c->d_h);
     const int n0 = c->n0 > 0 ? c->n0 : 2 * c->k;
     int lv = 0, n_leaf = c->N;
     if (c->causal) {
@@ -108,24 +100,28 @@ int validate(const elsaa_config* c, Shape* s)
     const int64_t per = (chunks + nseg - 1) / nseg;
     s->seg_len = (int)(per * 64);
     s->nseg = (int)((c->N + s->seg_len - 1) / s->seg_len);
+    if (!race_fwd_fits(*s) || !race_bwd_fits(*s))
+        return fail(ELSAA_ERR_UNSUPPORTED, "r = %d with d_h = %d in %s exceeds the RACE kernels' LDS", c->r,
+                    c->d_h, bf16 ? "bf16" : "float32");
     return ELSAA_OK;
 }
 
 struct SavedLayout {
-    size_t perm_q, perm_k, m, o_s, o_lr, total;
+    size_t perm_q, perm_k, m, o_s, o_lr, u_q, u_k, total;
 };
 
 SavedLayout saved_layout(const Shape& s)
 {
     SavedLayout L;
     const size_t bh = (size_t)s.B * s.H;
-    const size_t es = s.bf16 ? 2 : 4;
     size_t off = 0;
     L.perm_q = off; off = align256(off + bh * s.P() * 4);
     L.perm_k = off; off = align256(off + bh * s.P() * 4);
     L.m = off; off = align256(off + bh * s.N * 4);
-    L.o_s = off; off = align256(off + bh * s.N * s.D * es);
-    L.o_lr = off; off = align256(off + bh * s.N * s.D * es);
+    L.o_s = off; off = align256(off + bh * s.N * s.D * 4);   // float32: the backward's Delta cancels against it
+    L.o_lr = off; off = align256(off + bh * s.N * s.D * 4);   // float32, same reason (dDen)
+    L.u_q = off; off = align256(off + bh * s.N * race_proj_stride(s) * 4);
+    L.u_k = off; off = align256(off + bh * s.N * race_proj_stride(s) * 4);
     L.total = off;
     return L;
 }
@@ -145,6 +141,30 @@ FwdWorkspace fwd_workspace(const Shape& s)
     const size_t npart = s.causal ? bh * s.Lv * (size_t)(s.N / 2) : 0;
     W.part_o = off; off = align256(off + npart * s.D * 4);
     W.part_lse = off; off = align256(off + npart * 4);
+    W.total = off;
+    return W;
+}
+
+struct BwdWorkspace {
+    size_t rs, states_f, states_b, dq_lr, dk_lr, dv_lr, part_dq, part_dk, part_dv, total;
+};
+
+BwdWorkspace bwd_workspace(const Shape& s)
+{
+    BwdWorkspace W;
+    const size_t bh = (size_t)s.B * s.H;
+    const size_t bhn = bh * s.N;
+    const size_t npart = s.causal ? bh * s.Lv * (size_t)(s.N / 2) : 0;
+    size_t off = 0;
+    W.rs = off; off = align256(off + 5 * bhn * 4);
+    W.states_f = off; off = align256(off + race_state_floats(s) * 4);
+    W.states_b = off; off = align256(off + race_state_floats(s) * 4);
+    W.dq_lr = off; off = align256(off + bhn * s.D * 4);
+    W.dk_lr = off; off = align256(off + bhn * s.D * 4);
+    W.dv_lr = off; off = align256(off + bhn * s.D * 4);
+    W.part_dq = off; off = align256(off + npart * s.D * 4);
+    W.part_dk = off; off = align256(off + npart * s.D * 4);
+    W.part_dv = off; off = align256(off + npart * s.D * 4);
     W.total = off;
     return W;
 }
@@ -183,7 +203,7 @@ int elsaa_workspace_bytes(const elsaa_config* cfg, int pass, size_t* bytes)
     if (rc) return rc;
     if (!bytes) return fail(ELSAA_ERR_INVALID_ARG, "bytes is NULL");
     if (pass == 0) *bytes = fwd_workspace(s).total;
-    else if (pass == 1) *bytes = fwd_workspace(s).total;
+    else if (pass == 1) *bytes = bwd_workspace(s).total;
     else return fail(ELSAA_ERR_INVALID_ARG, "pass must be 0 (forward) or 1 (backward)");
     return ELSAA_OK;
 }
@@ -200,6 +220,8 @@ int elsaa_get_saved_layout(const elsaa_config* cfg, elsaa_saved_layout* out)
     out->m = L.m;
     out->o_sparse = L.o_s;
     out->o_lowrank = L.o_lr;
+    out->u_q = L.u_q;
+    out->u_k = L.u_k;
     out->total = L.total;
     return ELSAA_OK;
 }
@@ -221,8 +243,8 @@ int elsaa_select(const elsaa_config* cfg, const void* Q, const void* K, const fl
     uint8_t* kq = at<uint8_t>(workspace, W.keyq);
     uint8_t* kk = at<uint8_t>(workspace, W.keyk);
     hipError_t e;
-    if ((e = launch_hash(s, Q, W_sort, kq, stream)) != hipSuccess) return hip_fail(e, "hash(Q)");
-    if ((e = launch_hash(s, K, W_sort, kk, stream)) != hipSuccess) return hip_fail(e, "hash(K)");
+    if ((e = launch_project(s, Q, W_sort, nullptr, kq, nullptr, stream)) != hipSuccess) return hip_fail(e, "hash(Q)");
+    if ((e = launch_project(s, K, W_sort, nullptr, kk, nullptr, stream)) != hipSuccess) return hip_fail(e, "hash(K)");
     if ((e = launch_sort(s, kq, kk, perm_q, perm_k, stream)) != hipSuccess) return hip_fail(e, "sort");
     return ELSAA_OK;
 }
@@ -251,13 +273,15 @@ int elsaa_fwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     int32_t* pq = at<int32_t>(saved, SL.perm_q);
     int32_t* pk = at<int32_t>(saved, SL.perm_k);
     float* m = at<float>(saved, SL.m);
-    void* o_s = at<char>(saved, SL.o_s);
-    void* o_lr = at<char>(saved, SL.o_lr);
+    float* o_s = at<float>(saved, SL.o_s);
+    float* o_lr = at<float>(saved, SL.o_lr);
+    float* uq = at<float>(saved, SL.u_q);
+    float* uk = at<float>(saved, SL.u_k);
     hipError_t e;
-    if ((e = launch_hash(s, Q, W_sort, kq, stream)) != hipSuccess) return hip_fail(e, "hash(Q)");
-    if ((e = launch_hash(s, K, W_sort, kk, stream)) != hipSuccess) return hip_fail(e, "hash(K)");
+    if ((e = launch_project(s, Q, W_sort, W_race, kq, uq, stream)) != hipSuccess) return hip_fail(e, "project(Q)");
+    if ((e = launch_project(s, K, W_sort, W_race, kk, uk, stream)) != hipSuccess) return hip_fail(e, "project(K)");
     if ((e = launch_sort(s, kq, kk, pq, pk, stream)) != hipSuccess) return hip_fail(e, "sort");
-    if ((e = launch_race_fwd(s, Q, K, V, W_race, at<float>(workspace, W.states), o_lr, d_lr, stream)) != hipSuccess)
+    if ((e = launch_race_fwd(s, uq, uk, V, at<float>(workspace, W.states), o_lr, d_lr, stream)) != hipSuccess)
         return hip_fail(e, "race forward");
     if ((e = launch_sparse_fwd(s, Q, K, V, pq, pk, gates, o_lr, d_lr, at<float>(workspace, W.part_o),
                                at<float>(workspace, W.part_lse), O, lse, m, o_s, stream)) != hipSuccess)
@@ -274,7 +298,41 @@ int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     Shape s;
     int rc = validate(cfg, &s);
     if (rc) return rc;
-    return fail(ELSAA_ERR_UNSUPPORTED, "backward not built yet");
+    (void)W_sort;   // the selection is read from saved
+    if (!Q || !K || !V || !W_race || !dO || !lse || !d_lr || !saved || !dQ || !dK || !dV || !workspace)
+        return fail(ELSAA_ERR_INVALID_ARG, "a required pointer is NULL");
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(dO) || !aligned16(saved) ||
+        !aligned16(dQ) || !aligned16(dK) || !aligned16(dV) || !aligned16(workspace))
+        return fail(ELSAA_ERR_INVALID_ARG, "Q, K, V, dO, dQ, dK, dV, saved and workspace must be 16-byte aligned");
+    SavedLayout SL = saved_layout(s);
+    BwdWorkspace W = bwd_workspace(s);
+    if (saved_bytes < SL.total)
+        return fail(ELSAA_ERR_WORKSPACE, "saved buffer too small (%zu < %zu bytes)", saved_bytes, SL.total);
+    if (workspace_bytes < W.total)
+        return fail(ELSAA_ERR_WORKSPACE, "workspace too small (%zu < %zu bytes)", workspace_bytes, W.total);
+    void* sv = const_cast<void*>(saved);
+    const int32_t* pq = at<int32_t>(sv, SL.perm_q);
+    const int32_t* pk = at<int32_t>(sv, SL.perm_k);
+    const float* m = at<float>(sv, SL.m);
+    const float* o_s = at<float>(sv, SL.o_s);
+    const float* o_lr = at<float>(sv, SL.o_lr);
+    const float* uq = at<float>(sv, SL.u_q);
+    const float* uk = at<float>(sv, SL.u_k);
+    float* rs = at<float>(workspace, W.rs);
+    float* dq_lr = at<float>(workspace, W.dq_lr);
+    float* dk_lr = at<float>(workspace, W.dk_lr);
+    float* dv_lr = at<float>(workspace, W.dv_lr);
+    hipError_t e;
+    if ((e = launch_bwd_rows(s, dO, o_s, o_lr, m, lse, d_lr, gates, rs, dgates, stream)) != hipSuccess)
+        return hip_fail(e, "backward row scalars");
+    if ((e = launch_race_bwd(s, uq, uk, V, dO, W_race, rs, at<float>(workspace, W.states_f),
+                             at<float>(workspace, W.states_b), dq_lr, dk_lr, dv_lr, stream)) != hipSuccess)
+        return hip_fail(e, "race backward");
+    if ((e = launch_sparse_bwd(s, Q, K, V, dO, pq, pk, rs, dq_lr, dk_lr, dv_lr,
+                               at<float>(workspace, W.part_dq), at<float>(workspace, W.part_dk),
+                               at<float>(workspace, W.part_dv), dQ, dK, dV, stream)) != hipSuccess)
+        return hip_fail(e, "sparse backward");
+    return ELSAA_OK;
 }
 
 const char* elsaa_status_string(int status)

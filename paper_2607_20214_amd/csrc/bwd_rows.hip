@@ -1,0 +1,90 @@
+// bwd_rows.hip -- per-row scalars of the backward.
+//
+// For u = dO_i, with O = g_s m O_s + g_lr O_lr, m = d_s / D, D = d_s + lambda Den + eps,
+// O_s = N_s / (d_s + eps), O_lr = Num / (Den + eps):
+//   dm    = g_s <O_s, u>                      (dm / d log d_s = m (1 - m))
+//   sc_s  = g_s m                             (dO_s = sc_s u)
+//   Delta = sc_s <u, O_s> - dm m (1 - m)(d_s + eps) / d_s
+//   sc_lr = g_lr / (Den + eps)                (dNum = sc_lr u)
+//   dDen  = -g_lr <u, O_lr> / (Den + eps) - dm m lambda / D
+//   dg_s  = m <O_s, u>,  dg_lr = <O_lr, u>
+// Stored as rs[f][BHN] with f = 0: log2(d_s + eps), 1: Delta, 2: sc_s,
+// 3: sc_lr, 4: dDen.  16 lanes per row; O_s and O_lr are float32.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace elsaa {
+
+namespace {
+
+template <class T, int D>
+__global__ __launch_bounds__(256) void bwd_rows_kernel(const typename T::store_t* __restrict__ dO,
+                                                       const float* __restrict__ Os,
+                                                       const float* __restrict__ Olr,
+                                                       const float* __restrict__ m,
+                                                       const float* __restrict__ lse,
+                                                       const float* __restrict__ dlr,
+                                                       const float* __restrict__ gates,
+                                                       float* __restrict__ rs, float* __restrict__ dg,
+                                                       size_t BHN, float lambda, float eps)
+{
+    constexpr int PL = D / 16;   // elements per lane
+    const size_t row = (size_t)blockIdx.x * 16 + threadIdx.x / 16;
+    const int sub = threadIdx.x & 15;
+    if (row >= BHN) return;   // whole 16-lane groups leave together
+    float uos = 0.f, uol = 0.f;
+    const size_t base = row * D + sub * PL;
+#pragma unroll
+    for (int e = 0; e < PL; ++e) {
+        const float u = T::load(dO[base + e]);
+        uos += u * Os[base + e];
+        uol += u * Olr[base + e];
+    }
+    uos = row_sum16(uos);
+    uol = row_sum16(uol);
+    if (sub != 0) return;
+    const float gs = gates ? gates[row * 2] : 1.f;
+    const float gl = gates ? gates[row * 2 + 1] : 1.f;
+    const float mi = m[row], ls = lse[row], den = dlr[row];
+    const float rel = eps * __expf(fminf(-ls, 80.f));   // eps / d_s
+    const float dm = gs * uos;
+    const float scs = gs * mi;
+    const float delta = scs * uos - dm * mi * (1.f - mi) * (1.f + rel);
+    const float inv_den = 1.f / (den + eps);
+    const float Dtot = __expf(fminf(ls, 80.f)) + lambda * den + eps;
+    const float dden = -gl * uol * inv_den - dm * mi * lambda / Dtot;
+    rs[row] = (ls + log1pf(rel)) * kLog2e;
+    rs[BHN + row] = delta;
+    rs[2 * BHN + row] = scs;
+    rs[3 * BHN + row] = gl * inv_den;
+    rs[4 * BHN + row] = dden;
+    if (dg) {
+        dg[row * 2] = mi * uos;
+        dg[row * 2 + 1] = uol;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_bwd_rows(const Shape& s, const void* dO, const float* Os, const float* Olr,
+                           const float* m, const float* lse, const float* dlr, const float* gates,
+                           float* rs, float* dgates, hipStream_t st)
+{
+    const size_t BHN = (size_t)s.B * s.H * s.N;
+    dim3 grid((unsigned)((BHN + 15) / 16));
+#define ELSAA_LAUNCH(T_, D_)                                                                       \
+    hipLaunchKernelGGL((bwd_rows_kernel<T_, D_>), grid, dim3(256), 0, st,                          \
+                       (const T_::store_t*)dO, Os, Olr, m, \
+                       lse, dlr, gates, rs, dgates, BHN, s.lambda, s.eps)
+    if (s.bf16) {
+        if (s.D == 64) ELSAA_LAUNCH(BF16, 64);
+        else ELSAA_LAUNCH(BF16, 128);
+    } else {
+        if (s.D == 64) ELSAA_LAUNCH(F32, 64);
+        else ELSAA_LAUNCH(F32, 128);
+    }
+#undef ELSAA_LAUNCH
+    return hipGetLastError();
+}
+
+}  // namespace elsaa

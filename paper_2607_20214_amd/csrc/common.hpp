@@ -59,6 +59,17 @@ struct BF16 {
         for (int j = 0; j < 8; ++j) f[j] = __builtin_bit_cast(__bf16, f32_to_bf16(v[j]));
         return f;
     }
+    // v = hi + lo to about 2^-16 relative (both bf16): float32-accurate operand
+    static constexpr bool kSplit = true;
+    __device__ static __forceinline__ void split(const float* v, frag_t& hi, frag_t& lo)
+    {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const uint16_t h = f32_to_bf16(v[j]);
+            hi[j] = __builtin_bit_cast(__bf16, h);
+            lo[j] = __builtin_bit_cast(__bf16, f32_to_bf16(v[j] - bf16_to_f32(h)));
+        }
+    }
 };
 
 struct F32 {
@@ -90,7 +101,24 @@ struct F32 {
         for (int j = 0; j < 8; ++j) f[j] = v[j];
         return f;
     }
+    static constexpr bool kSplit = false;   // float32 operands are exact
+    __device__ static __forceinline__ void split(const float* v, frag_t& hi, frag_t& lo)
+    {
+        hi = pack(v);
+        lo = hi;
+    }
 };
+
+// a x (b_hi + b_lo): product with an operand kept in float32 accuracy
+template <class T>
+__device__ __forceinline__ f32x4 mma_split(typename T::frag_t a, const float* b, f32x4 c)
+{
+    typename T::frag_t hi, lo;
+    T::split(b, hi, lo);
+    c = T::mma(a, hi, c);
+    if (T::kSplit) c = T::mma(a, lo, c);
+    return c;
+}
 
 // 16-byte global load / store of raw bytes.
 __device__ __forceinline__ uint4 ldg16(const void* p) { return *(const uint4*)p; }
@@ -120,5 +148,13 @@ __device__ __forceinline__ float row_sum16(float v)    // sum over the 16 lanes 
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Row order of a 64-row tile fed through four 16-row score sub-tiles so that
+// the accumulators can be reused as a 32-wide k-step operand: register i of
+// sub-tile s in lane group g holds tile row key_of(s, g, i), and sub-tiles
+// 2m, 2m+1 together give lane group g the rows 32m + 8g .. 32m + 8g + 7.
+__device__ __forceinline__ int key_of(int s, int g, int i) { return 32 * (s >> 1) + 8 * g + 4 * (s & 1) + i; }
+// Tile row fed to operand row rho of sub-tile s (the inverse of key_of).
+__device__ __forceinline__ int krow_of(int s, int rho) { return 32 * (s >> 1) + 8 * (rho >> 2) + 4 * (s & 1) + (rho & 3); }
 
 }  // namespace elsaa

@@ -22,21 +22,45 @@ struct Shape {
     int64_t P() const { return causal ? (int64_t)Lv * (N / 2) : (int64_t)N; }  // perm length per (b,h)
 };
 
-// selection: hash keys then per-segment stable counting sort
-hipError_t launch_hash(const Shape& s, const void* X, const float* W_sort, uint8_t* keys,
-                       hipStream_t st);
+// selection: hash keys (and the RACE projections U = W_race x when W_race
+// is not null, [BH][N][race_proj_stride]) then per-segment stable counting sort
+hipError_t launch_project(const Shape& s, const void* X, const float* W_sort, const float* W_race,
+                          uint8_t* keys, float* U, hipStream_t st);
 hipError_t launch_sort(const Shape& s, const uint8_t* keyq, const uint8_t* keyk, int32_t* perm_q,
                        int32_t* perm_k, hipStream_t st);
 
-// RACE low-rank branch forward: segment states, scan, readout
-hipError_t launch_race_fwd(const Shape& s, const void* Q, const void* K, const void* V,
-                           const float* W_race, float* states, void* O_lr, float* d_lr,
-                           hipStream_t st);
+// RACE low-rank branch
+int race_padded_features(int r);            // r rounded up to 32, 64, 128 or 256
+int race_proj_stride(const Shape& s);        // floats per row of U (padded 4 * tables)
+size_t race_state_floats(const Shape& s);    // floats of one set of segment states
+bool race_fwd_fits(const Shape& s);          // kernels' LDS fits for this dtype / d / r
+bool race_bwd_fits(const Shape& s);
+// segment states S = mul * sum phi(u) (scale * val)', A = mul * sum aw phi(u);
+// scan_mode 0: total in every segment, 1: exclusive prefix, 2: exclusive suffix
+hipError_t launch_race_states(const Shape& s, const float* U, const void* Val, const float* vscale,
+                              const float* aw, float mul, float* states, int scan_mode, hipStream_t st);
+hipError_t launch_race_fwd(const Shape& s, const float* Uq, const float* Uk, const void* V,
+                           float* states, float* O_lr, float* d_lr, hipStream_t st);
+hipError_t launch_race_bwd(const Shape& s, const float* Uq, const float* Uk, const void* V,
+                           const void* dO, const float* W_race, const float* rs,
+                           float* states_f, float* states_b, float* dq_lr, float* dk_lr,
+                           float* dv_lr, hipStream_t st);
 
 // sortLSH sparse branch forward + fusion epilogue
 hipError_t launch_sparse_fwd(const Shape& s, const void* Q, const void* K, const void* V,
                              const int32_t* perm_q, const int32_t* perm_k, const float* gates,
-                             const void* O_lr, const float* d_lr, float* part_o, float* part_lse,
-                             void* O, float* lse, float* m, void* O_s, hipStream_t st);
+                             const float* O_lr, const float* d_lr, float* part_o, float* part_lse,
+                             void* O, float* lse, float* m, float* O_s, hipStream_t st);
+
+// backward: per-row scalars rs[5][BHN] (log2(d_s+eps), Delta, sc_s, sc_lr, dDen)
+hipError_t launch_bwd_rows(const Shape& s, const void* dO, const float* Os, const float* Olr,
+                           const float* m, const float* lse, const float* dlr, const float* gates,
+                           float* rs, float* dgates, hipStream_t st);
+// sparse backward; adds the float32 low-rank parts and writes dQ, dK, dV
+hipError_t launch_sparse_bwd(const Shape& s, const void* Q, const void* K, const void* V,
+                             const void* dO, const int32_t* perm_q, const int32_t* perm_k,
+                             const float* rs, const float* dq_lr, const float* dk_lr,
+                             const float* dv_lr, float* part_dq, float* part_dk, float* part_dv,
+                             void* dQ, void* dK, void* dV, hipStream_t st);
 
 }  // namespace elsaa

@@ -1,0 +1,553 @@
+// race_bwd.hip -- backward of the RACE low-rank branch (Alg. 2 / Alg. 3 differentiated).
+//
+// With dNum_i = g_lr dO_i / (Den_i + eps) and dDen_i (row scalars of the
+// backward preprocess), and V~_j = [V_j, 1], dN~_i = [dNum_i, dDen_i]:
+//   dphi(q_i) = (1/L) sum_{j <= i} <dN~_i, V~_j> phi(k_j)          (kernel LB1, forward time)
+//   dphi(k_j) = (1/L) sum_{i >= j} <dN~_i, V~_j> phi(q_i)          (kernel LB2, reverse time)
+//   dV_j      = (1/L) sum_{i >= j} <phi(q_i), phi(k_j)> dNum_i      (kernel LB3, reverse time)
+// (non-causal: all i, j).  Each is a linear-attention pass over 64-token
+// chunks with a running state: LB1 reads S = sum phi(k) V', A = sum phi(k)
+// (the forward's segment prefix states); LB2 and LB3 read the suffix states
+// dS = (1/L) sum phi(q) dNum', dA = (1/L) sum phi(q) dDen.  LB1 and LB2
+// contract their state over d, so each wave owns a quarter of the features;
+// LB3 contracts over the features, so each wave owns a quarter of d.
+// dphi is chained through phi = prod sigmoid(2 beta v t), t = tanh(W x) to
+// du, and dQ (dK) = du W on MFMA.  W and the running states enter the MFMAs
+// split into bf16 hi + lo parts (float32 accuracy): their products cancel
+// against the dDen terms.  Outputs are float32 [BH][N][D] parts the sparse
+// backward adds to its own.
+#include "internal.hpp"
+#include "race_common.hpp"
+
+namespace elsaa {
+
+using namespace race;
+
+namespace {
+
+struct LbArgs {
+    const float* Uq;        // projections of Q rows [BH][N][RP/4]
+    const float* Uk;        // projections of K rows
+    const void* V;
+    const void* dO;
+    const float* W;
+    const float* rs;        // row scalars (sc_lr at 3*BHN, dDen at 4*BHN)
+    const float* states;    // LB1: forward prefix states; LB2/LB3: backward suffix states
+    float* out;             // float32 [BH][N][D]
+    int H, N, L, seg_len, nseg, causal;
+    size_t BHN;
+    float two_beta, beta, inv_L;
+};
+
+template <class T, int D, int RP>
+struct Lb1Smem {
+    using S = typename T::store_t;
+    S wt[D][w_kdim<RP>() + kPad];  // W' = W_hi' + W_lo'
+    S wl[T::bytes == 2 ? D : 1][w_kdim<RP>() + kPad];   // (no low part for float32)
+    S vt[D][kC + kPad];            // V chunk transposed
+    S dn[kC][D + kPad];            // dNum chunk, rows
+    S pkt[RP][kC + kPad];          // Phi_K transposed
+    S gg[kC][kC + kPad];           // G[i][j] = <dNum_i, V_j> + dDen_i, j <= i
+    float ts[kC][RP / 4];          // tanh(W q) of the chunk's queries
+    S du[kC][w_kdim<RP>() + kPad];
+    float dden[kC];
+};
+
+template <class T, int D, int RP>
+struct Lb2Smem {
+    using S = typename T::store_t;
+    S wt[D][w_kdim<RP>() + kPad];  // W' = W_hi' + W_lo'
+    S wl[T::bytes == 2 ? D : 1][w_kdim<RP>() + kPad];   // (no low part for float32)
+    S vr[kC][D + kPad];            // V chunk, rows
+    S dnt[D][kC + kPad];           // dNum / L chunk, transposed
+    S pqt[RP][kC + kPad];          // Phi_Q transposed
+    S ggt[kC][kC + kPad];          // G'[j][i] / L, i >= j
+    float ts[kC][RP / 4];          // tanh(W k) of the chunk's keys
+    S du[kC][w_kdim<RP>() + kPad];
+    float dden[kC];
+};
+
+template <class T, int D, int RP>
+struct Lb3Smem {
+    using S = typename T::store_t;
+    S dnt[D][kC + kPad];           // dNum / L chunk, transposed
+    S pk[kC][RP + kPad];           // Phi_K rows
+    S pq[kC][RP + kPad];           // Phi_Q rows
+    S pqt[RP][kC + kPad];          // Phi_Q transposed
+    S mt[kC][kC + kPad];           // M'[j][i] = <phi(k_j), phi(q_i)>, i >= j
+};
+
+template <class T, int D, int RP>
+constexpr bool bwd_fits()
+{
+    return sizeof(Lb1Smem<T, D, RP>) <= kMaxLds && sizeof(Lb2Smem<T, D, RP>) <= kMaxLds &&
+           sizeof(Lb3Smem<T, D, RP>) <= kMaxLds;
+}
+
+// du [64 rows][p] x (W_hi + W_lo) [p][D] -> float32 rows [16w, 16w + 16) of out (all D)
+template <class T, int D, int RP>
+__device__ __forceinline__ void du_times_w(const typename T::store_t (*du)[w_kdim<RP>() + kPad],
+                                           const typename T::store_t (*wt)[w_kdim<RP>() + kPad],
+                                           const typename T::store_t (*wl)[w_kdim<RP>() + kPad],
+                                           float* out, int t0, int N)
+{
+    constexpr int DT = D / 16, KP = w_kdim<RP>() / 32;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int g = lane >> 4, col = lane & 15;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+        f32x4 acc = {0, 0, 0, 0};
+#pragma unroll
+        for (int kp = 0; kp < KP; ++kp) {
+            const auto df = T::ld8(&du[16 * w + col][32 * kp + 8 * g]);
+            acc = T::mma(df, T::ld8(&wt[16 * dt + col][32 * kp + 8 * g]), acc);
+            if (T::bytes == 2) acc = T::mma(df, T::ld8(&wl[16 * dt + col][32 * kp + 8 * g]), acc);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int tok = t0 + 16 * w + 4 * g + i;
+            if (tok < N) out[(size_t)tok * D + 16 * dt + col] = acc[i];
+        }
+    }
+}
+
+// ---------------------------------------------------------------- LB1: dQ
+template <class T, int D, int RP>
+__global__ __launch_bounds__(kThreads) void race_dq_kernel(LbArgs a)
+{
+    using St = typename T::store_t;
+    using F = typename T::frag_t;
+    constexpr int DT = D / 16, KS = D / 32, FT = RP / 16, NFT = (FT + 3) / 4;
+    __shared__ Lb1Smem<T, D, RP> sm;
+    const int seg = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+    const size_t bh = (size_t)b * a.H + h;
+    const float* Uq = a.Uq + bh * a.N * (RP / 4);
+    const float* Uk = a.Uk + bh * a.N * (RP / 4);
+    const St* V = (const St*)a.V + bh * a.N * D;
+    const St* dO = (const St*)a.dO + bh * a.N * D;
+    const float* sclr = a.rs + 3 * a.BHN + bh * a.N;
+    const float* dden = a.rs + 4 * a.BHN + bh * a.N;
+    float* out = a.out + bh * a.N * D;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int g = lane >> 4, col = lane & 15;
+
+    load_wt<T, D, w_kdim<RP>()>(sm.wt, sm.wl, a.W + (size_t)h * a.L * 4 * D, a.L);
+    for (int it = threadIdx.x; it < kC * (w_kdim<RP>() + kPad); it += kThreads)
+        (&sm.du[0][0])[it] = T::store(0.f);
+    // state S'[d][f] for the wave's features f = 16 (w + 4j) + col, and A[f]
+    f32x4 St_[NFT][DT];
+    float ar[NFT];
+    const float* st_in = a.states + (bh * a.nseg + seg) * (size_t)(RP * D + RP);
+#pragma unroll
+    for (int j = 0; j < NFT; ++j) {
+        const int ft = w + 4 * j;
+        ar[j] = ft < FT ? st_in[RP * D + 16 * ft + col] : 0.f;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                St_[j][dt][i] = ft < FT ? st_in[(size_t)(16 * ft + col) * D + 16 * dt + 4 * g + i] : 0.f;
+    }
+
+    const int t_beg = seg * a.seg_len, t_end = min(a.N, t_beg + a.seg_len);
+    for (int t0 = t_beg; t0 < t_end; t0 += kC) {
+        __syncthreads();
+        stage_r<T, D>(sm.dn, dO, t0, a.N, sclr);
+        if (threadIdx.x < kC) sm.dden[threadIdx.x] = (t0 + threadIdx.x < a.N) ? dden[t0 + threadIdx.x] : 0.f;
+        features<T, RP>(Uq, t0, a.N, a.L, a.two_beta, nullptr, nullptr, sm.ts);
+        if (a.causal) {
+            stage_t<T, D>(sm.vt, V, t0, a.N);
+            features<T, RP>(Uk, t0, a.N, a.L, a.two_beta, nullptr, sm.pkt, nullptr);
+        }
+        __syncthreads();
+        if (a.causal) {
+            // G rows [16w, 16w + 16): <dNum_i, V_j> + dDen_i for j <= i
+            for (int kt = 0; kt < 4; ++kt) {
+                f32x4 acc = {0, 0, 0, 0};
+                if (kt <= w) {
+                    const int tok = t0 + 16 * kt + col;
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks) {
+                        F vf;
+                        if (tok < a.N) vf = T::ld8(V + (size_t)tok * D + 32 * ks + 8 * g);
+                        else {
+                            float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                            vf = T::pack(z);
+                        }
+                        acc = T::mma(T::ld8(&sm.dn[16 * w + col][32 * ks + 8 * g]), vf, acc);
+                    }
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int qi = 16 * w + 4 * g + i, kj = 16 * kt + col;
+                    sm.gg[qi][kj] = T::store(kj <= qi ? acc[i] + sm.dden[qi] : 0.f);
+                }
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < NFT; ++j) {
+            const int ft = w + 4 * j;
+            if (ft >= FT) break;
+            for (int qt = 0; qt < 4; ++qt) {
+                f32x4 acc = {0, 0, 0, 0};
+#pragma unroll
+                for (int ds = 0; ds < KS; ++ds) {
+                    float sv[8];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        sv[i] = St_[j][2 * ds][i];
+                        sv[4 + i] = St_[j][2 * ds + 1][i];
+                    }
+                    acc = mma_split<T>(T::ld44(&sm.dn[16 * qt + col][32 * ds + 4 * g], &sm.dn[16 * qt + col][32 * ds + 16 + 4 * g]),
+                                       sv, acc);
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[i] += ar[j] * sm.dden[16 * qt + 4 * g + i];
+                if (a.causal) {
+#pragma unroll
+                    for (int kk = 0; kk < 2; ++kk)
+                        acc = T::mma(T::ld8(&sm.gg[16 * qt + col][32 * kk + 8 * g]),
+                                     T::ld8(&sm.pkt[16 * ft + col][32 * kk + 8 * g]), acc);
+                }
+                acc *= a.inv_L;
+                chain_rule<T, RP>(acc, qt, ft, a.L, a.beta, sm.ts, sm.du);
+            }
+        }
+        __syncthreads();
+        du_times_w<T, D, RP>(sm.du, sm.wt, sm.wl, out, t0, a.N);
+        if (a.causal) {
+            // S' += V' Phi_K (chunk), A += Phi_K' 1
+#pragma unroll
+            for (int j = 0; j < NFT; ++j) {
+                const int ft = w + 4 * j;
+                if (ft >= FT) break;
+#pragma unroll
+                for (int kk = 0; kk < 2; ++kk) {
+                    const F bf = T::ld8(&sm.pkt[16 * ft + col][32 * kk + 8 * g]);
+#pragma unroll
+                    for (int dt = 0; dt < DT; ++dt)
+                        St_[j][dt] = T::mma(T::ld8(&sm.vt[16 * dt + col][32 * kk + 8 * g]), bf, St_[j][dt]);
+                }
+                float s = 0.f;
+#pragma unroll
+                for (int k = 0; k < 16; ++k) s += T::load(sm.pkt[16 * ft + col][16 * g + k]);
+                ar[j] += wave_sum16(s);
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------- LB2: dK
+template <class T, int D, int RP>
+__global__ __launch_bounds__(kThreads) void race_dk_kernel(LbArgs a)
+{
+    using St = typename T::store_t;
+    using F = typename T::frag_t;
+    constexpr int DT = D / 16, KS = D / 32, FT = RP / 16, NFT = (FT + 3) / 4;
+    __shared__ Lb2Smem<T, D, RP> sm;
+    const int seg = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+    const size_t bh = (size_t)b * a.H + h;
+    const float* Uq = a.Uq + bh * a.N * (RP / 4);
+    const float* Uk = a.Uk + bh * a.N * (RP / 4);
+    const St* V = (const St*)a.V + bh * a.N * D;
+    const St* dO = (const St*)a.dO + bh * a.N * D;
+    const float* sclr = a.rs + 3 * a.BHN + bh * a.N;
+    const float* dden = a.rs + 4 * a.BHN + bh * a.N;
+    float* out = a.out + bh * a.N * D;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int g = lane >> 4, col = lane & 15;
+
+    load_wt<T, D, w_kdim<RP>()>(sm.wt, sm.wl, a.W + (size_t)h * a.L * 4 * D, a.L);
+    for (int it = threadIdx.x; it < kC * (w_kdim<RP>() + kPad); it += kThreads)
+        (&sm.du[0][0])[it] = T::store(0.f);
+    f32x4 St_[NFT][DT];
+    float ar[NFT];
+    const float* st_in = a.states + (bh * a.nseg + seg) * (size_t)(RP * D + RP);
+#pragma unroll
+    for (int j = 0; j < NFT; ++j) {
+        const int ft = w + 4 * j;
+        ar[j] = ft < FT ? st_in[RP * D + 16 * ft + col] : 0.f;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                St_[j][dt][i] = ft < FT ? st_in[(size_t)(16 * ft + col) * D + 16 * dt + 4 * g + i] : 0.f;
+    }
+
+    const int t_beg = seg * a.seg_len, t_end = min(a.N, t_beg + a.seg_len);
+    const int nch = (t_end - t_beg + kC - 1) / kC;
+    for (int c = nch - 1; c >= 0; --c) {
+        const int t0 = t_beg + c * kC;
+        __syncthreads();
+        stage_r<T, D>(sm.vr, V, t0, a.N);
+        if (threadIdx.x < kC) sm.dden[threadIdx.x] = (t0 + threadIdx.x < a.N) ? dden[t0 + threadIdx.x] : 0.f;
+        features<T, RP>(Uk, t0, a.N, a.L, a.two_beta, nullptr, nullptr, sm.ts);
+        if (a.causal) {
+            stage_t<T, D>(sm.dnt, dO, t0, a.N, sclr, a.inv_L);
+            features<T, RP>(Uq, t0, a.N, a.L, a.two_beta, nullptr, sm.pqt, nullptr);
+        }
+        __syncthreads();
+        if (a.causal) {
+            // G' rows j in [16w, 16w + 16): (<V_j, dNum_i> + dDen_i) / L for i >= j
+            for (int it = 0; it < 4; ++it) {
+                f32x4 acc = {0, 0, 0, 0};
+                if (it >= w) {
+                    const int tok = t0 + 16 * it + col;
+                    const float sc = tok < a.N ? sclr[tok] : 0.f;
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks) {
+                        float v8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                        if (tok < a.N) {
+                            const F raw = T::ld8(dO + (size_t)tok * D + 32 * ks + 8 * g);
+#pragma unroll
+                            for (int e = 0; e < 8; ++e) v8[e] = (float)raw[e] * sc;
+                        }
+                        acc = T::mma(T::ld8(&sm.vr[16 * w + col][32 * ks + 8 * g]), T::pack(v8), acc);
+                    }
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int kj = 16 * w + 4 * g + i, qi = 16 * it + col;
+                    sm.ggt[kj][qi] = T::store(qi >= kj ? (acc[i] + sm.dden[qi]) * a.inv_L : 0.f);
+                }
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < NFT; ++j) {
+            const int ft = w + 4 * j;
+            if (ft >= FT) break;
+            for (int kt = 0; kt < 4; ++kt) {
+                f32x4 acc = {0, 0, 0, 0};
+#pragma unroll
+                for (int ds = 0; ds < KS; ++ds) {
+                    float sv[8];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        sv[i] = St_[j][2 * ds][i];
+                        sv[4 + i] = St_[j][2 * ds + 1][i];
+                    }
+                    acc = mma_split<T>(T::ld44(&sm.vr[16 * kt + col][32 * ds + 4 * g], &sm.vr[16 * kt + col][32 * ds + 16 + 4 * g]),
+                                       sv, acc);
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[i] += ar[j];
+                if (a.causal) {
+#pragma unroll
+                    for (int kk = 0; kk < 2; ++kk)
+                        acc = T::mma(T::ld8(&sm.ggt[16 * kt + col][32 * kk + 8 * g]),
+                                     T::ld8(&sm.pqt[16 * ft + col][32 * kk + 8 * g]), acc);
+                }
+                chain_rule<T, RP>(acc, kt, ft, a.L, a.beta, sm.ts, sm.du);
+            }
+        }
+        __syncthreads();
+        du_times_w<T, D, RP>(sm.du, sm.wt, sm.wl, out, t0, a.N);
+        if (a.causal) {
+            // dS' += (dNum / L)' Phi_Q (chunk), dA += (1/L) Phi_Q' dDen
+#pragma unroll
+            for (int j = 0; j < NFT; ++j) {
+                const int ft = w + 4 * j;
+                if (ft >= FT) break;
+#pragma unroll
+                for (int kk = 0; kk < 2; ++kk) {
+                    const F bf = T::ld8(&sm.pqt[16 * ft + col][32 * kk + 8 * g]);
+#pragma unroll
+                    for (int dt = 0; dt < DT; ++dt)
+                        St_[j][dt] = T::mma(T::ld8(&sm.dnt[16 * dt + col][32 * kk + 8 * g]), bf, St_[j][dt]);
+                }
+                float s = 0.f;
+#pragma unroll
+                for (int k = 0; k < 16; ++k) s += T::load(sm.pqt[16 * ft + col][16 * g + k]) * sm.dden[16 * g + k];
+                ar[j] += wave_sum16(s) * a.inv_L;
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------- LB3: dV
+template <class T, int D, int RP>
+__global__ __launch_bounds__(kThreads) void race_dv_kernel(LbArgs a)
+{
+    using St = typename T::store_t;
+    using F = typename T::frag_t;
+    constexpr int DW = D / 64, FS = RP / 32;
+    __shared__ Lb3Smem<T, D, RP> sm;
+    const int seg = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+    const size_t bh = (size_t)b * a.H + h;
+    const float* Uq = a.Uq + bh * a.N * (RP / 4);
+    const float* Uk = a.Uk + bh * a.N * (RP / 4);
+    const St* dO = (const St*)a.dO + bh * a.N * D;
+    const float* sclr = a.rs + 3 * a.BHN + bh * a.N;
+    float* out = a.out + bh * a.N * D;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int g = lane >> 4, col = lane & 15;
+
+    const float* st_in = a.states + (bh * a.nseg + seg) * (size_t)(RP * D + RP);
+    f32x4 S[RP / 16][DW];
+#pragma unroll
+    for (int ft = 0; ft < RP / 16; ++ft)
+#pragma unroll
+        for (int j = 0; j < DW; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                S[ft][j][i] = st_in[(size_t)(16 * ft + 4 * g + i) * D + 16 * (w * DW + j) + col];
+
+    const int t_beg = seg * a.seg_len, t_end = min(a.N, t_beg + a.seg_len);
+    const int nch = (t_end - t_beg + kC - 1) / kC;
+    for (int c = nch - 1; c >= 0; --c) {
+        const int t0 = t_beg + c * kC;
+        __syncthreads();
+        features<T, RP>(Uk, t0, a.N, a.L, a.two_beta, sm.pk, nullptr, nullptr);
+        if (a.causal) {
+            stage_t<T, D>(sm.dnt, dO, t0, a.N, sclr, a.inv_L);
+            features<T, RP>(Uq, t0, a.N, a.L, a.two_beta, sm.pq, sm.pqt, nullptr);
+        }
+        __syncthreads();
+        if (a.causal) {
+            // M' rows j in [16w, 16w + 16): <phi(k_j), phi(q_i)> for i >= j
+            for (int it = 0; it < 4; ++it) {
+                f32x4 acc = {0, 0, 0, 0};
+                if (it >= w) {
+#pragma unroll
+                    for (int fs = 0; fs < FS; ++fs)
+                        acc = T::mma(T::ld8(&sm.pk[16 * w + col][32 * fs + 8 * g]),
+                                     T::ld8(&sm.pq[16 * it + col][32 * fs + 8 * g]), acc);
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int kj = 16 * w + 4 * g + i, qi = 16 * it + col;
+                    sm.mt[kj][qi] = T::store(qi >= kj ? acc[i] : 0.f);
+                }
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) {
+            f32x4 acc[DW];
+#pragma unroll
+            for (int j = 0; j < DW; ++j) acc[j] = f32x4{0, 0, 0, 0};
+#pragma unroll
+            for (int fs = 0; fs < FS; ++fs) {
+                const F af = T::ld44(&sm.pk[16 * kt + col][32 * fs + 4 * g], &sm.pk[16 * kt + col][32 * fs + 16 + 4 * g]);
+#pragma unroll
+                for (int j = 0; j < DW; ++j) {
+                    float sv[8];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        sv[i] = S[2 * fs][j][i];
+                        sv[4 + i] = S[2 * fs + 1][j][i];
+                    }
+                    acc[j] = mma_split<T>(af, sv, acc[j]);
+                }
+            }
+            if (a.causal) {
+#pragma unroll
+                for (int kk = 0; kk < 2; ++kk) {
+                    const F af = T::ld8(&sm.mt[16 * kt + col][32 * kk + 8 * g]);
+#pragma unroll
+                    for (int j = 0; j < DW; ++j)
+                        acc[j] = T::mma(af, T::ld8(&sm.dnt[16 * (w * DW + j) + col][32 * kk + 8 * g]), acc[j]);
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int tok = t0 + 16 * kt + 4 * g + i;
+                if (tok >= a.N) continue;
+#pragma unroll
+                for (int j = 0; j < DW; ++j) out[(size_t)tok * D + 16 * (w * DW + j) + col] = acc[j][i];
+            }
+        }
+        if (a.causal) {
+            // dS += Phi_Q' (dNum / L) (chunk)
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk) {
+                F bv[DW];
+#pragma unroll
+                for (int j = 0; j < DW; ++j) bv[j] = T::ld8(&sm.dnt[16 * (w * DW + j) + col][32 * kk + 8 * g]);
+#pragma unroll
+                for (int ft = 0; ft < RP / 16; ++ft) {
+                    const F af = T::ld8(&sm.pqt[16 * ft + col][32 * kk + 8 * g]);
+#pragma unroll
+                    for (int j = 0; j < DW; ++j) S[ft][j] = T::mma(af, bv[j], S[ft][j]);
+                }
+            }
+        }
+    }
+}
+
+template <class T, int D, int RP>
+struct BwdFn {
+    static hipError_t run(const Shape& s, const LbArgs& a1, const LbArgs& a2, const LbArgs& a3, hipStream_t st)
+    {
+        if constexpr (!bwd_fits<T, D, RP>()) {
+            return hipErrorInvalidConfiguration;
+        } else {
+            dim3 grid(s.nseg, s.H, s.B);
+            hipLaunchKernelGGL((race_dq_kernel<T, D, RP>), grid, dim3(kThreads), 0, st, a1);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+            hipLaunchKernelGGL((race_dk_kernel<T, D, RP>), grid, dim3(kThreads), 0, st, a2);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            hipLaunchKernelGGL((race_dv_kernel<T, D, RP>), grid, dim3(kThreads), 0, st, a3);
+            return hipGetLastError();
+        }
+    }
+};
+
+template <class T, int D, int RP>
+struct BwdFitsFn {
+    static hipError_t run(const Shape&) { return bwd_fits<T, D, RP>() ? hipSuccess : hipErrorInvalidConfiguration; }
+};
+
+template <template <class, int, int> class Fn, class... A>
+hipError_t dispatch(const Shape& s, A&&... args)
+{
+    const int rp = race_padded_features(s.r);
+#define ELSAA_RP(T_, D_)                                                        \
+    switch (rp) {                                                               \
+        case 32: return Fn<T_, D_, 32>::run(s, args...);                        \
+        case 64: return Fn<T_, D_, 64>::run(s, args...);                        \
+        case 128: return Fn<T_, D_, 128>::run(s, args...);                      \
+        default: return Fn<T_, D_, 256>::run(s, args...);                       \
+    }
+    if (s.bf16) {
+        if (s.D == 64) { ELSAA_RP(BF16, 64) }
+        ELSAA_RP(BF16, 128)
+    }
+    if (s.D == 64) { ELSAA_RP(F32, 64) }
+    ELSAA_RP(F32, 128)
+#undef ELSAA_RP
+}
+
+}  // namespace
+
+bool race_bwd_fits(const Shape& s) { return dispatch<BwdFitsFn>(s) == hipSuccess; }
+
+hipError_t launch_race_bwd(const Shape& s, const float* Uq, const float* Uk, const void* V,
+                           const void* dO, const float* W_race, const float* rs,
+                           float* states_f, float* states_b, float* dq_lr, float* dk_lr,
+                           float* dv_lr, hipStream_t st)
+{
+    const size_t BHN = (size_t)s.B * s.H * s.N;
+    // forward prefix states of phi(k) V' and phi(k); backward suffix states
+    // of phi(q) dNum' / L and phi(q) dDen / L
+    hipError_t e = launch_race_states(s, Uk, V, nullptr, nullptr, 1.f, states_f, s.causal ? 1 : 0, st);
+    if (e != hipSuccess) return e;
+    e = launch_race_states(s, Uq, dO, rs + 3 * BHN, rs + 4 * BHN, 1.f / (float)s.L, states_b,
+                           s.causal ? 2 : 0, st);
+    if (e != hipSuccess) return e;
+    LbArgs a;
+    a.Uq = Uq; a.Uk = Uk; a.V = V; a.dO = dO; a.W = W_race; a.rs = rs;
+    a.H = s.H; a.N = s.N; a.L = s.L; a.seg_len = s.seg_len; a.nseg = s.nseg; a.causal = s.causal;
+    a.BHN = BHN;
+    a.two_beta = 2.f * s.beta; a.beta = s.beta; a.inv_L = 1.f / (float)s.L;
+    LbArgs a1 = a, a2 = a, a3 = a;
+    a1.states = states_f; a1.out = dq_lr;
+    a2.states = states_b; a2.out = dk_lr;
+    a3.states = states_b; a3.out = dv_lr;
+    return dispatch<BwdFn>(s, a1, a2, a3, st);
+}
+
+}  // namespace elsaa

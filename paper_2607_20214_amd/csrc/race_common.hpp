@@ -1,0 +1,187 @@
+// race_common.hpp -- device helpers of the RACE low-rank kernels (forward and backward).
+//
+// Features (Alg. 2): for table l, u = W_l x (4 projections), t = tanh(u), and
+// for bucket c of the hypercube {+-1}^4 (bit b of c set <-> v_cb = +1)
+//   phi_c = exp(beta t.v_c) / sum_c' exp(beta t.v_c') = prod_b sigmoid(2 beta v_cb t_b).
+// The projections u = W x are computed once per row by the projection kernel
+// and stored in float32; chunks are 64 tokens; each workgroup is 4 waves,
+// wave w handles tokens 16w .. 16w+15 of a chunk when computing features.
+#pragma once
+#include "common.hpp"
+
+namespace elsaa {
+namespace race {
+
+constexpr int kC = 64;
+constexpr int kThreads = 256;
+constexpr int kPad = 8;
+constexpr size_t kMaxLds = 160 * 1024;
+
+// projection count padded to whole 32-wide k-steps (backward du x W)
+template <int RP> constexpr int w_kdim() { return RP / 4 < 32 ? 32 : RP / 4; }
+
+// W' of one head split as W = W_hi + W_lo (W_lo is zero for float32 storage):
+// wt_hi[d][row], wt_lo[d][row], rows 4l + b (l < L), zero up to WK.
+template <class T, int D, int WK>
+__device__ void load_wt(typename T::store_t (*wt_hi)[WK + kPad], typename T::store_t (*wt_lo)[WK + kPad],
+                        const float* W, int L)
+{
+    for (int it = threadIdx.x; it < WK * D; it += kThreads) {
+        const int row = it % WK, c = it / WK;
+        const float w = row < 4 * L ? W[(size_t)row * D + c] : 0.f;
+        const typename T::store_t hi = T::store(w);
+        wt_hi[c][row] = hi;
+        if (T::bytes == 2) wt_lo[c][row] = T::store(w - T::load(hi));
+    }
+}
+
+// Rows [t0, t0 + 64) of X (zero past N), each multiplied by scale[row] when
+// scale != nullptr, into a transposed tile xt[d][token].
+template <class T, int D>
+__device__ void stage_t(typename T::store_t (*xt)[kC + kPad], const typename T::store_t* X,
+                        int t0, int N, const float* scale = nullptr, float mul = 1.f)
+{
+    using S = typename T::store_t;
+    constexpr int PER = 16 / T::bytes;
+    constexpr int CH = D / PER;
+    for (int it = threadIdx.x; it < (kC / 2) * CH; it += kThreads) {
+        const int p = it & (kC / 2 - 1), c = it / (kC / 2);
+        const int r0 = t0 + 2 * p, r1 = r0 + 1;
+        uint4 a = make_uint4(0, 0, 0, 0), b = make_uint4(0, 0, 0, 0);
+        if (r0 < N) a = ldg16(X + (size_t)r0 * D + c * PER);
+        if (r1 < N) b = ldg16(X + (size_t)r1 * D + c * PER);
+        const S* ea = (const S*)&a;
+        const S* eb = (const S*)&b;
+        const float s0 = (scale && r0 < N) ? scale[r0] * mul : mul;
+        const float s1 = (scale && r1 < N) ? scale[r1] * mul : mul;
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            S* dst = &xt[c * PER + j][2 * p];
+            if (scale || mul != 1.f) {
+                dst[0] = T::store(T::load(ea[j]) * s0);
+                dst[1] = T::store(T::load(eb[j]) * s1);
+            } else {
+                dst[0] = ea[j];
+                dst[1] = eb[j];
+            }
+        }
+    }
+}
+
+// Rows [t0, t0 + 64) of X (zero past N), optionally scaled per row, row-major.
+template <class T, int D>
+__device__ void stage_r(typename T::store_t (*x)[D + kPad], const typename T::store_t* X, int t0,
+                        int N, const float* scale = nullptr)
+{
+    using S = typename T::store_t;
+    constexpr int PER = 16 / T::bytes;
+    constexpr int CH = D / PER;
+    for (int it = threadIdx.x; it < kC * CH; it += kThreads) {
+        const int row = it % kC, c = it / kC;
+        const int r = t0 + row;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (r < N) v = ldg16(X + (size_t)r * D + c * PER);
+        if (scale) {
+            const float s = r < N ? scale[r] : 0.f;
+            S* e = (S*)&v;
+#pragma unroll
+            for (int j = 0; j < PER; ++j) e[j] = T::store(T::load(e[j]) * s);
+        }
+        *(uint4*)&x[row][c * PER] = v;
+    }
+}
+
+// Features of chunk tokens [t0 + 16w, t0 + 16w + 16) for every table, from
+// the stored projections U[token][4 * table + bit] (float32, row stride RP/4).
+// Writes phi (as T) row-major into ph[token][feature] and/or transposed into
+// pht[feature][token], and t = tanh(u) into ts[token][4 * table + bit].
+template <class T, int RP>
+__device__ void features(const float* U, int t0, int N, int L, float two_beta,
+                         typename T::store_t (*ph)[RP + kPad], typename T::store_t (*pht)[kC + kPad],
+                         float (*ts)[RP / 4])
+{
+    constexpr int UP = RP / 4;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int g = lane >> 4, col = lane & 15;
+    const int tl = 16 * wv + col;
+    const int tok = t0 + tl;
+#pragma unroll
+    for (int tb = g; tb < RP / 16; tb += 4) {   // this lane: table tb of token tl
+        f32x4 u = {0, 0, 0, 0};
+        if (tok < N) u = *(const f32x4*)(U + (size_t)tok * UP + 4 * tb);
+        const bool live = tb < L && tok < N;
+        float t[4], sp[4], sn[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            t[i] = tanhf(u[i]);
+            sp[i] = 1.f / (1.f + __expf(-two_beta * t[i]));
+            sn[i] = 1.f / (1.f + __expf(two_beta * t[i]));
+        }
+        if (ts) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) ts[tl][4 * tb + i] = t[i];
+        }
+        float phi[16];
+#pragma unroll
+        for (int c = 0; c < 16; ++c) {
+            const float v = ((c & 1) ? sp[0] : sn[0]) * ((c & 2) ? sp[1] : sn[1]) *
+                            ((c & 4) ? sp[2] : sn[2]) * ((c & 8) ? sp[3] : sn[3]);
+            phi[c] = live ? v : 0.f;
+        }
+        if (ph) {
+#pragma unroll
+            for (int c = 0; c < 16; ++c) ph[tl][16 * tb + c] = T::store(phi[c]);
+        }
+        if (pht) {
+#pragma unroll
+            for (int c = 0; c < 16; ++c) pht[16 * tb + c][tl] = T::store(phi[c]);
+        }
+    }
+}
+
+// Chain rule from a feature-gradient tile to the projection gradients du.
+// dphi: accumulator tile of 16 rows x the 16 features of table tb (lane
+// (g, col) register i holds row 16*qt + 4g + i, feature c = col).  With
+// phi_c = prod_b sigmoid(2 beta v_cb t_b) and t = tanh(u):
+//   dt_b = beta * sum_c dphi_c phi_c (v_cb - tanh(beta t_b)),  du_b = dt_b (1 - t_b^2)
+// (tanh(beta t_b) = sigmoid(2 beta t_b) - sigmoid(-2 beta t_b) is the mean of v_cb
+// under phi).  Writes du[row][4 tb + b], zero for padded tables.
+template <class T, int RP>
+__device__ __forceinline__ void chain_rule(f32x4 dphi, int qt, int tb, int L, float beta,
+                                           const float (*ts)[RP / 4],
+                                           typename T::store_t (*du)[w_kdim<RP>() + kPad])
+{
+    const int lane = threadIdx.x & 63;
+    const int g = lane >> 4, col = lane & 15;
+    const float two_beta = 2.f * beta;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int row = 16 * qt + 4 * g + i;
+        float t[4], sp[4], sn[4];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            t[b] = ts[row][4 * tb + b];
+            sp[b] = 1.f / (1.f + __expf(-two_beta * t[b]));
+            sn[b] = 1.f / (1.f + __expf(two_beta * t[b]));
+        }
+        float phi = 1.f;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) phi *= ((col >> b) & 1) ? sp[b] : sn[b];
+        const float x = dphi[i] * phi;
+        const float s0 = row_sum16(x);
+        float sb[4];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) sb[b] = row_sum16(((col >> b) & 1) ? x : -x);
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            if (col == b) {
+                const float dt = beta * (sb[b] - (sp[b] - sn[b]) * s0);
+                const float v = dt * (1.f - t[b] * t[b]);
+                du[row][4 * tb + b] = T::store(tb < L ? v : 0.f);
+            }
+        }
+    }
+}
+
+}  // namespace race
+}  // namespace elsaa

@@ -1,9 +1,12 @@
-// select.hip -- sortLSH selection: sign hash and per-segment stable sort.
+// select.hip -- sortLSH selection (sign hash, per-segment stable sort) and
+// the RACE projections of the same rows.
 //
 // Hash (Alg. 4, step "Hash"): bit t of row x is set iff the float32 fused
 // multiply-add chain over e = 0..d-1 of W_sort[h][t][e] * x[e] is > 0; the key
 // is the rank of the bit code in the reflected Gray sequence so neighbouring
-// buckets differ in one bit (sorted Hamming LSH, Sec. 3).
+// buckets differ in one bit (sorted Hamming LSH, Sec. 3).  The same pass over
+// Q or K also computes the RACE projections u = W_race x (Alg. 2), so each
+// input row is read once for both branches' hashing.
 // Sort (Alg. 4, step "Sort"; one call per half-segment of each level of
 // Alg. 5): ascending by (key, token index), i.e. a stable counting sort over
 // at most 2^sort_bits buckets, one workgroup per sorted list.
@@ -12,60 +15,125 @@
 
 namespace elsaa {
 
-constexpr int kHashRows = 64;
+constexpr int kProjRows = 64;
+constexpr int kProjThreads = 256;
+constexpr int kProjPad = 8;
 
-template <class T>
-__global__ __launch_bounds__(kHashRows) void hash_kernel(const typename T::store_t* __restrict__ X,
-                                                         const float* __restrict__ W,
-                                                         uint8_t* __restrict__ keys, int H, int N,
-                                                         int D, int bits)
+// Per 64-row tile of X (Q or K of one (b,h)): the sortLSH bucket key of every
+// row and, when W_race is given, the RACE projections u = W_race x of every
+// row in float32 accuracy: W = W_hi + W_lo split into two bf16 parts for the
+// bf16 MFMA path (the residual is below 2^-16 relative), plain float32 MFMA
+// for float32 storage.  u is stored [BH][N][UP] (UP = padded projections).
+template <class T, int D, int WR>
+struct ProjSmem {
+    typename T::store_t x[kProjRows][D + kProjPad];
+    typename T::store_t whi[WR][D + kProjPad];
+    typename T::store_t wlo[T::bytes == 2 ? WR : 1][D + kProjPad];   // (no low part for float32)
+    float ws[8][D];
+    uint32_t code[kProjRows];
+};
+
+template <class T, int D, int WR>
+__global__ __launch_bounds__(kProjThreads) void proj_kernel(const typename T::store_t* __restrict__ X,
+                                                            const float* __restrict__ Wsort,
+                                                            const float* __restrict__ Wrace,
+                                                            uint8_t* __restrict__ keys,
+                                                            float* __restrict__ U, int H, int N,
+                                                            int bits, int L, int UP)
 {
-    __shared__ float w_s[8 * 128];
-    __shared__ float x_s[kHashRows * 129];
+    using S = typename T::store_t;
+    using F = typename T::frag_t;
+    constexpr int PER = 16 / T::bytes;
+    constexpr int CH = D / PER;
+    constexpr int KS = D / 32;
+    __shared__ ProjSmem<T, D, WR> sm;
     const int h = blockIdx.y, b = blockIdx.z;
-    const int row0 = blockIdx.x * kHashRows;
-    const int rows = min(kHashRows, N - row0);
-    const size_t rowbase = ((size_t)b * H + h) * N + row0;
-    for (int e = threadIdx.x; e < bits * D; e += kHashRows) w_s[e] = W[(size_t)h * bits * D + e];
-    // the tile's rows are contiguous in memory: read it in 16-byte pieces
-    constexpr int per16 = 16 / T::bytes;
-    const int nchunk = rows * D / per16;
-    const uint4* src = (const uint4*)(X + rowbase * D);
-    for (int c = threadIdx.x; c < nchunk; c += kHashRows) {
-        uint4 v = src[c];
-        const typename T::store_t* e = (const typename T::store_t*)&v;
-        const int flat = c * per16;
-        const int r = flat / D, col = flat % D;
-#pragma unroll
-        for (int j = 0; j < per16; ++j) x_s[r * (D + 1) + col + j] = T::load(e[j]);
+    const int row0 = blockIdx.x * kProjRows;
+    const int rows = min(kProjRows, N - row0);
+    const size_t bh = (size_t)b * H + h;
+    const S* Xt = X + (bh * N + row0) * D;
+    for (int e = threadIdx.x; e < bits * D; e += kProjThreads) sm.ws[e / D][e % D] = Wsort[(size_t)h * bits * D + e];
+    for (int it = threadIdx.x; it < kProjRows * CH; it += kProjThreads) {
+        const int r = it / CH, c = it % CH;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (r < rows) v = ldg16(Xt + (size_t)r * D + c * PER);
+        *(uint4*)&sm.x[r][c * PER] = v;
+    }
+    if (threadIdx.x < kProjRows) sm.code[threadIdx.x] = 0;
+    if (Wrace) {
+        for (int it = threadIdx.x; it < WR * D; it += kProjThreads) {
+            const int row = it / D, c = it % D;
+            const float w = row < 4 * L ? Wrace[((size_t)h * L * 4 + row) * D + c] : 0.f;
+            const S hi = T::store(w);
+            sm.whi[row][c] = hi;
+            if (T::bytes == 2) sm.wlo[row][c] = T::store(w - T::load(hi));
+        }
     }
     __syncthreads();
-    const int t = threadIdx.x;
-    if (t >= rows) return;
-    uint32_t code = 0;
-    for (int bit = 0; bit < bits; ++bit) {
-        float p = 0.0f;
-        const float* w = w_s + bit * D;
-        const float* x = x_s + t * (D + 1);
-        for (int e = 0; e < D; ++e) p = __builtin_fmaf(w[e], x[e], p);
-        if (p > 0.0f) code |= 1u << bit;
+    // hash: thread (row, bit group) runs the float32 fma chains of its bits
+    {
+        const int r = threadIdx.x & (kProjRows - 1);
+        uint32_t c = 0;
+        for (int bit = threadIdx.x / kProjRows; bit < bits; bit += kProjThreads / kProjRows) {
+            float p = 0.0f;
+            for (int e = 0; e < D; ++e) p = __builtin_fmaf(sm.ws[bit][e], T::load(sm.x[r][e]), p);
+            if (p > 0.0f) c |= 1u << bit;
+        }
+        if (c) atomicOr(&sm.code[r], c);
     }
-    uint32_t rank = code;
-    for (uint32_t s = code >> 1; s; s >>= 1) rank ^= s;
-    keys[rowbase + t] = (uint8_t)rank;
+    __syncthreads();
+    if (threadIdx.x < rows) {
+        const uint32_t code = sm.code[threadIdx.x];
+        uint32_t rank = code;
+        for (uint32_t sft = code >> 1; sft; sft >>= 1) rank ^= sft;
+        keys[bh * N + row0 + threadIdx.x] = (uint8_t)rank;
+    }
+    if (!Wrace) return;
+    // u[token][p] for the wave's 16 tokens: A = W rows, B = X rows
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int g = lane >> 4, col = lane & 15;
+    const int tl = 16 * w + col;
+    F xf[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) xf[ks] = T::ld8(&sm.x[tl][32 * ks + 8 * g]);
+#pragma unroll
+    for (int pt = 0; pt < WR / 16; ++pt) {
+        f32x4 acc = {0, 0, 0, 0};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            acc = T::mma(T::ld8(&sm.whi[16 * pt + col][32 * ks + 8 * g]), xf[ks], acc);
+            if (T::bytes == 2) acc = T::mma(T::ld8(&sm.wlo[16 * pt + col][32 * ks + 8 * g]), xf[ks], acc);
+        }
+        const int p0 = 16 * pt + 4 * g;
+        if (tl < rows && p0 < UP) *(f32x4*)(U + (bh * N + row0 + tl) * UP + p0) = acc;
+    }
 }
 
-hipError_t launch_hash(const Shape& s, const void* X, const float* W_sort, uint8_t* keys,
-                       hipStream_t st)
+template <class T, int D>
+hipError_t launch_proj_t(const Shape& s, const void* X, const float* W_sort, const float* W_race,
+                         uint8_t* keys, float* U, hipStream_t st)
 {
-    dim3 grid((s.N + kHashRows - 1) / kHashRows, s.H, s.B);
-    if (s.bf16)
-        hipLaunchKernelGGL(hash_kernel<BF16>, grid, dim3(kHashRows), 0, st,
-                           (const uint16_t*)X, W_sort, keys, s.H, s.N, s.D, s.sort_bits);
-    else
-        hipLaunchKernelGGL(hash_kernel<F32>, grid, dim3(kHashRows), 0, st, (const float*)X,
-                           W_sort, keys, s.H, s.N, s.D, s.sort_bits);
+    dim3 grid((s.N + kProjRows - 1) / kProjRows, s.H, s.B);
+    const int UP = race_proj_stride(s);
+    const int wr = UP < 16 ? 16 : UP;
+#define ELSAA_PROJ(WR_)                                                                          \
+    hipLaunchKernelGGL((proj_kernel<T, D, WR_>), grid, dim3(kProjThreads), 0, st,                 \
+                       (const typename T::store_t*)X, W_sort, W_race, keys, U, s.H, s.N,          \
+                       s.sort_bits, s.L, UP)
+    if (wr == 16) ELSAA_PROJ(16);
+    else if (wr == 32) ELSAA_PROJ(32);
+    else ELSAA_PROJ(64);
+#undef ELSAA_PROJ
     return hipGetLastError();
+}
+
+hipError_t launch_project(const Shape& s, const void* X, const float* W_sort, const float* W_race,
+                          uint8_t* keys, float* U, hipStream_t st)
+{
+    if (s.bf16) return s.D == 64 ? launch_proj_t<BF16, 64>(s, X, W_sort, W_race, keys, U, st)
+                                 : launch_proj_t<BF16, 128>(s, X, W_sort, W_race, keys, U, st);
+    return s.D == 64 ? launch_proj_t<F32, 64>(s, X, W_sort, W_race, keys, U, st)
+                     : launch_proj_t<F32, 128>(s, X, W_sort, W_race, keys, U, st);
 }
 
 // --------------------------------------------------------------------------

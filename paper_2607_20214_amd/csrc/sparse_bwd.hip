@@ -1,0 +1,517 @@
+// sparse_bwd.hip -- backward of the sortLSH sparse branch.
+//
+// With the selection fixed, the sparse branch is exact softmax attention
+// restricted to each query's support S(i), normalised by d_s + eps.  Its
+// gradient (no formula in the paper; the exact derivative of the forward):
+//   P_ij  = exp(z_ij - log(d_s,i + eps)),  z_ij = tau <Q_i, K_j>
+//   dO_s  = g_s m dO            (row scale sc_s = g_s m)
+//   dz_ij = P_ij (<dO_s,i, V_j> - Delta_i)
+//   dQ_i += tau sum_j dz_ij K_j;  dK_j += tau sum_i dz_ij Q_i;  dV_j += sum_i P_ij dO_s,i
+// where Delta_i = <dO_s,i, O_s,i> - dm_i m_i (1 - m_i)(d_s,i + eps)/d_s,i also
+// carries the gradient through the denominator-aware multiplier m.
+//
+// Two passes, no atomics: a query-centric pass (dQ; one workgroup per 64
+// queries, keys streamed through LDS) and a key-centric pass (dK, dV; one
+// workgroup per 64 keys, queries streamed through LDS).  Both have the three
+// modes of the forward (non-causal blocks, causal levels, causal leaf).  The
+// level passes write per-level partials by natural token index; the leaf
+// passes add the partials of every level and the low-rank gradient and
+// store the final dQ, dK, dV in the storage dtype.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace elsaa {
+
+namespace {
+
+constexpr int kT = 64;
+constexpr int kThreads = 256;
+constexpr int kPad = 8;
+
+enum Mode { kBlocks = 0, kLevels = 1, kLeaf = 2 };
+
+struct BArgs {
+    const void* Q;
+    const void* K;
+    const void* V;
+    const void* dO;
+    const int32_t* perm_q;
+    const int32_t* perm_k;
+    const float* rs;          // row scalars, see internal.hpp
+    const float* dq_lr;       // float32 [BHN][D] low-rank parts
+    const float* dk_lr;
+    const float* dv_lr;
+    float* part_dq;           // float32 [BH][Lv][N/2][D] per-level partials
+    float* part_dk;
+    float* part_dv;
+    void* dQ;
+    void* dK;
+    void* dV;
+    int H, N, k, Lv, n_leaf;
+    size_t BHN;
+    float tau, tau2;
+};
+
+// Rows [0, 64) of X listed in idx (-1 = zero row) into a row-major tile and,
+// when xt != nullptr, its transpose.
+template <class T, int D>
+__device__ __forceinline__ void stage_rows(const typename T::store_t* X, const int32_t* idx,
+                                           typename T::store_t (*x)[D + kPad],
+                                           typename T::store_t (*xt)[kT + kPad])
+{
+    using S = typename T::store_t;
+    constexpr int PER = 16 / T::bytes;
+    constexpr int CH = D / PER;
+    if (x) {
+        for (int it = threadIdx.x; it < kT * CH; it += kThreads) {
+            const int row = it & (kT - 1), c = it / kT;
+            const int tok = idx[row];
+            uint4 v = make_uint4(0, 0, 0, 0);
+            if (tok >= 0) v = ldg16(X + (size_t)tok * D + c * PER);
+            *(uint4*)&x[row][c * PER] = v;
+        }
+    }
+    if (xt) {
+        for (int it = threadIdx.x; it < (kT / 2) * CH; it += kThreads) {
+            const int p = it & (kT / 2 - 1), c = it / (kT / 2);
+            const int t0 = idx[2 * p], t1 = idx[2 * p + 1];
+            uint4 a = make_uint4(0, 0, 0, 0), b = make_uint4(0, 0, 0, 0);
+            if (t0 >= 0) a = ldg16(X + (size_t)t0 * D + c * PER);
+            if (t1 >= 0) b = ldg16(X + (size_t)t1 * D + c * PER);
+            const S* ea = (const S*)&a;
+            const S* eb = (const S*)&b;
+#pragma unroll
+            for (int j = 0; j < PER; ++j) {
+                S* dst = &xt[c * PER + j][2 * p];
+                dst[0] = ea[j];
+                dst[1] = eb[j];
+            }
+        }
+    }
+}
+
+template <class T, int D>
+struct DqSmem {
+    typename T::store_t k[kT][D + kPad];
+    typename T::store_t v[kT][D + kPad];
+    typename T::store_t kt[D][kT + kPad];
+    int32_t idx[kT];
+};
+
+template <class T, int D>
+struct DkvSmem {
+    typename T::store_t q[kT][D + kPad];
+    typename T::store_t o[kT][D + kPad];
+    typename T::store_t qt[D][kT + kPad];
+    typename T::store_t ot[D][kT + kPad];
+    int32_t idx[kT];
+    int32_t ktok[kT];
+    float lse2[kT], delta[kT], scs[kT];
+};
+
+// Compact slot of token t in the level-l list of future (or past) halves.
+__device__ __forceinline__ size_t level_slot(size_t bh, int Lv, int l, int N, int t, int future)
+{
+    const int hl = N >> (l + 1);
+    const int s2 = t / (2 * hl);
+    return (bh * Lv + l) * (size_t)(N / 2) + (size_t)s2 * hl + (t - s2 * 2 * hl - (future ? hl : 0));
+}
+
+// ------------------------------------------------------------------------
+// dQ: query-centric
+// ------------------------------------------------------------------------
+template <class T, int D, int MODE>
+__global__ __launch_bounds__(kThreads) void sparse_dq_kernel(BArgs a)
+{
+    using S = typename T::store_t;
+    using F = typename T::frag_t;
+    constexpr int KS = D / 32, DT = D / 16;
+    __shared__ DqSmem<T, D> sm;
+    const int h = blockIdx.y, b = blockIdx.z;
+    const size_t bh = (size_t)b * a.H + h;
+    const int N = a.N;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int g = lane >> 4, qq = lane & 15;
+    const S* Q = (const S*)a.Q + bh * N * D;
+    const S* K = (const S*)a.K + bh * N * D;
+    const S* V = (const S*)a.V + bh * N * D;
+    const S* dO = (const S*)a.dO + bh * N * D;
+
+    int level = 0, half = N, qpos, qtok, kbeg, kend, bq = 1;
+    const int32_t* klist = nullptr;
+    const int tile = blockIdx.x;
+    if (MODE == kBlocks) {
+        bq = min(a.k, N);
+        const int p0 = tile * kT;
+        qpos = p0 + 16 * w + qq;
+        qtok = qpos < N ? a.perm_q[bh * N + qpos] : -1;
+        const int plast = min(p0 + kT, N) - 1;
+        kbeg = (p0 / bq) * bq;
+        kend = min(N, (plast / bq + 1) * bq);
+        klist = a.perm_k + bh * N;
+    } else if (MODE == kLevels) {
+        const int per_level = (N / 2) / kT;
+        level = tile / per_level;
+        const int t = tile - level * per_level;
+        half = N >> (level + 1);
+        const int seg = (t * kT) / half;
+        const int p0 = t * kT - seg * half;
+        bq = min(a.k, half);
+        qpos = p0 + 16 * w + qq;
+        const size_t lbase = (bh * a.Lv + level) * (size_t)(N / 2) + (size_t)seg * half;
+        qtok = a.perm_q[lbase + qpos];
+        kbeg = (p0 / bq) * bq;
+        kend = min(half, ((p0 + kT - 1) / bq + 1) * bq);
+        klist = a.perm_k + lbase;
+    } else {
+        const int q0 = tile * kT;
+        qtok = q0 + 16 * w + qq;
+        qpos = qtok;
+        kbeg = (q0 / a.n_leaf) * a.n_leaf;
+        kend = q0 + kT;
+    }
+    const int blk_lo = (MODE == kLeaf) ? 0 : (qpos / bq) * bq;
+    const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), blk_lo + bq);
+
+    float lse2 = 0.f, delta = 0.f, scs = 0.f;
+    F qf[KS], df[KS];
+    {
+        float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        const F zf = T::pack(z);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) { qf[ks] = zf; df[ks] = zf; }
+    }
+    if (qtok >= 0) {
+        const size_t row = bh * N + qtok;
+        lse2 = a.rs[row];
+        delta = a.rs[a.BHN + row];
+        scs = a.rs[2 * a.BHN + row];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            qf[ks] = T::ld8(Q + (size_t)qtok * D + 32 * ks + 8 * g);
+            df[ks] = T::ld8(dO + (size_t)qtok * D + 32 * ks + 8 * g);
+        }
+    }
+    f32x4 acc[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) acc[dt] = f32x4{0, 0, 0, 0};
+
+    for (int k0 = kbeg; k0 < kend; k0 += kT) {
+        __syncthreads();
+        if (threadIdx.x < kT) {
+            const int p = k0 + threadIdx.x;
+            int tok = -1;
+            if (p < kend) tok = (MODE == kLeaf) ? p : klist[p];
+            sm.idx[threadIdx.x] = tok;
+        }
+        __syncthreads();
+        stage_rows<T, D>(K, sm.idx, sm.k, sm.kt);
+        stage_rows<T, D>(V, sm.idx, sm.v, nullptr);
+        __syncthreads();
+        f32x4 dz[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            f32x4 st = {0, 0, 0, 0}, dp = {0, 0, 0, 0};
+            const int kr = krow_of(s, qq);
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                st = T::mma(T::ld8(&sm.k[kr][32 * ks + 8 * g]), qf[ks], st);
+                dp = T::mma(T::ld8(&sm.v[kr][32 * ks + 8 * g]), df[ks], dp);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int p = k0 + key_of(s, g, i);
+                bool ok = p < kend && qtok >= 0;
+                if (MODE == kLeaf) ok = ok && p <= qtok;
+                else ok = ok && p >= blk_lo && p < blk_hi;
+                const float P = ok ? fast_exp2(st[i] * a.tau2 - lse2) : 0.f;
+                dz[s][i] = P * (scs * dp[i] - delta);
+            }
+        }
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+            float v8[8];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                v8[j] = dz[2 * kk][j];
+                v8[4 + j] = dz[2 * kk + 1][j];
+            }
+            const F bf = T::pack(v8);
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+                acc[dt] = T::mma(T::ld8(&sm.kt[16 * dt + qq][32 * kk + 8 * g]), bf, acc[dt]);
+        }
+    }
+    if (qtok < 0) return;
+    if (MODE == kLevels) {
+        float* out = a.part_dq + level_slot(bh, a.Lv, level, N, qtok, 1) * D;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) *(f32x4*)(out + 16 * dt + 4 * g) = acc[dt] * a.tau;
+        return;
+    }
+    const size_t row = bh * N + qtok;
+    f32x4 tot[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+        tot[dt] = acc[dt] * a.tau + *(const f32x4*)(a.dq_lr + row * D + 16 * dt + 4 * g);
+    if (MODE == kLeaf) {
+        const int q0 = blockIdx.x * kT;
+        for (int l = 0; l < a.Lv; ++l) {
+            const int hl = N >> (l + 1);
+            if (((q0 / hl) & 1) == 0) continue;
+            const float* pp = a.part_dq + level_slot(bh, a.Lv, l, N, qtok, 1) * D;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) tot[dt] += *(const f32x4*)(pp + 16 * dt + 4 * g);
+        }
+    }
+    S* out = (S*)a.dQ + row * D;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) out[16 * dt + 4 * g + i] = T::store(tot[dt][i]);
+}
+
+// ------------------------------------------------------------------------
+// dK, dV: key-centric
+// ------------------------------------------------------------------------
+template <class T, int D, int MODE>
+__global__ __launch_bounds__(kThreads) void sparse_dkv_kernel(BArgs a)
+{
+    using S = typename T::store_t;
+    using F = typename T::frag_t;
+    constexpr int KS = D / 32, DT = D / 16;
+    __shared__ DkvSmem<T, D> sm;
+    const int h = blockIdx.y, b = blockIdx.z;
+    const size_t bh = (size_t)b * a.H + h;
+    const int N = a.N;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int g = lane >> 4, col = lane & 15;
+    const S* Q = (const S*)a.Q + bh * N * D;
+    const S* K = (const S*)a.K + bh * N * D;
+    const S* V = (const S*)a.V + bh * N * D;
+    const S* dO = (const S*)a.dO + bh * N * D;
+
+    int level = 0, half = N, kpos, ktok, qbeg, qend, bq = 1, j0 = 0;
+    const int32_t* qlist = nullptr;
+    const int32_t* klist = nullptr;
+    const int tile = blockIdx.x;
+    if (MODE == kBlocks) {
+        bq = min(a.k, N);
+        const int p0 = tile * kT;
+        kpos = p0 + 16 * w + col;
+        klist = a.perm_k + bh * N;
+        ktok = kpos < N ? klist[kpos] : -1;
+        const int plast = min(p0 + kT, N) - 1;
+        qbeg = (p0 / bq) * bq;
+        qend = min(N, (plast / bq + 1) * bq);
+        qlist = a.perm_q + bh * N;
+        j0 = p0;
+    } else if (MODE == kLevels) {
+        const int per_level = (N / 2) / kT;
+        level = tile / per_level;
+        const int t = tile - level * per_level;
+        half = N >> (level + 1);
+        const int seg = (t * kT) / half;
+        const int p0 = t * kT - seg * half;
+        bq = min(a.k, half);
+        kpos = p0 + 16 * w + col;
+        const size_t lbase = (bh * a.Lv + level) * (size_t)(N / 2) + (size_t)seg * half;
+        klist = a.perm_k + lbase;
+        ktok = klist[kpos];
+        qbeg = (p0 / bq) * bq;
+        qend = min(half, ((p0 + kT - 1) / bq + 1) * bq);
+        qlist = a.perm_q + lbase;
+        j0 = p0;
+    } else {
+        j0 = tile * kT;
+        ktok = j0 + 16 * w + col;
+        kpos = ktok;
+        qbeg = j0;
+        qend = (j0 / a.n_leaf + 1) * a.n_leaf;
+    }
+    const int blk_lo = (MODE == kLeaf) ? 0 : (kpos / bq) * bq;
+    const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), blk_lo + bq);
+    if (threadIdx.x < kT) {
+        int t = -1;
+        const int p = j0 + threadIdx.x;
+        if (MODE == kLeaf) t = p;
+        else if (MODE == kLevels) t = klist[p];
+        else t = p < N ? klist[p] : -1;
+        sm.ktok[threadIdx.x] = t;
+    }
+
+    F kf[KS], vf[KS];
+    {
+        float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        const F zf = T::pack(z);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) { kf[ks] = zf; vf[ks] = zf; }
+    }
+    if (ktok >= 0) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            kf[ks] = T::ld8(K + (size_t)ktok * D + 32 * ks + 8 * g);
+            vf[ks] = T::ld8(V + (size_t)ktok * D + 32 * ks + 8 * g);
+        }
+    }
+    f32x4 ak[DT], av[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) { ak[dt] = f32x4{0, 0, 0, 0}; av[dt] = f32x4{0, 0, 0, 0}; }
+
+    for (int q0 = qbeg; q0 < qend; q0 += kT) {
+        __syncthreads();
+        if (threadIdx.x < kT) {
+            const int p = q0 + threadIdx.x;
+            int tok = -1;
+            if (p < qend) tok = (MODE == kLeaf) ? p : qlist[p];
+            sm.idx[threadIdx.x] = tok;
+            float l2 = 0.f, de = 0.f, sc = 0.f;
+            if (tok >= 0) {
+                const size_t row = bh * N + tok;
+                l2 = a.rs[row];
+                de = a.rs[a.BHN + row];
+                sc = a.rs[2 * a.BHN + row];
+            }
+            sm.lse2[threadIdx.x] = l2;
+            sm.delta[threadIdx.x] = de;
+            sm.scs[threadIdx.x] = sc;
+        }
+        __syncthreads();
+        stage_rows<T, D>(Q, sm.idx, sm.q, sm.qt);
+        stage_rows<T, D>(dO, sm.idx, sm.o, sm.ot);
+        __syncthreads();
+        float pv[4][4], dz[4][4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            f32x4 st = {0, 0, 0, 0}, dp = {0, 0, 0, 0};
+            const int qr = krow_of(s, col);
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                st = T::mma(T::ld8(&sm.q[qr][32 * ks + 8 * g]), kf[ks], st);
+                dp = T::mma(T::ld8(&sm.o[qr][32 * ks + 8 * g]), vf[ks], dp);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int ql = key_of(s, g, i);
+                const int p = q0 + ql;
+                bool ok = p < qend && ktok >= 0;
+                if (MODE == kLeaf) ok = ok && p >= ktok;
+                else ok = ok && p >= blk_lo && p < blk_hi;
+                const float P = ok ? fast_exp2(st[i] * a.tau2 - sm.lse2[ql]) : 0.f;
+                const float sc = sm.scs[ql];
+                pv[s][i] = P * sc;
+                dz[s][i] = P * (sc * dp[i] - sm.delta[ql]);
+            }
+        }
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+            float p8[8], z8[8];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                p8[j] = pv[2 * kk][j];
+                p8[4 + j] = pv[2 * kk + 1][j];
+                z8[j] = dz[2 * kk][j];
+                z8[4 + j] = dz[2 * kk + 1][j];
+            }
+            const F pf = T::pack(p8), zf = T::pack(z8);
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                av[dt] = T::mma(pf, T::ld8(&sm.ot[16 * dt + col][32 * kk + 8 * g]), av[dt]);
+                ak[dt] = T::mma(zf, T::ld8(&sm.qt[16 * dt + col][32 * kk + 8 * g]), ak[dt]);
+            }
+        }
+    }
+    __syncthreads();
+    // accumulator rows are keys 16w + 4g + i, columns d = 16 dt + col
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int kl = 16 * w + 4 * g + i;
+        const int kt = sm.ktok[kl];
+        if (kt < 0) continue;
+        if (MODE == kLevels) {
+            const size_t slot = level_slot(bh, a.Lv, level, N, kt, 0);
+            float* pk = a.part_dk + slot * D;
+            float* pv2 = a.part_dv + slot * D;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                pk[16 * dt + col] = ak[dt][i] * a.tau;
+                pv2[16 * dt + col] = av[dt][i];
+            }
+            continue;
+        }
+        const size_t row = bh * N + kt;
+        float tk[DT], tv[DT];
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+            tk[dt] = ak[dt][i] * a.tau + a.dk_lr[row * D + 16 * dt + col];
+            tv[dt] = av[dt][i] + a.dv_lr[row * D + 16 * dt + col];
+        }
+        if (MODE == kLeaf) {
+            for (int l = 0; l < a.Lv; ++l) {
+                const int hl = N >> (l + 1);
+                if (((j0 / hl) & 1) != 0) continue;   // keys of past halves only
+                const size_t slot = level_slot(bh, a.Lv, l, N, kt, 0);
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) {
+                    tk[dt] += a.part_dk[slot * D + 16 * dt + col];
+                    tv[dt] += a.part_dv[slot * D + 16 * dt + col];
+                }
+            }
+        }
+        S* ok = (S*)a.dK + row * D;
+        S* ov = (S*)a.dV + row * D;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+            ok[16 * dt + col] = T::store(tk[dt]);
+            ov[16 * dt + col] = T::store(tv[dt]);
+        }
+    }
+}
+
+template <class T, int D>
+hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st)
+{
+    hipError_t e;
+    if (!s.causal) {
+        dim3 grid((s.N + kT - 1) / kT, s.H, s.B);
+        hipLaunchKernelGGL((sparse_dq_kernel<T, D, kBlocks>), grid, dim3(kThreads), 0, st, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL((sparse_dkv_kernel<T, D, kBlocks>), grid, dim3(kThreads), 0, st, a);
+        return hipGetLastError();
+    }
+    if (s.Lv > 0) {
+        dim3 grid(s.Lv * (s.N / 2) / kT, s.H, s.B);
+        hipLaunchKernelGGL((sparse_dq_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL((sparse_dkv_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    dim3 grid(s.N / kT, s.H, s.B);
+    hipLaunchKernelGGL((sparse_dq_kernel<T, D, kLeaf>), grid, dim3(kThreads), 0, st, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL((sparse_dkv_kernel<T, D, kLeaf>), grid, dim3(kThreads), 0, st, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_sparse_bwd(const Shape& s, const void* Q, const void* K, const void* V,
+                             const void* dO, const int32_t* perm_q, const int32_t* perm_k,
+                             const float* rs, const float* dq_lr, const float* dk_lr,
+                             const float* dv_lr, float* part_dq, float* part_dk, float* part_dv,
+                             void* dQ, void* dK, void* dV, hipStream_t st)
+{
+    BArgs a;
+    a.Q = Q; a.K = K; a.V = V; a.dO = dO;
+    a.perm_q = perm_q; a.perm_k = perm_k; a.rs = rs;
+    a.dq_lr = dq_lr; a.dk_lr = dk_lr; a.dv_lr = dv_lr;
+    a.part_dq = part_dq; a.part_dk = part_dk; a.part_dv = part_dv;
+    a.dQ = dQ; a.dK = dK; a.dV = dV;
+    a.H = s.H; a.N = s.N; a.k = s.k; a.Lv = s.Lv; a.n_leaf = s.n_leaf;
+    a.BHN = (size_t)s.B * s.H * s.N;
+    a.tau = s.tau; a.tau2 = s.tau * kLog2e;
+    if (s.bf16) return s.D == 64 ? launch_t<BF16, 64>(s, a, st) : launch_t<BF16, 128>(s, a, st);
+    return s.D == 64 ? launch_t<F32, 64>(s, a, st) : launch_t<F32, 128>(s, a, st);
+}
+
+}  // namespace elsaa

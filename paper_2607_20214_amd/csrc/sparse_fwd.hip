@@ -49,25 +49,18 @@ struct Args {
     const int32_t* perm_q;
     const int32_t* perm_k;
     const float* gates;
-    const void* O_lr;
+    const float* O_lr;
     const float* d_lr;
     float* part_o;
     float* part_lse;
     void* O;
     float* lse;
     float* m;
-    void* O_s;
+    float* O_s;
     int H, N, k, Lv, n_leaf;
     float tau2;      // tau * log2(e)
     float lambda, eps;
 };
-
-// Key row index inside the 64-key tile held by register i of score
-// sub-tile s for lane group g: sub-tiles 2m and 2m+1 together cover keys
-// 32m..32m+31 so that lane group g holds keys 32m + 8g .. 32m + 8g + 7.
-__device__ __forceinline__ int key_of(int s, int g, int i) { return 32 * (s >> 1) + 8 * g + 4 * (s & 1) + i; }
-// K row fed to A-operand row rho of sub-tile s (the inverse of key_of).
-__device__ __forceinline__ int krow_of(int s, int rho) { return 32 * (s >> 1) + 8 * (rho >> 2) + 4 * (s & 1) + (rho & 3); }
 
 template <class T, int D>
 __device__ __forceinline__ void load_kv(Smem<T, D>& sm, const typename T::store_t* K,
@@ -296,19 +289,17 @@ __global__ __launch_bounds__(kThreads) void sparse_fwd_kernel(Args a)
         gs = a.gates[row * 2 + 0];
         gl = a.gates[row * 2 + 1];
     }
-    const S* olr = (const S*)a.O_lr + row * D;
+    const float* olr = a.O_lr + row * D;
     S* out = (S*)a.O + row * D;
-    S* os = (S*)a.O_s + row * D;
+    float* os = a.O_s + row * D;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
         const int c0 = 16 * dt + 4 * g;
+        const f32x4 o_s = acc[dt] * inv_den;
+        *(f32x4*)(os + c0) = o_s;
+        const f32x4 o_l = *(const f32x4*)(olr + c0);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const float o_s = acc[dt][i] * inv_den;
-            const float o = gs * mf * o_s + gl * T::load(olr[c0 + i]);
-            out[c0 + i] = T::store(o);
-            os[c0 + i] = T::store(o_s);
-        }
+        for (int i = 0; i < 4; ++i) out[c0 + i] = T::store(gs * mf * o_s[i] + gl * o_l[i]);
     }
     if (g == 0) {
         a.lse[row] = lse_nat;
@@ -339,8 +330,8 @@ hipError_t launch_t(const Shape& s, const Args& a, hipStream_t st)
 
 hipError_t launch_sparse_fwd(const Shape& s, const void* Q, const void* K, const void* V,
                              const int32_t* perm_q, const int32_t* perm_k, const float* gates,
-                             const void* O_lr, const float* d_lr, float* part_o, float* part_lse,
-                             void* O, float* lse, float* m, void* O_s, hipStream_t st)
+                             const float* O_lr, const float* d_lr, float* part_o, float* part_lse,
+                             void* O, float* lse, float* m, float* O_s, hipStream_t st)
 {
     Args a;
     a.Q = Q; a.K = K; a.V = V;

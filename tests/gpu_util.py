@@ -73,3 +73,13 @@ def compare_heads(name, got, want, tol, heads=None):
             worst = max(worst, e)
             assert e <= tol, f"{name} (b={b}, h={h}): relative error {e:.3e} > {tol:.1e}"
     return worst
+
+
+def run_gpu_fwd_bwd(cfg: E.Config, inp: dict, gates=None, want_dgates=False):
+    """Forward then backward on the GPU; returns numpy dQ, dK, dV (and dgates)."""
+    got, (q, k, v, ws, wr, g, saved, lse, dlr) = run_gpu_fwd(cfg, inp, gates)
+    do = to_dev(inp["dO"], cfg.torch_dtype)
+    res = E.bwd(cfg, q, k, v, wr, do, lse, dlr, saved, gates=g, want_dgates=want_dgates)
+    torch.cuda.synchronize()
+    names = ("dQ", "dK", "dV", "dgates")[:len(res)]
+    return got, {n: t.float().cpu().numpy() for n, t in zip(names, res)}

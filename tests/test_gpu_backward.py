@@ -1,0 +1,98 @@
+"""GPU parity of the backward (dQ, dK, dV, gate gradients) against the oracle."""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import TOL, cfg_of, head_cfg_of, rel_err, run_gpu_fwd_bwd, say
+from paper_2607_20214_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def _w(name, B, H, N, d, k, r, causal, dtype, recipe="iid", seed=60, **kw):
+    qs = d ** -0.25 if recipe == "iid" else 1.0
+    return W.Workload(name, B, H, N, d, k, r, causal, dtype, recipe=recipe, qk_scale=qs, seed=seed,
+                      centres=kw.pop("centres", 16), **kw)
+
+
+SMALL = [
+    _w("nc-f32-512", 1, 1, 512, 64, 32, 32, False, "f32"),
+    _w("nc-bf16-ragged-300", 1, 2, 300, 64, 64, 64, False, "bf16", recipe="clustered"),
+    _w("nc-bf16-d128-k48-777", 1, 1, 777, 128, 48, 128, False, "bf16"),
+    _w("c-bf16-d128-1024", 1, 2, 1024, 128, 64, 128, True, "bf16"),
+    _w("c-bf16-d64-2048-clustered", 1, 2, 2048, 64, 128, 64, True, "bf16", recipe="clustered"),
+    _w("c-f32-d64-512", 1, 1, 512, 64, 32, 32, True, "f32"),
+    _w("c-f32-d128-512", 1, 1, 512, 128, 32, 64, True, "f32"),
+    _w("c-bf16-leaf-only-256", 2, 1, 256, 64, 128, 48, True, "bf16"),
+    _w("c-bf16-r256-1024", 1, 1, 1024, 128, 128, 256, True, "bf16", recipe="mixed", centres=8),
+    _w("c-bf16-n0-3x-768", 1, 1, 768, 64, 128, 64, True, "bf16"),
+]
+
+
+def _check(w, gates=None, lam=1.0, heads=None, q_mask=None, k_mask=None, want_dgates=False):
+    cfg = cfg_of(w, lam=lam)
+    inp = W.make_inputs(w, with_grad=True)
+    say(f"[bwd] {w.name}: B={w.B} H={w.H} N={w.N} d={w.d} k={w.k} r={w.r} causal={w.causal} {w.dtype}")
+    _, got = run_gpu_fwd_bwd(cfg, inp, gates, want_dgates=want_dgates)
+    tol = TOL[w.dtype]
+    hc = head_cfg_of(cfg)
+    errs = {}
+    for b in range(w.B):
+        for h in range(w.H):
+            if heads is not None and (b, h) not in heads:
+                continue
+            ref = oracle.backward(hc, inp["Q"][b, h], inp["K"][b, h], inp["V"][b, h], inp["W_sort"][h],
+                                  inp["W_race"][h], inp["dO"][b, h],
+                                  gates=None if gates is None else gates[b, h], q_mask=q_mask,
+                                  k_mask=k_mask)
+            for name, msk in (("dQ", q_mask), ("dK", k_mask), ("dV", k_mask), ("dgates", None)):
+                if name not in got:
+                    continue
+                rows = slice(None) if msk is None else (msk > 0)
+                e = rel_err(got[name][b, h][rows], ref[name][rows])
+                errs[name] = max(errs.get(name, 0.0), e)
+                assert e <= tol, f"{name} (b={b}, h={h}): {e:.3e} > {tol}"
+    say("   errors:", {k: f"{v:.2e}" for k, v in errs.items()})
+
+
+@pytest.mark.parametrize("w", SMALL, ids=[w.name for w in SMALL])
+def test_backward_small(w):
+    _check(w)
+
+
+def test_backward_gates_lambda_and_gate_gradients():
+    w = _w("c-bf16-gates", 1, 2, 1024, 64, 64, 64, True, "bf16", seed=61)
+    _check(w, gates=W.make_gates(w), lam=0.37, want_dgates=True)
+    w2 = _w("nc-f32-gates", 1, 1, 512, 64, 32, 32, False, "f32", seed=62)
+    _check(w2, gates=W.make_gates(w2), lam=0.0, want_dgates=True)
+
+
+def test_backward_clustered_4k_workload():
+    _check(W.CLUSTERED_4K, heads={(0, 0), (1, 5)})
+
+
+def test_backward_causal_16k_workload_sampled_heads():
+    _check(W.CAUSAL_16K, heads={(0, 0), (0, 11)})
+
+
+def test_backward_causal_64k_mixed_workload_sampled_rows():
+    w = W.CAUSAL_64K_MIXED
+    rng = np.random.default_rng(6)
+    qm = np.zeros(w.N, np.uint8)
+    km = np.zeros(w.N, np.uint8)
+    qm[rng.choice(w.N, 200, replace=False)] = 1
+    km[rng.choice(w.N, 200, replace=False)] = 1
+    qm[-64:] = 1
+    km[:64] = 1
+    _check(w, heads={(0, 1), (0, 6)}, q_mask=qm, k_mask=km)
+
+
+def test_backward_is_deterministic():
+    w = _w("c-bf16-det", 1, 2, 2048, 128, 128, 128, True, "bf16", seed=63)
+    cfg = cfg_of(w)
+    inp = W.make_inputs(w, with_grad=True)
+    say(f"[bwd-det] {w.name}")
+    _, a = run_gpu_fwd_bwd(cfg, inp)
+    _, b = run_gpu_fwd_bwd(cfg, inp)
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
