@@ -138,6 +138,16 @@ int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
               void* dQ, void* dK, void* dV, float* dgates,
               void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Opt-in kernel timing.  While enabled, every kernel launch of the library
+ * is bracketed by two HIP events recorded on its stream (one extra event pair
+ * per launch, no synchronisation); elsaa_profile_count / elsaa_profile_get
+ * wait for the recorded launches and report, per kernel name, the summed
+ * event time in milliseconds and the number of launches.  Enabling clears
+ * the previous totals.  Process-wide; disabled by default. */
+int elsaa_profile_enable(int on);
+int elsaa_profile_count(void);
+int elsaa_profile_get(int index, char* name, size_t name_len, double* total_ms, int64_t* launches);
+
 const char* elsaa_status_string(int status);
 const char* elsaa_last_error(void);
 

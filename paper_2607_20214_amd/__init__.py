@@ -90,6 +90,10 @@ def load():
         lib.elsaa_select.argtypes = [P, P, P, P, P, P, P, S, P]
         lib.elsaa_fwd.argtypes = [P, P, P, P, P, P, P, P, P, P, P, S, P, S, P]
         lib.elsaa_bwd.argtypes = [P, P, P, P, P, P, P, P, P, P, P, S, P, P, P, P, P, S, P]
+        lib.elsaa_profile_enable.argtypes = [C.c_int]
+        lib.elsaa_profile_count.argtypes = []
+        lib.elsaa_profile_get.argtypes = [C.c_int, C.c_char_p, S, C.POINTER(C.c_double),
+                                          C.POINTER(C.c_int64)]
         lib.elsaa_status_string.restype = C.c_char_p
         lib.elsaa_status_string.argtypes = [C.c_int]
         lib.elsaa_last_error.restype = C.c_char_p
@@ -108,6 +112,23 @@ def _p(t: Optional[torch.Tensor]):
 
 def _stream(dev) -> C.c_void_p:
     return C.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+
+
+def profile_enable(on: bool = True):
+    """Start (clearing old totals) or stop per-kernel event timing in the library."""
+    _check(load().elsaa_profile_enable(int(on)))
+
+
+def profile_read() -> dict:
+    """{kernel name: (total ms, launches)} recorded since profile_enable(True)."""
+    lib = load()
+    out = {}
+    for i in range(lib.elsaa_profile_count()):
+        buf = C.create_string_buffer(128)
+        ms, n = C.c_double(), C.c_int64()
+        _check(lib.elsaa_profile_get(i, buf, 128, C.byref(ms), C.byref(n)))
+        out[buf.value.decode()] = (ms.value, n.value)
+    return out
 
 
 def num_levels(cfg: Config) -> int:

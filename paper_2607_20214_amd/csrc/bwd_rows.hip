@@ -72,18 +72,18 @@ hipError_t launch_bwd_rows(const Shape& s, const void* dO, const float* Os, cons
 {
     const size_t BHN = (size_t)s.B * s.H * s.N;
     dim3 grid((unsigned)((BHN + 15) / 16));
-#define ELSAA_LAUNCH(T_, D_)                                                                       \
-    hipLaunchKernelGGL((bwd_rows_kernel<T_, D_>), grid, dim3(256), 0, st,                          \
+#define ELSAA_ROWS(T_, D_)                                                                       \
+    ELSAA_LAUNCH("bwd_rows", (bwd_rows_kernel<T_, D_>), grid, dim3(256), 0, st,                          \
                        (const T_::store_t*)dO, Os, Olr, m, \
                        lse, dlr, gates, rs, dgates, BHN, s.lambda, s.eps)
     if (s.bf16) {
-        if (s.D == 64) ELSAA_LAUNCH(BF16, 64);
-        else ELSAA_LAUNCH(BF16, 128);
+        if (s.D == 64) ELSAA_ROWS(BF16, 64);
+        else ELSAA_ROWS(BF16, 128);
     } else {
-        if (s.D == 64) ELSAA_LAUNCH(F32, 64);
-        else ELSAA_LAUNCH(F32, 128);
+        if (s.D == 64) ELSAA_ROWS(F32, 64);
+        else ELSAA_ROWS(F32, 128);
     }
-#undef ELSAA_LAUNCH
+#undef ELSAA_ROWS
     return hipGetLastError();
 }
 

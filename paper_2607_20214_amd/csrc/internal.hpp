@@ -22,6 +22,27 @@ struct Shape {
     int64_t P() const { return causal ? (int64_t)Lv * (N / 2) : (int64_t)N; }  // perm length per (b,h)
 };
 
+// Opt-in per-kernel event timing (elsaa_profile_enable): construct around a
+// launch; records an event pair on the stream when profiling is on.
+class ProfScope {
+public:
+    ProfScope(const char* name, hipStream_t st);
+    ~ProfScope();
+    ProfScope(const ProfScope&) = delete;
+    ProfScope& operator=(const ProfScope&) = delete;
+
+private:
+    hipStream_t stream_;
+    bool active_;
+};
+
+// hipLaunchKernelGGL with profiling: ELSAA_LAUNCH("name", kernel, grid, block, lds, stream, args...)
+#define ELSAA_LAUNCH(name, kernel, grid, block, lds, stream, ...)                 \
+    do {                                                                           \
+        ::elsaa::ProfScope prof_scope_(name, stream);                              \
+        hipLaunchKernelGGL(kernel, grid, block, lds, stream, __VA_ARGS__);         \
+    } while (0)
+
 // selection: hash keys (and the RACE projections U = W_race x when W_race
 // is not null, [BH][N][race_proj_stride]) then per-segment stable counting sort
 hipError_t launch_project(const Shape& s, const void* X, const float* W_sort, const float* W_race,

@@ -485,12 +485,12 @@ struct BwdFn {
             return hipErrorInvalidConfiguration;
         } else {
             dim3 grid(s.nseg, s.H, s.B);
-            hipLaunchKernelGGL((race_dq_kernel<T, D, RP>), grid, dim3(kThreads), 0, st, a1);
+            ELSAA_LAUNCH("race_dq", (race_dq_kernel<T, D, RP>), grid, dim3(kThreads), 0, st, a1);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
-            hipLaunchKernelGGL((race_dk_kernel<T, D, RP>), grid, dim3(kThreads), 0, st, a2);
+            ELSAA_LAUNCH("race_dk", (race_dk_kernel<T, D, RP>), grid, dim3(kThreads), 0, st, a2);
             if ((e = hipGetLastError()) != hipSuccess) return e;
-            hipLaunchKernelGGL((race_dv_kernel<T, D, RP>), grid, dim3(kThreads), 0, st, a3);
+            ELSAA_LAUNCH("race_dv", (race_dv_kernel<T, D, RP>), grid, dim3(kThreads), 0, st, a3);
             return hipGetLastError();
         }
     }

@@ -311,11 +311,11 @@ hipError_t launch_states_t(const Shape& s, const StateArgs& a, int scan_mode, hi
         return hipErrorInvalidConfiguration;
     } else {
         dim3 grid(s.nseg, s.H, s.B);
-        hipLaunchKernelGGL((race_state_kernel<T, D, RP>), grid, dim3(kThreads), 0, st, a);
+        ELSAA_LAUNCH("race_state", (race_state_kernel<T, D, RP>), grid, dim3(kThreads), 0, st, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         const int per = RP * D + RP;
-        hipLaunchKernelGGL(race_scan_kernel, dim3((per + 255) / 256, s.B * s.H), dim3(256), 0, st,
+        ELSAA_LAUNCH("race_scan", race_scan_kernel, dim3((per + 255) / 256, s.B * s.H), dim3(256), 0, st,
                            a.states, s.nseg, per, scan_mode);
         return hipGetLastError();
     }
@@ -328,7 +328,7 @@ hipError_t launch_out_t(const Shape& s, const OutArgs& a, hipStream_t st)
         return hipErrorInvalidConfiguration;
     } else {
         dim3 grid(s.nseg, s.H, s.B);
-        hipLaunchKernelGGL((race_out_kernel<T, D, RP>), grid, dim3(kThreads), 0, st, a);
+        ELSAA_LAUNCH("race_out", (race_out_kernel<T, D, RP>), grid, dim3(kThreads), 0, st, a);
         return hipGetLastError();
     }
 }

@@ -117,7 +117,7 @@ hipError_t launch_proj_t(const Shape& s, const void* X, const float* W_sort, con
     const int UP = race_proj_stride(s);
     const int wr = UP < 16 ? 16 : UP;
 #define ELSAA_PROJ(WR_)                                                                          \
-    hipLaunchKernelGGL((proj_kernel<T, D, WR_>), grid, dim3(kProjThreads), 0, st,                 \
+    ELSAA_LAUNCH("project", (proj_kernel<T, D, WR_>), grid, dim3(kProjThreads), 0, st,                 \
                        (const typename T::store_t*)X, W_sort, W_race, keys, U, s.H, s.N,          \
                        s.sort_bits, s.L, UP)
     if (wr == 16) ELSAA_PROJ(16);
@@ -231,7 +231,7 @@ hipError_t launch_sort(const Shape& s, const uint8_t* keyq, const uint8_t* keyk,
     const int tasks = s.causal ? (1 << (s.Lv + 1)) - 2 : 2;
     if (tasks <= 0) return hipSuccess;
     dim3 grid(tasks, s.H, s.B);
-    hipLaunchKernelGGL(sort_kernel, grid, dim3(kSortThreads), 0, st, keyq, keyk, perm_q, perm_k,
+    ELSAA_LAUNCH("sort", sort_kernel, grid, dim3(kSortThreads), 0, st, keyq, keyk, perm_q, perm_k,
                        s.H, s.N, s.causal, s.Lv, s.sort_bits);
     return hipGetLastError();
 }

@@ -474,22 +474,22 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st)
     hipError_t e;
     if (!s.causal) {
         dim3 grid((s.N + kT - 1) / kT, s.H, s.B);
-        hipLaunchKernelGGL((sparse_dq_kernel<T, D, kBlocks>), grid, dim3(kThreads), 0, st, a);
+        ELSAA_LAUNCH("sparse_dq_blocks", (sparse_dq_kernel<T, D, kBlocks>), grid, dim3(kThreads), 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        hipLaunchKernelGGL((sparse_dkv_kernel<T, D, kBlocks>), grid, dim3(kThreads), 0, st, a);
+        ELSAA_LAUNCH("sparse_dkv_blocks", (sparse_dkv_kernel<T, D, kBlocks>), grid, dim3(kThreads), 0, st, a);
         return hipGetLastError();
     }
     if (s.Lv > 0) {
         dim3 grid(s.Lv * (s.N / 2) / kT, s.H, s.B);
-        hipLaunchKernelGGL((sparse_dq_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
+        ELSAA_LAUNCH("sparse_dq_levels", (sparse_dq_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        hipLaunchKernelGGL((sparse_dkv_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
+        ELSAA_LAUNCH("sparse_dkv_levels", (sparse_dkv_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     dim3 grid(s.N / kT, s.H, s.B);
-    hipLaunchKernelGGL((sparse_dq_kernel<T, D, kLeaf>), grid, dim3(kThreads), 0, st, a);
+    ELSAA_LAUNCH("sparse_dq_leaf", (sparse_dq_kernel<T, D, kLeaf>), grid, dim3(kThreads), 0, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL((sparse_dkv_kernel<T, D, kLeaf>), grid, dim3(kThreads), 0, st, a);
+    ELSAA_LAUNCH("sparse_dkv_leaf", (sparse_dkv_kernel<T, D, kLeaf>), grid, dim3(kThreads), 0, st, a);
     return hipGetLastError();
 }
 

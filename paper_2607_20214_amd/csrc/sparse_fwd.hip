@@ -312,17 +312,17 @@ hipError_t launch_t(const Shape& s, const Args& a, hipStream_t st)
 {
     if (!s.causal) {
         dim3 grid((s.N + kQT - 1) / kQT, s.H, s.B);
-        hipLaunchKernelGGL((sparse_fwd_kernel<T, D, kBlocks>), grid, dim3(kThreads), 0, st, a);
+        ELSAA_LAUNCH("sparse_fwd_blocks", (sparse_fwd_kernel<T, D, kBlocks>), grid, dim3(kThreads), 0, st, a);
         return hipGetLastError();
     }
     if (s.Lv > 0) {
         dim3 grid(s.Lv * (s.N / 2) / kQT, s.H, s.B);
-        hipLaunchKernelGGL((sparse_fwd_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
+        ELSAA_LAUNCH("sparse_fwd_levels", (sparse_fwd_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     dim3 grid(s.N / kQT, s.H, s.B);
-    hipLaunchKernelGGL((sparse_fwd_kernel<T, D, kLeaf>), grid, dim3(kThreads), 0, st, a);
+    ELSAA_LAUNCH("sparse_fwd_leaf", (sparse_fwd_kernel<T, D, kLeaf>), grid, dim3(kThreads), 0, st, a);
     return hipGetLastError();
 }
 
