@@ -146,7 +146,7 @@ FwdWorkspace fwd_workspace(const Shape& s)
 }
 
 struct BwdWorkspace {
-    size_t rs, states_f, states_b, dq_lr, dk_lr, dv_lr, part_dq, part_dk, part_dv, total;
+    size_t rs, states_f, states_b, wt_hi, wt_lo, dq_lr, dk_lr, dv_lr, part_dq, part_dk, part_dv, total;
 };
 
 BwdWorkspace bwd_workspace(const Shape& s)
@@ -159,6 +159,8 @@ BwdWorkspace bwd_workspace(const Shape& s)
     W.rs = off; off = align256(off + 5 * bhn * 4);
     W.states_f = off; off = align256(off + race_state_floats(s) * 4);
     W.states_b = off; off = align256(off + race_state_floats(s) * 4);
+    W.wt_hi = off; off = align256(off + race_wt_bytes(s));
+    W.wt_lo = off; off = align256(off + race_wt_bytes(s));
     W.dq_lr = off; off = align256(off + bhn * s.D * 4);
     W.dk_lr = off; off = align256(off + bhn * s.D * 4);
     W.dv_lr = off; off = align256(off + bhn * s.D * 4);
@@ -326,7 +328,8 @@ int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     if ((e = launch_bwd_rows(s, dO, o_s, o_lr, m, lse, d_lr, gates, rs, dgates, stream)) != hipSuccess)
         return hip_fail(e, "backward row scalars");
     if ((e = launch_race_bwd(s, uq, uk, V, dO, W_race, rs, at<float>(workspace, W.states_f),
-                             at<float>(workspace, W.states_b), dq_lr, dk_lr, dv_lr, stream)) != hipSuccess)
+                             at<float>(workspace, W.states_b), at<char>(workspace, W.wt_hi),
+                             at<char>(workspace, W.wt_lo), dq_lr, dk_lr, dv_lr, stream)) != hipSuccess)
         return hip_fail(e, "race backward");
     if ((e = launch_sparse_bwd(s, Q, K, V, dO, pq, pk, rs, dq_lr, dk_lr, dv_lr,
                                at<float>(workspace, W.part_dq), at<float>(workspace, W.part_dk),

@@ -109,6 +109,17 @@ struct F32 {
     }
 };
 
+// (a_hi + a_lo) x b: product with the A operand kept in float32 accuracy
+template <class T>
+__device__ __forceinline__ f32x4 mma_split_a(const float* a, typename T::frag_t b, f32x4 c)
+{
+    typename T::frag_t hi, lo;
+    T::split(a, hi, lo);
+    c = T::mma(hi, b, c);
+    if (T::kSplit) c = T::mma(lo, b, c);
+    return c;
+}
+
 // a x (b_hi + b_lo): product with an operand kept in float32 accuracy
 template <class T>
 __device__ __forceinline__ f32x4 mma_split(typename T::frag_t a, const float* b, f32x4 c)

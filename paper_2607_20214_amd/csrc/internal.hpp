@@ -62,10 +62,11 @@ hipError_t launch_race_states(const Shape& s, const float* U, const void* Val, c
                               const float* aw, float mul, float* states, int scan_mode, hipStream_t st);
 hipError_t launch_race_fwd(const Shape& s, const float* Uq, const float* Uk, const void* V,
                            float* states, float* O_lr, float* d_lr, hipStream_t st);
+size_t race_wt_bytes(const Shape& s);       // one of the W' hi / lo buffers
 hipError_t launch_race_bwd(const Shape& s, const float* Uq, const float* Uk, const void* V,
                            const void* dO, const float* W_race, const float* rs,
-                           float* states_f, float* states_b, float* dq_lr, float* dk_lr,
-                           float* dv_lr, hipStream_t st);
+                           float* states_f, float* states_b, void* wt_hi, void* wt_lo,
+                           float* dq_lr, float* dk_lr, float* dv_lr, hipStream_t st);
 
 // sortLSH sparse branch forward + fusion epilogue
 hipError_t launch_sparse_fwd(const Shape& s, const void* Q, const void* K, const void* V,

@@ -30,7 +30,8 @@ struct LbArgs {
     const float* Uk;        // projections of K rows
     const void* V;
     const void* dO;
-    const float* W;
+    const void* wt_hi;      // W' split hi + lo, storage dtype [H][D][w_kdim]
+    const void* wt_lo;
     const float* rs;        // row scalars (sc_lr at 3*BHN, dDen at 4*BHN)
     const float* states;    // LB1: forward prefix states; LB2/LB3: backward suffix states
     float* out;             // float32 [BH][N][D]
@@ -42,8 +43,6 @@ struct LbArgs {
 template <class T, int D, int RP>
 struct Lb1Smem {
     using S = typename T::store_t;
-    S wt[D][w_kdim<RP>() + kPad];  // W' = W_hi' + W_lo'
-    S wl[T::bytes == 2 ? D : 1][w_kdim<RP>() + kPad];   // (no low part for float32)
     S vt[D][kC + kPad];            // V chunk transposed
     S dn[kC][D + kPad];            // dNum chunk, rows
     S pkt[RP][kC + kPad];          // Phi_K transposed
@@ -51,13 +50,12 @@ struct Lb1Smem {
     float ts[kC][RP / 4];          // tanh(W q) of the chunk's queries
     S du[kC][w_kdim<RP>() + kPad];
     float dden[kC];
+    float a_state[RP];             // A = sum phi(k) of the keys before the chunk
 };
 
 template <class T, int D, int RP>
 struct Lb2Smem {
     using S = typename T::store_t;
-    S wt[D][w_kdim<RP>() + kPad];  // W' = W_hi' + W_lo'
-    S wl[T::bytes == 2 ? D : 1][w_kdim<RP>() + kPad];   // (no low part for float32)
     S vr[kC][D + kPad];            // V chunk, rows
     S dnt[D][kC + kPad];           // dNum / L chunk, transposed
     S pqt[RP][kC + kPad];          // Phi_Q transposed
@@ -65,6 +63,7 @@ struct Lb2Smem {
     float ts[kC][RP / 4];          // tanh(W k) of the chunk's keys
     S du[kC][w_kdim<RP>() + kPad];
     float dden[kC];
+    float a_state[RP];             // dA = (1/L) sum phi(q) dDen of the queries after the chunk
 };
 
 template <class T, int D, int RP>
@@ -84,14 +83,14 @@ constexpr bool bwd_fits()
            sizeof(Lb3Smem<T, D, RP>) <= kMaxLds;
 }
 
-// du [64 rows][p] x (W_hi + W_lo) [p][D] -> float32 rows [16w, 16w + 16) of out (all D)
+// du [64 rows][p] x (W_hi + W_lo) [p][D] -> float32 rows [16w, 16w + 16) of out (all D);
+// W' (hi, lo) [D][w_kdim] of this head is read from global memory (L2-resident).
 template <class T, int D, int RP>
 __device__ __forceinline__ void du_times_w(const typename T::store_t (*du)[w_kdim<RP>() + kPad],
-                                           const typename T::store_t (*wt)[w_kdim<RP>() + kPad],
-                                           const typename T::store_t (*wl)[w_kdim<RP>() + kPad],
+                                           const typename T::store_t* wth, const typename T::store_t* wtl,
                                            float* out, int t0, int N)
 {
-    constexpr int DT = D / 16, KP = w_kdim<RP>() / 32;
+    constexpr int DT = D / 16, WK = w_kdim<RP>(), KP = WK / 32;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int g = lane >> 4, col = lane & 15;
 #pragma unroll
@@ -100,8 +99,9 @@ __device__ __forceinline__ void du_times_w(const typename T::store_t (*du)[w_kdi
 #pragma unroll
         for (int kp = 0; kp < KP; ++kp) {
             const auto df = T::ld8(&du[16 * w + col][32 * kp + 8 * g]);
-            acc = T::mma(df, T::ld8(&wt[16 * dt + col][32 * kp + 8 * g]), acc);
-            if (T::bytes == 2) acc = T::mma(df, T::ld8(&wl[16 * dt + col][32 * kp + 8 * g]), acc);
+            const size_t o = (size_t)(16 * dt + col) * WK + 32 * kp + 8 * g;
+            acc = T::mma(df, T::ld8(wth + o), acc);
+            if (T::kSplit) acc = T::mma(df, T::ld8(wtl + o), acc);
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -111,9 +111,24 @@ __device__ __forceinline__ void du_times_w(const typename T::store_t (*du)[w_kdi
     }
 }
 
+// W' = W_hi' + W_lo' of every head, [H][D][WK] (rows 4l + b, zero past 4L).
+template <class T>
+__global__ __launch_bounds__(256) void race_wt_kernel(const float* W, typename T::store_t* hi,
+                                                      typename T::store_t* lo, int L, int D, int WK)
+{
+    const int h = blockIdx.y;
+    const int it = blockIdx.x * 256 + threadIdx.x;
+    if (it >= D * WK) return;
+    const int d = it / WK, p = it % WK;
+    const float w = p < 4 * L ? W[((size_t)h * 4 * L + p) * D + d] : 0.f;
+    const typename T::store_t vh = T::store(w);
+    hi[((size_t)h * D + d) * WK + p] = vh;
+    lo[((size_t)h * D + d) * WK + p] = T::store(T::kSplit ? w - T::load(vh) : 0.f);
+}
+
 // ---------------------------------------------------------------- LB1: dQ
 template <class T, int D, int RP>
-__global__ __launch_bounds__(kThreads) void race_dq_kernel(LbArgs a)
+__global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
 {
     using St = typename T::store_t;
     using F = typename T::frag_t;
@@ -131,17 +146,17 @@ __global__ __launch_bounds__(kThreads) void race_dq_kernel(LbArgs a)
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int g = lane >> 4, col = lane & 15;
 
-    load_wt<T, D, w_kdim<RP>()>(sm.wt, sm.wl, a.W + (size_t)h * a.L * 4 * D, a.L);
+    const St* wth = (const St*)a.wt_hi + (size_t)h * D * w_kdim<RP>();
+    const St* wtl = (const St*)a.wt_lo + (size_t)h * D * w_kdim<RP>();
     for (int it = threadIdx.x; it < kC * (w_kdim<RP>() + kPad); it += kThreads)
         (&sm.du[0][0])[it] = T::store(0.f);
-    // state S'[d][f] for the wave's features f = 16 (w + 4j) + col, and A[f]
+    // state S'[d][f] for the wave's features f = 16 (w + 4j) + col; A[f] in LDS
     f32x4 St_[NFT][DT];
-    float ar[NFT];
     const float* st_in = a.states + (bh * a.nseg + seg) * (size_t)(RP * D + RP);
+    for (int f = threadIdx.x; f < RP; f += kThreads) sm.a_state[f] = st_in[RP * D + f];
 #pragma unroll
     for (int j = 0; j < NFT; ++j) {
         const int ft = w + 4 * j;
-        ar[j] = ft < FT ? st_in[RP * D + 16 * ft + col] : 0.f;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -185,6 +200,7 @@ __global__ __launch_bounds__(kThreads) void race_dq_kernel(LbArgs a)
             }
         }
         __syncthreads();
+        // dphi(q)' tiles [features of table ft] x [16 queries]: S G-terms + A dDen + intra
 #pragma unroll
         for (int j = 0; j < NFT; ++j) {
             const int ft = w + 4 * j;
@@ -199,23 +215,24 @@ __global__ __launch_bounds__(kThreads) void race_dq_kernel(LbArgs a)
                         sv[i] = St_[j][2 * ds][i];
                         sv[4 + i] = St_[j][2 * ds + 1][i];
                     }
-                    acc = mma_split<T>(T::ld44(&sm.dn[16 * qt + col][32 * ds + 4 * g], &sm.dn[16 * qt + col][32 * ds + 16 + 4 * g]),
-                                       sv, acc);
+                    acc = mma_split_a<T>(sv, T::ld44(&sm.dn[16 * qt + col][32 * ds + 4 * g],
+                                                     &sm.dn[16 * qt + col][32 * ds + 16 + 4 * g]), acc);
                 }
+                const float ddq = sm.dden[16 * qt + col];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) acc[i] += ar[j] * sm.dden[16 * qt + 4 * g + i];
+                for (int i = 0; i < 4; ++i) acc[i] += sm.a_state[16 * ft + 4 * g + i] * ddq;
                 if (a.causal) {
 #pragma unroll
                     for (int kk = 0; kk < 2; ++kk)
-                        acc = T::mma(T::ld8(&sm.gg[16 * qt + col][32 * kk + 8 * g]),
-                                     T::ld8(&sm.pkt[16 * ft + col][32 * kk + 8 * g]), acc);
+                        acc = T::mma(T::ld8(&sm.pkt[16 * ft + col][32 * kk + 8 * g]),
+                                     T::ld8(&sm.gg[16 * qt + col][32 * kk + 8 * g]), acc);
                 }
                 acc *= a.inv_L;
-                chain_rule<T, RP>(acc, qt, ft, a.L, a.beta, sm.ts, sm.du);
+                chain_rule_t<T, RP>(acc, qt, ft, a.L, a.beta, sm.ts, sm.du);
             }
         }
         __syncthreads();
-        du_times_w<T, D, RP>(sm.du, sm.wt, sm.wl, out, t0, a.N);
+        du_times_w<T, D, RP>(sm.du, wth, wtl, out, t0, a.N);
         if (a.causal) {
             // S' += V' Phi_K (chunk), A += Phi_K' 1
 #pragma unroll
@@ -229,10 +246,11 @@ __global__ __launch_bounds__(kThreads) void race_dq_kernel(LbArgs a)
                     for (int dt = 0; dt < DT; ++dt)
                         St_[j][dt] = T::mma(T::ld8(&sm.vt[16 * dt + col][32 * kk + 8 * g]), bf, St_[j][dt]);
                 }
-                float s = 0.f;
-#pragma unroll
-                for (int k = 0; k < 16; ++k) s += T::load(sm.pkt[16 * ft + col][16 * g + k]);
-                ar[j] += wave_sum16(s);
+            }
+            for (int f = threadIdx.x; f < RP; f += kThreads) {
+                float sacc = 0.f;
+                for (int k = 0; k < kC; ++k) sacc += T::load(sm.pkt[f][k]);
+                sm.a_state[f] += sacc;
             }
         }
     }
@@ -240,7 +258,7 @@ __global__ __launch_bounds__(kThreads) void race_dq_kernel(LbArgs a)
 
 // ---------------------------------------------------------------- LB2: dK
 template <class T, int D, int RP>
-__global__ __launch_bounds__(kThreads) void race_dk_kernel(LbArgs a)
+__global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
 {
     using St = typename T::store_t;
     using F = typename T::frag_t;
@@ -258,16 +276,16 @@ __global__ __launch_bounds__(kThreads) void race_dk_kernel(LbArgs a)
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int g = lane >> 4, col = lane & 15;
 
-    load_wt<T, D, w_kdim<RP>()>(sm.wt, sm.wl, a.W + (size_t)h * a.L * 4 * D, a.L);
+    const St* wth = (const St*)a.wt_hi + (size_t)h * D * w_kdim<RP>();
+    const St* wtl = (const St*)a.wt_lo + (size_t)h * D * w_kdim<RP>();
     for (int it = threadIdx.x; it < kC * (w_kdim<RP>() + kPad); it += kThreads)
         (&sm.du[0][0])[it] = T::store(0.f);
     f32x4 St_[NFT][DT];
-    float ar[NFT];
     const float* st_in = a.states + (bh * a.nseg + seg) * (size_t)(RP * D + RP);
+    for (int f = threadIdx.x; f < RP; f += kThreads) sm.a_state[f] = st_in[RP * D + f];
 #pragma unroll
     for (int j = 0; j < NFT; ++j) {
         const int ft = w + 4 * j;
-        ar[j] = ft < FT ? st_in[RP * D + 16 * ft + col] : 0.f;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -314,6 +332,7 @@ __global__ __launch_bounds__(kThreads) void race_dk_kernel(LbArgs a)
             }
         }
         __syncthreads();
+        // dphi(k)' tiles [features of table ft] x [16 keys]: dS V + dA + intra
 #pragma unroll
         for (int j = 0; j < NFT; ++j) {
             const int ft = w + 4 * j;
@@ -328,22 +347,22 @@ __global__ __launch_bounds__(kThreads) void race_dk_kernel(LbArgs a)
                         sv[i] = St_[j][2 * ds][i];
                         sv[4 + i] = St_[j][2 * ds + 1][i];
                     }
-                    acc = mma_split<T>(T::ld44(&sm.vr[16 * kt + col][32 * ds + 4 * g], &sm.vr[16 * kt + col][32 * ds + 16 + 4 * g]),
-                                       sv, acc);
+                    acc = mma_split_a<T>(sv, T::ld44(&sm.vr[16 * kt + col][32 * ds + 4 * g],
+                                                     &sm.vr[16 * kt + col][32 * ds + 16 + 4 * g]), acc);
                 }
 #pragma unroll
-                for (int i = 0; i < 4; ++i) acc[i] += ar[j];
+                for (int i = 0; i < 4; ++i) acc[i] += sm.a_state[16 * ft + 4 * g + i];
                 if (a.causal) {
 #pragma unroll
                     for (int kk = 0; kk < 2; ++kk)
-                        acc = T::mma(T::ld8(&sm.ggt[16 * kt + col][32 * kk + 8 * g]),
-                                     T::ld8(&sm.pqt[16 * ft + col][32 * kk + 8 * g]), acc);
+                        acc = T::mma(T::ld8(&sm.pqt[16 * ft + col][32 * kk + 8 * g]),
+                                     T::ld8(&sm.ggt[16 * kt + col][32 * kk + 8 * g]), acc);
                 }
-                chain_rule<T, RP>(acc, kt, ft, a.L, a.beta, sm.ts, sm.du);
+                chain_rule_t<T, RP>(acc, kt, ft, a.L, a.beta, sm.ts, sm.du);
             }
         }
         __syncthreads();
-        du_times_w<T, D, RP>(sm.du, sm.wt, sm.wl, out, t0, a.N);
+        du_times_w<T, D, RP>(sm.du, wth, wtl, out, t0, a.N);
         if (a.causal) {
             // dS' += (dNum / L)' Phi_Q (chunk), dA += (1/L) Phi_Q' dDen
 #pragma unroll
@@ -357,10 +376,11 @@ __global__ __launch_bounds__(kThreads) void race_dk_kernel(LbArgs a)
                     for (int dt = 0; dt < DT; ++dt)
                         St_[j][dt] = T::mma(T::ld8(&sm.dnt[16 * dt + col][32 * kk + 8 * g]), bf, St_[j][dt]);
                 }
-                float s = 0.f;
-#pragma unroll
-                for (int k = 0; k < 16; ++k) s += T::load(sm.pqt[16 * ft + col][16 * g + k]) * sm.dden[16 * g + k];
-                ar[j] += wave_sum16(s) * a.inv_L;
+            }
+            for (int f = threadIdx.x; f < RP; f += kThreads) {
+                float sacc = 0.f;
+                for (int k = 0; k < kC; ++k) sacc += T::load(sm.pqt[f][k]) * sm.dden[k];
+                sm.a_state[f] += sacc * a.inv_L;
             }
         }
     }
@@ -525,11 +545,31 @@ hipError_t dispatch(const Shape& s, A&&... args)
 
 bool race_bwd_fits(const Shape& s) { return dispatch<BwdFitsFn>(s) == hipSuccess; }
 
+size_t race_wt_bytes(const Shape& s)
+{
+    const int rp = race_padded_features(s.r);
+    const size_t wk = rp / 4 < 32 ? 32 : rp / 4;
+    return (size_t)s.H * s.D * wk * (s.bf16 ? 2 : 4);
+}
+
 hipError_t launch_race_bwd(const Shape& s, const float* Uq, const float* Uk, const void* V,
                            const void* dO, const float* W_race, const float* rs,
-                           float* states_f, float* states_b, float* dq_lr, float* dk_lr,
-                           float* dv_lr, hipStream_t st)
+                           float* states_f, float* states_b, void* wt_hi, void* wt_lo,
+                           float* dq_lr, float* dk_lr, float* dv_lr, hipStream_t st)
 {
+    {
+        const int rp = race_padded_features(s.r);
+        const int wk = rp / 4 < 32 ? 32 : rp / 4;
+        dim3 grid((s.D * wk + 255) / 256, s.H);
+        if (s.bf16)
+            ELSAA_LAUNCH("race_wt", race_wt_kernel<BF16>, grid, dim3(256), 0, st, W_race,
+                         (uint16_t*)wt_hi, (uint16_t*)wt_lo, s.L, s.D, wk);
+        else
+            ELSAA_LAUNCH("race_wt", race_wt_kernel<F32>, grid, dim3(256), 0, st, W_race, (float*)wt_hi,
+                         (float*)wt_lo, s.L, s.D, wk);
+        hipError_t e0 = hipGetLastError();
+        if (e0 != hipSuccess) return e0;
+    }
     const size_t BHN = (size_t)s.B * s.H * s.N;
     // forward prefix states of phi(k) V' and phi(k); backward suffix states
     // of phi(q) dNum' / L and phi(q) dDen / L
@@ -539,7 +579,7 @@ hipError_t launch_race_bwd(const Shape& s, const float* Uq, const float* Uk, con
                            s.causal ? 2 : 0, st);
     if (e != hipSuccess) return e;
     LbArgs a;
-    a.Uq = Uq; a.Uk = Uk; a.V = V; a.dO = dO; a.W = W_race; a.rs = rs;
+    a.Uq = Uq; a.Uk = Uk; a.V = V; a.dO = dO; a.wt_hi = wt_hi; a.wt_lo = wt_lo; a.rs = rs;
     a.H = s.H; a.N = s.N; a.L = s.L; a.seg_len = s.seg_len; a.nseg = s.nseg; a.causal = s.causal;
     a.BHN = BHN;
     a.two_beta = 2.f * s.beta; a.beta = s.beta; a.inv_L = 1.f / (float)s.L;

@@ -20,21 +20,6 @@ constexpr size_t kMaxLds = 160 * 1024;
 // projection count padded to whole 32-wide k-steps (backward du x W)
 template <int RP> constexpr int w_kdim() { return RP / 4 < 32 ? 32 : RP / 4; }
 
-// W' of one head split as W = W_hi + W_lo (W_lo is zero for float32 storage):
-// wt_hi[d][row], wt_lo[d][row], rows 4l + b (l < L), zero up to WK.
-template <class T, int D, int WK>
-__device__ void load_wt(typename T::store_t (*wt_hi)[WK + kPad], typename T::store_t (*wt_lo)[WK + kPad],
-                        const float* W, int L)
-{
-    for (int it = threadIdx.x; it < WK * D; it += kThreads) {
-        const int row = it % WK, c = it / WK;
-        const float w = row < 4 * L ? W[(size_t)row * D + c] : 0.f;
-        const typename T::store_t hi = T::store(w);
-        wt_hi[c][row] = hi;
-        if (T::bytes == 2) wt_lo[c][row] = T::store(w - T::load(hi));
-    }
-}
-
 // Rows [t0, t0 + 64) of X (zero past N), each multiplied by scale[row] when
 // scale != nullptr, into a transposed tile xt[d][token].
 template <class T, int D>
@@ -139,48 +124,56 @@ __device__ void features(const float* U, int t0, int N, int L, float two_beta,
     }
 }
 
-// Chain rule from a feature-gradient tile to the projection gradients du.
-// dphi: accumulator tile of 16 rows x the 16 features of table tb (lane
-// (g, col) register i holds row 16*qt + 4g + i, feature c = col).  With
-// phi_c = prod_b sigmoid(2 beta v_cb t_b) and t = tanh(u):
+// Chain rule from a transposed feature-gradient tile to the projection
+// gradients du.  dphi: accumulator tile of the 16 features of table tb x 16
+// rows (lane (g, col) register i holds feature c = 4g + i of row
+// 16*qt + col).  With phi_c = prod_b sigmoid(2 beta v_cb t_b), t = tanh(u):
 //   dt_b = beta * sum_c dphi_c phi_c (v_cb - tanh(beta t_b)),  du_b = dt_b (1 - t_b^2)
-// (tanh(beta t_b) = sigmoid(2 beta t_b) - sigmoid(-2 beta t_b) is the mean of v_cb
-// under phi).  Writes du[row][4 tb + b], zero for padded tables.
+// (tanh(beta t_b) = sigmoid(2 beta t_b) - sigmoid(-2 beta t_b) is the mean of
+// v_cb under phi).  Sums over c: 4 registers, then the 4 lane groups.  Lane
+// group g writes du[row][4 tb + g] (zero for padded tables).
 template <class T, int RP>
-__device__ __forceinline__ void chain_rule(f32x4 dphi, int qt, int tb, int L, float beta,
-                                           const float (*ts)[RP / 4],
-                                           typename T::store_t (*du)[w_kdim<RP>() + kPad])
+__device__ __forceinline__ void chain_rule_t(f32x4 dphi, int qt, int tb, int L, float beta,
+                                             const float (*ts)[RP / 4],
+                                             typename T::store_t (*du)[w_kdim<RP>() + kPad])
 {
     const int lane = threadIdx.x & 63;
     const int g = lane >> 4, col = lane & 15;
+    const int row = 16 * qt + col;
     const float two_beta = 2.f * beta;
+    float t[4], sp[4], sn[4];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+        t[b] = ts[row][4 * tb + b];
+        sp[b] = 1.f / (1.f + __expf(-two_beta * t[b]));
+        sn[b] = 1.f / (1.f + __expf(two_beta * t[b]));
+    }
+    // features c = 4g + i: bits 0, 1 from i, bits 2, 3 from g
+    const float hi = ((g & 1) ? sp[2] : sn[2]) * ((g & 2) ? sp[3] : sn[3]);
+    float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int row = 16 * qt + 4 * g + i;
-        float t[4], sp[4], sn[4];
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-            t[b] = ts[row][4 * tb + b];
-            sp[b] = 1.f / (1.f + __expf(-two_beta * t[b]));
-            sn[b] = 1.f / (1.f + __expf(two_beta * t[b]));
-        }
-        float phi = 1.f;
-#pragma unroll
-        for (int b = 0; b < 4; ++b) phi *= ((col >> b) & 1) ? sp[b] : sn[b];
+        const float phi = ((i & 1) ? sp[0] : sn[0]) * ((i & 2) ? sp[1] : sn[1]) * hi;
         const float x = dphi[i] * phi;
-        const float s0 = row_sum16(x);
-        float sb[4];
-#pragma unroll
-        for (int b = 0; b < 4; ++b) sb[b] = row_sum16(((col >> b) & 1) ? x : -x);
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-            if (col == b) {
-                const float dt = beta * (sb[b] - (sp[b] - sn[b]) * s0);
-                const float v = dt * (1.f - t[b] * t[b]);
-                du[row][4 * tb + b] = T::store(tb < L ? v : 0.f);
-            }
-        }
+        s0 += x;
+        s1 += (i & 1) ? x : -x;
+        s2 += (i & 2) ? x : -x;
     }
+    // bits 2 and 3 are constant within the lane group
+    s3 = (g & 2) ? s0 : -s0;
+    const float s2g = (g & 1) ? s0 : -s0;
+    s0 = wave_sum16(s0);
+    s1 = wave_sum16(s1);
+    s2 = wave_sum16(s2);
+    const float s2b = wave_sum16(s2g);
+    s3 = wave_sum16(s3);
+    // sums over c of x_c v_cb for b = 0..3
+    const float sb[4] = {s1, s2, s2b, s3};
+    float v = 0.f;
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+        if (b == g) v = beta * (sb[b] - (sp[b] - sn[b]) * s0) * (1.f - t[b] * t[b]);
+    du[row][4 * tb + g] = T::store(tb < L ? v : 0.f);
 }
 
 }  // namespace race

@@ -53,7 +53,8 @@ struct BArgs {
 };
 
 // Rows [0, 64) of X listed in idx (-1 = zero row) into a row-major tile and,
-// when xt != nullptr, its transpose.
+// when xt != nullptr, its transpose.  Each thread loads 16-byte pieces of a
+// pair of rows once and writes them to both layouts.
 template <class T, int D>
 __device__ __forceinline__ void stage_rows(const typename T::store_t* X, const int32_t* idx,
                                            typename T::store_t (*x)[D + kPad],
@@ -62,22 +63,15 @@ __device__ __forceinline__ void stage_rows(const typename T::store_t* X, const i
     using S = typename T::store_t;
     constexpr int PER = 16 / T::bytes;
     constexpr int CH = D / PER;
-    if (x) {
-        for (int it = threadIdx.x; it < kT * CH; it += kThreads) {
-            const int row = it & (kT - 1), c = it / kT;
-            const int tok = idx[row];
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (tok >= 0) v = ldg16(X + (size_t)tok * D + c * PER);
-            *(uint4*)&x[row][c * PER] = v;
-        }
-    }
-    if (xt) {
-        for (int it = threadIdx.x; it < (kT / 2) * CH; it += kThreads) {
-            const int p = it & (kT / 2 - 1), c = it / (kT / 2);
-            const int t0 = idx[2 * p], t1 = idx[2 * p + 1];
-            uint4 a = make_uint4(0, 0, 0, 0), b = make_uint4(0, 0, 0, 0);
-            if (t0 >= 0) a = ldg16(X + (size_t)t0 * D + c * PER);
-            if (t1 >= 0) b = ldg16(X + (size_t)t1 * D + c * PER);
+    for (int it = threadIdx.x; it < (kT / 2) * CH; it += kThreads) {
+        const int p = it & (kT / 2 - 1), c = it / (kT / 2);
+        const int t0 = idx[2 * p], t1 = idx[2 * p + 1];
+        uint4 a = make_uint4(0, 0, 0, 0), b = make_uint4(0, 0, 0, 0);
+        if (t0 >= 0) a = ldg16(X + (size_t)t0 * D + c * PER);
+        if (t1 >= 0) b = ldg16(X + (size_t)t1 * D + c * PER);
+        *(uint4*)&x[2 * p][c * PER] = a;
+        *(uint4*)&x[2 * p + 1][c * PER] = b;
+        if (xt) {
             const S* ea = (const S*)&a;
             const S* eb = (const S*)&b;
 #pragma unroll
@@ -121,7 +115,7 @@ __device__ __forceinline__ size_t level_slot(size_t bh, int Lv, int l, int N, in
 // dQ: query-centric
 // ------------------------------------------------------------------------
 template <class T, int D, int MODE>
-__global__ __launch_bounds__(kThreads) void sparse_dq_kernel(BArgs a)
+__global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
 {
     using S = typename T::store_t;
     using F = typename T::frag_t;
@@ -275,7 +269,7 @@ __global__ __launch_bounds__(kThreads) void sparse_dq_kernel(BArgs a)
 // dK, dV: key-centric
 // ------------------------------------------------------------------------
 template <class T, int D, int MODE>
-__global__ __launch_bounds__(kThreads) void sparse_dkv_kernel(BArgs a)
+__global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
 {
     using S = typename T::store_t;
     using F = typename T::frag_t;
