@@ -138,6 +138,45 @@ int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
               void* dQ, void* dK, void* dV, float* dgates,
               void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Dense projections of the attention block (Alg. 1 and Alg. 6: Q = X W_Q,
+ * K = X W_K, V = X W_V before the operator, O_head W_O after it; the paper
+ * keeps these matrices dense, Sec. 1 and the parameter-overhead appendix).
+ *
+ * elsaa_gemm computes C = op(A) op(B) with op(A) [M,K], op(B) [K,N],
+ * C [M,N], bfloat16 operands and float32 accumulation; C is bfloat16 or
+ * float32 (c_dtype).  op(X) = X, or X^T when trans_x = 1, of the STORED
+ * matrix X: A is stored [M,K] (trans_a = 0) or [K,M] (trans_a = 1), B is
+ * stored [K,N] (trans_b = 0) or [N,K] (trans_b = 1).
+ *
+ * Each stored matrix (and C) is in one of two layouts, chosen per operand:
+ *   plain       row-major with row stride ld (elements), ld >= its columns;
+ *   head-major  (x_heads = Hx > 0) the stored matrix of R rows and Hx * dh
+ *               columns is kept as [R / seq][Hx][seq][dh] contiguous: row
+ *               r = b * seq + n, column c = h * dh + e lives at
+ *               ((b * Hx + h) * seq + n) * dh + e.  This is the [B,H,N,d_h]
+ *               layout of Q, K, V, O and their gradients, so the projections
+ *               read and write attention tensors without a reshape copy.
+ *               dh = columns / Hx must be a multiple of 8 and R a multiple
+ *               of seq; ld is ignored.
+ * Requirements: M, N, K >= 1 and multiples of 8, plain ld multiples of 8,
+ * pointers 16-byte aligned, A / B / C not overlapping.  A and B are never
+ * written.  When the output has few tiles and K is long, the K range is
+ * split over workgroups whose float32 partial products go to `workspace`
+ * (elsaa_gemm_workspace_bytes; 0 when no split is used) and are summed in a
+ * fixed order, so results are deterministic run to run. */
+typedef struct {
+    int32_t M, N, K;
+    int32_t trans_a, trans_b;
+    int64_t lda, ldb, ldc;
+    int32_t a_heads, b_heads, c_heads;   /* 0 = plain, Hx > 0 = head-major */
+    int32_t seq;                         /* rows per sequence of head-major operands */
+    int32_t c_dtype;                     /* elsaa_dtype of C */
+} elsaa_gemm_desc;
+
+int elsaa_gemm_workspace_bytes(const elsaa_gemm_desc* desc, size_t* bytes);
+int elsaa_gemm(const elsaa_gemm_desc* desc, const void* A, const void* B, void* C,
+               void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Opt-in kernel timing.  While enabled, every kernel launch of the library
  * is bracketed by two HIP events recorded on its stream (one extra event pair
  * per launch, no synchronisation); elsaa_profile_count / elsaa_profile_get

@@ -191,3 +191,6 @@ def head_cfg(w, **over) -> HeadCfg:
               sort_bits=w.sort_bits, n0=getattr(w, "base_len", None))
     kw.update(over)
     return HeadCfg(**kw)
+
+
+from .projections import gemm, heads_to_matrix, matrix_to_heads  # noqa: E402,F401

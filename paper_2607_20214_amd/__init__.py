@@ -45,6 +45,13 @@ class _SavedLayout(C.Structure):
                 ("u_k", C.c_size_t), ("total", C.c_size_t)]
 
 
+class _GemmDesc(C.Structure):
+    _fields_ = [("M", C.c_int32), ("N", C.c_int32), ("K", C.c_int32), ("trans_a", C.c_int32),
+                ("trans_b", C.c_int32), ("lda", C.c_int64), ("ldb", C.c_int64), ("ldc", C.c_int64),
+                ("a_heads", C.c_int32), ("b_heads", C.c_int32), ("c_heads", C.c_int32),
+                ("seq", C.c_int32), ("c_dtype", C.c_int32)]
+
+
 @dataclasses.dataclass
 class Config:
     """Operator settings (names follow the paper; see include/elsaa.h)."""
@@ -90,6 +97,8 @@ def load():
         lib.elsaa_select.argtypes = [P, P, P, P, P, P, P, S, P]
         lib.elsaa_fwd.argtypes = [P, P, P, P, P, P, P, P, P, P, P, S, P, S, P]
         lib.elsaa_bwd.argtypes = [P, P, P, P, P, P, P, P, P, P, P, S, P, P, P, P, P, S, P]
+        lib.elsaa_gemm_workspace_bytes.argtypes = [P, C.POINTER(C.c_size_t)]
+        lib.elsaa_gemm.argtypes = [P, P, P, P, P, S, P]
         lib.elsaa_profile_enable.argtypes = [C.c_int]
         lib.elsaa_profile_count.argtypes = []
         lib.elsaa_profile_get.argtypes = [C.c_int, C.c_char_p, S, C.POINTER(C.c_double),
@@ -265,3 +274,73 @@ def bwd(cfg: Config, q, k, v, w_race, do, lse, d_lr, saved, gates=None, want_dga
                             _p(bufs.dv), _p(dg), _p(bufs.workspace), bufs.workspace.numel(),
                             _stream(dev)))
     return (bufs.dq, bufs.dk, bufs.dv) + ((dg,) if want_dgates else ())
+
+
+# ---------------------------------------------------------------------------
+# dense projections (elsaa_gemm)
+# ---------------------------------------------------------------------------
+def _matrix(name, t):
+    """(rows, cols, ld, heads, seq) of a stored operand: a 2-D tensor with unit
+    column stride (plain) or a contiguous 4-D [B, H, S, dh] tensor (head-major,
+    logical rows B*S and columns H*dh)."""
+    if t.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError(f"{name}: unsupported dtype {t.dtype}")
+    if t.dim() == 2:
+        if t.stride(1) != 1:
+            raise ValueError(f"{name}: the last dimension must be contiguous")
+        return t.shape[0], t.shape[1], t.stride(0), 0, 0
+    if t.dim() == 4:
+        if not t.is_contiguous():
+            raise ValueError(f"{name}: head-major operands must be contiguous [B, H, S, dh]")
+        Bb, H, S, dh = t.shape
+        return Bb * S, H * dh, 0, H, S
+    raise ValueError(f"{name}: expected a 2-D matrix or a 4-D [B, H, S, dh] tensor")
+
+
+def gemm_plan(a, b, trans_a=False, trans_b=False, out=None):
+    """Descriptor of out = op(a) op(b) (see gemm)."""
+    ar, ac, lda, ah, aseq = _matrix("a", a)
+    br, bc, ldb, bh, bseq = _matrix("b", b)
+    M, K = (ac, ar) if trans_a else (ar, ac)
+    K2, N = (bc, br) if trans_b else (br, bc)
+    if K != K2:
+        raise ValueError(f"inner dimensions differ: {K} vs {K2}")
+    cr, cc, ldc, ch, cseq = _matrix("out", out) if out is not None else (M, N, N, 0, 0)
+    if (cr, cc) != (M, N):
+        raise ValueError(f"out: expected a {M} x {N} matrix, got {cr} x {cc}")
+    seqs = {s for s in (aseq, bseq, cseq) if s}
+    if len(seqs) > 1:
+        raise ValueError(f"head-major operands with different sequence lengths {sorted(seqs)}")
+    seq = seqs.pop() if seqs else 0
+    c_dtype = BF16 if out is None or out.dtype == torch.bfloat16 else F32
+    return _GemmDesc(M, N, K, int(trans_a), int(trans_b), lda, ldb, ldc, ah, bh, ch, seq, c_dtype)
+
+
+def gemm_workspace_bytes(desc: _GemmDesc) -> int:
+    n = C.c_size_t()
+    _check(load().elsaa_gemm_workspace_bytes(C.byref(desc), C.byref(n)))
+    return n.value
+
+
+def gemm(a, b, trans_a=False, trans_b=False, out=None, out_dtype=torch.bfloat16,
+         workspace: Optional[torch.Tensor] = None):
+    """out = op(a) @ op(b) on the matrix cores: bfloat16 operands, float32
+    accumulation, op(x) = x.T when trans_x.  Operands and `out` are 2-D
+    matrices (unit column stride) or contiguous head-major [B, H, S, dh]
+    tensors standing for the [B*S, H*dh] matrix.  Without `out`, a plain
+    [M, N] tensor of out_dtype is allocated."""
+    if a.dtype != torch.bfloat16 or b.dtype != torch.bfloat16:
+        raise ValueError("gemm operands must be bfloat16")
+    if a.device != b.device:
+        raise ValueError("operands on different devices")
+    desc = gemm_plan(a, b, trans_a, trans_b, out)
+    if out is None:
+        out = torch.empty(desc.M, desc.N, dtype=out_dtype, device=a.device)
+        desc.ldc = desc.N
+        desc.c_dtype = BF16 if out_dtype == torch.bfloat16 else F32
+    ws = gemm_workspace_bytes(desc)
+    if ws and (workspace is None or workspace.numel() < ws):
+        workspace = torch.empty(ws, dtype=torch.uint8, device=a.device)
+    _check(load().elsaa_gemm(C.byref(desc), _p(a), _p(b), _p(out), _p(workspace) if ws else None,
+                             workspace.numel() if ws else 0, _stream(a.device)))
+    return out

@@ -30,6 +30,23 @@ int hip_fail(hipError_t e, const char* what)
     return fail(ELSAA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+}  // namespace
+
+int elsaa::api_fail(int code, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int elsaa::api_hip_fail(hipError_t e, const char* what) { return hip_fail(e, what); }
+
+namespace {
+
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // Levels of the causal recursion (Alg. 5): smallest Lv with N / 2^Lv <= n0;

@@ -158,6 +158,20 @@ __device__ __forceinline__ float row_sum16(float v)    // sum over the 16 lanes 
     return v;
 }
 
+// Transposed LDS read of 16-bit data (ds_read_b64_tr_b16, gfx950).  Within
+// each group of 16 lanes, lane s supplies the LDS address of 4 contiguous
+// elements; lane i receives element i % 4 of the pieces supplied by lanes
+// i / 4 + 4 j, j = 0..3.  When lane s points at row kb + s / 4, columns
+// c0 + 4 (s % 4) of a tile stored [k][c] (c contiguous), lane i receives
+// column c0 + i at rows kb .. kb + 3: four consecutive k of one operand row.
+__device__ __forceinline__ bf16x4 lds_read_tr4(const uint16_t* p)
+{
+    typedef short s16x4 __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
+    return __builtin_bit_cast(bf16x4, v);
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Row order of a 64-row tile fed through four 16-row score sub-tiles so that

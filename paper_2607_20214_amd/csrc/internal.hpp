@@ -22,6 +22,10 @@ struct Shape {
     int64_t P() const { return causal ? (int64_t)Lv * (N / 2) : (int64_t)N; }  // perm length per (b,h)
 };
 
+// Record an error message for elsaa_last_error() and return `code`.
+int api_fail(int code, const char* fmt, ...);
+int api_hip_fail(hipError_t e, const char* what);
+
 // Opt-in per-kernel event timing (elsaa_profile_enable): construct around a
 // launch; records an event pair on the stream when profiling is on.
 class ProfScope {

@@ -177,3 +177,9 @@ BLOCK_32K = Workload("block-32k-dmodel1024-bf16", 1, 16, 32768, 64, 128, 128, Tr
                      recipe="iid", seed=5, d_model=1024)
 
 WORKLOADS = {w.name: w for w in (TINY_FP32, CLUSTERED_4K, CAUSAL_16K, CAUSAL_64K_MIXED, BLOCK_32K)}
+
+
+def random_matrix(seed: int, tid: int, shape, scale: float = 1.0) -> np.ndarray:
+    """Seeded N(0, scale^2) float32 array rounded to bf16 values (matrix-core
+    operands of the projection tests)."""
+    return bf16_round(_normal(seed, tid, shape) * np.float32(scale))

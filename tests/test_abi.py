@@ -85,3 +85,41 @@ def test_workspace_too_small_is_rejected():
     rc = lib.elsaa_fwd(C.byref(c), fake, fake, fake, fake, fake, None, fake, fake, fake, fake, 16,
                        fake, 1 << 30, None)
     assert rc == -3
+
+
+def _gdesc(**kw):
+    d = E._GemmDesc(M=256, N=256, K=256, trans_a=0, trans_b=0, lda=256, ldb=256, ldc=256,
+                    a_heads=0, b_heads=0, c_heads=0, seq=0, c_dtype=E.BF16)
+    for k, v in kw.items():
+        setattr(d, k, v)
+    return d
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(M=0), -1), (dict(K=-8), -1), (dict(M=100), -2), (dict(trans_a=2), -1), (dict(c_dtype=5), -1),
+    (dict(lda=100), -1), (dict(ldb=260), -1), (dict(a_heads=3, seq=256), -1),
+    (dict(a_heads=4, seq=100), -1), (dict(a_heads=2, lda=0, seq=256), None),
+    (dict(b_heads=64, seq=256), -2), (dict(N=192, b_heads=2, seq=256), -2),
+])
+def test_gemm_validation(kw, status):
+    lib = E.load()
+    d = _gdesc(**kw)
+    fake = C.c_void_p(1 << 20)   # never dereferenced: validation fails before any launch
+    rc = lib.elsaa_gemm(C.byref(d), fake, fake, None if status is None else fake, None, 0, None)
+    if status is None:           # the only error left is the NULL output pointer
+        assert rc == -1 and b"C is NULL" in lib.elsaa_last_error()
+    else:
+        assert rc == status, lib.elsaa_last_error()
+
+
+def test_gemm_split_workspace_and_checks():
+    lib = E.load()
+    d = _gdesc(M=1024, N=3072, K=32768, lda=1024, ldb=3072, ldc=3072, trans_a=1)
+    n = E.gemm_workspace_bytes(d)
+    assert n > 0 and n % (1024 * 3072 * 4) == 0      # float32 partials, whole planes
+    assert E.gemm_workspace_bytes(_gdesc()) == 0      # 4 tiles, K = 256: no split
+    fake = C.c_void_p(1 << 20)
+    assert lib.elsaa_gemm(C.byref(d), fake, fake, fake, None, 0, None) == -1
+    assert lib.elsaa_gemm(C.byref(d), fake, fake, fake, fake, n - 1, None) == -3
+    bad = C.c_void_p((1 << 20) + 8)
+    assert lib.elsaa_gemm(C.byref(_gdesc()), bad, fake, fake, None, 0, None) == -1
