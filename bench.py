@@ -68,6 +68,14 @@ def kernel_model(w, Lv: int) -> dict:
     m["sparse_dq_blocks"] = (bh * N * (4 * D * s + D * s + 12), bh * N * min(k, N) * 6 * D)
     m["sparse_dkv_blocks"] = (bh * N * (4 * D * s + 2 * D * s + 12), bh * N * min(k, N) * 8 * D)
     del seg_states, n0
+    if w.d_model:
+        # the six dense products of one block step (bf16 operands; Q/K/V, dO
+        # written bf16, Y and the gradients of X and the weights float32)
+        T, dm = w.B * w.N, w.d_model
+        prods = [(T, 3 * dm, dm, 2), (T, dm, dm, 4), (T, dm, dm, 2),
+                 (dm, dm, T, 4), (T, dm, 3 * dm, 4), (dm, 3 * dm, T, 4)]
+        m["gemm"] = (sum(2 * (M * K + K * N_) + o * M * N_ for M, N_, K, o in prods),
+                     sum(2 * M * N_ * K for M, N_, K, _ in prods))
     return m
 
 
@@ -87,6 +95,7 @@ KERNEL_SOURCES = {
     "race_dk": ["race_bwd.hip", "race_common.hpp", "common.hpp"],
     "race_dv": ["race_bwd.hip", "race_common.hpp", "common.hpp"],
     "bwd_rows": ["bwd_rows.hip", "common.hpp"],
+    "gemm": ["gemm.hip", "common.hpp"], "gemm_reduce": ["gemm.hip"],
 }
 
 
@@ -144,6 +153,45 @@ def cpu_baseline(w, inp, min_seconds: float = 10.0) -> dict:
                       f"{dt:.1f} s, scaled to {total} heads"}
 
 
+def cpu_baseline_block(w, inp, blk, min_seconds: float = 10.0) -> dict:
+    """Oracle of one attention-block step on a bounded sample: the six
+    float64 products on a slice of the tokens and the operator forward +
+    backward on whole heads, each scaled to the full step."""
+    import numpy as np
+    import oracle
+
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
+    T, dm = w.B * w.N, w.d_model
+    rows = 2048
+    X = blk["X"].reshape(T, dm)[:rows]
+    dY = blk["dY"].reshape(T, dm)[:rows]
+    Wqkv = np.concatenate([blk["W_Q"], blk["W_K"], blk["W_V"]], axis=1)
+    t0 = time.perf_counter()
+    qkv = oracle.gemm(X, Wqkv)
+    O = qkv[:, :dm]
+    oracle.gemm(O, blk["W_O"])
+    dO = oracle.gemm(dY, blk["W_O"], False, True)
+    oracle.gemm(O, dY, True, False)
+    oracle.gemm(qkv, Wqkv, False, True)
+    oracle.gemm(X, qkv, True, False)
+    t_gemm = (time.perf_counter() - t0) * T / rows
+    del dO
+    hc = oracle.head_cfg(w)
+    done = 0
+    t1 = time.perf_counter()
+    for h in range(w.H):
+        args = (inp["Q"][0, h], inp["K"][0, h], inp["V"][0, h], inp["W_sort"][h], inp["W_race"][h])
+        oracle.forward(hc, *args)
+        oracle.backward(hc, *args, inp["dO"][0, h])
+        done += 1
+        if time.perf_counter() - t1 >= min_seconds:
+            break
+    t_att = (time.perf_counter() - t1) * (w.B * w.H) / done
+    return {"value": T / (t_gemm + t_att), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"projections on {rows} of {T} tokens and the operator on {done} of "
+                      f"{w.B * w.H} heads, scaled to the full step"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -186,6 +234,35 @@ def main():
         o, lse, dlr, saved = E.fwd(cfg, q, k, v, ws, wr, buffers=bufs)
         E.bwd(cfg, q, k, v, wr, do, lse, dlr, saved, buffers=bufs)
 
+    blk = None
+    if w.d_model:
+        # one attention-block step: projections on the matrix cores around the
+        # operator, all attention tensors head-major [B, 3H or H, N, d_h]
+        assert w.B == 1, "the block step keeps Q, K, V as heads of one [1, 3H, N, d] buffer"
+        blk = W.make_block_inputs(w)
+        Tn, dm, H = w.B * w.N, w.d_model, w.H
+        bf = torch.bfloat16
+        X = to(blk["X"].reshape(Tn, dm), bf)
+        dY = to(blk["dY"].reshape(Tn, dm), bf)
+        Wqkv = to(np.concatenate([blk["W_Q"], blk["W_K"], blk["W_V"]], axis=1), bf)
+        Wo = to(blk["W_O"], bf)
+        qkv = torch.empty(1, 3 * H, w.N, w.d, dtype=bf, device=dev)
+        dqkv = torch.empty_like(qkv)
+        do_h = torch.empty(1, H, w.N, w.d, dtype=bf, device=dev)
+        q, k, v = qkv[:, :H], qkv[:, H:2 * H], qkv[:, 2 * H:]
+        bufs.dq, bufs.dk, bufs.dv = dqkv[:, :H], dqkv[:, H:2 * H], dqkv[:, 2 * H:]
+        gws = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+
+        def step():
+            E.gemm(X, Wqkv, out=qkv, workspace=gws)
+            o, lse, dlr, saved = E.fwd(cfg, q, k, v, ws, wr, buffers=bufs)
+            E.gemm(o, Wo, out_dtype=torch.float32, workspace=gws)                # Y
+            E.gemm(dY, Wo, trans_b=True, out=do_h, workspace=gws)                # dO
+            E.gemm(o, dY, trans_a=True, out_dtype=torch.float32, workspace=gws)  # dW_O
+            E.bwd(cfg, q, k, v, wr, do_h, lse, dlr, saved, buffers=bufs)
+            E.gemm(dqkv, Wqkv, trans_b=True, out_dtype=torch.float32, workspace=gws)  # dX
+            E.gemm(X, dqkv, trans_a=True, out_dtype=torch.float32, workspace=gws)     # dW_qkv
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -207,6 +284,8 @@ def main():
     avg_s = ms_total / launches / 1e3
     model = kernel_model(w, Lv)
     nbytes, nflops = model.get(dom, (0, 0))
+    per_launch = launches // args.steps          # launches of that kernel in one step
+    nbytes, nflops = nbytes / per_launch, nflops / per_launch
     t_hbm = nbytes / (PEAK_HBM_GBS * 1e9)
     peak_tf = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     t_mma = nflops / (peak_tf * 1e12)
@@ -224,8 +303,11 @@ def main():
     roof["algorithmic_bytes_per_launch"] = nbytes
     roof["algorithmic_flops_per_launch"] = nflops
 
+    metric = "ELSAA fwd+bwd tokens/sec at N=16k,d_h=128; % HBM/MFMA roofline"
+    if blk is not None:
+        metric = "ELSAA attention-block step (projections + operator) fwd+bwd tokens/sec"
     result = {
-        "metric": "ELSAA fwd+bwd tokens/sec at N=16k,d_h=128; % HBM/MFMA roofline",
+        "metric": metric,
         "value": tokens / elapsed,
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -238,12 +320,12 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "N": w.N, "d_h": w.d, "k": w.k, "r": w.r,
-                   "causal": w.causal, "levels": Lv},
+                   "causal": w.causal, "levels": Lv, **({"d_model": w.d_model} if blk else {})},
         "roofline": roof,
         "kernel_ms_per_step": {n: round(t, 4) for n, t in sorted(per_step.items(), key=lambda x: -x[1])},
     }
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(w, inp)
+        result["cpu_baseline"] = cpu_baseline_block(w, inp, blk) if blk else cpu_baseline(w, inp)
     print(json.dumps(result), flush=True)
 
 
