@@ -25,13 +25,8 @@ constexpr float kLn2 = 0.6931471805599453f;
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
-// Round to nearest even; inputs here are finite.
-__device__ __forceinline__ uint16_t f32_to_bf16(float f)
-{
-    uint32_t u = __float_as_uint(f);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
-}
+// Round to nearest even (v_cvt_pk_bf16_f32 on gfx950).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 
 // Storage traits: element type in HBM / LDS and the 8-slot operand fragment.
 struct BF16 {
@@ -56,7 +51,7 @@ struct BF16 {
     {
         frag_t f;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) f[j] = __builtin_bit_cast(__bf16, f32_to_bf16(v[j]));
+        for (int j = 0; j < 8; ++j) f[j] = (__bf16)v[j];
         return f;
     }
     // v = hi + lo to about 2^-16 relative (both bf16): float32-accurate operand

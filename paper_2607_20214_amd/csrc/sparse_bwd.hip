@@ -19,6 +19,7 @@
 // store the final dQ, dK, dV in the storage dtype.
 #include "common.hpp"
 #include "internal.hpp"
+#include "tile.hpp"
 
 namespace elsaa {
 
@@ -462,10 +463,271 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
     }
 }
 
+// ------------------------------------------------------------------------
+// Whole sorted blocks at once (b = BQ in {64, 128}): one workgroup per block
+// of BQ sorted queries and the BQ sorted keys they see (Alg. 4 blocks; the
+// per-level SortLSH calls of Alg. 5).  BQ / 16 waves each own 16 keys (their
+// K, V rows in registers, dK^T and dV^T accumulators); the block's queries
+// stream through LDS in tiles of 64 with the next tile's rows loaded into
+// registers meanwhile.  Per tile: S = Q K^T and dP = dO V^T (query rows from
+// LDS), P and dS in registers, dV^T += dO^T P and dK^T += Q^T dS with the
+// transposed operands read from the query tiles, then dS^T goes to LDS and
+// the tile's complete dQ^T = K^T dS^T is formed from the block's K tile.
+// Every input row is read once per block and dQ, dK, dV are each written
+// once: partials by natural token index (levels) or the final sums with the
+// low-rank parts in the storage dtype (non-causal blocks).
+// ------------------------------------------------------------------------
+template <class T, int D, int BQ, int MODE>
+__global__ __launch_bounds__(BQ * 4, BQ == 64 ? 3 : 1) void sparse_bwd_block_kernel(BArgs a)
+{
+    using S = typename T::store_t;
+    using F = typename T::frag_t;
+    constexpr int NW = BQ / 16, NT = 64 * NW;
+    constexpr int KS = D / 32, DT = D / 16, NQT = BQ / 64;
+    using TD = tile::Tile<T, D, NT>;        // Q, dO, K tiles (rows of D)
+    using TS = tile::Tile<T, 64, NT>;       // dS^T tile (BQ rows of 64 queries)
+    constexpr int PT = TD::PER_THREAD;
+    static_assert(BQ * 64 <= 2 * 64 * D, "dS^T fits in the query tiles");
+    __shared__ __attribute__((aligned(16))) S sk[BQ * D];
+    __shared__ __attribute__((aligned(16))) S sqo[2 * 64 * D];   // Q tile, dO tile; later dS^T
+    __shared__ float s_l2[64], s_de[64], s_sc[64];
+    __shared__ int s_qt[64];
+    S* const sq = sqo;
+    S* const so = sqo + 64 * D;
+    S* const sds = sqo;
+
+    const int h = blockIdx.y, b = blockIdx.z;
+    const size_t bh = (size_t)b * a.H + h;
+    const int N = a.N;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int g = lane >> 4, col = lane & 15;
+    const S* Q = (const S*)a.Q + bh * N * D;
+    const S* K = (const S*)a.K + bh * N * D;
+    const S* V = (const S*)a.V + bh * N * D;
+    const S* dO = (const S*)a.dO + bh * N * D;
+
+    // ---- the block: sorted positions [p0, p0 + nv) of its query and key lists
+    int level = 0, nv;
+    const int32_t* ql;
+    const int32_t* kl;
+    if (MODE == kLevels) {
+        const int per_level = (N / 2) / BQ;
+        level = blockIdx.x / per_level;
+        const int t = blockIdx.x - level * per_level;
+        const size_t base = (bh * a.Lv + level) * (size_t)(N / 2) + (size_t)t * BQ;
+        ql = a.perm_q + base;
+        kl = a.perm_k + base;
+        nv = BQ;
+    } else {
+        const int p0 = blockIdx.x * BQ;
+        ql = a.perm_q + bh * N + p0;
+        kl = a.perm_k + bh * N + p0;
+        nv = min(BQ, N - p0);
+    }
+
+    // ---- K tile of the block, Q / dO tile 0, this lane's V rows
+    uint4 rq[PT], ro[PT];
+    int qtk[PT];
+    float l2 = 0.f, de = 0.f, sc = 0.f;
+    int qtok_t = -1;
+    auto qtokens = [&](int qt) {
+#pragma unroll
+        for (int j = 0; j < PT; ++j) {
+            const int r = 64 * qt + TD::row_of(j);
+            qtk[j] = r < nv ? ql[r] : -1;
+        }
+        qtok_t = -1;
+        if (threadIdx.x < 64) {
+            const int r = 64 * qt + threadIdx.x;
+            qtok_t = r < nv ? ql[r] : -1;
+        }
+    };
+    auto qload = [&]() {
+        TD::load(Q, qtk, rq);
+        TD::load(dO, qtk, ro);
+        l2 = de = sc = 0.f;
+        if (qtok_t >= 0) {
+            const size_t row = bh * N + qtok_t;
+            l2 = a.rs[row];
+            de = a.rs[a.BHN + row];
+            sc = a.rs[2 * a.BHN + row];
+        }
+    };
+    {
+        int ktk[PT];
+        uint4 rk[PT];
+#pragma unroll
+        for (int kt = 0; kt < NQT; ++kt) {
+#pragma unroll
+            for (int j = 0; j < PT; ++j) {
+                const int r = 64 * kt + TD::row_of(j);
+                ktk[j] = r < nv ? kl[r] : -1;
+            }
+            TD::load(K, ktk, rk);
+            TD::store(sk, rk, 64 * kt);
+        }
+    }
+    const int kloc = 16 * w + col;                       // this lane's key within the block
+    const int ktok = kloc < nv ? kl[kloc] : -1;
+    F vf[KS];
+    {
+        float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) vf[ks] = T::pack(z);
+        if (ktok >= 0)
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) vf[ks] = T::ld8(V + (size_t)ktok * D + 32 * ks + 8 * g);
+    }
+    qtokens(0);
+    qload();
+    // (this lane's K row is read from the block's K tile when needed)
+
+    f32x4 akT[DT], avT[DT];                              // rows d = 16 dt + 4 g + i, column = this key
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) { akT[dt] = f32x4{0, 0, 0, 0}; avT[dt] = f32x4{0, 0, 0, 0}; }
+
+    for (int qt = 0; qt < NQT; ++qt) {
+        if (qt > 0) __syncthreads();                     // previous dS^T / dQ phase done
+        TD::store(sq, rq);
+        TD::store(so, ro);
+        if (threadIdx.x < 64) {
+            s_l2[threadIdx.x] = l2;
+            s_de[threadIdx.x] = de;
+            s_sc[threadIdx.x] = sc;
+            s_qt[threadIdx.x] = qtok_t;
+        }
+        __syncthreads();
+        if (qt + 1 < NQT) {                              // next tile in flight
+            qtokens(qt + 1);
+            qload();
+        }
+
+        // S and dP for the 64 queries x this wave's 16 keys (rows: queries);
+        // P sc and dS packed at once as the 32-query k-step operands
+        F pf[2], zf[2];
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+            float p8[8], z8[8];
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2) {
+                const int s = 2 * kk + h2;
+                f32x4 st = {0, 0, 0, 0}, dp = {0, 0, 0, 0};
+                const int qr = krow_of(s, col);
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+                    st = T::mma(TD::row8(sq, qr, 32 * ks + 8 * g), TD::row8(sk, kloc, 32 * ks + 8 * g), st);
+                    dp = T::mma(TD::row8(so, qr, 32 * ks + 8 * g), vf[ks], dp);
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int q = key_of(s, g, i);
+                    const bool ok = ktok >= 0 && s_qt[q] >= 0;
+                    const float P = ok ? fast_exp2(st[i] * a.tau2 - s_l2[q]) : 0.f;
+                    const float c = s_sc[q];
+                    p8[4 * h2 + i] = P * c;
+                    z8[4 * h2 + i] = P * (c * dp[i] - s_de[q]);
+                }
+            }
+            pf[kk] = T::pack(p8);
+            zf[kk] = T::pack(z8);
+        }
+        // dV^T += dO^T (P sc), dK^T += Q^T dS over two 32-query k-steps
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                avT[dt] = T::mma(TD::col8(so, 32 * kk, 16 * dt), pf[kk], avT[dt]);
+                akT[dt] = T::mma(TD::col8(sq, 32 * kk, 16 * dt), zf[kk], akT[dt]);
+            }
+        __syncthreads();                                 // query tiles no longer read
+        // dS^T [key][query] into the query-tile space: slots 8g + j of k-step kk
+        // hold queries 32 kk + 8 g + j, eight consecutive queries per write
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+            const int q0 = 32 * kk + 8 * g;
+            S* dst = &sds[TS::off(kloc, q0 / TS::EPC) + q0 % TS::EPC];
+            if constexpr (T::bytes == 2) {
+                *(F*)dst = zf[kk];
+            } else {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) dst[j] = zf[kk][j];
+            }
+        }
+        __syncthreads();
+        // dQ^T = K^T dS^T for this tile: DT x 4 output tiles spread over the
+        // waves, each wave's tiles sharing one 16-row slice dt of K^T when it
+        // has four or more
+        constexpr int TILES = DT * 4, PER_W = TILES / NW;
+        static_assert(TILES % NW == 0 && (PER_W % 4 == 0 || 4 % PER_W == 0), "dQ tiles per wave");
+        f32x4 dq[PER_W];
+#pragma unroll
+        for (int u = 0; u < PER_W; ++u) dq[u] = f32x4{0, 0, 0, 0};
+#pragma unroll
+        for (int kb = 0; kb < BQ; kb += 32) {
+            F kt_frag = TD::col8(sk, kb, 16 * ((w * PER_W) / 4));
+#pragma unroll
+            for (int u = 0; u < PER_W; ++u) {
+                const int tix = w * PER_W + u, dt = tix / 4, qtile = tix % 4;
+                if (u > 0 && qtile == 0) kt_frag = TD::col8(sk, kb, 16 * dt);
+                dq[u] = T::mma(kt_frag, TS::col8(sds, kb, 16 * qtile), dq[u]);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < PER_W; ++u) {
+            const int tix = w * PER_W + u, dt = tix / 4, qtile = tix % 4;
+            const int qtok = s_qt[16 * qtile + col];
+            if (qtok < 0) continue;
+            const int d0 = 16 * dt + 4 * g;
+            if (MODE == kLevels) {
+                float* out = a.part_dq + level_slot(bh, a.Lv, level, N, qtok, 1) * D + d0;
+                *(f32x4*)out = dq[u] * a.tau;
+            } else {
+                const size_t row = bh * N + qtok;
+                const f32x4 v = dq[u] * a.tau + *(const f32x4*)(a.dq_lr + row * D + d0);
+                S* out = (S*)a.dQ + row * D + d0;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) out[i] = T::store(v[i]);
+            }
+        }
+    }
+
+    // ---- dK, dV of this lane's key: rows d = 16 dt + 4 g + i
+    if (ktok < 0) return;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+        const int d0 = 16 * dt + 4 * g;
+        if (MODE == kLevels) {
+            const size_t slot = level_slot(bh, a.Lv, level, N, ktok, 0);
+            *(f32x4*)(a.part_dk + slot * D + d0) = akT[dt] * a.tau;
+            *(f32x4*)(a.part_dv + slot * D + d0) = avT[dt];
+        } else {
+            const size_t row = bh * N + ktok;
+            const f32x4 vk = akT[dt] * a.tau + *(const f32x4*)(a.dk_lr + row * D + d0);
+            const f32x4 vv = avT[dt] + *(const f32x4*)(a.dv_lr + row * D + d0);
+            S* ok = (S*)a.dK + row * D + d0;
+            S* ov = (S*)a.dV + row * D + d0;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                ok[i] = T::store(vk[i]);
+                ov[i] = T::store(vv[i]);
+            }
+        }
+    }
+}
+
 template <class T, int D>
 hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st)
 {
     hipError_t e;
+    // whole-block kernel: b in {64, 128}, blocks never straddle a segment
+    const int bq = s.k;
+    const bool whole = (bq == 64 || bq == 128) && (s.causal ? (s.n_leaf % bq == 0) : true);
+    if (whole && !s.causal) {
+        dim3 grid((s.N + bq - 1) / bq, s.H, s.B);
+        if (bq == 64) ELSAA_LAUNCH("sparse_bwd_blocks", (sparse_bwd_block_kernel<T, D, 64, kBlocks>), grid, dim3(256), 0, st, a);
+        else ELSAA_LAUNCH("sparse_bwd_blocks", (sparse_bwd_block_kernel<T, D, 128, kBlocks>), grid, dim3(512), 0, st, a);
+        return hipGetLastError();
+    }
     if (!s.causal) {
         dim3 grid((s.N + kT - 1) / kT, s.H, s.B);
         ELSAA_LAUNCH("sparse_dq_blocks", (sparse_dq_kernel<T, D, kBlocks>), grid, dim3(kThreads), 0, st, a);
@@ -473,7 +735,12 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st)
         ELSAA_LAUNCH("sparse_dkv_blocks", (sparse_dkv_kernel<T, D, kBlocks>), grid, dim3(kThreads), 0, st, a);
         return hipGetLastError();
     }
-    if (s.Lv > 0) {
+    if (s.Lv > 0 && whole) {
+        dim3 grid(s.Lv * (s.N / 2) / bq, s.H, s.B);
+        if (bq == 64) ELSAA_LAUNCH("sparse_bwd_levels", (sparse_bwd_block_kernel<T, D, 64, kLevels>), grid, dim3(256), 0, st, a);
+        else ELSAA_LAUNCH("sparse_bwd_levels", (sparse_bwd_block_kernel<T, D, 128, kLevels>), grid, dim3(512), 0, st, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    } else if (s.Lv > 0) {
         dim3 grid(s.Lv * (s.N / 2) / kT, s.H, s.B);
         ELSAA_LAUNCH("sparse_dq_levels", (sparse_dq_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;

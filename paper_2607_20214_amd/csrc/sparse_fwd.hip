@@ -1,11 +1,13 @@
 // sparse_fwd.hip -- sortLSH sparse branch forward and the fusion epilogue.
 //
 // One workgroup = 4 waves = 64 queries (16 per wave); keys stream through
-// LDS in tiles of 64 rows gathered by the sorted index lists (K row-major,
-// V transposed so both MFMA operands read 16 contiguous bytes).  Scores are
-// computed transposed (S^T = K Q^T) so each lane owns one query: the running
-// max and denominator of the online softmax are lane-local plus two
-// cross-row shuffles, and P^T feeds O^T = V^T P^T straight from registers.
+// LDS in tiles of 64 rows gathered by the sorted index lists (tile.hpp: K
+// and V row-major, chunk-swizzled; V^T operands come from transposed LDS
+// reads).  The rows of the next tile are loaded into registers while the
+// current one is consumed.  Scores are computed transposed (S^T = K Q^T) so
+// each lane owns one query: the running max and denominator of the online
+// softmax are lane-local plus two cross-row shuffles, and P^T feeds
+// O^T = V^T P^T straight from registers.
 //
 // Three modes share the tile loop:
 //   kBlocks  non-causal Alg. 4: the query tile of sorted positions
@@ -23,6 +25,7 @@
 //   O = g_s m O_s + g_lr O_lr.
 #include "common.hpp"
 #include "internal.hpp"
+#include "tile.hpp"
 
 namespace elsaa {
 
@@ -31,16 +34,8 @@ namespace {
 constexpr int kQT = 64;       // queries per workgroup
 constexpr int kKT = 64;       // keys per LDS tile
 constexpr int kThreads = 256;
-constexpr int kPad = 8;       // LDS row padding (elements)
 
 enum Mode { kBlocks = 0, kLevels = 1, kLeaf = 2 };
-
-template <class T, int D>
-struct Smem {
-    typename T::store_t k[kKT][D + kPad];
-    typename T::store_t vt[D][kKT + kPad];
-    int32_t kidx[kKT];
-};
 
 struct Args {
     const void* Q;
@@ -62,37 +57,6 @@ struct Args {
     float lambda, eps;
 };
 
-template <class T, int D>
-__device__ __forceinline__ void load_kv(Smem<T, D>& sm, const typename T::store_t* K,
-                                        const typename T::store_t* V)
-{
-    using S = typename T::store_t;
-    constexpr int PER = 16 / T::bytes;   // elements per 16-byte chunk
-    constexpr int CH = D / PER;          // chunks per row
-    for (int it = threadIdx.x; it < kKT * CH; it += kThreads) {
-        const int row = it & (kKT - 1), c = it / kKT;
-        const int tok = sm.kidx[row];
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (tok >= 0) v = ldg16(K + (size_t)tok * D + c * PER);
-        *(uint4*)&sm.k[row][c * PER] = v;
-    }
-    for (int it = threadIdx.x; it < (kKT / 2) * CH; it += kThreads) {
-        const int p = it & (kKT / 2 - 1), c = it / (kKT / 2);
-        const int t0 = sm.kidx[2 * p], t1 = sm.kidx[2 * p + 1];
-        uint4 a = make_uint4(0, 0, 0, 0), b = make_uint4(0, 0, 0, 0);
-        if (t0 >= 0) a = ldg16(V + (size_t)t0 * D + c * PER);
-        if (t1 >= 0) b = ldg16(V + (size_t)t1 * D + c * PER);
-        const S* ea = (const S*)&a;
-        const S* eb = (const S*)&b;
-#pragma unroll
-        for (int j = 0; j < PER; ++j) {
-            S* dst = &sm.vt[c * PER + j][2 * p];
-            dst[0] = ea[j];
-            dst[1] = eb[j];
-        }
-    }
-}
-
 template <class T, int D, int MODE>
 __global__ __launch_bounds__(kThreads) void sparse_fwd_kernel(Args a)
 {
@@ -100,7 +64,10 @@ __global__ __launch_bounds__(kThreads) void sparse_fwd_kernel(Args a)
     using F = typename T::frag_t;
     constexpr int KS = D / 32;   // k-steps over the head dim
     constexpr int DT = D / 16;   // 16-wide tiles of the head dim
-    __shared__ Smem<T, D> sm;
+    using Tl = tile::Tile<T, D>;
+    constexpr int PT = Tl::PER_THREAD;
+    __shared__ __attribute__((aligned(16))) S sk[kKT * D];
+    __shared__ __attribute__((aligned(16))) S sv[kKT * D];
 
     const int h = blockIdx.y, b = blockIdx.z;
     const size_t bh = (size_t)b * a.H + h;
@@ -169,17 +136,33 @@ __global__ __launch_bounds__(kThreads) void sparse_fwd_kernel(Args a)
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) acc[dt] = f32x4{0, 0, 0, 0};
 
-    for (int k0 = kbeg; k0 < kend; k0 += kKT) {
-        __syncthreads();
-        if (threadIdx.x < kKT) {
-            const int p = k0 + threadIdx.x;
-            int tok = -1;
-            if (p < kend) tok = (MODE == kLeaf) ? p : klist[p];
-            sm.kidx[threadIdx.x] = tok;
+    // rows of the key tile at k0 that this thread stages (-1 = none)
+    auto tokens = [&](int k0, int (&tok)[PT]) {
+#pragma unroll
+        for (int j = 0; j < PT; ++j) {
+            const int p = k0 + Tl::row_of(j);
+            tok[j] = p < kend ? ((MODE == kLeaf) ? p : klist[p]) : -1;
         }
+    };
+    const int ntiles = (kend - kbeg + kKT - 1) / kKT;
+    int tok[PT];
+    uint4 rk[PT], rv[PT];
+    tokens(kbeg, tok);
+    Tl::load(K, tok, rk);
+    Tl::load(V, tok, rv);
+    if (ntiles > 1) tokens(kbeg + kKT, tok);
+
+    for (int t = 0; t < ntiles; ++t) {
+        const int k0 = kbeg + t * kKT;
+        if (t > 0) __syncthreads();          // previous tile consumed
+        Tl::store(sk, rk);
+        Tl::store(sv, rv);
         __syncthreads();
-        load_kv<T, D>(sm, K, V);
-        __syncthreads();
+        if (t + 1 < ntiles) {                // next tile's rows in flight during this one
+            Tl::load(K, tok, rk);
+            Tl::load(V, tok, rv);
+            if (t + 2 < ntiles) tokens(k0 + 2 * kKT, tok);
+        }
 
         // S^T for the 64 keys of the tile (4 sub-tiles of 16 keys)
         f32x4 st[4];
@@ -189,7 +172,7 @@ __global__ __launch_bounds__(kThreads) void sparse_fwd_kernel(Args a)
             const int kr = krow_of(s, qq);
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks)
-                st[s] = T::mma(T::ld8(&sm.k[kr][32 * ks + 8 * g]), qf[ks], st[s]);
+                st[s] = T::mma(Tl::row8(sk, kr, 32 * ks + 8 * g), qf[ks], st[s]);
         }
         // scale to log2 units and mask
         float tmax = -INFINITY;
@@ -235,7 +218,7 @@ __global__ __launch_bounds__(kThreads) void sparse_fwd_kernel(Args a)
             const F pf = T::pack(pv);
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt)
-                acc[dt] = T::mma(T::ld8(&sm.vt[16 * dt + qq][32 * kk + 8 * g]), pf, acc[dt]);
+                acc[dt] = T::mma(Tl::col8(sv, 32 * kk, 16 * dt), pf, acc[dt]);
         }
     }
 
