@@ -42,7 +42,7 @@ struct BArgs {
     const float* dq_lr;       // float32 [BHN][D] low-rank parts
     const float* dk_lr;
     const float* dv_lr;
-    float* part_dq;           // float32 [BH][Lv][N/2][D] per-level partials
+    float* part_dq;           // [BH][Lv][N/2][D] per-level partials, float32
     float* part_dk;
     float* part_dv;
     void* dQ;
@@ -487,13 +487,13 @@ __global__ __launch_bounds__(BQ * 4, BQ == 64 ? 3 : 1) void sparse_bwd_block_ker
     using TD = tile::Tile<T, D, NT>;        // Q, dO, K tiles (rows of D)
     using TS = tile::Tile<T, 64, NT>;       // dS^T tile (BQ rows of 64 queries)
     constexpr int PT = TD::PER_THREAD;
-    static_assert(BQ * 64 <= 2 * 64 * D, "dS^T fits in the query tiles");
-    __shared__ __attribute__((aligned(16))) S sk[BQ * D];
-    __shared__ __attribute__((aligned(16))) S sqo[2 * 64 * D];   // Q tile, dO tile; later dS^T
+    static_assert(TS::elems(BQ) <= 2 * TD::elems(64), "dS^T fits in the query tiles");
+    __shared__ __attribute__((aligned(16))) S sk[TD::elems(BQ)];
+    __shared__ __attribute__((aligned(16))) S sqo[2 * TD::elems(64)];   // Q tile, dO tile; later dS^T
     __shared__ float s_l2[64], s_de[64], s_sc[64];
     __shared__ int s_qt[64];
     S* const sq = sqo;
-    S* const so = sqo + 64 * D;
+    S* const so = sqo + TD::elems(64);
     S* const sds = sqo;
 
     const int h = blockIdx.y, b = blockIdx.z;
@@ -645,7 +645,7 @@ __global__ __launch_bounds__(BQ * 4, BQ == 64 ? 3 : 1) void sparse_bwd_block_ker
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
             const int q0 = 32 * kk + 8 * g;
-            S* dst = &sds[TS::off(kloc, q0 / TS::EPC) + q0 % TS::EPC];
+            S* dst = &sds[TS::row(kloc) + q0];
             if constexpr (T::bytes == 2) {
                 *(F*)dst = zf[kk];
             } else {

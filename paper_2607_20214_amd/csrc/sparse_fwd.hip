@@ -46,8 +46,8 @@ struct Args {
     const float* gates;
     const float* O_lr;
     const float* d_lr;
-    float* part_o;
-    float* part_lse;
+    float* part_o;            // [BH][Lv][N/2][D] normalised level outputs (float32: O_s feeds
+    float* part_lse;          // Delta of the backward, where bf16 rounding costs accuracy)
     void* O;
     float* lse;
     float* m;
@@ -58,7 +58,7 @@ struct Args {
 };
 
 template <class T, int D, int MODE>
-__global__ __launch_bounds__(kThreads) void sparse_fwd_kernel(Args a)
+__global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
 {
     using S = typename T::store_t;
     using F = typename T::frag_t;
@@ -66,8 +66,8 @@ __global__ __launch_bounds__(kThreads) void sparse_fwd_kernel(Args a)
     constexpr int DT = D / 16;   // 16-wide tiles of the head dim
     using Tl = tile::Tile<T, D>;
     constexpr int PT = Tl::PER_THREAD;
-    __shared__ __attribute__((aligned(16))) S sk[kKT * D];
-    __shared__ __attribute__((aligned(16))) S sv[kKT * D];
+    __shared__ __attribute__((aligned(16))) S sk[Tl::elems(kKT)];
+    __shared__ __attribute__((aligned(16))) S sv[Tl::elems(kKT)];
 
     const int h = blockIdx.y, b = blockIdx.z;
     const size_t bh = (size_t)b * a.H + h;
@@ -231,8 +231,7 @@ __global__ __launch_bounds__(kThreads) void sparse_fwd_kernel(Args a)
         const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
         float* po = a.part_o + slot * D;
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-            *(f32x4*)(po + 16 * dt + 4 * g) = acc[dt] * inv;
+        for (int dt = 0; dt < DT; ++dt) *(f32x4*)(po + 16 * dt + 4 * g) = acc[dt] * inv;
         if (g == 0) a.part_lse[slot] = (m_run + __log2f(l_run)) * kLn2;
         return;
     }

@@ -1,16 +1,18 @@
 // tile.hpp -- LDS tiles of gathered rows for the sparse-branch kernels.
 //
-// A tile holds up to 64 rows of D elements, row-major with no padding.  The
-// 16-byte chunks of each row are permuted by an XOR swizzle of the row index
-// so that the three access patterns of the kernels hit distinct LDS banks:
+// A tile holds rows of D elements, row-major with a pad of 8 elements per
+// row.  Row r of the tile is placed in LDS row slot slot_of(r), a fixed
+// permutation of the row index's low five bits, chosen so that the three
+// access patterns of the kernels hit distinct LDS banks:
 //   * 16-byte operand reads of 16 rows (consecutive rows, or the interleaved
 //     row order of key_of / krow_of), one chunk per lane;
 //   * transposed operand reads (ds_read_b64_tr_b16): 4 consecutive rows by
 //     32 contiguous bytes per 16-lane group;
 //   * 16-byte stores of whole rows by consecutive lanes.
-// Rows are staged global -> registers -> LDS by all threads of the
-// workgroup; the global loads of the next tile are issued before the
-// current tile is consumed.
+// Within a row, elements stay in order, so every operand address is one row
+// base per lane plus compile-time offsets.  Rows are staged
+// global -> registers -> LDS by all threads of the workgroup; the global
+// loads of the next tile are issued before the current tile is consumed.
 #pragma once
 #include "common.hpp"
 
@@ -18,14 +20,13 @@ namespace elsaa {
 namespace tile {
 
 constexpr int kRows = 64;
+constexpr int kPad = 8;
 
-// Chunk permutation of row r for rows of CPR chunks (CPR >= 8).
-template <int CPR>
-__device__ __forceinline__ int swz(int r)
+// LDS row slot of tile row r: low five bits (b0..b4) -> (b2^b4, b0, b1, b3, b4).
+__device__ __forceinline__ int slot_of(int r)
 {
-    const int b24 = ((r >> 2) ^ (r >> 4)) & 1;
-    if (CPR >= 16) return b24 | ((r & 1) << 1) | ((r & 2) << 1) | (r & 8);
-    return b24 | ((r & 2)) | ((r >> 1) & 4);
+    const int lo = (((r >> 2) ^ (r >> 4)) & 1) | ((r & 3) << 1) | (r & 24);
+    return (r & ~31) | lo;
 }
 
 // Tiles of 64 rows of D elements staged by NT threads.
@@ -35,11 +36,16 @@ struct Tile {
     using F = typename T::frag_t;
     static constexpr int EPC = 16 / T::bytes;         // elements per 16-byte chunk
     static constexpr int CPR = D / EPC;               // chunks per row
+    static constexpr int LD = D + kPad;               // LDS row stride (elements)
     static constexpr int PER_THREAD = kRows * CPR / NT;   // chunks staged per thread
     static_assert(CPR >= 8 && PER_THREAD >= 1, "tile shape");
 
+    // elements of an LDS tile of `rows` rows
+    static constexpr int elems(int rows) { return rows * LD; }
+    // element offset of row r
+    __device__ static __forceinline__ int row(int r) { return slot_of(r) * LD; }
     // element offset of chunk c of row r
-    __device__ static __forceinline__ int off(int r, int c) { return r * D + ((c ^ swz<CPR>(r)) * EPC); }
+    __device__ static __forceinline__ int off(int r, int c) { return row(r) + c * EPC; }
 
     // row of the j-th chunk this thread stages (and the chunk index)
     __device__ static __forceinline__ int row_of(int j) { return (threadIdx.x + NT * j) / CPR; }
@@ -62,8 +68,9 @@ struct Tile {
     // 8-slot operand fragment: elements [e0, e0 + 8) of row r (e0 % 8 == 0)
     __device__ static __forceinline__ F row8(const S* t, int r, int e0)
     {
-        if (T::bytes == 2) return T::ld8(&t[off(r, e0 / EPC)]);
-        return T::ld44(&t[off(r, e0 / EPC)], &t[off(r, e0 / EPC + 1)]);
+        const S* p = &t[row(r) + e0];
+        if (T::bytes == 2) return T::ld8(p);
+        return T::ld44(p, p + 4);
     }
 
     // 8-slot operand fragment of the transposed tile: lane (i = lane % 16,
@@ -76,15 +83,14 @@ struct Tile {
         if constexpr (T::bytes == 2) {
             // 16-bit: two transposed reads of 4 rows each
             const int e = c0 + 4 * (i & 3);
-            const S* p0 = &t[off(r + (i >> 2), e / EPC) + (e % EPC)];
-            const S* p1 = &t[off(r + 4 + (i >> 2), e / EPC) + (e % EPC)];
+            const S* p0 = &t[row(r + (i >> 2)) + e];
+            const S* p1 = &t[row(r + 4 + (i >> 2)) + e];
             const bf16x4 lo = lds_read_tr4((const uint16_t*)p0), hi = lds_read_tr4((const uint16_t*)p1);
             return F{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
         } else {
-            const int e = c0 + i;
             F f;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) f[j] = t[off(r + j, e / EPC) + (e % EPC)];
+            for (int j = 0; j < 8; ++j) f[j] = t[row(r + j) + c0 + i];
             return f;
         }
     }
