@@ -111,7 +111,7 @@ int validate(const elsaa_config* c, Shape* s)
     // RACE segments: enough workgroups to fill the chip, whole 64-token chunks
     const int64_t chunks = (c->N + 63) / 64;
     const int64_t bh = (int64_t)c->B * c->H;
-    int64_t nseg = (512 + bh - 1) / bh;
+    int64_t nseg = (512 + bh - 1) / bh;     // about two segment workgroups per compute unit
     if (nseg > chunks) nseg = chunks;
     if (nseg < 1) nseg = 1;
     const int64_t per = (chunks + nseg - 1) / nseg;

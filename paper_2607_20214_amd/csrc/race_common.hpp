@@ -17,6 +17,21 @@ constexpr int kThreads = 256;
 constexpr int kPad = 8;
 constexpr size_t kMaxLds = 160 * 1024;
 
+// sigmoid(x) and sigmoid(-x) from the hardware exp and reciprocal (about one
+// ulp each; exp overflow gives 0 for the vanishing side)
+__device__ __forceinline__ void sigmoid_pair(float x, float& sp, float& sn)
+{
+    sp = __builtin_amdgcn_rcpf(1.f + __expf(-x));
+    sn = __builtin_amdgcn_rcpf(1.f + __expf(x));
+}
+
+// tanh(u) = 1 - 2 / (1 + e^{2u}), absolute error about 1e-7 (the features use
+// t only through sigmoid(2 beta t) and the chain rule through 1 - t^2)
+__device__ __forceinline__ float tanh_abs(float u)
+{
+    return 1.f - 2.f * __builtin_amdgcn_rcpf(1.f + __expf(2.f * u));
+}
+
 // projection count padded to whole 32-wide k-steps (backward du x W)
 template <int RP> constexpr int w_kdim() { return RP / 4 < 32 ? 32 : RP / 4; }
 
@@ -98,9 +113,8 @@ __device__ void features(const float* U, int t0, int N, int L, float two_beta,
         float t[4], sp[4], sn[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            t[i] = tanhf(u[i]);
-            sp[i] = 1.f / (1.f + __expf(-two_beta * t[i]));
-            sn[i] = 1.f / (1.f + __expf(two_beta * t[i]));
+            t[i] = tanh_abs(u[i]);
+            sigmoid_pair(two_beta * t[i], sp[i], sn[i]);
         }
         if (ts) {
 #pragma unroll
@@ -145,8 +159,7 @@ __device__ __forceinline__ void chain_rule_t(f32x4 dphi, int qt, int tb, int L, 
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
         t[b] = ts[row][4 * tb + b];
-        sp[b] = 1.f / (1.f + __expf(-two_beta * t[b]));
-        sn[b] = 1.f / (1.f + __expf(two_beta * t[b]));
+        sigmoid_pair(two_beta * t[b], sp[b], sn[b]);
     }
     // features c = 4g + i: bits 0, 1 from i, bits 2, 3 from g
     const float hi = ((g & 1) ? sp[2] : sn[2]) * ((g & 2) ? sp[3] : sn[3]);

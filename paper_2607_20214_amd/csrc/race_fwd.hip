@@ -123,25 +123,30 @@ __global__ __launch_bounds__(kThreads) void race_state_kernel(StateArgs a)
 }
 
 // mode 0: total in every segment; 1: exclusive prefix; 2: exclusive suffix.
+// Each thread owns one element of the state and walks the segments in
+// batches of kBatch independent loads.
 __global__ __launch_bounds__(256) void race_scan_kernel(float* states, int nseg, int per, int mode)
 {
+    constexpr int kBatch = 16;
     const size_t bh = blockIdx.y;
     const int e = blockIdx.x * 256 + threadIdx.x;
     if (e >= per) return;
     float* base = states + bh * (size_t)nseg * per + e;
     float run = 0.f;
-    if (mode == 2) {
-        for (int s = nseg - 1; s >= 0; --s) {
-            const float v = base[(size_t)s * per];
-            base[(size_t)s * per] = run;
-            run += v;
+    for (int s0 = 0; s0 < nseg; s0 += kBatch) {
+        float v[kBatch];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const int s = mode == 2 ? nseg - 1 - (s0 + j) : s0 + j;
+            v[j] = (s0 + j < nseg) ? base[(size_t)s * per] : 0.f;
         }
-        return;
-    }
-    for (int s = 0; s < nseg; ++s) {
-        const float v = base[(size_t)s * per];
-        if (mode == 1) base[(size_t)s * per] = run;
-        run += v;
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            if (s0 + j >= nseg) break;
+            const int s = mode == 2 ? nseg - 1 - (s0 + j) : s0 + j;
+            if (mode != 0) base[(size_t)s * per] = run;
+            run += v[j];
+        }
     }
     if (mode == 0)
         for (int s = 0; s < nseg; ++s) base[(size_t)s * per] = run;
