@@ -27,7 +27,6 @@ namespace {
 
 constexpr int kT = 64;
 constexpr int kThreads = 256;
-constexpr int kPad = 8;
 
 enum Mode { kBlocks = 0, kLevels = 1, kLeaf = 2 };
 
@@ -53,57 +52,6 @@ struct BArgs {
     float tau, tau2;
 };
 
-// Rows [0, 64) of X listed in idx (-1 = zero row) into a row-major tile and,
-// when xt != nullptr, its transpose.  Each thread loads 16-byte pieces of a
-// pair of rows once and writes them to both layouts.
-template <class T, int D>
-__device__ __forceinline__ void stage_rows(const typename T::store_t* X, const int32_t* idx,
-                                           typename T::store_t (*x)[D + kPad],
-                                           typename T::store_t (*xt)[kT + kPad])
-{
-    using S = typename T::store_t;
-    constexpr int PER = 16 / T::bytes;
-    constexpr int CH = D / PER;
-    for (int it = threadIdx.x; it < (kT / 2) * CH; it += kThreads) {
-        const int p = it & (kT / 2 - 1), c = it / (kT / 2);
-        const int t0 = idx[2 * p], t1 = idx[2 * p + 1];
-        uint4 a = make_uint4(0, 0, 0, 0), b = make_uint4(0, 0, 0, 0);
-        if (t0 >= 0) a = ldg16(X + (size_t)t0 * D + c * PER);
-        if (t1 >= 0) b = ldg16(X + (size_t)t1 * D + c * PER);
-        *(uint4*)&x[2 * p][c * PER] = a;
-        *(uint4*)&x[2 * p + 1][c * PER] = b;
-        if (xt) {
-            const S* ea = (const S*)&a;
-            const S* eb = (const S*)&b;
-#pragma unroll
-            for (int j = 0; j < PER; ++j) {
-                S* dst = &xt[c * PER + j][2 * p];
-                dst[0] = ea[j];
-                dst[1] = eb[j];
-            }
-        }
-    }
-}
-
-template <class T, int D>
-struct DqSmem {
-    typename T::store_t k[kT][D + kPad];
-    typename T::store_t v[kT][D + kPad];
-    typename T::store_t kt[D][kT + kPad];
-    int32_t idx[kT];
-};
-
-template <class T, int D>
-struct DkvSmem {
-    typename T::store_t q[kT][D + kPad];
-    typename T::store_t o[kT][D + kPad];
-    typename T::store_t qt[D][kT + kPad];
-    typename T::store_t ot[D][kT + kPad];
-    int32_t idx[kT];
-    int32_t ktok[kT];
-    float lse2[kT], delta[kT], scs[kT];
-};
-
 // Compact slot of token t in the level-l list of future (or past) halves.
 __device__ __forceinline__ size_t level_slot(size_t bh, int Lv, int l, int N, int t, int future)
 {
@@ -113,7 +61,11 @@ __device__ __forceinline__ size_t level_slot(size_t bh, int Lv, int l, int N, in
 }
 
 // ------------------------------------------------------------------------
-// dQ: query-centric
+// dQ: query-centric.  One workgroup per 64 queries (16 per wave, one per
+// lane column); key tiles of 64 rows stream through LDS (tile.hpp) with the
+// next tile's rows loaded into registers meanwhile.  Per tile: S^T = K Q^T
+// and dP^T = V dO^T (key rows from LDS, this lane's query in registers),
+// dS^T in registers, dQ^T += K^T dS^T with K^T from the transposed LDS read.
 // ------------------------------------------------------------------------
 template <class T, int D, int MODE>
 __global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
@@ -121,7 +73,10 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
     using S = typename T::store_t;
     using F = typename T::frag_t;
     constexpr int KS = D / 32, DT = D / 16;
-    __shared__ DqSmem<T, D> sm;
+    using TD = tile::Tile<T, D, kThreads>;
+    constexpr int PT = TD::PER_THREAD;
+    __shared__ __attribute__((aligned(16))) S sk[TD::elems(kT)];
+    __shared__ __attribute__((aligned(16))) S sv[TD::elems(kT)];
     const int h = blockIdx.y, b = blockIdx.z;
     const size_t bh = (size_t)b * a.H + h;
     const int N = a.N;
@@ -168,6 +123,22 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
     const int blk_lo = (MODE == kLeaf) ? 0 : (qpos / bq) * bq;
     const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), blk_lo + bq);
 
+    // key rows of the tile at k0 that this thread stages (-1 = none)
+    auto tokens = [&](int k0, int (&tok)[PT]) {
+#pragma unroll
+        for (int j = 0; j < PT; ++j) {
+            const int p = k0 + TD::row_of(j);
+            tok[j] = p < kend ? ((MODE == kLeaf) ? p : klist[p]) : -1;
+        }
+    };
+    const int ntiles = (kend - kbeg + kT - 1) / kT;
+    int tok[PT];
+    uint4 rk[PT], rv[PT];
+    tokens(kbeg, tok);
+    TD::load(K, tok, rk);
+    TD::load(V, tok, rv);
+    if (ntiles > 1) tokens(kbeg + kT, tok);
+
     float lse2 = 0.f, delta = 0.f, scs = 0.f;
     F qf[KS], df[KS];
     {
@@ -187,54 +158,47 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
             df[ks] = T::ld8(dO + (size_t)qtok * D + 32 * ks + 8 * g);
         }
     }
-    f32x4 acc[DT];
+    f32x4 acc[DT];   // dQ^T: rows d = 16 dt + 4 g + i, column = this lane's query
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) acc[dt] = f32x4{0, 0, 0, 0};
 
-    for (int k0 = kbeg; k0 < kend; k0 += kT) {
+    for (int t = 0; t < ntiles; ++t) {
+        const int k0 = kbeg + t * kT;
+        if (t > 0) __syncthreads();
+        TD::store(sk, rk);
+        TD::store(sv, rv);
         __syncthreads();
-        if (threadIdx.x < kT) {
-            const int p = k0 + threadIdx.x;
-            int tok = -1;
-            if (p < kend) tok = (MODE == kLeaf) ? p : klist[p];
-            sm.idx[threadIdx.x] = tok;
-        }
-        __syncthreads();
-        stage_rows<T, D>(K, sm.idx, sm.k, sm.kt);
-        stage_rows<T, D>(V, sm.idx, sm.v, nullptr);
-        __syncthreads();
-        f32x4 dz[4];
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            f32x4 st = {0, 0, 0, 0}, dp = {0, 0, 0, 0};
-            const int kr = krow_of(s, qq);
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                st = T::mma(T::ld8(&sm.k[kr][32 * ks + 8 * g]), qf[ks], st);
-                dp = T::mma(T::ld8(&sm.v[kr][32 * ks + 8 * g]), df[ks], dp);
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int p = k0 + key_of(s, g, i);
-                bool ok = p < kend && qtok >= 0;
-                if (MODE == kLeaf) ok = ok && p <= qtok;
-                else ok = ok && p >= blk_lo && p < blk_hi;
-                const float P = ok ? fast_exp2(st[i] * a.tau2 - lse2) : 0.f;
-                dz[s][i] = P * (scs * dp[i] - delta);
-            }
+        if (t + 1 < ntiles) {
+            TD::load(K, tok, rk);
+            TD::load(V, tok, rv);
+            if (t + 2 < ntiles) tokens(k0 + 2 * kT, tok);
         }
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
             float v8[8];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                v8[j] = dz[2 * kk][j];
-                v8[4 + j] = dz[2 * kk + 1][j];
+            for (int h2 = 0; h2 < 2; ++h2) {
+                const int s = 2 * kk + h2;
+                f32x4 st = {0, 0, 0, 0}, dp = {0, 0, 0, 0};
+                const int kr = krow_of(s, qq);
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+                    st = T::mma(TD::row8(sk, kr, 32 * ks + 8 * g), qf[ks], st);
+                    dp = T::mma(TD::row8(sv, kr, 32 * ks + 8 * g), df[ks], dp);
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int p = k0 + key_of(s, g, i);
+                    bool ok = p < kend && qtok >= 0;
+                    if (MODE == kLeaf) ok = ok && p <= qtok;
+                    else ok = ok && p >= blk_lo && p < blk_hi;
+                    const float P = ok ? fast_exp2(st[i] * a.tau2 - lse2) : 0.f;
+                    v8[4 * h2 + i] = P * (scs * dp[i] - delta);
+                }
             }
             const F bf = T::pack(v8);
 #pragma unroll
-            for (int dt = 0; dt < DT; ++dt)
-                acc[dt] = T::mma(T::ld8(&sm.kt[16 * dt + qq][32 * kk + 8 * g]), bf, acc[dt]);
+            for (int dt = 0; dt < DT; ++dt) acc[dt] = T::mma(TD::col8(sk, 32 * kk, 16 * dt), bf, acc[dt]);
         }
     }
     if (qtok < 0) return;
@@ -267,7 +231,11 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
 }
 
 // ------------------------------------------------------------------------
-// dK, dV: key-centric
+// dK, dV: key-centric.  One workgroup per 64 keys (16 per wave, one per lane
+// column, K and V rows in registers); query tiles of 64 rows stream through
+// LDS with the next tile's rows and row scalars loaded meanwhile.  Per tile:
+// S = Q K^T and dP = dO V^T (query rows from LDS), then dV^T += dO^T P and
+// dK^T += Q^T dS with the transposed operands read from the query tiles.
 // ------------------------------------------------------------------------
 template <class T, int D, int MODE>
 __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
@@ -275,7 +243,12 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
     using S = typename T::store_t;
     using F = typename T::frag_t;
     constexpr int KS = D / 32, DT = D / 16;
-    __shared__ DkvSmem<T, D> sm;
+    using TD = tile::Tile<T, D, kThreads>;
+    constexpr int PT = TD::PER_THREAD;
+    __shared__ __attribute__((aligned(16))) S sq[TD::elems(kT)];
+    __shared__ __attribute__((aligned(16))) S so[TD::elems(kT)];
+    __shared__ float s_l2[kT], s_de[kT], s_sc[kT];
+    __shared__ int s_ok[kT];
     const int h = blockIdx.y, b = blockIdx.z;
     const size_t bh = (size_t)b * a.H + h;
     const int N = a.N;
@@ -326,14 +299,39 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
     }
     const int blk_lo = (MODE == kLeaf) ? 0 : (kpos / bq) * bq;
     const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), blk_lo + bq);
-    if (threadIdx.x < kT) {
-        int t = -1;
-        const int p = j0 + threadIdx.x;
-        if (MODE == kLeaf) t = p;
-        else if (MODE == kLevels) t = klist[p];
-        else t = p < N ? klist[p] : -1;
-        sm.ktok[threadIdx.x] = t;
-    }
+
+    // query rows of the tile at q0 that this thread stages, and the scalars
+    // of query q0 + threadIdx.x (threads < 64)
+    auto tokens = [&](int q0, int (&tok)[PT], int& qt) {
+#pragma unroll
+        for (int j = 0; j < PT; ++j) {
+            const int p = q0 + TD::row_of(j);
+            tok[j] = p < qend ? ((MODE == kLeaf) ? p : qlist[p]) : -1;
+        }
+        qt = -1;
+        if (threadIdx.x < kT) {
+            const int p = q0 + threadIdx.x;
+            qt = p < qend ? ((MODE == kLeaf) ? p : qlist[p]) : -1;
+        }
+    };
+    float l2 = 0.f, de = 0.f, sc = 0.f;
+    auto scalars = [&](int qt) {
+        l2 = de = sc = 0.f;
+        if (qt >= 0) {
+            const size_t row = bh * N + qt;
+            l2 = a.rs[row];
+            de = a.rs[a.BHN + row];
+            sc = a.rs[2 * a.BHN + row];
+        }
+    };
+    const int ntiles = (qend - qbeg + kT - 1) / kT;
+    int tok[PT], qt_cur, qt_next = -1;
+    uint4 rq[PT], ro[PT];
+    tokens(qbeg, tok, qt_cur);
+    TD::load(Q, tok, rq);
+    TD::load(dO, tok, ro);
+    scalars(qt_cur);
+    if (ntiles > 1) tokens(qbeg + kT, tok, qt_next);
 
     F kf[KS], vf[KS];
     {
@@ -349,118 +347,106 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
             vf[ks] = T::ld8(V + (size_t)ktok * D + 32 * ks + 8 * g);
         }
     }
-    f32x4 ak[DT], av[DT];
+    f32x4 akT[DT], avT[DT];   // rows d = 16 dt + 4 g + i, column = this lane's key
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) { ak[dt] = f32x4{0, 0, 0, 0}; av[dt] = f32x4{0, 0, 0, 0}; }
+    for (int dt = 0; dt < DT; ++dt) { akT[dt] = f32x4{0, 0, 0, 0}; avT[dt] = f32x4{0, 0, 0, 0}; }
 
-    for (int q0 = qbeg; q0 < qend; q0 += kT) {
-        __syncthreads();
+    for (int t = 0; t < ntiles; ++t) {
+        const int q0 = qbeg + t * kT;
+        if (t > 0) __syncthreads();
+        TD::store(sq, rq);
+        TD::store(so, ro);
         if (threadIdx.x < kT) {
-            const int p = q0 + threadIdx.x;
-            int tok = -1;
-            if (p < qend) tok = (MODE == kLeaf) ? p : qlist[p];
-            sm.idx[threadIdx.x] = tok;
-            float l2 = 0.f, de = 0.f, sc = 0.f;
-            if (tok >= 0) {
-                const size_t row = bh * N + tok;
-                l2 = a.rs[row];
-                de = a.rs[a.BHN + row];
-                sc = a.rs[2 * a.BHN + row];
-            }
-            sm.lse2[threadIdx.x] = l2;
-            sm.delta[threadIdx.x] = de;
-            sm.scs[threadIdx.x] = sc;
+            s_l2[threadIdx.x] = l2;
+            s_de[threadIdx.x] = de;
+            s_sc[threadIdx.x] = sc;
+            s_ok[threadIdx.x] = qt_cur >= 0;
         }
         __syncthreads();
-        stage_rows<T, D>(Q, sm.idx, sm.q, sm.qt);
-        stage_rows<T, D>(dO, sm.idx, sm.o, sm.ot);
-        __syncthreads();
-        float pv[4][4], dz[4][4];
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            f32x4 st = {0, 0, 0, 0}, dp = {0, 0, 0, 0};
-            const int qr = krow_of(s, col);
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                st = T::mma(T::ld8(&sm.q[qr][32 * ks + 8 * g]), kf[ks], st);
-                dp = T::mma(T::ld8(&sm.o[qr][32 * ks + 8 * g]), vf[ks], dp);
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int ql = key_of(s, g, i);
-                const int p = q0 + ql;
-                bool ok = p < qend && ktok >= 0;
-                if (MODE == kLeaf) ok = ok && p >= ktok;
-                else ok = ok && p >= blk_lo && p < blk_hi;
-                const float P = ok ? fast_exp2(st[i] * a.tau2 - sm.lse2[ql]) : 0.f;
-                const float sc = sm.scs[ql];
-                pv[s][i] = P * sc;
-                dz[s][i] = P * (sc * dp[i] - sm.delta[ql]);
-            }
+        if (t + 1 < ntiles) {
+            TD::load(Q, tok, rq);
+            TD::load(dO, tok, ro);
+            scalars(qt_next);
+            qt_cur = qt_next;
+            if (t + 2 < ntiles) tokens(q0 + 2 * kT, tok, qt_next);
         }
+        F pf[2], zf[2];
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
             float p8[8], z8[8];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                p8[j] = pv[2 * kk][j];
-                p8[4 + j] = pv[2 * kk + 1][j];
-                z8[j] = dz[2 * kk][j];
-                z8[4 + j] = dz[2 * kk + 1][j];
-            }
-            const F pf = T::pack(p8), zf = T::pack(z8);
+            for (int h2 = 0; h2 < 2; ++h2) {
+                const int s = 2 * kk + h2;
+                f32x4 st = {0, 0, 0, 0}, dp = {0, 0, 0, 0};
+                const int qr = krow_of(s, col);
 #pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-                av[dt] = T::mma(pf, T::ld8(&sm.ot[16 * dt + col][32 * kk + 8 * g]), av[dt]);
-                ak[dt] = T::mma(zf, T::ld8(&sm.qt[16 * dt + col][32 * kk + 8 * g]), ak[dt]);
-            }
-        }
-    }
-    __syncthreads();
-    // accumulator rows are keys 16w + 4g + i, columns d = 16 dt + col
+                for (int ks = 0; ks < KS; ++ks) {
+                    st = T::mma(TD::row8(sq, qr, 32 * ks + 8 * g), kf[ks], st);
+                    dp = T::mma(TD::row8(so, qr, 32 * ks + 8 * g), vf[ks], dp);
+                }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int kl = 16 * w + 4 * g + i;
-        const int kt = sm.ktok[kl];
-        if (kt < 0) continue;
-        if (MODE == kLevels) {
-            const size_t slot = level_slot(bh, a.Lv, level, N, kt, 0);
-            float* pk = a.part_dk + slot * D;
-            float* pv2 = a.part_dv + slot * D;
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-                pk[16 * dt + col] = ak[dt][i] * a.tau;
-                pv2[16 * dt + col] = av[dt][i];
-            }
-            continue;
-        }
-        const size_t row = bh * N + kt;
-        float tk[DT], tv[DT];
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-            tk[dt] = ak[dt][i] * a.tau + a.dk_lr[row * D + 16 * dt + col];
-            tv[dt] = av[dt][i] + a.dv_lr[row * D + 16 * dt + col];
-        }
-        if (MODE == kLeaf) {
-            for (int l = 0; l < a.Lv; ++l) {
-                const int hl = N >> (l + 1);
-                if (((j0 / hl) & 1) != 0) continue;   // keys of past halves only
-                const size_t slot = level_slot(bh, a.Lv, l, N, kt, 0);
-#pragma unroll
-                for (int dt = 0; dt < DT; ++dt) {
-                    tk[dt] += a.part_dk[slot * D + 16 * dt + col];
-                    tv[dt] += a.part_dv[slot * D + 16 * dt + col];
+                for (int i = 0; i < 4; ++i) {
+                    const int ql = key_of(s, g, i);
+                    const int p = q0 + ql;
+                    bool ok = ktok >= 0 && s_ok[ql];
+                    if (MODE == kLeaf) ok = ok && p >= ktok;
+                    else ok = ok && p >= blk_lo && p < blk_hi;
+                    const float P = ok ? fast_exp2(st[i] * a.tau2 - s_l2[ql]) : 0.f;
+                    const float c = s_sc[ql];
+                    p8[4 * h2 + i] = P * c;
+                    z8[4 * h2 + i] = P * (c * dp[i] - s_de[ql]);
                 }
             }
+            pf[kk] = T::pack(p8);
+            zf[kk] = T::pack(z8);
         }
-        S* ok = (S*)a.dK + row * D;
-        S* ov = (S*)a.dV + row * D;
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                avT[dt] = T::mma(TD::col8(so, 32 * kk, 16 * dt), pf[kk], avT[dt]);
+                akT[dt] = T::mma(TD::col8(sq, 32 * kk, 16 * dt), zf[kk], akT[dt]);
+            }
+    }
+
+    if (ktok < 0) return;
+    if (MODE == kLevels) {
+        const size_t slot = level_slot(bh, a.Lv, level, N, ktok, 0);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-            ok[16 * dt + col] = T::store(tk[dt]);
-            ov[16 * dt + col] = T::store(tv[dt]);
+            *(f32x4*)(a.part_dk + slot * D + 16 * dt + 4 * g) = akT[dt] * a.tau;
+            *(f32x4*)(a.part_dv + slot * D + 16 * dt + 4 * g) = avT[dt];
+        }
+        return;
+    }
+    const size_t row = bh * N + ktok;
+    f32x4 tk[DT], tv[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+        tk[dt] = akT[dt] * a.tau + *(const f32x4*)(a.dk_lr + row * D + 16 * dt + 4 * g);
+        tv[dt] = avT[dt] + *(const f32x4*)(a.dv_lr + row * D + 16 * dt + 4 * g);
+    }
+    if (MODE == kLeaf) {
+        for (int l = 0; l < a.Lv; ++l) {
+            const int hl = N >> (l + 1);
+            if (((j0 / hl) & 1) != 0) continue;   // keys of past halves only
+            const size_t slot = level_slot(bh, a.Lv, l, N, ktok, 0);
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                tk[dt] += *(const f32x4*)(a.part_dk + slot * D + 16 * dt + 4 * g);
+                tv[dt] += *(const f32x4*)(a.part_dv + slot * D + 16 * dt + 4 * g);
+            }
         }
     }
+    S* ok_ = (S*)a.dK + row * D;
+    S* ov = (S*)a.dV + row * D;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            ok_[16 * dt + 4 * g + i] = T::store(tk[dt][i]);
+            ov[16 * dt + 4 * g + i] = T::store(tv[dt][i]);
+        }
 }
 
 // ------------------------------------------------------------------------
