@@ -28,9 +28,10 @@ PEAK_F32_TFLOPS = 157.3        # fp32 matrix
 def kernel_model(w, Lv: int) -> dict:
     """Algorithmic bytes and flops per launch of each kernel (name -> (bytes, flops)).
 
-    Counts what the method must move or compute: every input row it needs is
-    read once per pass that needs it, outputs are written once at their
-    storage precision; scratch partials between kernels are not counted.
+    Counts what each kernel must move or compute: every input row it needs is
+    read once, every output written once at its storage precision; level
+    partials count as outputs of the level kernels and inputs of the leaf
+    kernels, which is what the decomposition into kernels requires.
     """
     s = 2 if w.dtype == "bf16" else 4
     bh = w.B * w.H
@@ -55,16 +56,22 @@ def kernel_model(w, Lv: int) -> dict:
     m["race_dv"] = (bh * N * (2 * P * 4 + D * s + 4 + D * s), bh * N * (2 * r * D * 2 + C * (r + D)))
     # sparse branch: interactions per query, 4D flops each forward (QK^T, PV)
     lvl_inter = half * min(k, half) if w.causal else 0
-    m["sparse_fwd_levels"] = (Lv * bh * half * (3 * D * s + 8), Lv * bh * lvl_inter * 4 * D)
-    m["sparse_fwd_leaf"] = (bh * N * (3 * D * s + D * 4 + 4 + D * s + 12),
+    lvl_pos = Lv * bh * half      # (level, position) slots of the partials
+    m["sparse_fwd_levels"] = (lvl_pos * (3 * D * s + 8 + D * 4 + 4), Lv * bh * lvl_inter * 4 * D)
+    m["sparse_fwd_leaf"] = (bh * N * (3 * D * s + D * 4 + 4 + D * s + D * 4 + 8) + lvl_pos * (D * 4 + 4),
                             bh * (N // n_leaf) * (n_leaf * (n_leaf + 1) // 2) * 4 * D)
     m["sparse_fwd_blocks"] = (bh * N * (3 * D * s + 8 + D * 4 + 4 + D * s + 12), bh * N * min(k, N) * 4 * D)
     m["bwd_rows"] = (bh * N * (D * s + 2 * D * 4 + 12 + 20), bh * N * 4 * D)
     m["sparse_dq_levels"] = (Lv * bh * half * (4 * D * s + 8 + D * 4), Lv * bh * lvl_inter * 6 * D)
     m["sparse_dkv_levels"] = (Lv * bh * half * (4 * D * s + 8 + 2 * D * 4), Lv * bh * lvl_inter * 8 * D)
+    # whole-block backward: Q, dO, K, V rows once, 3 row scalars + 2 indices
+    # per position, dQ / dK / dV level partials (float32) written once
+    m["sparse_bwd_levels"] = (Lv * bh * half * (4 * D * s + 20 + 3 * D * 4), Lv * bh * lvl_inter * 14 * D)
+    m["sparse_bwd_blocks"] = (bh * N * (4 * D * s + 20 + 3 * D * 4 + 3 * D * s), bh * N * min(k, N) * 14 * D)
     leaf_inter = bh * (N // n_leaf) * (n_leaf * (n_leaf + 1) // 2)
-    m["sparse_dq_leaf"] = (bh * N * (4 * D * s + D * s + 12), leaf_inter * 6 * D)
-    m["sparse_dkv_leaf"] = (bh * N * (4 * D * s + 2 * D * s + 12), leaf_inter * 8 * D)
+    m["sparse_dq_leaf"] = (bh * N * (4 * D * s + 12 + D * 4 + D * s) + lvl_pos * D * 4, leaf_inter * 6 * D)
+    m["sparse_dkv_leaf"] = (bh * N * (4 * D * s + 12 + 2 * D * 4 + 2 * D * s) + lvl_pos * 2 * D * 4,
+                            leaf_inter * 8 * D)
     m["sparse_dq_blocks"] = (bh * N * (4 * D * s + D * s + 12), bh * N * min(k, N) * 6 * D)
     m["sparse_dkv_blocks"] = (bh * N * (4 * D * s + 2 * D * s + 12), bh * N * min(k, N) * 8 * D)
     del seg_states, n0
@@ -103,8 +110,8 @@ def sources_of(kernel: str):
     if kernel in KERNEL_SOURCES:
         return KERNEL_SOURCES[kernel]
     if kernel.startswith("sparse_fwd"):
-        return ["sparse_fwd.hip", "common.hpp"]
-    return ["sparse_bwd.hip", "common.hpp"]
+        return ["sparse_fwd.hip", "tile.hpp", "common.hpp"]
+    return ["sparse_bwd.hip", "tile.hpp", "common.hpp"]
 
 
 def read_traffic(kernel: str, workload: str):
