@@ -165,32 +165,33 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
     }
 
     const int t_beg = seg * a.seg_len, t_end = min(a.N, t_beg + a.seg_len);
+    URegs<RP> uq, uk;                    // projections of the chunk, loaded one chunk ahead
+    uq.load(Uq, t_beg, a.N);
+    if (a.causal) uk.load(Uk, t_beg, a.N);
     for (int t0 = t_beg; t0 < t_end; t0 += kC) {
         __syncthreads();
         stage_r<T, D>(sm.dn, dO, t0, a.N, sclr);
         if (threadIdx.x < kC) sm.dden[threadIdx.x] = (t0 + threadIdx.x < a.N) ? dden[t0 + threadIdx.x] : 0.f;
-        features<T, RP>(Uq, t0, a.N, a.L, a.two_beta, nullptr, nullptr, sm.ts);
+        features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, nullptr, nullptr, sm.ts);
         if (a.causal) {
             stage_t<T, D>(sm.vt, V, t0, a.N);
-            features<T, RP>(Uk, t0, a.N, a.L, a.two_beta, nullptr, sm.pkt, nullptr);
+            features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, nullptr, sm.pkt, nullptr);
         }
         __syncthreads();
+        if (t0 + kC < t_end) {
+            uq.load(Uq, t0 + kC, a.N);
+            if (a.causal) uk.load(Uk, t0 + kC, a.N);
+        }
         if (a.causal) {
             // G rows [16w, 16w + 16): <dNum_i, V_j> + dDen_i for j <= i
             for (int kt = 0; kt < 4; ++kt) {
                 f32x4 acc = {0, 0, 0, 0};
                 if (kt <= w) {
-                    const int tok = t0 + 16 * kt + col;
+                    // V rows of keys 16 kt .. 16 kt + 15 from the transposed chunk tile
 #pragma unroll
-                    for (int ks = 0; ks < KS; ++ks) {
-                        F vf;
-                        if (tok < a.N) vf = T::ld8(V + (size_t)tok * D + 32 * ks + 8 * g);
-                        else {
-                            float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-                            vf = T::pack(z);
-                        }
-                        acc = T::mma(T::ld8(&sm.dn[16 * w + col][32 * ks + 8 * g]), vf, acc);
-                    }
+                    for (int ks = 0; ks < KS; ++ks)
+                        acc = T::mma(T::ld8(&sm.dn[16 * w + col][32 * ks + 8 * g]),
+                                     col8_t<T, kC + kPad>(sm.vt, 32 * ks, 16 * kt), acc);
                 }
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
@@ -201,34 +202,44 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
         }
         __syncthreads();
         // dphi(q)' tiles [features of table ft] x [16 queries]: S G-terms + A dDen + intra
+        // (the state's hi / lo bf16 split is made once per chunk and k-step)
 #pragma unroll
         for (int j = 0; j < NFT; ++j) {
             const int ft = w + 4 * j;
             if (ft >= FT) break;
-            for (int qt = 0; qt < 4; ++qt) {
-                f32x4 acc = {0, 0, 0, 0};
+            f32x4 acc[4];
 #pragma unroll
-                for (int ds = 0; ds < KS; ++ds) {
-                    float sv[8];
+            for (int qt = 0; qt < 4; ++qt) acc[qt] = f32x4{0, 0, 0, 0};
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        sv[i] = St_[j][2 * ds][i];
-                        sv[4 + i] = St_[j][2 * ds + 1][i];
-                    }
-                    acc = mma_split_a<T>(sv, T::ld44(&sm.dn[16 * qt + col][32 * ds + 4 * g],
-                                                     &sm.dn[16 * qt + col][32 * ds + 16 + 4 * g]), acc);
+            for (int ds = 0; ds < KS; ++ds) {
+                float sv[8];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    sv[i] = St_[j][2 * ds][i];
+                    sv[4 + i] = St_[j][2 * ds + 1][i];
                 }
+                F shi, slo;
+                T::split(sv, shi, slo);
+#pragma unroll
+                for (int qt = 0; qt < 4; ++qt) {
+                    const F bf = T::ld44(&sm.dn[16 * qt + col][32 * ds + 4 * g],
+                                         &sm.dn[16 * qt + col][32 * ds + 16 + 4 * g]);
+                    acc[qt] = T::mma(shi, bf, acc[qt]);
+                    if (T::kSplit) acc[qt] = T::mma(slo, bf, acc[qt]);
+                }
+            }
+            for (int qt = 0; qt < 4; ++qt) {
                 const float ddq = sm.dden[16 * qt + col];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) acc[i] += sm.a_state[16 * ft + 4 * g + i] * ddq;
+                for (int i = 0; i < 4; ++i) acc[qt][i] += sm.a_state[16 * ft + 4 * g + i] * ddq;
                 if (a.causal) {
 #pragma unroll
                     for (int kk = 0; kk < 2; ++kk)
-                        acc = T::mma(T::ld8(&sm.pkt[16 * ft + col][32 * kk + 8 * g]),
-                                     T::ld8(&sm.gg[16 * qt + col][32 * kk + 8 * g]), acc);
+                        acc[qt] = T::mma(T::ld8(&sm.pkt[16 * ft + col][32 * kk + 8 * g]),
+                                         T::ld8(&sm.gg[16 * qt + col][32 * kk + 8 * g]), acc[qt]);
                 }
-                acc *= a.inv_L;
-                chain_rule_t<T, RP>(acc, qt, ft, a.L, a.beta, sm.ts, sm.du);
+                acc[qt] *= a.inv_L;
+                chain_rule_t<T, RP>(acc[qt], qt, ft, a.L, a.beta, sm.ts, sm.du);
             }
         }
         __syncthreads();
@@ -295,70 +306,80 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
 
     const int t_beg = seg * a.seg_len, t_end = min(a.N, t_beg + a.seg_len);
     const int nch = (t_end - t_beg + kC - 1) / kC;
+    URegs<RP> uq, uk;                    // projections of the chunk, loaded one chunk ahead
+    uk.load(Uk, t_beg + (nch - 1) * kC, a.N);
+    if (a.causal) uq.load(Uq, t_beg + (nch - 1) * kC, a.N);
     for (int c = nch - 1; c >= 0; --c) {
         const int t0 = t_beg + c * kC;
         __syncthreads();
         stage_r<T, D>(sm.vr, V, t0, a.N);
         if (threadIdx.x < kC) sm.dden[threadIdx.x] = (t0 + threadIdx.x < a.N) ? dden[t0 + threadIdx.x] : 0.f;
-        features<T, RP>(Uk, t0, a.N, a.L, a.two_beta, nullptr, nullptr, sm.ts);
+        features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, nullptr, nullptr, sm.ts);
         if (a.causal) {
             stage_t<T, D>(sm.dnt, dO, t0, a.N, sclr, a.inv_L);
-            features<T, RP>(Uq, t0, a.N, a.L, a.two_beta, nullptr, sm.pqt, nullptr);
+            features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, nullptr, sm.pqt, nullptr);
         }
         __syncthreads();
+        if (c > 0) {
+            uk.load(Uk, t0 - kC, a.N);
+            if (a.causal) uq.load(Uq, t0 - kC, a.N);
+        }
         if (a.causal) {
             // G' rows j in [16w, 16w + 16): (<V_j, dNum_i> + dDen_i) / L for i >= j
             for (int it = 0; it < 4; ++it) {
                 f32x4 acc = {0, 0, 0, 0};
                 if (it >= w) {
-                    const int tok = t0 + 16 * it + col;
-                    const float sc = tok < a.N ? sclr[tok] : 0.f;
+                    // dNum / L rows of queries 16 it .. 16 it + 15 from the transposed chunk tile
 #pragma unroll
-                    for (int ks = 0; ks < KS; ++ks) {
-                        float v8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-                        if (tok < a.N) {
-                            const F raw = T::ld8(dO + (size_t)tok * D + 32 * ks + 8 * g);
-#pragma unroll
-                            for (int e = 0; e < 8; ++e) v8[e] = (float)raw[e] * sc;
-                        }
-                        acc = T::mma(T::ld8(&sm.vr[16 * w + col][32 * ks + 8 * g]), T::pack(v8), acc);
-                    }
+                    for (int ks = 0; ks < KS; ++ks)
+                        acc = T::mma(T::ld8(&sm.vr[16 * w + col][32 * ks + 8 * g]),
+                                     col8_t<T, kC + kPad>(sm.dnt, 32 * ks, 16 * it), acc);
                 }
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int kj = 16 * w + 4 * g + i, qi = 16 * it + col;
-                    sm.ggt[kj][qi] = T::store(qi >= kj ? (acc[i] + sm.dden[qi]) * a.inv_L : 0.f);
+                    sm.ggt[kj][qi] = T::store(qi >= kj ? acc[i] + sm.dden[qi] * a.inv_L : 0.f);
                 }
             }
         }
         __syncthreads();
         // dphi(k)' tiles [features of table ft] x [16 keys]: dS V + dA + intra
+        // (the state's hi / lo bf16 split is made once per chunk and k-step)
 #pragma unroll
         for (int j = 0; j < NFT; ++j) {
             const int ft = w + 4 * j;
             if (ft >= FT) break;
-            for (int kt = 0; kt < 4; ++kt) {
-                f32x4 acc = {0, 0, 0, 0};
+            f32x4 acc[4];
 #pragma unroll
-                for (int ds = 0; ds < KS; ++ds) {
-                    float sv[8];
+            for (int kt = 0; kt < 4; ++kt) acc[kt] = f32x4{0, 0, 0, 0};
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        sv[i] = St_[j][2 * ds][i];
-                        sv[4 + i] = St_[j][2 * ds + 1][i];
-                    }
-                    acc = mma_split_a<T>(sv, T::ld44(&sm.vr[16 * kt + col][32 * ds + 4 * g],
-                                                     &sm.vr[16 * kt + col][32 * ds + 16 + 4 * g]), acc);
+            for (int ds = 0; ds < KS; ++ds) {
+                float sv[8];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    sv[i] = St_[j][2 * ds][i];
+                    sv[4 + i] = St_[j][2 * ds + 1][i];
                 }
+                F shi, slo;
+                T::split(sv, shi, slo);
 #pragma unroll
-                for (int i = 0; i < 4; ++i) acc[i] += sm.a_state[16 * ft + 4 * g + i];
+                for (int kt = 0; kt < 4; ++kt) {
+                    const F bf = T::ld44(&sm.vr[16 * kt + col][32 * ds + 4 * g],
+                                         &sm.vr[16 * kt + col][32 * ds + 16 + 4 * g]);
+                    acc[kt] = T::mma(shi, bf, acc[kt]);
+                    if (T::kSplit) acc[kt] = T::mma(slo, bf, acc[kt]);
+                }
+            }
+            for (int kt = 0; kt < 4; ++kt) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[kt][i] += sm.a_state[16 * ft + 4 * g + i];
                 if (a.causal) {
 #pragma unroll
                     for (int kk = 0; kk < 2; ++kk)
-                        acc = T::mma(T::ld8(&sm.pqt[16 * ft + col][32 * kk + 8 * g]),
-                                     T::ld8(&sm.ggt[16 * kt + col][32 * kk + 8 * g]), acc);
+                        acc[kt] = T::mma(T::ld8(&sm.pqt[16 * ft + col][32 * kk + 8 * g]),
+                                         T::ld8(&sm.ggt[16 * kt + col][32 * kk + 8 * g]), acc[kt]);
                 }
-                chain_rule_t<T, RP>(acc, kt, ft, a.L, a.beta, sm.ts, sm.du);
+                chain_rule_t<T, RP>(acc[kt], kt, ft, a.L, a.beta, sm.ts, sm.du);
             }
         }
         __syncthreads();
@@ -388,7 +409,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
 
 // ---------------------------------------------------------------- LB3: dV
 template <class T, int D, int RP>
-__global__ __launch_bounds__(kThreads) void race_dv_kernel(LbArgs a)
+__global__ __launch_bounds__(kThreads, 2) void race_dv_kernel(LbArgs a)
 {
     using St = typename T::store_t;
     using F = typename T::frag_t;
@@ -416,15 +437,22 @@ __global__ __launch_bounds__(kThreads) void race_dv_kernel(LbArgs a)
 
     const int t_beg = seg * a.seg_len, t_end = min(a.N, t_beg + a.seg_len);
     const int nch = (t_end - t_beg + kC - 1) / kC;
+    URegs<RP> uq, uk;                    // projections of the chunk, loaded one chunk ahead
+    uk.load(Uk, t_beg + (nch - 1) * kC, a.N);
+    if (a.causal) uq.load(Uq, t_beg + (nch - 1) * kC, a.N);
     for (int c = nch - 1; c >= 0; --c) {
         const int t0 = t_beg + c * kC;
         __syncthreads();
-        features<T, RP>(Uk, t0, a.N, a.L, a.two_beta, sm.pk, nullptr, nullptr);
+        features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, sm.pk, nullptr, nullptr);
         if (a.causal) {
             stage_t<T, D>(sm.dnt, dO, t0, a.N, sclr, a.inv_L);
-            features<T, RP>(Uq, t0, a.N, a.L, a.two_beta, sm.pq, sm.pqt, nullptr);
+            features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, sm.pq, sm.pqt, nullptr);
         }
         __syncthreads();
+        if (c > 0) {
+            uk.load(Uk, t0 - kC, a.N);
+            if (a.causal) uq.load(Uq, t0 - kC, a.N);
+        }
         if (a.causal) {
             // M' rows j in [16w, 16w + 16): <phi(k_j), phi(q_i)> for i >= j
             for (int it = 0; it < 4; ++it) {
@@ -443,25 +471,37 @@ __global__ __launch_bounds__(kThreads) void race_dv_kernel(LbArgs a)
             }
         }
         __syncthreads();
+        f32x4 accs[4][DW];
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt) {
-            f32x4 acc[DW];
+        for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-            for (int j = 0; j < DW; ++j) acc[j] = f32x4{0, 0, 0, 0};
+            for (int j = 0; j < DW; ++j) accs[kt][j] = f32x4{0, 0, 0, 0};
 #pragma unroll
-            for (int fs = 0; fs < FS; ++fs) {
+        for (int fs = 0; fs < FS; ++fs) {
+            F shi[DW], slo[DW];
+#pragma unroll
+            for (int j = 0; j < DW; ++j) {
+                float sv[8];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    sv[i] = S[2 * fs][j][i];
+                    sv[4 + i] = S[2 * fs + 1][j][i];
+                }
+                T::split(sv, shi[j], slo[j]);
+            }
+#pragma unroll
+            for (int kt = 0; kt < 4; ++kt) {
                 const F af = T::ld44(&sm.pk[16 * kt + col][32 * fs + 4 * g], &sm.pk[16 * kt + col][32 * fs + 16 + 4 * g]);
 #pragma unroll
                 for (int j = 0; j < DW; ++j) {
-                    float sv[8];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        sv[i] = S[2 * fs][j][i];
-                        sv[4 + i] = S[2 * fs + 1][j][i];
-                    }
-                    acc[j] = mma_split<T>(af, sv, acc[j]);
+                    accs[kt][j] = T::mma(af, shi[j], accs[kt][j]);
+                    if (T::kSplit) accs[kt][j] = T::mma(af, slo[j], accs[kt][j]);
                 }
             }
+        }
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) {
+            f32x4 (&acc)[DW] = accs[kt];
             if (a.causal) {
 #pragma unroll
                 for (int kk = 0; kk < 2; ++kk) {

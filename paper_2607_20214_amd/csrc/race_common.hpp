@@ -32,6 +32,26 @@ __device__ __forceinline__ float tanh_abs(float u)
     return 1.f - 2.f * __builtin_amdgcn_rcpf(1.f + __expf(2.f * u));
 }
 
+// 8-slot operand fragment from a tile stored transposed, xt[k][n] (row
+// stride LD elements): lane (i = lane % 16, g = lane / 16) receives column
+// c0 + i at rows kb + 8 g + j, j = 0..7 (16-bit: two transposed LDS reads).
+template <class T, int LD>
+__device__ __forceinline__ typename T::frag_t col8_t(const typename T::store_t (*xt)[LD], int kb, int c0)
+{
+    const int lane = threadIdx.x & 63, g = lane >> 4, i = lane & 15;
+    const int r = kb + 8 * g;
+    if constexpr (T::bytes == 2) {
+        const bf16x4 lo = lds_read_tr4((const uint16_t*)&xt[r + (i >> 2)][c0 + 4 * (i & 3)]);
+        const bf16x4 hi = lds_read_tr4((const uint16_t*)&xt[r + 4 + (i >> 2)][c0 + 4 * (i & 3)]);
+        return typename T::frag_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    } else {
+        typename T::frag_t f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) f[j] = xt[r + j][c0 + i];
+        return f;
+    }
+}
+
 // projection count padded to whole 32-wide k-steps (backward du x W)
 template <int RP> constexpr int w_kdim() { return RP / 4 < 32 ? 32 : RP / 4; }
 
@@ -91,24 +111,45 @@ __device__ void stage_r(typename T::store_t (*x)[D + kPad], const typename T::st
     }
 }
 
+// Projections u of the tables this lane handles for chunk tokens
+// [t0 + 16w, t0 + 16w + 16) (table tb = g + 4 m of token 16w + col), loaded
+// ahead of features_from so that the next chunk's loads overlap this one.
+template <int RP>
+struct URegs {
+    static constexpr int NU = (RP / 16 + 3) / 4;
+    f32x4 u[NU];
+    __device__ __forceinline__ void load(const float* U, int t0, int N)
+    {
+        const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+        const int g = lane >> 4, col = lane & 15;
+        const int tok = t0 + 16 * wv + col;
+#pragma unroll
+        for (int m = 0; m < NU; ++m) {
+            const int tb = g + 4 * m;
+            u[m] = f32x4{0, 0, 0, 0};
+            if (tb < RP / 16 && tok < N) u[m] = *(const f32x4*)(U + (size_t)tok * (RP / 4) + 4 * tb);
+        }
+    }
+};
+
 // Features of chunk tokens [t0 + 16w, t0 + 16w + 16) for every table, from
-// the stored projections U[token][4 * table + bit] (float32, row stride RP/4).
+// the projections in ur (URegs::load of the same chunk).
 // Writes phi (as T) row-major into ph[token][feature] and/or transposed into
 // pht[feature][token], and t = tanh(u) into ts[token][4 * table + bit].
 template <class T, int RP>
-__device__ void features(const float* U, int t0, int N, int L, float two_beta,
-                         typename T::store_t (*ph)[RP + kPad], typename T::store_t (*pht)[kC + kPad],
-                         float (*ts)[RP / 4])
+__device__ void features_from(const URegs<RP>& ur, int t0, int N, int L, float two_beta,
+                              typename T::store_t (*ph)[RP + kPad], typename T::store_t (*pht)[kC + kPad],
+                              float (*ts)[RP / 4])
 {
-    constexpr int UP = RP / 4;
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int g = lane >> 4, col = lane & 15;
     const int tl = 16 * wv + col;
     const int tok = t0 + tl;
 #pragma unroll
-    for (int tb = g; tb < RP / 16; tb += 4) {   // this lane: table tb of token tl
-        f32x4 u = {0, 0, 0, 0};
-        if (tok < N) u = *(const f32x4*)(U + (size_t)tok * UP + 4 * tb);
+    for (int m = 0; m < URegs<RP>::NU; ++m) {   // this lane: table tb of token tl
+        const int tb = g + 4 * m;
+        if (tb >= RP / 16) break;
+        const f32x4 u = ur.u[m];
         const bool live = tb < L && tok < N;
         float t[4], sp[4], sn[4];
 #pragma unroll
@@ -136,6 +177,17 @@ __device__ void features(const float* U, int t0, int N, int L, float two_beta,
             for (int c = 0; c < 16; ++c) pht[16 * tb + c][tl] = T::store(phi[c]);
         }
     }
+}
+
+// features_from with the projections loaded on the spot.
+template <class T, int RP>
+__device__ void features(const float* U, int t0, int N, int L, float two_beta,
+                         typename T::store_t (*ph)[RP + kPad], typename T::store_t (*pht)[kC + kPad],
+                         float (*ts)[RP / 4])
+{
+    URegs<RP> ur;
+    ur.load(U, t0, N);
+    features_from<T, RP>(ur, t0, N, L, two_beta, ph, pht, ts);
 }
 
 // Chain rule from a transposed feature-gradient tile to the projection

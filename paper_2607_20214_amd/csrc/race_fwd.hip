@@ -82,6 +82,8 @@ __global__ __launch_bounds__(kThreads) void race_state_kernel(StateArgs a)
         for (int j = 0; j < DW; ++j) S[ft][j] = f32x4{0, 0, 0, 0};
 
     const int t_beg = seg * a.seg_len, t_end = min(a.N, t_beg + a.seg_len);
+    URegs<RP> ur;                        // projections of the chunk, loaded one chunk ahead
+    ur.load(U, t_beg, a.N);
     for (int t0 = t_beg; t0 < t_end; t0 += kC) {
         __syncthreads();
         stage_t<T, D>(sm.vt, Vl, t0, a.N, vs);
@@ -89,8 +91,9 @@ __global__ __launch_bounds__(kThreads) void race_state_kernel(StateArgs a)
             const int r = t0 + threadIdx.x;
             sm.aw[threadIdx.x] = (r < a.N) ? (aw ? aw[r] : 1.f) : 0.f;
         }
-        features<T, RP>(U, t0, a.N, a.L, a.two_beta, nullptr, sm.pht, nullptr);
+        features_from<T, RP>(ur, t0, a.N, a.L, a.two_beta, nullptr, sm.pht, nullptr);
         __syncthreads();
+        if (t0 + kC < t_end) ur.load(U, t0 + kC, a.N);
         // S[f][cols of wave] += Phi'[f][rows] V[rows][cols]
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
@@ -164,7 +167,7 @@ struct OutArgs {
 };
 
 template <class T, int D, int RP>
-__global__ __launch_bounds__(kThreads) void race_out_kernel(OutArgs a)
+__global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
 {
     using St = typename T::store_t;
     using F = typename T::frag_t;
@@ -193,12 +196,19 @@ __global__ __launch_bounds__(kThreads) void race_out_kernel(OutArgs a)
     for (int f = threadIdx.x; f < RP; f += kThreads) sm.a_state[f] = st_in[RP * D + f];
 
     const int t_beg = seg * a.seg_len, t_end = min(a.N, t_beg + a.seg_len);
+    URegs<RP> uq, uk;                    // projections of the chunk, loaded one chunk ahead
+    uq.load(Uq, t_beg, a.N);
+    if (a.causal) uk.load(Uk, t_beg, a.N);
     for (int t0 = t_beg; t0 < t_end; t0 += kC) {
         __syncthreads();
         stage_t<T, D>(sm.vt, V, t0, a.N);
-        features<T, RP>(Uq, t0, a.N, a.L, a.two_beta, sm.phq, nullptr, nullptr);
-        if (a.causal) features<T, RP>(Uk, t0, a.N, a.L, a.two_beta, sm.phk, sm.phkt, nullptr);
+        features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, sm.phq, nullptr, nullptr);
+        if (a.causal) features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, sm.phk, sm.phkt, nullptr);
         __syncthreads();
+        if (t0 + kC < t_end) {
+            uq.load(Uq, t0 + kC, a.N);
+            if (a.causal) uk.load(Uk, t0 + kC, a.N);
+        }
         // Den, inter part: (1/L) Phi_Q . A   (4 threads per query)
         {
             const int q = threadIdx.x >> 2, part = threadIdx.x & 3;
@@ -235,36 +245,49 @@ __global__ __launch_bounds__(kThreads) void race_out_kernel(OutArgs a)
             }
         }
         __syncthreads();
-        // Num for the wave's d columns, all 64 queries
+        // Num for the wave's d columns, all 64 queries: inter-chunk part with S
+        // in float32 accuracy (hi / lo bf16 split made once per chunk), then
+        // the masked intra-chunk part
+        f32x4 num[4][DW];
 #pragma unroll
-        for (int qt = 0; qt < 4; ++qt) {
-            f32x4 num[DW];
+        for (int qt = 0; qt < 4; ++qt)
 #pragma unroll
-            for (int j = 0; j < DW; ++j) num[j] = f32x4{0, 0, 0, 0};
+            for (int j = 0; j < DW; ++j) num[qt][j] = f32x4{0, 0, 0, 0};
 #pragma unroll
-            for (int fs = 0; fs < FS; ++fs) {
+        for (int fs = 0; fs < FS; ++fs) {
+            F shi[DW], slo[DW];
+#pragma unroll
+            for (int j = 0; j < DW; ++j) {
+                float sv[8];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    sv[i] = S[2 * fs][j][i];
+                    sv[4 + i] = S[2 * fs + 1][j][i];
+                }
+                T::split(sv, shi[j], slo[j]);
+            }
+#pragma unroll
+            for (int qt = 0; qt < 4; ++qt) {
                 const F af = T::ld44(&sm.phq[16 * qt + col][32 * fs + 4 * g],
                                      &sm.phq[16 * qt + col][32 * fs + 16 + 4 * g]);
 #pragma unroll
                 for (int j = 0; j < DW; ++j) {
-                    float sv[8];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        sv[i] = S[2 * fs][j][i];
-                        sv[4 + i] = S[2 * fs + 1][j][i];
-                    }
-                    num[j] = mma_split<T>(af, sv, num[j]);   // S in float32 accuracy
+                    num[qt][j] = T::mma(af, shi[j], num[qt][j]);
+                    if (T::kSplit) num[qt][j] = T::mma(af, slo[j], num[qt][j]);
                 }
             }
+        }
 #pragma unroll
-            for (int j = 0; j < DW; ++j) num[j] *= a.inv_L;
+        for (int qt = 0; qt < 4; ++qt) {
+#pragma unroll
+            for (int j = 0; j < DW; ++j) num[qt][j] *= a.inv_L;
             if (a.causal) {
 #pragma unroll
                 for (int kk = 0; kk < 2; ++kk) {
                     const F af = T::ld8(&sm.mm[16 * qt + col][32 * kk + 8 * g]);
 #pragma unroll
                     for (int j = 0; j < DW; ++j)
-                        num[j] = T::mma(af, T::ld8(&sm.vt[16 * (w * DW + j) + col][32 * kk + 8 * g]), num[j]);
+                        num[qt][j] = T::mma(af, T::ld8(&sm.vt[16 * (w * DW + j) + col][32 * kk + 8 * g]), num[qt][j]);
                 }
             }
 #pragma unroll
@@ -275,7 +298,7 @@ __global__ __launch_bounds__(kThreads) void race_out_kernel(OutArgs a)
                 const float den = sm.den_a[ql] + (a.causal ? sm.den_b[ql] : 0.f);
                 const float inv = 1.f / (den + a.eps);
 #pragma unroll
-                for (int j = 0; j < DW; ++j) Olr[(size_t)tok * D + 16 * (w * DW + j) + col] = num[j][i] * inv;
+                for (int j = 0; j < DW; ++j) Olr[(size_t)tok * D + 16 * (w * DW + j) + col] = num[qt][j][i] * inv;
             }
         }
         if (threadIdx.x < kC && t0 + threadIdx.x < a.N)
