@@ -94,9 +94,14 @@ int elsaa_workspace_bytes(const elsaa_config* cfg, int pass, size_t* bytes);
  *                   the backward's <dO, O_s> and <dO, O_lr> cancel against
  *                   <dO, V_j> terms);
  *   u_q, u_k        float32 [B,H,N,P] RACE projections u = W_race x of the Q and K
- *                   rows (P = 4 L rounded up to 8, 16, 32 or 64; padded tables 0). */
+ *                   rows (P = 4 L rounded up to 8, 16, 32 or 64; padded tables 0);
+ *   race_states     float32 RACE segment states phi(k) V' and phi(k) of the key
+ *                   rows before each sequence segment (causal; the totals when
+ *                   non-causal), [B*H][segments][r_p * d_h + r_p] with r_p = r
+ *                   rounded up to 32, 64, 128 or 256; the segment length is an
+ *                   internal choice, so only the library reads this region. */
 typedef struct {
-    size_t perm_q, perm_k, m, o_sparse, o_lowrank, u_q, u_k, total;
+    size_t perm_q, perm_k, m, o_sparse, o_lowrank, u_q, u_k, race_states, total;
 } elsaa_saved_layout;
 int elsaa_get_saved_layout(const elsaa_config* cfg, elsaa_saved_layout* out);
 

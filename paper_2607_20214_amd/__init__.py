@@ -42,7 +42,7 @@ class _Config(C.Structure):
 class _SavedLayout(C.Structure):
     _fields_ = [("perm_q", C.c_size_t), ("perm_k", C.c_size_t), ("m", C.c_size_t),
                 ("o_sparse", C.c_size_t), ("o_lowrank", C.c_size_t), ("u_q", C.c_size_t),
-                ("u_k", C.c_size_t), ("total", C.c_size_t)]
+                ("u_k", C.c_size_t), ("race_states", C.c_size_t), ("total", C.c_size_t)]
 
 
 class _GemmDesc(C.Structure):

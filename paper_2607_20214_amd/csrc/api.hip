@@ -124,7 +124,7 @@ int validate(const elsaa_config* c, Shape* s)
 }
 
 struct SavedLayout {
-    size_t perm_q, perm_k, m, o_s, o_lr, u_q, u_k, total;
+    size_t perm_q, perm_k, m, o_s, o_lr, u_q, u_k, race_states, total;
 };
 
 SavedLayout saved_layout(const Shape& s)
@@ -139,12 +139,13 @@ SavedLayout saved_layout(const Shape& s)
     L.o_lr = off; off = align256(off + bh * s.N * s.D * 4);   // float32, same reason (dDen)
     L.u_q = off; off = align256(off + bh * s.N * race_proj_stride(s) * 4);
     L.u_k = off; off = align256(off + bh * s.N * race_proj_stride(s) * 4);
+    L.race_states = off; off = align256(off + race_state_floats(s) * 4);   // RACE segment prefix states
     L.total = off;
     return L;
 }
 
 struct FwdWorkspace {
-    size_t keyq, keyk, states, part_o, part_lse, total;
+    size_t keyq, keyk, part_o, part_lse, total;
 };
 
 FwdWorkspace fwd_workspace(const Shape& s)
@@ -154,7 +155,6 @@ FwdWorkspace fwd_workspace(const Shape& s)
     size_t off = 0;
     W.keyq = off; off = align256(off + bh * s.N);
     W.keyk = off; off = align256(off + bh * s.N);
-    W.states = off; off = align256(off + race_state_floats(s) * 4);
     const size_t npart = s.causal ? bh * s.Lv * (size_t)(s.N / 2) : 0;
     W.part_o = off; off = align256(off + npart * s.D * 4);
     W.part_lse = off; off = align256(off + npart * 4);
@@ -163,7 +163,7 @@ FwdWorkspace fwd_workspace(const Shape& s)
 }
 
 struct BwdWorkspace {
-    size_t rs, states_f, states_b, wt_hi, wt_lo, dq_lr, dk_lr, dv_lr, part_dq, part_dk, part_dv, total;
+    size_t rs, states_b, wt_hi, wt_lo, dq_lr, dk_lr, dv_lr, part_dq, part_dk, part_dv, total;
 };
 
 BwdWorkspace bwd_workspace(const Shape& s)
@@ -174,7 +174,6 @@ BwdWorkspace bwd_workspace(const Shape& s)
     const size_t npart = s.causal ? bh * s.Lv * (size_t)(s.N / 2) : 0;
     size_t off = 0;
     W.rs = off; off = align256(off + 5 * bhn * 4);
-    W.states_f = off; off = align256(off + race_state_floats(s) * 4);
     W.states_b = off; off = align256(off + race_state_floats(s) * 4);
     W.wt_hi = off; off = align256(off + race_wt_bytes(s));
     W.wt_lo = off; off = align256(off + race_wt_bytes(s));
@@ -241,6 +240,7 @@ int elsaa_get_saved_layout(const elsaa_config* cfg, elsaa_saved_layout* out)
     out->o_lowrank = L.o_lr;
     out->u_q = L.u_q;
     out->u_k = L.u_k;
+    out->race_states = L.race_states;
     out->total = L.total;
     return ELSAA_OK;
 }
@@ -300,7 +300,7 @@ int elsaa_fwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     if ((e = launch_project(s, Q, W_sort, W_race, kq, uq, stream)) != hipSuccess) return hip_fail(e, "project(Q)");
     if ((e = launch_project(s, K, W_sort, W_race, kk, uk, stream)) != hipSuccess) return hip_fail(e, "project(K)");
     if ((e = launch_sort(s, kq, kk, pq, pk, stream)) != hipSuccess) return hip_fail(e, "sort");
-    if ((e = launch_race_fwd(s, uq, uk, V, at<float>(workspace, W.states), o_lr, d_lr, stream)) != hipSuccess)
+    if ((e = launch_race_fwd(s, uq, uk, V, at<float>(saved, SL.race_states), o_lr, d_lr, stream)) != hipSuccess)
         return hip_fail(e, "race forward");
     if ((e = launch_sparse_fwd(s, Q, K, V, pq, pk, gates, o_lr, d_lr, at<float>(workspace, W.part_o),
                                at<float>(workspace, W.part_lse), O, lse, m, o_s, stream)) != hipSuccess)
@@ -344,7 +344,7 @@ int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     hipError_t e;
     if ((e = launch_bwd_rows(s, dO, o_s, o_lr, m, lse, d_lr, gates, rs, dgates, stream)) != hipSuccess)
         return hip_fail(e, "backward row scalars");
-    if ((e = launch_race_bwd(s, uq, uk, V, dO, W_race, rs, at<float>(workspace, W.states_f),
+    if ((e = launch_race_bwd(s, uq, uk, V, dO, W_race, rs, at<float>(sv, SL.race_states),
                              at<float>(workspace, W.states_b), at<char>(workspace, W.wt_hi),
                              at<char>(workspace, W.wt_lo), dq_lr, dk_lr, dv_lr, stream)) != hipSuccess)
         return hip_fail(e, "race backward");

@@ -67,9 +67,10 @@ hipError_t launch_race_states(const Shape& s, const float* U, const void* Val, c
 hipError_t launch_race_fwd(const Shape& s, const float* Uq, const float* Uk, const void* V,
                            float* states, float* O_lr, float* d_lr, hipStream_t st);
 size_t race_wt_bytes(const Shape& s);       // one of the W' hi / lo buffers
+// states_f: the forward's segment prefix states (elsaa_fwd keeps them in saved)
 hipError_t launch_race_bwd(const Shape& s, const float* Uq, const float* Uk, const void* V,
                            const void* dO, const float* W_race, const float* rs,
-                           float* states_f, float* states_b, void* wt_hi, void* wt_lo,
+                           const float* states_f, float* states_b, void* wt_hi, void* wt_lo,
                            float* dq_lr, float* dk_lr, float* dv_lr, hipStream_t st);
 
 // sortLSH sparse branch forward + fusion epilogue

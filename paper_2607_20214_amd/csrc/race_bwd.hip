@@ -594,7 +594,7 @@ size_t race_wt_bytes(const Shape& s)
 
 hipError_t launch_race_bwd(const Shape& s, const float* Uq, const float* Uk, const void* V,
                            const void* dO, const float* W_race, const float* rs,
-                           float* states_f, float* states_b, void* wt_hi, void* wt_lo,
+                           const float* states_f, float* states_b, void* wt_hi, void* wt_lo,
                            float* dq_lr, float* dk_lr, float* dv_lr, hipStream_t st)
 {
     {
@@ -611,12 +611,10 @@ hipError_t launch_race_bwd(const Shape& s, const float* Uq, const float* Uk, con
         if (e0 != hipSuccess) return e0;
     }
     const size_t BHN = (size_t)s.B * s.H * s.N;
-    // forward prefix states of phi(k) V' and phi(k); backward suffix states
-    // of phi(q) dNum' / L and phi(q) dDen / L
-    hipError_t e = launch_race_states(s, Uk, V, nullptr, nullptr, 1.f, states_f, s.causal ? 1 : 0, st);
-    if (e != hipSuccess) return e;
-    e = launch_race_states(s, Uq, dO, rs + 3 * BHN, rs + 4 * BHN, 1.f / (float)s.L, states_b,
-                           s.causal ? 2 : 0, st);
+    // backward suffix states of phi(q) dNum' / L and phi(q) dDen / L (the
+    // forward prefix states of phi(k) V' and phi(k) come from the forward)
+    hipError_t e = launch_race_states(s, Uq, dO, rs + 3 * BHN, rs + 4 * BHN, 1.f / (float)s.L, states_b,
+                                      s.causal ? 2 : 0, st);
     if (e != hipSuccess) return e;
     LbArgs a;
     a.Uq = Uq; a.Uk = Uk; a.V = V; a.dO = dO; a.wt_hi = wt_hi; a.wt_lo = wt_lo; a.rs = rs;
