@@ -71,12 +71,19 @@ __global__ __launch_bounds__(kProjThreads) void proj_kernel(const typename T::st
     }
     __syncthreads();
     // hash: thread (row, bit group) runs the float32 fma chains of its bits
+    // over the row, read from LDS in 16-byte pieces
     {
         const int r = threadIdx.x & (kProjRows - 1);
         uint32_t c = 0;
         for (int bit = threadIdx.x / kProjRows; bit < bits; bit += kProjThreads / kProjRows) {
             float p = 0.0f;
-            for (int e = 0; e < D; ++e) p = __builtin_fmaf(sm.ws[bit][e], T::load(sm.x[r][e]), p);
+#pragma unroll 4
+            for (int e0 = 0; e0 < D; e0 += PER) {
+                const uint4 v = *(const uint4*)&sm.x[r][e0];
+                const S* xs = (const S*)&v;
+#pragma unroll
+                for (int j = 0; j < PER; ++j) p = __builtin_fmaf(sm.ws[bit][e0 + j], T::load(xs[j]), p);
+            }
             if (p > 0.0f) c |= 1u << bit;
         }
         if (c) atomicOr(&sm.code[r], c);
