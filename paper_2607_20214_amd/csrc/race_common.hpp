@@ -17,12 +17,15 @@ constexpr int kThreads = 256;
 constexpr int kPad = 8;
 constexpr size_t kMaxLds = 160 * 1024;
 
-// sigmoid(x) and sigmoid(-x) from the hardware exp and reciprocal (about one
-// ulp each; exp overflow gives 0 for the vanishing side)
+// sigmoid(x) and sigmoid(-x) from one hardware exp and reciprocal: with
+// e = exp(-|x|) in (0, 1], sigmoid(|x|) = 1 / (1 + e) and
+// sigmoid(-|x|) = e / (1 + e), each within a few ulp and without overflow.
 __device__ __forceinline__ void sigmoid_pair(float x, float& sp, float& sn)
 {
-    sp = __builtin_amdgcn_rcpf(1.f + __expf(-x));
-    sn = __builtin_amdgcn_rcpf(1.f + __expf(x));
+    const float e = __expf(-fabsf(x));
+    const float big = __builtin_amdgcn_rcpf(1.f + e), small = e * big;
+    sp = x >= 0.f ? big : small;
+    sn = x >= 0.f ? small : big;
 }
 
 // tanh(u) = 1 - 2 / (1 + e^{2u}), absolute error about 1e-7 (the features use
