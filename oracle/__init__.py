@@ -39,7 +39,8 @@ class _Cfg(C.Structure):
     _fields_ = [("N", C.c_int32), ("d", C.c_int32), ("k", C.c_int32), ("r", C.c_int32),
                 ("race_bits", C.c_int32), ("sort_bits", C.c_int32), ("n0", C.c_int32),
                 ("causal", C.c_int32), ("beta", C.c_double), ("lam", C.c_double),
-                ("eps", C.c_double), ("scale", C.c_double)]
+                ("eps", C.c_double), ("scale", C.c_double), ("neighbors", C.c_int32),
+                ("m_one", C.c_int32)]
 
 
 @dataclass
@@ -57,11 +58,13 @@ class HeadCfg:
     lam: float = 1.0
     eps: float = 1e-6
     scale: float = 0.0     # <= 0 -> 1/sqrt(d)
+    neighbors: int = 0     # r neighbouring sorted blocks on each side
+    m_one: bool = False    # Sort_Lsh_RACE ablation: m_sparse = 1
 
     def c(self) -> _Cfg:
         return _Cfg(self.N, self.d, self.k, self.r, self.race_bits, self.sort_bits,
                     self.n0 if self.n0 is not None else 2 * self.k, int(self.causal),
-                    self.beta, self.lam, self.eps, self.scale)
+                    self.beta, self.lam, self.eps, self.scale, self.neighbors, int(self.m_one))
 
     @property
     def L(self) -> int:
@@ -82,8 +85,8 @@ def _load():
         lib.ora_support_size.restype = C.c_int64
         lib.ora_support.argtypes = [P, P, P, P, P, P]
         lib.ora_features.argtypes = [C.c_int, C.c_int, P, C.c_int, C.c_int, C.c_double, P, P]
-        lib.ora_forward.argtypes = [P] + [P] * 13
-        lib.ora_backward.argtypes = [P] + [P] * 13
+        lib.ora_forward.argtypes = [P] + [P] * 14
+        lib.ora_backward.argtypes = [P] + [P] * 15
         _lib = lib
     return _lib
 
@@ -154,34 +157,40 @@ def features(X, Wrace, race_bits: int, beta: float) -> np.ndarray:
     return out
 
 
-def forward(cfg: HeadCfg, Q, K, V, Wsort, Wrace, gates=None, row_mask=None) -> dict:
-    """Forward of one head; returns O, lse, d_lr, m, O_s, O_lr (float64)."""
+def forward(cfg: HeadCfg, Q, K, V, Wsort, Wrace, gates=None, row_mask=None, lam_rows=None) -> dict:
+    """Forward of one head; returns O, lse, d_lr, m, O_s, O_lr (float64).
+    lam_rows: per-token lambda_i [N] (None: the scalar cfg.lam)."""
     Q, K, V, Wsort, Wrace = map(_f32, (Q, K, V, Wsort, Wrace))
     g = None if gates is None else _f32(gates)
+    lr = None if lam_rows is None else _f32(lam_rows)
     msk = None if row_mask is None else np.ascontiguousarray(row_mask, dtype=np.uint8)
     N, d = cfg.N, cfg.d
     out = {"O": np.zeros((N, d)), "lse": np.zeros(N), "d_lr": np.zeros(N), "m": np.zeros(N),
            "O_s": np.zeros((N, d)), "O_lr": np.zeros((N, d))}
     c = cfg.c()
     _check(_load().ora_forward(C.byref(c), _ptr(Q), _ptr(K), _ptr(V), _ptr(Wsort), _ptr(Wrace),
-                               _ptr(g), _ptr(msk), _ptr(out["O"]), _ptr(out["lse"]), _ptr(out["d_lr"]),
+                               _ptr(g), _ptr(lr), _ptr(msk), _ptr(out["O"]), _ptr(out["lse"]), _ptr(out["d_lr"]),
                                _ptr(out["m"]), _ptr(out["O_s"]), _ptr(out["O_lr"])), "forward")
     return out
 
 
-def backward(cfg: HeadCfg, Q, K, V, Wsort, Wrace, dO, gates=None, q_mask=None, k_mask=None) -> dict:
-    """Backward of one head; returns dQ, dK, dV (and dgates [N,2]) in float64."""
+def backward(cfg: HeadCfg, Q, K, V, Wsort, Wrace, dO, gates=None, q_mask=None, k_mask=None,
+             lam_rows=None) -> dict:
+    """Backward of one head; returns dQ, dK, dV, dgates [N,2] and dlambda [N]
+    (d/dlambda_i) in float64."""
     Q, K, V, Wsort, Wrace, dO = map(_f32, (Q, K, V, Wsort, Wrace, dO))
     g = None if gates is None else _f32(gates)
+    lr = None if lam_rows is None else _f32(lam_rows)
     qm = None if q_mask is None else np.ascontiguousarray(q_mask, dtype=np.uint8)
     km = None if k_mask is None else np.ascontiguousarray(k_mask, dtype=np.uint8)
     N, d = cfg.N, cfg.d
     out = {"dQ": np.zeros((N, d)), "dK": np.zeros((N, d)), "dV": np.zeros((N, d)),
-           "dgates": np.zeros((N, 2))}
+           "dgates": np.zeros((N, 2)), "dlambda": np.zeros(N)}
     c = cfg.c()
     _check(_load().ora_backward(C.byref(c), _ptr(Q), _ptr(K), _ptr(V), _ptr(Wsort), _ptr(Wrace),
-                                _ptr(g), _ptr(dO), _ptr(qm), _ptr(km), _ptr(out["dQ"]), _ptr(out["dK"]),
-                                _ptr(out["dV"]), _ptr(out["dgates"])), "backward")
+                                _ptr(g), _ptr(lr), _ptr(dO), _ptr(qm), _ptr(km), _ptr(out["dQ"]),
+                                _ptr(out["dK"]), _ptr(out["dV"]), _ptr(out["dgates"]),
+                                _ptr(out["dlambda"])), "backward")
     return out
 
 

@@ -35,8 +35,14 @@
  *                       log-sum-exp form of Alg. 6; fused output of
  *                       Eq. (elsaa_fusion_output).
  *   ora_backward        exact gradient of ora_forward with respect to Q, K,
- *                       V (and the gate values) with the selection, W_sort
- *                       and W_race held fixed; the paper gives no backward.
+ *                       V (and the gate values and the per-token lambda_i)
+ *                       with the selection, W_sort and W_race held fixed;
+ *                       the paper gives no backward.
+ * Variants the paper names: r neighbouring sorted blocks on each side of a
+ * query's own block (Sec. 6 cost discussion, "Neighbor blocks" of the
+ * hyper-parameter table; 0 in the main setting), a per-token coefficient
+ * lambda_i (Eq. m_sparse with query-dependent lambda) and the Sort_Lsh_RACE
+ * ablation that fixes m_sparse = 1 (Sec. 7).
  */
 #include <math.h>
 #include <stdint.h>
@@ -52,6 +58,8 @@ typedef struct {
     int32_t n0;         /* causal base length N_0 */
     int32_t causal;
     double beta, lambda, eps, scale;  /* scale <= 0 -> 1/sqrt(d) */
+    int32_t neighbors;  /* r neighbouring sorted blocks on each side (0 = own block only) */
+    int32_t m_one;      /* 1: m_sparse = 1 (the Sort_Lsh_RACE ablation) */
 } ora_cfg;
 
 enum { ORA_OK = 0, ORA_EINVAL = -1, ORA_ENOMEM = -2 };
@@ -65,6 +73,7 @@ static int cfg_ok(const ora_cfg* c)
         return 0;
     if (c->r < (1 << c->race_bits) || c->r % (1 << c->race_bits)) return 0;
     if (!(c->eps > 0) || !(c->lambda >= 0) || !(c->beta > 0)) return 0;
+    if (c->neighbors < 0 || (c->m_one != 0 && c->m_one != 1)) return 0;
     return 1;
 }
 
@@ -215,7 +224,8 @@ static void emit(sup_ctx* x, int32_t qi, int32_t kj)
 /* SortLSH(Qs, Ks; b) on token lists (Alg. 4): sort both lists by
  * (hash key, list position), cut into consecutive blocks of
  * b' = min(b, n) (the last block may be shorter), and let the t-th query
- * block see the t-th key block. */
+ * block see the t-th key block and its r neighbouring key blocks on each
+ * side (r = neighbors, clipped to the list). */
 static void sortlsh_lists(sup_ctx* x, const int32_t* qtok, int nq, const int32_t* ktok, int nk)
 {
     int n = nq > nk ? nq : nk;
@@ -230,10 +240,11 @@ static void sortlsh_lists(sup_ctx* x, const int32_t* qtok, int nq, const int32_t
     sort_positions(nk, keys, ok, tmp);
     {
         const int bq = x->c->k < nq ? x->c->k : nq;
+        const int r = x->c->neighbors;
         for (int p = 0; p < nq; ++p) {
             const int t = p / bq;
-            const int k0 = t * bq;
-            const int k1 = (t + 1) * bq < nk ? (t + 1) * bq : nk;
+            const int k0 = t - r > 0 ? (t - r) * bq : 0;
+            const int k1 = (t + r + 1) * bq < nk ? (t + r + 1) * bq : nk;
             for (int q = k0; q < k1; ++q) emit(x, qtok[oq[p]], ktok[ok[q]]);
         }
     }
@@ -491,9 +502,14 @@ static double gate_of(const float* gates, int i, int which)
 
 /* Full forward for one head into fwd_state (all rows; row_mask limits the
  * sparse sums to the marked rows when not NULL). */
+static double lambda_of(const ora_cfg* c, const float* lam_rows, int i)
+{
+    return lam_rows ? (double)lam_rows[i] : c->lambda;
+}
+
 static int forward_all(const ora_cfg* c, const float* Q, const float* K, const float* V,
-                       const float* Wsort, const float* Wrace, const uint8_t* row_mask,
-                       fwd_state* st, int64_t** rp_out, int32_t** cols_out)
+                       const float* Wsort, const float* Wrace, const float* lam_rows,
+                       const uint8_t* row_mask, fwd_state* st, int64_t** rp_out, int32_t** cols_out)
 {
     const int N = c->N, d = c->d, r = c->r;
     const int L = r >> c->race_bits;
@@ -520,20 +536,22 @@ static int forward_all(const ora_cfg* c, const float* Q, const float* K, const f
         const double den = st->Den[i] + c->eps;
         for (int e = 0; e < d; ++e) st->Olr[(size_t)i * d + e] /= den;
     }
-    /* log D = logsumexp(log d_s, log lambda + log d_lr, log eps); m = d_s / D */
+    /* log D = logsumexp(log d_s, log lambda_i + log d_lr, log eps); m = d_s / D
+     * (m = 1 in the Sort_Lsh_RACE ablation) */
     for (int i = 0; i < N; ++i) {
         if (row_mask && !row_mask[i]) continue;
+        const double lam = lambda_of(c, lam_rows, i);
         double t[3];
         int nt = 0;
         t[nt++] = st->lse[i];
-        if (c->lambda > 0 && st->Den[i] > 0) t[nt++] = log(c->lambda) + log(st->Den[i]);
+        if (lam > 0 && st->Den[i] > 0) t[nt++] = log(lam) + log(st->Den[i]);
         t[nt++] = log(c->eps);
         double mx = t[0];
         for (int a = 1; a < nt; ++a) if (t[a] > mx) mx = t[a];
         double s = 0;
         for (int a = 0; a < nt; ++a) s += exp(t[a] - mx);
         st->logD[i] = mx + log(s);
-        st->m[i] = exp(st->lse[i] - st->logD[i]);
+        st->m[i] = c->m_one ? 1.0 : exp(st->lse[i] - st->logD[i]);
     }
     free(phq); free(phk);
     *rp_out = rp;
@@ -566,10 +584,11 @@ static void free_state(fwd_state* st)
  *   dlr[N]    d_lr = Den
  *   m[N]      denominator-aware multiplier
  *   Os[N][d], Olr[N][d]  branch outputs
+ * lam_rows (optional): per-token lambda_i [N] (NULL: the scalar c->lambda).
  * row_mask (optional): only marked rows of O, lse, m, Os are computed
  * (Olr and dlr are always computed for every row). */
 int ora_forward(const ora_cfg* c, const float* Q, const float* K, const float* V,
-                const float* Wsort, const float* Wrace, const float* gates,
+                const float* Wsort, const float* Wrace, const float* gates, const float* lam_rows,
                 const uint8_t* row_mask, double* O, double* lse, double* dlr, double* m,
                 double* Os, double* Olr)
 {
@@ -579,7 +598,7 @@ int ora_forward(const ora_cfg* c, const float* Q, const float* K, const float* V
     int rc = alloc_state(&st, N, d);
     int64_t* rp = NULL;
     int32_t* cols = NULL;
-    if (rc == ORA_OK) rc = forward_all(c, Q, K, V, Wsort, Wrace, row_mask, &st, &rp, &cols);
+    if (rc == ORA_OK) rc = forward_all(c, Q, K, V, Wsort, Wrace, lam_rows, row_mask, &st, &rp, &cols);
     if (rc == ORA_OK) {
         for (int i = 0; i < N; ++i) {
             const int on = !row_mask || row_mask[i];
@@ -643,21 +662,22 @@ static void feature_vjp(const ora_cfg* c, const float* x, const float* Wrace, co
 }
 
 /* Backward of one head.  dO[N][d] is the upstream gradient of O.
- * Outputs dQ, dK, dV [N][d] (required) and dgates [N][2] (optional:
- * d/dg_sparse, d/dg_lr).  q_mask / k_mask (optional) restrict the sparse
+ * Outputs dQ, dK, dV [N][d] (required), dgates [N][2] (optional:
+ * d/dg_sparse, d/dg_lr) and dlambda [N] (optional: d/dlambda_i; the
+ * gradient of a scalar lambda is their sum).  q_mask / k_mask (optional) restrict the sparse
  * part of dQ (rows) and of dK, dV (keys) to the marked indices; the
  * low-rank part is always computed for every row, so unmarked rows hold
  * only that part. */
 int ora_backward(const ora_cfg* c, const float* Q, const float* K, const float* V,
-                 const float* Wsort, const float* Wrace, const float* gates, const float* dO,
-                 const uint8_t* q_mask, const uint8_t* k_mask,
-                 double* dQ, double* dK, double* dV, double* dgates)
+                 const float* Wsort, const float* Wrace, const float* gates, const float* lam_rows,
+                 const float* dO, const uint8_t* q_mask, const uint8_t* k_mask,
+                 double* dQ, double* dK, double* dV, double* dgates, double* dlambda)
 {
     if (!cfg_ok(c) || !Q || !K || !V || !Wsort || !Wrace || !dO || !dQ || !dK || !dV)
         return ORA_EINVAL;
     const int N = c->N, d = c->d, r = c->r, g = c->race_bits, R = 1 << g;
     const int L = r >> g;
-    const double tau = tau_of(c), eps = c->eps, lam = c->lambda;
+    const double tau = tau_of(c), eps = c->eps;
     fwd_state st;
     int64_t *rp = NULL, *tp = NULL;
     int32_t *cols = NULL, *tcols = NULL;
@@ -665,7 +685,7 @@ int ora_backward(const ora_cfg* c, const float* Q, const float* K, const float* 
     double *phq = NULL, *phk = NULL, *dphq = NULL, *dphk = NULL;
     double *A = NULL, *Bm = NULL;
     int rc = alloc_state(&st, N, d);
-    if (rc == ORA_OK) rc = forward_all(c, Q, K, V, Wsort, Wrace, NULL, &st, &rp, &cols);
+    if (rc == ORA_OK) rc = forward_all(c, Q, K, V, Wsort, Wrace, lam_rows, NULL, &st, &rp, &cols);
     if (rc) goto out;
     memset(dQ, 0, sizeof(double) * (size_t)N * d);
     memset(dK, 0, sizeof(double) * (size_t)N * d);
@@ -681,7 +701,9 @@ int ora_backward(const ora_cfg* c, const float* Q, const float* K, const float* 
      *   dO_s = g_s m u;   dm = g_s <O_s, u>;   dO_lr = g_lr u
      *   Delta = <dO_s, O_s> - dm m (1-m) (d_s+eps)/d_s        (dm/dlog d_s = m(1-m))
      *   dNum = dO_lr / (Den+eps)
-     *   dDen = -<dO_lr, O_lr>/(Den+eps) - dm m lambda / D      (dm/dDen = -m lambda/D) */
+     *   dDen = -<dO_lr, O_lr>/(Den+eps) - dm m lambda / D      (dm/dDen = -m lambda/D)
+     *   dlambda = -dm m Den / D                                 (dm/dlambda = -m Den/D)
+     * With m fixed to 1 (Sort_Lsh_RACE) every dm term vanishes. */
     for (int i = 0; i < N; ++i) {
         const double gs = gate_of(gates, i, 0), gl = gate_of(gates, i, 1);
         const double mi = st.m[i];
@@ -691,7 +713,8 @@ int ora_backward(const ora_cfg* c, const float* Q, const float* K, const float* 
             uos += ue * st.Os[(size_t)i * d + e];
             uol += ue * st.Olr[(size_t)i * d + e];
         }
-        const double dm = gs * uos;
+        const double dm = c->m_one ? 0.0 : gs * uos;
+        const double lam = lambda_of(c, lam_rows, i);
         const double rel = eps * exp(-st.lse[i]);   /* eps / d_s */
         for (int e = 0; e < d; ++e) {
             const double ue = dO[(size_t)i * d + e];
@@ -705,6 +728,7 @@ int ora_backward(const ora_cfg* c, const float* Q, const float* K, const float* 
             dgates[(size_t)i * 2 + 0] = mi * uos;
             dgates[(size_t)i * 2 + 1] = uol;
         }
+        if (dlambda) dlambda[i] = -dm * mi * st.Den[i] / exp(st.logD[i]);
     }
 
     /* Sparse part: for j in S(i), P_ij = e^{z_ij}/(d_s+eps),

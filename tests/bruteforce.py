@@ -59,23 +59,27 @@ def with_margin(rng, shape, W, min_margin=1e-3, scale=1.0):
 PAD = None
 
 
-def _sortlsh_pairs(qs, ks, kq, kk, pad_key, b):
-    """Pairs (query, key) of SortLSH(qs, ks; b): sort by (hash, position), equal blocks."""
+def _sortlsh_pairs(qs, ks, kq, kk, pad_key, b, r=0):
+    """Pairs (query, key) of SortLSH(qs, ks; b): sort by (hash, position), equal
+    blocks; query block t sees key blocks t - r .. t + r (those that exist)."""
     def hk(tok, table):
         return pad_key if tok is PAD else table[tok]
     oq = sorted(range(len(qs)), key=lambda p: (hk(qs[p], kq), p))
     ok = sorted(range(len(ks)), key=lambda p: (hk(ks[p], kk), p))
     bb = min(b, len(qs))
+    key_blocks = [ok[t0:t0 + bb] for t0 in range(0, len(ks), bb)]
     out = []
-    for t0 in range(0, len(qs), bb):
+    for t, t0 in enumerate(range(0, len(qs), bb)):
+        seen = [q for u in range(t - r, t + r + 1) if 0 <= u < len(key_blocks) for q in key_blocks[u]]
         for p in oq[t0:t0 + bb]:
-            for q in ok[t0:t0 + bb]:
+            for q in seen:
                 out.append((qs[p], ks[q]))
     return out
 
 
-def causal_support_mask(N, n0, b, kq, kk, pad_key=0):
-    """N x N boolean support of Alg. 5's CausalSparse (padding tokens dropped)."""
+def causal_support_mask(N, n0, b, kq, kk, pad_key=0, r=0):
+    """N x N boolean support of Alg. 5's CausalSparse (padding tokens dropped);
+    r neighbouring blocks per SortLSH call."""
     M = np.zeros((N, N), dtype=np.int64)
 
     def rec(toks):
@@ -91,7 +95,7 @@ def causal_support_mask(N, n0, b, kq, kk, pad_key=0):
         m = len(toks) // 2
         rec(toks[:m])
         rec(toks[m:])
-        for i, j in _sortlsh_pairs(toks[m:], toks[:m], kq, kk, pad_key, b):
+        for i, j in _sortlsh_pairs(toks[m:], toks[:m], kq, kk, pad_key, b, r):
             if i is not PAD and j is not PAD:
                 M[i, j] += 1
 
@@ -99,9 +103,9 @@ def causal_support_mask(N, n0, b, kq, kk, pad_key=0):
     return M
 
 
-def noncausal_support_mask(N, b, kq, kk):
+def noncausal_support_mask(N, b, kq, kk, r=0):
     M = np.zeros((N, N), dtype=np.int64)
-    for i, j in _sortlsh_pairs(list(range(N)), list(range(N)), kq, kk, 0, b):
+    for i, j in _sortlsh_pairs(list(range(N)), list(range(N)), kq, kk, 0, b, r):
         M[i, j] += 1
     return M
 
@@ -191,8 +195,9 @@ def race_features_sigmoid(X, Wrace, beta):
     return S.prod(axis=-1).reshape(X.shape[0], L << g)
 
 
-def dense_forward_np(Q, K, V, mask, phq, phk, L, causal, eps, lam, tau, gates=None):
-    """Materialised forward from an explicit support mask and explicit features."""
+def dense_forward_np(Q, K, V, mask, phq, phk, L, causal, eps, lam, tau, gates=None, m_one=False):
+    """Materialised forward from an explicit support mask and explicit features
+    (lam: scalar or per-row array; m_one: the m_sparse = 1 ablation)."""
     Q, K, V = (np.asarray(a, np.float64) for a in (Q, K, V))
     N = Q.shape[0]
     Z = tau * Q @ K.T
@@ -204,15 +209,16 @@ def dense_forward_np(Q, K, V, mask, phq, phk, L, causal, eps, lam, tau, gates=No
         M = np.tril(M)
     Den = M.sum(axis=1)
     Olr = (M @ V) / (Den + eps)[:, None]
-    m = ds / (ds + lam * Den + eps)
+    m = np.ones(N) if m_one else ds / (ds + np.asarray(lam, np.float64) * Den + eps)
     gs = np.ones(N) if gates is None else gates[:, 0].astype(np.float64)
     gl = np.ones(N) if gates is None else gates[:, 1].astype(np.float64)
     O = (gs * m)[:, None] * Os + gl[:, None] * Olr
     return dict(O=O, O_s=Os, O_lr=Olr, lse=np.log(ds), d_lr=Den, m=m)
 
 
-def dense_forward_torch(Q, K, V, mask, Wrace, beta, causal, eps, lam, tau, gates=None):
-    """Same materialised forward in PyTorch float64 (features from Wrace), differentiable."""
+def dense_forward_torch(Q, K, V, mask, Wrace, beta, causal, eps, lam, tau, gates=None, m_one=False):
+    """Same materialised forward in PyTorch float64 (features from Wrace),
+    differentiable (lam: a float or a per-row float64 tensor)."""
     L, g, d = Wrace.shape
     Wr = torch.as_tensor(np.asarray(Wrace, np.float64))
     Vs = torch.as_tensor(_vertex_signs(g))
@@ -232,7 +238,7 @@ def dense_forward_torch(Q, K, V, mask, Wrace, beta, causal, eps, lam, tau, gates
         M = torch.tril(M)
     Den = M.sum(dim=1)
     Olr = (M @ V) / (Den + eps)[:, None]
-    m = ds / (ds + lam * Den + eps)
+    m = torch.ones_like(ds) if m_one else ds / (ds + lam * Den + eps)
     N = Q.shape[0]
     if gates is None:
         gs = torch.ones(N, dtype=torch.float64)
