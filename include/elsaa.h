@@ -72,6 +72,9 @@ typedef struct {
     float lambda;           /* fusion coefficient lambda >= 0 (Eq. m_sparse)                 */
     float eps;              /* numerical floor eps > 0                                       */
     float scale;            /* score scale tau; <= 0 selects 1/sqrt(d_h)                     */
+    int32_t neighbors;      /* r >= 0: each sorted query block also sees the r neighbouring  */
+                            /* sorted key blocks on each side (Sec. 6; 0 = the main setting)  */
+    int32_t m_one;          /* 1: m_sparse = 1, the Sort_Lsh_RACE ablation (Sec. 7); 0: ELSAA */
 } elsaa_config;
 
 /* Number of causal recursion levels Lv (0 for non-causal): the smallest Lv
@@ -121,26 +124,31 @@ int elsaa_select(const elsaa_config* cfg, const void* Q, const void* K, const fl
                  int32_t* perm_q, int32_t* perm_k, void* workspace, size_t workspace_bytes,
                  hipStream_t stream);
 
-/* Forward (Alg. 1 / Alg. 6 without the projections).  Writes
+/* Forward (Alg. 1 / Alg. 6 without the projections).  gates is [B,H,N,2]
+ * float32 (g_sparse, g_lr) or NULL (all 1); lambda_rows is the per-token
+ * coefficient lambda_i of Eq. m_sparse, [B,H,N] float32 >= 0, or NULL (the
+ * scalar cfg->lambda for every token).  Writes
  *   O        [B,H,N,d_h] storage dtype, fused output;
  *   lse      [B,H,N] float32, log d_sparse (log of the sparse denominator);
  *   d_lr     [B,H,N] float32, RACE denominator proxy Den;
- *   saved    selection, m, O_s, O_lr and the RACE projections for the backward
- *            (elsaa_saved_layout). */
+ *   saved    selection, m, O_s, O_lr, the RACE projections and states for
+ *            the backward (elsaa_saved_layout). */
 int elsaa_fwd(const elsaa_config* cfg, const void* Q, const void* K, const void* V,
-              const float* W_sort, const float* W_race, const float* gates,
+              const float* W_sort, const float* W_race, const float* gates, const float* lambda_rows,
               void* O, float* lse, float* d_lr, void* saved, size_t saved_bytes,
               void* workspace, size_t workspace_bytes, hipStream_t stream);
 
-/* Backward.  dO is the upstream gradient of O; lse, d_lr and saved are what
- * elsaa_fwd wrote for the same inputs.  Writes dQ, dK, dV [B,H,N,d_h]
- * (storage dtype) and, when dgates is not NULL, dgates [B,H,N,2] float32
- * (d/dg_sparse, d/dg_lr).  W_sort is not read (the selection comes from
- * saved) and may be NULL. */
+/* Backward.  dO is the upstream gradient of O; gates, lambda_rows, lse, d_lr
+ * and saved are what elsaa_fwd was given / wrote for the same inputs.
+ * Writes dQ, dK, dV [B,H,N,d_h] (storage dtype) and, when not NULL,
+ * dgates [B,H,N,2] float32 (d/dg_sparse, d/dg_lr) and dlambda [B,H,N]
+ * float32 (d/dlambda_i; the gradient of a scalar lambda is their sum, that
+ * of lambda = exp(l) is lambda times it; zero when m_one).  W_sort is not
+ * read (the selection comes from saved) and may be NULL. */
 int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void* V,
-              const float* W_sort, const float* W_race, const float* gates, const void* dO,
-              const float* lse, const float* d_lr, const void* saved, size_t saved_bytes,
-              void* dQ, void* dK, void* dV, float* dgates,
+              const float* W_sort, const float* W_race, const float* gates, const float* lambda_rows,
+              const void* dO, const float* lse, const float* d_lr, const void* saved, size_t saved_bytes,
+              void* dQ, void* dK, void* dV, float* dgates, float* dlambda,
               void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Dense projections of the attention block (Alg. 1 and Alg. 6: Q = X W_Q,

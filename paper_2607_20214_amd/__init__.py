@@ -36,7 +36,8 @@ class _Config(C.Structure):
                 ("k", C.c_int32), ("r", C.c_int32), ("race_bits", C.c_int32),
                 ("sort_bits", C.c_int32), ("n0", C.c_int32), ("causal", C.c_int32),
                 ("dtype", C.c_int32), ("beta", C.c_float), ("lam", C.c_float),
-                ("eps", C.c_float), ("scale", C.c_float)]
+                ("eps", C.c_float), ("scale", C.c_float), ("neighbors", C.c_int32),
+                ("m_one", C.c_int32)]
 
 
 class _SavedLayout(C.Structure):
@@ -70,12 +71,14 @@ class Config:
     lam: float = 1.0
     eps: float = 1e-6
     scale: float = 0.0      # <= 0 -> 1/sqrt(d_h)
+    neighbors: int = 0      # neighbouring sorted blocks seen on each side
+    m_one: bool = False     # m_sparse = 1 (the Sort_Lsh_RACE ablation)
 
     def c(self) -> _Config:
         return _Config(self.B, self.H, self.N, self.d_h, self.k, self.r, self.race_bits,
                        self.sort_bits, self.n0, int(self.causal),
                        BF16 if self.dtype == "bf16" else F32, self.beta, self.lam, self.eps,
-                       self.scale)
+                       self.scale, self.neighbors, int(self.m_one))
 
     @property
     def torch_dtype(self):
@@ -95,8 +98,8 @@ def load():
         lib.elsaa_workspace_bytes.argtypes = [P, C.c_int, C.POINTER(C.c_size_t)]
         lib.elsaa_get_saved_layout.argtypes = [P, P]
         lib.elsaa_select.argtypes = [P, P, P, P, P, P, P, S, P]
-        lib.elsaa_fwd.argtypes = [P, P, P, P, P, P, P, P, P, P, P, S, P, S, P]
-        lib.elsaa_bwd.argtypes = [P, P, P, P, P, P, P, P, P, P, P, S, P, P, P, P, P, S, P]
+        lib.elsaa_fwd.argtypes = [P, P, P, P, P, P, P, P, P, P, P, P, S, P, S, P]
+        lib.elsaa_bwd.argtypes = [P, P, P, P, P, P, P, P, P, P, P, P, S, P, P, P, P, P, P, S, P]
         lib.elsaa_gemm_workspace_bytes.argtypes = [P, C.POINTER(C.c_size_t)]
         lib.elsaa_gemm.argtypes = [P, P, P, P, P, S, P]
         lib.elsaa_profile_enable.argtypes = [C.c_int]
@@ -200,7 +203,7 @@ def _check_tensor(name, t, shape, dtype, dev):
                          f"got {t.dtype} {tuple(t.shape)} on {t.device}")
 
 
-def _check_inputs(cfg, q, k, v, w_sort, w_race, gates=None, extra=()):
+def _check_inputs(cfg, q, k, v, w_sort, w_race, gates=None, extra=(), lam_rows=None):
     dev = q.device
     shp = (cfg.B, cfg.H, cfg.N, cfg.d_h)
     for name, t in (("q", q), ("k", k), ("v", v)) + tuple(extra):
@@ -212,6 +215,8 @@ def _check_inputs(cfg, q, k, v, w_sort, w_race, gates=None, extra=()):
                       torch.float32, dev)
     if gates is not None:
         _check_tensor("gates", gates, (cfg.B, cfg.H, cfg.N, 2), torch.float32, dev)
+    if lam_rows is not None:
+        _check_tensor("lam_rows", lam_rows, (cfg.B, cfg.H, cfg.N), torch.float32, dev)
     return dev
 
 
@@ -248,32 +253,36 @@ def select(cfg: Config, q, k, w_sort, workspace: Optional[torch.Tensor] = None):
     return pq, pk
 
 
-def fwd(cfg: Config, q, k, v, w_sort, w_race, gates=None, buffers: Optional[Buffers] = None):
-    """Forward; returns (o, lse, d_lr, saved)."""
-    dev = _check_inputs(cfg, q, k, v, w_sort, w_race, gates)
+def fwd(cfg: Config, q, k, v, w_sort, w_race, gates=None, buffers: Optional[Buffers] = None,
+        lam_rows=None):
+    """Forward; returns (o, lse, d_lr, saved).  lam_rows: per-token lambda_i
+    [B, H, N] float32 (None: the scalar cfg.lam)."""
+    dev = _check_inputs(cfg, q, k, v, w_sort, w_race, gates, lam_rows=lam_rows)
     bufs = buffers or Buffers(cfg, dev, backward=False)
     c = cfg.c()
     _check(load().elsaa_fwd(C.byref(c), _p(q), _p(k), _p(v), _p(w_sort), _p(w_race), _p(gates),
-                            _p(bufs.o), _p(bufs.lse), _p(bufs.d_lr), _p(bufs.saved),
+                            _p(lam_rows), _p(bufs.o), _p(bufs.lse), _p(bufs.d_lr), _p(bufs.saved),
                             bufs.saved.numel(), _p(bufs.workspace), bufs.workspace.numel(),
                             _stream(dev)))
     return bufs.o, bufs.lse, bufs.d_lr, bufs.saved
 
 
 def bwd(cfg: Config, q, k, v, w_race, do, lse, d_lr, saved, gates=None, want_dgates=False,
-        buffers: Optional[Buffers] = None):
-    """Backward; returns (dq, dk, dv) or (dq, dk, dv, dgates)."""
-    dev = _check_inputs(cfg, q, k, v, None, w_race, gates, extra=(("do", do),))
+        buffers: Optional[Buffers] = None, lam_rows=None, want_dlambda=False):
+    """Backward; returns (dq, dk, dv), followed by dgates [B, H, N, 2] when
+    want_dgates and by dlambda [B, H, N] when want_dlambda."""
+    dev = _check_inputs(cfg, q, k, v, None, w_race, gates, extra=(("do", do),), lam_rows=lam_rows)
     bufs = buffers
     if bufs is None:
         bufs = Buffers(cfg, dev, backward=True)
     dg = torch.empty(cfg.B, cfg.H, cfg.N, 2, dtype=torch.float32, device=dev) if want_dgates else None
+    dl = torch.empty(cfg.B, cfg.H, cfg.N, dtype=torch.float32, device=dev) if want_dlambda else None
     c = cfg.c()
-    _check(load().elsaa_bwd(C.byref(c), _p(q), _p(k), _p(v), None, _p(w_race), _p(gates), _p(do),
-                            _p(lse), _p(d_lr), _p(saved), saved.numel(), _p(bufs.dq), _p(bufs.dk),
-                            _p(bufs.dv), _p(dg), _p(bufs.workspace), bufs.workspace.numel(),
-                            _stream(dev)))
-    return (bufs.dq, bufs.dk, bufs.dv) + ((dg,) if want_dgates else ())
+    _check(load().elsaa_bwd(C.byref(c), _p(q), _p(k), _p(v), None, _p(w_race), _p(gates),
+                            _p(lam_rows), _p(do), _p(lse), _p(d_lr), _p(saved), saved.numel(),
+                            _p(bufs.dq), _p(bufs.dk), _p(bufs.dv), _p(dg), _p(dl),
+                            _p(bufs.workspace), bufs.workspace.numel(), _stream(dev)))
+    return (bufs.dq, bufs.dk, bufs.dv) + ((dg,) if want_dgates else ()) + ((dl,) if want_dlambda else ())
 
 
 # ---------------------------------------------------------------------------

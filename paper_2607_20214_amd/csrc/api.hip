@@ -81,6 +81,8 @@ int validate(const elsaa_config* c, Shape* s)
     if (!(c->lambda >= 0) || !std::isfinite(c->lambda)) return fail(ELSAA_ERR_INVALID_ARG, "lambda must be finite and >= 0");
     if (!(c->eps > 0) || !std::isfinite(c->eps)) return fail(ELSAA_ERR_INVALID_ARG, "eps must be finite and > 0");
     if (!std::isfinite(c->scale)) return fail(ELSAA_ERR_INVALID_ARG, "scale must be finite");
+    if (c->neighbors < 0) return fail(ELSAA_ERR_INVALID_ARG, "neighbors must be >= 0 (got %d)", c->neighbors);
+    if (c->m_one != 0 && c->m_one != 1) return fail(ELSAA_ERR_INVALID_ARG, "m_one must be 0 or 1");
     // GPU path limits
     if (c->d_h != 64 && c->d_h != 128) return fail(ELSAA_ERR_UNSUPPORTED, "d_h must be 64 or 128 (got %d)", c->d_h);
     if (c->race_bits != 4) return fail(ELSAA_ERR_UNSUPPORTED, "the GPU path implements race_bits = 4 only (got %d)", c->race_bits);
@@ -108,6 +110,8 @@ int validate(const elsaa_config* c, Shape* s)
     s->causal = c->causal; s->bf16 = bf16;
     s->beta = c->beta; s->lambda = c->lambda; s->eps = c->eps;
     s->tau = c->scale > 0 ? c->scale : 1.0f / std::sqrt((float)c->d_h);
+    s->neighbors = c->neighbors;
+    s->m_one = c->m_one;
     // RACE segments: enough workgroups to fill the chip, whole 64-token chunks
     const int64_t chunks = (c->N + 63) / 64;
     const int64_t bh = (int64_t)c->B * c->H;
@@ -269,7 +273,7 @@ int elsaa_select(const elsaa_config* cfg, const void* Q, const void* K, const fl
 }
 
 int elsaa_fwd(const elsaa_config* cfg, const void* Q, const void* K, const void* V,
-              const float* W_sort, const float* W_race, const float* gates,
+              const float* W_sort, const float* W_race, const float* gates, const float* lambda_rows,
               void* O, float* lse, float* d_lr, void* saved, size_t saved_bytes,
               void* workspace, size_t workspace_bytes, hipStream_t stream)
 {
@@ -302,16 +306,16 @@ int elsaa_fwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     if ((e = launch_sort(s, kq, kk, pq, pk, stream)) != hipSuccess) return hip_fail(e, "sort");
     if ((e = launch_race_fwd(s, uq, uk, V, at<float>(saved, SL.race_states), o_lr, d_lr, stream)) != hipSuccess)
         return hip_fail(e, "race forward");
-    if ((e = launch_sparse_fwd(s, Q, K, V, pq, pk, gates, o_lr, d_lr, at<float>(workspace, W.part_o),
+    if ((e = launch_sparse_fwd(s, Q, K, V, pq, pk, gates, lambda_rows, o_lr, d_lr, at<float>(workspace, W.part_o),
                                at<float>(workspace, W.part_lse), O, lse, m, o_s, stream)) != hipSuccess)
         return hip_fail(e, "sparse forward");
     return ELSAA_OK;
 }
 
 int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void* V,
-              const float* W_sort, const float* W_race, const float* gates, const void* dO,
-              const float* lse, const float* d_lr, const void* saved, size_t saved_bytes,
-              void* dQ, void* dK, void* dV, float* dgates,
+              const float* W_sort, const float* W_race, const float* gates, const float* lambda_rows,
+              const void* dO, const float* lse, const float* d_lr, const void* saved, size_t saved_bytes,
+              void* dQ, void* dK, void* dV, float* dgates, float* dlambda,
               void* workspace, size_t workspace_bytes, hipStream_t stream)
 {
     Shape s;
@@ -342,7 +346,8 @@ int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     float* dk_lr = at<float>(workspace, W.dk_lr);
     float* dv_lr = at<float>(workspace, W.dv_lr);
     hipError_t e;
-    if ((e = launch_bwd_rows(s, dO, o_s, o_lr, m, lse, d_lr, gates, rs, dgates, stream)) != hipSuccess)
+    if ((e = launch_bwd_rows(s, dO, o_s, o_lr, m, lse, d_lr, gates, lambda_rows, rs, dgates, dlambda, stream)) !=
+        hipSuccess)
         return hip_fail(e, "backward row scalars");
     if ((e = launch_race_bwd(s, uq, uk, V, dO, W_race, rs, at<float>(sv, SL.race_states),
                              at<float>(workspace, W.states_b), at<char>(workspace, W.wt_hi),

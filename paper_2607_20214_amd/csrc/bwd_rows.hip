@@ -7,7 +7,8 @@
 //   Delta = sc_s <u, O_s> - dm m (1 - m)(d_s + eps) / d_s
 //   sc_lr = g_lr / (Den + eps)                (dNum = sc_lr u)
 //   dDen  = -g_lr <u, O_lr> / (Den + eps) - dm m lambda / D
-//   dg_s  = m <O_s, u>,  dg_lr = <O_lr, u>
+//   dg_s  = m <O_s, u>,  dg_lr = <O_lr, u>,  dlambda = -dm m Den / D
+// (lambda per token when given; with m fixed to 1 every dm term is zero).
 // Stored as rs[f][BHN] with f = 0: log2(d_s + eps), 1: Delta, 2: sc_s,
 // 3: sc_lr, 4: dDen.  16 lanes per row; O_s and O_lr are float32.
 #include "common.hpp"
@@ -25,8 +26,10 @@ __global__ __launch_bounds__(256) void bwd_rows_kernel(const typename T::store_t
                                                        const float* __restrict__ lse,
                                                        const float* __restrict__ dlr,
                                                        const float* __restrict__ gates,
+                                                       const float* __restrict__ lam_rows,
                                                        float* __restrict__ rs, float* __restrict__ dg,
-                                                       size_t BHN, float lambda, float eps)
+                                                       float* __restrict__ dlam, size_t BHN, float lambda,
+                                                       float eps, int m_one)
 {
     constexpr int PL = D / 16;   // elements per lane
     const size_t row = (size_t)blockIdx.x * 16 + threadIdx.x / 16;
@@ -47,12 +50,13 @@ __global__ __launch_bounds__(256) void bwd_rows_kernel(const typename T::store_t
     const float gl = gates ? gates[row * 2 + 1] : 1.f;
     const float mi = m[row], ls = lse[row], den = dlr[row];
     const float rel = eps * __expf(fminf(-ls, 80.f));   // eps / d_s
-    const float dm = gs * uos;
+    const float dm = m_one ? 0.f : gs * uos;
+    const float lam = lam_rows ? lam_rows[row] : lambda;
     const float scs = gs * mi;
     const float delta = scs * uos - dm * mi * (1.f - mi) * (1.f + rel);
     const float inv_den = 1.f / (den + eps);
-    const float Dtot = __expf(fminf(ls, 80.f)) + lambda * den + eps;
-    const float dden = -gl * uol * inv_den - dm * mi * lambda / Dtot;
+    const float Dtot = __expf(fminf(ls, 80.f)) + lam * den + eps;
+    const float dden = -gl * uol * inv_den - dm * mi * lam / Dtot;
     rs[row] = (ls + log1pf(rel)) * kLog2e;
     rs[BHN + row] = delta;
     rs[2 * BHN + row] = scs;
@@ -62,20 +66,22 @@ __global__ __launch_bounds__(256) void bwd_rows_kernel(const typename T::store_t
         dg[row * 2] = mi * uos;
         dg[row * 2 + 1] = uol;
     }
+    if (dlam) dlam[row] = -dm * mi * den / Dtot;
 }
 
 }  // namespace
 
 hipError_t launch_bwd_rows(const Shape& s, const void* dO, const float* Os, const float* Olr,
                            const float* m, const float* lse, const float* dlr, const float* gates,
-                           float* rs, float* dgates, hipStream_t st)
+                           const float* lambda_rows, float* rs, float* dgates, float* dlambda,
+                           hipStream_t st)
 {
     const size_t BHN = (size_t)s.B * s.H * s.N;
     dim3 grid((unsigned)((BHN + 15) / 16));
 #define ELSAA_ROWS(T_, D_)                                                                       \
     ELSAA_LAUNCH("bwd_rows", (bwd_rows_kernel<T_, D_>), grid, dim3(256), 0, st,                          \
                        (const T_::store_t*)dO, Os, Olr, m, \
-                       lse, dlr, gates, rs, dgates, BHN, s.lambda, s.eps)
+                       lse, dlr, gates, lambda_rows, rs, dgates, dlambda, BHN, s.lambda, s.eps, s.m_one)
     if (s.bf16) {
         if (s.D == 64) ELSAA_ROWS(BF16, 64);
         else ELSAA_ROWS(BF16, 128);

@@ -19,6 +19,8 @@ struct Shape {
     int bf16;             // storage dtype: 1 bf16, 0 float32
     float beta, lambda, eps, tau;
     int seg_len, nseg;    // RACE sequence segments (multiple of the 64-token chunk)
+    int neighbors;        // r neighbouring sorted blocks on each side
+    int m_one;            // m_sparse fixed to 1
     int64_t P() const { return causal ? (int64_t)Lv * (N / 2) : (int64_t)N; }  // perm length per (b,h)
 };
 
@@ -76,13 +78,15 @@ hipError_t launch_race_bwd(const Shape& s, const float* Uq, const float* Uk, con
 // sortLSH sparse branch forward + fusion epilogue
 hipError_t launch_sparse_fwd(const Shape& s, const void* Q, const void* K, const void* V,
                              const int32_t* perm_q, const int32_t* perm_k, const float* gates,
+                             const float* lambda_rows,
                              const float* O_lr, const float* d_lr, float* part_o, float* part_lse,
                              void* O, float* lse, float* m, float* O_s, hipStream_t st);
 
 // backward: per-row scalars rs[5][BHN] (log2(d_s+eps), Delta, sc_s, sc_lr, dDen)
 hipError_t launch_bwd_rows(const Shape& s, const void* dO, const float* Os, const float* Olr,
                            const float* m, const float* lse, const float* dlr, const float* gates,
-                           float* rs, float* dgates, hipStream_t st);
+                           const float* lambda_rows, float* rs, float* dgates, float* dlambda,
+                           hipStream_t st);
 // sparse backward; adds the float32 low-rank parts and writes dQ, dK, dV
 hipError_t launch_sparse_bwd(const Shape& s, const void* Q, const void* K, const void* V,
                              const void* dO, const int32_t* perm_q, const int32_t* perm_k,

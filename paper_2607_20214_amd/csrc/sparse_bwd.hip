@@ -48,6 +48,7 @@ struct BArgs {
     void* dK;
     void* dV;
     int H, N, k, Lv, n_leaf;
+    int nbr;                  // neighbouring sorted blocks on each side
     size_t BHN;
     float tau, tau2;
 };
@@ -96,8 +97,8 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
         qpos = p0 + 16 * w + qq;
         qtok = qpos < N ? a.perm_q[bh * N + qpos] : -1;
         const int plast = min(p0 + kT, N) - 1;
-        kbeg = (p0 / bq) * bq;
-        kend = min(N, (plast / bq + 1) * bq);
+        kbeg = max(0, (p0 / bq - a.nbr) * bq);
+        kend = min(N, (plast / bq + 1 + a.nbr) * bq);
         klist = a.perm_k + bh * N;
     } else if (MODE == kLevels) {
         const int per_level = (N / 2) / kT;
@@ -110,8 +111,8 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
         qpos = p0 + 16 * w + qq;
         const size_t lbase = (bh * a.Lv + level) * (size_t)(N / 2) + (size_t)seg * half;
         qtok = a.perm_q[lbase + qpos];
-        kbeg = (p0 / bq) * bq;
-        kend = min(half, ((p0 + kT - 1) / bq + 1) * bq);
+        kbeg = max(0, (p0 / bq - a.nbr) * bq);
+        kend = min(half, ((p0 + kT - 1) / bq + 1 + a.nbr) * bq);
         klist = a.perm_k + lbase;
     } else {
         const int q0 = tile * kT;
@@ -120,8 +121,8 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
         kbeg = (q0 / a.n_leaf) * a.n_leaf;
         kend = q0 + kT;
     }
-    const int blk_lo = (MODE == kLeaf) ? 0 : (qpos / bq) * bq;
-    const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), blk_lo + bq);
+    const int blk_lo = (MODE == kLeaf) ? 0 : max(0, (qpos / bq - a.nbr) * bq);
+    const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), (qpos / bq + 1 + a.nbr) * bq);
 
     // key rows of the tile at k0 that this thread stages (-1 = none)
     auto tokens = [&](int k0, int (&tok)[PT]) {
@@ -270,8 +271,8 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
         klist = a.perm_k + bh * N;
         ktok = kpos < N ? klist[kpos] : -1;
         const int plast = min(p0 + kT, N) - 1;
-        qbeg = (p0 / bq) * bq;
-        qend = min(N, (plast / bq + 1) * bq);
+        qbeg = max(0, (p0 / bq - a.nbr) * bq);
+        qend = min(N, (plast / bq + 1 + a.nbr) * bq);
         qlist = a.perm_q + bh * N;
         j0 = p0;
     } else if (MODE == kLevels) {
@@ -286,8 +287,8 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
         const size_t lbase = (bh * a.Lv + level) * (size_t)(N / 2) + (size_t)seg * half;
         klist = a.perm_k + lbase;
         ktok = klist[kpos];
-        qbeg = (p0 / bq) * bq;
-        qend = min(half, ((p0 + kT - 1) / bq + 1) * bq);
+        qbeg = max(0, (p0 / bq - a.nbr) * bq);
+        qend = min(half, ((p0 + kT - 1) / bq + 1 + a.nbr) * bq);
         qlist = a.perm_q + lbase;
         j0 = p0;
     } else {
@@ -297,8 +298,8 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
         qbeg = j0;
         qend = (j0 / a.n_leaf + 1) * a.n_leaf;
     }
-    const int blk_lo = (MODE == kLeaf) ? 0 : (kpos / bq) * bq;
-    const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), blk_lo + bq);
+    const int blk_lo = (MODE == kLeaf) ? 0 : max(0, (kpos / bq - a.nbr) * bq);
+    const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), (kpos / bq + 1 + a.nbr) * bq);
 
     // query rows of the tile at q0 that this thread stages, and the scalars
     // of query q0 + threadIdx.x (threads < 64)
@@ -707,7 +708,7 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st)
     hipError_t e;
     // whole-block kernel: b in {64, 128}, blocks never straddle a segment
     const int bq = s.k;
-    const bool whole = (bq == 64 || bq == 128) && (s.causal ? (s.n_leaf % bq == 0) : true);
+    const bool whole = (bq == 64 || bq == 128) && s.neighbors == 0 && (s.causal ? (s.n_leaf % bq == 0) : true);
     if (whole && !s.causal) {
         dim3 grid((s.N + bq - 1) / bq, s.H, s.B);
         if (bq == 64) ELSAA_LAUNCH("sparse_bwd_blocks", (sparse_bwd_block_kernel<T, D, 64, kBlocks>), grid, dim3(256), 0, st, a);
@@ -755,6 +756,7 @@ hipError_t launch_sparse_bwd(const Shape& s, const void* Q, const void* K, const
     a.part_dq = part_dq; a.part_dk = part_dk; a.part_dv = part_dv;
     a.dQ = dQ; a.dK = dK; a.dV = dV;
     a.H = s.H; a.N = s.N; a.k = s.k; a.Lv = s.Lv; a.n_leaf = s.n_leaf;
+    a.nbr = s.neighbors;
     a.BHN = (size_t)s.B * s.H * s.N;
     a.tau = s.tau; a.tau2 = s.tau * kLog2e;
     if (s.bf16) return s.D == 64 ? launch_t<BF16, 64>(s, a, st) : launch_t<BF16, 128>(s, a, st);

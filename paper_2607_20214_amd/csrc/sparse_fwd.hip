@@ -44,6 +44,7 @@ struct Args {
     const int32_t* perm_q;
     const int32_t* perm_k;
     const float* gates;
+    const float* lam_rows;    // per-token lambda_i or null (scalar lambda)
     const float* O_lr;
     const float* d_lr;
     float* part_o;            // [BH][Lv][N/2][D] normalised level outputs (float32: O_s feeds
@@ -53,6 +54,8 @@ struct Args {
     float* m;
     float* O_s;
     int H, N, k, Lv, n_leaf;
+    int nbr;         // neighbouring sorted blocks on each side
+    int m_one;       // m_sparse fixed to 1
     float tau2;      // tau * log2(e)
     float lambda, eps;
 };
@@ -86,14 +89,15 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
     int bq = 1;                         // block size b' (kBlocks / kLevels)
     const int32_t* klist = nullptr;     // sorted key list (kBlocks / kLevels)
     const int tile = blockIdx.x;
+    // sorted query block t sees the sorted key blocks t - nbr .. t + nbr
     if (MODE == kBlocks) {
         bq = min(a.k, N);
         const int p0 = tile * kQT;
         qpos = p0 + 16 * w + qq;
         qtok = qpos < N ? a.perm_q[bh * N + qpos] : -1;
         const int plast = min(p0 + kQT, N) - 1;
-        kbeg = (p0 / bq) * bq;
-        kend = min(N, (plast / bq + 1) * bq);
+        kbeg = max(0, (p0 / bq - a.nbr) * bq);
+        kend = min(N, (plast / bq + 1 + a.nbr) * bq);
         klist = a.perm_k + bh * N;
     } else if (MODE == kLevels) {
         const int per_level = (N / 2) / kQT;
@@ -107,8 +111,8 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
         const size_t lbase = (bh * a.Lv + level) * (size_t)(N / 2) + (size_t)seg * half;
         qtok = a.perm_q[lbase + qpos];
         const int plast = p0 + kQT - 1;
-        kbeg = (p0 / bq) * bq;
-        kend = min(half, (plast / bq + 1) * bq);
+        kbeg = max(0, (p0 / bq - a.nbr) * bq);
+        kend = min(half, (plast / bq + 1 + a.nbr) * bq);
         klist = a.perm_k + lbase;
     } else {
         const int q0 = tile * kQT;
@@ -117,8 +121,8 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
         kbeg = (q0 / a.n_leaf) * a.n_leaf;
         kend = q0 + kQT;
     }
-    const int blk_lo = (MODE == kLeaf) ? 0 : (qpos / bq) * bq;
-    const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), blk_lo + bq);
+    const int blk_lo = (MODE == kLeaf) ? 0 : max(0, (qpos / bq - a.nbr) * bq);
+    const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), (qpos / bq + 1 + a.nbr) * bq);
 
     // ---- this lane's query fragments (B operand of S^T = K Q^T) ---------
     F qf[KS];
@@ -265,7 +269,8 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
     const float lse_nat = (m_run + __log2f(l_run)) * kLn2;       // log d_s
     const float inv_den = 1.f / (l_run + a.eps * fast_exp2(-m_run)); // 1 / (d_s + eps), rescaled
     const float dl = a.d_lr[row];
-    const float mf = 1.f / (1.f + __expf(__logf(a.lambda * dl + a.eps) - lse_nat));
+    const float lam = a.lam_rows ? a.lam_rows[row] : a.lambda;
+    const float mf = a.m_one ? 1.f : 1.f / (1.f + __expf(__logf(lam * dl + a.eps) - lse_nat));
     float gs = 1.f, gl = 1.f;
     if (a.gates) {
         gs = a.gates[row * 2 + 0];
@@ -312,13 +317,14 @@ hipError_t launch_t(const Shape& s, const Args& a, hipStream_t st)
 
 hipError_t launch_sparse_fwd(const Shape& s, const void* Q, const void* K, const void* V,
                              const int32_t* perm_q, const int32_t* perm_k, const float* gates,
-                             const float* O_lr, const float* d_lr, float* part_o, float* part_lse,
+                             const float* lambda_rows, const float* O_lr, const float* d_lr, float* part_o, float* part_lse,
                              void* O, float* lse, float* m, float* O_s, hipStream_t st)
 {
     Args a;
     a.Q = Q; a.K = K; a.V = V;
     a.perm_q = perm_q; a.perm_k = perm_k;
-    a.gates = gates; a.O_lr = O_lr; a.d_lr = d_lr;
+    a.gates = gates; a.lam_rows = lambda_rows; a.O_lr = O_lr; a.d_lr = d_lr;
+    a.nbr = s.neighbors; a.m_one = s.m_one;
     a.part_o = part_o; a.part_lse = part_lse;
     a.O = O; a.lse = lse; a.m = m; a.O_s = O_s;
     a.H = s.H; a.N = s.N; a.k = s.k; a.Lv = s.Lv; a.n_leaf = s.n_leaf;

@@ -36,7 +36,7 @@ import numpy as np
 _T_Q, _T_K, _T_V, _T_DO = 1, 2, 3, 4
 _T_CENTRES, _T_ASSIGN, _T_KNOISE, _T_PICK, _T_QNOISE = 10, 11, 12, 13, 14
 _T_X, _T_WQ, _T_WK, _T_WV, _T_WO, _T_DY = 20, 21, 22, 23, 24, 25
-_T_WSORT, _T_WRACE, _T_GATES = 100, 101, 102
+_T_WSORT, _T_WRACE, _T_GATES, _T_LAMBDA = 100, 101, 102, 103
 
 
 def bf16_round(x: np.ndarray) -> np.ndarray:
@@ -140,6 +140,12 @@ def make_gates(w: Workload) -> np.ndarray:
     """Token-wise gate values (g_sparse, g_lr) in (0.05, 0.95), shape [B,H,N,2]."""
     g = _rng(w.seed, _T_GATES).uniform(0.05, 0.95, size=(w.B, w.H, w.N, 2))
     return g.astype(np.float32)
+
+
+def make_lambda_rows(w: Workload, lo: float = 0.05, hi: float = 3.0) -> np.ndarray:
+    """Token-wise fusion coefficients lambda_i in (lo, hi), shape [B,H,N]."""
+    lam = _rng(w.seed, _T_LAMBDA).uniform(lo, hi, size=(w.B, w.H, w.N))
+    return lam.astype(np.float32)
 
 
 def make_block_inputs(w: Workload) -> dict:

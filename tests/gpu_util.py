@@ -34,26 +34,27 @@ def head_cfg_of(cfg: E.Config) -> oracle.HeadCfg:
     return oracle.HeadCfg(N=cfg.N, d=cfg.d_h, k=cfg.k, r=cfg.r, causal=cfg.causal,
                           race_bits=cfg.race_bits, sort_bits=cfg.sort_bits,
                           n0=cfg.n0 if cfg.n0 > 0 else None, beta=cfg.beta, lam=cfg.lam,
-                          eps=cfg.eps, scale=cfg.scale)
+                          eps=cfg.eps, scale=cfg.scale, neighbors=cfg.neighbors, m_one=cfg.m_one)
 
 
 def to_dev(x: np.ndarray, dtype) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(x)).to("cuda").to(dtype).contiguous()
 
 
-def run_gpu_fwd(cfg: E.Config, inp: dict, gates=None):
+def run_gpu_fwd(cfg: E.Config, inp: dict, gates=None, lam_rows=None):
     dt = cfg.torch_dtype
     q, k, v = (to_dev(inp[n], dt) for n in ("Q", "K", "V"))
     ws = to_dev(inp["W_sort"], torch.float32)
     wr = to_dev(inp["W_race"], torch.float32)
     g = None if gates is None else to_dev(gates, torch.float32)
-    o, lse, dlr, saved = E.fwd(cfg, q, k, v, ws, wr, gates=g)
+    lr = None if lam_rows is None else to_dev(lam_rows, torch.float32)
+    o, lse, dlr, saved = E.fwd(cfg, q, k, v, ws, wr, gates=g, lam_rows=lr)
     torch.cuda.synchronize()
     sv = E.saved_views(cfg, saved)
     out = {"O": o, "lse": lse, "d_lr": dlr, "m": sv["m"], "O_s": sv["o_sparse"],
            "O_lr": sv["o_lowrank"], "perm_q": sv["perm_q"], "perm_k": sv["perm_k"]}
     return {k_: t.float().cpu().numpy() if t.is_floating_point() else t.cpu().numpy()
-            for k_, t in out.items()}, (q, k, v, ws, wr, g, saved, lse, dlr)
+            for k_, t in out.items()}, (q, k, v, ws, wr, g, saved, lse, dlr, lr)
 
 
 def rel_err(a, b) -> float:
@@ -75,11 +76,14 @@ def compare_heads(name, got, want, tol, heads=None):
     return worst
 
 
-def run_gpu_fwd_bwd(cfg: E.Config, inp: dict, gates=None, want_dgates=False):
-    """Forward then backward on the GPU; returns numpy dQ, dK, dV (and dgates)."""
-    got, (q, k, v, ws, wr, g, saved, lse, dlr) = run_gpu_fwd(cfg, inp, gates)
+def run_gpu_fwd_bwd(cfg: E.Config, inp: dict, gates=None, want_dgates=False, lam_rows=None,
+                    want_dlambda=False):
+    """Forward then backward on the GPU; returns numpy dQ, dK, dV (and dgates,
+    dlambda when asked for)."""
+    got, (q, k, v, ws, wr, g, saved, lse, dlr, lr) = run_gpu_fwd(cfg, inp, gates, lam_rows)
     do = to_dev(inp["dO"], cfg.torch_dtype)
-    res = E.bwd(cfg, q, k, v, wr, do, lse, dlr, saved, gates=g, want_dgates=want_dgates)
+    res = E.bwd(cfg, q, k, v, wr, do, lse, dlr, saved, gates=g, want_dgates=want_dgates,
+                lam_rows=lr, want_dlambda=want_dlambda)
     torch.cuda.synchronize()
-    names = ("dQ", "dK", "dV", "dgates")[:len(res)]
+    names = ["dQ", "dK", "dV"] + (["dgates"] if want_dgates else []) + (["dlambda"] if want_dlambda else [])
     return got, {n: t.float().cpu().numpy() for n, t in zip(names, res)}

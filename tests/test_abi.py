@@ -69,8 +69,8 @@ def test_null_pointers_are_rejected_before_any_launch():
     cfg = _cfg()
     c = cfg.c()
     lib = E.load()
-    rc = lib.elsaa_fwd(C.byref(c), None, None, None, None, None, None, None, None, None, None, 0,
-                       None, 0, None)
+    rc = lib.elsaa_fwd(C.byref(c), None, None, None, None, None, None, None, None, None, None, None,
+                       0, None, 0, None)
     assert rc == -1
     rc = lib.elsaa_select(C.byref(c), None, None, None, None, None, None, 0, None)
     assert rc == -1
@@ -82,9 +82,19 @@ def test_workspace_too_small_is_rejected():
     c = cfg.c()
     lib = E.load()
     fake = C.c_void_p(1 << 20)   # aligned, never dereferenced: the size check fails first
-    rc = lib.elsaa_fwd(C.byref(c), fake, fake, fake, fake, fake, None, fake, fake, fake, fake, 16,
-                       fake, 1 << 30, None)
+    rc = lib.elsaa_fwd(C.byref(c), fake, fake, fake, fake, fake, None, None, fake, fake, fake, fake,
+                       16, fake, 1 << 30, None)
     assert rc == -3
+
+
+@pytest.mark.parametrize("over", [dict(neighbors=-1), dict(m_one=2)])
+def test_variant_fields_are_validated(over):
+    cfg = _cfg(**over)
+    c = cfg.c()
+    fake = C.c_void_p(1 << 20)
+    rc = E.load().elsaa_fwd(C.byref(c), fake, fake, fake, fake, fake, None, None, fake, fake, fake,
+                            fake, 1 << 40, fake, 1 << 40, None)
+    assert rc == -1
 
 
 def _gdesc(**kw):
