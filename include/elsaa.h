@@ -151,6 +151,61 @@ int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
               void* dQ, void* dK, void* dV, float* dgates, float* dlambda,
               void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Token-wise rules that feed the fusion: the gate network and the
+ * query-dependent lambda.
+ *   gates (Sec. 3.3, Alg. 1; the two-layer SiLU MLP with two independent,
+ *   unnormalised sigmoid outputs of the experimental setup):
+ *       (g_sparse, g_lr)_i = sigmoid(W2 SiLU(W1 q_i + b1) + b2)
+ *   lambda (the query-dependent coefficient of the ELSAA configuration
+ *   appendix, q_i detached from this path):
+ *       lambda_i = max(lambda_min, c + sigmoid(w . q_i + b))
+ * q_i is row i of the head's Q; every head has its own parameters.  The
+ * caller keeps c >= 0 (it is used as given); lambda_min is 1e-6 in the paper.
+ * Layouts (float32, contiguous, W1 and w 16-byte aligned):
+ *   W1 [H, G, d_h], b1 [H, G], W2 [H, 2, G] (row 0 -> g_sparse), b2 [H, 2];
+ *   w [H, d_h], b [H], c [H].
+ * gate_hidden G is 0 (no gate network), 64 or 128 (the paper's text and
+ * vision widths); lambda_rule is 0 or 1; at least one must be on.  Pointers
+ * of a rule that is off are not read. */
+typedef struct {
+    int32_t gate_hidden;
+    const float* W1;
+    const float* b1;
+    const float* W2;
+    const float* b2;
+    int32_t lambda_rule;
+    const float* lam_w;
+    const float* lam_b;
+    const float* lam_c;
+    float lambda_min;
+} elsaa_token_rules;
+
+/* Forward of the rules: writes gates [B,H,N,2] (when gate_hidden > 0) and
+ * lambda_rows [B,H,N] (when lambda_rule), both float32, ready to pass to
+ * elsaa_fwd / elsaa_bwd.  Q is the operator's Q (cfg->dtype storage). */
+int elsaa_token_rules_fwd(const elsaa_config* cfg, const elsaa_token_rules* rules, const void* Q,
+                          float* gates, float* lambda_rows, hipStream_t stream);
+
+/* Bytes of the workspace elsaa_token_rules_bwd needs (per-workgroup partial
+ * sums of the parameter gradients). */
+int elsaa_token_rules_workspace_bytes(const elsaa_config* cfg, const elsaa_token_rules* rules,
+                                      size_t* bytes);
+
+/* Backward of the rules, given dgates and dlambda (what elsaa_bwd wrote):
+ *   dQ      accumulated IN PLACE: dQ += d/dQ of sum(dgates * gates), the
+ *           gate network's contribution (the lambda path is detached);
+ *           NULL skips it;
+ *   dW1, db1, dW2, db2, dlam_w, dlam_b, dlam_c: parameter gradients with the
+ *           shapes of the parameters, summed over B and N (overwritten);
+ *           any may be NULL.
+ * dgates is read when gate_hidden > 0, dlambda when lambda_rule.  The sums
+ * are taken in a fixed order (deterministic). */
+int elsaa_token_rules_bwd(const elsaa_config* cfg, const elsaa_token_rules* rules, const void* Q,
+                          const float* dgates, const float* dlambda, void* dQ,
+                          float* dW1, float* db1, float* dW2, float* db2,
+                          float* dlam_w, float* dlam_b, float* dlam_c,
+                          void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Dense projections of the attention block (Alg. 1 and Alg. 6: Q = X W_Q,
  * K = X W_K, V = X W_V before the operator, O_head W_O after it; the paper
  * keeps these matrices dense, Sec. 1 and the parameter-overhead appendix).

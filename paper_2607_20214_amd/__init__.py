@@ -46,6 +46,12 @@ class _SavedLayout(C.Structure):
                 ("u_k", C.c_size_t), ("race_states", C.c_size_t), ("total", C.c_size_t)]
 
 
+class _TokenRules(C.Structure):
+    _fields_ = [("gate_hidden", C.c_int32), ("W1", C.c_void_p), ("b1", C.c_void_p), ("W2", C.c_void_p),
+                ("b2", C.c_void_p), ("lambda_rule", C.c_int32), ("lam_w", C.c_void_p),
+                ("lam_b", C.c_void_p), ("lam_c", C.c_void_p), ("lambda_min", C.c_float)]
+
+
 class _GemmDesc(C.Structure):
     _fields_ = [("M", C.c_int32), ("N", C.c_int32), ("K", C.c_int32), ("trans_a", C.c_int32),
                 ("trans_b", C.c_int32), ("lda", C.c_int64), ("ldb", C.c_int64), ("ldc", C.c_int64),
@@ -102,6 +108,9 @@ def load():
         lib.elsaa_bwd.argtypes = [P, P, P, P, P, P, P, P, P, P, P, P, S, P, P, P, P, P, P, S, P]
         lib.elsaa_gemm_workspace_bytes.argtypes = [P, C.POINTER(C.c_size_t)]
         lib.elsaa_gemm.argtypes = [P, P, P, P, P, S, P]
+        lib.elsaa_token_rules_fwd.argtypes = [P, P, P, P, P, P]
+        lib.elsaa_token_rules_workspace_bytes.argtypes = [P, P, C.POINTER(C.c_size_t)]
+        lib.elsaa_token_rules_bwd.argtypes = [P, P, P, P, P, P] + [P] * 7 + [P, S, P]
         lib.elsaa_profile_enable.argtypes = [C.c_int]
         lib.elsaa_profile_count.argtypes = []
         lib.elsaa_profile_get.argtypes = [C.c_int, C.c_char_p, S, C.POINTER(C.c_double),
@@ -352,4 +361,90 @@ def gemm(a, b, trans_a=False, trans_b=False, out=None, out_dtype=torch.bfloat16,
         workspace = torch.empty(ws, dtype=torch.uint8, device=a.device)
     _check(load().elsaa_gemm(C.byref(desc), _p(a), _p(b), _p(out), _p(workspace) if ws else None,
                              workspace.numel() if ws else 0, _stream(a.device)))
+    return out
+
+
+# ---------------------------------------------------------------------------
+# token-wise rules: gate network and query-dependent lambda
+# ---------------------------------------------------------------------------
+@dataclasses.dataclass
+class TokenRules:
+    """Parameters of the gate network (W1 [H, G, d_h], b1 [H, G], W2 [H, 2, G],
+    b2 [H, 2]) and of the lambda rule (lam_w [H, d_h], lam_b [H], lam_c [H]),
+    float32 tensors on the device; leave a rule's tensors None to switch it off."""
+    W1: Optional[torch.Tensor] = None
+    b1: Optional[torch.Tensor] = None
+    W2: Optional[torch.Tensor] = None
+    b2: Optional[torch.Tensor] = None
+    lam_w: Optional[torch.Tensor] = None
+    lam_b: Optional[torch.Tensor] = None
+    lam_c: Optional[torch.Tensor] = None
+    lambda_min: float = 1e-6
+
+    @property
+    def gate_hidden(self) -> int:
+        return 0 if self.W1 is None else self.W1.shape[1]
+
+    @property
+    def has_lambda(self) -> bool:
+        return self.lam_w is not None
+
+    def c(self, cfg: Config) -> _TokenRules:
+        H, d = cfg.H, cfg.d_h
+        G = self.gate_hidden
+        dev = None
+        if G:
+            for name, t, shp in (("W1", self.W1, (H, G, d)), ("b1", self.b1, (H, G)),
+                                 ("W2", self.W2, (H, 2, G)), ("b2", self.b2, (H, 2))):
+                _check_tensor(name, t, shp, torch.float32, t.device if dev is None else dev)
+                dev = t.device
+        if self.has_lambda:
+            for name, t, shp in (("lam_w", self.lam_w, (H, d)), ("lam_b", self.lam_b, (H,)),
+                                 ("lam_c", self.lam_c, (H,))):
+                _check_tensor(name, t, shp, torch.float32, t.device if dev is None else dev)
+                dev = t.device
+        return _TokenRules(G, _p(self.W1), _p(self.b1), _p(self.W2), _p(self.b2), int(self.has_lambda),
+                           _p(self.lam_w), _p(self.lam_b), _p(self.lam_c), self.lambda_min)
+
+
+def token_rules_fwd(cfg: Config, rules: TokenRules, q):
+    """(gates [B, H, N, 2] or None, lambda_rows [B, H, N] or None) of the rules."""
+    dev = _check_inputs(cfg, q, q, q, None, None)
+    gates = torch.empty(cfg.B, cfg.H, cfg.N, 2, dtype=torch.float32, device=dev) if rules.gate_hidden else None
+    lam = torch.empty(cfg.B, cfg.H, cfg.N, dtype=torch.float32, device=dev) if rules.has_lambda else None
+    c, r = cfg.c(), rules.c(cfg)
+    _check(load().elsaa_token_rules_fwd(C.byref(c), C.byref(r), _p(q), _p(gates), _p(lam), _stream(dev)))
+    return gates, lam
+
+
+def token_rules_bwd(cfg: Config, rules: TokenRules, q, dgates=None, dlambda=None, dq=None):
+    """Parameter gradients of the rules (dict of tensors shaped like the
+    parameters); when dq is given, the gate network's gradient with respect
+    to q is added to it in place."""
+    dev = _check_inputs(cfg, q, q, q, None, None)
+    G = rules.gate_hidden
+    if G:
+        _check_tensor("dgates", dgates, (cfg.B, cfg.H, cfg.N, 2), torch.float32, dev)
+    if rules.has_lambda:
+        _check_tensor("dlambda", dlambda, (cfg.B, cfg.H, cfg.N), torch.float32, dev)
+    if dq is not None:
+        _check_tensor("dq", dq, (cfg.B, cfg.H, cfg.N, cfg.d_h), cfg.torch_dtype, dev)
+    H, d = cfg.H, cfg.d_h
+    f = lambda *shp: torch.empty(*shp, dtype=torch.float32, device=dev)   # noqa: E731
+    out = {}
+    if G:
+        out.update(dW1=f(H, G, d), db1=f(H, G), dW2=f(H, 2, G), db2=f(H, 2))
+    if rules.has_lambda:
+        out.update(dlam_w=f(H, d), dlam_b=f(H), dlam_c=f(H))
+    c, r = cfg.c(), rules.c(cfg)
+    n = C.c_size_t()
+    lib = load()
+    _check(lib.elsaa_token_rules_workspace_bytes(C.byref(c), C.byref(r), C.byref(n)))
+    ws = torch.empty(max(n.value, 256), dtype=torch.uint8, device=dev)
+    g = out.get
+    _check(lib.elsaa_token_rules_bwd(C.byref(c), C.byref(r), _p(q), _p(dgates if G else None),
+                                     _p(dlambda if rules.has_lambda else None), _p(dq),
+                                     _p(g("dW1")), _p(g("db1")), _p(g("dW2")), _p(g("db2")),
+                                     _p(g("dlam_w")), _p(g("dlam_b")), _p(g("dlam_c")),
+                                     _p(ws), ws.numel(), _stream(dev)))
     return out

@@ -196,6 +196,29 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 template <class P>
 P* at(void* base, size_t off) { return (P*)((char*)base + off); }
 
+int check_rules(const elsaa_token_rules* r, TrParams* p)
+{
+    if (!r) return fail(ELSAA_ERR_INVALID_ARG, "rules is NULL");
+    if (r->gate_hidden != 0 && r->gate_hidden != 64 && r->gate_hidden != 128)
+        return fail(ELSAA_ERR_UNSUPPORTED, "gate_hidden must be 0, 64 or 128 (got %d)", r->gate_hidden);
+    if (r->lambda_rule != 0 && r->lambda_rule != 1) return fail(ELSAA_ERR_INVALID_ARG, "lambda_rule must be 0 or 1");
+    if (r->gate_hidden == 0 && r->lambda_rule == 0) return fail(ELSAA_ERR_INVALID_ARG, "no rule is on");
+    if (r->gate_hidden && (!r->W1 || !r->b1 || !r->W2 || !r->b2))
+        return fail(ELSAA_ERR_INVALID_ARG, "gate network parameters must not be NULL");
+    if (r->lambda_rule && (!r->lam_w || !r->lam_b || !r->lam_c))
+        return fail(ELSAA_ERR_INVALID_ARG, "lambda rule parameters must not be NULL");
+    if ((r->gate_hidden && !aligned16(r->W1)) || (r->lambda_rule && !aligned16(r->lam_w)))
+        return fail(ELSAA_ERR_INVALID_ARG, "W1 and lam_w must be 16-byte aligned");
+    if (r->lambda_rule && (!(r->lambda_min >= 0) || !std::isfinite(r->lambda_min)))
+        return fail(ELSAA_ERR_INVALID_ARG, "lambda_min must be finite and >= 0");
+    p->G = r->gate_hidden;
+    p->lam = r->lambda_rule;
+    p->W1 = r->W1; p->b1 = r->b1; p->W2 = r->W2; p->b2 = r->b2;
+    p->lw = r->lam_w; p->lb = r->lam_b; p->lc = r->lam_c;
+    p->lam_min = r->lambda_min;
+    return ELSAA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -357,6 +380,64 @@ int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
                                at<float>(workspace, W.part_dq), at<float>(workspace, W.part_dk),
                                at<float>(workspace, W.part_dv), dQ, dK, dV, stream)) != hipSuccess)
         return hip_fail(e, "sparse backward");
+    return ELSAA_OK;
+}
+
+int elsaa_token_rules_fwd(const elsaa_config* cfg, const elsaa_token_rules* rules, const void* Q,
+                          float* gates, float* lambda_rows, hipStream_t stream)
+{
+    Shape s;
+    int rc = validate(cfg, &s);
+    if (rc) return rc;
+    TrParams p;
+    if ((rc = check_rules(rules, &p))) return rc;
+    if (!Q) return fail(ELSAA_ERR_INVALID_ARG, "Q is NULL");
+    if (!aligned16(Q)) return fail(ELSAA_ERR_INVALID_ARG, "Q must be 16-byte aligned");
+    if (p.G && !gates) return fail(ELSAA_ERR_INVALID_ARG, "gates is NULL");
+    if (p.lam && !lambda_rows) return fail(ELSAA_ERR_INVALID_ARG, "lambda_rows is NULL");
+    if (p.G && ((uintptr_t)gates & 7)) return fail(ELSAA_ERR_INVALID_ARG, "gates must be 8-byte aligned");
+    hipError_t e = launch_token_rules_fwd(s, p, Q, p.G ? gates : nullptr, p.lam ? lambda_rows : nullptr, stream);
+    if (e != hipSuccess) return hip_fail(e, "token rules forward");
+    return ELSAA_OK;
+}
+
+int elsaa_token_rules_workspace_bytes(const elsaa_config* cfg, const elsaa_token_rules* rules, size_t* bytes)
+{
+    Shape s;
+    int rc = validate(cfg, &s);
+    if (rc) return rc;
+    TrParams p;
+    if ((rc = check_rules(rules, &p))) return rc;
+    if (!bytes) return fail(ELSAA_ERR_INVALID_ARG, "bytes is NULL");
+    *bytes = token_rules_workspace_bytes(s, p.G, p.lam != 0);
+    return ELSAA_OK;
+}
+
+int elsaa_token_rules_bwd(const elsaa_config* cfg, const elsaa_token_rules* rules, const void* Q,
+                          const float* dgates, const float* dlambda, void* dQ,
+                          float* dW1, float* db1, float* dW2, float* db2,
+                          float* dlam_w, float* dlam_b, float* dlam_c,
+                          void* workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    Shape s;
+    int rc = validate(cfg, &s);
+    if (rc) return rc;
+    TrParams p;
+    if ((rc = check_rules(rules, &p))) return rc;
+    if (!Q || !workspace) return fail(ELSAA_ERR_INVALID_ARG, "Q and workspace must not be NULL");
+    if (!aligned16(Q) || !aligned16(workspace) || (dQ && !aligned16(dQ)))
+        return fail(ELSAA_ERR_INVALID_ARG, "Q, dQ and workspace must be 16-byte aligned");
+    if (p.G && !dgates) return fail(ELSAA_ERR_INVALID_ARG, "dgates is NULL");
+    if (p.G && ((uintptr_t)dgates & 7)) return fail(ELSAA_ERR_INVALID_ARG, "dgates must be 8-byte aligned");
+    if (p.lam && !dlambda) return fail(ELSAA_ERR_INVALID_ARG, "dlambda is NULL");
+    if (workspace_bytes < token_rules_workspace_bytes(s, p.G, p.lam != 0))
+        return fail(ELSAA_ERR_WORKSPACE, "workspace too small (elsaa_token_rules_workspace_bytes)");
+    TrGrads g = {dW1, db1, dW2, db2, dlam_w, dlam_b, dlam_c};
+    if (!p.G) g.dW1 = g.db1 = g.dW2 = g.db2 = nullptr;
+    if (!p.lam) g.dlw = g.dlb = g.dlc = nullptr;
+    hipError_t e = launch_token_rules_bwd(s, p, Q, p.G ? dgates : nullptr, p.lam ? dlambda : nullptr,
+                                          p.G ? dQ : nullptr, g, (float*)workspace, stream);
+    if (e != hipSuccess) return hip_fail(e, "token rules backward");
     return ELSAA_OK;
 }
 

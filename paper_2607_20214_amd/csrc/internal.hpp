@@ -94,4 +94,36 @@ hipError_t launch_sparse_bwd(const Shape& s, const void* Q, const void* K, const
                              const float* dv_lr, float* part_dq, float* part_dk, float* part_dv,
                              void* dQ, void* dK, void* dV, hipStream_t st);
 
+// token-wise rules: gate network and query-dependent lambda (token_rules.hip)
+struct TrParams {
+    int G;                              // gate hidden width: 0, 64 or 128
+    int lam;                            // 1: lambda rule on
+    const float *W1, *b1, *W2, *b2;     // [H][G][D], [H][G], [H][2][G], [H][2]
+    const float *lw, *lb, *lc;          // [H][D], [H], [H]
+    float lam_min;
+};
+struct TrGrads {
+    float *dW1, *db1, *dW2, *db2, *dlw, *dlb, *dlc;   // any may be null
+};
+// float offsets of one workgroup's partial sums of the parameter gradients
+struct TrLayout {
+    int G, D, lam;
+    __host__ __device__ constexpr int w1() const { return 0; }
+    __host__ __device__ constexpr int lw() const { return G * D; }
+    __host__ __device__ constexpr int b1() const { return lw() + (lam ? D : 0); }
+    __host__ __device__ constexpr int w2() const { return b1() + G; }
+    __host__ __device__ constexpr int b2() const { return w2() + 2 * G; }
+    __host__ __device__ constexpr int lb() const { return b2() + (G ? 2 : 0); }
+    __host__ __device__ constexpr int lc() const { return lb() + (lam ? 1 : 0); }
+    __host__ __device__ constexpr int total() const { return lc() + (lam ? 1 : 0); }
+    __host__ __device__ constexpr int stride() const { return (total() + 63) & ~63; }
+};
+size_t token_rules_workspace_bytes(const Shape& s, int G, bool lam);
+hipError_t launch_token_rules_fwd(const Shape& s, const TrParams& p, const void* Q, float* gates,
+                                  float* lambda_rows, hipStream_t st);
+// dQ (may be null) is accumulated in place; part: token_rules_workspace_bytes
+hipError_t launch_token_rules_bwd(const Shape& s, const TrParams& p, const void* Q, const float* dgates,
+                                  const float* dlambda, void* dQ, const TrGrads& gr, float* part,
+                                  hipStream_t st);
+
 }  // namespace elsaa

@@ -37,6 +37,7 @@ _T_Q, _T_K, _T_V, _T_DO = 1, 2, 3, 4
 _T_CENTRES, _T_ASSIGN, _T_KNOISE, _T_PICK, _T_QNOISE = 10, 11, 12, 13, 14
 _T_X, _T_WQ, _T_WK, _T_WV, _T_WO, _T_DY = 20, 21, 22, 23, 24, 25
 _T_WSORT, _T_WRACE, _T_GATES, _T_LAMBDA = 100, 101, 102, 103
+_T_RULES, _T_RULE_GRADS = 110, 111
 
 
 def bf16_round(x: np.ndarray) -> np.ndarray:
@@ -146,6 +147,34 @@ def make_lambda_rows(w: Workload, lo: float = 0.05, hi: float = 3.0) -> np.ndarr
     """Token-wise fusion coefficients lambda_i in (lo, hi), shape [B,H,N]."""
     lam = _rng(w.seed, _T_LAMBDA).uniform(lo, hi, size=(w.B, w.H, w.N))
     return lam.astype(np.float32)
+
+
+def make_rule_params(w: Workload, G: int, lam: bool = True) -> dict:
+    """Parameters of the token-wise rules for every head: gate network
+    W1 [H,G,d] ~ N(0, 1/d), b1 [H,G] ~ N(0, 0.1^2), W2 [H,2,G] ~ N(0, 1/G),
+    b2 [H,2] ~ N(0, 0.1^2); lambda rule w [H,d] ~ N(0, 0.05^2), b [H] ~
+    N(0, 0.1^2), c [H] uniform in (0.2, 0.4).  float32."""
+    rng = _rng(w.seed, _T_RULES)
+    H, d = w.H, w.d
+    out = {}
+    if G:
+        out["W1"] = (rng.standard_normal((H, G, d)) / np.sqrt(d)).astype(np.float32)
+        out["b1"] = (rng.standard_normal((H, G)) * 0.1).astype(np.float32)
+        out["W2"] = (rng.standard_normal((H, 2, G)) / np.sqrt(G)).astype(np.float32)
+        out["b2"] = (rng.standard_normal((H, 2)) * 0.1).astype(np.float32)
+    if lam:
+        out["lam_w"] = (rng.standard_normal((H, d)) * 0.05).astype(np.float32)
+        out["lam_b"] = (rng.standard_normal(H) * 0.1).astype(np.float32)
+        out["lam_c"] = rng.uniform(0.2, 0.4, size=H).astype(np.float32)
+    return out
+
+
+def make_rule_grads(w: Workload) -> dict:
+    """Upstream gradients of the rules' outputs: dgates [B,H,N,2] and
+    dlambda [B,H,N], N(0,1) float32."""
+    rng = _rng(w.seed, _T_RULE_GRADS)
+    return {"dgates": rng.standard_normal((w.B, w.H, w.N, 2)).astype(np.float32),
+            "dlambda": rng.standard_normal((w.B, w.H, w.N)).astype(np.float32)}
 
 
 def make_block_inputs(w: Workload) -> dict:

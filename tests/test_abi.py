@@ -133,3 +133,36 @@ def test_gemm_split_workspace_and_checks():
     assert lib.elsaa_gemm(C.byref(d), fake, fake, fake, fake, n - 1, None) == -3
     bad = C.c_void_p((1 << 20) + 8)
     assert lib.elsaa_gemm(C.byref(_gdesc()), bad, fake, fake, None, 0, None) == -1
+
+
+def _rules(**kw):
+    fake = 1 << 20                 # aligned, never dereferenced: validation fails first
+    r = E._TokenRules(64, fake, fake, fake, fake, 1, fake, fake, fake, 1e-6)
+    for k, v in kw.items():
+        setattr(r, k, v)
+    return r
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(gate_hidden=32), -2), (dict(gate_hidden=0, lambda_rule=0), -1), (dict(lambda_rule=2), -1),
+    (dict(W1=None), -1), (dict(lam_c=None), -1), (dict(W1=(1 << 20) + 4), -1),
+    (dict(lambda_min=-1.0), -1), (dict(gate_hidden=0, W1=None, b1=None), 0),
+])
+def test_token_rules_validation(kw, status):
+    lib = E.load()
+    c = _cfg().c()
+    r = _rules(**kw)
+    n = C.c_size_t()
+    rc = lib.elsaa_token_rules_workspace_bytes(C.byref(c), C.byref(r), C.byref(n))
+    assert rc == status
+    if status == 0:
+        assert n.value > 0
+        fake = C.c_void_p(1 << 20)
+        # a too-small workspace is caught before any launch
+        rc = lib.elsaa_token_rules_bwd(C.byref(c), C.byref(r), fake, None, fake, fake, *([None] * 7),
+                                       fake, 16, None)
+        assert rc == -3
+        # the lambda rule's gradient input is required
+        rc = lib.elsaa_token_rules_bwd(C.byref(c), C.byref(r), fake, None, None, fake, *([None] * 7),
+                                       fake, 1 << 40, None)
+        assert rc == -1
