@@ -25,7 +25,7 @@ PEAK_BF16_TFLOPS = 2500.0      # dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3        # fp32 matrix
 
 
-def kernel_model(w, Lv: int) -> dict:
+def kernel_model(w, Lv: int, rules_G: int = 0, rules_lam: bool = False, rules_part_bytes: int = 0) -> dict:
     """Algorithmic bytes and flops per launch of each kernel (name -> (bytes, flops)).
 
     Counts what each kernel must move or compute: every input row it needs is
@@ -75,6 +75,18 @@ def kernel_model(w, Lv: int) -> dict:
     m["sparse_dq_blocks"] = (bh * N * (4 * D * s + D * s + 12), bh * N * min(k, N) * 6 * D)
     m["sparse_dkv_blocks"] = (bh * N * (4 * D * s + 2 * D * s + 12), bh * N * min(k, N) * 8 * D)
     del seg_states, n0
+    if rules_G or rules_lam:
+        # token-wise rules: q read once; gates (8 B) and lambda (4 B) per row;
+        # the backward also reads dgates / dlambda, adds into dQ (read +
+        # write) and writes one partial-sum record per workgroup
+        G = rules_G
+        gx = G + (1 if rules_lam else 0)
+        out_b = (8 if G else 0) + (4 if rules_lam else 0)
+        rec = G * D + (D if rules_lam else 0) + 3 * G + (2 if G else 0) + (2 if rules_lam else 0)
+        m["token_rules_fwd"] = (bh * N * (D * s + out_b), bh * N * (2 * D * gx + 4 * G))
+        m["token_rules_bwd"] = (bh * N * (D * s + out_b + (2 * D * s if G else 0)) + rules_part_bytes,
+                                bh * N * (2 * D * gx * 2 + (2 * D * G) + 8 * G))
+        m["token_rules_reduce"] = (rules_part_bytes + w.H * rec * 4, rules_part_bytes // 4)
     if w.d_model:
         # the six dense products of one block step (bf16 operands; Q/K/V, dO
         # written bf16, Y and the gradients of X and the weights float32)
@@ -103,6 +115,9 @@ KERNEL_SOURCES = {
     "race_dv": ["race_bwd.hip", "race_common.hpp", "common.hpp"],
     "bwd_rows": ["bwd_rows.hip", "common.hpp"],
     "gemm": ["gemm.hip", "common.hpp"], "gemm_reduce": ["gemm.hip"],
+    "token_rules_fwd": ["token_rules.hip", "tile.hpp", "common.hpp"],
+    "token_rules_bwd": ["token_rules.hip", "tile.hpp", "common.hpp"],
+    "token_rules_reduce": ["token_rules.hip"],
 }
 
 
@@ -206,6 +221,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="causal-16k-d128-bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--rules", action="store_true",
+                    help="add the token-wise rules (gate network of hidden width 64 and the "
+                         "query-dependent lambda) around the operator in every step")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of 1 GiB (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -249,6 +267,20 @@ def main():
     def step():
         o, lse, dlr, saved = E.fwd(cfg, q, k, v, ws, wr, buffers=bufs)
         E.bwd(cfg, q, k, v, wr, do, lse, dlr, saved, buffers=bufs)
+
+    rules_G, rules_part = 0, 0
+    if args.rules:
+        rules_G = 64
+        rp = W.make_rule_params(w, rules_G, True)
+        rules = E.TokenRules(**{n: to(a, torch.float32) for n, a in rp.items()})
+        rules_part = E.token_rules_workspace_bytes(cfg, rules)
+
+        def step():
+            gates, lam = E.token_rules_fwd(cfg, rules, q)
+            o, lse, dlr, saved = E.fwd(cfg, q, k, v, ws, wr, gates=gates, buffers=bufs, lam_rows=lam)
+            dq, _, _, dg, dl = E.bwd(cfg, q, k, v, wr, do, lse, dlr, saved, gates=gates, want_dgates=True,
+                                     buffers=bufs, lam_rows=lam, want_dlambda=True)
+            E.token_rules_bwd(cfg, rules, q, dg, dl, dq=dq)
 
     blk = None
     if w.d_model:
@@ -298,21 +330,26 @@ def main():
     dom = max(per_step, key=per_step.get)
     ms_total, launches = prof[dom]
     avg_s = ms_total / launches / 1e3
-    model = kernel_model(w, Lv)
-    nbytes, nflops = model.get(dom, (0, 0))
-    per_launch = launches // args.steps          # launches of that kernel in one step
-    nbytes, nflops = nbytes / per_launch, nflops / per_launch
-    t_hbm = nbytes / (PEAK_HBM_GBS * 1e9)
+    model = kernel_model(w, Lv, rules_G, bool(args.rules), rules_part)
     peak_tf = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
-    t_mma = nflops / (peak_tf * 1e12)
-    if t_hbm >= t_mma:
-        ach = nbytes / avg_s / 1e9
-        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(ach / PEAK_HBM_GBS, 4)}
-    else:
-        ach = nflops / avg_s / 1e12
-        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": peak_tf, "unit": "TFLOP/s",
-                "frac": round(ach / peak_tf, 4)}
+
+    def roofline_of(name):
+        """(roofline dict, bytes, flops per launch) of one kernel from its
+        algorithmic model and its measured average launch time."""
+        tot_ms, n = prof[name]
+        avg = tot_ms / n / 1e3
+        b_, f_ = model.get(name, (0, 0))
+        per = n // args.steps
+        b_, f_ = b_ / per, f_ / per
+        if b_ / (PEAK_HBM_GBS * 1e9) >= f_ / (peak_tf * 1e12):
+            a_ = b_ / avg / 1e9
+            return {"bound": "hbm", "achieved": round(a_, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": round(a_ / PEAK_HBM_GBS, 4)}, b_, f_
+        a_ = f_ / avg / 1e12
+        return {"bound": "mfma", "achieved": round(a_, 2), "peak": peak_tf, "unit": "TFLOP/s",
+                "frac": round(a_ / peak_tf, 4)}, b_, f_
+
+    roof, nbytes, nflops = roofline_of(dom)
     roof["traffic"] = read_traffic(dom, w.name)
     roof["kernel"] = dom
     roof["avg_launch_ms"] = round(avg_s * 1e3, 4)
@@ -339,7 +376,11 @@ def main():
                    "causal": w.causal, "levels": Lv, **({"d_model": w.d_model} if blk else {})},
         "roofline": roof,
         "kernel_ms_per_step": {n: round(t, 4) for n, t in sorted(per_step.items(), key=lambda x: -x[1])},
+        "kernel_roofline_frac": {n: (roofline_of(n)[0]["bound"], roofline_of(n)[0]["frac"])
+                                 for n in sorted(per_step, key=lambda x: -per_step[x]) if n in model},
     }
+    if args.rules:
+        result["config"]["rules"] = {"gate_hidden": rules_G, "lambda_rule": True}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline_block(w, inp, blk) if blk else cpu_baseline(w, inp)
     print(json.dumps(result), flush=True)

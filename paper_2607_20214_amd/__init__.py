@@ -417,7 +417,16 @@ def token_rules_fwd(cfg: Config, rules: TokenRules, q):
     return gates, lam
 
 
-def token_rules_bwd(cfg: Config, rules: TokenRules, q, dgates=None, dlambda=None, dq=None):
+def token_rules_workspace_bytes(cfg: Config, rules: TokenRules) -> int:
+    """Bytes of the backward's partial-sum workspace (one record per workgroup)."""
+    c, r = cfg.c(), rules.c(cfg)
+    n = C.c_size_t()
+    _check(load().elsaa_token_rules_workspace_bytes(C.byref(c), C.byref(r), C.byref(n)))
+    return n.value
+
+
+def token_rules_bwd(cfg: Config, rules: TokenRules, q, dgates=None, dlambda=None, dq=None,
+                    workspace: Optional[torch.Tensor] = None):
     """Parameter gradients of the rules (dict of tensors shaped like the
     parameters); when dq is given, the gate network's gradient with respect
     to q is added to it in place."""
@@ -437,10 +446,10 @@ def token_rules_bwd(cfg: Config, rules: TokenRules, q, dgates=None, dlambda=None
     if rules.has_lambda:
         out.update(dlam_w=f(H, d), dlam_b=f(H), dlam_c=f(H))
     c, r = cfg.c(), rules.c(cfg)
-    n = C.c_size_t()
     lib = load()
-    _check(lib.elsaa_token_rules_workspace_bytes(C.byref(c), C.byref(r), C.byref(n)))
-    ws = torch.empty(max(n.value, 256), dtype=torch.uint8, device=dev)
+    need = token_rules_workspace_bytes(cfg, rules)
+    ws = workspace if workspace is not None and workspace.numel() >= need else \
+        torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
     g = out.get
     _check(lib.elsaa_token_rules_bwd(C.byref(c), C.byref(r), _p(q), _p(dgates if G else None),
                                      _p(dlambda if rules.has_lambda else None), _p(dq),

@@ -29,6 +29,8 @@
 #include "internal.hpp"
 #include "tile.hpp"
 
+#include <type_traits>
+
 namespace elsaa {
 namespace {
 
@@ -59,6 +61,7 @@ struct TokenRules {
     static constexpr int CBW = D / 16 / NW;          // dW1 column blocks per wave
     static constexpr int HALVES = RT / 64;           // 64-row staging passes per tile
     static constexpr bool SPLIT = T::bytes == 2;     // W1 as bf16 hi + lo
+    static constexpr bool DQ_EARLY = G <= 64 && T::bytes == 2;   // dQ rows fetched before the products
     using S = typename T::store_t;
     using F = typename T::frag_t;
     using TQ = tile::Tile<T, D, NT>;                 // rows of D elements (q, W1)
@@ -287,11 +290,26 @@ struct TokenRules {
             store_rows(sm.qt, rg);
             if (row0 + RT < rend) load_rows(X, row0 + RT, N, rg);
             __syncthreads();
+            // the row gradients and the dQ rows this wave adds to, loaded
+            // before the products so that their latency is hidden
+            const size_t rb = (size_t)bh * N + row0 + wr0 + 8 * g;   // row of (s, i): rb + 4s + i
+            const int rleft = rend - (row0 + wr0 + 8 * g);           // rows of the group before rend
+            float2 dgv[2][4];
+            float dlv[2][4];
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const bool ok = 4 * s + i < rleft;
+                    dgv[s][i] = (G > 0 && ok) ? *(const float2*)&a.dg[(rb + 4 * s + i) * 2] : make_float2(0.f, 0.f);
+                    dlv[s][i] = (LAM && ok && rho == 0) ? a.dlam[rb + 4 * s + i] : 0.f;
+                }
+            DqRegs dqv;
+            if constexpr (G > 0 && DQ_EARLY)
+                if (a.dQ) dq_load((const S*)a.dQ + (size_t)bh * N * D, row0, wr0, rend, dqv);
             {
                 f32x4 acc[2][NB];
                 first_layer(sm, wr0, acc);
-                const size_t rb = (size_t)bh * N + row0 + wr0 + 8 * g;   // row of (s, i): rb + 4s + i
-                const int rleft = rend - (row0 + wr0 + 8 * g);           // rows of the group before rend
                 if constexpr (G > 0) {
                     float z2[2][2][4], dz0[2][4], dz1[2][4];
                     second_layer(sm, acc, b20, b21, z2);
@@ -299,8 +317,7 @@ struct TokenRules {
                     for (int s = 0; s < 2; ++s)
 #pragma unroll
                         for (int i = 0; i < 4; ++i) {
-                            const bool ok = 4 * s + i < rleft;
-                            const float2 d = ok ? *(const float2*)&a.dg[(rb + 4 * s + i) * 2] : make_float2(0.f, 0.f);
+                            const float2 d = dgv[s][i];
                             const float g0 = sigm(z2[0][s][i]), g1 = sigm(z2[1][s][i]);
                             dz0[s][i] = d.x * g0 * (1.f - g0);
                             dz1[s][i] = d.y * g1 * (1.f - g1);
@@ -336,8 +353,7 @@ struct TokenRules {
                         for (int i = 0; i < 4; ++i) {
                             tv[s][i] = 0.f;
                             if (rho == 0) {
-                                const bool ok = 4 * s + i < rleft;
-                                const float dl = ok ? a.dlam[rb + 4 * s + i] : 0.f;
+                                const float dl = dlv[s][i];
                                 const float sl = sigm(acc[s][NG][i] + lb);
                                 const float e = (lc + sl >= a.lam_min) ? dl : 0.f;
                                 const float t = e * sl * (1.f - sl);
@@ -368,25 +384,12 @@ struct TokenRules {
             if constexpr (G > 0) {
                 if (a.dQ) {
                     S* dQ = (S*)a.dQ + (size_t)bh * N * D;
+                    if constexpr (DQ_EARLY) {
+#pragma unroll
+                        for (int cbk = 0; cbk < D / 16; ++cbk) dq_block(sb, dQ, cbk, row0, wr0, rend, dqv);
+                    } else {
 #pragma unroll 1
-                    for (int cbk = 0; cbk < D / 16; ++cbk) {
-                        f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
-#pragma unroll
-                        for (int kn = 0; kn < G / 32; ++kn) {
-                            const F ah = TQ::col8(sm.whi, 32 * kn, 16 * cbk);
-                            const F al = SPLIT ? TQ::col8(sm.wlo, 32 * kn, 16 * cbk) : ah;
-#pragma unroll
-                            for (int r = 0; r < 2; ++r) {
-                                const F bz = TZ::col8(sb.zt, 32 * kn, wr0 + 16 * r);
-                                acc[r] = T::mma(ah, bz, acc[r]);
-                                if constexpr (SPLIT) acc[r] = T::mma(al, bz, acc[r]);
-                            }
-                        }
-#pragma unroll
-                        for (int r = 0; r < 2; ++r) {
-                            const int row = row0 + wr0 + 16 * r + rho;
-                            if (row < rend) add4(dQ + (size_t)row * D + 16 * cbk + 4 * g, acc[r]);
-                        }
+                        for (int cbk = 0; cbk < D / 16; ++cbk) dq_block(sb, dQ, cbk, row0, wr0, rend, dqv);
                     }
                 }
             }
@@ -458,19 +461,64 @@ struct TokenRules {
         }
     }
 
-    // p[0..3] += v (storage precision)
-    __device__ static void add4(S* p, f32x4 v)
+    // the wave's dQ values in the q^T accumulator layout: [cbk][r] holds
+    // columns 16 cbk + 4g .. +3 of row row0 + wr0 + 16 r + lane % 16
+    using DqPiece = typename std::conditional<T::bytes == 2, uint2, float4>::type;
+    struct DqRegs {
+        DqPiece v[D / 16][2];
+    };
+    // dq += W1^T dz1 for columns 16 cbk .. +15 of the wave's own rows (q^T
+    // layout: the lane holds 4 consecutive columns of one row)
+    __device__ static void dq_block(const SmemB& sb, S* dQ, int cbk, int row0, int wr0, int rend, const DqRegs& dqv)
+    {
+        const int lane = threadIdx.x & 63, g = lane >> 4, rho = lane & 15;
+        DqPiece old[2];
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            const int row = row0 + wr0 + 16 * r + rho;
+            if constexpr (DQ_EARLY) old[r] = dqv.v[cbk][r];
+            else old[r] = row < rend ? *(const DqPiece*)(dQ + (size_t)row * D + 16 * cbk + 4 * g) : DqPiece{};
+        }
+        f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+        for (int kn = 0; kn < G / 32; ++kn) {
+            const F ah = TQ::col8(sb.m.whi, 32 * kn, 16 * cbk);
+            const F al = SPLIT ? TQ::col8(sb.m.wlo, 32 * kn, 16 * cbk) : ah;
+#pragma unroll
+            for (int r = 0; r < 2; ++r) {
+                const F bz = TZ::col8(sb.zt, 32 * kn, wr0 + 16 * r);
+                acc[r] = T::mma(ah, bz, acc[r]);
+                if constexpr (SPLIT) acc[r] = T::mma(al, bz, acc[r]);
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            const int row = row0 + wr0 + 16 * r + rho;
+            if (row < rend) dq_store(dQ + (size_t)row * D + 16 * cbk + 4 * g, old[r], acc[r]);
+        }
+    }
+
+    __device__ static void dq_load(const S* dQ, int row0, int wr0, int rend, DqRegs& q)
+    {
+        const int lane = threadIdx.x & 63, g = lane >> 4, rho = lane & 15;
+#pragma unroll
+        for (int cbk = 0; cbk < D / 16; ++cbk)
+#pragma unroll
+            for (int r = 0; r < 2; ++r) {
+                const int row = row0 + wr0 + 16 * r + rho;
+                q.v[cbk][r] = row < rend ? *(const DqPiece*)(dQ + (size_t)row * D + 16 * cbk + 4 * g) : DqPiece{};
+            }
+    }
+    // p[0..3] = old + v (storage precision)
+    __device__ static void dq_store(S* p, DqPiece o, f32x4 v)
     {
         if constexpr (T::bytes == 2) {
-            const uint2 o = *(const uint2*)p;
             const float x0 = bf16_to_f32(o.x & 0xffff) + v[0], x1 = bf16_to_f32(o.x >> 16) + v[1];
             const float x2 = bf16_to_f32(o.y & 0xffff) + v[2], x3 = bf16_to_f32(o.y >> 16) + v[3];
             *(uint2*)p = make_uint2(f32_to_bf16(x0) | ((uint32_t)f32_to_bf16(x1) << 16),
                                     f32_to_bf16(x2) | ((uint32_t)f32_to_bf16(x3) << 16));
         } else {
-            float4 o = *(const float4*)p;
-            o.x += v[0]; o.y += v[1]; o.z += v[2]; o.w += v[3];
-            *(float4*)p = o;
+            *(float4*)p = make_float4(o.x + v[0], o.y + v[1], o.z + v[2], o.w + v[3]);
         }
     }
 };
