@@ -6,6 +6,7 @@
 #include <string>
 
 #include "elsaa.h"
+#include "causal.hpp"
 #include "internal.hpp"
 
 using namespace elsaa;
@@ -98,8 +99,7 @@ int validate(const elsaa_config* c, Shape* s)
                         "causal N = %d with n0 = %d needs zero-token padding of an odd segment (not on the GPU path)",
                         c->N, n0);
         n_leaf = c->N >> lv;
-        if (n_leaf % 64)
-            return fail(ELSAA_ERR_UNSUPPORTED, "causal leaf length N / 2^Lv = %d must be a multiple of 64", n_leaf);
+        if (lv > kMaxLevels) return fail(ELSAA_ERR_UNSUPPORTED, "more than %d causal levels", kMaxLevels);
     }
     s->B = c->B; s->H = c->H; s->N = c->N; s->D = c->d_h;
     s->k = c->k;

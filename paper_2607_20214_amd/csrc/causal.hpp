@@ -1,0 +1,61 @@
+// causal.hpp -- workgroup numbering over the causal recursion (Alg. 5
+// unrolled): level l has 2^l segments whose future halves hold
+// half_l = N >> (l + 1) sorted queries (and whose past halves hold as many
+// sorted keys); the leaves are the N / n_leaf runs of n_leaf tokens.
+// Segment and leaf lengths need not be multiples of the 64-row tile: each
+// segment (leaf) gets ceil(length / 64) tiles, the last one ragged, so a
+// tile never straddles two segments (leaves).
+#pragma once
+#include <hip/hip_runtime.h>
+
+namespace elsaa {
+
+constexpr int kMaxLevels = 26;
+constexpr int kRowTile = 64;
+
+struct LevelTiles {
+    int first[kMaxLevels + 1];   // first tile of level l; first[Lv] = tiles of all levels
+    int per_leaf;                // tiles per leaf
+    int leaves;                  // N / n_leaf
+    int leaf_tiles() const { return per_leaf * leaves; }
+};
+
+inline LevelTiles level_tiles(int N, int Lv, int n_leaf)
+{
+    LevelTiles t = {};
+    int acc = 0;
+    for (int l = 0; l < Lv; ++l) {
+        t.first[l] = acc;
+        const int half = N >> (l + 1);
+        acc += (1 << l) * ((half + kRowTile - 1) / kRowTile);
+    }
+    t.first[Lv] = acc;
+    t.per_leaf = (n_leaf + kRowTile - 1) / kRowTile;
+    t.leaves = N / n_leaf;
+    return t;
+}
+
+// tile -> (level, half length, segment, first sorted position of the tile)
+__device__ __forceinline__ void level_tile(const LevelTiles& lt, int Lv, int N, int tile, int& level,
+                                           int& half, int& seg, int& p0)
+{
+    level = 0;
+    while (level + 1 < Lv && tile >= lt.first[level + 1]) ++level;
+    const int t = tile - lt.first[level];
+    half = N >> (level + 1);
+    const int tps = (half + kRowTile - 1) / kRowTile;
+    seg = t / tps;
+    p0 = (t - seg * tps) * kRowTile;
+}
+
+// tile -> (first token of its leaf, first token of the tile, end of the leaf)
+__device__ __forceinline__ void leaf_tile(const LevelTiles& lt, int n_leaf, int tile, int& lbeg, int& t0,
+                                          int& lend)
+{
+    const int leaf = tile / lt.per_leaf;
+    lbeg = leaf * n_leaf;
+    t0 = lbeg + (tile - leaf * lt.per_leaf) * kRowTile;
+    lend = lbeg + n_leaf;
+}
+
+}  // namespace elsaa

@@ -19,6 +19,7 @@
 // store the final dQ, dK, dV in the storage dtype.
 #include "common.hpp"
 #include "internal.hpp"
+#include "causal.hpp"
 #include "tile.hpp"
 
 namespace elsaa {
@@ -27,6 +28,7 @@ namespace {
 
 constexpr int kT = 64;
 constexpr int kThreads = 256;
+static_assert(kT == kRowTile, "causal tiles are numbered in 64-row tiles");
 
 enum Mode { kBlocks = 0, kLevels = 1, kLeaf = 2 };
 
@@ -48,6 +50,7 @@ struct BArgs {
     void* dK;
     void* dV;
     int H, N, k, Lv, n_leaf;
+    LevelTiles lt;            // causal tile numbering
     int nbr;                  // neighbouring sorted blocks on each side
     size_t BHN;
     float tau, tau2;
@@ -101,25 +104,22 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
         kend = min(N, (plast / bq + 1 + a.nbr) * bq);
         klist = a.perm_k + bh * N;
     } else if (MODE == kLevels) {
-        const int per_level = (N / 2) / kT;
-        level = tile / per_level;
-        const int t = tile - level * per_level;
-        half = N >> (level + 1);
-        const int seg = (t * kT) / half;
-        const int p0 = t * kT - seg * half;
+        int seg, p0;
+        level_tile(a.lt, a.Lv, N, tile, level, half, seg, p0);
         bq = min(a.k, half);
         qpos = p0 + 16 * w + qq;
         const size_t lbase = (bh * a.Lv + level) * (size_t)(N / 2) + (size_t)seg * half;
-        qtok = a.perm_q[lbase + qpos];
+        qtok = qpos < half ? a.perm_q[lbase + qpos] : -1;
         kbeg = max(0, (p0 / bq - a.nbr) * bq);
-        kend = min(half, ((p0 + kT - 1) / bq + 1 + a.nbr) * bq);
+        kend = min(half, ((min(p0 + kT, half) - 1) / bq + 1 + a.nbr) * bq);
         klist = a.perm_k + lbase;
     } else {
-        const int q0 = tile * kT;
+        int q0, lend;
+        leaf_tile(a.lt, a.n_leaf, tile, kbeg, q0, lend);
         qtok = q0 + 16 * w + qq;
         qpos = qtok;
-        kbeg = (q0 / a.n_leaf) * a.n_leaf;
-        kend = q0 + kT;
+        if (qtok >= lend) qtok = -1;
+        kend = min(q0 + kT, lend);
     }
     const int blk_lo = (MODE == kLeaf) ? 0 : max(0, (qpos / bq - a.nbr) * bq);
     const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), (qpos / bq + 1 + a.nbr) * bq);
@@ -215,10 +215,10 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
     for (int dt = 0; dt < DT; ++dt)
         tot[dt] = acc[dt] * a.tau + *(const f32x4*)(a.dq_lr + row * D + 16 * dt + 4 * g);
     if (MODE == kLeaf) {
-        const int q0 = blockIdx.x * kT;
+        const int lbeg = (blockIdx.x / a.lt.per_leaf) * a.n_leaf;
         for (int l = 0; l < a.Lv; ++l) {
             const int hl = N >> (l + 1);
-            if (((q0 / hl) & 1) == 0) continue;
+            if (((lbeg / hl) & 1) == 0) continue;
             const float* pp = a.part_dq + level_slot(bh, a.Lv, l, N, qtok, 1) * D;
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) tot[dt] += *(const f32x4*)(pp + 16 * dt + 4 * g);
@@ -276,27 +276,25 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
         qlist = a.perm_q + bh * N;
         j0 = p0;
     } else if (MODE == kLevels) {
-        const int per_level = (N / 2) / kT;
-        level = tile / per_level;
-        const int t = tile - level * per_level;
-        half = N >> (level + 1);
-        const int seg = (t * kT) / half;
-        const int p0 = t * kT - seg * half;
+        int seg, p0;
+        level_tile(a.lt, a.Lv, N, tile, level, half, seg, p0);
         bq = min(a.k, half);
         kpos = p0 + 16 * w + col;
         const size_t lbase = (bh * a.Lv + level) * (size_t)(N / 2) + (size_t)seg * half;
         klist = a.perm_k + lbase;
-        ktok = klist[kpos];
+        ktok = kpos < half ? klist[kpos] : -1;
         qbeg = max(0, (p0 / bq - a.nbr) * bq);
-        qend = min(half, ((p0 + kT - 1) / bq + 1 + a.nbr) * bq);
+        qend = min(half, ((min(p0 + kT, half) - 1) / bq + 1 + a.nbr) * bq);
         qlist = a.perm_q + lbase;
         j0 = p0;
     } else {
-        j0 = tile * kT;
+        int lbeg, lend;
+        leaf_tile(a.lt, a.n_leaf, tile, lbeg, j0, lend);
         ktok = j0 + 16 * w + col;
         kpos = ktok;
+        if (ktok >= lend) ktok = -1;
         qbeg = j0;
-        qend = (j0 / a.n_leaf + 1) * a.n_leaf;
+        qend = lend;
     }
     const int blk_lo = (MODE == kLeaf) ? 0 : max(0, (kpos / bq - a.nbr) * bq);
     const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), (kpos / bq + 1 + a.nbr) * bq);
@@ -428,9 +426,10 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
         tv[dt] = avT[dt] + *(const f32x4*)(a.dv_lr + row * D + 16 * dt + 4 * g);
     }
     if (MODE == kLeaf) {
+        const int lbeg = (blockIdx.x / a.lt.per_leaf) * a.n_leaf;
         for (int l = 0; l < a.Lv; ++l) {
             const int hl = N >> (l + 1);
-            if (((j0 / hl) & 1) != 0) continue;   // keys of past halves only
+            if (((lbeg / hl) & 1) != 0) continue;   // keys of past halves only
             const size_t slot = level_slot(bh, a.Lv, l, N, ktok, 0);
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) {
@@ -728,13 +727,13 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st)
         else ELSAA_LAUNCH("sparse_bwd_levels", (sparse_bwd_block_kernel<T, D, 128, kLevels>), grid, dim3(512), 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     } else if (s.Lv > 0) {
-        dim3 grid(s.Lv * (s.N / 2) / kT, s.H, s.B);
+        dim3 grid(a.lt.first[s.Lv], s.H, s.B);
         ELSAA_LAUNCH("sparse_dq_levels", (sparse_dq_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         ELSAA_LAUNCH("sparse_dkv_levels", (sparse_dkv_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    dim3 grid(s.N / kT, s.H, s.B);
+    dim3 grid(a.lt.leaf_tiles(), s.H, s.B);
     ELSAA_LAUNCH("sparse_dq_leaf", (sparse_dq_kernel<T, D, kLeaf>), grid, dim3(kThreads), 0, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     ELSAA_LAUNCH("sparse_dkv_leaf", (sparse_dkv_kernel<T, D, kLeaf>), grid, dim3(kThreads), 0, st, a);
@@ -756,6 +755,7 @@ hipError_t launch_sparse_bwd(const Shape& s, const void* Q, const void* K, const
     a.part_dq = part_dq; a.part_dk = part_dk; a.part_dv = part_dv;
     a.dQ = dQ; a.dK = dK; a.dV = dV;
     a.H = s.H; a.N = s.N; a.k = s.k; a.Lv = s.Lv; a.n_leaf = s.n_leaf;
+    if (s.causal) a.lt = level_tiles(s.N, s.Lv, s.n_leaf);
     a.nbr = s.neighbors;
     a.BHN = (size_t)s.B * s.H * s.N;
     a.tau = s.tau; a.tau2 = s.tau * kLog2e;

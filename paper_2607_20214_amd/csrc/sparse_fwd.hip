@@ -25,6 +25,7 @@
 //   O = g_s m O_s + g_lr O_lr.
 #include "common.hpp"
 #include "internal.hpp"
+#include "causal.hpp"
 #include "tile.hpp"
 
 namespace elsaa {
@@ -34,6 +35,7 @@ namespace {
 constexpr int kQT = 64;       // queries per workgroup
 constexpr int kKT = 64;       // keys per LDS tile
 constexpr int kThreads = 256;
+static_assert(kQT == kRowTile, "causal tiles are numbered in 64-query tiles");
 
 enum Mode { kBlocks = 0, kLevels = 1, kLeaf = 2 };
 
@@ -54,6 +56,7 @@ struct Args {
     float* m;
     float* O_s;
     int H, N, k, Lv, n_leaf;
+    LevelTiles lt;   // causal tile numbering
     int nbr;         // neighbouring sorted blocks on each side
     int m_one;       // m_sparse fixed to 1
     float tau2;      // tau * log2(e)
@@ -100,26 +103,23 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
         kend = min(N, (plast / bq + 1 + a.nbr) * bq);
         klist = a.perm_k + bh * N;
     } else if (MODE == kLevels) {
-        const int per_level = (N / 2) / kQT;
-        level = tile / per_level;
-        const int t = tile - level * per_level;
-        half = N >> (level + 1);
-        seg = (t * kQT) / half;
-        const int p0 = t * kQT - seg * half;
+        int p0;
+        level_tile(a.lt, a.Lv, N, tile, level, half, seg, p0);
         bq = min(a.k, half);
         qpos = p0 + 16 * w + qq;
         const size_t lbase = (bh * a.Lv + level) * (size_t)(N / 2) + (size_t)seg * half;
-        qtok = a.perm_q[lbase + qpos];
-        const int plast = p0 + kQT - 1;
+        qtok = qpos < half ? a.perm_q[lbase + qpos] : -1;
+        const int plast = min(p0 + kQT, half) - 1;
         kbeg = max(0, (p0 / bq - a.nbr) * bq);
         kend = min(half, (plast / bq + 1 + a.nbr) * bq);
         klist = a.perm_k + lbase;
     } else {
-        const int q0 = tile * kQT;
+        int q0, lend;
+        leaf_tile(a.lt, a.n_leaf, tile, kbeg, q0, lend);
         qtok = q0 + 16 * w + qq;
         qpos = qtok;
-        kbeg = (q0 / a.n_leaf) * a.n_leaf;
-        kend = q0 + kQT;
+        if (qtok >= lend) qtok = -1;
+        kend = min(q0 + kQT, lend);
     }
     const int blk_lo = (MODE == kLeaf) ? 0 : max(0, (qpos / bq - a.nbr) * bq);
     const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), (qpos / bq + 1 + a.nbr) * bq);
@@ -241,11 +241,12 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
     }
 
     if (MODE == kLeaf) {
-        // merge the partial of every level whose future half holds this tile
-        const int q0 = blockIdx.x * kQT;
+        // merge the partial of every level whose future half holds this leaf
+        const int lbeg = (blockIdx.x / a.lt.per_leaf) * a.n_leaf;
         for (int l = 0; l < a.Lv; ++l) {
             const int hl = N >> (l + 1);
-            if (((q0 / hl) & 1) == 0) continue;
+            if (((lbeg / hl) & 1) == 0) continue;
+            if (qtok < 0) continue;
             const int s2 = qtok / (2 * hl);
             const size_t slot = (bh * a.Lv + l) * (size_t)(N / 2) + (size_t)s2 * hl +
                                 (qtok - s2 * 2 * hl - hl);
@@ -303,12 +304,12 @@ hipError_t launch_t(const Shape& s, const Args& a, hipStream_t st)
         return hipGetLastError();
     }
     if (s.Lv > 0) {
-        dim3 grid(s.Lv * (s.N / 2) / kQT, s.H, s.B);
+        dim3 grid(a.lt.first[s.Lv], s.H, s.B);
         ELSAA_LAUNCH("sparse_fwd_levels", (sparse_fwd_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    dim3 grid(s.N / kQT, s.H, s.B);
+    dim3 grid(a.lt.leaf_tiles(), s.H, s.B);
     ELSAA_LAUNCH("sparse_fwd_leaf", (sparse_fwd_kernel<T, D, kLeaf>), grid, dim3(kThreads), 0, st, a);
     return hipGetLastError();
 }
@@ -328,6 +329,7 @@ hipError_t launch_sparse_fwd(const Shape& s, const void* Q, const void* K, const
     a.part_o = part_o; a.part_lse = part_lse;
     a.O = O; a.lse = lse; a.m = m; a.O_s = O_s;
     a.H = s.H; a.N = s.N; a.k = s.k; a.Lv = s.Lv; a.n_leaf = s.n_leaf;
+    if (s.causal) a.lt = level_tiles(s.N, s.Lv, s.n_leaf);
     a.tau2 = s.tau * kLog2e;
     a.lambda = s.lambda; a.eps = s.eps;
     if (s.bf16) return s.D == 64 ? launch_t<BF16, 64>(s, a, st) : launch_t<BF16, 128>(s, a, st);

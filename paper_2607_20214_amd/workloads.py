@@ -211,7 +211,12 @@ CAUSAL_64K_MIXED = Workload("causal-64k-mixed-bf16", 1, 8, 65536, 128, 256, 256,
 BLOCK_32K = Workload("block-32k-dmodel1024-bf16", 1, 16, 32768, 64, 128, 128, True, "bf16",
                      recipe="iid", seed=5, d_model=1024)
 
-WORKLOADS = {w.name: w for w in (TINY_FP32, CLUSTERED_4K, CAUSAL_16K, CAUSAL_64K_MIXED, BLOCK_32K)}
+# the paper's causal text setting (block size 256, base length 4096, RACE
+# with 4 tables of 4 bits) at its ArXiv length N = 32000: three levels of
+# 16000 / 8000 / 4000 sorted queries and leaves of 4000 tokens
+TEXT_32K = Workload("causal-32k-text-b256-n04096-bf16", 1, 16, 32000, 128, 256, 64, True, "bf16",
+                    recipe="iid", qk_scale=128 ** -0.25, n0=4096, seed=6)
+WORKLOADS = {w.name: w for w in (TINY_FP32, CLUSTERED_4K, CAUSAL_16K, CAUSAL_64K_MIXED, BLOCK_32K, TEXT_32K)}
 
 
 def random_matrix(seed: int, tid: int, shape, scale: float = 1.0) -> np.ndarray:

@@ -36,7 +36,7 @@ def _cfg(**kw):
     (dict(N=0), -1), (dict(k=0), -1), (dict(r=40), -1), (dict(sort_bits=9), -1),
     (dict(eps=0.0), -1), (dict(lam=-1.0), -1), (dict(beta=0.0), -1), (dict(dtype="f16"), None),
     (dict(d_h=96), -2), (dict(race_bits=3, r=64), -2), (dict(r=512), -2),
-    (dict(N=300, k=32), -2), (dict(N=96, k=16), -2),
+    (dict(N=300, k=32), -2), (dict(N=98, k=16), -2),
 ])
 def test_host_validation_rejects(kw, status):
     if status is None:
