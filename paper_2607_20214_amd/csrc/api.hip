@@ -3,6 +3,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "elsaa.h"
@@ -196,6 +197,60 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 template <class P>
 P* at(void* base, size_t off) { return (P*)((char*)base + off); }
 
+// A second stream per device on which the sparse branch's causal levels run
+// while the caller's stream runs the low-rank branch (they share no buffer;
+// the leaf kernels need both).  Fork: an event on the caller's stream that
+// the side stream waits for; join: the reverse.  Host-side enqueueing of a
+// fork / join pair holds a per-device lock, so that concurrent calls cannot
+// interleave their event records.  Default priority, created on first use
+// and kept until the process ends; without it both parts run on the
+// caller's stream.
+struct Side {
+    std::mutex mu;
+    bool init = false;
+    bool ok = false;
+    hipStream_t stream = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+};
+constexpr int kMaxDevices = 64;
+Side g_side[kMaxDevices];
+
+Side* side_stream()
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    Side& sd = g_side[dev];
+    std::lock_guard<std::mutex> lk(sd.mu);
+    if (!sd.init) {
+        sd.init = true;
+        sd.ok = hipStreamCreateWithFlags(&sd.stream, hipStreamNonBlocking) == hipSuccess &&
+                hipEventCreateWithFlags(&sd.fork, hipEventDisableTiming) == hipSuccess &&
+                hipEventCreateWithFlags(&sd.join, hipEventDisableTiming) == hipSuccess;
+    }
+    return sd.ok ? &sd : nullptr;
+}
+
+// Run first(side) on the side stream and second(main) on `main`, both after
+// what `main` already holds; `main` then waits for both.
+template <class A, class B>
+hipError_t fork_join(hipStream_t main, A first, B second)
+{
+    Side* sd = side_stream();
+    if (!sd) {
+        hipError_t e = first(main);
+        return e != hipSuccess ? e : second(main);
+    }
+    std::lock_guard<std::mutex> lk(sd->mu);
+    hipError_t e;
+    if ((e = hipEventRecord(sd->fork, main)) != hipSuccess) return e;
+    if ((e = hipStreamWaitEvent(sd->stream, sd->fork, 0)) != hipSuccess) return e;
+    const hipError_t e1 = first(sd->stream);
+    const hipError_t e2 = second(main);
+    if ((e = hipEventRecord(sd->join, sd->stream)) != hipSuccess) return e;
+    if ((e = hipStreamWaitEvent(main, sd->join, 0)) != hipSuccess) return e;
+    return e1 != hipSuccess ? e1 : e2;
+}
+
 int check_rules(const elsaa_token_rules* r, TrParams* p)
 {
     if (!r) return fail(ELSAA_ERR_INVALID_ARG, "rules is NULL");
@@ -326,11 +381,23 @@ int elsaa_fwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     hipError_t e;
     if ((e = launch_project(s, Q, W_sort, W_race, kq, uq, stream)) != hipSuccess) return hip_fail(e, "project(Q)");
     if ((e = launch_project(s, K, W_sort, W_race, kk, uk, stream)) != hipSuccess) return hip_fail(e, "project(K)");
-    if ((e = launch_sort(s, kq, kk, pq, pk, stream)) != hipSuccess) return hip_fail(e, "sort");
-    if ((e = launch_race_fwd(s, uq, uk, V, at<float>(saved, SL.race_states), o_lr, d_lr, stream)) != hipSuccess)
-        return hip_fail(e, "race forward");
-    if ((e = launch_sparse_fwd(s, Q, K, V, pq, pk, gates, lambda_rows, o_lr, d_lr, at<float>(workspace, W.part_o),
-                               at<float>(workspace, W.part_lse), O, lse, m, o_s, stream)) != hipSuccess)
+    float* part_o = at<float>(workspace, W.part_o);
+    float* part_lse = at<float>(workspace, W.part_lse);
+    // selection and the causal levels on the side stream, the low-rank branch
+    // on the caller's stream; the leaf (or sorted blocks) with the fusion
+    // epilogue after both
+    e = fork_join(
+        stream,
+        [&](hipStream_t st) {
+            hipError_t r = launch_sort(s, kq, kk, pq, pk, st);
+            if (r != hipSuccess) return r;
+            return launch_sparse_fwd(s, Q, K, V, pq, pk, gates, lambda_rows, o_lr, d_lr, part_o, part_lse, O,
+                                     lse, m, o_s, st, kSparseLevels);
+        },
+        [&](hipStream_t st) { return launch_race_fwd(s, uq, uk, V, at<float>(saved, SL.race_states), o_lr, d_lr, st); });
+    if (e != hipSuccess) return hip_fail(e, "selection / levels / race forward");
+    if ((e = launch_sparse_fwd(s, Q, K, V, pq, pk, gates, lambda_rows, o_lr, d_lr, part_o, part_lse, O, lse, m,
+                               o_s, stream, kSparseFinal)) != hipSuccess)
         return hip_fail(e, "sparse forward");
     return ELSAA_OK;
 }
@@ -372,13 +439,25 @@ int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     if ((e = launch_bwd_rows(s, dO, o_s, o_lr, m, lse, d_lr, gates, lambda_rows, rs, dgates, dlambda, stream)) !=
         hipSuccess)
         return hip_fail(e, "backward row scalars");
-    if ((e = launch_race_bwd(s, uq, uk, V, dO, W_race, rs, at<float>(sv, SL.race_states),
-                             at<float>(workspace, W.states_b), at<char>(workspace, W.wt_hi),
-                             at<char>(workspace, W.wt_lo), dq_lr, dk_lr, dv_lr, stream)) != hipSuccess)
-        return hip_fail(e, "race backward");
-    if ((e = launch_sparse_bwd(s, Q, K, V, dO, pq, pk, rs, dq_lr, dk_lr, dv_lr,
-                               at<float>(workspace, W.part_dq), at<float>(workspace, W.part_dk),
-                               at<float>(workspace, W.part_dv), dQ, dK, dV, stream)) != hipSuccess)
+    float* part_dq = at<float>(workspace, W.part_dq);
+    float* part_dk = at<float>(workspace, W.part_dk);
+    float* part_dv = at<float>(workspace, W.part_dv);
+    // the causal levels' backward on the side stream, the low-rank backward on
+    // the caller's stream; the leaf (or sorted blocks), which add the
+    // low-rank gradients, after both
+    auto levels = [&](hipStream_t st) {
+        return launch_sparse_bwd(s, Q, K, V, dO, pq, pk, rs, dq_lr, dk_lr, dv_lr, part_dq, part_dk, part_dv, dQ,
+                                 dK, dV, st, kSparseLevels);
+    };
+    auto race = [&](hipStream_t st) {
+        return launch_race_bwd(s, uq, uk, V, dO, W_race, rs, at<float>(sv, SL.race_states),
+                               at<float>(workspace, W.states_b), at<char>(workspace, W.wt_hi),
+                               at<char>(workspace, W.wt_lo), dq_lr, dk_lr, dv_lr, st);
+    };
+    if ((e = levels(stream)) != hipSuccess) return hip_fail(e, "sparse levels backward");
+    if ((e = race(stream)) != hipSuccess) return hip_fail(e, "race backward");
+    if ((e = launch_sparse_bwd(s, Q, K, V, dO, pq, pk, rs, dq_lr, dk_lr, dv_lr, part_dq, part_dk, part_dv, dQ, dK,
+                               dV, stream, kSparseFinal)) != hipSuccess)
         return hip_fail(e, "sparse backward");
     return ELSAA_OK;
 }

@@ -75,12 +75,18 @@ hipError_t launch_race_bwd(const Shape& s, const float* Uq, const float* Uk, con
                            const float* states_f, float* states_b, void* wt_hi, void* wt_lo,
                            float* dq_lr, float* dk_lr, float* dv_lr, hipStream_t st);
 
+// which kernels of a sparse-branch pass to launch: the causal levels (they
+// need only the selection), the rest (leaf or sorted blocks, which also need
+// the low-rank branch), or both
+enum SparsePart { kSparseLevels = 1, kSparseFinal = 2, kSparseAll = 3 };
+
 // sortLSH sparse branch forward + fusion epilogue
 hipError_t launch_sparse_fwd(const Shape& s, const void* Q, const void* K, const void* V,
                              const int32_t* perm_q, const int32_t* perm_k, const float* gates,
                              const float* lambda_rows,
                              const float* O_lr, const float* d_lr, float* part_o, float* part_lse,
-                             void* O, float* lse, float* m, float* O_s, hipStream_t st);
+                             void* O, float* lse, float* m, float* O_s, hipStream_t st,
+                             int parts = kSparseAll);
 
 // backward: per-row scalars rs[5][BHN] (log2(d_s+eps), Delta, sc_s, sc_lr, dDen)
 hipError_t launch_bwd_rows(const Shape& s, const void* dO, const float* Os, const float* Olr,
@@ -92,7 +98,7 @@ hipError_t launch_sparse_bwd(const Shape& s, const void* Q, const void* K, const
                              const void* dO, const int32_t* perm_q, const int32_t* perm_k,
                              const float* rs, const float* dq_lr, const float* dk_lr,
                              const float* dv_lr, float* part_dq, float* part_dk, float* part_dv,
-                             void* dQ, void* dK, void* dV, hipStream_t st);
+                             void* dQ, void* dK, void* dV, hipStream_t st, int parts = kSparseAll);
 
 // token-wise rules: gate network and query-dependent lambda (token_rules.hip)
 struct TrParams {

@@ -702,37 +702,41 @@ __global__ __launch_bounds__(BQ * 4, BQ == 64 ? 3 : 1) void sparse_bwd_block_ker
 }
 
 template <class T, int D>
-hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st)
+hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
 {
     hipError_t e;
     // whole-block kernel: b in {64, 128}, blocks never straddle a segment
     const int bq = s.k;
     const bool whole = (bq == 64 || bq == 128) && s.neighbors == 0 && (s.causal ? (s.n_leaf % bq == 0) : true);
-    if (whole && !s.causal) {
-        dim3 grid((s.N + bq - 1) / bq, s.H, s.B);
-        if (bq == 64) ELSAA_LAUNCH("sparse_bwd_blocks", (sparse_bwd_block_kernel<T, D, 64, kBlocks>), grid, dim3(256), 0, st, a);
-        else ELSAA_LAUNCH("sparse_bwd_blocks", (sparse_bwd_block_kernel<T, D, 128, kBlocks>), grid, dim3(512), 0, st, a);
-        return hipGetLastError();
-    }
     if (!s.causal) {
+        if (!(parts & kSparseFinal)) return hipSuccess;
+        if (whole) {
+            dim3 grid((s.N + bq - 1) / bq, s.H, s.B);
+            if (bq == 64) ELSAA_LAUNCH("sparse_bwd_blocks", (sparse_bwd_block_kernel<T, D, 64, kBlocks>), grid, dim3(256), 0, st, a);
+            else ELSAA_LAUNCH("sparse_bwd_blocks", (sparse_bwd_block_kernel<T, D, 128, kBlocks>), grid, dim3(512), 0, st, a);
+            return hipGetLastError();
+        }
         dim3 grid((s.N + kT - 1) / kT, s.H, s.B);
         ELSAA_LAUNCH("sparse_dq_blocks", (sparse_dq_kernel<T, D, kBlocks>), grid, dim3(kThreads), 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         ELSAA_LAUNCH("sparse_dkv_blocks", (sparse_dkv_kernel<T, D, kBlocks>), grid, dim3(kThreads), 0, st, a);
         return hipGetLastError();
     }
-    if (s.Lv > 0 && whole) {
-        dim3 grid(s.Lv * (s.N / 2) / bq, s.H, s.B);
-        if (bq == 64) ELSAA_LAUNCH("sparse_bwd_levels", (sparse_bwd_block_kernel<T, D, 64, kLevels>), grid, dim3(256), 0, st, a);
-        else ELSAA_LAUNCH("sparse_bwd_levels", (sparse_bwd_block_kernel<T, D, 128, kLevels>), grid, dim3(512), 0, st, a);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    } else if (s.Lv > 0) {
-        dim3 grid(a.lt.first[s.Lv], s.H, s.B);
-        ELSAA_LAUNCH("sparse_dq_levels", (sparse_dq_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        ELSAA_LAUNCH("sparse_dkv_levels", (sparse_dkv_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (s.Lv > 0 && (parts & kSparseLevels)) {
+        if (whole) {
+            dim3 grid(s.Lv * (s.N / 2) / bq, s.H, s.B);
+            if (bq == 64) ELSAA_LAUNCH("sparse_bwd_levels", (sparse_bwd_block_kernel<T, D, 64, kLevels>), grid, dim3(256), 0, st, a);
+            else ELSAA_LAUNCH("sparse_bwd_levels", (sparse_bwd_block_kernel<T, D, 128, kLevels>), grid, dim3(512), 0, st, a);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        } else {
+            dim3 grid(a.lt.first[s.Lv], s.H, s.B);
+            ELSAA_LAUNCH("sparse_dq_levels", (sparse_dq_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            ELSAA_LAUNCH("sparse_dkv_levels", (sparse_dkv_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
     }
+    if (!(parts & kSparseFinal)) return hipSuccess;
     dim3 grid(a.lt.leaf_tiles(), s.H, s.B);
     ELSAA_LAUNCH("sparse_dq_leaf", (sparse_dq_kernel<T, D, kLeaf>), grid, dim3(kThreads), 0, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -746,7 +750,7 @@ hipError_t launch_sparse_bwd(const Shape& s, const void* Q, const void* K, const
                              const void* dO, const int32_t* perm_q, const int32_t* perm_k,
                              const float* rs, const float* dq_lr, const float* dk_lr,
                              const float* dv_lr, float* part_dq, float* part_dk, float* part_dv,
-                             void* dQ, void* dK, void* dV, hipStream_t st)
+                             void* dQ, void* dK, void* dV, hipStream_t st, int parts)
 {
     BArgs a;
     a.Q = Q; a.K = K; a.V = V; a.dO = dO;
@@ -759,8 +763,8 @@ hipError_t launch_sparse_bwd(const Shape& s, const void* Q, const void* K, const
     a.nbr = s.neighbors;
     a.BHN = (size_t)s.B * s.H * s.N;
     a.tau = s.tau; a.tau2 = s.tau * kLog2e;
-    if (s.bf16) return s.D == 64 ? launch_t<BF16, 64>(s, a, st) : launch_t<BF16, 128>(s, a, st);
-    return s.D == 64 ? launch_t<F32, 64>(s, a, st) : launch_t<F32, 128>(s, a, st);
+    if (s.bf16) return s.D == 64 ? launch_t<BF16, 64>(s, a, st, parts) : launch_t<BF16, 128>(s, a, st, parts);
+    return s.D == 64 ? launch_t<F32, 64>(s, a, st, parts) : launch_t<F32, 128>(s, a, st, parts);
 }
 
 }  // namespace elsaa

@@ -296,19 +296,21 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
 }
 
 template <class T, int D>
-hipError_t launch_t(const Shape& s, const Args& a, hipStream_t st)
+hipError_t launch_t(const Shape& s, const Args& a, hipStream_t st, int parts)
 {
     if (!s.causal) {
+        if (!(parts & kSparseFinal)) return hipSuccess;
         dim3 grid((s.N + kQT - 1) / kQT, s.H, s.B);
         ELSAA_LAUNCH("sparse_fwd_blocks", (sparse_fwd_kernel<T, D, kBlocks>), grid, dim3(kThreads), 0, st, a);
         return hipGetLastError();
     }
-    if (s.Lv > 0) {
+    if (s.Lv > 0 && (parts & kSparseLevels)) {
         dim3 grid(a.lt.first[s.Lv], s.H, s.B);
         ELSAA_LAUNCH("sparse_fwd_levels", (sparse_fwd_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
+    if (!(parts & kSparseFinal)) return hipSuccess;
     dim3 grid(a.lt.leaf_tiles(), s.H, s.B);
     ELSAA_LAUNCH("sparse_fwd_leaf", (sparse_fwd_kernel<T, D, kLeaf>), grid, dim3(kThreads), 0, st, a);
     return hipGetLastError();
@@ -319,7 +321,7 @@ hipError_t launch_t(const Shape& s, const Args& a, hipStream_t st)
 hipError_t launch_sparse_fwd(const Shape& s, const void* Q, const void* K, const void* V,
                              const int32_t* perm_q, const int32_t* perm_k, const float* gates,
                              const float* lambda_rows, const float* O_lr, const float* d_lr, float* part_o, float* part_lse,
-                             void* O, float* lse, float* m, float* O_s, hipStream_t st)
+                             void* O, float* lse, float* m, float* O_s, hipStream_t st, int parts)
 {
     Args a;
     a.Q = Q; a.K = K; a.V = V;
@@ -332,8 +334,8 @@ hipError_t launch_sparse_fwd(const Shape& s, const void* Q, const void* K, const
     if (s.causal) a.lt = level_tiles(s.N, s.Lv, s.n_leaf);
     a.tau2 = s.tau * kLog2e;
     a.lambda = s.lambda; a.eps = s.eps;
-    if (s.bf16) return s.D == 64 ? launch_t<BF16, 64>(s, a, st) : launch_t<BF16, 128>(s, a, st);
-    return s.D == 64 ? launch_t<F32, 64>(s, a, st) : launch_t<F32, 128>(s, a, st);
+    if (s.bf16) return s.D == 64 ? launch_t<BF16, 64>(s, a, st, parts) : launch_t<BF16, 128>(s, a, st, parts);
+    return s.D == 64 ? launch_t<F32, 64>(s, a, st, parts) : launch_t<F32, 128>(s, a, st, parts);
 }
 
 }  // namespace elsaa
