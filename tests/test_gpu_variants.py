@@ -1,7 +1,7 @@
 """GPU parity of the operator variants against the oracle: neighbouring
-sorted blocks (r >= 1 blocks on each side of a query's own block, Sec. 3 and
-the causal algorithm), token-wise lambda_i with its gradient (learned and
-query-dependent lambda), and the m_sparse = 1 ablation (Sec. 7)."""
+sorted blocks (r >= 1 blocks on each side of a query's own block, the
+(2r+1)s-key variant of Sec. 6), token-wise lambda_i with its gradient
+(learned and query-dependent lambda), and the m_sparse = 1 ablation (Sec. 7)."""
 import numpy as np
 import pytest
 
