@@ -17,19 +17,23 @@ namespace elsaa {
 
 constexpr int kProjRows = 64;
 constexpr int kProjThreads = 256;
+constexpr int kProjWaves = kProjThreads / kWave;
 constexpr int kProjPad = 8;
+constexpr int kProjTarget = 1024;      // workgroups per launch (about four per CU)
 
-// Per 64-row tile of X (Q or K of one (b,h)): the sortLSH bucket key of every
-// row and, when W_race is given, the RACE projections u = W_race x of every
-// row in float32 accuracy: W = W_hi + W_lo split into two bf16 parts for the
-// bf16 MFMA path (the residual is below 2^-16 relative), plain float32 MFMA
-// for float32 storage.  u is stored [BH][N][UP] (UP = padded projections).
+// A workgroup walks a chunk of 64-row tiles of X (Q or K of one (b,h)); for
+// every row it writes the sortLSH bucket key and, when W_race is given, the
+// RACE projections u = W_race x in float32 accuracy: W = W_hi + W_lo split
+// into two bf16 parts for the bf16 MFMA path (the residual is below 2^-16
+// relative), plain float32 MFMA for float32 storage.  u is stored
+// [BH][N][UP] (UP = padded projections).  W is staged once per workgroup;
+// the next tile's rows are loaded into registers while the current one is
+// hashed and projected.
 template <class T, int D, int WR>
 struct ProjSmem {
     typename T::store_t x[kProjRows][D + kProjPad];
     typename T::store_t whi[WR][D + kProjPad];
     typename T::store_t wlo[T::bytes == 2 ? WR : 1][D + kProjPad];   // (no low part for float32)
-    float ws[8][D];
     uint32_t code[kProjRows];
 };
 
@@ -39,80 +43,102 @@ __global__ __launch_bounds__(kProjThreads) void proj_kernel(const typename T::st
                                                             const float* __restrict__ Wrace,
                                                             uint8_t* __restrict__ keys,
                                                             float* __restrict__ U, int H, int N,
-                                                            int bits, int L, int UP)
+                                                            int bits, int L, int UP, int chunk_rows)
 {
     using S = typename T::store_t;
     using F = typename T::frag_t;
-    constexpr int PER = 16 / T::bytes;
-    constexpr int CH = D / PER;
+    constexpr int PER = 16 / T::bytes;           // elements per 16-byte piece
+    constexpr int CH = D / PER;                  // pieces per row
     constexpr int KS = D / 32;
+    constexpr int PT = kProjRows * CH / kProjThreads;   // pieces staged per thread
     __shared__ ProjSmem<T, D, WR> sm;
     const int h = blockIdx.y, b = blockIdx.z;
-    const int row0 = blockIdx.x * kProjRows;
-    const int rows = min(kProjRows, N - row0);
     const size_t bh = (size_t)b * H + h;
-    const S* Xt = X + (bh * N + row0) * D;
-    for (int e = threadIdx.x; e < bits * D; e += kProjThreads) sm.ws[e / D][e % D] = Wsort[(size_t)h * bits * D + e];
-    for (int it = threadIdx.x; it < kProjRows * CH; it += kProjThreads) {
-        const int r = it / CH, c = it % CH;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (r < rows) v = ldg16(Xt + (size_t)r * D + c * PER);
-        *(uint4*)&sm.x[r][c * PER] = v;
-    }
-    if (threadIdx.x < kProjRows) sm.code[threadIdx.x] = 0;
+    const int rbeg = blockIdx.x * chunk_rows;
+    const int rend = min(N, rbeg + chunk_rows);
+    const S* Xh = X + bh * N * D;
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+
+    // rows [row0, row0 + 64) -> registers (zero past rend)
+    uint4 rx[PT];
+    auto load = [&](int row0) {
+#pragma unroll
+        for (int j = 0; j < PT; ++j) {
+            const int it = threadIdx.x + kProjThreads * j;
+            const int r = it / CH, c = it % CH;
+            rx[j] = row0 + r < rend ? ldg16(Xh + (size_t)(row0 + r) * D + c * PER) : make_uint4(0, 0, 0, 0);
+        }
+    };
+    load(rbeg);
     if (Wrace) {
         for (int it = threadIdx.x; it < WR * D; it += kProjThreads) {
             const int row = it / D, c = it % D;
-            const float w = row < 4 * L ? Wrace[((size_t)h * L * 4 + row) * D + c] : 0.f;
-            const S hi = T::store(w);
+            const float wv = row < 4 * L ? Wrace[((size_t)h * L * 4 + row) * D + c] : 0.f;
+            const S hi = T::store(wv);
             sm.whi[row][c] = hi;
-            if (T::bytes == 2) sm.wlo[row][c] = T::store(w - T::load(hi));
+            if (T::bytes == 2) sm.wlo[row][c] = T::store(wv - T::load(hi));
         }
     }
-    __syncthreads();
-    // hash: thread (row, bit group) runs the float32 fma chains of its bits
-    // over the row, read from LDS in 16-byte pieces
-    {
-        const int r = threadIdx.x & (kProjRows - 1);
-        uint32_t c = 0;
-        for (int bit = threadIdx.x / kProjRows; bit < bits; bit += kProjThreads / kProjRows) {
-            float p = 0.0f;
+    const float* ws_h = Wsort + (size_t)h * bits * D;
+    int tix = 0;
+    for (int row0 = rbeg; row0 < rend; row0 += kProjRows, ++tix) {
+        __syncthreads();                          // previous tile consumed
+#pragma unroll
+        for (int j = 0; j < PT; ++j) {
+            const int it = threadIdx.x + kProjThreads * j;
+            *(uint4*)&sm.x[it / CH][(it % CH) * PER] = rx[j];
+        }
+        if (threadIdx.x < kProjRows) sm.code[threadIdx.x] = 0;
+        __syncthreads();
+        if (row0 + kProjRows < rend) load(row0 + kProjRows);
+        const int rows = min(kProjRows, rend - row0);
+
+        // hash: lane = row; the wave runs the float32 fma chains of the bits
+        // assigned to it on this tile (the assignment rotates over tiles so
+        // the waves share the bits evenly); W_sort row is wave-uniform
+        {
+            uint32_t c = 0;
+            for (int bit = (w + kProjWaves - (tix % kProjWaves)) % kProjWaves; bit < bits; bit += kProjWaves) {
+                const float* wrow = ws_h + (size_t)bit * D;
+                float p = 0.0f;
 #pragma unroll 4
-            for (int e0 = 0; e0 < D; e0 += PER) {
-                const uint4 v = *(const uint4*)&sm.x[r][e0];
-                const S* xs = (const S*)&v;
+                for (int e0 = 0; e0 < D; e0 += PER) {
+                    const uint4 v = *(const uint4*)&sm.x[lane][e0];
+                    const S* xs = (const S*)&v;
 #pragma unroll
-                for (int j = 0; j < PER; ++j) p = __builtin_fmaf(sm.ws[bit][e0 + j], T::load(xs[j]), p);
+                    for (int j = 0; j < PER; ++j) p = __builtin_fmaf(wrow[e0 + j], T::load(xs[j]), p);
+                }
+                if (p > 0.0f) c |= 1u << bit;
             }
-            if (p > 0.0f) c |= 1u << bit;
+            if (c) atomicOr(&sm.code[lane], c);
         }
-        if (c) atomicOr(&sm.code[r], c);
-    }
-    __syncthreads();
-    if (threadIdx.x < rows) {
-        const uint32_t code = sm.code[threadIdx.x];
-        uint32_t rank = code;
-        for (uint32_t sft = code >> 1; sft; sft >>= 1) rank ^= sft;
-        keys[bh * N + row0 + threadIdx.x] = (uint8_t)rank;
-    }
-    if (!Wrace) return;
-    // u[token][p] for the wave's 16 tokens: A = W rows, B = X rows
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int g = lane >> 4, col = lane & 15;
-    const int tl = 16 * w + col;
-    F xf[KS];
+        // u[token][p] for the wave's 16 tokens: A = W rows, B = X rows
+        if (Wrace) {
+            const int g = lane >> 4, col = lane & 15;
+            const int tl = 16 * w + col;
+            F xf[KS];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) xf[ks] = T::ld8(&sm.x[tl][32 * ks + 8 * g]);
+            for (int ks = 0; ks < KS; ++ks) xf[ks] = T::ld8(&sm.x[tl][32 * ks + 8 * g]);
 #pragma unroll
-    for (int pt = 0; pt < WR / 16; ++pt) {
-        f32x4 acc = {0, 0, 0, 0};
+            for (int pt = 0; pt < WR / 16; ++pt) {
+                f32x4 acc = {0, 0, 0, 0};
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            acc = T::mma(T::ld8(&sm.whi[16 * pt + col][32 * ks + 8 * g]), xf[ks], acc);
-            if (T::bytes == 2) acc = T::mma(T::ld8(&sm.wlo[16 * pt + col][32 * ks + 8 * g]), xf[ks], acc);
+                for (int ks = 0; ks < KS; ++ks) {
+                    acc = T::mma(T::ld8(&sm.whi[16 * pt + col][32 * ks + 8 * g]), xf[ks], acc);
+                    if (T::bytes == 2) acc = T::mma(T::ld8(&sm.wlo[16 * pt + col][32 * ks + 8 * g]), xf[ks], acc);
+                }
+                const int p0 = 16 * pt + 4 * g;
+                if (tl < rows && p0 < UP) *(f32x4*)(U + (bh * N + row0 + tl) * UP + p0) = acc;
+            }
         }
-        const int p0 = 16 * pt + 4 * g;
-        if (tl < rows && p0 < UP) *(f32x4*)(U + (bh * N + row0 + tl) * UP + p0) = acc;
+        __syncthreads();
+        if (threadIdx.x < rows) {
+            const uint32_t code = sm.code[threadIdx.x];
+            uint32_t rank = code;
+            for (uint32_t sft = code >> 1; sft; sft >>= 1) rank ^= sft;
+            keys[bh * N + row0 + threadIdx.x] = (uint8_t)rank;
+        }
     }
 }
 
@@ -120,13 +146,19 @@ template <class T, int D>
 hipError_t launch_proj_t(const Shape& s, const void* X, const float* W_sort, const float* W_race,
                          uint8_t* keys, float* U, hipStream_t st)
 {
-    dim3 grid((s.N + kProjRows - 1) / kProjRows, s.H, s.B);
+    const int64_t tiles = (s.N + kProjRows - 1) / kProjRows;
+    const int64_t bh = (int64_t)s.B * s.H;
+    int64_t want = (kProjTarget + bh - 1) / bh;
+    if (want > tiles) want = tiles;
+    const int64_t per = (tiles + want - 1) / want;
+    const int chunk_rows = (int)(per * kProjRows);
+    dim3 grid((s.N + chunk_rows - 1) / chunk_rows, s.H, s.B);
     const int UP = race_proj_stride(s);
     const int wr = UP < 16 ? 16 : UP;
 #define ELSAA_PROJ(WR_)                                                                          \
     ELSAA_LAUNCH("project", (proj_kernel<T, D, WR_>), grid, dim3(kProjThreads), 0, st,                 \
                        (const typename T::store_t*)X, W_sort, W_race, keys, U, s.H, s.N,          \
-                       s.sort_bits, s.L, UP)
+                       s.sort_bits, s.L, UP, chunk_rows)
     if (wr == 16) ELSAA_PROJ(16);
     else if (wr == 32) ELSAA_PROJ(32);
     else ELSAA_PROJ(64);
