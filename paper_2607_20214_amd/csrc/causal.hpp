@@ -58,4 +58,24 @@ __device__ __forceinline__ void leaf_tile(const LevelTiles& lt, int n_leaf, int 
     lend = lbeg + n_leaf;
 }
 
+// This workgroup's (tile, h, b) in a grid of (tiles, H, B), renumbered so
+// that consecutive tiles run on the same XCD: the chip deals workgroups to
+// its 8 XCDs round-robin by linear id, and each XCD has its own L2, so
+// neighbouring tiles that read the same rows (the tiles of one causal leaf,
+// the query tiles of one sorted block) share them through one L2.  Linear
+// ids 8 q + x (q < total / 8) become tile x * (total / 8) + q; a remainder
+// of fewer than 8 keeps its own numbering.
+__device__ __forceinline__ void xcd_tile(int& tile, int& h, int& b)
+{
+    const int nx = gridDim.x, ny = gridDim.y;
+    const int total = nx * ny * gridDim.z;
+    const int lin = blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z);
+    const int per = total >> 3;
+    const int t = lin < 8 * per ? (lin & 7) * per + (lin >> 3) : lin;
+    tile = t % nx;
+    const int rest = t / nx;
+    h = rest % ny;
+    b = rest / ny;
+}
+
 }  // namespace elsaa

@@ -81,7 +81,8 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
     constexpr int PT = TD::PER_THREAD;
     __shared__ __attribute__((aligned(16))) S sk[TD::elems(kT)];
     __shared__ __attribute__((aligned(16))) S sv[TD::elems(kT)];
-    const int h = blockIdx.y, b = blockIdx.z;
+    int tile, h, b;
+    xcd_tile(tile, h, b);
     const size_t bh = (size_t)b * a.H + h;
     const int N = a.N;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -93,7 +94,6 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
 
     int level = 0, half = N, qpos, qtok, kbeg, kend, bq = 1;
     const int32_t* klist = nullptr;
-    const int tile = blockIdx.x;
     if (MODE == kBlocks) {
         bq = min(a.k, N);
         const int p0 = tile * kT;
@@ -215,7 +215,7 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
     for (int dt = 0; dt < DT; ++dt)
         tot[dt] = acc[dt] * a.tau + *(const f32x4*)(a.dq_lr + row * D + 16 * dt + 4 * g);
     if (MODE == kLeaf) {
-        const int lbeg = (blockIdx.x / a.lt.per_leaf) * a.n_leaf;
+        const int lbeg = (tile / a.lt.per_leaf) * a.n_leaf;
         for (int l = 0; l < a.Lv; ++l) {
             const int hl = N >> (l + 1);
             if (((lbeg / hl) & 1) == 0) continue;
@@ -250,7 +250,8 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
     __shared__ __attribute__((aligned(16))) S so[TD::elems(kT)];
     __shared__ float s_l2[kT], s_de[kT], s_sc[kT];
     __shared__ int s_ok[kT];
-    const int h = blockIdx.y, b = blockIdx.z;
+    int tile, h, b;
+    xcd_tile(tile, h, b);
     const size_t bh = (size_t)b * a.H + h;
     const int N = a.N;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -263,7 +264,6 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
     int level = 0, half = N, kpos, ktok, qbeg, qend, bq = 1, j0 = 0;
     const int32_t* qlist = nullptr;
     const int32_t* klist = nullptr;
-    const int tile = blockIdx.x;
     if (MODE == kBlocks) {
         bq = min(a.k, N);
         const int p0 = tile * kT;
@@ -426,7 +426,7 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
         tv[dt] = avT[dt] + *(const f32x4*)(a.dv_lr + row * D + 16 * dt + 4 * g);
     }
     if (MODE == kLeaf) {
-        const int lbeg = (blockIdx.x / a.lt.per_leaf) * a.n_leaf;
+        const int lbeg = (tile / a.lt.per_leaf) * a.n_leaf;
         for (int l = 0; l < a.Lv; ++l) {
             const int hl = N >> (l + 1);
             if (((lbeg / hl) & 1) != 0) continue;   // keys of past halves only

@@ -75,7 +75,8 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
     __shared__ __attribute__((aligned(16))) S sk[Tl::elems(kKT)];
     __shared__ __attribute__((aligned(16))) S sv[Tl::elems(kKT)];
 
-    const int h = blockIdx.y, b = blockIdx.z;
+    int tile, h, b;
+    xcd_tile(tile, h, b);
     const size_t bh = (size_t)b * a.H + h;
     const int N = a.N;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -91,7 +92,6 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
     int kbeg, kend;                     // key positions [kbeg, kend) scanned by the tile
     int bq = 1;                         // block size b' (kBlocks / kLevels)
     const int32_t* klist = nullptr;     // sorted key list (kBlocks / kLevels)
-    const int tile = blockIdx.x;
     // sorted query block t sees the sorted key blocks t - nbr .. t + nbr
     if (MODE == kBlocks) {
         bq = min(a.k, N);
@@ -242,7 +242,7 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
 
     if (MODE == kLeaf) {
         // merge the partial of every level whose future half holds this leaf
-        const int lbeg = (blockIdx.x / a.lt.per_leaf) * a.n_leaf;
+        const int lbeg = (tile / a.lt.per_leaf) * a.n_leaf;
         for (int l = 0; l < a.Lv; ++l) {
             const int hl = N >> (l + 1);
             if (((lbeg / hl) & 1) == 0) continue;
