@@ -130,18 +130,35 @@ __device__ __forceinline__ f32x4 mma_split(typename T::frag_t a, const float* b,
 __device__ __forceinline__ uint4 ldg16(const void* p) { return *(const uint4*)p; }
 __device__ __forceinline__ void stg16(void* p, uint4 v) { *(uint4*)p = v; }
 
+// The values of lanes l & ~16 (lo) and l | 16 (hi) in every lane l, from one
+// gfx950 v_permlane16_swap of v with itself (no LDS traffic); xpair32 does the
+// same for lane bit 5.
+struct LanePair {
+    float lo, hi;
+};
+__device__ __forceinline__ LanePair xpair16(float v)
+{
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return {__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+__device__ __forceinline__ LanePair xpair32(float v)
+{
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return {__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+
 __device__ __forceinline__ float wave_max16(float v)   // max over lanes l, l^16, l^32, l^48
 {
-    v = fmaxf(v, __shfl_xor(v, 16));
-    v = fmaxf(v, __shfl_xor(v, 32));
-    return v;
+    const LanePair a = xpair16(v);
+    const LanePair b = xpair32(fmaxf(a.lo, a.hi));
+    return fmaxf(b.lo, b.hi);
 }
 
 __device__ __forceinline__ float wave_sum16(float v)   // sum over lanes l, l^16, l^32, l^48
 {
-    v += __shfl_xor(v, 16);
-    v += __shfl_xor(v, 32);
-    return v;
+    const LanePair a = xpair16(v);
+    const LanePair b = xpair32(a.lo + a.hi);
+    return b.lo + b.hi;
 }
 
 __device__ __forceinline__ float row_sum16(float v)    // sum over the 16 lanes of a row group

@@ -44,12 +44,13 @@ template <class T, int D, int RP>
 struct Lb1Smem {
     using S = typename T::store_t;
     S vt[D][kC + kPad];            // V chunk transposed
-    S dn[kC][D + kPad];            // dNum chunk, rows
+    S dn[kC][D + kPad];            // dO chunk, rows (dNum_i = sc_lr,i dO_i: the products apply sc_lr)
     S pkt[RP][kC + kPad];          // Phi_K transposed
     S gg[kC][kC + kPad];           // G[i][j] = <dNum_i, V_j> + dDen_i, j <= i
     float ts[kC][RP / 4];          // tanh(W q) of the chunk's queries
     S du[kC][w_kdim<RP>() + kPad];
     float dden[kC];
+    float sc[kC];                  // sc_lr of the chunk's queries
     float a_state[RP];             // A = sum phi(k) of the keys before the chunk
 };
 
@@ -83,30 +84,40 @@ constexpr bool bwd_fits()
            sizeof(Lb3Smem<T, D, RP>) <= kMaxLds;
 }
 
-// du [64 rows][p] x (W_hi + W_lo) [p][D] -> float32 rows [16w, 16w + 16) of out (all D);
-// W' (hi, lo) [D][w_kdim] of this head is read from global memory (L2-resident).
+// du [64 rows][p] x (W_hi + W_lo) [p][D] -> float32 rows [t0, t0 + 64) of out.
+// Computed transposed, out' = W' du': wave w forms the d-tiles dt = w, w + 4,
+// ... for all four 16-row tiles, so it reads only those rows of W' (hi, lo)
+// [D][w_kdim] (L2-resident), and lane (g, col) holds d = 16 dt + 4 g + i of
+// row 16 tt + col: one 16-byte store per lane and tile.
 template <class T, int D, int RP>
 __device__ __forceinline__ void du_times_w(const typename T::store_t (*du)[w_kdim<RP>() + kPad],
                                            const typename T::store_t* wth, const typename T::store_t* wtl,
                                            float* out, int t0, int N)
 {
+    using F = typename T::frag_t;
     constexpr int DT = D / 16, WK = w_kdim<RP>(), KP = WK / 32;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int g = lane >> 4, col = lane & 15;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-        f32x4 acc = {0, 0, 0, 0};
+    for (int dt = w; dt < DT; dt += 4) {
+        F wh[KP], wl[KP];
 #pragma unroll
         for (int kp = 0; kp < KP; ++kp) {
-            const auto df = T::ld8(&du[16 * w + col][32 * kp + 8 * g]);
             const size_t o = (size_t)(16 * dt + col) * WK + 32 * kp + 8 * g;
-            acc = T::mma(df, T::ld8(wth + o), acc);
-            if (T::kSplit) acc = T::mma(df, T::ld8(wtl + o), acc);
+            wh[kp] = T::ld8(wth + o);
+            if (T::kSplit) wl[kp] = T::ld8(wtl + o);
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int tok = t0 + 16 * w + 4 * g + i;
-            if (tok < N) out[(size_t)tok * D + 16 * dt + col] = acc[i];
+        for (int tt = 0; tt < 4; ++tt) {
+            f32x4 acc = {0, 0, 0, 0};
+#pragma unroll
+            for (int kp = 0; kp < KP; ++kp) {
+                const F df = T::ld8(&du[16 * tt + col][32 * kp + 8 * g]);
+                acc = T::mma(wh[kp], df, acc);
+                if (T::kSplit) acc = T::mma(wl[kp], df, acc);
+            }
+            const int tok = t0 + 16 * tt + col;
+            if (tok < N) *(f32x4*)(out + (size_t)tok * D + 16 * dt + 4 * g) = acc;
         }
     }
 }
@@ -170,8 +181,12 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
     if (a.causal) uk.load(Uk, t_beg, a.N);
     for (int t0 = t_beg; t0 < t_end; t0 += kC) {
         __syncthreads();
-        stage_r<T, D>(sm.dn, dO, t0, a.N, sclr);
-        if (threadIdx.x < kC) sm.dden[threadIdx.x] = (t0 + threadIdx.x < a.N) ? dden[t0 + threadIdx.x] : 0.f;
+        stage_r<T, D>(sm.dn, dO, t0, a.N);
+        if (threadIdx.x < kC) {
+            const bool in = t0 + threadIdx.x < a.N;
+            sm.dden[threadIdx.x] = in ? dden[t0 + threadIdx.x] : 0.f;
+            sm.sc[threadIdx.x] = in ? sclr[t0 + threadIdx.x] : 0.f;
+        }
         features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, nullptr, nullptr, sm.ts);
         if (a.causal) {
             stage_t<T, D>(sm.vt, V, t0, a.N);
@@ -183,7 +198,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
             if (a.causal) uk.load(Uk, t0 + kC, a.N);
         }
         if (a.causal) {
-            // G rows [16w, 16w + 16): <dNum_i, V_j> + dDen_i for j <= i
+            // G rows [16w, 16w + 16): sc_lr,i <dO_i, V_j> + dDen_i for j <= i
             for (int kt = 0; kt < 4; ++kt) {
                 f32x4 acc = {0, 0, 0, 0};
                 if (kt <= w) {
@@ -196,12 +211,12 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int qi = 16 * w + 4 * g + i, kj = 16 * kt + col;
-                    sm.gg[qi][kj] = T::store(kj <= qi ? acc[i] + sm.dden[qi] : 0.f);
+                    sm.gg[qi][kj] = T::store(kj <= qi ? acc[i] * sm.sc[qi] + sm.dden[qi] : 0.f);
                 }
             }
         }
         __syncthreads();
-        // dphi(q)' tiles [features of table ft] x [16 queries]: S G-terms + A dDen + intra
+        // dphi(q)' tiles [features of table ft] x [16 queries]: sc_lr S dO + A dDen + intra
         // (the state's hi / lo bf16 split is made once per chunk and k-step)
 #pragma unroll
         for (int j = 0; j < NFT; ++j) {
@@ -229,9 +244,9 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
                 }
             }
             for (int qt = 0; qt < 4; ++qt) {
-                const float ddq = sm.dden[16 * qt + col];
+                const float ddq = sm.dden[16 * qt + col], scq = sm.sc[16 * qt + col];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) acc[qt][i] += sm.a_state[16 * ft + 4 * g + i] * ddq;
+                for (int i = 0; i < 4; ++i) acc[qt][i] = acc[qt][i] * scq + sm.a_state[16 * ft + 4 * g + i] * ddq;
                 if (a.causal) {
 #pragma unroll
                     for (int kk = 0; kk < 2; ++kk)
@@ -258,11 +273,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
                         St_[j][dt] = T::mma(T::ld8(&sm.vt[16 * dt + col][32 * kk + 8 * g]), bf, St_[j][dt]);
                 }
             }
-            for (int f = threadIdx.x; f < RP; f += kThreads) {
-                float sacc = 0.f;
-                for (int k = 0; k < kC; ++k) sacc += T::load(sm.pkt[f][k]);
-                sm.a_state[f] += sacc;
-            }
+            add_chunk_sums<T, RP>(sm.pkt, nullptr, 1.f, sm.a_state);
         }
     }
 }
@@ -398,11 +409,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
                         St_[j][dt] = T::mma(T::ld8(&sm.dnt[16 * dt + col][32 * kk + 8 * g]), bf, St_[j][dt]);
                 }
             }
-            for (int f = threadIdx.x; f < RP; f += kThreads) {
-                float sacc = 0.f;
-                for (int k = 0; k < kC; ++k) sacc += T::load(sm.pqt[f][k]) * sm.dden[k];
-                sm.a_state[f] += sacc * a.inv_L;
-            }
+            add_chunk_sums<T, RP>(sm.pqt, sm.dden, a.inv_L, sm.a_state);
         }
     }
 }

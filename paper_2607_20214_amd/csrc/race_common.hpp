@@ -55,6 +55,32 @@ __device__ __forceinline__ typename T::frag_t col8_t(const typename T::store_t (
     }
 }
 
+// a_state[f] += scale * sum over the chunk's tokens k of xt[f][k] (* wk[k] when
+// wk is not null), xt a transposed feature tile [RP][kC + kPad]; all threads,
+// 256 / RP per feature (16-byte LDS reads, then a lane reduction).
+template <class T, int RP>
+__device__ __forceinline__ void add_chunk_sums(const typename T::store_t (*xt)[kC + kPad], const float* wk,
+                                               float scale, float* a_state)
+{
+    constexpr int TPF = RP >= kThreads ? 1 : kThreads / RP;   // threads per feature
+    constexpr int PER = kC / TPF;                               // tokens per thread
+    static_assert(PER % 8 == 0, "chunk split");
+    for (int f0 = 0; f0 < RP; f0 += kThreads / TPF) {
+        const int f = f0 + (int)threadIdx.x / TPF, part = threadIdx.x % TPF;
+        float s = 0.f;
+#pragma unroll
+        for (int k8 = 0; k8 < PER; k8 += 8) {
+            const int k = part * PER + k8;
+            const auto v = T::ld8(&xt[f][k]);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) s += wk ? (float)v[j] * wk[k + j] : (float)v[j];
+        }
+#pragma unroll
+        for (int m = 1; m < TPF; m <<= 1) s += __shfl_xor(s, m);
+        if (part == 0) a_state[f] += s * scale;
+    }
+}
+
 // projection count padded to whole 32-wide k-steps (backward du x W)
 template <int RP> constexpr int w_kdim() { return RP / 4 < 32 ? 32 : RP / 4; }
 
@@ -218,25 +244,24 @@ __device__ __forceinline__ void chain_rule_t(f32x4 dphi, int qt, int tb, int L, 
     }
     // features c = 4g + i: bits 0, 1 from i, bits 2, 3 from g
     const float hi = ((g & 1) ? sp[2] : sn[2]) * ((g & 2) ? sp[3] : sn[3]);
-    float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+    float p0 = 0.f, p1 = 0.f, p2 = 0.f;       // sums over i of x, x v_c0, x v_c1
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const float phi = ((i & 1) ? sp[0] : sn[0]) * ((i & 2) ? sp[1] : sn[1]) * hi;
         const float x = dphi[i] * phi;
-        s0 += x;
-        s1 += (i & 1) ? x : -x;
-        s2 += (i & 2) ? x : -x;
+        p0 += x;
+        p1 += (i & 1) ? x : -x;
+        p2 += (i & 2) ? x : -x;
     }
-    // bits 2 and 3 are constant within the lane group
-    s3 = (g & 2) ? s0 : -s0;
-    const float s2g = (g & 1) ? s0 : -s0;
-    s0 = wave_sum16(s0);
-    s1 = wave_sum16(s1);
-    s2 = wave_sum16(s2);
-    const float s2b = wave_sum16(s2g);
-    s3 = wave_sum16(s3);
+    // over the lane groups: g & 1 (lane bit 4) is feature bit 2, g >> 1 (lane
+    // bit 5) feature bit 3; each exchange gives both the sum and the
+    // difference of the two groups
+    const LanePair a0 = xpair16(p0), a1 = xpair16(p1), a2 = xpair16(p2);
+    const LanePair b0 = xpair32(a0.lo + a0.hi), bd = xpair32(a0.hi - a0.lo);
+    const LanePair b1 = xpair32(a1.lo + a1.hi), b2 = xpair32(a2.lo + a2.hi);
+    const float s0 = b0.lo + b0.hi;            // sum over c of x_c
     // sums over c of x_c v_cb for b = 0..3
-    const float sb[4] = {s1, s2, s2b, s3};
+    const float sb[4] = {b1.lo + b1.hi, b2.lo + b2.hi, bd.lo + bd.hi, b0.hi - b0.lo};
     float v = 0.f;
 #pragma unroll
     for (int b = 0; b < 4; ++b)
