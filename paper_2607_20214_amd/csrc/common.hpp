@@ -126,6 +126,19 @@ __device__ __forceinline__ f32x4 mma_split(typename T::frag_t a, const float* b,
     return c;
 }
 
+// Four consecutive outputs of one row in the storage dtype, one store.
+template <class T>
+__device__ __forceinline__ void store4(typename T::store_t* p, f32x4 v)
+{
+    if constexpr (T::bytes == 2) {
+        const uint32_t lo = (uint32_t)T::store(v[0]) | ((uint32_t)T::store(v[1]) << 16);
+        const uint32_t hi = (uint32_t)T::store(v[2]) | ((uint32_t)T::store(v[3]) << 16);
+        *(uint2*)p = make_uint2(lo, hi);
+    } else {
+        *(f32x4*)p = v;
+    }
+}
+
 // 16-byte global load / store of raw bytes.
 __device__ __forceinline__ uint4 ldg16(const void* p) { return *(const uint4*)p; }
 __device__ __forceinline__ void stg16(void* p, uint4 v) { *(uint4*)p = v; }

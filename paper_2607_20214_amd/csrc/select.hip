@@ -186,6 +186,7 @@ hipError_t launch_project(const Shape& s, const void* X, const float* W_sort, co
 
 constexpr int kSortThreads = 256;
 constexpr int kSortWaves = kSortThreads / kWave;
+constexpr int kKeyCache = 16384;       // keys of a list staged in LDS (longer lists read the rest from HBM)
 
 __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint8_t* __restrict__ keyq,
                                                             const uint8_t* __restrict__ keyk,
@@ -196,6 +197,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint8_t* __res
     __shared__ int hist[256];
     __shared__ int base[256];
     __shared__ int cnt[kSortWaves][256];
+    __shared__ uint8_t kc[kKeyCache];
     const int h = blockIdx.y, b = blockIdx.z;
     const int task = blockIdx.x;
     const int nb = 1 << bits;
@@ -226,7 +228,26 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint8_t* __res
 
     for (int i = threadIdx.x; i < nb; i += kSortThreads) hist[i] = 0;
     __syncthreads();
-    for (int i = threadIdx.x; i < len; i += kSortThreads) atomicAdd(&hist[key[i]], 1);
+    // histogram; the first kKeyCache keys are staged in LDS on the way, eight
+    // loads per thread in flight at a time
+    const int ncache = min(len, kKeyCache);
+    for (int i0 = 0; i0 < ncache; i0 += 8 * kSortThreads) {
+        uint8_t v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int i = i0 + j * kSortThreads + threadIdx.x;
+            v[j] = i < ncache ? key[i] : 0;
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int i = i0 + j * kSortThreads + threadIdx.x;
+            if (i < ncache) {
+                kc[i] = v[j];
+                atomicAdd(&hist[v[j]], 1);
+            }
+        }
+    }
+    for (int i = ncache + threadIdx.x; i < len; i += kSortThreads) atomicAdd(&hist[key[i]], 1);
     __syncthreads();
     if (threadIdx.x == 0) {
         int acc = 0;
@@ -239,7 +260,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint8_t* __res
         __syncthreads();
         const int i = c0 + threadIdx.x;
         const bool valid = i < len;
-        const int kk = valid ? key[i] : 0;
+        const int kk = valid ? (i < ncache ? kc[i] : key[i]) : 0;
         // lanes of this wave holding the same key
         uint64_t same = __ballot(valid);
         for (int bit = 0; bit < bits; ++bit) {

@@ -64,6 +64,19 @@ __device__ __forceinline__ size_t level_slot(size_t bh, int Lv, int l, int N, in
     return (bh * Lv + l) * (size_t)(N / 2) + (size_t)s2 * hl + (t - s2 * 2 * hl - (future ? hl : 0));
 }
 
+// Causal levels whose partials the leaf starting at token lbeg adds: bit l
+// is set when the leaf lies in the future half (future = true) or in the
+// past half of its level-l segment.
+__device__ __forceinline__ unsigned leaf_levels(int lbeg, int N, int Lv, bool future)
+{
+    unsigned mask = 0;
+    for (int l = 0; l < Lv; ++l) {
+        const int hl = N >> (l + 1);
+        if ((((lbeg / hl) & 1) != 0) == future) mask |= 1u << l;
+    }
+    return mask;
+}
+
 // ------------------------------------------------------------------------
 // dQ: query-centric.  One workgroup per 64 queries (16 per wave, one per
 // lane column); key tiles of 64 rows stream through LDS (tile.hpp) with the
@@ -209,26 +222,46 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
         for (int dt = 0; dt < DT; ++dt) *(f32x4*)(out + 16 * dt + 4 * g) = acc[dt] * a.tau;
         return;
     }
+    // dQ = this pass + the low-rank part + (leaf) the partials of the levels
+    // where the query was a future query, added in that order; the rows are
+    // fetched two at a time so their loads are in flight together
     const size_t row = bh * N + qtok;
     f32x4 tot[DT];
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-        tot[dt] = acc[dt] * a.tau + *(const f32x4*)(a.dq_lr + row * D + 16 * dt + 4 * g);
-    if (MODE == kLeaf) {
-        const int lbeg = (tile / a.lt.per_leaf) * a.n_leaf;
-        for (int l = 0; l < a.Lv; ++l) {
-            const int hl = N >> (l + 1);
-            if (((lbeg / hl) & 1) == 0) continue;
-            const float* pp = a.part_dq + level_slot(bh, a.Lv, l, N, qtok, 1) * D;
+    for (int dt = 0; dt < DT; ++dt) tot[dt] = acc[dt] * a.tau;
+    unsigned lmask = MODE == kLeaf ? leaf_levels((tile / a.lt.per_leaf) * a.n_leaf, N, a.Lv, true) : 0u;
+    bool lr = true;
+    for (;;) {
+        const float* src[2];
+        bool use[2];
 #pragma unroll
-            for (int dt = 0; dt < DT; ++dt) tot[dt] += *(const f32x4*)(pp + 16 * dt + 4 * g);
+        for (int j = 0; j < 2; ++j) {
+            src[j] = a.dq_lr + row * D;
+            use[j] = j == 0 && lr;
+            if (!use[j] && lmask) {
+                const int l = __builtin_ctz(lmask);
+                lmask &= lmask - 1;
+                src[j] = a.part_dq + level_slot(bh, a.Lv, l, N, qtok, 1) * D;
+                use[j] = true;
+            }
         }
+        lr = false;
+        f32x4 x[2][DT];
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+            if (use[j])
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) x[j][dt] = *(const f32x4*)(src[j] + 16 * dt + 4 * g);
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+            if (use[j])
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) tot[dt] += x[j][dt];
+        if (!lmask) break;
     }
     S* out = (S*)a.dQ + row * D;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) out[16 * dt + 4 * g + i] = T::store(tot[dt][i]);
+    for (int dt = 0; dt < DT; ++dt) store4<T>(out + 16 * dt + 4 * g, tot[dt]);
 }
 
 // ------------------------------------------------------------------------
@@ -418,35 +451,63 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
         }
         return;
     }
+    // dK, dV = this pass + the low-rank parts + (leaf) the partials of the
+    // levels where the key was a past key, added in that order; the rows are
+    // fetched two (dK, dV) pairs at a time so their loads are in flight together
     const size_t row = bh * N + ktok;
     f32x4 tk[DT], tv[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
-        tk[dt] = akT[dt] * a.tau + *(const f32x4*)(a.dk_lr + row * D + 16 * dt + 4 * g);
-        tv[dt] = avT[dt] + *(const f32x4*)(a.dv_lr + row * D + 16 * dt + 4 * g);
+        tk[dt] = akT[dt] * a.tau;
+        tv[dt] = avT[dt];
     }
-    if (MODE == kLeaf) {
-        const int lbeg = (tile / a.lt.per_leaf) * a.n_leaf;
-        for (int l = 0; l < a.Lv; ++l) {
-            const int hl = N >> (l + 1);
-            if (((lbeg / hl) & 1) != 0) continue;   // keys of past halves only
-            const size_t slot = level_slot(bh, a.Lv, l, N, ktok, 0);
+    unsigned lmask = MODE == kLeaf ? leaf_levels((tile / a.lt.per_leaf) * a.n_leaf, N, a.Lv, false) : 0u;
+    bool lr = true;
+    for (;;) {
+        const float* sk_[2];
+        const float* sv_[2];
+        bool use[2];
 #pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-                tk[dt] += *(const f32x4*)(a.part_dk + slot * D + 16 * dt + 4 * g);
-                tv[dt] += *(const f32x4*)(a.part_dv + slot * D + 16 * dt + 4 * g);
+        for (int j = 0; j < 2; ++j) {
+            sk_[j] = a.dk_lr + row * D;
+            sv_[j] = a.dv_lr + row * D;
+            use[j] = j == 0 && lr;
+            if (!use[j] && lmask) {
+                const int l = __builtin_ctz(lmask);
+                lmask &= lmask - 1;
+                const size_t slot = level_slot(bh, a.Lv, l, N, ktok, 0);
+                sk_[j] = a.part_dk + slot * D;
+                sv_[j] = a.part_dv + slot * D;
+                use[j] = true;
             }
         }
+        lr = false;
+        f32x4 xk[2][DT], xv[2][DT];
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+            if (use[j])
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) {
+                    xk[j][dt] = *(const f32x4*)(sk_[j] + 16 * dt + 4 * g);
+                    xv[j][dt] = *(const f32x4*)(sv_[j] + 16 * dt + 4 * g);
+                }
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+            if (use[j])
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) {
+                    tk[dt] += xk[j][dt];
+                    tv[dt] += xv[j][dt];
+                }
+        if (!lmask) break;
     }
     S* ok_ = (S*)a.dK + row * D;
     S* ov = (S*)a.dV + row * D;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            ok_[16 * dt + 4 * g + i] = T::store(tk[dt][i]);
-            ov[16 * dt + 4 * g + i] = T::store(tv[dt][i]);
-        }
+    for (int dt = 0; dt < DT; ++dt) {
+        store4<T>(ok_ + 16 * dt + 4 * g, tk[dt]);
+        store4<T>(ov + 16 * dt + 4 * g, tv[dt]);
+    }
 }
 
 // ------------------------------------------------------------------------
@@ -670,9 +731,7 @@ __global__ __launch_bounds__(BQ * 4, BQ == 64 ? 3 : 1) void sparse_bwd_block_ker
             } else {
                 const size_t row = bh * N + qtok;
                 const f32x4 v = dq[u] * a.tau + *(const f32x4*)(a.dq_lr + row * D + d0);
-                S* out = (S*)a.dQ + row * D + d0;
-#pragma unroll
-                for (int i = 0; i < 4; ++i) out[i] = T::store(v[i]);
+                store4<T>((S*)a.dQ + row * D + d0, v);
             }
         }
     }
@@ -690,13 +749,8 @@ __global__ __launch_bounds__(BQ * 4, BQ == 64 ? 3 : 1) void sparse_bwd_block_ker
             const size_t row = bh * N + ktok;
             const f32x4 vk = akT[dt] * a.tau + *(const f32x4*)(a.dk_lr + row * D + d0);
             const f32x4 vv = avT[dt] + *(const f32x4*)(a.dv_lr + row * D + d0);
-            S* ok = (S*)a.dK + row * D + d0;
-            S* ov = (S*)a.dV + row * D + d0;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                ok[i] = T::store(vk[i]);
-                ov[i] = T::store(vv[i]);
-            }
+            store4<T>((S*)a.dK + row * D + d0, vk);
+            store4<T>((S*)a.dV + row * D + d0, vv);
         }
     }
 }

@@ -240,27 +240,49 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
         return;
     }
 
-    if (MODE == kLeaf) {
-        // merge the partial of every level whose future half holds this leaf
+    if (MODE == kLeaf && qtok >= 0) {
+        // merge the partial of every level whose future half holds this leaf,
+        // in level order; the partials are fetched two levels at a time so
+        // their loads are in flight together
         const int lbeg = (tile / a.lt.per_leaf) * a.n_leaf;
-        for (int l = 0; l < a.Lv; ++l) {
-            const int hl = N >> (l + 1);
-            if (((lbeg / hl) & 1) == 0) continue;
-            if (qtok < 0) continue;
-            const int s2 = qtok / (2 * hl);
-            const size_t slot = (bh * a.Lv + l) * (size_t)(N / 2) + (size_t)s2 * hl +
-                                (qtok - s2 * 2 * hl - hl);
-            const float pl = a.part_lse[slot] * kLog2e;
-            const float m_new = fmaxf(m_run, pl);
-            const float c_old = fast_exp2(m_run - m_new), c_new = fast_exp2(pl - m_new);
-            const float* po = a.part_o + slot * D;
+        unsigned lmask = 0;
+        for (int l = 0; l < a.Lv; ++l)
+            if (((lbeg / (N >> (l + 1))) & 1) != 0) lmask |= 1u << l;
+        while (lmask) {
+            size_t slot[2];
+            bool use[2];
 #pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-                const f32x4 v = *(const f32x4*)(po + 16 * dt + 4 * g);
-                acc[dt] = acc[dt] * c_old + v * c_new;
+            for (int j = 0; j < 2; ++j) {
+                use[j] = lmask != 0;
+                slot[j] = 0;
+                if (use[j]) {
+                    const int l = __builtin_ctz(lmask);
+                    lmask &= lmask - 1;
+                    const int hl = N >> (l + 1);
+                    const int s2 = qtok / (2 * hl);
+                    slot[j] = (bh * a.Lv + l) * (size_t)(N / 2) + (size_t)s2 * hl + (qtok - s2 * 2 * hl - hl);
+                }
             }
-            l_run = l_run * c_old + c_new;
-            m_run = m_new;
+            float pl[2];
+            f32x4 v[2][DT];
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                if (use[j]) {
+                    pl[j] = a.part_lse[slot[j]] * kLog2e;
+                    const float* po = a.part_o + slot[j] * D;
+#pragma unroll
+                    for (int dt = 0; dt < DT; ++dt) v[j][dt] = *(const f32x4*)(po + 16 * dt + 4 * g);
+                }
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                if (use[j]) {
+                    const float m_new = fmaxf(m_run, pl[j]);
+                    const float c_old = fast_exp2(m_run - m_new), c_new = fast_exp2(pl[j] - m_new);
+#pragma unroll
+                    for (int dt = 0; dt < DT; ++dt) acc[dt] = acc[dt] * c_old + v[j][dt] * c_new;
+                    l_run = l_run * c_old + c_new;
+                    m_run = m_new;
+                }
         }
     }
 
@@ -286,8 +308,7 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
         const f32x4 o_s = acc[dt] * inv_den;
         *(f32x4*)(os + c0) = o_s;
         const f32x4 o_l = *(const f32x4*)(olr + c0);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) out[c0 + i] = T::store(gs * mf * o_s[i] + gl * o_l[i]);
+        store4<T>(out + c0, o_s * (gs * mf) + o_l * gl);
     }
     if (g == 0) {
         a.lse[row] = lse_nat;
