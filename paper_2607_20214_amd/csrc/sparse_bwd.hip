@@ -600,22 +600,23 @@ __global__ __launch_bounds__(BQ * 4, BQ == 64 ? 3 : 1) void sparse_bwd_block_ker
             sc = a.rs[2 * a.BHN + row];
         }
     };
-    {
-        int ktk[PT];
-        uint4 rk[PT];
-#pragma unroll
-        for (int kt = 0; kt < NQT; ++kt) {
-#pragma unroll
-            for (int j = 0; j < PT; ++j) {
-                const int r = 64 * kt + TD::row_of(j);
-                ktk[j] = r < nv ? kl[r] : -1;
-            }
-            TD::load(K, ktk, rk);
-            TD::store(sk, rk, 64 * kt);
-        }
-    }
+    // every index first (K tile rows, this lane's key, query tile 0), then
+    // every row (K tile, V rows, Q / dO tile 0), so the block starts after
+    // two round trips to memory instead of one per dependent step
     const int kloc = 16 * w + col;                       // this lane's key within the block
+    int ktk[NQT][PT];
+#pragma unroll
+    for (int kt = 0; kt < NQT; ++kt)
+#pragma unroll
+        for (int j = 0; j < PT; ++j) {
+            const int r = 64 * kt + TD::row_of(j);
+            ktk[kt][j] = r < nv ? kl[r] : -1;
+        }
     const int ktok = kloc < nv ? kl[kloc] : -1;
+    qtokens(0);
+    uint4 rk[NQT][PT];
+#pragma unroll
+    for (int kt = 0; kt < NQT; ++kt) TD::load(K, ktk[kt], rk[kt]);
     F vf[KS];
     {
         float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
@@ -625,8 +626,9 @@ __global__ __launch_bounds__(BQ * 4, BQ == 64 ? 3 : 1) void sparse_bwd_block_ker
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) vf[ks] = T::ld8(V + (size_t)ktok * D + 32 * ks + 8 * g);
     }
-    qtokens(0);
     qload();
+#pragma unroll
+    for (int kt = 0; kt < NQT; ++kt) TD::store(sk, rk[kt], 64 * kt);
     // (this lane's K row is read from the block's K tile when needed)
 
     f32x4 akT[DT], avT[DT];                              // rows d = 16 dt + 4 g + i, column = this key
