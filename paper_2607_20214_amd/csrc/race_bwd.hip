@@ -98,23 +98,27 @@ __device__ __forceinline__ void du_times_w(const typename T::store_t (*du)[w_kdi
     constexpr int DT = D / 16, WK = w_kdim<RP>(), KP = WK / 32;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int g = lane >> 4, col = lane & 15;
+    constexpr int NDW = DT / 4;            // d-tiles of this wave
+    F wh[NDW][KP], wl[NDW][KP];
 #pragma unroll
-    for (int dt = w; dt < DT; dt += 4) {
-        F wh[KP], wl[KP];
+    for (int u = 0; u < NDW; ++u)          // every W' piece of the wave first
 #pragma unroll
         for (int kp = 0; kp < KP; ++kp) {
-            const size_t o = (size_t)(16 * dt + col) * WK + 32 * kp + 8 * g;
-            wh[kp] = T::ld8(wth + o);
-            if (T::kSplit) wl[kp] = T::ld8(wtl + o);
+            const size_t o = (size_t)(16 * (w + 4 * u) + col) * WK + 32 * kp + 8 * g;
+            wh[u][kp] = T::ld8(wth + o);
+            if (T::kSplit) wl[u][kp] = T::ld8(wtl + o);
         }
+#pragma unroll
+    for (int u = 0; u < NDW; ++u) {
+        const int dt = w + 4 * u;
 #pragma unroll
         for (int tt = 0; tt < 4; ++tt) {
             f32x4 acc = {0, 0, 0, 0};
 #pragma unroll
             for (int kp = 0; kp < KP; ++kp) {
                 const F df = T::ld8(&du[16 * tt + col][32 * kp + 8 * g]);
-                acc = T::mma(wh[kp], df, acc);
-                if (T::kSplit) acc = T::mma(wl[kp], df, acc);
+                acc = T::mma(wh[u][kp], df, acc);
+                if (T::kSplit) acc = T::mma(wl[u][kp], df, acc);
             }
             const int tok = t0 + 16 * tt + col;
             if (tok < N) *(f32x4*)(out + (size_t)tok * D + 16 * dt + 4 * g) = acc;

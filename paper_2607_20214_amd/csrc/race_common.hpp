@@ -84,8 +84,10 @@ __device__ __forceinline__ void add_chunk_sums(const typename T::store_t (*xt)[k
 // projection count padded to whole 32-wide k-steps (backward du x W)
 template <int RP> constexpr int w_kdim() { return RP / 4 < 32 ? 32 : RP / 4; }
 
-// Rows [t0, t0 + 64) of X (zero past N), each multiplied by scale[row] when
-// scale != nullptr, into a transposed tile xt[d][token].
+// Rows [t0, t0 + 64) of X (zero past N), each multiplied by scale[row] * mul
+// when scale != nullptr (by mul otherwise), into a transposed tile
+// xt[d][token].  Every load of the thread is issued before the first LDS
+// store, so staging costs one round trip to memory.
 template <class T, int D>
 __device__ void stage_t(typename T::store_t (*xt)[kC + kPad], const typename T::store_t* X,
                         int t0, int N, const float* scale = nullptr, float mul = 1.f)
@@ -93,31 +95,42 @@ __device__ void stage_t(typename T::store_t (*xt)[kC + kPad], const typename T::
     using S = typename T::store_t;
     constexpr int PER = 16 / T::bytes;
     constexpr int CH = D / PER;
-    for (int it = threadIdx.x; it < (kC / 2) * CH; it += kThreads) {
+    constexpr int ITEMS = (kC / 2) * CH, PT = ITEMS / kThreads;
+    static_assert(ITEMS % kThreads == 0, "staging split");
+    uint4 va[PT], vb[PT];
+    float sa[PT], sb[PT];
+#pragma unroll
+    for (int j = 0; j < PT; ++j) {
+        const int it = threadIdx.x + j * kThreads;
         const int p = it & (kC / 2 - 1), c = it / (kC / 2);
         const int r0 = t0 + 2 * p, r1 = r0 + 1;
-        uint4 a = make_uint4(0, 0, 0, 0), b = make_uint4(0, 0, 0, 0);
-        if (r0 < N) a = ldg16(X + (size_t)r0 * D + c * PER);
-        if (r1 < N) b = ldg16(X + (size_t)r1 * D + c * PER);
-        const S* ea = (const S*)&a;
-        const S* eb = (const S*)&b;
-        const float s0 = (scale && r0 < N) ? scale[r0] * mul : mul;
-        const float s1 = (scale && r1 < N) ? scale[r1] * mul : mul;
+        va[j] = r0 < N ? ldg16(X + (size_t)r0 * D + c * PER) : make_uint4(0, 0, 0, 0);
+        vb[j] = r1 < N ? ldg16(X + (size_t)r1 * D + c * PER) : make_uint4(0, 0, 0, 0);
+        sa[j] = (scale && r0 < N) ? scale[r0] * mul : mul;
+        sb[j] = (scale && r1 < N) ? scale[r1] * mul : mul;
+    }
 #pragma unroll
-        for (int j = 0; j < PER; ++j) {
-            S* dst = &xt[c * PER + j][2 * p];
+    for (int j = 0; j < PT; ++j) {
+        const int it = threadIdx.x + j * kThreads;
+        const int p = it & (kC / 2 - 1), c = it / (kC / 2);
+        const S* ea = (const S*)&va[j];
+        const S* eb = (const S*)&vb[j];
+#pragma unroll
+        for (int e = 0; e < PER; ++e) {
+            S* dst = &xt[c * PER + e][2 * p];
             if (scale || mul != 1.f) {
-                dst[0] = T::store(T::load(ea[j]) * s0);
-                dst[1] = T::store(T::load(eb[j]) * s1);
+                dst[0] = T::store(T::load(ea[e]) * sa[j]);
+                dst[1] = T::store(T::load(eb[e]) * sb[j]);
             } else {
-                dst[0] = ea[j];
-                dst[1] = eb[j];
+                dst[0] = ea[e];
+                dst[1] = eb[e];
             }
         }
     }
 }
 
-// Rows [t0, t0 + 64) of X (zero past N), optionally scaled per row, row-major.
+// Rows [t0, t0 + 64) of X (zero past N), optionally scaled per row, row-major;
+// all loads issued before the LDS stores.
 template <class T, int D>
 __device__ void stage_r(typename T::store_t (*x)[D + kPad], const typename T::store_t* X, int t0,
                         int N, const float* scale = nullptr)
@@ -125,18 +138,28 @@ __device__ void stage_r(typename T::store_t (*x)[D + kPad], const typename T::st
     using S = typename T::store_t;
     constexpr int PER = 16 / T::bytes;
     constexpr int CH = D / PER;
-    for (int it = threadIdx.x; it < kC * CH; it += kThreads) {
+    constexpr int ITEMS = kC * CH, PT = ITEMS / kThreads;
+    static_assert(ITEMS % kThreads == 0, "staging split");
+    uint4 v[PT];
+    float sc[PT];
+#pragma unroll
+    for (int j = 0; j < PT; ++j) {
+        const int it = threadIdx.x + j * kThreads;
         const int row = it % kC, c = it / kC;
         const int r = t0 + row;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (r < N) v = ldg16(X + (size_t)r * D + c * PER);
-        if (scale) {
-            const float s = r < N ? scale[r] : 0.f;
-            S* e = (S*)&v;
+        v[j] = r < N ? ldg16(X + (size_t)r * D + c * PER) : make_uint4(0, 0, 0, 0);
+        sc[j] = (scale && r < N) ? scale[r] : 0.f;
+    }
 #pragma unroll
-            for (int j = 0; j < PER; ++j) e[j] = T::store(T::load(e[j]) * s);
+    for (int j = 0; j < PT; ++j) {
+        const int it = threadIdx.x + j * kThreads;
+        const int row = it % kC, c = it / kC;
+        if (scale) {
+            S* e = (S*)&v[j];
+#pragma unroll
+            for (int q = 0; q < PER; ++q) e[q] = T::store(T::load(e[q]) * sc[j]);
         }
-        *(uint4*)&x[row][c * PER] = v;
+        *(uint4*)&x[row][c * PER] = v[j];
     }
 }
 
