@@ -86,47 +86,61 @@ template <int RP> constexpr int w_kdim() { return RP / 4 < 32 ? 32 : RP / 4; }
 
 // Rows [t0, t0 + 64) of X (zero past N), each multiplied by scale[row] * mul
 // when scale != nullptr (by mul otherwise), into a transposed tile
-// xt[d][token].  Every load of the thread is issued before the first LDS
-// store, so staging costs one round trip to memory.
+// xt[d][token].  load() issues every global load of the thread into
+// registers and store() writes them to LDS, so a caller can load the next
+// chunk while the current one is consumed; stage_t does both at once.
+template <class T, int D>
+struct StageT {
+    using S = typename T::store_t;
+    static constexpr int PER = 16 / T::bytes;
+    static constexpr int CH = D / PER;
+    static constexpr int ITEMS = (kC / 2) * CH, PT = ITEMS / kThreads;
+    static_assert(ITEMS % kThreads == 0, "staging split");
+    uint4 va[PT], vb[PT];
+    float sa[PT], sb[PT];
+    __device__ __forceinline__ void load(const S* X, int t0, int N, const float* scale, float mul)
+    {
+#pragma unroll
+        for (int j = 0; j < PT; ++j) {
+            const int it = threadIdx.x + j * kThreads;
+            const int p = it & (kC / 2 - 1), c = it / (kC / 2);
+            const int r0 = t0 + 2 * p, r1 = r0 + 1;
+            va[j] = r0 < N ? ldg16(X + (size_t)r0 * D + c * PER) : make_uint4(0, 0, 0, 0);
+            vb[j] = r1 < N ? ldg16(X + (size_t)r1 * D + c * PER) : make_uint4(0, 0, 0, 0);
+            sa[j] = (scale && r0 < N) ? scale[r0] * mul : mul;
+            sb[j] = (scale && r1 < N) ? scale[r1] * mul : mul;
+        }
+    }
+    __device__ __forceinline__ void store(S (*xt)[kC + kPad], bool scaled) const
+    {
+#pragma unroll
+        for (int j = 0; j < PT; ++j) {
+            const int it = threadIdx.x + j * kThreads;
+            const int p = it & (kC / 2 - 1), c = it / (kC / 2);
+            const S* ea = (const S*)&va[j];
+            const S* eb = (const S*)&vb[j];
+#pragma unroll
+            for (int e = 0; e < PER; ++e) {
+                S* dst = &xt[c * PER + e][2 * p];
+                if (scaled) {
+                    dst[0] = T::store(T::load(ea[e]) * sa[j]);
+                    dst[1] = T::store(T::load(eb[e]) * sb[j]);
+                } else {
+                    dst[0] = ea[e];
+                    dst[1] = eb[e];
+                }
+            }
+        }
+    }
+};
+
 template <class T, int D>
 __device__ void stage_t(typename T::store_t (*xt)[kC + kPad], const typename T::store_t* X,
                         int t0, int N, const float* scale = nullptr, float mul = 1.f)
 {
-    using S = typename T::store_t;
-    constexpr int PER = 16 / T::bytes;
-    constexpr int CH = D / PER;
-    constexpr int ITEMS = (kC / 2) * CH, PT = ITEMS / kThreads;
-    static_assert(ITEMS % kThreads == 0, "staging split");
-    uint4 va[PT], vb[PT];
-    float sa[PT], sb[PT];
-#pragma unroll
-    for (int j = 0; j < PT; ++j) {
-        const int it = threadIdx.x + j * kThreads;
-        const int p = it & (kC / 2 - 1), c = it / (kC / 2);
-        const int r0 = t0 + 2 * p, r1 = r0 + 1;
-        va[j] = r0 < N ? ldg16(X + (size_t)r0 * D + c * PER) : make_uint4(0, 0, 0, 0);
-        vb[j] = r1 < N ? ldg16(X + (size_t)r1 * D + c * PER) : make_uint4(0, 0, 0, 0);
-        sa[j] = (scale && r0 < N) ? scale[r0] * mul : mul;
-        sb[j] = (scale && r1 < N) ? scale[r1] * mul : mul;
-    }
-#pragma unroll
-    for (int j = 0; j < PT; ++j) {
-        const int it = threadIdx.x + j * kThreads;
-        const int p = it & (kC / 2 - 1), c = it / (kC / 2);
-        const S* ea = (const S*)&va[j];
-        const S* eb = (const S*)&vb[j];
-#pragma unroll
-        for (int e = 0; e < PER; ++e) {
-            S* dst = &xt[c * PER + e][2 * p];
-            if (scale || mul != 1.f) {
-                dst[0] = T::store(T::load(ea[e]) * sa[j]);
-                dst[1] = T::store(T::load(eb[e]) * sb[j]);
-            } else {
-                dst[0] = ea[e];
-                dst[1] = eb[e];
-            }
-        }
-    }
+    StageT<T, D> st;
+    st.load(X, t0, N, scale, mul);
+    st.store(xt, scale || mul != 1.f);
 }
 
 // Rows [t0, t0 + 64) of X (zero past N), optionally scaled per row, row-major;
