@@ -188,15 +188,20 @@ constexpr int kSortThreads = 256;
 constexpr int kSortWaves = kSortThreads / kWave;
 constexpr int kKeyCache = 16384;       // keys of a list staged in LDS (longer lists read the rest from HBM)
 
+// One workgroup per list.  The list is cut into one contiguous quarter per
+// wave.  A histogram of every quarter gives each wave, for every bucket, the
+// output position of its first element of that bucket (all smaller buckets,
+// then the same bucket in earlier quarters); each wave then ranks its
+// quarter 64 keys at a time (lanes of equal key found by ballots over the
+// key bits) with no further synchronisation, so equal keys keep their index
+// order within the whole list.
 __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint8_t* __restrict__ keyq,
                                                             const uint8_t* __restrict__ keyk,
                                                             int32_t* __restrict__ perm_q,
                                                             int32_t* __restrict__ perm_k, int H,
                                                             int N, int causal, int Lv, int bits)
 {
-    __shared__ int hist[256];
-    __shared__ int base[256];
-    __shared__ int cnt[kSortWaves][256];
+    __shared__ int hist[kSortWaves][256];   // per quarter; then its running output positions
     __shared__ uint8_t kc[kKeyCache];
     const int h = blockIdx.y, b = blockIdx.z;
     const int task = blockIdx.x;
@@ -225,63 +230,78 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint8_t* __res
     }
     const uint8_t* key = (is_k ? keyk : keyq) + bh * N + start;
     int32_t* out = (is_k ? perm_k : perm_q) + out_off;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+    const int quarter = (len + kSortWaves - 1) / kSortWaves;
+    const int qbeg = min(len, wave * quarter), qend = min(len, qbeg + quarter);
 
-    for (int i = threadIdx.x; i < nb; i += kSortThreads) hist[i] = 0;
+    for (int i = threadIdx.x; i < kSortWaves * 256; i += kSortThreads) (&hist[0][0])[i] = 0;
     __syncthreads();
-    // histogram; the first kKeyCache keys are staged in LDS on the way, eight
-    // loads per thread in flight at a time
-    const int ncache = min(len, kKeyCache);
-    for (int i0 = 0; i0 < ncache; i0 += 8 * kSortThreads) {
+    // the quarter's histogram; the first kKeyCache keys of the list are staged
+    // in LDS on the way, eight loads per lane in flight at a time
+    for (int i0 = qbeg; i0 < qend; i0 += 8 * kWave) {
         uint8_t v[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            const int i = i0 + j * kSortThreads + threadIdx.x;
-            v[j] = i < ncache ? key[i] : 0;
+            const int i = i0 + j * kWave + lane;
+            v[j] = i < qend ? key[i] : 0;
         }
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            const int i = i0 + j * kSortThreads + threadIdx.x;
-            if (i < ncache) {
-                kc[i] = v[j];
-                atomicAdd(&hist[v[j]], 1);
+            const int i = i0 + j * kWave + lane;
+            if (i < qend) {
+                if (i < kKeyCache) kc[i] = v[j];
+                atomicAdd(&hist[wave][v[j]], 1);
             }
         }
     }
-    for (int i = ncache + threadIdx.x; i < len; i += kSortThreads) atomicAdd(&hist[key[i]], 1);
     __syncthreads();
-    if (threadIdx.x == 0) {
-        int acc = 0;
-        for (int i = 0; i < nb; ++i) { base[i] = acc; acc += hist[i]; }
+    // first output position of bucket c in quarter w: all keys < c, then key c
+    // in quarters before w (one wave scans the buckets, 64 at a time)
+    if (wave == 0) {
+        int carry = 0;
+        for (int c0 = 0; c0 < nb; c0 += kWave) {
+            const int c = c0 + lane;
+            int cnt[kSortWaves], tot = 0;
+#pragma unroll
+            for (int w = 0; w < kSortWaves; ++w) {
+                cnt[w] = c < nb ? hist[w][c] : 0;
+                tot += cnt[w];
+            }
+            int incl = tot;                                  // inclusive scan over the lanes
+#pragma unroll
+            for (int d = 1; d < kWave; d <<= 1) {
+                const int y = __shfl_up(incl, d);
+                if (lane >= d) incl += y;
+            }
+            int pos = carry + incl - tot;
+            if (c < nb)
+#pragma unroll
+                for (int w = 0; w < kSortWaves; ++w) {
+                    hist[w][c] = pos;
+                    pos += cnt[w];
+                }
+            carry += __shfl(incl, kWave - 1);
+        }
     }
-    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    __syncthreads();
+    // rank the quarter, 64 keys per step; hist[wave][c] is the next output
+    // position of bucket c in this quarter
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
-    for (int c0 = 0; c0 < len; c0 += kSortThreads) {
-        for (int i = threadIdx.x; i < kSortWaves * nb; i += kSortThreads) cnt[i / nb][i % nb] = 0;
-        __syncthreads();
-        const int i = c0 + threadIdx.x;
-        const bool valid = i < len;
-        const int kk = valid ? (i < ncache ? kc[i] : key[i]) : 0;
-        // lanes of this wave holding the same key
+    for (int i0 = qbeg; i0 < qend; i0 += kWave) {
+        const int i = i0 + lane;
+        const bool valid = i < qend;
+        const int kk = valid ? (i < kKeyCache ? kc[i] : key[i]) : 0;
         uint64_t same = __ballot(valid);
         for (int bit = 0; bit < bits; ++bit) {
-            uint64_t ones = __ballot(valid && ((kk >> bit) & 1));
+            const uint64_t ones = __ballot(valid && ((kk >> bit) & 1));
             same &= ((kk >> bit) & 1) ? ones : ~ones;
         }
-        const int rank_in_wave = __popcll(same & lt);
-        if (valid && rank_in_wave == 0) cnt[wave][kk] = __popcll(same);
-        __syncthreads();
-        if (valid) {
-            int pos = base[kk] + rank_in_wave;
-            for (int w = 0; w < wave; ++w) pos += cnt[w][kk];
-            out[pos] = start + i;
-        }
-        __syncthreads();
-        for (int k2 = threadIdx.x; k2 < nb; k2 += kSortThreads) {
-            int add = 0;
-            for (int w = 0; w < kSortWaves; ++w) add += cnt[w][k2];
-            base[k2] += add;
-        }
-        __syncthreads();
+        const int rank = __popcll(same & lt);
+        const int pos = valid ? hist[wave][kk] + rank : 0;
+        __builtin_amdgcn_wave_barrier();                     // every lane has read before the leaders advance
+        if (valid) out[pos] = start + i;
+        if (valid && rank == 0) hist[wave][kk] += __popcll(same);
     }
 }
 
