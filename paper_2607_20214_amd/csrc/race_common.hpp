@@ -144,37 +144,50 @@ __device__ void stage_t(typename T::store_t (*xt)[kC + kPad], const typename T::
 }
 
 // Rows [t0, t0 + 64) of X (zero past N), optionally scaled per row, row-major;
-// all loads issued before the LDS stores.
+// load() / store() as in StageT, stage_r does both.
+template <class T, int D>
+struct StageR {
+    using S = typename T::store_t;
+    static constexpr int PER = 16 / T::bytes;
+    static constexpr int CH = D / PER;
+    static constexpr int ITEMS = kC * CH, PT = ITEMS / kThreads;
+    static_assert(ITEMS % kThreads == 0, "staging split");
+    uint4 v[PT];
+    float sc[PT];
+    __device__ __forceinline__ void load(const S* X, int t0, int N, const float* scale)
+    {
+#pragma unroll
+        for (int j = 0; j < PT; ++j) {
+            const int it = threadIdx.x + j * kThreads;
+            const int row = it % kC, c = it / kC;
+            const int r = t0 + row;
+            v[j] = r < N ? ldg16(X + (size_t)r * D + c * PER) : make_uint4(0, 0, 0, 0);
+            sc[j] = (scale && r < N) ? scale[r] : 0.f;
+        }
+    }
+    __device__ __forceinline__ void store(S (*x)[D + kPad], bool scaled)
+    {
+#pragma unroll
+        for (int j = 0; j < PT; ++j) {
+            const int it = threadIdx.x + j * kThreads;
+            const int row = it % kC, c = it / kC;
+            if (scaled) {
+                S* e = (S*)&v[j];
+#pragma unroll
+                for (int q = 0; q < PER; ++q) e[q] = T::store(T::load(e[q]) * sc[j]);
+            }
+            *(uint4*)&x[row][c * PER] = v[j];
+        }
+    }
+};
+
 template <class T, int D>
 __device__ void stage_r(typename T::store_t (*x)[D + kPad], const typename T::store_t* X, int t0,
                         int N, const float* scale = nullptr)
 {
-    using S = typename T::store_t;
-    constexpr int PER = 16 / T::bytes;
-    constexpr int CH = D / PER;
-    constexpr int ITEMS = kC * CH, PT = ITEMS / kThreads;
-    static_assert(ITEMS % kThreads == 0, "staging split");
-    uint4 v[PT];
-    float sc[PT];
-#pragma unroll
-    for (int j = 0; j < PT; ++j) {
-        const int it = threadIdx.x + j * kThreads;
-        const int row = it % kC, c = it / kC;
-        const int r = t0 + row;
-        v[j] = r < N ? ldg16(X + (size_t)r * D + c * PER) : make_uint4(0, 0, 0, 0);
-        sc[j] = (scale && r < N) ? scale[r] : 0.f;
-    }
-#pragma unroll
-    for (int j = 0; j < PT; ++j) {
-        const int it = threadIdx.x + j * kThreads;
-        const int row = it % kC, c = it / kC;
-        if (scale) {
-            S* e = (S*)&v[j];
-#pragma unroll
-            for (int q = 0; q < PER; ++q) e[q] = T::store(T::load(e[q]) * sc[j]);
-        }
-        *(uint4*)&x[row][c * PER] = v[j];
-    }
+    StageR<T, D> st;
+    st.load(X, t0, N, scale);
+    st.store(x, scale != nullptr);
 }
 
 // Projections u of the tables this lane handles for chunk tokens

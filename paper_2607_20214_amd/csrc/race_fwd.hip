@@ -82,23 +82,24 @@ __global__ __launch_bounds__(kThreads) void race_state_kernel(StateArgs a)
         for (int j = 0; j < DW; ++j) S[ft][j] = f32x4{0, 0, 0, 0};
 
     const int t_beg = seg * a.seg_len, t_end = min(a.N, t_beg + a.seg_len);
-    URegs<RP> ur;                        // projections and value rows of the chunk, loaded one chunk ahead
+    // projections, value rows and A weights of the chunk, loaded one chunk ahead
+    URegs<RP> ur;
     StageT<T, D> vr;
-    ur.load(U, t_beg, a.N);
-    vr.load(Vl, t_beg, a.N, vs, 1.f);
+    float awv = 0.f;
+    auto load_chunk = [&](int c0) {
+        ur.load(U, c0, a.N);
+        vr.load(Vl, c0, a.N, vs, 1.f);
+        const int r = c0 + threadIdx.x;
+        awv = (threadIdx.x < kC && r < a.N) ? (aw ? aw[r] : 1.f) : 0.f;
+    };
+    load_chunk(t_beg);
     for (int t0 = t_beg; t0 < t_end; t0 += kC) {
         __syncthreads();
         vr.store(sm.vt, vs != nullptr);
-        if (threadIdx.x < kC) {
-            const int r = t0 + threadIdx.x;
-            sm.aw[threadIdx.x] = (r < a.N) ? (aw ? aw[r] : 1.f) : 0.f;
-        }
+        if (threadIdx.x < kC) sm.aw[threadIdx.x] = awv;
         features_from<T, RP>(ur, t0, a.N, a.L, a.two_beta, nullptr, sm.pht, nullptr);
         __syncthreads();
-        if (t0 + kC < t_end) {
-            ur.load(U, t0 + kC, a.N);
-            vr.load(Vl, t0 + kC, a.N, vs, 1.f);
-        }
+        if (t0 + kC < t_end) load_chunk(t0 + kC);
         // S[f][cols of wave] += Phi'[f][rows] V[rows][cols]
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
