@@ -46,7 +46,8 @@ def kernel_model(w, Lv: int, rules_G: int = 0, rules_lam: bool = False, rules_pa
     seg_states = 0                 # RACE segment states are reported with race_state/scan
     half = N // 2
     m = {}
-    m["project"] = (bh * N * (D * s + 1 + P * 4), bh * N * 2 * D * (gs + P))
+    # one launch hashes and projects both Q and K
+    m["project"] = (2 * bh * N * (D * s + 1 + P * 4), 2 * bh * N * 2 * D * (gs + P))
     m["sort"] = (bh * (Lv if w.causal else 2) * N * 5, 0)
     # RACE: features, chunk states (r x d per 64-token chunk), readout
     C = 64

@@ -344,8 +344,8 @@ int elsaa_select(const elsaa_config* cfg, const void* Q, const void* K, const fl
     uint8_t* kq = at<uint8_t>(workspace, W.keyq);
     uint8_t* kk = at<uint8_t>(workspace, W.keyk);
     hipError_t e;
-    if ((e = launch_project(s, Q, W_sort, nullptr, kq, nullptr, stream)) != hipSuccess) return hip_fail(e, "hash(Q)");
-    if ((e = launch_project(s, K, W_sort, nullptr, kk, nullptr, stream)) != hipSuccess) return hip_fail(e, "hash(K)");
+    if ((e = launch_project(s, Q, K, W_sort, nullptr, kq, kk, nullptr, nullptr, stream)) != hipSuccess)
+        return hip_fail(e, "hash");
     if ((e = launch_sort(s, kq, kk, perm_q, perm_k, stream)) != hipSuccess) return hip_fail(e, "sort");
     return ELSAA_OK;
 }
@@ -379,8 +379,8 @@ int elsaa_fwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     float* uq = at<float>(saved, SL.u_q);
     float* uk = at<float>(saved, SL.u_k);
     hipError_t e;
-    if ((e = launch_project(s, Q, W_sort, W_race, kq, uq, stream)) != hipSuccess) return hip_fail(e, "project(Q)");
-    if ((e = launch_project(s, K, W_sort, W_race, kk, uk, stream)) != hipSuccess) return hip_fail(e, "project(K)");
+    if ((e = launch_project(s, Q, K, W_sort, W_race, kq, kk, uq, uk, stream)) != hipSuccess)
+        return hip_fail(e, "project");
     float* part_o = at<float>(workspace, W.part_o);
     float* part_lse = at<float>(workspace, W.part_lse);
     // selection and the causal levels on the side stream, the low-rank branch

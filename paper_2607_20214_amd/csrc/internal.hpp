@@ -51,8 +51,10 @@ private:
 
 // selection: hash keys (and the RACE projections U = W_race x when W_race
 // is not null, [BH][N][race_proj_stride]) then per-segment stable counting sort
-hipError_t launch_project(const Shape& s, const void* X, const float* W_sort, const float* W_race,
-                          uint8_t* keys, float* U, hipStream_t st);
+// (Q and K in one launch)
+hipError_t launch_project(const Shape& s, const void* Q, const void* K, const float* W_sort,
+                          const float* W_race, uint8_t* keyq, uint8_t* keyk, float* Uq, float* Uk,
+                          hipStream_t st);
 hipError_t launch_sort(const Shape& s, const uint8_t* keyq, const uint8_t* keyk, int32_t* perm_q,
                        int32_t* perm_k, hipStream_t st);
 

@@ -37,12 +37,16 @@ struct ProjSmem {
     uint32_t code[kProjRows];
 };
 
+// One launch covers Q and K: grid.z runs over 2B, the second half being K.
+struct ProjIO {
+    const void* X[2];     // Q rows, K rows
+    uint8_t* keys[2];
+    float* U[2];          // RACE projections (ignored when Wrace is null)
+};
+
 template <class T, int D, int WR>
-__global__ __launch_bounds__(kProjThreads) void proj_kernel(const typename T::store_t* __restrict__ X,
-                                                            const float* __restrict__ Wsort,
-                                                            const float* __restrict__ Wrace,
-                                                            uint8_t* __restrict__ keys,
-                                                            float* __restrict__ U, int H, int N,
+__global__ __launch_bounds__(kProjThreads) void proj_kernel(ProjIO io, const float* __restrict__ Wsort,
+                                                            const float* __restrict__ Wrace, int B, int H, int N,
                                                             int bits, int L, int UP, int chunk_rows)
 {
     using S = typename T::store_t;
@@ -52,11 +56,13 @@ __global__ __launch_bounds__(kProjThreads) void proj_kernel(const typename T::st
     constexpr int KS = D / 32;
     constexpr int PT = kProjRows * CH / kProjThreads;   // pieces staged per thread
     __shared__ ProjSmem<T, D, WR> sm;
-    const int h = blockIdx.y, b = blockIdx.z;
+    const int h = blockIdx.y, which = blockIdx.z >= B, b = blockIdx.z - (which ? B : 0);
     const size_t bh = (size_t)b * H + h;
     const int rbeg = blockIdx.x * chunk_rows;
     const int rend = min(N, rbeg + chunk_rows);
-    const S* Xh = X + bh * N * D;
+    const S* Xh = (const S*)io.X[which] + bh * N * D;
+    uint8_t* __restrict__ keys = io.keys[which];
+    float* __restrict__ U = io.U[which];
     const int lane = threadIdx.x & 63;
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 
@@ -72,12 +78,25 @@ __global__ __launch_bounds__(kProjThreads) void proj_kernel(const typename T::st
     };
     load(rbeg);
     if (Wrace) {
-        for (int it = threadIdx.x; it < WR * D; it += kProjThreads) {
-            const int row = it / D, c = it % D;
-            const float wv = row < 4 * L ? Wrace[((size_t)h * L * 4 + row) * D + c] : 0.f;
-            const S hi = T::store(wv);
-            sm.whi[row][c] = hi;
-            if (T::bytes == 2) sm.wlo[row][c] = T::store(wv - T::load(hi));
+        // W staged up to eight loads per thread at a time (one round trip each)
+        constexpr int PW = (WR * D) / kProjThreads < 8 ? (WR * D) / kProjThreads : 8;
+        static_assert(PW >= 1 && (WR * D) % (PW * kProjThreads) == 0, "W staging split");
+        for (int it0 = 0; it0 < WR * D; it0 += PW * kProjThreads) {
+            float wv[PW];
+#pragma unroll
+            for (int j = 0; j < PW; ++j) {
+                const int it = it0 + j * kProjThreads + threadIdx.x;
+                const int row = it / D, c = it % D;
+                wv[j] = row < 4 * L ? Wrace[((size_t)h * L * 4 + row) * D + c] : 0.f;
+            }
+#pragma unroll
+            for (int j = 0; j < PW; ++j) {
+                const int it = it0 + j * kProjThreads + threadIdx.x;
+                const int row = it / D, c = it % D;
+                const S hi = T::store(wv[j]);
+                sm.whi[row][c] = hi;
+                if (T::bytes == 2) sm.wlo[row][c] = T::store(wv[j] - T::load(hi));
+            }
         }
     }
     const float* ws_h = Wsort + (size_t)h * bits * D;
@@ -143,22 +162,21 @@ __global__ __launch_bounds__(kProjThreads) void proj_kernel(const typename T::st
 }
 
 template <class T, int D>
-hipError_t launch_proj_t(const Shape& s, const void* X, const float* W_sort, const float* W_race,
-                         uint8_t* keys, float* U, hipStream_t st)
+hipError_t launch_proj_t(const Shape& s, const ProjIO& io, const float* W_sort, const float* W_race, hipStream_t st)
 {
+    // about kProjTarget workgroups for both tensors together
     const int64_t tiles = (s.N + kProjRows - 1) / kProjRows;
-    const int64_t bh = (int64_t)s.B * s.H;
-    int64_t want = (kProjTarget + bh - 1) / bh;
+    const int64_t lists = 2 * (int64_t)s.B * s.H;
+    int64_t want = (kProjTarget + lists - 1) / lists;
     if (want > tiles) want = tiles;
     const int64_t per = (tiles + want - 1) / want;
     const int chunk_rows = (int)(per * kProjRows);
-    dim3 grid((s.N + chunk_rows - 1) / chunk_rows, s.H, s.B);
+    dim3 grid((s.N + chunk_rows - 1) / chunk_rows, s.H, 2 * s.B);
     const int UP = race_proj_stride(s);
     const int wr = UP < 16 ? 16 : UP;
 #define ELSAA_PROJ(WR_)                                                                          \
-    ELSAA_LAUNCH("project", (proj_kernel<T, D, WR_>), grid, dim3(kProjThreads), 0, st,                 \
-                       (const typename T::store_t*)X, W_sort, W_race, keys, U, s.H, s.N,          \
-                       s.sort_bits, s.L, UP, chunk_rows)
+    ELSAA_LAUNCH("project", (proj_kernel<T, D, WR_>), grid, dim3(kProjThreads), 0, st, io, W_sort, W_race, \
+                 s.B, s.H, s.N, s.sort_bits, s.L, UP, chunk_rows)
     if (wr == 16) ELSAA_PROJ(16);
     else if (wr == 32) ELSAA_PROJ(32);
     else ELSAA_PROJ(64);
@@ -166,13 +184,21 @@ hipError_t launch_proj_t(const Shape& s, const void* X, const float* W_sort, con
     return hipGetLastError();
 }
 
-hipError_t launch_project(const Shape& s, const void* X, const float* W_sort, const float* W_race,
-                          uint8_t* keys, float* U, hipStream_t st)
+hipError_t launch_project(const Shape& s, const void* Q, const void* K, const float* W_sort,
+                          const float* W_race, uint8_t* keyq, uint8_t* keyk, float* Uq, float* Uk,
+                          hipStream_t st)
 {
-    if (s.bf16) return s.D == 64 ? launch_proj_t<BF16, 64>(s, X, W_sort, W_race, keys, U, st)
-                                 : launch_proj_t<BF16, 128>(s, X, W_sort, W_race, keys, U, st);
-    return s.D == 64 ? launch_proj_t<F32, 64>(s, X, W_sort, W_race, keys, U, st)
-                     : launch_proj_t<F32, 128>(s, X, W_sort, W_race, keys, U, st);
+    ProjIO io;
+    io.X[0] = Q;
+    io.X[1] = K;
+    io.keys[0] = keyq;
+    io.keys[1] = keyk;
+    io.U[0] = Uq;
+    io.U[1] = Uk;
+    if (s.bf16) return s.D == 64 ? launch_proj_t<BF16, 64>(s, io, W_sort, W_race, st)
+                                 : launch_proj_t<BF16, 128>(s, io, W_sort, W_race, st);
+    return s.D == 64 ? launch_proj_t<F32, 64>(s, io, W_sort, W_race, st)
+                     : launch_proj_t<F32, 128>(s, io, W_sort, W_race, st);
 }
 
 // --------------------------------------------------------------------------
