@@ -502,33 +502,31 @@ __global__ __launch_bounds__(kThreads, 2) void race_dv_kernel(LbArgs a)
             }
 #pragma unroll
             for (int kt = 0; kt < 4; ++kt) {
-                const F af = T::ld44(&sm.pk[16 * kt + col][32 * fs + 4 * g], &sm.pk[16 * kt + col][32 * fs + 16 + 4 * g]);
+                const F bf = T::ld44(&sm.pk[16 * kt + col][32 * fs + 4 * g], &sm.pk[16 * kt + col][32 * fs + 16 + 4 * g]);
 #pragma unroll
                 for (int j = 0; j < DW; ++j) {
-                    accs[kt][j] = T::mma(af, shi[j], accs[kt][j]);
-                    if (T::kSplit) accs[kt][j] = T::mma(af, slo[j], accs[kt][j]);
+                    accs[kt][j] = T::mma(shi[j], bf, accs[kt][j]);
+                    if (T::kSplit) accs[kt][j] = T::mma(slo[j], bf, accs[kt][j]);
                 }
             }
         }
+        // dV^T: lane (g, col) holds d = 16 (w DW + j) + 4 g + i of key 16 kt + col
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt) {
             f32x4 (&acc)[DW] = accs[kt];
             if (a.causal) {
 #pragma unroll
                 for (int kk = 0; kk < 2; ++kk) {
-                    const F af = T::ld8(&sm.mt[16 * kt + col][32 * kk + 8 * g]);
+                    const F bf = T::ld8(&sm.mt[16 * kt + col][32 * kk + 8 * g]);
 #pragma unroll
                     for (int j = 0; j < DW; ++j)
-                        acc[j] = T::mma(af, T::ld8(&sm.dnt[16 * (w * DW + j) + col][32 * kk + 8 * g]), acc[j]);
+                        acc[j] = T::mma(T::ld8(&sm.dnt[16 * (w * DW + j) + col][32 * kk + 8 * g]), bf, acc[j]);
                 }
             }
+            const int tok = t0 + 16 * kt + col;
+            if (tok < a.N)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int tok = t0 + 16 * kt + 4 * g + i;
-                if (tok >= a.N) continue;
-#pragma unroll
-                for (int j = 0; j < DW; ++j) out[(size_t)tok * D + 16 * (w * DW + j) + col] = acc[j][i];
-            }
+                for (int j = 0; j < DW; ++j) *(f32x4*)(out + (size_t)tok * D + 16 * (w * DW + j) + 4 * g) = acc[j];
         }
         if (a.causal) {
             // dS += Phi_Q' (dNum / L) (chunk)

@@ -251,9 +251,10 @@ __global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
             }
         }
         __syncthreads();
-        // Num for the wave's d columns, all 64 queries: inter-chunk part with S
-        // in float32 accuracy (hi / lo bf16 split made once per chunk), then
-        // the masked intra-chunk part
+        // Num^T for the wave's d columns, all 64 queries (lane (g, col) holds
+        // d = 16 (w DW + j) + 4 g + i of query 16 qt + col): inter-chunk part
+        // with S in float32 accuracy (hi / lo bf16 split made once per chunk),
+        // then the masked intra-chunk part
         f32x4 num[4][DW];
 #pragma unroll
         for (int qt = 0; qt < 4; ++qt)
@@ -278,8 +279,8 @@ __global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
                                      &sm.phq[16 * qt + col][32 * fs + 16 + 4 * g]);
 #pragma unroll
                 for (int j = 0; j < DW; ++j) {
-                    num[qt][j] = T::mma(af, shi[j], num[qt][j]);
-                    if (T::kSplit) num[qt][j] = T::mma(af, slo[j], num[qt][j]);
+                    num[qt][j] = T::mma(shi[j], af, num[qt][j]);
+                    if (T::kSplit) num[qt][j] = T::mma(slo[j], af, num[qt][j]);
                 }
             }
         }
@@ -290,21 +291,20 @@ __global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
             if (a.causal) {
 #pragma unroll
                 for (int kk = 0; kk < 2; ++kk) {
-                    const F af = T::ld8(&sm.mm[16 * qt + col][32 * kk + 8 * g]);
+                    const F bf = T::ld8(&sm.mm[16 * qt + col][32 * kk + 8 * g]);
 #pragma unroll
                     for (int j = 0; j < DW; ++j)
-                        num[qt][j] = T::mma(af, T::ld8(&sm.vt[16 * (w * DW + j) + col][32 * kk + 8 * g]), num[qt][j]);
+                        num[qt][j] = T::mma(T::ld8(&sm.vt[16 * (w * DW + j) + col][32 * kk + 8 * g]), bf, num[qt][j]);
                 }
             }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int ql = 16 * qt + 4 * g + i;
-                const int tok = t0 + ql;
-                if (tok >= a.N) continue;
+            const int ql = 16 * qt + col;
+            const int tok = t0 + ql;
+            if (tok < a.N) {
                 const float den = sm.den_a[ql] + (a.causal ? sm.den_b[ql] : 0.f);
                 const float inv = 1.f / (den + a.eps);
 #pragma unroll
-                for (int j = 0; j < DW; ++j) Olr[(size_t)tok * D + 16 * (w * DW + j) + col] = num[qt][j][i] * inv;
+                for (int j = 0; j < DW; ++j)
+                    *(f32x4*)(Olr + (size_t)tok * D + 16 * (w * DW + j) + 4 * g) = num[qt][j] * inv;
             }
         }
         if (threadIdx.x < kC && t0 + threadIdx.x < a.N)
