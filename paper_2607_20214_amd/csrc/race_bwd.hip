@@ -202,21 +202,24 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
             if (a.causal) uk.load(Uk, t0 + kC, a.N);
         }
         if (a.causal) {
-            // G rows [16w, 16w + 16): sc_lr,i <dO_i, V_j> + dDen_i for j <= i
+            // G rows [16w, 16w + 16): sc_lr,i <dO_i, V_j> + dDen_i for j <= i,
+            // formed transposed (lane (g, col): keys 16 kt + 4 g + i of query
+            // 16 w + col) so each lane stores four entries of its row at once
+            const int qi = 16 * w + col;
+            const float scq = sm.sc[qi], ddq = sm.dden[qi];
             for (int kt = 0; kt < 4; ++kt) {
                 f32x4 acc = {0, 0, 0, 0};
                 if (kt <= w) {
                     // V rows of keys 16 kt .. 16 kt + 15 from the transposed chunk tile
 #pragma unroll
                     for (int ks = 0; ks < KS; ++ks)
-                        acc = T::mma(T::ld8(&sm.dn[16 * w + col][32 * ks + 8 * g]),
-                                     col8_t<T, kC + kPad>(sm.vt, 32 * ks, 16 * kt), acc);
+                        acc = T::mma(col8_t<T, kC + kPad>(sm.vt, 32 * ks, 16 * kt),
+                                     T::ld8(&sm.dn[16 * w + col][32 * ks + 8 * g]), acc);
                 }
+                f32x4 v;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int qi = 16 * w + 4 * g + i, kj = 16 * kt + col;
-                    sm.gg[qi][kj] = T::store(kj <= qi ? acc[i] * sm.sc[qi] + sm.dden[qi] : 0.f);
-                }
+                for (int i = 0; i < 4; ++i) v[i] = 16 * kt + 4 * g + i <= qi ? acc[i] * scq + ddq : 0.f;
+                store4<T>(&sm.gg[qi][16 * kt + 4 * g], v);
             }
         }
         __syncthreads();
@@ -340,21 +343,24 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
             if (a.causal) uq.load(Uq, t0 - kC, a.N);
         }
         if (a.causal) {
-            // G' rows j in [16w, 16w + 16): (<V_j, dNum_i> + dDen_i) / L for i >= j
+            // G' rows j in [16w, 16w + 16): (<V_j, dNum_i> + dDen_i) / L for
+            // i >= j, formed transposed (lane (g, col): queries 16 it + 4 g + i
+            // of key 16 w + col) so each lane stores four entries of its row at once
+            const int kj = 16 * w + col;
             for (int it = 0; it < 4; ++it) {
                 f32x4 acc = {0, 0, 0, 0};
                 if (it >= w) {
                     // dNum / L rows of queries 16 it .. 16 it + 15 from the transposed chunk tile
 #pragma unroll
                     for (int ks = 0; ks < KS; ++ks)
-                        acc = T::mma(T::ld8(&sm.vr[16 * w + col][32 * ks + 8 * g]),
-                                     col8_t<T, kC + kPad>(sm.dnt, 32 * ks, 16 * it), acc);
+                        acc = T::mma(col8_t<T, kC + kPad>(sm.dnt, 32 * ks, 16 * it),
+                                     T::ld8(&sm.vr[16 * w + col][32 * ks + 8 * g]), acc);
                 }
+                const f32x4 dd = *(const f32x4*)&sm.dden[16 * it + 4 * g];
+                f32x4 v;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int kj = 16 * w + 4 * g + i, qi = 16 * it + col;
-                    sm.ggt[kj][qi] = T::store(qi >= kj ? acc[i] + sm.dden[qi] * a.inv_L : 0.f);
-                }
+                for (int i = 0; i < 4; ++i) v[i] = 16 * it + 4 * g + i >= kj ? acc[i] + dd[i] * a.inv_L : 0.f;
+                store4<T>(&sm.ggt[kj][16 * it + 4 * g], v);
             }
         }
         __syncthreads();
@@ -465,20 +471,22 @@ __global__ __launch_bounds__(kThreads, 2) void race_dv_kernel(LbArgs a)
             if (a.causal) uq.load(Uq, t0 - kC, a.N);
         }
         if (a.causal) {
-            // M' rows j in [16w, 16w + 16): <phi(k_j), phi(q_i)> for i >= j
+            // M' rows j in [16w, 16w + 16): <phi(k_j), phi(q_i)> for i >= j,
+            // formed transposed (lane (g, col): queries 16 it + 4 g + i of key
+            // 16 w + col) so each lane stores four entries of its row at once
+            const int kj = 16 * w + col;
             for (int it = 0; it < 4; ++it) {
                 f32x4 acc = {0, 0, 0, 0};
                 if (it >= w) {
 #pragma unroll
                     for (int fs = 0; fs < FS; ++fs)
-                        acc = T::mma(T::ld8(&sm.pk[16 * w + col][32 * fs + 8 * g]),
-                                     T::ld8(&sm.pq[16 * it + col][32 * fs + 8 * g]), acc);
+                        acc = T::mma(T::ld8(&sm.pq[16 * it + col][32 * fs + 8 * g]),
+                                     T::ld8(&sm.pk[16 * w + col][32 * fs + 8 * g]), acc);
                 }
+                f32x4 v;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int kj = 16 * w + 4 * g + i, qi = 16 * it + col;
-                    sm.mt[kj][qi] = T::store(qi >= kj ? acc[i] : 0.f);
-                }
+                for (int i = 0; i < 4; ++i) v[i] = 16 * it + 4 * g + i >= kj ? acc[i] : 0.f;
+                store4<T>(&sm.mt[kj][16 * it + 4 * g], v);
             }
         }
         __syncthreads();

@@ -219,36 +219,43 @@ __global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
         {
             const int q = threadIdx.x >> 2, part = threadIdx.x & 3;
             float s = 0.f;
-            for (int f = part * (RP / 4); f < (part + 1) * (RP / 4); ++f)
-                s += T::load(sm.phq[q][f]) * sm.a_state[f];
+#pragma unroll
+            for (int f0 = part * (RP / 4); f0 < (part + 1) * (RP / 4); f0 += 8) {
+                const auto ph = T::ld8(&sm.phq[q][f0]);
+                const f32x4 a0 = *(const f32x4*)&sm.a_state[f0], a1 = *(const f32x4*)&sm.a_state[f0 + 4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) s += (float)ph[j] * a0[j] + (float)ph[4 + j] * a1[j];
+            }
             s += __shfl_xor(s, 1);
             s += __shfl_xor(s, 2);
             if (part == 0) sm.den_a[q] = s * a.inv_L;
         }
-        // intra-chunk kernel matrix rows [16w, 16w + 16) (causal)
+        // intra-chunk kernel matrix rows [16w, 16w + 16) (causal), formed
+        // transposed: lane (g, col) holds keys 16 kt + 4 g + i of query
+        // 16 w + col, so a row's four entries leave in one store and its sum
+        // is in-lane plus one exchange over the lane groups
         if (a.causal) {
-            float rs[4] = {0, 0, 0, 0};
+            const int qi = 16 * w + col;
+            float rs = 0.f;
             for (int kt = 0; kt < 4; ++kt) {
                 f32x4 mt = {0, 0, 0, 0};
                 if (kt <= w) {
 #pragma unroll
                     for (int fs = 0; fs < FS; ++fs)
-                        mt = T::mma(T::ld8(&sm.phq[16 * w + col][32 * fs + 8 * g]),
-                                    T::ld8(&sm.phk[16 * kt + col][32 * fs + 8 * g]), mt);
+                        mt = T::mma(T::ld8(&sm.phk[16 * kt + col][32 * fs + 8 * g]),
+                                    T::ld8(&sm.phq[16 * w + col][32 * fs + 8 * g]), mt);
                 }
+                f32x4 v;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int qi = 16 * w + 4 * g + i, kj = 16 * kt + col;
-                    const float v = (kj <= qi) ? mt[i] * a.inv_L : 0.f;
-                    rs[i] += v;
-                    sm.mm[qi][kj] = T::store(v);
+                    const int kj = 16 * kt + 4 * g + i;
+                    v[i] = (kj <= qi) ? mt[i] * a.inv_L : 0.f;
+                    rs += v[i];
                 }
+                store4<T>(&sm.mm[qi][16 * kt + 4 * g], v);
             }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float s = row_sum16(rs[i]);
-                if (col == 0) sm.den_b[16 * w + 4 * g + i] = s;
-            }
+            rs = wave_sum16(rs);
+            if (g == 0) sm.den_b[qi] = rs;
         }
         __syncthreads();
         // Num^T for the wave's d columns, all 64 queries (lane (g, col) holds
