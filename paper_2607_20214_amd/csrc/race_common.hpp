@@ -111,6 +111,8 @@ struct StageT {
             sb[j] = (scale && r1 < N) ? scale[r1] * mul : mul;
         }
     }
+    // the two rows of an item are adjacent in the transposed tile: one
+    // store per element pair
     __device__ __forceinline__ void store(S (*xt)[kC + kPad], bool scaled) const
     {
 #pragma unroll
@@ -121,14 +123,16 @@ struct StageT {
             const S* eb = (const S*)&vb[j];
 #pragma unroll
             for (int e = 0; e < PER; ++e) {
-                S* dst = &xt[c * PER + e][2 * p];
+                S x0 = ea[e], x1 = eb[e];
                 if (scaled) {
-                    dst[0] = T::store(T::load(ea[e]) * sa[j]);
-                    dst[1] = T::store(T::load(eb[e]) * sb[j]);
-                } else {
-                    dst[0] = ea[e];
-                    dst[1] = eb[e];
+                    x0 = T::store(T::load(x0) * sa[j]);
+                    x1 = T::store(T::load(x1) * sb[j]);
                 }
+                S* dst = &xt[c * PER + e][2 * p];
+                if constexpr (T::bytes == 2)
+                    *(uint32_t*)dst = (uint32_t)x0 | ((uint32_t)x1 << 16);
+                else
+                    *(float2*)dst = make_float2(x0, x1);
             }
         }
     }
@@ -236,10 +240,7 @@ __device__ void features_from(const URegs<RP>& ur, int t0, int N, int L, float t
             t[i] = tanh_abs(u[i]);
             sigmoid_pair(two_beta * t[i], sp[i], sn[i]);
         }
-        if (ts) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) ts[tl][4 * tb + i] = t[i];
-        }
+        if (ts) *(f32x4*)&ts[tl][4 * tb] = f32x4{t[0], t[1], t[2], t[3]};
         float phi[16];
 #pragma unroll
         for (int c = 0; c < 16; ++c) {
@@ -248,8 +249,9 @@ __device__ void features_from(const URegs<RP>& ur, int t0, int N, int L, float t
             phi[c] = live ? v : 0.f;
         }
         if (ph) {
-#pragma unroll
-            for (int c = 0; c < 16; ++c) ph[tl][16 * tb + c] = T::store(phi[c]);
+            using F = typename T::frag_t;
+            *(F*)&ph[tl][16 * tb] = T::pack(phi);
+            *(F*)&ph[tl][16 * tb + 8] = T::pack(phi + 8);
         }
         if (pht) {
 #pragma unroll
