@@ -160,6 +160,17 @@ __device__ __forceinline__ LanePair xpair32(float v)
     return {__uint_as_float(r[0]), __uint_as_float(r[1])};
 }
 
+// out[r] = v of lane (l % 16) + 16 r, for every lane l (three exchanges).
+__device__ __forceinline__ void gather16x4(float v, float (&out)[4])
+{
+    const LanePair a = xpair16(v);                  // rows 2s, 2s + 1 of this lane's half s
+    const LanePair b0 = xpair32(a.lo), b1 = xpair32(a.hi);
+    out[0] = b0.lo;
+    out[1] = b1.lo;
+    out[2] = b0.hi;
+    out[3] = b1.hi;
+}
+
 __device__ __forceinline__ float wave_max16(float v)   // max over lanes l, l^16, l^32, l^48
 {
     const LanePair a = xpair16(v);

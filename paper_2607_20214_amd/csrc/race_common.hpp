@@ -287,13 +287,12 @@ __device__ __forceinline__ void chain_rule_t(f32x4 dphi, int qt, int tb, int L, 
     const int lane = threadIdx.x & 63;
     const int g = lane >> 4, col = lane & 15;
     const int row = 16 * qt + col;
-    const float two_beta = 2.f * beta;
-    float t[4], sp[4], sn[4];
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-        t[b] = ts[row][4 * tb + b];
-        sigmoid_pair(two_beta * t[b], sp[b], sn[b]);
-    }
+    // lane group g evaluates bit g's sigmoid pair; the groups then share them
+    const float tg = ts[row][4 * tb + g];
+    float spg, sng, sp[4], sn[4];
+    sigmoid_pair(2.f * beta * tg, spg, sng);
+    gather16x4(spg, sp);
+    gather16x4(sng, sn);
     // features c = 4g + i: bits 0, 1 from i, bits 2, 3 from g
     const float hi = ((g & 1) ? sp[2] : sn[2]) * ((g & 2) ? sp[3] : sn[3]);
     float p0 = 0.f, p1 = 0.f, p2 = 0.f;       // sums over i of x, x v_c0, x v_c1
@@ -314,10 +313,8 @@ __device__ __forceinline__ void chain_rule_t(f32x4 dphi, int qt, int tb, int L, 
     const float s0 = b0.lo + b0.hi;            // sum over c of x_c
     // sums over c of x_c v_cb for b = 0..3
     const float sb[4] = {b1.lo + b1.hi, b2.lo + b2.hi, bd.lo + bd.hi, b0.hi - b0.lo};
-    float v = 0.f;
-#pragma unroll
-    for (int b = 0; b < 4; ++b)
-        if (b == g) v = beta * (sb[b] - (sp[b] - sn[b]) * s0) * (1.f - t[b] * t[b]);
+    const float sbg = g == 0 ? sb[0] : g == 1 ? sb[1] : g == 2 ? sb[2] : sb[3];
+    const float v = beta * (sbg - (spg - sng) * s0) * (1.f - tg * tg);
     du[row][4 * tb + g] = T::store(tb < L ? v : 0.f);
 }
 
