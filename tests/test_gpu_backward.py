@@ -87,6 +87,20 @@ def test_backward_causal_64k_mixed_workload_sampled_rows():
     _check(w, heads={(0, 1), (0, 6)}, q_mask=qm, k_mask=km)
 
 
+def test_backward_block_32k_attention_sampled_rows():
+    """Backward of the 32768-token, d_model 1024 block's attention (16 heads
+    of 64, seven levels) at full size, on sampled rows of two heads."""
+    w = W.BLOCK_32K
+    rng = np.random.default_rng(8)
+    qm = np.zeros(w.N, np.uint8)
+    km = np.zeros(w.N, np.uint8)
+    qm[rng.choice(w.N, 200, replace=False)] = 1
+    km[rng.choice(w.N, 200, replace=False)] = 1
+    qm[-64:] = 1
+    km[:64] = 1
+    _check(w, heads={(0, 4), (0, 9)}, q_mask=qm, k_mask=km)
+
+
 def test_backward_is_deterministic():
     w = _w("c-bf16-det", 1, 2, 2048, 128, 128, 128, True, "bf16", seed=63)
     cfg = cfg_of(w)
