@@ -60,7 +60,8 @@ typedef enum {
 typedef enum { ELSAA_F32 = 0, ELSAA_BF16 = 1 } elsaa_dtype;
 
 typedef struct {
-    int32_t B, H, N, d_h;   /* batch, heads, sequence length, head dim (64 or 128)          */
+    int32_t B, H, N, d_h;   /* batch, heads, sequence length, head dim (64 or 128);         */
+                            /* GPU path: N <= 2^26 and N * d_h * element bytes < 2^32        */
     int32_t k;              /* sortLSH block size b: keys per sorted block, 1 <= k           */
     int32_t r;              /* RACE features L * 2^race_bits (the low-rank rank)             */
     int32_t race_bits;      /* gamma, hash bits per RACE table (GPU path: 4)                 */

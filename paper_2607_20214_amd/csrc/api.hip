@@ -91,6 +91,9 @@ int validate(const elsaa_config* c, Shape* s)
     if (c->r > 256) return fail(ELSAA_ERR_UNSUPPORTED, "r must be <= 256 (got %d)", c->r);
     if ((int64_t)c->N > (1 << 26)) return fail(ELSAA_ERR_UNSUPPORTED, "N must be <= 2^26");
     const int bf16 = c->dtype == ELSAA_BF16;
+    // the sparse kernels address a head's rows with 32-bit byte offsets
+    if ((int64_t)c->N * c->d_h * (bf16 ? 2 : 4) >= ((int64_t)1 << 32))
+        return fail(ELSAA_ERR_UNSUPPORTED, "N * d_h * element bytes must be < 2^32 (one head's rows)");
     const int n0 = c->n0 > 0 ? c->n0 : 2 * c->k;
     int lv = 0, n_leaf = c->N;
     if (c->causal) {

@@ -52,6 +52,7 @@ struct BArgs {
     int H, N, k, Lv, n_leaf;
     LevelTiles lt;            // causal tile numbering
     int nbr;                  // neighbouring sorted blocks on each side
+    int nbx, nblk;            // whole-block kernel: blocks per head, blocks in all
     size_t BHN;
     float tau, tau2;
 };
@@ -511,18 +512,27 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
 }
 
 // ------------------------------------------------------------------------
-// Whole sorted blocks at once (b = BQ in {64, 128}): one workgroup per block
-// of BQ sorted queries and the BQ sorted keys they see (Alg. 4 blocks; the
-// per-level SortLSH calls of Alg. 5).  BQ / 16 waves each own 16 keys (their
-// K, V rows in registers, dK^T and dV^T accumulators); the block's queries
-// stream through LDS in tiles of 64 with the next tile's rows loaded into
-// registers meanwhile.  Per tile: S = Q K^T and dP = dO V^T (query rows from
-// LDS), P and dS in registers, dV^T += dO^T P and dK^T += Q^T dS with the
-// transposed operands read from the query tiles, then dS^T goes to LDS and
-// the tile's complete dQ^T = K^T dS^T is formed from the block's K tile.
-// Every input row is read once per block and dQ, dK, dV are each written
-// once: partials by natural token index (levels) or the final sums with the
-// low-rank parts in the storage dtype (non-causal blocks).
+// Whole sorted blocks at once (b = BQ in {64, 128}): each block is BQ sorted
+// queries and the BQ sorted keys they see (Alg. 4 blocks; the per-level
+// SortLSH calls of Alg. 5).  BQ / 16 waves each own 16 keys (their V rows in
+// registers, dK^T and dV^T accumulators); the block's queries stream through
+// LDS in tiles of 64 with the next tile's rows loaded into registers
+// meanwhile.  Per tile: S = Q K^T and dP = dO V^T (query rows from LDS), P
+// and dS in registers, dV^T += dO^T P and dK^T += Q^T dS with the transposed
+// operands read from the query tiles, then dS^T goes to LDS and the tile's
+// complete dQ^T = K^T dS^T is formed from the block's K tile.  Every input
+// row is read once per block and dQ, dK, dV are each written once: partials
+// by natural token index (levels) or the final sums with the low-rank parts
+// in the storage dtype (non-causal blocks).
+//
+// The grid holds as many workgroups as the device runs at once and each
+// walks the blocks id, id + gridDim.x, ...  The next block's loads overlap
+// the current block's last tile: its index lists at the start of the tile,
+// its V rows (into the V registers) and K rows once dP is formed, and its
+// first Q / dO tile at the end; the current block's dK, dV are stored once
+// the next block's rows are in LDS.  At the levels every block is full, so loads
+// and stores there carry no per-row branch and the compiler can wait for
+// exactly the loads it needs (its memory counter retires in order).
 // ------------------------------------------------------------------------
 template <class T, int D, int BQ, int MODE>
 __global__ __launch_bounds__(BQ * 4, BQ == 64 ? 3 : 1) void sparse_bwd_block_kernel(BArgs a)
@@ -534,6 +544,7 @@ __global__ __launch_bounds__(BQ * 4, BQ == 64 ? 3 : 1) void sparse_bwd_block_ker
     using TD = tile::Tile<T, D, NT>;        // Q, dO, K tiles (rows of D)
     using TS = tile::Tile<T, 64, NT>;       // dS^T tile (BQ rows of 64 queries)
     constexpr int PT = TD::PER_THREAD;
+    constexpr bool kFull = MODE == kLevels;  // every block holds BQ valid queries and keys
     static_assert(TS::elems(BQ) <= 2 * TD::elems(64), "dS^T fits in the query tiles");
     __shared__ __attribute__((aligned(16))) S sk[TD::elems(BQ)];
     __shared__ __attribute__((aligned(16))) S sqo[2 * TD::elems(64)];   // Q tile, dO tile; later dS^T
@@ -543,218 +554,310 @@ __global__ __launch_bounds__(BQ * 4, BQ == 64 ? 3 : 1) void sparse_bwd_block_ker
     S* const so = sqo + TD::elems(64);
     S* const sds = sqo;
 
-    const int h = blockIdx.y, b = blockIdx.z;
-    const size_t bh = (size_t)b * a.H + h;
     const int N = a.N;
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int g = lane >> 4, col = lane & 15;
-    const S* Q = (const S*)a.Q + bh * N * D;
-    const S* K = (const S*)a.K + bh * N * D;
-    const S* V = (const S*)a.V + bh * N * D;
-    const S* dO = (const S*)a.dO + bh * N * D;
+    const int w = threadIdx.x >> 6;
+    // lane coordinates from a fresh copy of the thread index at every block
+    // (lane-dependent LDS addresses are formed where used instead of held in
+    // registers across the block loop)
+    int tx, g, col, kloc;                                // kloc: this lane's key within a block
+    auto lanes = [&]() {
+        tx = threadIdx.x;
+        asm volatile("" : "+v"(tx));
+        g = (tx & 63) >> 4;
+        col = tx & 15;
+        kloc = 16 * w + col;
+    };
+    lanes();
 
-    // ---- the block: sorted positions [p0, p0 + nv) of its query and key lists
-    int level = 0, nv;
-    const int32_t* ql;
-    const int32_t* kl;
-    if (MODE == kLevels) {
-        const int per_level = (N / 2) / BQ;
-        level = blockIdx.x / per_level;
-        const int t = blockIdx.x - level * per_level;
-        const size_t base = (bh * a.Lv + level) * (size_t)(N / 2) + (size_t)t * BQ;
-        ql = a.perm_q + base;
-        kl = a.perm_k + base;
-        nv = BQ;
-    } else {
-        const int p0 = blockIdx.x * BQ;
-        ql = a.perm_q + bh * N + p0;
-        kl = a.perm_k + bh * N + p0;
-        nv = min(BQ, N - p0);
-    }
-
-    // ---- K tile of the block, Q / dO tile 0, this lane's V rows
-    uint4 rq[PT], ro[PT];
-    int qtk[PT];
-    float l2 = 0.f, de = 0.f, sc = 0.f;
-    int qtok_t = -1;
-    auto qtokens = [&](int qt) {
-#pragma unroll
-        for (int j = 0; j < PT; ++j) {
-            const int r = 64 * qt + TD::row_of(j);
-            qtk[j] = r < nv ? ql[r] : -1;
+    // ---- block id -> head and the sorted positions [p0, p0 + nv) of its lists
+    struct Blk {
+        size_t bh;
+        int level, nv;
+        const int32_t* ql;
+        const int32_t* kl;
+    };
+    auto block_of = [&](int id) {
+        Blk k;
+        const int x = id % a.nbx;
+        k.bh = (size_t)(id / a.nbx);                     // b * H + h
+        if (MODE == kLevels) {
+            const int per_level = (N / 2) / BQ;
+            k.level = x / per_level;
+            const int t = x - k.level * per_level;
+            const size_t base = (k.bh * a.Lv + k.level) * (size_t)(N / 2) + (size_t)t * BQ;
+            k.ql = a.perm_q + base;
+            k.kl = a.perm_k + base;
+            k.nv = BQ;
+        } else {
+            const int p0 = x * BQ;
+            k.level = 0;
+            k.ql = a.perm_q + k.bh * N + p0;
+            k.kl = a.perm_k + k.bh * N + p0;
+            k.nv = min(BQ, N - p0);
         }
-        qtok_t = -1;
-        if (threadIdx.x < 64) {
-            const int r = 64 * qt + threadIdx.x;
-            qtok_t = r < nv ? ql[r] : -1;
+        return k;
+    };
+    // index lists of a block: K tile rows, this lane's key, every query tile
+    struct Idx {
+        int ktk[NQT][PT];
+        int ktok;
+        int qtk[NQT][PT];
+        int qt1[NQT];                                    // query 64 qt + (tx % 64) (scalars, dQ rows)
+    };
+    auto indices = [&](const Blk& k, Idx& ix) {
+#pragma unroll
+        for (int t = 0; t < NQT; ++t) {
+#pragma unroll
+            for (int j = 0; j < PT; ++j) {
+                const int r = 64 * t + TD::row_of(j, tx);
+                ix.ktk[t][j] = (kFull || r < k.nv) ? k.kl[(uint32_t)r] : -1;
+                ix.qtk[t][j] = (kFull || r < k.nv) ? k.ql[(uint32_t)r] : -1;
+            }
+            const int r = 64 * t + (tx & 63);
+            ix.qt1[t] = (kFull || r < k.nv) ? k.ql[(uint32_t)r] : -1;
+        }
+        ix.ktok = (kFull || kloc < k.nv) ? k.kl[(uint32_t)kloc] : -1;
+    };
+    auto kload = [&](size_t bh, const Idx& ix, uint4 (&rk)[NQT][PT]) {
+        const S* K = (const S*)a.K + bh * N * D;
+#pragma unroll
+        for (int t = 0; t < NQT; ++t) {
+            if constexpr (kFull) TD::load_all(K, ix.ktk[t], rk[t], tx);
+            else TD::load(K, ix.ktk[t], rk[t], tx);
         }
     };
-    auto qload = [&]() {
-        TD::load(Q, qtk, rq);
-        TD::load(dO, qtk, ro);
-        l2 = de = sc = 0.f;
-        if (qtok_t >= 0) {
-            const size_t row = bh * N + qtok_t;
-            l2 = a.rs[row];
-            de = a.rs[a.BHN + row];
-            sc = a.rs[2 * a.BHN + row];
-        }
-    };
-    // every index first (K tile rows, this lane's key, query tile 0), then
-    // every row (K tile, V rows, Q / dO tile 0), so the block starts after
-    // two round trips to memory instead of one per dependent step
-    const int kloc = 16 * w + col;                       // this lane's key within the block
-    int ktk[NQT][PT];
-#pragma unroll
-    for (int kt = 0; kt < NQT; ++kt)
-#pragma unroll
-        for (int j = 0; j < PT; ++j) {
-            const int r = 64 * kt + TD::row_of(j);
-            ktk[kt][j] = r < nv ? kl[r] : -1;
-        }
-    const int ktok = kloc < nv ? kl[kloc] : -1;
-    qtokens(0);
-    uint4 rk[NQT][PT];
-#pragma unroll
-    for (int kt = 0; kt < NQT; ++kt) TD::load(K, ktk[kt], rk[kt]);
-    F vf[KS];
-    {
-        float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) vf[ks] = T::pack(z);
-        if (ktok >= 0)
+    auto vload = [&](size_t bh, int ktok, F (&vf)[KS]) {
+        const S* V = (const S*)a.V + bh * N * D;
+        if (kFull || ktok >= 0) {
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) vf[ks] = T::ld8(V + (size_t)ktok * D + 32 * ks + 8 * g);
-    }
-    qload();
+        } else {
+            float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
-    for (int kt = 0; kt < NQT; ++kt) TD::store(sk, rk[kt], 64 * kt);
-    // (this lane's K row is read from the block's K tile when needed)
-
-    f32x4 akT[DT], avT[DT];                              // rows d = 16 dt + 4 g + i, column = this key
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) { akT[dt] = f32x4{0, 0, 0, 0}; avT[dt] = f32x4{0, 0, 0, 0}; }
-
-    for (int qt = 0; qt < NQT; ++qt) {
-        if (qt > 0) __syncthreads();                     // previous dS^T / dQ phase done
-        TD::store(sq, rq);
-        TD::store(so, ro);
-        if (threadIdx.x < 64) {
-            s_l2[threadIdx.x] = l2;
-            s_de[threadIdx.x] = de;
-            s_sc[threadIdx.x] = sc;
-            s_qt[threadIdx.x] = qtok_t;
+            for (int ks = 0; ks < KS; ++ks) vf[ks] = T::pack(z);
         }
-        __syncthreads();
-        if (qt + 1 < NQT) {                              // next tile in flight
-            qtokens(qt + 1);
-            qload();
+    };
+    uint4 rq[PT], ro[PT];
+    float l2 = 0.f, de = 0.f, sc = 0.f;
+    // rows and row scalars of query tile qt (every thread reads the scalars
+    // of query 64 qt + tx % 64; threads < 64 publish them)
+    auto qload = [&](size_t bh, const Idx& ix, int qt) {
+        const S* Q = (const S*)a.Q + bh * N * D;
+        const S* dO = (const S*)a.dO + bh * N * D;
+        if constexpr (kFull) {
+            TD::load_all(Q, ix.qtk[qt], rq, tx);
+            TD::load_all(dO, ix.qtk[qt], ro, tx);
+        } else {
+            TD::load(Q, ix.qtk[qt], rq, tx);
+            TD::load(dO, ix.qtk[qt], ro, tx);
         }
+        const float* rs = a.rs + bh * N;
+        const uint32_t t = (uint32_t)max(ix.qt1[qt], 0);
+        l2 = rs[t];
+        de = (rs + a.BHN)[t];
+        sc = (rs + 2 * a.BHN)[t];
+    };
 
-        // S and dP for the 64 queries x this wave's 16 keys (rows: queries);
-        // P sc and dS packed at once as the 32-query k-step operands
-        F pf[2], zf[2];
+    // dK, dV of a lane's key: rows d = 16 dt + 4 g + i of the accumulators
+    f32x4 akT[DT], avT[DT];
+    auto store_dkv = [&](size_t bh, int level, int ktok) {
+        if (!(kFull || ktok >= 0)) return;
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-            float p8[8], z8[8];
-#pragma unroll
-            for (int h2 = 0; h2 < 2; ++h2) {
-                const int s = 2 * kk + h2;
-                f32x4 st = {0, 0, 0, 0}, dp = {0, 0, 0, 0};
-                const int qr = krow_of(s, col);
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    st = T::mma(TD::row8(sq, qr, 32 * ks + 8 * g), TD::row8(sk, kloc, 32 * ks + 8 * g), st);
-                    dp = T::mma(TD::row8(so, qr, 32 * ks + 8 * g), vf[ks], dp);
-                }
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int q = key_of(s, g, i);
-                    const bool ok = ktok >= 0 && s_qt[q] >= 0;
-                    const float P = ok ? fast_exp2(st[i] * a.tau2 - s_l2[q]) : 0.f;
-                    const float c = s_sc[q];
-                    p8[4 * h2 + i] = P * c;
-                    z8[4 * h2 + i] = P * (c * dp[i] - s_de[q]);
-                }
-            }
-            pf[kk] = T::pack(p8);
-            zf[kk] = T::pack(z8);
-        }
-        // dV^T += dO^T (P sc), dK^T += Q^T dS over two 32-query k-steps
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-                avT[dt] = T::mma(TD::col8(so, 32 * kk, 16 * dt), pf[kk], avT[dt]);
-                akT[dt] = T::mma(TD::col8(sq, 32 * kk, 16 * dt), zf[kk], akT[dt]);
-            }
-        __syncthreads();                                 // query tiles no longer read
-        // dS^T [key][query] into the query-tile space: slots 8g + j of k-step kk
-        // hold queries 32 kk + 8 g + j, eight consecutive queries per write
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-            const int q0 = 32 * kk + 8 * g;
-            S* dst = &sds[TS::row(kloc) + q0];
-            if constexpr (T::bytes == 2) {
-                *(F*)dst = zf[kk];
+        for (int dt = 0; dt < DT; ++dt) {
+            const int d0 = 16 * dt + 4 * g;
+            if (MODE == kLevels) {
+                const size_t slot = level_slot(bh, a.Lv, level, N, ktok, 0);
+                *(f32x4*)(a.part_dk + slot * D + d0) = akT[dt] * a.tau;
+                *(f32x4*)(a.part_dv + slot * D + d0) = avT[dt];
             } else {
-#pragma unroll
-                for (int j = 0; j < 8; ++j) dst[j] = zf[kk][j];
+                const size_t row = bh * N + ktok;
+                const f32x4 vk = akT[dt] * a.tau + *(const f32x4*)(a.dk_lr + row * D + d0);
+                const f32x4 vv = avT[dt] + *(const f32x4*)(a.dv_lr + row * D + d0);
+                store4<T>((S*)a.dK + row * D + d0, vk);
+                store4<T>((S*)a.dV + row * D + d0, vv);
             }
         }
-        __syncthreads();
-        // dQ^T = K^T dS^T for this tile: DT x 4 output tiles spread over the
-        // waves, each wave's tiles sharing one 16-row slice dt of K^T when it
-        // has four or more
-        constexpr int TILES = DT * 4, PER_W = TILES / NW;
-        static_assert(TILES % NW == 0 && (PER_W % 4 == 0 || 4 % PER_W == 0), "dQ tiles per wave");
-        f32x4 dq[PER_W];
+    };
+
+    int id = blockIdx.x;
+    Blk blk = block_of(id);
+    Idx ix;
+    indices(blk, ix);
+    uint4 rk[NQT][PT];
+    F vf[KS];
+    kload(blk.bh, ix, rk);
+    vload(blk.bh, ix.ktok, vf);
+    qload(blk.bh, ix, 0);
+    // a block's dK, dV leave once the next block's rows are in LDS (so no
+    // wait for those rows also waits for the stores): the previous block
+    size_t prev_bh = 0;
+    int prev_level = 0, prev_ktok = -1;
+    bool first = true;
+    for (;;) {
+        lanes();
+        const size_t bh = blk.bh;
+        const int level = blk.level;
+        const int ktok = ix.ktok;
+        if (!first) __syncthreads();                     // the previous block's dQ phase is done with LDS
 #pragma unroll
-        for (int u = 0; u < PER_W; ++u) dq[u] = f32x4{0, 0, 0, 0};
+        for (int t = 0; t < NQT; ++t) TD::store(sk, rk[t], 64 * t, tx);
+        // (this lane's K row is read from the block's K tile when needed)
+
+        const int nid = id + gridDim.x;
+        const bool has_next = nid < a.nblk;
+        Blk nblk = blk;
+        Idx nix;
+
 #pragma unroll
-        for (int kb = 0; kb < BQ; kb += 32) {
-            F kt_frag = TD::col8(sk, kb, 16 * ((w * PER_W) / 4));
+        for (int qt = 0; qt < NQT; ++qt) {
+            const bool last = qt + 1 == NQT;
+            if (qt > 0) __syncthreads();                 // previous dS^T / dQ phase done
+            TD::store(sq, rq, 0, tx);
+            TD::store(so, ro, 0, tx);
+            if (threadIdx.x < 64) {
+                s_l2[tx] = (kFull || ix.qt1[qt] >= 0) ? l2 : 0.f;
+                s_de[tx] = de;
+                s_sc[tx] = sc;
+                s_qt[tx] = ix.qt1[qt];
+            }
+            __syncthreads();
+            if (qt == 0) {                               // the previous block's dK, dV leave now
+                if (!first) store_dkv(prev_bh, prev_level, prev_ktok);
+                first = false;
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) { akT[dt] = f32x4{0, 0, 0, 0}; avT[dt] = f32x4{0, 0, 0, 0}; }
+            }
+            if (!last) {
+                qload(bh, ix, qt + 1);                   // next tile in flight
+            } else if (has_next) {
+                nblk = block_of(nid);                    // the next block's index lists
+                indices(nblk, nix);
+            }
+
+            // S and dP for the 64 queries x this wave's 16 keys (rows: queries);
+            // P sc and dS packed at once as the 32-query k-step operands
+            F pf[2], zf[2];
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk) {
+                float p8[8], z8[8];
+#pragma unroll
+                for (int h2 = 0; h2 < 2; ++h2) {
+                    const int s = 2 * kk + h2;
+                    f32x4 st = {0, 0, 0, 0}, dp = {0, 0, 0, 0};
+                    const int qr = krow_of(s, col);
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks) {
+                        st = T::mma(TD::row8(sq, qr, 32 * ks + 8 * g), TD::row8(sk, kloc, 32 * ks + 8 * g), st);
+                        dp = T::mma(TD::row8(so, qr, 32 * ks + 8 * g), vf[ks], dp);
+                    }
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int q = key_of(s, g, i);
+                        const bool ok = kFull || (ktok >= 0 && s_qt[q] >= 0);
+                        const float P = ok ? fast_exp2(st[i] * a.tau2 - s_l2[q]) : 0.f;
+                        const float c = s_sc[q];
+                        p8[4 * h2 + i] = P * c;
+                        z8[4 * h2 + i] = P * (c * dp[i] - s_de[q]);
+                    }
+                }
+                pf[kk] = T::pack(p8);
+                zf[kk] = T::pack(z8);
+            }
+            if (last && has_next) {                      // V and K rows of the next block
+                vload(nblk.bh, nix.ktok, vf);
+                kload(nblk.bh, nix, rk);
+            }
+            // dV^T += dO^T (P sc), dK^T += Q^T dS over two 32-query k-steps
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) {
+                    avT[dt] = T::mma(TD::col8(so, 32 * kk, 16 * dt, tx), pf[kk], avT[dt]);
+                    akT[dt] = T::mma(TD::col8(sq, 32 * kk, 16 * dt, tx), zf[kk], akT[dt]);
+                }
+            __syncthreads();                             // query tiles no longer read
+            // dS^T [key][query] into the query-tile space: slots 8g + j of k-step kk
+            // hold queries 32 kk + 8 g + j, eight consecutive queries per write
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk) {
+                const int q0 = 32 * kk + 8 * g;
+                S* dst = &sds[TS::row(kloc) + q0];
+                if constexpr (T::bytes == 2) {
+                    *(F*)dst = zf[kk];
+                } else {
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) dst[j] = zf[kk][j];
+                }
+            }
+            __syncthreads();
+            // dQ^T = K^T dS^T for this tile: DT x 4 output tiles spread over the
+            // waves, each wave's tiles sharing one 16-row slice dt of K^T when it
+            // has four or more
+            constexpr int TILES = DT * 4, PER_W = TILES / NW;
+            static_assert(TILES % NW == 0 && (PER_W % 4 == 0 || 4 % PER_W == 0), "dQ tiles per wave");
+            f32x4 dq[PER_W];
+#pragma unroll
+            for (int u = 0; u < PER_W; ++u) dq[u] = f32x4{0, 0, 0, 0};
+#pragma unroll
+            for (int kb = 0; kb < BQ; kb += 32) {
+                F kt_frag = TD::col8(sk, kb, 16 * ((w * PER_W) / 4), tx);
+#pragma unroll
+                for (int u = 0; u < PER_W; ++u) {
+                    const int tix = w * PER_W + u, dt = tix / 4, qtile = tix % 4;
+                    if (u > 0 && qtile == 0) kt_frag = TD::col8(sk, kb, 16 * dt, tx);
+                    dq[u] = T::mma(kt_frag, TS::col8(sds, kb, 16 * qtile, tx), dq[u]);
+                }
+            }
 #pragma unroll
             for (int u = 0; u < PER_W; ++u) {
                 const int tix = w * PER_W + u, dt = tix / 4, qtile = tix % 4;
-                if (u > 0 && qtile == 0) kt_frag = TD::col8(sk, kb, 16 * dt);
-                dq[u] = T::mma(kt_frag, TS::col8(sds, kb, 16 * qtile), dq[u]);
+                const int qtok = s_qt[16 * qtile + col];
+                if (!kFull && qtok < 0) continue;
+                const int d0 = 16 * dt + 4 * g;
+                if (MODE == kLevels) {
+                    float* out = a.part_dq + level_slot(bh, a.Lv, level, N, qtok, 1) * D + d0;
+                    *(f32x4*)out = dq[u] * a.tau;
+                } else {
+                    const size_t row = bh * N + qtok;
+                    const f32x4 v = dq[u] * a.tau + *(const f32x4*)(a.dq_lr + row * D + d0);
+                    store4<T>((S*)a.dQ + row * D + d0, v);
+                }
             }
         }
-#pragma unroll
-        for (int u = 0; u < PER_W; ++u) {
-            const int tix = w * PER_W + u, dt = tix / 4, qtile = tix % 4;
-            const int qtok = s_qt[16 * qtile + col];
-            if (qtok < 0) continue;
-            const int d0 = 16 * dt + 4 * g;
-            if (MODE == kLevels) {
-                float* out = a.part_dq + level_slot(bh, a.Lv, level, N, qtok, 1) * D + d0;
-                *(f32x4*)out = dq[u] * a.tau;
-            } else {
-                const size_t row = bh * N + qtok;
-                const f32x4 v = dq[u] * a.tau + *(const f32x4*)(a.dq_lr + row * D + d0);
-                store4<T>((S*)a.dQ + row * D + d0, v);
-            }
-        }
-    }
 
-    // ---- dK, dV of this lane's key: rows d = 16 dt + 4 g + i
-    if (ktok < 0) return;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-        const int d0 = 16 * dt + 4 * g;
-        if (MODE == kLevels) {
-            const size_t slot = level_slot(bh, a.Lv, level, N, ktok, 0);
-            *(f32x4*)(a.part_dk + slot * D + d0) = akT[dt] * a.tau;
-            *(f32x4*)(a.part_dv + slot * D + d0) = avT[dt];
-        } else {
-            const size_t row = bh * N + ktok;
-            const f32x4 vk = akT[dt] * a.tau + *(const f32x4*)(a.dk_lr + row * D + d0);
-            const f32x4 vv = avT[dt] + *(const f32x4*)(a.dv_lr + row * D + d0);
-            store4<T>((S*)a.dK + row * D + d0, vk);
-            store4<T>((S*)a.dV + row * D + d0, vv);
-        }
+        prev_bh = bh;
+        prev_level = level;
+        prev_ktok = ktok;
+        if (!has_next) break;
+        qload(nblk.bh, nix, 0);                          // the next block's first Q / dO tile
+        id = nid;
+        blk = nblk;
+        ix = nix;
     }
+    store_dkv(prev_bh, prev_level, prev_ktok);
+}
+
+// Whole-block launch: as many workgroups as the device runs at once (cached
+// per instantiation and device), each walking its share of the blocks.
+template <class T, int D, int BQ, int MODE>
+void launch_blocks(const char* name, BArgs a, int nbx, int BH, hipStream_t st)
+{
+    static int resident[64] = {0};
+    auto kern = sparse_bwd_block_kernel<T, D, BQ, MODE>;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = 0;
+    int& res = resident[dev & 63];
+    if (res == 0) {
+        int cus = 0, per = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+            cus = 256;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kern, BQ * 4, 0) != hipSuccess || per <= 0) per = 1;
+        res = cus * per;
+    }
+    a.nbx = nbx;
+    a.nblk = nbx * BH;
+    const int grid = a.nblk < res ? a.nblk : res;
+    ELSAA_LAUNCH(name, kern, dim3(grid), dim3(BQ * 4), 0, st, a);
 }
 
 template <class T, int D>
@@ -767,9 +870,9 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
     if (!s.causal) {
         if (!(parts & kSparseFinal)) return hipSuccess;
         if (whole) {
-            dim3 grid((s.N + bq - 1) / bq, s.H, s.B);
-            if (bq == 64) ELSAA_LAUNCH("sparse_bwd_blocks", (sparse_bwd_block_kernel<T, D, 64, kBlocks>), grid, dim3(256), 0, st, a);
-            else ELSAA_LAUNCH("sparse_bwd_blocks", (sparse_bwd_block_kernel<T, D, 128, kBlocks>), grid, dim3(512), 0, st, a);
+            const int nbx = (s.N + bq - 1) / bq;
+            if (bq == 64) launch_blocks<T, D, 64, kBlocks>("sparse_bwd_blocks", a, nbx, s.B * s.H, st);
+            else launch_blocks<T, D, 128, kBlocks>("sparse_bwd_blocks", a, nbx, s.B * s.H, st);
             return hipGetLastError();
         }
         dim3 grid((s.N + kT - 1) / kT, s.H, s.B);
@@ -780,9 +883,9 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
     }
     if (s.Lv > 0 && (parts & kSparseLevels)) {
         if (whole) {
-            dim3 grid(s.Lv * (s.N / 2) / bq, s.H, s.B);
-            if (bq == 64) ELSAA_LAUNCH("sparse_bwd_levels", (sparse_bwd_block_kernel<T, D, 64, kLevels>), grid, dim3(256), 0, st, a);
-            else ELSAA_LAUNCH("sparse_bwd_levels", (sparse_bwd_block_kernel<T, D, 128, kLevels>), grid, dim3(512), 0, st, a);
+            const int nbx = s.Lv * (s.N / 2) / bq;
+            if (bq == 64) launch_blocks<T, D, 64, kLevels>("sparse_bwd_levels", a, nbx, s.B * s.H, st);
+            else launch_blocks<T, D, 128, kLevels>("sparse_bwd_levels", a, nbx, s.B * s.H, st);
             if ((e = hipGetLastError()) != hipSuccess) return e;
         } else {
             dim3 grid(a.lt.first[s.Lv], s.H, s.B);

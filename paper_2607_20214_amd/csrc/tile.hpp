@@ -47,22 +47,41 @@ struct Tile {
     // element offset of chunk c of row r
     __device__ static __forceinline__ int off(int r, int c) { return row(r) + c * EPC; }
 
-    // row of the j-th chunk this thread stages (and the chunk index)
-    __device__ static __forceinline__ int row_of(int j) { return (threadIdx.x + NT * j) / CPR; }
-    __device__ static __forceinline__ int chunk_of(int j) { return (threadIdx.x + NT * j) % CPR; }
+    // Row of the j-th chunk thread tx stages (and the chunk index).  The
+    // helpers take the thread index as an argument (default threadIdx.x):
+    // a kernel that loops over work items passes a copy the compiler cannot
+    // hoist, so lane addresses are formed where used, not kept in registers.
+    __device__ static __forceinline__ int row_of(int j, int tx = threadIdx.x) { return (tx + NT * j) / CPR; }
+    __device__ static __forceinline__ int chunk_of(int j, int tx = threadIdx.x) { return (tx + NT * j) % CPR; }
 
-    // global -> registers: rows tok[j] (token index, -1 = none) of X
-    __device__ static __forceinline__ void load(const S* X, const int (&tok)[PER_THREAD], uint4 (&r)[PER_THREAD])
+    // global -> registers: rows tok[j] (token index, -1 = none) of X.  The
+    // byte offset from X fits 32 bits (rows of one head), so each address is
+    // the uniform base plus one 32-bit register per lane.
+    __device__ static __forceinline__ void load(const S* X, const int (&tok)[PER_THREAD], uint4 (&r)[PER_THREAD],
+                                                int tx = threadIdx.x)
     {
 #pragma unroll
-        for (int j = 0; j < PER_THREAD; ++j)
-            r[j] = tok[j] >= 0 ? ldg16(X + (size_t)tok[j] * D + chunk_of(j) * EPC) : make_uint4(0, 0, 0, 0);
+        for (int j = 0; j < PER_THREAD; ++j) {
+            const uint32_t off = (uint32_t)tok[j] * (uint32_t)(D * sizeof(S)) + (uint32_t)chunk_of(j, tx) * 16u;
+            r[j] = tok[j] >= 0 ? ldg16((const char*)X + off) : make_uint4(0, 0, 0, 0);
+        }
+    }
+    // the same when every tok[j] is a valid row (no per-row branch)
+    __device__ static __forceinline__ void load_all(const S* X, const int (&tok)[PER_THREAD],
+                                                    uint4 (&r)[PER_THREAD], int tx = threadIdx.x)
+    {
+#pragma unroll
+        for (int j = 0; j < PER_THREAD; ++j) {
+            const uint32_t off = (uint32_t)tok[j] * (uint32_t)(D * sizeof(S)) + (uint32_t)chunk_of(j, tx) * 16u;
+            r[j] = ldg16((const char*)X + off);
+        }
     }
     // registers -> LDS (rows row0 .. row0 + 63 of the tile)
-    __device__ static __forceinline__ void store(S* t, const uint4 (&r)[PER_THREAD], int row0 = 0)
+    __device__ static __forceinline__ void store(S* t, const uint4 (&r)[PER_THREAD], int row0 = 0,
+                                                 int tx = threadIdx.x)
     {
 #pragma unroll
-        for (int j = 0; j < PER_THREAD; ++j) *(uint4*)&t[off(row0 + row_of(j), chunk_of(j))] = r[j];
+        for (int j = 0; j < PER_THREAD; ++j) *(uint4*)&t[off(row0 + row_of(j, tx), chunk_of(j, tx))] = r[j];
     }
 
     // 8-slot operand fragment: elements [e0, e0 + 8) of row r (e0 % 8 == 0)
@@ -76,9 +95,9 @@ struct Tile {
     // 8-slot operand fragment of the transposed tile: lane (i = lane % 16,
     // g = lane / 16) receives column c0 + i at rows kb + 8g + j, j = 0..7
     // (c0 % 16 == 0).
-    __device__ static __forceinline__ F col8(const S* t, int kb, int c0)
+    __device__ static __forceinline__ F col8(const S* t, int kb, int c0, int tx = threadIdx.x)
     {
-        const int lane = threadIdx.x & 63, g = lane >> 4, i = lane & 15;
+        const int lane = tx & 63, g = lane >> 4, i = lane & 15;
         const int r = kb + 8 * g;
         if constexpr (T::bytes == 2) {
             // 16-bit: two transposed reads of 4 rows each

@@ -52,6 +52,15 @@ def test_host_validation_rejects(kw, status):
     assert E.load().elsaa_last_error().decode()
 
 
+def test_head_rows_must_fit_32_bit_offsets():
+    # N * d_h * element bytes reaches 2^32 for float32 rows at N = 2^23, d_h = 128
+    big = dict(N=1 << 23, d_h=128, k=64, r=64, causal=False)
+    with pytest.raises(E.ElsaaError) as ei:
+        E.num_levels(_cfg(dtype="f32", **big))
+    assert ei.value.status == -2
+    assert E.num_levels(_cfg(dtype="bf16", **big)) == 0
+
+
 def test_sizes_and_layout():
     cfg = _cfg(N=16384, H=16, d_h=128, k=128, r=128, B=1)
     assert E.num_levels(cfg) == 6
