@@ -445,9 +445,10 @@ int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     float* part_dq = at<float>(workspace, W.part_dq);
     float* part_dk = at<float>(workspace, W.part_dk);
     float* part_dv = at<float>(workspace, W.part_dv);
-    // the causal levels' backward on the side stream, the low-rank backward on
-    // the caller's stream; the leaf (or sorted blocks), which add the
-    // low-rank gradients, after both
+    // the causal levels' backward, then the low-rank backward, then the leaf
+    // (or sorted blocks), which add the level partials and low-rank
+    // gradients: its dQ kernel on the side stream beside its dK, dV kernel
+    // (one's memory-bound epilogues overlap the other's tile loops)
     auto levels = [&](hipStream_t st) {
         return launch_sparse_bwd(s, Q, K, V, dO, pq, pk, rs, dq_lr, dk_lr, dv_lr, part_dq, part_dk, part_dv, dQ,
                                  dK, dV, st, kSparseLevels);
@@ -459,8 +460,13 @@ int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     };
     if ((e = levels(stream)) != hipSuccess) return hip_fail(e, "sparse levels backward");
     if ((e = race(stream)) != hipSuccess) return hip_fail(e, "race backward");
-    if ((e = launch_sparse_bwd(s, Q, K, V, dO, pq, pk, rs, dq_lr, dk_lr, dv_lr, part_dq, part_dk, part_dv, dQ, dK,
-                               dV, stream, kSparseFinal)) != hipSuccess)
+    auto final_part = [&](int part) {
+        return [&, part](hipStream_t st) {
+            return launch_sparse_bwd(s, Q, K, V, dO, pq, pk, rs, dq_lr, dk_lr, dv_lr, part_dq, part_dk, part_dv, dQ,
+                                     dK, dV, st, part);
+        };
+    };
+    if ((e = fork_join(stream, final_part(kSparseFinalQ), final_part(kSparseFinalKV))) != hipSuccess)
         return hip_fail(e, "sparse backward");
     return ELSAA_OK;
 }

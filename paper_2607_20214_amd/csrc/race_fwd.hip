@@ -202,18 +202,21 @@ __global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
     for (int f = threadIdx.x; f < RP; f += kThreads) sm.a_state[f] = st_in[RP * D + f];
 
     const int t_beg = seg * a.seg_len, t_end = min(a.N, t_beg + a.seg_len);
-    URegs<RP> uq, uk;                    // projections of the chunk, loaded one chunk ahead
+    URegs<RP> uq, uk;                    // projections and V rows of the chunk, loaded one chunk ahead
+    StageT<T, D> vr;
     uq.load(Uq, t_beg, a.N);
     if (a.causal) uk.load(Uk, t_beg, a.N);
+    vr.load(V, t_beg, a.N, nullptr, 1.f);
     for (int t0 = t_beg; t0 < t_end; t0 += kC) {
         __syncthreads();
-        stage_t<T, D>(sm.vt, V, t0, a.N);
+        vr.store(sm.vt, false);
         features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, sm.phq, nullptr, nullptr);
         if (a.causal) features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, sm.phk, sm.phkt, nullptr);
         __syncthreads();
         if (t0 + kC < t_end) {
             uq.load(Uq, t0 + kC, a.N);
             if (a.causal) uk.load(Uk, t0 + kC, a.N);
+            vr.load(V, t0 + kC, a.N, nullptr, 1.f);
         }
         // Den, inter part: (1/L) Phi_Q . A   (4 threads per query)
         {

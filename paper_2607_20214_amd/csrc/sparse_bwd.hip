@@ -868,18 +868,23 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
     const int bq = s.k;
     const bool whole = (bq == 64 || bq == 128) && s.neighbors == 0 && (s.causal ? (s.n_leaf % bq == 0) : true);
     if (!s.causal) {
-        if (!(parts & kSparseFinal)) return hipSuccess;
         if (whole) {
+            if (!(parts & kSparseFinalQ)) return hipSuccess;
             const int nbx = (s.N + bq - 1) / bq;
             if (bq == 64) launch_blocks<T, D, 64, kBlocks>("sparse_bwd_blocks", a, nbx, s.B * s.H, st);
             else launch_blocks<T, D, 128, kBlocks>("sparse_bwd_blocks", a, nbx, s.B * s.H, st);
             return hipGetLastError();
         }
         dim3 grid((s.N + kT - 1) / kT, s.H, s.B);
-        ELSAA_LAUNCH("sparse_dq_blocks", (sparse_dq_kernel<T, D, kBlocks>), grid, dim3(kThreads), 0, st, a);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        ELSAA_LAUNCH("sparse_dkv_blocks", (sparse_dkv_kernel<T, D, kBlocks>), grid, dim3(kThreads), 0, st, a);
-        return hipGetLastError();
+        if (parts & kSparseFinalQ) {
+            ELSAA_LAUNCH("sparse_dq_blocks", (sparse_dq_kernel<T, D, kBlocks>), grid, dim3(kThreads), 0, st, a);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
+        if (parts & kSparseFinalKV) {
+            ELSAA_LAUNCH("sparse_dkv_blocks", (sparse_dkv_kernel<T, D, kBlocks>), grid, dim3(kThreads), 0, st, a);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
+        return hipSuccess;
     }
     if (s.Lv > 0 && (parts & kSparseLevels)) {
         if (whole) {
@@ -895,12 +900,16 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
             if ((e = hipGetLastError()) != hipSuccess) return e;
         }
     }
-    if (!(parts & kSparseFinal)) return hipSuccess;
     dim3 grid(a.lt.leaf_tiles(), s.H, s.B);
-    ELSAA_LAUNCH("sparse_dq_leaf", (sparse_dq_kernel<T, D, kLeaf>), grid, dim3(kThreads), 0, st, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    ELSAA_LAUNCH("sparse_dkv_leaf", (sparse_dkv_kernel<T, D, kLeaf>), grid, dim3(kThreads), 0, st, a);
-    return hipGetLastError();
+    if (parts & kSparseFinalQ) {
+        ELSAA_LAUNCH("sparse_dq_leaf", (sparse_dq_kernel<T, D, kLeaf>), grid, dim3(kThreads), 0, st, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if (parts & kSparseFinalKV) {
+        ELSAA_LAUNCH("sparse_dkv_leaf", (sparse_dkv_kernel<T, D, kLeaf>), grid, dim3(kThreads), 0, st, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 }  // namespace
