@@ -200,9 +200,10 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 template <class P>
 P* at(void* base, size_t off) { return (P*)((char*)base + off); }
 
-// A second stream per device on which the sparse branch's causal levels run
-// while the caller's stream runs the low-rank branch (they share no buffer;
-// the leaf kernels need both).  Fork: an event on the caller's stream that
+// A second stream per device for work that shares no buffer with what the
+// caller's stream runs meanwhile (the forward's sort beside the low-rank
+// branch, the backward leaf's dQ kernel beside its dK, dV kernel).  Fork: an
+// event on the caller's stream that
 // the side stream waits for; join: the reverse.  Host-side enqueueing of a
 // fork / join pair holds a per-device lock, so that concurrent calls cannot
 // interleave their event records.  Default priority, created on first use
@@ -386,18 +387,16 @@ int elsaa_fwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
         return hip_fail(e, "project");
     float* part_o = at<float>(workspace, W.part_o);
     float* part_lse = at<float>(workspace, W.part_lse);
-    // selection and the causal levels on the side stream, the low-rank branch
-    // on the caller's stream; the leaf (or sorted blocks) with the fusion
-    // epilogue after both
+    // the sort on the side stream beside the low-rank branch (its kernels and
+    // the level kernel's cannot share a compute unit, so the levels run after
+    // it rather than competing for the device), then the causal levels, then
+    // the leaf (or sorted blocks) with the fusion epilogue
     e = fork_join(
-        stream,
-        [&](hipStream_t st) {
-            hipError_t r = launch_sort(s, kq, kk, pq, pk, st);
-            if (r != hipSuccess) return r;
-            return launch_sparse_fwd(s, Q, K, V, pq, pk, gates, lambda_rows, o_lr, d_lr, part_o, part_lse, O,
-                                     lse, m, o_s, st, kSparseLevels);
-        },
+        stream, [&](hipStream_t st) { return launch_sort(s, kq, kk, pq, pk, st); },
         [&](hipStream_t st) { return launch_race_fwd(s, uq, uk, V, at<float>(saved, SL.race_states), o_lr, d_lr, st); });
+    if (e == hipSuccess)
+        e = launch_sparse_fwd(s, Q, K, V, pq, pk, gates, lambda_rows, o_lr, d_lr, part_o, part_lse, O, lse, m, o_s,
+                              stream, kSparseLevels);
     if (e != hipSuccess) return hip_fail(e, "selection / levels / race forward");
     if ((e = launch_sparse_fwd(s, Q, K, V, pq, pk, gates, lambda_rows, o_lr, d_lr, part_o, part_lse, O, lse, m,
                                o_s, stream, kSparseFinal)) != hipSuccess)
