@@ -202,8 +202,7 @@ P* at(void* base, size_t off) { return (P*)((char*)base + off); }
 
 // A second stream per device for work that shares no buffer with what the
 // caller's stream runs meanwhile (the forward's sort beside the low-rank
-// branch, the backward leaf's dQ kernel beside its dK, dV kernel).  Fork: an
-// event on the caller's stream that
+// branch).  Fork: an event on the caller's stream that
 // the side stream waits for; join: the reverse.  Host-side enqueueing of a
 // fork / join pair holds a per-device lock, so that concurrent calls cannot
 // interleave their event records.  Default priority, created on first use
@@ -446,8 +445,7 @@ int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     float* part_dv = at<float>(workspace, W.part_dv);
     // the causal levels' backward, then the low-rank backward, then the leaf
     // (or sorted blocks), which add the level partials and low-rank
-    // gradients: its dQ kernel on the side stream beside its dK, dV kernel
-    // (one's memory-bound epilogues overlap the other's tile loops)
+    // gradients (one kernel at a time: each kernel's time is its own)
     auto levels = [&](hipStream_t st) {
         return launch_sparse_bwd(s, Q, K, V, dO, pq, pk, rs, dq_lr, dk_lr, dv_lr, part_dq, part_dk, part_dv, dQ,
                                  dK, dV, st, kSparseLevels);
@@ -459,13 +457,8 @@ int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     };
     if ((e = levels(stream)) != hipSuccess) return hip_fail(e, "sparse levels backward");
     if ((e = race(stream)) != hipSuccess) return hip_fail(e, "race backward");
-    auto final_part = [&](int part) {
-        return [&, part](hipStream_t st) {
-            return launch_sparse_bwd(s, Q, K, V, dO, pq, pk, rs, dq_lr, dk_lr, dv_lr, part_dq, part_dk, part_dv, dQ,
-                                     dK, dV, st, part);
-        };
-    };
-    if ((e = fork_join(stream, final_part(kSparseFinalQ), final_part(kSparseFinalKV))) != hipSuccess)
+    if ((e = launch_sparse_bwd(s, Q, K, V, dO, pq, pk, rs, dq_lr, dk_lr, dv_lr, part_dq, part_dk, part_dv, dQ, dK,
+                               dV, stream, kSparseFinal)) != hipSuccess)
         return hip_fail(e, "sparse backward");
     return ELSAA_OK;
 }

@@ -79,8 +79,8 @@ hipError_t launch_race_bwd(const Shape& s, const float* Uq, const float* Uk, con
 
 // which kernels of a sparse-branch pass to launch: the causal levels (they
 // need only the selection), the rest (leaf or sorted blocks, which also need
-// the low-rank branch), or both.  The backward's rest splits into its dQ
-// kernel and its dK, dV kernel (the whole-block kernel counts as dQ).
+// the low-rank branch), or both.  The backward's rest can be split into its
+// dQ kernel and its dK, dV kernel (the whole-block kernel counts as dQ).
 enum SparsePart {
     kSparseLevels = 1,
     kSparseFinalQ = 2,
