@@ -54,8 +54,11 @@ def kernel_model(w, Lv: int, rules_G: int = 0, rules_lam: bool = False, rules_pa
     m["race_state"] = (bh * N * (P * 4 + D * s), bh * N * 2 * r * D)
     m["race_out"] = (bh * N * (2 * P * 4 + D * s + D * s + 4),
                      bh * N * (2 * r * D * (2 if w.causal else 1) + (C * (r + D) if w.causal else 0)))
-    m["race_dq"] = (bh * N * (2 * P * 4 + 2 * D * s + 8 + D * s),
-                    bh * N * (2 * r * D * 2 + C * (D + r) + 2 * P * D))
+    # LB1 / LB2 write du (wk values per row in the storage dtype); the sparse
+    # backward forms du W' where it adds the low-rank part
+    wk = max(32, P)
+    m["race_dq"] = (bh * N * (2 * P * 4 + 2 * D * s + 8 + wk * s),
+                    bh * N * (2 * r * D * 2 + C * (D + r)))
     m["race_dk"] = m["race_dq"]
     m["race_dv"] = (bh * N * (2 * P * 4 + D * s + 4 + D * s), bh * N * (2 * r * D * 2 + C * (r + D)))
     # sparse branch: interactions per query, 4D flops each forward (QK^T, PV)
@@ -71,13 +74,17 @@ def kernel_model(w, Lv: int, rules_G: int = 0, rules_lam: bool = False, rules_pa
     # whole-block backward: Q, dO, K, V rows once, 3 row scalars + 2 indices
     # per position, dQ / dK / dV level partials (float32) written once
     m["sparse_bwd_levels"] = (Lv * bh * half * (4 * D * s + 20 + 3 * D * 4), Lv * bh * lvl_inter * 14 * D)
-    m["sparse_bwd_blocks"] = (bh * N * (4 * D * s + 20 + 3 * D * 4 + 3 * D * s), bh * N * min(k, N) * 14 * D)
+    m["sparse_bwd_blocks"] = (bh * N * (4 * D * s + 20 + D * 4 + 2 * wk * s + 3 * D * s),
+                              bh * N * (min(k, N) * 14 * D + 2 * 2 * 2 * wk * D))
     leaf_inter = bh * (N // n_leaf) * (n_leaf * (n_leaf + 1) // 2)
-    m["sparse_dq_leaf"] = (bh * N * (4 * D * s + 12 + D * 4 + D * s) + lvl_pos * D * 4, leaf_inter * 6 * D)
-    m["sparse_dkv_leaf"] = (bh * N * (4 * D * s + 12 + 2 * D * 4 + 2 * D * s) + lvl_pos * 2 * D * 4,
-                            leaf_inter * 8 * D)
-    m["sparse_dq_blocks"] = (bh * N * (4 * D * s + D * s + 12), bh * N * min(k, N) * 6 * D)
-    m["sparse_dkv_blocks"] = (bh * N * (4 * D * s + 2 * D * s + 12), bh * N * min(k, N) * 8 * D)
+    lr_flops = bh * N * 2 * 2 * wk * D            # du W' with W in two bf16 parts
+    m["sparse_dq_leaf"] = (bh * N * (4 * D * s + 12 + wk * s + D * s) + lvl_pos * D * 4,
+                           leaf_inter * 6 * D + lr_flops)
+    m["sparse_dkv_leaf"] = (bh * N * (4 * D * s + 12 + D * 4 + wk * s + 2 * D * s) + lvl_pos * 2 * D * 4,
+                            leaf_inter * 8 * D + lr_flops)
+    m["sparse_dq_blocks"] = (bh * N * (4 * D * s + D * s + 12 + wk * s), bh * N * min(k, N) * 6 * D + lr_flops)
+    m["sparse_dkv_blocks"] = (bh * N * (4 * D * s + 2 * D * s + 12 + D * 4 + wk * s),
+                              bh * N * min(k, N) * 8 * D + lr_flops)
     del seg_states, n0
     if rules_G or rules_lam:
         # token-wise rules: q read once; gates (8 B) and lambda (4 B) per row;

@@ -171,7 +171,7 @@ FwdWorkspace fwd_workspace(const Shape& s)
 }
 
 struct BwdWorkspace {
-    size_t rs, states_b, wt_hi, wt_lo, dq_lr, dk_lr, dv_lr, part_dq, part_dk, part_dv, total;
+    size_t rs, states_b, wt_hi, wt_lo, du_q, du_k, dv_lr, part_dq, part_dk, part_dv, total;
 };
 
 BwdWorkspace bwd_workspace(const Shape& s)
@@ -185,8 +185,8 @@ BwdWorkspace bwd_workspace(const Shape& s)
     W.states_b = off; off = align256(off + race_state_floats(s) * 4);
     W.wt_hi = off; off = align256(off + race_wt_bytes(s));
     W.wt_lo = off; off = align256(off + race_wt_bytes(s));
-    W.dq_lr = off; off = align256(off + bhn * s.D * 4);
-    W.dk_lr = off; off = align256(off + bhn * s.D * 4);
+    W.du_q = off; off = align256(off + bhn * race_wk(s) * (s.bf16 ? 2 : 4));
+    W.du_k = off; off = align256(off + bhn * race_wk(s) * (s.bf16 ? 2 : 4));
     W.dv_lr = off; off = align256(off + bhn * s.D * 4);
     W.part_dq = off; off = align256(off + npart * s.D * 4);
     W.part_dk = off; off = align256(off + npart * s.D * 4);
@@ -433,8 +433,10 @@ int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     const float* uq = at<float>(sv, SL.u_q);
     const float* uk = at<float>(sv, SL.u_k);
     float* rs = at<float>(workspace, W.rs);
-    float* dq_lr = at<float>(workspace, W.dq_lr);
-    float* dk_lr = at<float>(workspace, W.dk_lr);
+    void* du_q = at<char>(workspace, W.du_q);
+    void* du_k = at<char>(workspace, W.du_k);
+    void* wt_hi = at<char>(workspace, W.wt_hi);
+    void* wt_lo = at<char>(workspace, W.wt_lo);
     float* dv_lr = at<float>(workspace, W.dv_lr);
     hipError_t e;
     if ((e = launch_bwd_rows(s, dO, o_s, o_lr, m, lse, d_lr, gates, lambda_rows, rs, dgates, dlambda, stream)) !=
@@ -447,18 +449,17 @@ int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     // (or sorted blocks), which add the level partials and low-rank
     // gradients (one kernel at a time: each kernel's time is its own)
     auto levels = [&](hipStream_t st) {
-        return launch_sparse_bwd(s, Q, K, V, dO, pq, pk, rs, dq_lr, dk_lr, dv_lr, part_dq, part_dk, part_dv, dQ,
-                                 dK, dV, st, kSparseLevels);
+        return launch_sparse_bwd(s, Q, K, V, dO, pq, pk, rs, du_q, du_k, wt_hi, wt_lo, dv_lr, part_dq, part_dk,
+                                 part_dv, dQ, dK, dV, st, kSparseLevels);
     };
     auto race = [&](hipStream_t st) {
         return launch_race_bwd(s, uq, uk, V, dO, W_race, rs, at<float>(sv, SL.race_states),
-                               at<float>(workspace, W.states_b), at<char>(workspace, W.wt_hi),
-                               at<char>(workspace, W.wt_lo), dq_lr, dk_lr, dv_lr, st);
+                               at<float>(workspace, W.states_b), wt_hi, wt_lo, du_q, du_k, dv_lr, st);
     };
     if ((e = levels(stream)) != hipSuccess) return hip_fail(e, "sparse levels backward");
     if ((e = race(stream)) != hipSuccess) return hip_fail(e, "race backward");
-    if ((e = launch_sparse_bwd(s, Q, K, V, dO, pq, pk, rs, dq_lr, dk_lr, dv_lr, part_dq, part_dk, part_dv, dQ, dK,
-                               dV, stream, kSparseFinal)) != hipSuccess)
+    if ((e = launch_sparse_bwd(s, Q, K, V, dO, pq, pk, rs, du_q, du_k, wt_hi, wt_lo, dv_lr, part_dq, part_dk,
+                               part_dv, dQ, dK, dV, stream, kSparseFinal)) != hipSuccess)
         return hip_fail(e, "sparse backward");
     return ELSAA_OK;
 }

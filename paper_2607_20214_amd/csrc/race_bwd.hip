@@ -12,10 +12,13 @@
 // contract their state over d, so each wave owns a quarter of the features;
 // LB3 contracts over the features, so each wave owns a quarter of d.
 // dphi is chained through phi = prod sigmoid(2 beta v t), t = tanh(W x) to
-// du, and dQ (dK) = du W on MFMA.  W and the running states enter the MFMAs
-// split into bf16 hi + lo parts (float32 accuracy): their products cancel
-// against the dDen terms.  Outputs are float32 [BH][N][D] parts the sparse
-// backward adds to its own.
+// du, the gradient of the projections u = W x.  LB1 and LB2 store du (storage
+// dtype, [BH][N][wk], wk = 4L padded to 32) and the sparse backward forms
+// dQ (dK) += du W on MFMA where it adds its own part, so only wk values per
+// row cross HBM instead of d float32 ones; this pass provides W' = W_hi' +
+// W_lo' ([H][D][wk], bf16 parts of float32 accuracy).  The running states
+// enter the MFMAs split the same way: their products cancel against the dDen
+// terms.  LB3 writes dV as float32 [BH][N][D].
 #include "internal.hpp"
 #include "race_common.hpp"
 
@@ -30,11 +33,9 @@ struct LbArgs {
     const float* Uk;        // projections of K rows
     const void* V;
     const void* dO;
-    const void* wt_hi;      // W' split hi + lo, storage dtype [H][D][w_kdim]
-    const void* wt_lo;
     const float* rs;        // row scalars (sc_lr at 3*BHN, dDen at 4*BHN)
     const float* states;    // LB1: forward prefix states; LB2/LB3: backward suffix states
-    float* out;             // float32 [BH][N][D]
+    void* out;              // LB1 / LB2: du rows, storage dtype [BH][N][wk]; LB3: float32 dV [BH][N][D]
     int H, N, L, seg_len, nseg, causal;
     size_t BHN;
     float two_beta, beta, inv_L;
@@ -84,45 +85,17 @@ constexpr bool bwd_fits()
            sizeof(Lb3Smem<T, D, RP>) <= kMaxLds;
 }
 
-// du [64 rows][p] x (W_hi + W_lo) [p][D] -> float32 rows [t0, t0 + 64) of out.
-// Computed transposed, out' = W' du': wave w forms the d-tiles dt = w, w + 4,
-// ... for all four 16-row tiles, so it reads only those rows of W' (hi, lo)
-// [D][w_kdim] (L2-resident), and lane (g, col) holds d = 16 dt + 4 g + i of
-// row 16 tt + col: one 16-byte store per lane and tile.
-template <class T, int D, int RP>
-__device__ __forceinline__ void du_times_w(const typename T::store_t (*du)[w_kdim<RP>() + kPad],
-                                           const typename T::store_t* wth, const typename T::store_t* wtl,
-                                           float* out, int t0, int N)
+// du rows [t0, t0 + 64) of the chunk (LDS, storage dtype) -> rows of out
+// [N][WK], 16 bytes per thread and store.
+template <class T, int RP>
+__device__ __forceinline__ void store_du(const typename T::store_t (*du)[w_kdim<RP>() + kPad],
+                                         typename T::store_t* out, int t0, int N)
 {
-    using F = typename T::frag_t;
-    constexpr int DT = D / 16, WK = w_kdim<RP>(), KP = WK / 32;
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int g = lane >> 4, col = lane & 15;
-    constexpr int NDW = DT / 4;            // d-tiles of this wave
-    F wh[NDW][KP], wl[NDW][KP];
-#pragma unroll
-    for (int u = 0; u < NDW; ++u)          // every W' piece of the wave first
-#pragma unroll
-        for (int kp = 0; kp < KP; ++kp) {
-            const size_t o = (size_t)(16 * (w + 4 * u) + col) * WK + 32 * kp + 8 * g;
-            wh[u][kp] = T::ld8(wth + o);
-            if (T::kSplit) wl[u][kp] = T::ld8(wtl + o);
-        }
-#pragma unroll
-    for (int u = 0; u < NDW; ++u) {
-        const int dt = w + 4 * u;
-#pragma unroll
-        for (int tt = 0; tt < 4; ++tt) {
-            f32x4 acc = {0, 0, 0, 0};
-#pragma unroll
-            for (int kp = 0; kp < KP; ++kp) {
-                const F df = T::ld8(&du[16 * tt + col][32 * kp + 8 * g]);
-                acc = T::mma(wh[u][kp], df, acc);
-                if (T::kSplit) acc = T::mma(wl[u][kp], df, acc);
-            }
-            const int tok = t0 + 16 * tt + col;
-            if (tok < N) *(f32x4*)(out + (size_t)tok * D + 16 * dt + 4 * g) = acc;
-        }
+    constexpr int WK = w_kdim<RP>(), PER = 16 / T::bytes, CH = WK / PER;
+    static_assert(WK % PER == 0, "du row of whole 16-byte pieces");
+    for (int it = threadIdx.x; it < kC * CH; it += kThreads) {
+        const int r = it / CH, c = it % CH;
+        if (t0 + r < N) stg16(out + (size_t)(t0 + r) * WK + c * PER, *(const uint4*)&du[r][c * PER]);
     }
 }
 
@@ -157,12 +130,10 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
     const St* dO = (const St*)a.dO + bh * a.N * D;
     const float* sclr = a.rs + 3 * a.BHN + bh * a.N;
     const float* dden = a.rs + 4 * a.BHN + bh * a.N;
-    float* out = a.out + bh * a.N * D;
+    St* du_out = (St*)a.out + bh * a.N * w_kdim<RP>();
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int g = lane >> 4, col = lane & 15;
 
-    const St* wth = (const St*)a.wt_hi + (size_t)h * D * w_kdim<RP>();
-    const St* wtl = (const St*)a.wt_lo + (size_t)h * D * w_kdim<RP>();
     for (int it = threadIdx.x; it < kC * (w_kdim<RP>() + kPad); it += kThreads)
         (&sm.du[0][0])[it] = T::store(0.f);
     // state S'[d][f] for the wave's features f = 16 (w + 4j) + col; A[f] in LDS
@@ -265,7 +236,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
             }
         }
         __syncthreads();
-        du_times_w<T, D, RP>(sm.du, wth, wtl, out, t0, a.N);
+        store_du<T, RP>(sm.du, du_out, t0, a.N);
         if (a.causal) {
             // S' += V' Phi_K (chunk), A += Phi_K' 1
 #pragma unroll
@@ -301,12 +272,10 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
     const St* dO = (const St*)a.dO + bh * a.N * D;
     const float* sclr = a.rs + 3 * a.BHN + bh * a.N;
     const float* dden = a.rs + 4 * a.BHN + bh * a.N;
-    float* out = a.out + bh * a.N * D;
+    St* du_out = (St*)a.out + bh * a.N * w_kdim<RP>();
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int g = lane >> 4, col = lane & 15;
 
-    const St* wth = (const St*)a.wt_hi + (size_t)h * D * w_kdim<RP>();
-    const St* wtl = (const St*)a.wt_lo + (size_t)h * D * w_kdim<RP>();
     for (int it = threadIdx.x; it < kC * (w_kdim<RP>() + kPad); it += kThreads)
         (&sm.du[0][0])[it] = T::store(0.f);
     f32x4 St_[NFT][DT];
@@ -404,7 +373,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
             }
         }
         __syncthreads();
-        du_times_w<T, D, RP>(sm.du, wth, wtl, out, t0, a.N);
+        store_du<T, RP>(sm.du, du_out, t0, a.N);
         if (a.causal) {
             // dS' += (dNum / L)' Phi_Q (chunk), dA += (1/L) Phi_Q' dDen
 #pragma unroll
@@ -438,7 +407,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dv_kernel(LbArgs a)
     const float* Uk = a.Uk + bh * a.N * (RP / 4);
     const St* dO = (const St*)a.dO + bh * a.N * D;
     const float* sclr = a.rs + 3 * a.BHN + bh * a.N;
-    float* out = a.out + bh * a.N * D;
+    float* out = (float*)a.out + bh * a.N * D;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int g = lane >> 4, col = lane & 15;
 
@@ -609,10 +578,16 @@ size_t race_wt_bytes(const Shape& s)
     return (size_t)s.H * s.D * wk * (s.bf16 ? 2 : 4);
 }
 
+int race_wk(const Shape& s)
+{
+    const int rp = race_padded_features(s.r);
+    return rp / 4 < 32 ? 32 : rp / 4;
+}
+
 hipError_t launch_race_bwd(const Shape& s, const float* Uq, const float* Uk, const void* V,
                            const void* dO, const float* W_race, const float* rs,
                            const float* states_f, float* states_b, void* wt_hi, void* wt_lo,
-                           float* dq_lr, float* dk_lr, float* dv_lr, hipStream_t st)
+                           void* du_q, void* du_k, float* dv_lr, hipStream_t st)
 {
     {
         const int rp = race_padded_features(s.r);
@@ -634,13 +609,13 @@ hipError_t launch_race_bwd(const Shape& s, const float* Uq, const float* Uk, con
                                       s.causal ? 2 : 0, st);
     if (e != hipSuccess) return e;
     LbArgs a;
-    a.Uq = Uq; a.Uk = Uk; a.V = V; a.dO = dO; a.wt_hi = wt_hi; a.wt_lo = wt_lo; a.rs = rs;
+    a.Uq = Uq; a.Uk = Uk; a.V = V; a.dO = dO; a.rs = rs;
     a.H = s.H; a.N = s.N; a.L = s.L; a.seg_len = s.seg_len; a.nseg = s.nseg; a.causal = s.causal;
     a.BHN = BHN;
     a.two_beta = 2.f * s.beta; a.beta = s.beta; a.inv_L = 1.f / (float)s.L;
     LbArgs a1 = a, a2 = a, a3 = a;
-    a1.states = states_f; a1.out = dq_lr;
-    a2.states = states_b; a2.out = dk_lr;
+    a1.states = states_f; a1.out = du_q;
+    a2.states = states_b; a2.out = du_k;
     a3.states = states_b; a3.out = dv_lr;
     return dispatch<BwdFn>(s, a1, a2, a3, st);
 }

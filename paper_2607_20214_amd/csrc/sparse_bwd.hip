@@ -40,16 +40,18 @@ struct BArgs {
     const int32_t* perm_q;
     const int32_t* perm_k;
     const float* rs;          // row scalars, see internal.hpp
-    const float* dq_lr;       // float32 [BHN][D] low-rank parts
-    const float* dk_lr;
-    const float* dv_lr;
+    const void* du_q;         // low-rank gradients of the Q / K projections, storage dtype [BHN][wk]
+    const void* du_k;
+    const void* wt_hi;        // W' = W_hi' + W_lo' per head, storage dtype [H][D][wk]
+    const void* wt_lo;
+    const float* dv_lr;       // float32 [BHN][D] low-rank dV
     float* part_dq;           // [BH][Lv][N/2][D] per-level partials, float32
     float* part_dk;
     float* part_dv;
     void* dQ;
     void* dK;
     void* dV;
-    int H, N, k, Lv, n_leaf;
+    int H, N, k, Lv, n_leaf, wk;
     LevelTiles lt;            // causal tile numbering
     int nbr;                  // neighbouring sorted blocks on each side
     int nbx, nblk;            // whole-block kernel: blocks per head, blocks in all
@@ -76,6 +78,24 @@ __device__ __forceinline__ unsigned leaf_levels(int lbeg, int N, int Lv, bool fu
         if ((((lbeg / hl) & 1) != 0) == future) mask |= 1u << l;
     }
     return mask;
+}
+
+// The low-rank part of dQ (dK) of one token for the 16-row slice dt of d:
+// (du W')^T, rows d = 16 dt + 4 g + i, the token in the lane's column (du_row
+// = its du row, wth / wtl = the head's W' parts).  The same matrix-core
+// products, in the same order, as the low-rank pass would use to form it.
+template <class T>
+__device__ __forceinline__ f32x4 lowrank_tile(const typename T::store_t* du_row, const typename T::store_t* wth,
+                                              const typename T::store_t* wtl, int wk, int g, int col, int dt)
+{
+    f32x4 acc = {0, 0, 0, 0};
+    for (int kp = 0; kp < wk; kp += 32) {
+        const typename T::frag_t df = T::ld8(du_row + kp + 8 * g);
+        const size_t o = (size_t)(16 * dt + col) * wk + kp + 8 * g;
+        acc = T::mma(T::ld8(wth + o), df, acc);
+        if (T::kSplit) acc = T::mma(T::ld8(wtl + o), df, acc);
+    }
+    return acc;
 }
 
 // ------------------------------------------------------------------------
@@ -216,37 +236,42 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
             for (int dt = 0; dt < DT; ++dt) acc[dt] = T::mma(TD::col8(sk, 32 * kk, 16 * dt), bf, acc[dt]);
         }
     }
-    if (qtok < 0) return;
     if (MODE == kLevels) {
+        if (qtok < 0) return;
         float* out = a.part_dq + level_slot(bh, a.Lv, level, N, qtok, 1) * D;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) *(f32x4*)(out + 16 * dt + 4 * g) = acc[dt] * a.tau;
         return;
     }
     // dQ = this pass + the low-rank part + (leaf) the partials of the levels
-    // where the query was a future query, added in that order; the rows are
-    // fetched two at a time so their loads are in flight together
-    const size_t row = bh * N + qtok;
+    // where the query was a future query, added in that order; the partial
+    // rows are fetched two at a time so their loads are in flight together.
+    // The low-rank part is a product across the wave's lanes, so every lane
+    // takes part (a lane without a query uses row 0 and discards the result).
     f32x4 tot[DT];
+    {
+        const S* du = (const S*)a.du_q + (bh * N + max(qtok, 0)) * a.wk;
+        const S* wth = (const S*)a.wt_hi + (bh % a.H) * D * a.wk;
+        const S* wtl = (const S*)a.wt_lo + (bh % a.H) * D * a.wk;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) tot[dt] = acc[dt] * a.tau;
+        for (int dt = 0; dt < DT; ++dt) tot[dt] = acc[dt] * a.tau + lowrank_tile<T>(du, wth, wtl, a.wk, g, qq, dt);
+    }
+    if (qtok < 0) return;
+    const size_t row = bh * N + qtok;
     unsigned lmask = MODE == kLeaf ? leaf_levels((tile / a.lt.per_leaf) * a.n_leaf, N, a.Lv, true) : 0u;
-    bool lr = true;
-    for (;;) {
+    while (lmask) {
         const float* src[2];
         bool use[2];
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-            src[j] = a.dq_lr + row * D;
-            use[j] = j == 0 && lr;
-            if (!use[j] && lmask) {
+            src[j] = a.part_dq;
+            use[j] = lmask != 0;
+            if (use[j]) {
                 const int l = __builtin_ctz(lmask);
                 lmask &= lmask - 1;
                 src[j] = a.part_dq + level_slot(bh, a.Lv, l, N, qtok, 1) * D;
-                use[j] = true;
             }
         }
-        lr = false;
         f32x4 x[2][DT];
 #pragma unroll
         for (int j = 0; j < 2; ++j)
@@ -258,7 +283,6 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
             if (use[j])
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt) tot[dt] += x[j][dt];
-        if (!lmask) break;
     }
     S* out = (S*)a.dQ + row * D;
 #pragma unroll
@@ -442,8 +466,8 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
             }
     }
 
-    if (ktok < 0) return;
     if (MODE == kLevels) {
+        if (ktok < 0) return;
         const size_t slot = level_slot(bh, a.Lv, level, N, ktok, 0);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
@@ -453,36 +477,40 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
         return;
     }
     // dK, dV = this pass + the low-rank parts + (leaf) the partials of the
-    // levels where the key was a past key, added in that order; the rows are
-    // fetched two (dK, dV) pairs at a time so their loads are in flight together
-    const size_t row = bh * N + ktok;
+    // levels where the key was a past key, added in that order; the partial
+    // rows are fetched two (dK, dV) pairs at a time so their loads are in
+    // flight together.  The low-rank dK part is a product across the wave's
+    // lanes, so every lane takes part (a lane without a key uses row 0).
     f32x4 tk[DT], tv[DT];
+    {
+        const S* du = (const S*)a.du_k + (bh * N + max(ktok, 0)) * a.wk;
+        const S* wth = (const S*)a.wt_hi + (bh % a.H) * D * a.wk;
+        const S* wtl = (const S*)a.wt_lo + (bh % a.H) * D * a.wk;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-        tk[dt] = akT[dt] * a.tau;
-        tv[dt] = avT[dt];
+        for (int dt = 0; dt < DT; ++dt) tk[dt] = akT[dt] * a.tau + lowrank_tile<T>(du, wth, wtl, a.wk, g, col, dt);
     }
+    if (ktok < 0) return;
+    const size_t row = bh * N + ktok;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) tv[dt] = avT[dt] + *(const f32x4*)(a.dv_lr + row * D + 16 * dt + 4 * g);
     unsigned lmask = MODE == kLeaf ? leaf_levels((tile / a.lt.per_leaf) * a.n_leaf, N, a.Lv, false) : 0u;
-    bool lr = true;
-    for (;;) {
+    while (lmask) {
         const float* sk_[2];
         const float* sv_[2];
         bool use[2];
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-            sk_[j] = a.dk_lr + row * D;
-            sv_[j] = a.dv_lr + row * D;
-            use[j] = j == 0 && lr;
-            if (!use[j] && lmask) {
+            sk_[j] = a.part_dk;
+            sv_[j] = a.part_dv;
+            use[j] = lmask != 0;
+            if (use[j]) {
                 const int l = __builtin_ctz(lmask);
                 lmask &= lmask - 1;
                 const size_t slot = level_slot(bh, a.Lv, l, N, ktok, 0);
                 sk_[j] = a.part_dk + slot * D;
                 sv_[j] = a.part_dv + slot * D;
-                use[j] = true;
             }
         }
-        lr = false;
         f32x4 xk[2][DT], xv[2][DT];
 #pragma unroll
         for (int j = 0; j < 2; ++j)
@@ -500,7 +528,6 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
                     tk[dt] += xk[j][dt];
                     tv[dt] += xv[j][dt];
                 }
-        if (!lmask) break;
     }
     S* ok_ = (S*)a.dK + row * D;
     S* ov = (S*)a.dV + row * D;
@@ -661,20 +688,31 @@ __global__ __launch_bounds__(BQ * 4, BQ == 64 ? 3 : 1) void sparse_bwd_block_ker
     // dK, dV of a lane's key: rows d = 16 dt + 4 g + i of the accumulators
     f32x4 akT[DT], avT[DT];
     auto store_dkv = [&](size_t bh, int level, int ktok) {
-        if (!(kFull || ktok >= 0)) return;
+        if (MODE == kLevels) {
+            if (!(kFull || ktok >= 0)) return;
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-            const int d0 = 16 * dt + 4 * g;
-            if (MODE == kLevels) {
+            for (int dt = 0; dt < DT; ++dt) {
+                const int d0 = 16 * dt + 4 * g;
                 const size_t slot = level_slot(bh, a.Lv, level, N, ktok, 0);
                 *(f32x4*)(a.part_dk + slot * D + d0) = akT[dt] * a.tau;
                 *(f32x4*)(a.part_dv + slot * D + d0) = avT[dt];
-            } else {
-                const size_t row = bh * N + ktok;
-                const f32x4 vk = akT[dt] * a.tau + *(const f32x4*)(a.dk_lr + row * D + d0);
-                const f32x4 vv = avT[dt] + *(const f32x4*)(a.dv_lr + row * D + d0);
-                store4<T>((S*)a.dK + row * D + d0, vk);
-                store4<T>((S*)a.dV + row * D + d0, vv);
+            }
+        } else {
+            // the low-rank dK part is a product across the wave's lanes: every
+            // lane takes part (a lane without a key uses row 0), then stores
+            const size_t wh = (bh % a.H) * D * a.wk;
+            const S* du = (const S*)a.du_k + (bh * N + max(ktok, 0)) * a.wk;
+            f32x4 lrk[DT];
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+                lrk[dt] = lowrank_tile<T>(du, (const S*)a.wt_hi + wh, (const S*)a.wt_lo + wh, a.wk, g, col, dt);
+            if (ktok < 0) return;
+            const size_t row = bh * N + ktok;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                const int d0 = 16 * dt + 4 * g;
+                store4<T>((S*)a.dK + row * D + d0, akT[dt] * a.tau + lrk[dt]);
+                store4<T>((S*)a.dV + row * D + d0, avT[dt] + *(const f32x4*)(a.dv_lr + row * D + d0));
             }
         }
     };
@@ -812,15 +850,20 @@ __global__ __launch_bounds__(BQ * 4, BQ == 64 ? 3 : 1) void sparse_bwd_block_ker
             for (int u = 0; u < PER_W; ++u) {
                 const int tix = w * PER_W + u, dt = tix / 4, qtile = tix % 4;
                 const int qtok = s_qt[16 * qtile + col];
-                if (!kFull && qtok < 0) continue;
                 const int d0 = 16 * dt + 4 * g;
                 if (MODE == kLevels) {
+                    if (!kFull && qtok < 0) continue;
                     float* out = a.part_dq + level_slot(bh, a.Lv, level, N, qtok, 1) * D + d0;
                     *(f32x4*)out = dq[u] * a.tau;
                 } else {
+                    // the low-rank part is a product across the wave's lanes:
+                    // every lane takes part (a lane without a query uses row 0)
+                    const size_t wh = (bh % a.H) * D * a.wk;
+                    const f32x4 lr = lowrank_tile<T>((const S*)a.du_q + (bh * N + max(qtok, 0)) * a.wk,
+                                                     (const S*)a.wt_hi + wh, (const S*)a.wt_lo + wh, a.wk, g, col, dt);
+                    if (qtok < 0) continue;
                     const size_t row = bh * N + qtok;
-                    const f32x4 v = dq[u] * a.tau + *(const f32x4*)(a.dq_lr + row * D + d0);
-                    store4<T>((S*)a.dQ + row * D + d0, v);
+                    store4<T>((S*)a.dQ + row * D + d0, dq[u] * a.tau + lr);
                 }
             }
         }
@@ -916,14 +959,15 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
 
 hipError_t launch_sparse_bwd(const Shape& s, const void* Q, const void* K, const void* V,
                              const void* dO, const int32_t* perm_q, const int32_t* perm_k,
-                             const float* rs, const float* dq_lr, const float* dk_lr,
-                             const float* dv_lr, float* part_dq, float* part_dk, float* part_dv,
+                             const float* rs, const void* du_q, const void* du_k, const void* wt_hi,
+                             const void* wt_lo, const float* dv_lr, float* part_dq, float* part_dk, float* part_dv,
                              void* dQ, void* dK, void* dV, hipStream_t st, int parts)
 {
     BArgs a;
     a.Q = Q; a.K = K; a.V = V; a.dO = dO;
     a.perm_q = perm_q; a.perm_k = perm_k; a.rs = rs;
-    a.dq_lr = dq_lr; a.dk_lr = dk_lr; a.dv_lr = dv_lr;
+    a.du_q = du_q; a.du_k = du_k; a.wt_hi = wt_hi; a.wt_lo = wt_lo; a.dv_lr = dv_lr;
+    a.wk = race_wk(s);
     a.part_dq = part_dq; a.part_dk = part_dk; a.part_dv = part_dv;
     a.dQ = dQ; a.dK = dK; a.dV = dV;
     a.H = s.H; a.N = s.N; a.k = s.k; a.Lv = s.Lv; a.n_leaf = s.n_leaf;
