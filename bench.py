@@ -82,6 +82,10 @@ def kernel_model(w, Lv: int, rules_G: int = 0, rules_lam: bool = False, rules_pa
                            leaf_inter * 6 * D + lr_flops)
     m["sparse_dkv_leaf"] = (bh * N * (4 * D * s + 12 + D * 4 + wk * s + 2 * D * s) + lvl_pos * 2 * D * 4,
                             leaf_inter * 8 * D + lr_flops)
+    # both leaf passes in one launch: each input row once, both low-rank parts,
+    # every level partial, dQ / dK / dV written once
+    m["sparse_leaf_bwd"] = (bh * N * (4 * D * s + 12 + 2 * wk * s + D * 4 + 3 * D * s) + lvl_pos * 3 * D * 4,
+                            leaf_inter * 14 * D + 2 * lr_flops)
     m["sparse_dq_blocks"] = (bh * N * (4 * D * s + D * s + 12 + wk * s), bh * N * min(k, N) * 6 * D + lr_flops)
     m["sparse_dkv_blocks"] = (bh * N * (4 * D * s + 2 * D * s + 12 + D * 4 + wk * s),
                               bh * N * min(k, N) * 8 * D + lr_flops)

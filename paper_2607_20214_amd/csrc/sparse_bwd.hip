@@ -106,7 +106,7 @@ __device__ __forceinline__ f32x4 lowrank_tile(const typename T::store_t* du_row,
 // dS^T in registers, dQ^T += K^T dS^T with K^T from the transposed LDS read.
 // ------------------------------------------------------------------------
 template <class T, int D, int MODE>
-__global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
+__device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, int b)
 {
     using S = typename T::store_t;
     using F = typename T::frag_t;
@@ -115,8 +115,6 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
     constexpr int PT = TD::PER_THREAD;
     __shared__ __attribute__((aligned(16))) S sk[TD::elems(kT)];
     __shared__ __attribute__((aligned(16))) S sv[TD::elems(kT)];
-    int tile, h, b;
-    xcd_tile(tile, h, b);
     const size_t bh = (size_t)b * a.H + h;
     const int N = a.N;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -297,7 +295,7 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
 // dK^T += Q^T dS with the transposed operands read from the query tiles.
 // ------------------------------------------------------------------------
 template <class T, int D, int MODE>
-__global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
+__device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h, int b)
 {
     using S = typename T::store_t;
     using F = typename T::frag_t;
@@ -308,8 +306,6 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
     __shared__ __attribute__((aligned(16))) S so[TD::elems(kT)];
     __shared__ float s_l2[kT], s_de[kT], s_sc[kT];
     __shared__ int s_ok[kT];
-    int tile, h, b;
-    xcd_tile(tile, h, b);
     const size_t bh = (size_t)b * a.H + h;
     const int N = a.N;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -536,6 +532,36 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
         store4<T>(ok_ + 16 * dt + 4 * g, tk[dt]);
         store4<T>(ov + 16 * dt + 4 * g, tv[dt]);
     }
+}
+
+template <class T, int D, int MODE>
+__global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
+{
+    int tile, h, b;
+    xcd_tile(tile, h, b);
+    sparse_dq_body<T, D, MODE>(a, tile, h, b);
+}
+
+template <class T, int D, int MODE>
+__global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
+{
+    int tile, h, b;
+    xcd_tile(tile, h, b);
+    sparse_dkv_body<T, D, MODE>(a, tile, h, b);
+}
+
+// Both leaf passes in one launch: the workgroups of a leaf (its query tiles
+// for dQ, then its key tiles for dK, dV) are consecutive, so they run on one
+// XCD at about the same time and the leaf's Q, K, V, dO rows, read by both
+// passes, come from that XCD's L2 the second time.
+template <class T, int D>
+__global__ __launch_bounds__(kThreads, 2) void sparse_leaf_bwd_kernel(BArgs a)
+{
+    int t2, h, b;
+    xcd_tile(t2, h, b);
+    const int per = a.lt.per_leaf, leaf = t2 / (2 * per), r = t2 - leaf * 2 * per;
+    if (r < per) sparse_dq_body<T, D, kLeaf>(a, leaf * per + r, h, b);
+    else sparse_dkv_body<T, D, kLeaf>(a, leaf * per + r - per, h, b);
 }
 
 // ------------------------------------------------------------------------
@@ -942,6 +968,11 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
             ELSAA_LAUNCH("sparse_dkv_levels", (sparse_dkv_kernel<T, D, kLevels>), grid, dim3(kThreads), 0, st, a);
             if ((e = hipGetLastError()) != hipSuccess) return e;
         }
+    }
+    if ((parts & kSparseFinal) == kSparseFinal) {
+        dim3 grid(2 * a.lt.leaf_tiles(), s.H, s.B);
+        ELSAA_LAUNCH("sparse_leaf_bwd", (sparse_leaf_bwd_kernel<T, D>), grid, dim3(kThreads), 0, st, a);
+        return hipGetLastError();
     }
     dim3 grid(a.lt.leaf_tiles(), s.H, s.B);
     if (parts & kSparseFinalQ) {
