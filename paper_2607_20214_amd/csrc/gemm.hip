@@ -204,6 +204,245 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GArgs a)
     }
 }
 
+// ---------------------------------------------------------------- large tiles
+// Workgroup tile 256 x 256 x 64 for products whose M and N are multiples of
+// 256 and K of 64: four waves in a 2 x 2 grid, each a 128 x 128 block of
+// 8 x 8 accumulators (256 float32 per lane, held in the accumulation
+// registers; one workgroup per compute unit).  Per 32-wide k-step a wave
+// reads 16 operand fragments for 64 matrix-core operations, half the LDS
+// traffic per operation of the 64 x 64 wave block, and one K-tile keeps the
+// matrix cores busy long enough to cover the next tile's global loads.
+namespace big {
+
+constexpr int BM = 256, BN = 256, BK = 64;
+constexpr int kLdD = BK + 8;       // [rows][k] row stride
+constexpr int kLdT = BM + 16;      // [k][rows] row stride
+constexpr int kTile = BM * kLdD;   // elements of one operand tile (either orientation)
+static_assert(BK * kLdT <= kTile, "tile orientations fit one buffer");
+static_assert(BK == 64, "two 32-wide k-steps per K-tile");
+constexpr int kChunks = BM * BK / 8 / kThreads;   // 16-byte chunks per thread per operand tile
+
+// Element offset of (row r, column c) split into a row part and a column
+// part.  Within an aligned block of rows that does not cross a sequence
+// (head-major operands have seq % 256 == 0 on this path), the row part is
+// affine in r with stride row_stride(); blk0 is the block's first row.
+__device__ __forceinline__ int64_t row_part(const Mat& m, int r, int blk0)
+{
+    if (m.heads == 0) return (int64_t)r * m.ld;
+    const int b = blk0 / m.seq;
+    return ((int64_t)r + (int64_t)b * (m.heads - 1) * m.seq) << m.dh_shift;
+}
+__device__ __forceinline__ int64_t row_stride(const Mat& m) { return m.heads == 0 ? m.ld : ((int64_t)1 << m.dh_shift); }
+__device__ __forceinline__ int64_t col_part(const Mat& m, int c)
+{
+    if (m.heads == 0) return c;
+    return (((int64_t)(c >> m.dh_shift) * m.seq) << m.dh_shift) + (c & ((1 << m.dh_shift) - 1));
+}
+
+// Global -> registers: K-tile [k0, k0 + 64) of the operand rows [x0, x0 + 256).
+// KMAJOR: stored [k][x], thread tx loads k-rows k0 + tx / 32 + 8 c at columns
+// x0 + 8 (tx % 32); else stored [x][k], rows x0 + tx / 8 + 32 c at k0 + 8 (tx % 8).
+// Each address is a per-thread offset fixed for the whole tile plus a
+// workgroup-uniform offset of the K-tile: the rows of a K-tile (KMAJOR) or of
+// the tile (else) lie in one sequence, and 64 consecutive k of a [x][k]
+// operand in one head (head widths >= 64 on this path).
+template <bool KMAJOR>
+struct Stream {
+    const uint16_t* p;
+    int64_t rs;      // element stride between rows of one sequence
+    int64_t toff;    // this thread's fixed element offset
+    __device__ __forceinline__ void init(const Mat& m, int x0)
+    {
+        const int tx = threadIdx.x;
+        p = (const uint16_t*)m.p;
+        rs = row_stride(m);
+        if (KMAJOR) toff = (int64_t)(tx >> 5) * rs + col_part(m, x0 + (tx & 31) * 8);
+        else toff = row_part(m, x0 + (tx >> 3), x0) + (tx & 7) * 8;
+    }
+    __device__ __forceinline__ void load(const Mat& m, int k0, uint4 (&r)[kChunks]) const
+    {
+        const uint16_t* q = p + (KMAJOR ? row_part(m, k0, k0) : col_part(m, k0));
+#pragma unroll
+        for (int c = 0; c < kChunks; ++c) r[c] = ldg16(q + (KMAJOR ? 8 : 32) * c * rs + toff);
+    }
+};
+
+template <bool KMAJOR>
+__device__ __forceinline__ void store(uint16_t* s, const uint4 (&r)[kChunks])
+{
+    const int tx = threadIdx.x;
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+        if (KMAJOR) *(uint4*)&s[((tx >> 5) + 8 * c) * kLdT + (tx & 31) * 8] = r[c];
+        else *(uint4*)&s[((tx >> 3) + 32 * c) * kLdD + (tx & 7) * 8] = r[c];
+    }
+}
+
+// Operand fragment of rows x0 .. x0+15 for k-step ks.
+template <bool KMAJOR>
+__device__ __forceinline__ bf16x8 frag(const uint16_t* s, int x0, int ks)
+{
+    const int lane = threadIdx.x & 63, g = lane >> 4, i = lane & 15;
+    if (KMAJOR) {
+        const uint16_t* p = &s[(32 * ks + 8 * g + (i >> 2)) * kLdT + x0 + 4 * (i & 3)];
+        const bf16x4 lo = lds_read_tr4(p), hi = lds_read_tr4(p + 4 * kLdT);
+        return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    }
+    return *(const bf16x8*)&s[(x0 + i) * kLdD + 32 * ks + 8 * g];
+}
+
+// acc += a x b with acc tied to accumulation registers: the 64 accumulators
+// fill all 256 of them, and with the builtin the register allocator moves
+// some through vector registers on every iteration.  The compiler does not
+// see this as a matrix-core instruction: the statements keep program order
+// (an accumulator is reused only after the 63 others), and reads of acc
+// after the last one are separated by the wait states in mfma_drain.
+__device__ __forceinline__ void mfma_acc(f32x4& acc, bf16x8 a, bf16x8 b)
+{
+    asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+__device__ __forceinline__ void mfma_drain()
+{
+    asm volatile("s_nop 15\n\ts_nop 15\n\ts_nop 15\n\ts_nop 15" ::: "memory");
+}
+
+template <bool TA, bool BKN, bool OUT_BF16>
+__global__ __launch_bounds__(kThreads, 1) void gemm_big_kernel(GArgs a)
+{
+    __shared__ __attribute__((aligned(16))) uint16_t lds[4][kTile];
+    uint16_t(*sa)[kTile] = lds;
+    uint16_t(*sb)[kTile] = lds + 2;
+    int sp, tm, tn;
+    tile_of(a, sp, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int kb = sp * a.kper, ke = min(a.K, kb + a.kper);
+    const int nkt = (ke - kb) / BK;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int wm = w & 1, wn = w >> 1;
+    const int g = lane >> 4, col = lane & 15;
+
+    f32x4 acc[8][8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[j][i] = f32x4{0, 0, 0, 0};
+
+    Stream<TA> gA;
+    Stream<BKN> gB;
+    gA.init(a.A, m0);
+    gB.init(a.B, n0);
+    // Pipeline: LDS buffer t & 1 holds K-tile t, the registers K-tile t + 1.
+    // An iteration runs k-step 0 of tile t (its fragments already read)
+    // while reading k-step 1's fragments, stores tile t + 1 to the other
+    // buffer, passes the one barrier, issues the global loads of tile t + 2,
+    // then runs k-step 1 while reading k-step 0 of tile t + 1.  LDS reads
+    // thus always proceed under matrix-core work, and a global load has one
+    // iteration to arrive.
+    uint4 ra[kChunks], rb[kChunks];
+    gA.load(a.A, kb, ra);
+    gB.load(a.B, kb, rb);
+    store<TA>(sa[0], ra);
+    store<BKN>(sb[0], rb);
+    if (nkt > 1) {
+        gA.load(a.A, kb + BK, ra);
+        gB.load(a.B, kb + BK, rb);
+    }
+    __syncthreads();
+    bf16x8 x0[8], y0[8], x1[8], y1[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        x0[j] = frag<BKN>(sb[0], 128 * wn + 16 * j, 0);
+        y0[j] = frag<TA>(sa[0], 128 * wm + 16 * j, 0);
+    }
+
+    for (int t = 0; t < nkt; ++t) {
+        const uint16_t* A_ = sa[t & 1];
+        const uint16_t* B_ = sb[t & 1];
+        const uint16_t* An = sa[(t + 1) & 1];
+        const uint16_t* Bn = sb[(t + 1) & 1];
+        // k-step 0 of tile t; group i also reads fragment i of k-step 1
+        // (the order is pinned so each group waits only for its own reads)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            x1[i] = frag<BKN>(B_, 128 * wn + 16 * i, 1);
+            y1[i] = frag<TA>(A_, 128 * wm + 16 * i, 1);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) mfma_acc(acc[j][i], x0[j], y0[i]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if (t + 1 < nkt) {
+            store<TA>(sa[(t + 1) & 1], ra);
+            store<BKN>(sb[(t + 1) & 1], rb);
+        }
+        __syncthreads();
+        if (t + 2 < nkt) {
+            gA.load(a.A, kb + (t + 2) * BK, ra);
+            gB.load(a.B, kb + (t + 2) * BK, rb);
+        }
+        // k-step 1 of tile t; group i also reads fragment i of k-step 0 of
+        // tile t + 1 (after the last tile these reads are unused)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            x0[i] = frag<BKN>(Bn, 128 * wn + 16 * i, 0);
+            y0[i] = frag<TA>(An, 128 * wm + 16 * i, 0);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) mfma_acc(acc[j][i], x1[j], y1[i]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+    __syncthreads();
+    mfma_drain();
+
+    if (OUT_BF16 && a.splits == 1) {
+        // bf16 output: the float32 accumulators pass through LDS (each wave
+        // its own 64 x 128 block per half, row stride 132) and leave as
+        // 16-byte pieces of C rows.  Accumulators are only ever stored, never
+        // operated on, so they stay in the accumulation registers.
+        constexpr int kLdC = 132;
+        float* cs = (float*)&lds[0][0] + w * 64 * kLdC;
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 8; ++j) *(f32x4*)&cs[(16 * i + col) * kLdC + 16 * j + 4 * g] = acc[j][4 * hh + i];
+            __syncthreads();
+#pragma unroll 4
+            for (int it = 0; it < 16; ++it) {
+                const int r = 4 * it + (lane >> 4), c8 = (lane & 15) * 8;
+                const f32x4 x = *(const f32x4*)&cs[r * kLdC + c8];
+                const f32x4 y = *(const f32x4*)&cs[r * kLdC + c8 + 4];
+                uint4 o;
+                o.x = f32_to_bf16(x[0]) | ((uint32_t)f32_to_bf16(x[1]) << 16);
+                o.y = f32_to_bf16(x[2]) | ((uint32_t)f32_to_bf16(x[3]) << 16);
+                o.z = f32_to_bf16(y[0]) | ((uint32_t)f32_to_bf16(y[1]) << 16);
+                o.w = f32_to_bf16(y[2]) | ((uint32_t)f32_to_bf16(y[3]) << 16);
+                const int m = m0 + 128 * wm + 64 * hh + r, n = n0 + 128 * wn + c8;
+                stg16((uint16_t*)a.C.p + row_part(a.C, m, m0) + col_part(a.C, n), o);
+            }
+            __syncthreads();
+        }
+        return;
+    }
+    // float32 output or split partials: lane holds
+    // C[m0 + 128 wm + 16 i + col][n0 + 128 wn + 16 j + 4 g + (0..3)]
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int m = m0 + 128 * wm + 16 * i + col;
+        const int64_t ro = a.splits > 1 ? ((int64_t)sp * a.M + m) * a.N : row_part(a.C, m, m0);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int n = n0 + 128 * wn + 16 * j + 4 * g;
+            if (a.splits > 1) *(f32x4*)(a.part + ro + n) = acc[j][i];
+            else *(f32x4*)((float*)a.C.p + ro + col_part(a.C, n)) = acc[j][i];
+        }
+    }
+}
+
+}  // namespace big
+
 // C = sum over splits of the partials, in split order.
 template <bool OUT_BF16>
 __global__ __launch_bounds__(256) void gemm_reduce_kernel(const float* part, Mat C, int M, int N, int splits)
@@ -225,23 +464,43 @@ __global__ __launch_bounds__(256) void gemm_reduce_kernel(const float* part, Mat
 }
 
 struct Plan {
+    bool big;                 // 256 x 256 tiles (gemm_big_kernel)
     int tiles_m, tiles_n, splits, kper;
     size_t ws_bytes;
 };
 
+// The large-tile kernel takes whole tiles only, head-major operands whose
+// sequences hold whole 256-row blocks (so no tile or K-tile crosses one) and
+// head-major A / B with heads at least 64 wide.
+bool big_fits(const elsaa_gemm_desc* d)
+{
+    if (d->M % big::BM || d->N % big::BN || d->K % big::BK) return false;
+    const bool hm = d->a_heads > 0 || d->b_heads > 0 || d->c_heads > 0;
+    if (hm && (d->seq <= 0 || d->seq % 256 != 0)) return false;
+    const int a_cols = d->trans_a ? d->M : d->K, b_cols = d->trans_b ? d->K : d->N;
+    if (d->a_heads > 0 && a_cols / d->a_heads < 64) return false;
+    if (d->b_heads > 0 && b_cols / d->b_heads < 64) return false;
+    return true;
+}
+
 Plan plan_of(const elsaa_gemm_desc* d)
 {
     Plan p;
-    p.tiles_m = (d->M + BM - 1) / BM;
-    p.tiles_n = (d->N + BN - 1) / BN;
+    p.big = big_fits(d);
+    const int bm = p.big ? big::BM : BM, bn = p.big ? big::BN : BN, bk = p.big ? big::BK : BK;
+    // workgroups resident per compute unit (256 compute units)
+    const int fill = p.big ? 256 : 512;
+    p.tiles_m = (d->M + bm - 1) / bm;
+    p.tiles_n = (d->N + bn - 1) / bn;
     const int tiles = p.tiles_m * p.tiles_n;
-    const int ktiles = (d->K + BK - 1) / BK;
+    const int ktiles = (d->K + bk - 1) / bk;
     int splits = 1;
-    // fewer than two workgroups per compute unit and a long K: split K,
-    // keeping at least 8 K-tiles per split
-    if (tiles < 512 && ktiles >= 16) splits = std::min((512 + tiles - 1) / tiles, ktiles / 8);
+    // fewer tiles than resident workgroups and a long K: split K into as
+    // many parts as fit in one round of resident workgroups, keeping at
+    // least 8 K-tiles per split
+    if (tiles < fill && ktiles >= 16) splits = std::max(1, std::min(fill / tiles, ktiles / 8));
     const int per = (ktiles + splits - 1) / splits;
-    p.kper = per * BK;
+    p.kper = per * bk;
     p.splits = (d->K + p.kper - 1) / p.kper;
     p.ws_bytes = p.splits > 1 ? (size_t)p.splits * d->M * d->N * sizeof(float) : 0;
     return p;
@@ -338,8 +597,10 @@ int elsaa_gemm(const elsaa_gemm_desc* d, const void* A, const void* B, void* C, 
     const dim3 grid(p.tiles_m * p.tiles_n * p.splits), block(kThreads);
     const bool bkn = d->trans_b == 0, out_bf16 = d->c_dtype == ELSAA_BF16;
 #define ELSAA_GEMM_CASE(TA, BKN, OB)                                                                 \
-    if (d->trans_a == TA && bkn == BKN && out_bf16 == OB)                                             \
-        ELSAA_LAUNCH("gemm", (gemm_kernel<TA, BKN, OB>), grid, block, 0, stream, a);
+    if (d->trans_a == TA && bkn == BKN && out_bf16 == OB) {                                           \
+        if (p.big) ELSAA_LAUNCH("gemm", (big::gemm_big_kernel<TA, BKN, OB>), grid, block, 0, stream, a); \
+        else ELSAA_LAUNCH("gemm", (gemm_kernel<TA, BKN, OB>), grid, block, 0, stream, a);              \
+    }
     ELSAA_GEMM_CASE(0, 0, 0) ELSAA_GEMM_CASE(0, 0, 1) ELSAA_GEMM_CASE(0, 1, 0) ELSAA_GEMM_CASE(0, 1, 1)
     ELSAA_GEMM_CASE(1, 0, 0) ELSAA_GEMM_CASE(1, 0, 1) ELSAA_GEMM_CASE(1, 1, 0) ELSAA_GEMM_CASE(1, 1, 1)
 #undef ELSAA_GEMM_CASE

@@ -34,7 +34,9 @@ def _check(got, ref, out_dtype, what=""):
         assert (err <= bound).all(), f"{what}: worst element ratio {(err / bound).max():.3f}"
 
 
-SHAPES = [(200, 136, 72), (384, 256, 320), (8, 8, 8)]
+# ragged and small shapes (128 x 128 tiles) and whole 256 x 256 tiles with K
+# a multiple of 64 (the large-tile kernel)
+SHAPES = [(200, 136, 72), (384, 256, 320), (8, 8, 8), (512, 256, 128), (256, 768, 192)]
 
 
 @pytest.mark.parametrize("shape,ta,tb,od", [
@@ -62,6 +64,19 @@ def test_gemm_split_k(ta, od):
     _check(got, oracle.gemm(A, B, ta, False), od, "split-K")
 
 
+@pytest.mark.parametrize("ta,tb,od", [(1, 0, torch.float32), (1, 1, torch.bfloat16), (0, 1, torch.float32)])
+def test_gemm_split_k_large_tiles(ta, tb, od):
+    """Whole 256 x 256 tiles with a long K: the large-tile kernel split over K."""
+    M, N, K = 256, 512, 8192
+    A = W.random_matrix(45 + ta, 1, (K, M) if ta else (M, K))
+    B = W.random_matrix(45 + tb, 2, (N, K) if tb else (K, N))
+    got = E.gemm(_t(A), _t(B), bool(ta), bool(tb), out_dtype=od)
+    torch.cuda.synchronize()
+    desc = E._GemmDesc(M, N, K, ta, tb, M if ta else K, K if tb else N, N, 0, 0, 0, 0, 0)
+    assert E.gemm_workspace_bytes(desc) > 0
+    _check(got, oracle.gemm(A, B, ta, tb), od, "split-K large tiles")
+
+
 def test_gemm_repeatable():
     A = _t(W.random_matrix(50, 1, (4096, 512)))
     B = _t(W.random_matrix(50, 2, (4096, 256)))
@@ -71,10 +86,11 @@ def test_gemm_repeatable():
     assert torch.equal(r1, r2)
 
 
-def test_block_projections_head_major():
+@pytest.mark.parametrize("Bb,S,H,dh", [(2, 96, 4, 16), (2, 256, 4, 64)])
+def test_block_projections_head_major(Bb, S, H, dh):
     """Every product of one attention block (fwd and bwd) with the attention
-    tensors in head-major [B, H, S, dh] storage."""
-    Bb, S, H, dh = 2, 96, 4, 16
+    tensors in head-major [B, H, S, dh] storage (the second size takes the
+    large-tile kernel for all six products)."""
     dm = H * dh
     X = W.random_matrix(60, 1, (Bb * S, dm))
     Wqkv = W.random_matrix(60, 2, (dm, 3 * dm), 0.1)
