@@ -221,6 +221,7 @@ constexpr int kTile = BM * kLdD;   // elements of one operand tile (either orien
 static_assert(BK * kLdT <= kTile, "tile orientations fit one buffer");
 static_assert(BK == 64, "two 32-wide k-steps per K-tile");
 constexpr int kChunks = BM * BK / 8 / kThreads;   // 16-byte chunks per thread per operand tile
+static_assert(kChunks == 8, "one chunk of each operand per group of eight operations");
 
 // Element offset of (row r, column c) split into a row part and a column
 // part.  Within an aligned block of rows that does not cross a sequence
@@ -259,23 +260,35 @@ struct Stream {
         if (KMAJOR) toff = (int64_t)(tx >> 5) * rs + col_part(m, x0 + (tx & 31) * 8);
         else toff = row_part(m, x0 + (tx >> 3), x0) + (tx & 7) * 8;
     }
+    // first element of K-tile k0 for chunk 0 (uniform part only)
+    __device__ __forceinline__ const uint16_t* tile(const Mat& m, int k0) const
+    {
+        return p + (KMAJOR ? row_part(m, k0, k0) : col_part(m, k0));
+    }
+    __device__ __forceinline__ uint4 chunk(const uint16_t* q, int c) const
+    {
+        return ldg16(q + (KMAJOR ? 8 : 32) * c * rs + toff);
+    }
     __device__ __forceinline__ void load(const Mat& m, int k0, uint4 (&r)[kChunks]) const
     {
-        const uint16_t* q = p + (KMAJOR ? row_part(m, k0, k0) : col_part(m, k0));
+        const uint16_t* q = tile(m, k0);
 #pragma unroll
-        for (int c = 0; c < kChunks; ++c) r[c] = ldg16(q + (KMAJOR ? 8 : 32) * c * rs + toff);
+        for (int c = 0; c < kChunks; ++c) r[c] = chunk(q, c);
     }
 };
 
 template <bool KMAJOR>
-__device__ __forceinline__ void store(uint16_t* s, const uint4 (&r)[kChunks])
+__device__ __forceinline__ void store1(uint16_t* s, uint4 v, int c)
 {
     const int tx = threadIdx.x;
+    if (KMAJOR) *(uint4*)&s[((tx >> 5) + 8 * c) * kLdT + (tx & 31) * 8] = v;
+    else *(uint4*)&s[((tx >> 3) + 32 * c) * kLdD + (tx & 7) * 8] = v;
+}
+template <bool KMAJOR>
+__device__ __forceinline__ void store(uint16_t* s, const uint4 (&r)[kChunks])
+{
 #pragma unroll
-    for (int c = 0; c < kChunks; ++c) {
-        if (KMAJOR) *(uint4*)&s[((tx >> 5) + 8 * c) * kLdT + (tx & 31) * 8] = r[c];
-        else *(uint4*)&s[((tx >> 3) + 32 * c) * kLdD + (tx & 7) * 8] = r[c];
-    }
+    for (int c = 0; c < kChunks; ++c) store1<KMAJOR>(s, r[c], c);
 }
 
 // Operand fragment of rows x0 .. x0+15 for k-step ks.
@@ -332,20 +345,32 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_big_kernel(GArgs a)
     gA.init(a.A, m0);
     gB.init(a.B, n0);
     // Pipeline: LDS buffer t & 1 holds K-tile t, the registers K-tile t + 1.
-    // An iteration runs k-step 0 of tile t (its fragments already read)
-    // while reading k-step 1's fragments, stores tile t + 1 to the other
-    // buffer, passes the one barrier, issues the global loads of tile t + 2,
-    // then runs k-step 1 while reading k-step 0 of tile t + 1.  LDS reads
-    // thus always proceed under matrix-core work, and a global load has one
-    // iteration to arrive.
+    // The first half of an iteration runs k-step 0 of tile t (fragments
+    // already read) in eight groups of eight operations; before group i it
+    // reads fragment pair i of k-step 1, stores chunk i of both operands of
+    // tile t + 1 to the other buffer and reloads those registers with chunk
+    // i of tile t + 2.  After the one barrier, the second half runs k-step 1
+    // the same way, reading k-step 0 of tile t + 1.  Spreading the loads and
+    // stores keeps the in-order wave from stalling on a burst of memory
+    // instructions while the matrix cores idle, and each load has a whole
+    // iteration to arrive.  Tile indices past the end are clamped to the
+    // last tile (the redundant loads and stores are never read), so the
+    // groups carry no branches.
     uint4 ra[kChunks], rb[kChunks];
     gA.load(a.A, kb, ra);
     gB.load(a.B, kb, rb);
     store<TA>(sa[0], ra);
     store<BKN>(sb[0], rb);
-    if (nkt > 1) {
-        gA.load(a.A, kb + BK, ra);
-        gB.load(a.B, kb + BK, rb);
+    {
+        // same issue order as the loop's loads (A and B chunks alternating),
+        // so the stores' waits count exactly across the loop entry
+        const uint16_t* qa = gA.tile(a.A, kb + min(1, nkt - 1) * BK);
+        const uint16_t* qb = gB.tile(a.B, kb + min(1, nkt - 1) * BK);
+#pragma unroll
+        for (int i = 0; i < kChunks; ++i) {
+            ra[i] = gA.chunk(qa, i);
+            rb[i] = gB.chunk(qb, i);
+        }
     }
     __syncthreads();
     bf16x8 x0[8], y0[8], x1[8], y1[8];
@@ -358,30 +383,25 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_big_kernel(GArgs a)
     for (int t = 0; t < nkt; ++t) {
         const uint16_t* A_ = sa[t & 1];
         const uint16_t* B_ = sb[t & 1];
-        const uint16_t* An = sa[(t + 1) & 1];
-        const uint16_t* Bn = sb[(t + 1) & 1];
-        // k-step 0 of tile t; group i also reads fragment i of k-step 1
-        // (the order is pinned so each group waits only for its own reads)
+        uint16_t* An = sa[(t + 1) & 1];
+        uint16_t* Bn = sb[(t + 1) & 1];
+        const int k2 = kb + min(t + 2, nkt - 1) * BK;
+        const uint16_t* qa = gA.tile(a.A, k2);
+        const uint16_t* qb = gB.tile(a.B, k2);
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             x1[i] = frag<BKN>(B_, 128 * wn + 16 * i, 1);
             y1[i] = frag<TA>(A_, 128 * wm + 16 * i, 1);
+            store1<TA>(An, ra[i], i);
+            store1<BKN>(Bn, rb[i], i);
+            ra[i] = gA.chunk(qa, i);
+            rb[i] = gB.chunk(qb, i);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int j = 0; j < 8; ++j) mfma_acc(acc[j][i], x0[j], y0[i]);
             __builtin_amdgcn_sched_barrier(0);
         }
-        if (t + 1 < nkt) {
-            store<TA>(sa[(t + 1) & 1], ra);
-            store<BKN>(sb[(t + 1) & 1], rb);
-        }
         __syncthreads();
-        if (t + 2 < nkt) {
-            gA.load(a.A, kb + (t + 2) * BK, ra);
-            gB.load(a.B, kb + (t + 2) * BK, rb);
-        }
-        // k-step 1 of tile t; group i also reads fragment i of k-step 0 of
-        // tile t + 1 (after the last tile these reads are unused)
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             x0[i] = frag<BKN>(Bn, 128 * wn + 16 * i, 0);
