@@ -156,21 +156,29 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
     if (a.causal) uk.load(Uk, t_beg, a.N);
     for (int t0 = t_beg; t0 < t_end; t0 += kC) {
         __syncthreads();
-        stage_r<T, D>(sm.dn, dO, t0, a.N);
-        if (threadIdx.x < kC) {
-            const bool in = t0 + threadIdx.x < a.N;
-            sm.dden[threadIdx.x] = in ? dden[t0 + threadIdx.x] : 0.f;
-            sm.sc[threadIdx.x] = in ? sclr[t0 + threadIdx.x] : 0.f;
-        }
+        // every global load of the chunk is issued first; the features (vector
+        // work) run while they are in flight, then the rows go to LDS
+        StageR<T, D> sdn;
+        sdn.load(dO, t0, a.N, nullptr);
+        StageT<T, D> svt;
+        if (a.causal) svt.load(V, t0, a.N, nullptr, 1.f);
+        const bool in = threadIdx.x < kC && t0 + (int)threadIdx.x < a.N;
+        const float ddv = in ? dden[t0 + threadIdx.x] : 0.f, scv = in ? sclr[t0 + threadIdx.x] : 0.f;
         features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, nullptr, nullptr, sm.ts);
-        if (a.causal) {
-            stage_t<T, D>(sm.vt, V, t0, a.N);
-            features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, nullptr, sm.pkt, nullptr);
+        if (a.causal) features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, nullptr, sm.pkt, nullptr);
+        sdn.store(sm.dn, false);
+        if (a.causal) svt.store(sm.vt, false);
+        if (threadIdx.x < kC) {
+            sm.dden[threadIdx.x] = ddv;
+            sm.sc[threadIdx.x] = scv;
         }
         __syncthreads();
-        if (t0 + kC < t_end) {
-            uq.load(Uq, t0 + kC, a.N);
-            if (a.causal) uk.load(Uk, t0 + kC, a.N);
+        {
+            // next chunk's projections (the last chunk reloads its own, so
+            // the loads are unconditional)
+            const int tn = t0 + kC < t_end ? t0 + kC : t0;
+            uq.load(Uq, tn, a.N);
+            if (a.causal) uk.load(Uk, tn, a.N);
         }
         if (a.causal) {
             // G rows [16w, 16w + 16): sc_lr,i <dO_i, V_j> + dDen_i for j <= i,
@@ -299,17 +307,24 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
     for (int c = nch - 1; c >= 0; --c) {
         const int t0 = t_beg + c * kC;
         __syncthreads();
-        stage_r<T, D>(sm.vr, V, t0, a.N);
-        if (threadIdx.x < kC) sm.dden[threadIdx.x] = (t0 + threadIdx.x < a.N) ? dden[t0 + threadIdx.x] : 0.f;
+        // loads first, features under them, then the LDS stores
+        StageR<T, D> svr;
+        svr.load(V, t0, a.N, nullptr);
+        StageT<T, D> sdn;
+        if (a.causal) sdn.load(dO, t0, a.N, sclr, a.inv_L);
+        const bool in = threadIdx.x < kC && t0 + (int)threadIdx.x < a.N;
+        const float ddv = in ? dden[t0 + threadIdx.x] : 0.f;
         features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, nullptr, nullptr, sm.ts);
-        if (a.causal) {
-            stage_t<T, D>(sm.dnt, dO, t0, a.N, sclr, a.inv_L);
-            features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, nullptr, sm.pqt, nullptr);
-        }
+        if (a.causal) features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, nullptr, sm.pqt, nullptr);
+        svr.store(sm.vr, false);
+        if (a.causal) sdn.store(sm.dnt, true);
+        if (threadIdx.x < kC) sm.dden[threadIdx.x] = ddv;
         __syncthreads();
-        if (c > 0) {
-            uk.load(Uk, t0 - kC, a.N);
-            if (a.causal) uq.load(Uq, t0 - kC, a.N);
+        {
+            // previous chunk's projections (unconditional: chunk 0 reloads its own)
+            const int tn = c > 0 ? t0 - kC : t0;
+            uk.load(Uk, tn, a.N);
+            if (a.causal) uq.load(Uq, tn, a.N);
         }
         if (a.causal) {
             // G' rows j in [16w, 16w + 16): (<V_j, dNum_i> + dDen_i) / L for
@@ -429,15 +444,20 @@ __global__ __launch_bounds__(kThreads, 2) void race_dv_kernel(LbArgs a)
     for (int c = nch - 1; c >= 0; --c) {
         const int t0 = t_beg + c * kC;
         __syncthreads();
+        // loads first, features under them, then the LDS stores
+        StageT<T, D> sdn;
+        if (a.causal) sdn.load(dO, t0, a.N, sclr, a.inv_L);
         features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, sm.pk, nullptr, nullptr);
         if (a.causal) {
-            stage_t<T, D>(sm.dnt, dO, t0, a.N, sclr, a.inv_L);
             features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, sm.pq, sm.pqt, nullptr);
+            sdn.store(sm.dnt, true);
         }
         __syncthreads();
-        if (c > 0) {
-            uk.load(Uk, t0 - kC, a.N);
-            if (a.causal) uq.load(Uq, t0 - kC, a.N);
+        {
+            // previous chunk's projections (unconditional: chunk 0 reloads its own)
+            const int tn = c > 0 ? t0 - kC : t0;
+            uk.load(Uk, tn, a.N);
+            if (a.causal) uq.load(Uq, tn, a.N);
         }
         if (a.causal) {
             // M' rows j in [16w, 16w + 16): <phi(k_j), phi(q_i)> for i >= j,

@@ -97,18 +97,25 @@ struct StageT {
     static constexpr int ITEMS = (kC / 2) * CH, PT = ITEMS / kThreads;
     static_assert(ITEMS % kThreads == 0, "staging split");
     uint4 va[PT], vb[PT];
-    float sa[PT], sb[PT];
+    float sa[PT], sb[PT];   // row scales as loaded (mul is applied in store())
+    float mul_;
+    int t0_, n_;
+    // Rows past N are loaded clamped to row N - 1 and zeroed in store(), so
+    // the loads carry no per-lane branches and later waits count exactly.
     __device__ __forceinline__ void load(const S* X, int t0, int N, const float* scale, float mul)
     {
+        t0_ = t0;
+        n_ = N;
+        mul_ = mul;
 #pragma unroll
         for (int j = 0; j < PT; ++j) {
             const int it = threadIdx.x + j * kThreads;
             const int p = it & (kC / 2 - 1), c = it / (kC / 2);
-            const int r0 = t0 + 2 * p, r1 = r0 + 1;
-            va[j] = r0 < N ? ldg16(X + (size_t)r0 * D + c * PER) : make_uint4(0, 0, 0, 0);
-            vb[j] = r1 < N ? ldg16(X + (size_t)r1 * D + c * PER) : make_uint4(0, 0, 0, 0);
-            sa[j] = (scale && r0 < N) ? scale[r0] * mul : mul;
-            sb[j] = (scale && r1 < N) ? scale[r1] * mul : mul;
+            const int r0 = min(t0 + 2 * p, N - 1), r1 = min(t0 + 2 * p + 1, N - 1);
+            va[j] = ldg16(X + (size_t)r0 * D + c * PER);
+            vb[j] = ldg16(X + (size_t)r1 * D + c * PER);
+            sa[j] = scale ? scale[r0] : 1.f;
+            sb[j] = scale ? scale[r1] : 1.f;
         }
     }
     // the two rows of an item are adjacent in the transposed tile: one
@@ -119,14 +126,15 @@ struct StageT {
         for (int j = 0; j < PT; ++j) {
             const int it = threadIdx.x + j * kThreads;
             const int p = it & (kC / 2 - 1), c = it / (kC / 2);
+            const bool in0 = t0_ + 2 * p < n_, in1 = t0_ + 2 * p + 1 < n_;
             const S* ea = (const S*)&va[j];
             const S* eb = (const S*)&vb[j];
 #pragma unroll
             for (int e = 0; e < PER; ++e) {
-                S x0 = ea[e], x1 = eb[e];
+                S x0 = in0 ? ea[e] : T::store(0.f), x1 = in1 ? eb[e] : T::store(0.f);
                 if (scaled) {
-                    x0 = T::store(T::load(x0) * sa[j]);
-                    x1 = T::store(T::load(x1) * sb[j]);
+                    x0 = T::store(T::load(x0) * (sa[j] * mul_));
+                    x1 = T::store(T::load(x1) * (sb[j] * mul_));
                 }
                 S* dst = &xt[c * PER + e][2 * p];
                 if constexpr (T::bytes == 2)
@@ -158,15 +166,19 @@ struct StageR {
     static_assert(ITEMS % kThreads == 0, "staging split");
     uint4 v[PT];
     float sc[PT];
+    int t0_, n_;
+    // rows past N: loaded clamped, zeroed in store() (see StageT)
     __device__ __forceinline__ void load(const S* X, int t0, int N, const float* scale)
     {
+        t0_ = t0;
+        n_ = N;
 #pragma unroll
         for (int j = 0; j < PT; ++j) {
             const int it = threadIdx.x + j * kThreads;
             const int row = it % kC, c = it / kC;
-            const int r = t0 + row;
-            v[j] = r < N ? ldg16(X + (size_t)r * D + c * PER) : make_uint4(0, 0, 0, 0);
-            sc[j] = (scale && r < N) ? scale[r] : 0.f;
+            const int r = min(t0 + row, N - 1);
+            v[j] = ldg16(X + (size_t)r * D + c * PER);
+            sc[j] = scale ? scale[r] : 0.f;
         }
     }
     __device__ __forceinline__ void store(S (*x)[D + kPad], bool scaled)
@@ -175,6 +187,7 @@ struct StageR {
         for (int j = 0; j < PT; ++j) {
             const int it = threadIdx.x + j * kThreads;
             const int row = it % kC, c = it / kC;
+            if (t0_ + row >= n_) v[j] = make_uint4(0, 0, 0, 0);
             if (scaled) {
                 S* e = (S*)&v[j];
 #pragma unroll
@@ -201,16 +214,18 @@ template <int RP>
 struct URegs {
     static constexpr int NU = (RP / 16 + 3) / 4;
     f32x4 u[NU];
+    // Rows past N and tables past RP / 16 load clamped in-range values
+    // (features_from zeroes those rows' features and skips those tables), so
+    // the loads carry no per-lane branches.
     __device__ __forceinline__ void load(const float* U, int t0, int N)
     {
         const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
         const int g = lane >> 4, col = lane & 15;
-        const int tok = t0 + 16 * wv + col;
+        const int tok = min(t0 + 16 * wv + col, N - 1);
 #pragma unroll
         for (int m = 0; m < NU; ++m) {
-            const int tb = g + 4 * m;
-            u[m] = f32x4{0, 0, 0, 0};
-            if (tb < RP / 16 && tok < N) u[m] = *(const f32x4*)(U + (size_t)tok * (RP / 4) + 4 * tb);
+            const int tb = min(g + 4 * m, RP / 16 - 1);
+            u[m] = *(const f32x4*)(U + (size_t)tok * (RP / 4) + 4 * tb);
         }
     }
 };

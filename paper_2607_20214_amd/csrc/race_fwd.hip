@@ -89,17 +89,17 @@ __global__ __launch_bounds__(kThreads) void race_state_kernel(StateArgs a)
     auto load_chunk = [&](int c0) {
         ur.load(U, c0, a.N);
         vr.load(Vl, c0, a.N, vs, 1.f);
-        const int r = c0 + threadIdx.x;
-        awv = (threadIdx.x < kC && r < a.N) ? (aw ? aw[r] : 1.f) : 0.f;
+        const int r = min(c0 + (int)threadIdx.x, a.N - 1);
+        awv = aw ? aw[r] : 1.f;   // masked to the chunk's rows where stored
     };
     load_chunk(t_beg);
     for (int t0 = t_beg; t0 < t_end; t0 += kC) {
         __syncthreads();
         vr.store(sm.vt, vs != nullptr);
-        if (threadIdx.x < kC) sm.aw[threadIdx.x] = awv;
+        if (threadIdx.x < kC) sm.aw[threadIdx.x] = t0 + (int)threadIdx.x < a.N ? awv : 0.f;
         features_from<T, RP>(ur, t0, a.N, a.L, a.two_beta, nullptr, sm.pht, nullptr);
         __syncthreads();
-        if (t0 + kC < t_end) load_chunk(t0 + kC);
+        load_chunk(t0 + kC < t_end ? t0 + kC : t0);   // the last chunk reloads its own (unconditional loads)
         // S[f][cols of wave] += Phi'[f][rows] V[rows][cols]
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
@@ -213,10 +213,12 @@ __global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
         features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, sm.phq, nullptr, nullptr);
         if (a.causal) features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, sm.phk, sm.phkt, nullptr);
         __syncthreads();
-        if (t0 + kC < t_end) {
-            uq.load(Uq, t0 + kC, a.N);
-            if (a.causal) uk.load(Uk, t0 + kC, a.N);
-            vr.load(V, t0 + kC, a.N, nullptr, 1.f);
+        {
+            // next chunk's rows (the last chunk reloads its own: unconditional loads)
+            const int tn = t0 + kC < t_end ? t0 + kC : t0;
+            uq.load(Uq, tn, a.N);
+            if (a.causal) uk.load(Uk, tn, a.N);
+            vr.load(V, tn, a.N, nullptr, 1.f);
         }
         // Den, inter part: (1/L) Phi_Q . A   (4 threads per query)
         {
