@@ -43,7 +43,15 @@ def kernel_model(w, Lv: int, rules_G: int = 0, rules_lam: bool = False, rules_pa
     gs = w.sort_bits
     n0 = w.base_len
     n_leaf = N >> Lv
-    seg_states = 0                 # RACE segment states are reported with race_state/scan
+    # RACE segment states (features padded to 32, 64, 128 or 256, times
+    # [d | 1]), one set per 64-token-chunk segment: written by race_state,
+    # read and written by race_scan, read once per workgroup by the passes
+    rp = next(x for x in (32, 64, 128, 256) if x >= r)
+    chunks = (N + 63) // 64
+    nseg = max(1, min(chunks, (512 + bh - 1) // bh))
+    seg_len = ((chunks + nseg - 1) // nseg) * 64
+    nseg = (N + seg_len - 1) // seg_len
+    seg_states = bh * nseg * (rp * D + rp) * 4
     half = N // 2
     m = {}
     # one launch hashes and projects both Q and K
@@ -51,16 +59,19 @@ def kernel_model(w, Lv: int, rules_G: int = 0, rules_lam: bool = False, rules_pa
     m["sort"] = (bh * (Lv if w.causal else 2) * N * 5, 0)
     # RACE: features, chunk states (r x d per 64-token chunk), readout
     C = 64
-    m["race_state"] = (bh * N * (P * 4 + D * s), bh * N * 2 * r * D)
-    m["race_out"] = (bh * N * (2 * P * 4 + D * s + D * s + 4),
+    m["race_state"] = (bh * N * (P * 4 + D * s) + seg_states, bh * N * 2 * r * D)
+    m["race_scan"] = (2 * seg_states, 0)
+    # O_lr is float32 (saved for the backward)
+    m["race_out"] = (bh * N * (2 * P * 4 + D * s + D * 4 + 4) + seg_states,
                      bh * N * (2 * r * D * (2 if w.causal else 1) + (C * (r + D) if w.causal else 0)))
     # LB1 / LB2 write du (wk values per row in the storage dtype); the sparse
     # backward forms du W' where it adds the low-rank part
     wk = max(32, P)
-    m["race_dq"] = (bh * N * (2 * P * 4 + 2 * D * s + 8 + wk * s),
+    m["race_dq"] = (bh * N * (2 * P * 4 + 2 * D * s + 8 + wk * s) + seg_states,
                     bh * N * (2 * r * D * 2 + C * (D + r)))
     m["race_dk"] = m["race_dq"]
-    m["race_dv"] = (bh * N * (2 * P * 4 + D * s + 4 + D * s), bh * N * (2 * r * D * 2 + C * (r + D)))
+    # dV of the low-rank branch is float32
+    m["race_dv"] = (bh * N * (2 * P * 4 + D * s + 4 + D * 4) + seg_states, bh * N * (2 * r * D * 2 + C * (r + D)))
     # sparse branch: interactions per query, 4D flops each forward (QK^T, PV)
     lvl_inter = half * min(k, half) if w.causal else 0
     lvl_pos = Lv * bh * half      # (level, position) slots of the partials
@@ -89,7 +100,7 @@ def kernel_model(w, Lv: int, rules_G: int = 0, rules_lam: bool = False, rules_pa
     m["sparse_dq_blocks"] = (bh * N * (4 * D * s + D * s + 12 + wk * s), bh * N * min(k, N) * 6 * D + lr_flops)
     m["sparse_dkv_blocks"] = (bh * N * (4 * D * s + 2 * D * s + 12 + D * 4 + wk * s),
                               bh * N * min(k, N) * 8 * D + lr_flops)
-    del seg_states, n0
+    del n0
     if rules_G or rules_lam:
         # token-wise rules: q read once; gates (8 B) and lambda (4 B) per row;
         # the backward also reads dgates / dlambda, adds into dQ (read +
