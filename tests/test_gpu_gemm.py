@@ -148,3 +148,38 @@ def test_block_projections_full_size_sampled():
     ref2 = oracle.gemm(X[:, r2], dQm[:, c2], True, False)
     got2 = dwqkv.cpu().numpy()[np.ix_(r2, c2)].astype(np.float64)
     _check(got2, ref2, torch.float32, "dW rows/cols")
+
+
+def test_block_projections_full_size_other_products():
+    """The block's other four products at full size (32768 tokens, d_model
+    1024, head-major attention tensors), as the benchmark launches them:
+    Y = O W_O, dO = dY W_O^T (head-major bf16 out), dW_O = O^T dY (split
+    over K) and dX = dQKV W_qkv^T, checked on sampled rows / columns."""
+    w = W.BLOCK_32K
+    S, dm, H = w.N, w.d_model, w.H
+    dh = dm // H
+    O = W.random_matrix(80, 1, (1, H, S, dh))
+    Wo = W.random_matrix(80, 2, (dm, dm), 0.02)
+    dY = W.random_matrix(80, 3, (S, dm))
+    dQKV = W.random_matrix(80, 4, (1, 3 * H, S, dh))
+    Wqkv = W.random_matrix(80, 5, (dm, 3 * dm), 0.02)
+    y = E.gemm(_t(O), _t(Wo), out_dtype=torch.float32)
+    do = torch.empty(1, H, S, dh, dtype=torch.bfloat16, device=DEV)
+    E.gemm(_t(dY), _t(Wo), trans_b=True, out=do)
+    dwo = E.gemm(_t(O), _t(dY), trans_a=True, out_dtype=torch.float32)
+    dx = E.gemm(_t(dQKV), _t(Wqkv), trans_b=True, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    Om = O[0].transpose(1, 0, 2).reshape(S, dm)
+    dQm = dQKV[0].transpose(1, 0, 2).reshape(S, 3 * dm)
+    rng = np.random.default_rng(81)
+    rows = np.sort(rng.choice(S, 48, replace=False))
+    ridx = torch.from_numpy(rows).to(DEV)
+    _check(y[ridx], oracle.gemm(Om[rows], Wo), torch.float32, "Y rows")
+    got = do[0].permute(1, 0, 2).reshape(S, dm)[ridx]
+    _check(got, oracle.gemm(dY[rows], Wo, False, True), torch.bfloat16, "dO rows")
+    _check(dx[ridx], oracle.gemm(dQm[rows], Wqkv, False, True), torch.float32, "dX rows")
+    r2 = np.sort(rng.choice(dm, 16, replace=False))
+    c2 = np.sort(rng.choice(dm, 16, replace=False))
+    ref2 = oracle.gemm(Om[:, r2], dY[:, c2], True, False)
+    got2 = dwo.cpu().numpy()[np.ix_(r2, c2)].astype(np.float64)
+    _check(got2, ref2, torch.float32, "dW_O rows/cols")
