@@ -29,7 +29,9 @@ PEAK_F32_TFLOPS = 157.3        # fp32 matrix
 
 
 def kernel_model(w, Lv: int, rules_G: int = 0, rules_lam: bool = False, rules_part_bytes: int = 0) -> dict:
-    """Algorithmic bytes and flops per launch of each kernel (name -> (bytes, flops)).
+    """Algorithmic bytes and flops of each kernel in one step, summed over its
+    launches in the step (name -> (bytes, flops)); per-launch figures are
+    these divided by the launches per step.
 
     Counts what each kernel must move or compute: every input row it needs is
     read once, every output written once at its storage precision; level
@@ -59,8 +61,10 @@ def kernel_model(w, Lv: int, rules_G: int = 0, rules_lam: bool = False, rules_pa
     m["sort"] = (bh * (Lv if w.causal else 2) * N * 5, 0)
     # RACE: features, chunk states (r x d per 64-token chunk), readout
     C = 64
-    m["race_state"] = (bh * N * (P * 4 + D * s) + seg_states, bh * N * 2 * r * D)
-    m["race_scan"] = (2 * seg_states, 0)
+    # two launches each per step: the forward's key states and prefix scan,
+    # the backward's query suffix states and scan
+    m["race_state"] = (2 * (bh * N * (P * 4 + D * s) + seg_states), 2 * bh * N * 2 * r * D)
+    m["race_scan"] = (2 * 2 * seg_states, 0)
     # O_lr is float32 (saved for the backward)
     m["race_out"] = (bh * N * (2 * P * 4 + D * s + D * 4 + 4) + seg_states,
                      bh * N * (2 * r * D * (2 if w.causal else 1) + (C * (r + D) if w.causal else 0)))
