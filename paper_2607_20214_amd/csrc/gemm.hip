@@ -1,11 +1,15 @@
 // gemm.hip -- bfloat16 matrix-core GEMM for the dense projections around the
 // attention operator (Alg. 1 / Alg. 6: Q, K, V = X W_{Q,K,V}; O_head W_O).
 //
-// Workgroup tile 128 x 128 x 64, four waves in a 2 x 2 grid, each wave a
-// 64 x 64 block of 4 x 4 accumulators of v_mfma_f32_16x16x32_bf16.  The
-// kernel computes C^T tiles (the B operand feeds the MFMA's first input) so
-// that every lane ends with four consecutive columns of one C row, which
-// makes the stores 8- or 16-byte vectors.
+// Two kernels.  Products whose M and N are multiples of 256 and K of 64 run
+// gemm_big_kernel (256 x 256 tiles, one workgroup per compute unit, 128 x 128
+// per wave with the accumulators in the accumulation registers; see the
+// large-tile section).  Every other shape runs gemm_kernel: workgroup tile
+// 128 x 128 x 64, four waves in a 2 x 2 grid, each wave a 64 x 64 block of
+// 4 x 4 accumulators of v_mfma_f32_16x16x32_bf16.  Both compute C^T tiles
+// (the B operand feeds the MFMA's first input) so that every lane ends with
+// four consecutive columns of one C row, which makes the stores 8- or
+// 16-byte vectors.
 //
 // Operands are staged through LDS in the orientation in which they are
 // stored: a tile whose contraction dimension is contiguous is read with
