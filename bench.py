@@ -74,8 +74,8 @@ def kernel_model(w, Lv: int, rules_G: int = 0, rules_lam: bool = False, rules_pa
     m["race_dq"] = (bh * N * (2 * P * 4 + 2 * D * s + 8 + wk * s) + seg_states,
                     bh * N * (2 * r * D * 2 + C * (D + r)))
     m["race_dk"] = m["race_dq"]
-    # dV of the low-rank branch is float32
-    m["race_dv"] = (bh * N * (2 * P * 4 + D * s + 4 + D * 4) + seg_states, bh * N * (2 * r * D * 2 + C * (r + D)))
+    # dV of the low-rank branch is written in the storage dtype
+    m["race_dv"] = (bh * N * (2 * P * 4 + D * s + 4 + D * s) + seg_states, bh * N * (2 * r * D * 2 + C * (r + D)))
     # sparse branch: interactions per query, 4D flops each forward (QK^T, PV)
     lvl_inter = half * min(k, half) if w.causal else 0
     lvl_pos = Lv * bh * half      # (level, position) slots of the partials
@@ -89,20 +89,20 @@ def kernel_model(w, Lv: int, rules_G: int = 0, rules_lam: bool = False, rules_pa
     # whole-block backward: Q, dO, K, V rows once, 3 row scalars + 2 indices
     # per position, dQ / dK / dV level partials (float32) written once
     m["sparse_bwd_levels"] = (Lv * bh * half * (4 * D * s + 20 + 3 * D * 4), Lv * bh * lvl_inter * 14 * D)
-    m["sparse_bwd_blocks"] = (bh * N * (4 * D * s + 20 + D * 4 + 2 * wk * s + 3 * D * s),
+    m["sparse_bwd_blocks"] = (bh * N * (4 * D * s + 20 + D * s + 2 * wk * s + 3 * D * s),
                               bh * N * (min(k, N) * 14 * D + 2 * 2 * 2 * wk * D))
     leaf_inter = bh * (N // n_leaf) * (n_leaf * (n_leaf + 1) // 2)
     lr_flops = bh * N * 2 * 2 * wk * D            # du W' with W in two bf16 parts
     m["sparse_dq_leaf"] = (bh * N * (4 * D * s + 12 + wk * s + D * s) + lvl_pos * D * 4,
                            leaf_inter * 6 * D + lr_flops)
-    m["sparse_dkv_leaf"] = (bh * N * (4 * D * s + 12 + D * 4 + wk * s + 2 * D * s) + lvl_pos * 2 * D * 4,
+    m["sparse_dkv_leaf"] = (bh * N * (4 * D * s + 12 + D * s + wk * s + 2 * D * s) + lvl_pos * 2 * D * 4,
                             leaf_inter * 8 * D + lr_flops)
     # both leaf passes in one launch: each input row once, both low-rank parts,
     # every level partial, dQ / dK / dV written once
-    m["sparse_leaf_bwd"] = (bh * N * (4 * D * s + 12 + 2 * wk * s + D * 4 + 3 * D * s) + lvl_pos * 3 * D * 4,
+    m["sparse_leaf_bwd"] = (bh * N * (4 * D * s + 12 + 2 * wk * s + D * s + 3 * D * s) + lvl_pos * 3 * D * 4,
                             leaf_inter * 14 * D + 2 * lr_flops)
     m["sparse_dq_blocks"] = (bh * N * (4 * D * s + D * s + 12 + wk * s), bh * N * min(k, N) * 6 * D + lr_flops)
-    m["sparse_dkv_blocks"] = (bh * N * (4 * D * s + 2 * D * s + 12 + D * 4 + wk * s),
+    m["sparse_dkv_blocks"] = (bh * N * (4 * D * s + 2 * D * s + 12 + D * s + wk * s),
                               bh * N * min(k, N) * 8 * D + lr_flops)
     del n0
     if rules_G or rules_lam:

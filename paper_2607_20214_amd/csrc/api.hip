@@ -187,7 +187,7 @@ BwdWorkspace bwd_workspace(const Shape& s)
     W.wt_lo = off; off = align256(off + race_wt_bytes(s));
     W.du_q = off; off = align256(off + bhn * race_wk(s) * (s.bf16 ? 2 : 4));
     W.du_k = off; off = align256(off + bhn * race_wk(s) * (s.bf16 ? 2 : 4));
-    W.dv_lr = off; off = align256(off + bhn * s.D * 4);
+    W.dv_lr = off; off = align256(off + bhn * s.D * (s.bf16 ? 2 : 4));   // storage dtype
     W.part_dq = off; off = align256(off + npart * s.D * 4);
     W.part_dk = off; off = align256(off + npart * s.D * 4);
     W.part_dv = off; off = align256(off + npart * s.D * 4);
@@ -437,7 +437,7 @@ int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     void* du_k = at<char>(workspace, W.du_k);
     void* wt_hi = at<char>(workspace, W.wt_hi);
     void* wt_lo = at<char>(workspace, W.wt_lo);
-    float* dv_lr = at<float>(workspace, W.dv_lr);
+    void* dv_lr = at<uint8_t>(workspace, W.dv_lr);
     hipError_t e;
     if ((e = launch_bwd_rows(s, dO, o_s, o_lr, m, lse, d_lr, gates, lambda_rows, rs, dgates, dlambda, stream)) !=
         hipSuccess)

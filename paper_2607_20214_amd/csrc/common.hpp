@@ -139,6 +139,19 @@ __device__ __forceinline__ void store4(typename T::store_t* p, f32x4 v)
     }
 }
 
+// Four consecutive elements of the storage dtype as float32, one load.
+template <class T>
+__device__ __forceinline__ f32x4 load4(const typename T::store_t* p)
+{
+    if constexpr (T::bytes == 2) {
+        const uint2 v = *(const uint2*)p;
+        return f32x4{bf16_to_f32(v.x & 0xffffu), bf16_to_f32(v.x >> 16), bf16_to_f32(v.y & 0xffffu),
+                     bf16_to_f32(v.y >> 16)};
+    } else {
+        return *(const f32x4*)p;
+    }
+}
+
 // 16-byte global load / store of raw bytes.
 __device__ __forceinline__ uint4 ldg16(const void* p) { return *(const uint4*)p; }
 __device__ __forceinline__ void stg16(void* p, uint4 v) { *(uint4*)p = v; }

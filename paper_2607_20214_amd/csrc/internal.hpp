@@ -74,11 +74,11 @@ size_t race_wt_bytes(const Shape& s);       // one of the W' hi / lo buffers
 int race_wk(const Shape& s);                // columns of W' and of a du row (4 L padded to 32)
 // states_f: the forward's segment prefix states (elsaa_fwd keeps them in saved);
 // du_q, du_k: gradients of the RACE projections of the Q / K rows, storage
-// dtype [BH][N][race_wk]; dv_lr: float32 [BH][N][D]; wt_hi / wt_lo receive W'
+// dtype [BH][N][race_wk]; dv_lr: storage dtype [BH][N][D]; wt_hi / wt_lo receive W'
 hipError_t launch_race_bwd(const Shape& s, const float* Uq, const float* Uk, const void* V,
                            const void* dO, const float* W_race, const float* rs,
                            const float* states_f, float* states_b, void* wt_hi, void* wt_lo,
-                           void* du_q, void* du_k, float* dv_lr, hipStream_t st);
+                           void* du_q, void* du_k, void* dv_lr, hipStream_t st);
 
 // which kernels of a sparse-branch pass to launch: the causal levels (they
 // need only the selection), the rest (leaf or sorted blocks, which also need
@@ -105,11 +105,12 @@ hipError_t launch_bwd_rows(const Shape& s, const void* dO, const float* Os, cons
                            const float* m, const float* lse, const float* dlr, const float* gates,
                            const float* lambda_rows, float* rs, float* dgates, float* dlambda,
                            hipStream_t st);
-// sparse backward; adds the float32 low-rank parts and writes dQ, dK, dV
+// sparse backward; adds the low-rank parts (du W' for dQ and dK, the dV rows)
+// and writes dQ, dK, dV
 hipError_t launch_sparse_bwd(const Shape& s, const void* Q, const void* K, const void* V,
                              const void* dO, const int32_t* perm_q, const int32_t* perm_k,
                              const float* rs, const void* du_q, const void* du_k, const void* wt_hi,
-                             const void* wt_lo, const float* dv_lr, float* part_dq, float* part_dk, float* part_dv,
+                             const void* wt_lo, const void* dv_lr, float* part_dq, float* part_dk, float* part_dv,
                              void* dQ, void* dK, void* dV, hipStream_t st, int parts = kSparseAll);
 
 // token-wise rules: gate network and query-dependent lambda (token_rules.hip)

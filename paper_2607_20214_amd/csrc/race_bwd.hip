@@ -18,7 +18,8 @@
 // row cross HBM instead of d float32 ones; this pass provides W' = W_hi' +
 // W_lo' ([H][D][wk], bf16 parts of float32 accuracy).  The running states
 // enter the MFMAs split the same way: their products cancel against the dDen
-// terms.  LB3 writes dV as float32 [BH][N][D].
+// terms.  LB3 writes dV in the storage dtype [BH][N][D]; the sparse backward
+// adds it to its float32 dV before the final rounding.
 #include "internal.hpp"
 #include "race_common.hpp"
 
@@ -35,7 +36,7 @@ struct LbArgs {
     const void* dO;
     const float* rs;        // row scalars (sc_lr at 3*BHN, dDen at 4*BHN)
     const float* states;    // LB1: forward prefix states; LB2/LB3: backward suffix states
-    void* out;              // LB1 / LB2: du rows, storage dtype [BH][N][wk]; LB3: float32 dV [BH][N][D]
+    void* out;              // LB1 / LB2: du rows [BH][N][wk]; LB3: dV rows [BH][N][D] (storage dtype)
     int H, N, L, seg_len, nseg, causal;
     size_t BHN;
     float two_beta, beta, inv_L;
@@ -422,7 +423,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dv_kernel(LbArgs a)
     const float* Uk = a.Uk + bh * a.N * (RP / 4);
     const St* dO = (const St*)a.dO + bh * a.N * D;
     const float* sclr = a.rs + 3 * a.BHN + bh * a.N;
-    float* out = (float*)a.out + bh * a.N * D;
+    St* out = (St*)a.out + bh * a.N * D;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int g = lane >> 4, col = lane & 15;
 
@@ -523,7 +524,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dv_kernel(LbArgs a)
             const int tok = t0 + 16 * kt + col;
             if (tok < a.N)
 #pragma unroll
-                for (int j = 0; j < DW; ++j) *(f32x4*)(out + (size_t)tok * D + 16 * (w * DW + j) + 4 * g) = acc[j];
+                for (int j = 0; j < DW; ++j) store4<T>(out + (size_t)tok * D + 16 * (w * DW + j) + 4 * g, acc[j]);
         }
         if (a.causal) {
             // dS += Phi_Q' (dNum / L) (chunk)
@@ -607,7 +608,7 @@ int race_wk(const Shape& s)
 hipError_t launch_race_bwd(const Shape& s, const float* Uq, const float* Uk, const void* V,
                            const void* dO, const float* W_race, const float* rs,
                            const float* states_f, float* states_b, void* wt_hi, void* wt_lo,
-                           void* du_q, void* du_k, float* dv_lr, hipStream_t st)
+                           void* du_q, void* du_k, void* dv_lr, hipStream_t st)
 {
     {
         const int rp = race_padded_features(s.r);

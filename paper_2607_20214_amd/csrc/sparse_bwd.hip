@@ -44,7 +44,7 @@ struct BArgs {
     const void* du_k;
     const void* wt_hi;        // W' = W_hi' + W_lo' per head, storage dtype [H][D][wk]
     const void* wt_lo;
-    const float* dv_lr;       // float32 [BHN][D] low-rank dV
+    const void* dv_lr;        // storage dtype [BHN][D] low-rank dV
     float* part_dq;           // [BH][Lv][N/2][D] per-level partials, float32
     float* part_dk;
     float* part_dv;
@@ -488,7 +488,7 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
     if (ktok < 0) return;
     const size_t row = bh * N + ktok;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) tv[dt] = avT[dt] + *(const f32x4*)(a.dv_lr + row * D + 16 * dt + 4 * g);
+    for (int dt = 0; dt < DT; ++dt) tv[dt] = avT[dt] + load4<T>((const S*)a.dv_lr + row * D + 16 * dt + 4 * g);
     unsigned lmask = MODE == kLeaf ? leaf_levels((tile / a.lt.per_leaf) * a.n_leaf, N, a.Lv, false) : 0u;
     while (lmask) {
         const float* sk_[2];
@@ -738,7 +738,7 @@ __global__ __launch_bounds__(BQ * 4, BQ == 64 ? 3 : 1) void sparse_bwd_block_ker
             for (int dt = 0; dt < DT; ++dt) {
                 const int d0 = 16 * dt + 4 * g;
                 store4<T>((S*)a.dK + row * D + d0, akT[dt] * a.tau + lrk[dt]);
-                store4<T>((S*)a.dV + row * D + d0, avT[dt] + *(const f32x4*)(a.dv_lr + row * D + d0));
+                store4<T>((S*)a.dV + row * D + d0, avT[dt] + load4<T>((const S*)a.dv_lr + row * D + d0));
             }
         }
     };
@@ -991,7 +991,7 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
 hipError_t launch_sparse_bwd(const Shape& s, const void* Q, const void* K, const void* V,
                              const void* dO, const int32_t* perm_q, const int32_t* perm_k,
                              const float* rs, const void* du_q, const void* du_k, const void* wt_hi,
-                             const void* wt_lo, const float* dv_lr, float* part_dq, float* part_dk, float* part_dv,
+                             const void* wt_lo, const void* dv_lr, float* part_dq, float* part_dk, float* part_dv,
                              void* dQ, void* dK, void* dV, hipStream_t st, int parts)
 {
     BArgs a;
