@@ -100,8 +100,8 @@ __global__ __launch_bounds__(kProjThreads) void proj_kernel(ProjIO io, const flo
         }
     }
     const float* ws_h = Wsort + (size_t)h * bits * D;
-    int tix = 0;
-    for (int row0 = rbeg; row0 < rend; row0 += kProjRows, ++tix) {
+    static_assert(2 * kProjWaves >= 8, "two hash bits per wave cover sort_bits <= 8");
+    for (int row0 = rbeg; row0 < rend; row0 += kProjRows) {
         __syncthreads();                          // previous tile consumed
 #pragma unroll
         for (int j = 0; j < PT; ++j) {
@@ -113,23 +113,27 @@ __global__ __launch_bounds__(kProjThreads) void proj_kernel(ProjIO io, const flo
         if (row0 + kProjRows < rend) load(row0 + kProjRows);
         const int rows = min(kProjRows, rend - row0);
 
-        // hash: lane = row; the wave runs the float32 fma chains of the bits
-        // assigned to it on this tile (the assignment rotates over tiles so
-        // the waves share the bits evenly); W_sort row is wave-uniform
-        {
-            uint32_t c = 0;
-            for (int bit = (w + kProjWaves - (tix % kProjWaves)) % kProjWaves; bit < bits; bit += kProjWaves) {
-                const float* wrow = ws_h + (size_t)bit * D;
-                float p = 0.0f;
+        // hash: lane = row; wave w runs the float32 fma chains of bits w and
+        // w + 4 (sort_bits <= 8) side by side over the same row reads, so a
+        // second bit adds little to the chain latency; W_sort rows are
+        // wave-uniform.  Each chain keeps the order e = 0 .. d-1.
+        if (w < bits) {
+            const int b1 = w + kProjWaves < bits ? w + kProjWaves : w;
+            const float* w0 = ws_h + (size_t)w * D;
+            const float* w1 = ws_h + (size_t)b1 * D;
+            float p0 = 0.0f, p1 = 0.0f;
 #pragma unroll 4
-                for (int e0 = 0; e0 < D; e0 += PER) {
-                    const uint4 v = *(const uint4*)&sm.x[lane][e0];
-                    const S* xs = (const S*)&v;
+            for (int e0 = 0; e0 < D; e0 += PER) {
+                const uint4 v = *(const uint4*)&sm.x[lane][e0];
+                const S* xs = (const S*)&v;
 #pragma unroll
-                    for (int j = 0; j < PER; ++j) p = __builtin_fmaf(wrow[e0 + j], T::load(xs[j]), p);
+                for (int j = 0; j < PER; ++j) {
+                    const float xv = T::load(xs[j]);
+                    p0 = __builtin_fmaf(w0[e0 + j], xv, p0);
+                    p1 = __builtin_fmaf(w1[e0 + j], xv, p1);
                 }
-                if (p > 0.0f) c |= 1u << bit;
             }
+            const uint32_t c = (p0 > 0.0f ? 1u << w : 0u) | (p1 > 0.0f ? 1u << b1 : 0u);
             if (c) atomicOr(&sm.code[lane], c);
         }
         // u[token][p] for the wave's 16 tokens: A = W rows, B = X rows
