@@ -57,6 +57,23 @@ def run_gpu_fwd(cfg: E.Config, inp: dict, gates=None, lam_rows=None):
             for k_, t in out.items()}, (q, k, v, ws, wr, g, saved, lse, dlr, lr)
 
 
+def elem_stats(got, ref) -> dict:
+    """Error figures of one tensor against the oracle:
+      rel   max|d| / max|ref|            (the bar the tests assert)
+      l2    ||d|| / ||ref||
+      elem  max over elements of |d| / (|ref| + rms(ref)): each element
+            against its own size, the tensor's rms as the floor."""
+    g = np.asarray(got, dtype=np.float64)
+    r = np.asarray(ref, dtype=np.float64)
+    d = np.abs(g - r)
+    mx = float(np.max(np.abs(r))) if r.size else 0.0
+    nr = float(np.linalg.norm(r))
+    rms = nr / np.sqrt(max(r.size, 1))
+    return {"rel": float(d.max()) / (mx if mx > 0 else 1.0) if d.size else 0.0,
+            "l2": float(np.linalg.norm(d)) / (nr if nr > 0 else 1.0),
+            "elem": float(np.max(d / (np.abs(r) + (rms if rms > 0 else 1.0)))) if d.size else 0.0}
+
+
 def rel_err(a, b) -> float:
     den = float(np.max(np.abs(b)))
     return float(np.max(np.abs(a.astype(np.float64) - b))) / (den if den > 0 else 1.0)

@@ -3,7 +3,7 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_util import TOL, cfg_of, head_cfg_of, rel_err, run_gpu_fwd_bwd, say
+from gpu_util import TOL, cfg_of, elem_stats, head_cfg_of, run_gpu_fwd_bwd, say
 from paper_2607_20214_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
@@ -49,9 +49,10 @@ def _check(w, gates=None, lam=1.0, heads=None, q_mask=None, k_mask=None, want_dg
                 if name not in got:
                     continue
                 rows = slice(None) if msk is None else (msk > 0)
-                e = rel_err(got[name][b, h][rows], ref[name][rows])
-                errs[name] = max(errs.get(name, 0.0), e)
-                assert e <= tol, f"{name} (b={b}, h={h}): {e:.3e} > {tol}"
+                st = elem_stats(got[name][b, h][rows], ref[name][rows])
+                for key, v in st.items():
+                    errs[f"{name}.{key}"] = max(errs.get(f"{name}.{key}", 0.0), v)
+                assert st["rel"] <= tol, f"{name} (b={b}, h={h}): {st['rel']:.3e} > {tol}"
     say("   errors:", {k: f"{v:.2e}" for k, v in errs.items()})
 
 
@@ -68,11 +69,14 @@ def test_backward_gates_lambda_and_gate_gradients():
 
 
 def test_backward_clustered_4k_workload():
-    _check(W.CLUSTERED_4K, heads={(0, 0), (1, 5)})
+    """All 16 heads (B = 2, H = 8) of the clustered 4K workload."""
+    _check(W.CLUSTERED_4K)
 
 
-def test_backward_causal_16k_workload_sampled_heads():
-    _check(W.CAUSAL_16K, heads={(0, 0), (0, 11)})
+@pytest.mark.timeout(900)
+def test_backward_causal_16k_workload_all_heads():
+    """All 16 heads of the 16K causal workload (the measured one), every row."""
+    _check(W.CAUSAL_16K)
 
 
 def test_backward_causal_64k_mixed_workload_sampled_rows():

@@ -3,7 +3,7 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_util import TOL, cfg_of, compare_heads, head_cfg_of, rel_err, run_gpu_fwd, say
+from gpu_util import TOL, cfg_of, elem_stats, head_cfg_of, run_gpu_fwd, say
 from paper_2607_20214_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
@@ -52,9 +52,10 @@ def _check_case(w, gates=None, lam=1.0, heads=None, row_mask=None):
             rows = slice(None) if row_mask is None else (row_mask > 0)
             for name in ("O", "O_s", "O_lr", "d_lr", "m"):
                 r_ = rows if name not in ("O_lr", "d_lr") else slice(None)
-                e = rel_err(got[name][b, h][r_], ref[name][r_])
-                errs[name] = max(errs.get(name, 0.0), e)
-                assert e <= tol, f"{name} (b={b}, h={h}): {e:.3e} > {tol}"
+                st = elem_stats(got[name][b, h][r_], ref[name][r_])
+                for key, v in st.items():
+                    errs[f"{name}.{key}"] = max(errs.get(f"{name}.{key}", 0.0), v)
+                assert st["rel"] <= tol, f"{name} (b={b}, h={h}): {st['rel']:.3e} > {tol}"
             e = float(np.max(np.abs(got["lse"][b, h][rows] - ref["lse"][rows])))
             errs["lse(abs)"] = max(errs.get("lse(abs)", 0.0), e)
             assert e <= tol, f"lse (b={b}, h={h}): {e:.3e}"
@@ -78,11 +79,14 @@ def test_forward_tiny_fp32_workload():
 
 
 def test_forward_clustered_4k_workload():
-    _check_case(W.CLUSTERED_4K, heads={(0, 0), (1, 7), (0, 3)})
+    """All 16 heads (B = 2, H = 8) of the clustered 4K workload."""
+    _check_case(W.CLUSTERED_4K)
 
 
-def test_forward_causal_16k_workload_sampled_heads():
-    _check_case(W.CAUSAL_16K, heads={(0, 0), (0, 15)})
+@pytest.mark.timeout(600)
+def test_forward_causal_16k_workload_all_heads():
+    """All 16 heads of the 16K causal workload (the measured one), every row."""
+    _check_case(W.CAUSAL_16K)
 
 
 def test_forward_causal_64k_mixed_workload_sampled_rows():
