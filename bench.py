@@ -28,104 +28,105 @@ PEAK_BF16_TFLOPS = 2500.0      # dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3        # fp32 matrix
 
 
-def kernel_model(w, Lv: int, rules_G: int = 0, rules_lam: bool = False, rules_part_bytes: int = 0) -> dict:
-    """Algorithmic bytes and flops of each kernel in one step, summed over its
-    launches in the step (name -> (bytes, flops)); per-launch figures are
-    these divided by the launches per step.
+def survey_units(w, Lv: int, rules_G: int = 0, rules_lam: bool = False, rules_part_bytes: int = 0) -> dict:
+    """Algorithmic bytes and flops per step of each unit of the hot path, in
+    the accounting of the method's complexity (the Theta(N s) sparse term and
+    the Theta(N L_s 2^gamma) RACE term turned into bytes): every input the
+    step must read is counted once, every output written once; partial
+    results that one kernel hands to the next are NOT counted.
 
-    Counts what each kernel must move or compute: every input row it needs is
-    read once, every output written once at its storage precision; level
-    partials count as outputs of the level kernels and inputs of the leaf
-    kernels, which is what the decomposition into kernels requires.
+    Returns {unit: (bytes, flops, kernels)}; a unit is one kernel or the few
+    kernels that together compute one step of the path.  Per head, with s the
+    element size, N tokens, d = d_h, Lv causal levels:
+      selection      2Nds + 2N (hash: Q, K read, keys written) and the perm
+                     writes, 8N non-causal or 4N per level
+      sparse fwd     3Nds + 4Nd + 12N (leaf / blocks) and 1.5Nds + 4N per level
+      low-rank fwd   N (3ds + 4d + 4)
+      sparse bwd     4Nds + 12Nd + 8N (leaf / blocks) and 2Nds + 4N per level
+      low-rank bwd   2 N (3ds + 4d + 4)
+      fusion         N (ds + 4d + 8), fused into the sparse leaf / blocks kernel
+                     (O_lr and d_lr read, O and m written; O_s never leaves it)
+      bwd rows       N (ds + 8d + 12)  (dO, O_s and O_lr read, row scalars)
+    Flops: 4d per sparse interaction forward, 10d backward (recompute
+    included); low-rank forward 4r(d+1) + 4dL gamma per token plus
+    2C(r+d+1) causal (C = 64), backward 2.25 times that; bwd rows 4d per row.
     """
     s = 2 if w.dtype == "bf16" else 4
     bh = w.B * w.H
     N, D, k, r, L = w.N, w.d, w.k, w.r, w.L
-    P = 4 * L                      # RACE projections per row
-    gs = w.sort_bits
-    n0 = w.base_len
-    n_leaf = N >> Lv
-    # RACE segment states (features padded to 32, 64, 128 or 256, times
-    # [d | 1]), one set per 64-token-chunk segment: written by race_state,
-    # read and written by race_scan, read once per workgroup by the passes
-    rp = next(x for x in (32, 64, 128, 256) if x >= r)
-    chunks = (N + 63) // 64
-    nseg = max(1, min(chunks, (512 + bh - 1) // bh))
-    seg_len = ((chunks + nseg - 1) // nseg) * 64
-    nseg = (N + seg_len - 1) // seg_len
-    seg_states = bh * nseg * (rp * D + rp) * 4
-    half = N // 2
-    m = {}
-    # one launch hashes and projects both Q and K
-    m["project"] = (2 * bh * N * (D * s + 1 + P * 4), 2 * bh * N * 2 * D * (gs + P))
-    m["sort"] = (bh * (Lv if w.causal else 2) * N * 5, 0)
-    # RACE: features, chunk states (r x d per 64-token chunk), readout
+    gs, g = w.sort_bits, w.race_bits
     C = 64
-    # two launches each per step: the forward's key states and prefix scan,
-    # the backward's query suffix states and scan
-    m["race_state"] = (2 * (bh * N * (P * 4 + D * s) + seg_states), 2 * bh * N * 2 * r * D)
-    m["race_scan"] = (2 * 2 * seg_states, 0)
-    # O_lr is float32 (saved for the backward)
-    m["race_out"] = (bh * N * (2 * P * 4 + D * s + D * 4 + 4) + seg_states,
-                     bh * N * (2 * r * D * (2 if w.causal else 1) + (C * (r + D) if w.causal else 0)))
-    # LB1 / LB2 write du (wk values per row in the storage dtype); the sparse
-    # backward forms du W' where it adds the low-rank part
-    wk = max(32, P)
-    m["race_dq"] = (bh * N * (2 * P * 4 + 2 * D * s + 8 + wk * s) + seg_states,
-                    bh * N * (2 * r * D * 2 + C * (D + r)))
-    m["race_dk"] = m["race_dq"]
-    # dV of the low-rank branch is written in the storage dtype
-    m["race_dv"] = (bh * N * (2 * P * 4 + D * s + 4 + D * s) + seg_states, bh * N * (2 * r * D * 2 + C * (r + D)))
-    # sparse branch: interactions per query, 4D flops each forward (QK^T, PV)
-    lvl_inter = half * min(k, half) if w.causal else 0
-    lvl_pos = Lv * bh * half      # (level, position) slots of the partials
-    m["sparse_fwd_levels"] = (lvl_pos * (3 * D * s + 8 + D * 4 + 4), Lv * bh * lvl_inter * 4 * D)
-    m["sparse_fwd_leaf"] = (bh * N * (3 * D * s + D * 4 + 4 + D * s + D * 4 + 8) + lvl_pos * (D * 4 + 4),
-                            bh * (N // n_leaf) * (n_leaf * (n_leaf + 1) // 2) * 4 * D)
-    m["sparse_fwd_blocks"] = (bh * N * (3 * D * s + 8 + D * 4 + 4 + D * s + 12), bh * N * min(k, N) * 4 * D)
-    m["bwd_rows"] = (bh * N * (D * s + 2 * D * 4 + 12 + 20), bh * N * 4 * D)
-    m["sparse_dq_levels"] = (Lv * bh * half * (4 * D * s + 8 + D * 4), Lv * bh * lvl_inter * 6 * D)
-    m["sparse_dkv_levels"] = (Lv * bh * half * (4 * D * s + 8 + 2 * D * 4), Lv * bh * lvl_inter * 8 * D)
-    # whole-block backward: Q, dO, K, V rows once, 3 row scalars + 2 indices
-    # per position, dQ / dK / dV level partials (float32) written once
-    m["sparse_bwd_levels"] = (Lv * bh * half * (4 * D * s + 20 + 3 * D * 4), Lv * bh * lvl_inter * 14 * D)
-    m["sparse_bwd_blocks"] = (bh * N * (4 * D * s + 20 + D * s + 2 * wk * s + 3 * D * s),
-                              bh * N * (min(k, N) * 14 * D + 2 * 2 * 2 * wk * D))
-    leaf_inter = bh * (N // n_leaf) * (n_leaf * (n_leaf + 1) // 2)
-    lr_flops = bh * N * 2 * 2 * wk * D            # du W' with W in two bf16 parts
-    m["sparse_dq_leaf"] = (bh * N * (4 * D * s + 12 + wk * s + D * s) + lvl_pos * D * 4,
-                           leaf_inter * 6 * D + lr_flops)
-    m["sparse_dkv_leaf"] = (bh * N * (4 * D * s + 12 + D * s + wk * s + 2 * D * s) + lvl_pos * 2 * D * 4,
-                            leaf_inter * 8 * D + lr_flops)
-    # both leaf passes in one launch: each input row once, both low-rank parts,
-    # every level partial, dQ / dK / dV written once
-    m["sparse_leaf_bwd"] = (bh * N * (4 * D * s + 12 + 2 * wk * s + D * s + 3 * D * s) + lvl_pos * 3 * D * 4,
-                            leaf_inter * 14 * D + 2 * lr_flops)
-    m["sparse_dq_blocks"] = (bh * N * (4 * D * s + D * s + 12 + wk * s), bh * N * min(k, N) * 6 * D + lr_flops)
-    m["sparse_dkv_blocks"] = (bh * N * (4 * D * s + 2 * D * s + 12 + D * s + wk * s),
-                              bh * N * min(k, N) * 8 * D + lr_flops)
-    del n0
+    u = {}
+    u["project"] = (bh * (2 * N * D * s + 2 * N), bh * N * 2 * 2 * D * gs, ["project"])
+    u["sort"] = (bh * (4 * N * Lv if w.causal else 8 * N), 0, ["sort"])
+    lr_tok_bytes = 3 * D * s + 4 * D + 4
+    lr_tok_flops = 4 * r * (D + 1) + 4 * D * L * g + (2 * C * (r + D + 1) if w.causal else 0)
+    u["lowrank_fwd"] = (bh * N * lr_tok_bytes, bh * N * lr_tok_flops,
+                        ["race_state_fwd", "race_scan_fwd", "race_out"])
+    u["lowrank_bwd"] = (2 * bh * N * lr_tok_bytes, int(2.25 * bh * N * lr_tok_flops),
+                        ["race_state_bwd", "race_scan_bwd", "race_dq", "race_dk", "race_dv", "race_wt"])
+    u["bwd_rows"] = (bh * N * (D * s + 8 * D + 12), bh * N * 4 * D, ["bwd_rows"])
+    base_fwd = bh * (3 * N * D * s + 4 * N * D + 12 * N) + bh * N * (D * s + 4 * D + 8)
+    base_bwd = bh * (4 * N * D * s + 12 * N * D + 8 * N)
+    if w.causal:
+        half = N // 2
+        n_leaf = N >> Lv
+        lvl_inter = bh * Lv * half * min(k, half)
+        leaf_inter = bh * (N // n_leaf) * (n_leaf * (n_leaf + 1) // 2)
+        u["sparse_fwd_levels"] = (bh * Lv * (3 * half * D * s + 4 * N), lvl_inter * 4 * D, ["sparse_fwd_levels"])
+        u["sparse_fwd_leaf"] = (base_fwd, leaf_inter * 4 * D, ["sparse_fwd_leaf"])
+        u["sparse_bwd_levels"] = (bh * Lv * (2 * N * D * s + 4 * N), lvl_inter * 10 * D,
+                                  ["sparse_bwd_levels", "sparse_dq_levels", "sparse_dkv_levels"])
+        u["sparse_bwd_leaf"] = (base_bwd, leaf_inter * 10 * D,
+                                ["sparse_leaf_bwd", "sparse_dq_leaf", "sparse_dkv_leaf"])
+    else:
+        inter = bh * N * min(k, N)
+        u["sparse_fwd_blocks"] = (base_fwd, inter * 4 * D, ["sparse_fwd_blocks"])
+        u["sparse_bwd_blocks"] = (base_bwd, inter * 10 * D,
+                                  ["sparse_bwd_blocks", "sparse_dq_blocks", "sparse_dkv_blocks"])
     if rules_G or rules_lam:
-        # token-wise rules: q read once; gates (8 B) and lambda (4 B) per row;
-        # the backward also reads dgates / dlambda, adds into dQ (read +
-        # write) and writes one partial-sum record per workgroup
+        # token-wise rules (outside the operator): q read once; gates (8 B) and
+        # lambda (4 B) per row; the backward also reads dgates / dlambda and
+        # adds into dQ (read + write); the reduction reads the partial records
         G = rules_G
         gx = G + (1 if rules_lam else 0)
         out_b = (8 if G else 0) + (4 if rules_lam else 0)
-        rec = G * D + (D if rules_lam else 0) + 3 * G + (2 if G else 0) + (2 if rules_lam else 0)
-        m["token_rules_fwd"] = (bh * N * (D * s + out_b), bh * N * (2 * D * gx + 4 * G))
-        m["token_rules_bwd"] = (bh * N * (D * s + out_b + (2 * D * s if G else 0)) + rules_part_bytes,
-                                bh * N * (2 * D * gx * 2 + (2 * D * G) + 8 * G))
-        m["token_rules_reduce"] = (rules_part_bytes + w.H * rec * 4, rules_part_bytes // 4)
+        u["token_rules_fwd"] = (bh * N * (D * s + out_b), bh * N * (2 * D * gx + 4 * G), ["token_rules_fwd"])
+        u["token_rules_bwd"] = (bh * N * (D * s + out_b + (2 * D * s if G else 0)),
+                                bh * N * (2 * D * gx * 2 + (2 * D * G) + 8 * G),
+                                ["token_rules_bwd", "token_rules_reduce"])
     if w.d_model:
-        # the six dense products of one block step (bf16 operands; Q/K/V, dO
-        # written bf16, Y and the gradients of X and the weights float32)
+        # the six dense products of one block step (bf16 operands; QKV and dO
+        # written bf16, Y and the gradients of X and of the weights float32)
         T, dm = w.B * w.N, w.d_model
         prods = [(T, 3 * dm, dm, 2), (T, dm, dm, 4), (T, dm, dm, 2),
                  (dm, dm, T, 4), (T, dm, 3 * dm, 4), (dm, 3 * dm, T, 4)]
-        m["gemm"] = (sum(2 * (M * K + K * N_) + o * M * N_ for M, N_, K, o in prods),
-                     sum(2 * M * N_ * K for M, N_, K, _ in prods))
-    return m
+        u["gemm"] = (sum(2 * (M * K + K * N_) + o * M * N_ for M, N_, K, o in prods),
+                     sum(2 * M * N_ * K for M, N_, K, _ in prods), ["gemm", "gemm_reduce"])
+    return u
+
+
+def kernel_model(w, Lv: int) -> dict:
+    """Bytes each sparse-branch kernel actually has to move as the path is
+    split into kernels (name -> bytes per step): the survey accounting above
+    plus the level partials (storage dtype), which the level kernels write and the
+    leaf kernels read back.  Reported beside the algorithmic figure so the
+    cost of the split is visible; not a roofline numerator."""
+    s = 2 if w.dtype == "bf16" else 4
+    bh = w.B * w.H
+    N, D = w.N, w.d
+    if not w.causal:
+        return {}
+    half = N // 2
+    ps = s                          # level partials are kept in the storage dtype
+    lvl_pos = Lv * bh * half        # (level, position) slots of the partials
+    wk = max(32, 4 * w.L)
+    return {
+        "sparse_fwd_levels": lvl_pos * (3 * D * s + 8 + D * ps + 4),
+        "sparse_fwd_leaf": bh * N * (3 * D * s + 8 * D + 4 + D * s + 8) + lvl_pos * (D * ps + 4),
+        "sparse_bwd_levels": lvl_pos * (4 * D * s + 20 + 3 * D * ps),
+        "sparse_leaf_bwd": bh * N * (4 * D * s + 12 + 2 * wk * s + D * s + 3 * D * s) + lvl_pos * 3 * D * ps,
+    }
 
 
 def source_digest(names) -> str:
@@ -138,8 +139,10 @@ def source_digest(names) -> str:
 
 KERNEL_SOURCES = {
     "project": ["select.hip", "common.hpp"], "sort": ["select.hip"],
-    "race_state": ["race_fwd.hip", "race_common.hpp", "common.hpp"],
-    "race_scan": ["race_fwd.hip"], "race_out": ["race_fwd.hip", "race_common.hpp", "common.hpp"],
+    "race_state_fwd": ["race_fwd.hip", "race_common.hpp", "common.hpp"],
+    "race_state_bwd": ["race_fwd.hip", "race_common.hpp", "common.hpp"],
+    "race_scan_fwd": ["race_fwd.hip"], "race_scan_bwd": ["race_fwd.hip"],
+    "race_out": ["race_fwd.hip", "race_common.hpp", "common.hpp"],
     "race_dq": ["race_bwd.hip", "race_common.hpp", "common.hpp"],
     "race_dk": ["race_bwd.hip", "race_common.hpp", "common.hpp"],
     "race_dv": ["race_bwd.hip", "race_common.hpp", "common.hpp"],
@@ -179,30 +182,73 @@ def read_traffic(kernel: str, workload: str):
         return None
 
 
-def cpu_baseline(w, inp, min_seconds: float = 10.0) -> dict:
-    """Oracle forward + backward over the full sequence of as many heads as
-    fit in about min_seconds (at least one), scaled to whole-job tokens/s
-    (the job is B * H such heads)."""
+def cpu_model() -> str:
+    """Model name of the host CPU (first 'model name' line of /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_heads(w, inp, hc, backward: bool, min_seconds: float):
+    """Run the oracle on whole heads until about min_seconds have passed (at
+    least one head); returns (heads done, seconds).  The oracle's backward
+    computes the forward state itself, so one backward call is a complete
+    forward + backward of the head."""
     import oracle
 
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
+    done, t0 = 0, time.perf_counter()
+    for b in range(w.B):
+        for h in range(w.H):
+            args = (inp["Q"][b, h], inp["K"][b, h], inp["V"][b, h], inp["W_sort"][h], inp["W_race"][h])
+            if backward:
+                oracle.backward(hc, *args, inp["dO"][b, h])
+            else:
+                oracle.forward(hc, *args)
+            done += 1
+            if time.perf_counter() - t0 >= min_seconds:
+                return done, time.perf_counter() - t0
+    return done, time.perf_counter() - t0
+
+
+def cpu_baseline(w, inp, min_seconds: float = 10.0) -> dict:
+    """The fp64 oracle on the host cores, on a bounded sample of whole heads,
+    scaled to whole-job tokens/s (the job is B * H heads).  The forward and
+    the forward + backward (one oracle backward call, which computes its
+    forward state itself) are timed separately; value is the latter, or the
+    forward alone for forward-only workloads.  Small workloads also get a
+    single-thread figure."""
+    import oracle
+
+    threads = oracle.threads()
     hc = oracle.head_cfg(w)
-    heads = [(b, h) for b in range(w.B) for h in range(w.H)]
-    done = 0
-    t0 = time.perf_counter()
-    for b, h in heads:
-        args = (inp["Q"][b, h], inp["K"][b, h], inp["V"][b, h], inp["W_sort"][h], inp["W_race"][h])
-        oracle.forward(hc, *args)
-        oracle.backward(hc, *args, inp["dO"][b, h])
-        done += 1
-        if time.perf_counter() - t0 >= min_seconds:
-            break
-    dt = time.perf_counter() - t0
-    total = len(heads)
-    return {"value": w.B * w.N * done / (dt * total), "unit": "tokens/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"{done} of {total} heads, all {w.N} tokens each, forward + backward in "
-                      f"{dt:.1f} s, scaled to {total} heads"}
+    total = w.B * w.H
+    nf, tf = _oracle_heads(w, inp, hc, False, min_seconds / 3)
+    fwd_tps = w.B * w.N * nf / (tf * total)
+    out = {"unit": "tokens/s", "cores": threads, "kind": "oracle", "cpu": cpu_model(),
+           "fwd_value": fwd_tps}
+    if w.backward:
+        nb, tb = _oracle_heads(w, inp, hc, True, min_seconds)
+        out["value"] = w.B * w.N * nb / (tb * total)
+        out["sample"] = (f"forward alone on {nf} of {total} heads ({tf:.1f} s); forward + backward (one "
+                         f"oracle backward call per head) on {nb} of {total} heads ({tb:.1f} s); all "
+                         f"{w.N} tokens of each head; {threads} threads; scaled to {total} heads")
+    else:
+        out["value"] = fwd_tps
+        out["sample"] = (f"forward on {nf} of {total} heads, all {w.N} tokens each ({tf:.1f} s); "
+                         f"{threads} threads; scaled to {total} heads")
+    if w.B * w.N * w.H <= 65536:
+        oracle.threads(1)
+        try:
+            n1, t1 = _oracle_heads(w, inp, hc, w.backward, min_seconds / 2)
+        finally:
+            oracle.threads(threads)
+        out["single_thread_value"] = w.B * w.N * n1 / (t1 * total)
+    return out
 
 
 def cpu_baseline_block(w, inp, blk, min_seconds: float = 10.0) -> dict:
@@ -212,7 +258,7 @@ def cpu_baseline_block(w, inp, blk, min_seconds: float = 10.0) -> dict:
     import numpy as np
     import oracle
 
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
+    threads = oracle.threads()
     T, dm = w.B * w.N, w.d_model
     rows = 2048
     X = blk["X"].reshape(T, dm)[:rows]
@@ -222,26 +268,31 @@ def cpu_baseline_block(w, inp, blk, min_seconds: float = 10.0) -> dict:
     qkv = oracle.gemm(X, Wqkv)
     O = qkv[:, :dm]
     oracle.gemm(O, blk["W_O"])
-    dO = oracle.gemm(dY, blk["W_O"], False, True)
+    oracle.gemm(dY, blk["W_O"], False, True)
     oracle.gemm(O, dY, True, False)
     oracle.gemm(qkv, Wqkv, False, True)
     oracle.gemm(X, qkv, True, False)
     t_gemm = (time.perf_counter() - t0) * T / rows
-    del dO
     hc = oracle.head_cfg(w)
-    done = 0
-    t1 = time.perf_counter()
-    for h in range(w.H):
-        args = (inp["Q"][0, h], inp["K"][0, h], inp["V"][0, h], inp["W_sort"][h], inp["W_race"][h])
-        oracle.forward(hc, *args)
-        oracle.backward(hc, *args, inp["dO"][0, h])
-        done += 1
-        if time.perf_counter() - t1 >= min_seconds:
-            break
-    t_att = (time.perf_counter() - t1) * (w.B * w.H) / done
+    done, dt = _oracle_heads(w, inp, hc, True, min_seconds)
+    t_att = dt * (w.B * w.H) / done
     return {"value": T / (t_gemm + t_att), "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"projections on {rows} of {T} tokens and the operator on {done} of "
-                      f"{w.B * w.H} heads, scaled to the full step"}
+            "cpu": cpu_model(),
+            "sample": f"projections on {rows} of {T} tokens and the operator forward + backward (one "
+                      f"oracle backward call per head) on {done} of {w.B * w.H} heads, scaled to the "
+                      f"full step"}
+
+
+def roofline_entry(nbytes, nflops, seconds, peak_tf):
+    """Roofline of work (bytes, flops) done in `seconds`: bound by whichever
+    of HBM and the matrix cores would take longer at peak."""
+    if nbytes / (PEAK_HBM_GBS * 1e9) >= nflops / (peak_tf * 1e12):
+        a = nbytes / seconds / 1e9
+        return {"bound": "hbm", "achieved": round(a, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(a / PEAK_HBM_GBS, 4)}
+    a = nflops / seconds / 1e12
+    return {"bound": "mfma", "achieved": round(a, 2), "peak": peak_tf, "unit": "TFLOP/s",
+            "frac": round(a / peak_tf, 4)}
 
 
 def main():
@@ -283,23 +334,30 @@ def main():
         return
     cfg = E.Config(B=w.B, H=w.H, N=w.N, d_h=w.d, k=w.k, r=w.r, causal=w.causal, dtype=w.dtype,
                    race_bits=w.race_bits, sort_bits=w.sort_bits, n0=w.n0 or 0)
-    inp = W.make_inputs(w, with_grad=True)
+    inp = W.make_inputs(w, with_grad=w.backward)
     dt = cfg.torch_dtype
 
     def to(x, t):
         return torch.from_numpy(np.ascontiguousarray(x)).to(dev).to(t).contiguous()
 
-    q, k, v, do = (to(inp[n], dt) for n in ("Q", "K", "V", "dO"))
+    q, k, v = (to(inp[n], dt) for n in ("Q", "K", "V"))
+    do = to(inp["dO"], dt) if w.backward else None
     ws, wr = to(inp["W_sort"], torch.float32), to(inp["W_race"], torch.float32)
-    bufs = E.Buffers(cfg, dev, backward=True)
+    bufs = E.Buffers(cfg, dev, backward=w.backward)
     Lv = E.num_levels(cfg)
 
     def step():
         o, lse, dlr, saved = E.fwd(cfg, q, k, v, ws, wr, buffers=bufs)
         E.bwd(cfg, q, k, v, wr, do, lse, dlr, saved, buffers=bufs)
 
+    if not w.backward:
+        def step():
+            E.fwd(cfg, q, k, v, ws, wr, buffers=bufs)
+
     rules_G, rules_part = 0, 0
     if args.rules:
+        if not w.backward:
+            raise SystemExit("--rules needs a forward + backward workload")
         rules_G = 64
         rp = W.make_rule_params(w, rules_G, True)
         rules = E.TokenRules(**{n: to(a, torch.float32) for n, a in rp.items()})
@@ -315,31 +373,17 @@ def main():
     blk = None
     if w.d_model:
         # one attention-block step: projections on the matrix cores around the
-        # operator, all attention tensors head-major [B, 3H or H, N, d_h]
-        assert w.B == 1, "the block step keeps Q, K, V as heads of one [1, 3H, N, d] buffer"
-        blk = W.make_block_inputs(w)
-        Tn, dm, H = w.B * w.N, w.d_model, w.H
-        bf = torch.bfloat16
-        X = to(blk["X"].reshape(Tn, dm), bf)
-        dY = to(blk["dY"].reshape(Tn, dm), bf)
-        Wqkv = to(np.concatenate([blk["W_Q"], blk["W_K"], blk["W_V"]], axis=1), bf)
-        Wo = to(blk["W_O"], bf)
-        qkv = torch.empty(1, 3 * H, w.N, w.d, dtype=bf, device=dev)
-        dqkv = torch.empty_like(qkv)
-        do_h = torch.empty(1, H, w.N, w.d, dtype=bf, device=dev)
-        q, k, v = qkv[:, :H], qkv[:, H:2 * H], qkv[:, 2 * H:]
-        bufs.dq, bufs.dk, bufs.dv = dqkv[:, :H], dqkv[:, H:2 * H], dqkv[:, 2 * H:]
-        gws = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+        # operator, every attention tensor head-major [1, 3H or H, N, d_h]
+        from paper_2607_20214_amd.block import AttentionBlock
 
-        def step():
-            E.gemm(X, Wqkv, out=qkv, workspace=gws)
-            o, lse, dlr, saved = E.fwd(cfg, q, k, v, ws, wr, buffers=bufs)
-            E.gemm(o, Wo, out_dtype=torch.float32, workspace=gws)                # Y
-            E.gemm(dY, Wo, trans_b=True, out=do_h, workspace=gws)                # dO
-            E.gemm(o, dY, trans_a=True, out_dtype=torch.float32, workspace=gws)  # dW_O
-            E.bwd(cfg, q, k, v, wr, do_h, lse, dlr, saved, buffers=bufs)
-            E.gemm(dqkv, Wqkv, trans_b=True, out_dtype=torch.float32, workspace=gws)  # dX
-            E.gemm(X, dqkv, trans_a=True, out_dtype=torch.float32, workspace=gws)     # dW_qkv
+        blk = W.make_block_inputs(w)
+        Tn, dm = w.B * w.N, w.d_model
+        bf = torch.bfloat16
+        block = AttentionBlock(cfg, to(blk["X"].reshape(Tn, dm), bf), to(blk["dY"].reshape(Tn, dm), bf),
+                               to(np.concatenate([blk["W_Q"], blk["W_K"], blk["W_V"]], axis=1), bf),
+                               to(blk["W_O"], bf), ws, wr)
+        del bufs, q, k, v, do
+        step = block.step
 
     for _ in range(args.warmup):
         step()
@@ -365,40 +409,66 @@ def main():
     E.profile_enable(False)
 
     elapsed = t1 - t0
+    ms_step = elapsed / args.steps * 1e3
     tokens = w.B * w.N * args.steps
     per_step = {name: ms / args.steps for name, (ms, n) in prof.items()}
-    dom = max(per_step, key=per_step.get)
-    ms_total, launches = prof[dom]
-    avg_s = ms_total / launches / 1e3
-    model = kernel_model(w, Lv, rules_G, bool(args.rules), rules_part)
+    units = survey_units(w, Lv, rules_G, bool(args.rules), rules_part)
     peak_tf = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
 
-    def roofline_of(name):
-        """(roofline dict, bytes, flops per launch) of one kernel from its
-        algorithmic model and its measured average launch time."""
-        tot_ms, n = prof[name]
-        avg = tot_ms / n / 1e3
-        b_, f_ = model.get(name, (0, 0))
+    # per-unit roofline: algorithmic bytes / flops of the unit per step over
+    # the summed per-step time of its kernels
+    unit_rows = {}
+    for name, (nb, nf, kernels) in units.items():
+        ran = [kn for kn in kernels if kn in prof]
+        if not ran:
+            continue
+        ms = sum(per_step[kn] for kn in ran)
+        unit_rows[name] = (ms, nb, nf, ran)
+    # the dominant unit (largest time per step); for a unit of one kernel the
+    # figures are per launch over that kernel's average launch duration
+    dom = max(unit_rows, key=lambda n: unit_rows[n][0])
+    ms, nb, nf, ran = unit_rows[dom]
+    if len(ran) == 1:
+        tot_ms, n = prof[ran[0]]
         per = n // args.steps
-        b_, f_ = b_ / per, f_ / per
-        if b_ / (PEAK_HBM_GBS * 1e9) >= f_ / (peak_tf * 1e12):
-            a_ = b_ / avg / 1e9
-            return {"bound": "hbm", "achieved": round(a_, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                    "frac": round(a_ / PEAK_HBM_GBS, 4)}, b_, f_
-        a_ = f_ / avg / 1e12
-        return {"bound": "mfma", "achieved": round(a_, 2), "peak": peak_tf, "unit": "TFLOP/s",
-                "frac": round(a_ / peak_tf, 4)}, b_, f_
+        avg_s = tot_ms / n / 1e3
+        nb, nf = nb / per, nf / per
+        roof = roofline_entry(nb, nf, avg_s, peak_tf)
+        roof["traffic"] = read_traffic(ran[0], w.name)
+        roof["kernel"] = ran[0]
+        roof["avg_launch_ms"] = round(avg_s * 1e3, 4)
+        roof["algorithmic_bytes_per_launch"] = nb
+        roof["algorithmic_flops_per_launch"] = nf
+    else:
+        roof = roofline_entry(nb, nf, ms / 1e3, peak_tf)
+        roof["traffic"] = None
+        roof["kernel"] = dom
+        roof["kernels"] = ran
+        roof["ms_per_step"] = round(ms, 4)
+        roof["algorithmic_bytes_per_step"] = nb
+        roof["algorithmic_flops_per_step"] = nf
+    # the whole step against the same accounting
+    step_b = sum(r_[1] for r_ in unit_rows.values())
+    step_f = sum(r_[2] for r_ in unit_rows.values())
+    step_roof = roofline_entry(step_b, step_f, ms_step / 1e3, peak_tf)
+    step_roof["algorithmic_bytes_per_step"] = step_b
+    step_roof["algorithmic_flops_per_step"] = step_f
+    # what the split into kernels moves (the sparse kernels' level partials)
+    km = kernel_model(w, Lv)
+    kmodel = {}
+    for kn, b_ in km.items():
+        if kn in prof:
+            tot_ms, n = prof[kn]
+            kmodel[kn] = {"bytes_per_launch": b_ / (n // args.steps),
+                          "frac": round(b_ / (n // args.steps) / (tot_ms / n / 1e3) / 1e9 / PEAK_HBM_GBS, 4),
+                          "traffic": read_traffic(kn, w.name)}
 
-    roof, nbytes, nflops = roofline_of(dom)
-    roof["traffic"] = read_traffic(dom, w.name)
-    roof["kernel"] = dom
-    roof["avg_launch_ms"] = round(avg_s * 1e3, 4)
-    roof["algorithmic_bytes_per_launch"] = nbytes
-    roof["algorithmic_flops_per_launch"] = nflops
-
-    metric = "ELSAA fwd+bwd tokens/sec at N=16k,d_h=128; % HBM/MFMA roofline"
     if blk is not None:
         metric = "ELSAA attention-block step (projections + operator) fwd+bwd tokens/sec"
+    elif not w.backward:
+        metric = "ELSAA forward tokens/sec (forward-only workload)"
+    else:
+        metric = "ELSAA fwd+bwd tokens/sec at N=16k,d_h=128; % HBM/MFMA roofline"
     result = {
         "metric": metric,
         "value": tokens / elapsed,
@@ -406,7 +476,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": elapsed / args.steps * 1e3,
+        "ms_per_step": ms_step,
         "profiled_ms_per_step": (t3 - t2) / args.steps * 1e3,
         "higher_is_better": True,
         "scaling": "weak",
@@ -414,16 +484,19 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "N": w.N, "d_h": w.d, "k": w.k, "r": w.r,
-                   "causal": w.causal, "levels": Lv, **({"d_model": w.d_model} if blk else {})},
+                   "causal": w.causal, "levels": Lv, "backward": w.backward,
+                   **({"d_model": w.d_model} if blk is not None else {})},
         "roofline": roof,
+        "roofline_step": step_roof,
+        "roofline_units": {n: {**roofline_entry(r_[1], r_[2], r_[0] / 1e3, peak_tf), "ms_per_step": round(r_[0], 4)}
+                           for n, r_ in sorted(unit_rows.items(), key=lambda x: -x[1][0])},
+        "roofline_kernel_model": kmodel,
         "kernel_ms_per_step": {n: round(t, 4) for n, t in sorted(per_step.items(), key=lambda x: -x[1])},
-        "kernel_roofline_frac": {n: (roofline_of(n)[0]["bound"], roofline_of(n)[0]["frac"])
-                                 for n in sorted(per_step, key=lambda x: -per_step[x]) if n in model},
     }
     if args.rules:
         result["config"]["rules"] = {"gate_hidden": rules_G, "lambda_rule": True}
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline_block(w, inp, blk) if blk else cpu_baseline(w, inp)
+        result["cpu_baseline"] = cpu_baseline_block(w, inp, blk) if blk is not None else cpu_baseline(w, inp)
     print(json.dumps(result), flush=True)
 
 

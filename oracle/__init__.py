@@ -87,6 +87,7 @@ def _load():
         lib.ora_features.argtypes = [C.c_int, C.c_int, P, C.c_int, C.c_int, C.c_double, P, P]
         lib.ora_forward.argtypes = [P] + [P] * 14
         lib.ora_backward.argtypes = [P] + [P] * 15
+        lib.ora_threads.argtypes = [C.c_int]
         _lib = lib
     return _lib
 
@@ -102,6 +103,12 @@ def _ptr(a):
 def _check(rc, what):
     if rc != 0:
         raise RuntimeError(f"oracle {what} failed with code {rc}")
+
+
+def threads(n: int = 0) -> int:
+    """Set the oracle's OpenMP thread count for later calls (n > 0) and
+    return the count in effect (timing runs only)."""
+    return _load().ora_threads(int(n))
 
 
 def hash_keys(X, W, bits: int) -> np.ndarray:

@@ -45,6 +45,7 @@
  * ablation that fixes m_sparse = 1 (Sec. 7).
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -852,4 +853,12 @@ out:
     free(dOs); free(Delta); free(lse1); free(dNum); free(dDen);
     free(phq); free(phk); free(dphq); free(dphk); free(A); free(Bm);
     return rc;
+}
+
+/* Threads of the OpenMP loops above, for timing runs: n > 0 sets the count
+ * used by later calls; returns the count now in effect.  No arithmetic. */
+int ora_threads(int n)
+{
+    if (n > 0) omp_set_num_threads(n);
+    return omp_get_max_threads();
 }

@@ -357,11 +357,14 @@ hipError_t launch_states_t(const Shape& s, const StateArgs& a, int scan_mode, hi
         return hipErrorInvalidConfiguration;
     } else {
         dim3 grid(s.nseg, s.H, s.B);
-        ELSAA_LAUNCH("race_state", (race_state_kernel<T, D, RP>), grid, dim3(kThreads), 0, st, a);
+        // the forward sums key rows, the backward (vscale set) query rows
+        const bool bwd = a.vscale != nullptr;
+        ELSAA_LAUNCH(bwd ? "race_state_bwd" : "race_state_fwd", (race_state_kernel<T, D, RP>), grid, dim3(kThreads),
+                     0, st, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         const int per = RP * D + RP;
-        ELSAA_LAUNCH("race_scan", race_scan_kernel, dim3((per + 255) / 256, s.B * s.H), dim3(256), 0, st,
+        ELSAA_LAUNCH(bwd ? "race_scan_bwd" : "race_scan_fwd", race_scan_kernel, dim3((per + 255) / 256, s.B * s.H), dim3(256), 0, st,
                            a.states, s.nseg, per, scan_mode);
         return hipGetLastError();
     }
