@@ -26,12 +26,23 @@
  * batch.  gates is float32 [B, H, N, 2] = (g_sparse, g_lr) or NULL (all 1).
  *
  * Memory: every pointer except cfg is a device pointer owned by the caller.
- * The library never allocates, frees or synchronises: it enqueues kernels on
- * the given stream and returns; results are valid once the stream has
- * completed.  `saved` (elsaa_saved_bytes) is written by elsaa_fwd and read
- * by elsaa_bwd; `workspace` (elsaa_workspace_bytes) is scratch for one call
- * and may be reused by the next call on the same stream.  Calls that share a
- * workspace on different streams race.
+ * The library never allocates or frees device memory and never synchronises
+ * the caller's stream: it enqueues kernels and returns; results are valid
+ * once the given stream has completed.  `saved` (elsaa_saved_bytes) is
+ * written by elsaa_fwd and read by elsaa_bwd; `workspace`
+ * (elsaa_workspace_bytes) is scratch for one call and may be reused by the
+ * next call on the same stream.  Calls that share a workspace on different
+ * streams race.
+ *
+ * Library-owned HIP objects: on its first call on a device, elsaa_fwd
+ * creates one non-blocking stream of default priority and two events on
+ * that device and keeps them until the process ends.  Each elsaa_fwd call
+ * records an event on the given stream, runs the sort of the selection on
+ * that second stream while the given stream runs the low-rank branch, and
+ * makes the given stream wait for the second stream before the sparse
+ * kernels (also when a launch in between failed), so the call behaves as if
+ * everything ran on the given stream.  Concurrent elsaa_fwd calls on one
+ * device share the second stream, so their sorts run one after another.
  *
  * Errors: every entry point validates all arguments on the host before any
  * launch, so a rejected call writes nothing and leaves the stream untouched.

@@ -8,6 +8,7 @@
 
 #include "elsaa.h"
 #include "causal.hpp"
+#include "fork_join.hpp"
 #include "internal.hpp"
 
 using namespace elsaa;
@@ -164,7 +165,7 @@ FwdWorkspace fwd_workspace(const Shape& s)
     W.keyq = off; off = align256(off + bh * s.N);
     W.keyk = off; off = align256(off + bh * s.N);
     const size_t npart = s.causal ? bh * s.Lv * (size_t)(s.N / 2) : 0;
-    W.part_o = off; off = align256(off + npart * s.D * 4);
+    W.part_o = off; off = align256(off + npart * s.D * (s.bf16 ? 2 : 4));   // storage dtype
     W.part_lse = off; off = align256(off + npart * 4);
     W.total = off;
     return W;
@@ -188,9 +189,9 @@ BwdWorkspace bwd_workspace(const Shape& s)
     W.du_q = off; off = align256(off + bhn * race_wk(s) * (s.bf16 ? 2 : 4));
     W.du_k = off; off = align256(off + bhn * race_wk(s) * (s.bf16 ? 2 : 4));
     W.dv_lr = off; off = align256(off + bhn * s.D * (s.bf16 ? 2 : 4));   // storage dtype
-    W.part_dq = off; off = align256(off + npart * s.D * 4);
-    W.part_dk = off; off = align256(off + npart * s.D * 4);
-    W.part_dv = off; off = align256(off + npart * s.D * 4);
+    W.part_dq = off; off = align256(off + npart * s.D * (s.bf16 ? 2 : 4));   // storage dtype
+    W.part_dk = off; off = align256(off + npart * s.D * (s.bf16 ? 2 : 4));
+    W.part_dv = off; off = align256(off + npart * s.D * (s.bf16 ? 2 : 4));
     W.total = off;
     return W;
 }
@@ -233,8 +234,12 @@ Side* side_stream()
     return sd.ok ? &sd : nullptr;
 }
 
-// Run first(side) on the side stream and second(main) on `main`, both after
-// what `main` already holds; `main` then waits for both.
+hipError_t record_event(hipEvent_t e, hipStream_t s) { return hipEventRecord(e, s); }
+hipError_t clear_error() { return hipGetLastError(); }
+const StreamOps kHipStreamOps = {record_event, hipStreamWaitEvent, hipStreamSynchronize, clear_error};
+
+// first(side) on the device's side stream beside second(main) (fork_join.hpp);
+// without a side stream both run on `main` in order.
 template <class A, class B>
 hipError_t fork_join(hipStream_t main, A first, B second)
 {
@@ -244,14 +249,7 @@ hipError_t fork_join(hipStream_t main, A first, B second)
         return e != hipSuccess ? e : second(main);
     }
     std::lock_guard<std::mutex> lk(sd->mu);
-    hipError_t e;
-    if ((e = hipEventRecord(sd->fork, main)) != hipSuccess) return e;
-    if ((e = hipStreamWaitEvent(sd->stream, sd->fork, 0)) != hipSuccess) return e;
-    const hipError_t e1 = first(sd->stream);
-    const hipError_t e2 = second(main);
-    if ((e = hipEventRecord(sd->join, sd->stream)) != hipSuccess) return e;
-    if ((e = hipStreamWaitEvent(main, sd->join, 0)) != hipSuccess) return e;
-    return e1 != hipSuccess ? e1 : e2;
+    return elsaa::fork_join(kHipStreamOps, main, sd->stream, sd->fork, sd->join, first, second);
 }
 
 int check_rules(const elsaa_token_rules* r, TrParams* p)
@@ -384,7 +382,7 @@ int elsaa_fwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     hipError_t e;
     if ((e = launch_project(s, Q, K, W_sort, W_race, kq, kk, uq, uk, stream)) != hipSuccess)
         return hip_fail(e, "project");
-    float* part_o = at<float>(workspace, W.part_o);
+    void* part_o = at<char>(workspace, W.part_o);
     float* part_lse = at<float>(workspace, W.part_lse);
     // the sort on the side stream beside the low-rank branch (its kernels and
     // the level kernel's cannot share a compute unit, so the levels run after
@@ -442,9 +440,9 @@ int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     if ((e = launch_bwd_rows(s, dO, o_s, o_lr, m, lse, d_lr, gates, lambda_rows, rs, dgates, dlambda, stream)) !=
         hipSuccess)
         return hip_fail(e, "backward row scalars");
-    float* part_dq = at<float>(workspace, W.part_dq);
-    float* part_dk = at<float>(workspace, W.part_dk);
-    float* part_dv = at<float>(workspace, W.part_dv);
+    void* part_dq = at<char>(workspace, W.part_dq);
+    void* part_dk = at<char>(workspace, W.part_dk);
+    void* part_dv = at<char>(workspace, W.part_dv);
     // the causal levels' backward, then the low-rank backward, then the leaf
     // (or sorted blocks), which add the level partials and low-rank
     // gradients (one kernel at a time: each kernel's time is its own)

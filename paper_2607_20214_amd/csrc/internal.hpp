@@ -92,11 +92,12 @@ enum SparsePart {
     kSparseAll = kSparseLevels | kSparseFinal
 };
 
-// sortLSH sparse branch forward + fusion epilogue
+// sortLSH sparse branch forward + fusion epilogue; the causal level partials
+// part_o ([BH][Lv][N/2][D]) are kept in the storage dtype
 hipError_t launch_sparse_fwd(const Shape& s, const void* Q, const void* K, const void* V,
                              const int32_t* perm_q, const int32_t* perm_k, const float* gates,
                              const float* lambda_rows,
-                             const float* O_lr, const float* d_lr, float* part_o, float* part_lse,
+                             const float* O_lr, const float* d_lr, void* part_o, float* part_lse,
                              void* O, float* lse, float* m, float* O_s, hipStream_t st,
                              int parts = kSparseAll);
 
@@ -106,11 +107,12 @@ hipError_t launch_bwd_rows(const Shape& s, const void* dO, const float* Os, cons
                            const float* lambda_rows, float* rs, float* dgates, float* dlambda,
                            hipStream_t st);
 // sparse backward; adds the low-rank parts (du W' for dQ and dK, the dV rows)
-// and writes dQ, dK, dV
+// and writes dQ, dK, dV; the causal level partials part_dq / part_dk / part_dv
+// ([BH][Lv][N/2][D]) are kept in the storage dtype
 hipError_t launch_sparse_bwd(const Shape& s, const void* Q, const void* K, const void* V,
                              const void* dO, const int32_t* perm_q, const int32_t* perm_k,
                              const float* rs, const void* du_q, const void* du_k, const void* wt_hi,
-                             const void* wt_lo, const void* dv_lr, float* part_dq, float* part_dk, float* part_dv,
+                             const void* wt_lo, const void* dv_lr, void* part_dq, void* part_dk, void* part_dv,
                              void* dQ, void* dK, void* dV, hipStream_t st, int parts = kSparseAll);
 
 // token-wise rules: gate network and query-dependent lambda (token_rules.hip)

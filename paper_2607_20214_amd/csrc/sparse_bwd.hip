@@ -14,9 +14,10 @@
 // queries, keys streamed through LDS) and a key-centric pass (dK, dV; one
 // workgroup per 64 keys, queries streamed through LDS).  Both have the three
 // modes of the forward (non-causal blocks, causal levels, causal leaf).  The
-// level passes write per-level partials by natural token index; the leaf
-// passes add the partials of every level and the low-rank gradient and
-// store the final dQ, dK, dV in the storage dtype.
+// level passes write per-level partials by natural token index in the
+// storage dtype (each level's contribution rounded once; the sum over levels
+// is float32); the leaf passes add the partials of every level and the
+// low-rank gradient and store the final dQ, dK, dV in the storage dtype.
 #include "common.hpp"
 #include "internal.hpp"
 #include "causal.hpp"
@@ -45,9 +46,9 @@ struct BArgs {
     const void* wt_hi;        // W' = W_hi' + W_lo' per head, storage dtype [H][D][wk]
     const void* wt_lo;
     const void* dv_lr;        // storage dtype [BHN][D] low-rank dV
-    float* part_dq;           // [BH][Lv][N/2][D] per-level partials, float32
-    float* part_dk;
-    float* part_dv;
+    void* part_dq;            // [BH][Lv][N/2][D] per-level partials, storage dtype
+    void* part_dk;
+    void* part_dv;
     void* dQ;
     void* dK;
     void* dV;
@@ -236,9 +237,9 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
     }
     if (MODE == kLevels) {
         if (qtok < 0) return;
-        float* out = a.part_dq + level_slot(bh, a.Lv, level, N, qtok, 1) * D;
+        S* out = (S*)a.part_dq + level_slot(bh, a.Lv, level, N, qtok, 1) * D;
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) *(f32x4*)(out + 16 * dt + 4 * g) = acc[dt] * a.tau;
+        for (int dt = 0; dt < DT; ++dt) store4<T>(out + 16 * dt + 4 * g, acc[dt] * a.tau);
         return;
     }
     // dQ = this pass + the low-rank part + (leaf) the partials of the levels
@@ -258,16 +259,16 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
     const size_t row = bh * N + qtok;
     unsigned lmask = MODE == kLeaf ? leaf_levels((tile / a.lt.per_leaf) * a.n_leaf, N, a.Lv, true) : 0u;
     while (lmask) {
-        const float* src[2];
+        const S* src[2];
         bool use[2];
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-            src[j] = a.part_dq;
+            src[j] = (const S*)a.part_dq;
             use[j] = lmask != 0;
             if (use[j]) {
                 const int l = __builtin_ctz(lmask);
                 lmask &= lmask - 1;
-                src[j] = a.part_dq + level_slot(bh, a.Lv, l, N, qtok, 1) * D;
+                src[j] = (const S*)a.part_dq + level_slot(bh, a.Lv, l, N, qtok, 1) * D;
             }
         }
         f32x4 x[2][DT];
@@ -275,7 +276,7 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
         for (int j = 0; j < 2; ++j)
             if (use[j])
 #pragma unroll
-                for (int dt = 0; dt < DT; ++dt) x[j][dt] = *(const f32x4*)(src[j] + 16 * dt + 4 * g);
+                for (int dt = 0; dt < DT; ++dt) x[j][dt] = load4<T>(src[j] + 16 * dt + 4 * g);
 #pragma unroll
         for (int j = 0; j < 2; ++j)
             if (use[j])
@@ -467,8 +468,8 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
         const size_t slot = level_slot(bh, a.Lv, level, N, ktok, 0);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-            *(f32x4*)(a.part_dk + slot * D + 16 * dt + 4 * g) = akT[dt] * a.tau;
-            *(f32x4*)(a.part_dv + slot * D + 16 * dt + 4 * g) = avT[dt];
+            store4<T>((S*)a.part_dk + slot * D + 16 * dt + 4 * g, akT[dt] * a.tau);
+            store4<T>((S*)a.part_dv + slot * D + 16 * dt + 4 * g, avT[dt]);
         }
         return;
     }
@@ -491,20 +492,20 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
     for (int dt = 0; dt < DT; ++dt) tv[dt] = avT[dt] + load4<T>((const S*)a.dv_lr + row * D + 16 * dt + 4 * g);
     unsigned lmask = MODE == kLeaf ? leaf_levels((tile / a.lt.per_leaf) * a.n_leaf, N, a.Lv, false) : 0u;
     while (lmask) {
-        const float* sk_[2];
-        const float* sv_[2];
+        const S* sk_[2];
+        const S* sv_[2];
         bool use[2];
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-            sk_[j] = a.part_dk;
-            sv_[j] = a.part_dv;
+            sk_[j] = (const S*)a.part_dk;
+            sv_[j] = (const S*)a.part_dv;
             use[j] = lmask != 0;
             if (use[j]) {
                 const int l = __builtin_ctz(lmask);
                 lmask &= lmask - 1;
                 const size_t slot = level_slot(bh, a.Lv, l, N, ktok, 0);
-                sk_[j] = a.part_dk + slot * D;
-                sv_[j] = a.part_dv + slot * D;
+                sk_[j] = (const S*)a.part_dk + slot * D;
+                sv_[j] = (const S*)a.part_dv + slot * D;
             }
         }
         f32x4 xk[2][DT], xv[2][DT];
@@ -513,8 +514,8 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
             if (use[j])
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt) {
-                    xk[j][dt] = *(const f32x4*)(sk_[j] + 16 * dt + 4 * g);
-                    xv[j][dt] = *(const f32x4*)(sv_[j] + 16 * dt + 4 * g);
+                    xk[j][dt] = load4<T>(sk_[j] + 16 * dt + 4 * g);
+                    xv[j][dt] = load4<T>(sv_[j] + 16 * dt + 4 * g);
                 }
 #pragma unroll
         for (int j = 0; j < 2; ++j)
@@ -720,8 +721,8 @@ __global__ __launch_bounds__(BQ * 4, BQ == 64 ? 3 : 1) void sparse_bwd_block_ker
             for (int dt = 0; dt < DT; ++dt) {
                 const int d0 = 16 * dt + 4 * g;
                 const size_t slot = level_slot(bh, a.Lv, level, N, ktok, 0);
-                *(f32x4*)(a.part_dk + slot * D + d0) = akT[dt] * a.tau;
-                *(f32x4*)(a.part_dv + slot * D + d0) = avT[dt];
+                store4<T>((S*)a.part_dk + slot * D + d0, akT[dt] * a.tau);
+                store4<T>((S*)a.part_dv + slot * D + d0, avT[dt]);
             }
         } else {
             // the low-rank dK part is a product across the wave's lanes: every
@@ -879,8 +880,8 @@ __global__ __launch_bounds__(BQ * 4, BQ == 64 ? 3 : 1) void sparse_bwd_block_ker
                 const int d0 = 16 * dt + 4 * g;
                 if (MODE == kLevels) {
                     if (!kFull && qtok < 0) continue;
-                    float* out = a.part_dq + level_slot(bh, a.Lv, level, N, qtok, 1) * D + d0;
-                    *(f32x4*)out = dq[u] * a.tau;
+                    S* out = (S*)a.part_dq + level_slot(bh, a.Lv, level, N, qtok, 1) * D + d0;
+                    store4<T>(out, dq[u] * a.tau);
                 } else {
                     // the low-rank part is a product across the wave's lanes:
                     // every lane takes part (a lane without a query uses row 0)
@@ -991,7 +992,7 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
 hipError_t launch_sparse_bwd(const Shape& s, const void* Q, const void* K, const void* V,
                              const void* dO, const int32_t* perm_q, const int32_t* perm_k,
                              const float* rs, const void* du_q, const void* du_k, const void* wt_hi,
-                             const void* wt_lo, const void* dv_lr, float* part_dq, float* part_dk, float* part_dv,
+                             const void* wt_lo, const void* dv_lr, void* part_dq, void* part_dk, void* part_dv,
                              void* dQ, void* dK, void* dV, hipStream_t st, int parts)
 {
     BArgs a;

@@ -49,8 +49,8 @@ struct Args {
     const float* lam_rows;    // per-token lambda_i or null (scalar lambda)
     const float* O_lr;
     const float* d_lr;
-    float* part_o;            // [BH][Lv][N/2][D] normalised level outputs (float32: O_s feeds
-    float* part_lse;          // Delta of the backward, where bf16 rounding costs accuracy)
+    void* part_o;             // [BH][Lv][N/2][D] normalised level outputs, storage dtype
+    float* part_lse;          // [BH][Lv][N/2] log of each level's denominator
     void* O;
     float* lse;
     float* m;
@@ -233,9 +233,9 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
         const size_t slot = (bh * a.Lv + level) * (size_t)(N / 2) + (size_t)s2 * half +
                             (qtok - s2 * 2 * half - half);
         const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-        float* po = a.part_o + slot * D;
+        S* po = (S*)a.part_o + slot * D;
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) *(f32x4*)(po + 16 * dt + 4 * g) = acc[dt] * inv;
+        for (int dt = 0; dt < DT; ++dt) store4<T>(po + 16 * dt + 4 * g, acc[dt] * inv);
         if (g == 0) a.part_lse[slot] = (m_run + __log2f(l_run)) * kLn2;
         return;
     }
@@ -269,9 +269,9 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
             for (int j = 0; j < 2; ++j)
                 if (use[j]) {
                     pl[j] = a.part_lse[slot[j]] * kLog2e;
-                    const float* po = a.part_o + slot[j] * D;
+                    const S* po = (const S*)a.part_o + slot[j] * D;
 #pragma unroll
-                    for (int dt = 0; dt < DT; ++dt) v[j][dt] = *(const f32x4*)(po + 16 * dt + 4 * g);
+                    for (int dt = 0; dt < DT; ++dt) v[j][dt] = load4<T>(po + 16 * dt + 4 * g);
                 }
 #pragma unroll
             for (int j = 0; j < 2; ++j)
@@ -341,7 +341,7 @@ hipError_t launch_t(const Shape& s, const Args& a, hipStream_t st, int parts)
 
 hipError_t launch_sparse_fwd(const Shape& s, const void* Q, const void* K, const void* V,
                              const int32_t* perm_q, const int32_t* perm_k, const float* gates,
-                             const float* lambda_rows, const float* O_lr, const float* d_lr, float* part_o, float* part_lse,
+                             const float* lambda_rows, const float* O_lr, const float* d_lr, void* part_o, float* part_lse,
                              void* O, float* lse, float* m, float* O_s, hipStream_t st, int parts)
 {
     Args a;
