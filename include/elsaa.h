@@ -136,6 +136,20 @@ int elsaa_select(const elsaa_config* cfg, const void* Q, const void* K, const fl
                  int32_t* perm_q, int32_t* perm_k, void* workspace, size_t workspace_bytes,
                  hipStream_t stream);
 
+/* The selection above for callers that cannot allocate: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation.  Same
+ * arguments and results as elsaa_select (perm_q, perm_k are the caller's),
+ * without `workspace`: the hash keys (2 * B*H*N bytes, each half 256-byte
+ * aligned) go to a fixed 32 MiB device array inside the library, which every
+ * device the library runs on holds until the process ends.  Rejects
+ * B*H*N above 16777088 tokens with ELSAA_ERR_WORKSPACE before any launch.
+ * Calls no allocating routine (the device address of the array is looked up
+ * once per device, on the first call with that device current).  All calls
+ * on one device share the array: calls that overlap on one device (other
+ * streams, other threads) race; calls on one stream are ordered. */
+int elsaa_select_noalloc(const elsaa_config* cfg, const void* Q, const void* K, const float* W_sort,
+                         int32_t* perm_q, int32_t* perm_k, hipStream_t stream);
+
 /* Forward (Alg. 1 / Alg. 6 without the projections).  gates is [B,H,N,2]
  * float32 (g_sparse, g_lr) or NULL (all 1); lambda_rows is the per-token
  * coefficient lambda_i of Eq. m_sparse, [B,H,N] float32 >= 0, or NULL (the

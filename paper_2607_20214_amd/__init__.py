@@ -104,6 +104,7 @@ def load():
         lib.elsaa_workspace_bytes.argtypes = [P, C.c_int, C.POINTER(C.c_size_t)]
         lib.elsaa_get_saved_layout.argtypes = [P, P]
         lib.elsaa_select.argtypes = [P, P, P, P, P, P, P, S, P]
+        lib.elsaa_select_noalloc.argtypes = [P, P, P, P, P, P, P]
         lib.elsaa_fwd.argtypes = [P, P, P, P, P, P, P, P, P, P, P, P, S, P, S, P]
         lib.elsaa_bwd.argtypes = [P, P, P, P, P, P, P, P, P, P, P, P, S, P, P, P, P, P, P, S, P]
         lib.elsaa_gemm_workspace_bytes.argtypes = [P, C.POINTER(C.c_size_t)]
@@ -260,6 +261,19 @@ def select(cfg: Config, q, k, w_sort, workspace: Optional[torch.Tensor] = None):
     _check(load().elsaa_select(C.byref(c), _p(q), _p(k), _p(w_sort), _p(pq), _p(pk), _p(workspace),
                                workspace.numel(), _stream(dev)))
     return pq, pk
+
+
+def select_noalloc(cfg: Config, q, k, w_sort, perm_q: torch.Tensor, perm_k: torch.Tensor):
+    """The selection into the caller's perm_q, perm_k through
+    elsaa_select_noalloc (no allocation: the library's fixed scratch)."""
+    dev = _check_inputs(cfg, q, k, k, w_sort, None)
+    ps = _perm_shape(cfg)
+    _check_tensor("perm_q", perm_q, ps, torch.int32, dev)
+    _check_tensor("perm_k", perm_k, ps, torch.int32, dev)
+    c = cfg.c()
+    _check(load().elsaa_select_noalloc(C.byref(c), _p(q), _p(k), _p(w_sort), _p(perm_q), _p(perm_k),
+                                       _stream(dev)))
+    return perm_q, perm_k
 
 
 def fwd(cfg: Config, q, k, v, w_sort, w_race, gates=None, buffers: Optional[Buffers] = None,

@@ -252,6 +252,40 @@ hipError_t fork_join(hipStream_t main, A first, B second)
     return elsaa::fork_join(kHipStreamOps, main, sd->stream, sd->fork, sd->join, first, second);
 }
 
+// Fixed device scratch of the entry point that allocates nothing
+// (elsaa_select_noalloc): the hash keys of the Q and K rows.  In host code
+// `scratch` names a host-side stand-in, not the device array, so only the
+// per-device address from hipGetSymbolAddress is ever handed to a kernel.
+constexpr size_t kNoallocScratchBytes = (size_t)32 << 20;
+__device__ __attribute__((aligned(256))) uint8_t scratch[kNoallocScratchBytes];
+
+struct ScratchAddr {
+    std::once_flag once;
+    void* ptr = nullptr;
+    hipError_t err = hipSuccess;
+};
+ScratchAddr g_scratch[kMaxDevices];
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept.
+hipError_t scratch_address(void** out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    ScratchAddr& sa = g_scratch[dev];
+    std::call_once(sa.once, [&sa]() {
+        void* p = nullptr;
+        sa.err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (sa.err == hipSuccess) sa.ptr = p;
+    });
+    if (sa.err != hipSuccess) return sa.err;
+    if (!sa.ptr) return hipErrorInvalidSymbol;
+    *out = sa.ptr;
+    return hipSuccess;
+}
+
 int check_rules(const elsaa_token_rules* r, TrParams* p)
 {
     if (!r) return fail(ELSAA_ERR_INVALID_ARG, "rules is NULL");
@@ -345,6 +379,31 @@ int elsaa_select(const elsaa_config* cfg, const void* Q, const void* K, const fl
     uint8_t* kq = at<uint8_t>(workspace, W.keyq);
     uint8_t* kk = at<uint8_t>(workspace, W.keyk);
     hipError_t e;
+    if ((e = launch_project(s, Q, K, W_sort, nullptr, kq, kk, nullptr, nullptr, stream)) != hipSuccess)
+        return hip_fail(e, "hash");
+    if ((e = launch_sort(s, kq, kk, perm_q, perm_k, stream)) != hipSuccess) return hip_fail(e, "sort");
+    return ELSAA_OK;
+}
+
+int elsaa_select_noalloc(const elsaa_config* cfg, const void* Q, const void* K, const float* W_sort,
+                         int32_t* perm_q, int32_t* perm_k, hipStream_t stream)
+{
+    Shape s;
+    int rc = validate(cfg, &s);
+    if (rc) return rc;
+    if (!Q || !K || !W_sort || !perm_q || !perm_k) return fail(ELSAA_ERR_INVALID_ARG, "a required pointer is NULL");
+    if (!aligned16(Q) || !aligned16(K)) return fail(ELSAA_ERR_INVALID_ARG, "Q and K must be 16-byte aligned");
+    const size_t bhn = (size_t)s.B * s.H * s.N;
+    const size_t keyk = align256(bhn);
+    if (keyk + bhn > kNoallocScratchBytes)
+        return fail(ELSAA_ERR_WORKSPACE, "B*H*N = %zu tokens need %zu bytes of scratch; the fixed scratch holds %zu",
+                    bhn, keyk + bhn, kNoallocScratchBytes);
+    void* base = nullptr;
+    hipError_t e;
+    if ((e = scratch_address(&base)) != hipSuccess) return hip_fail(e, "scratch address");
+    uint8_t* kq = (uint8_t*)base;
+    uint8_t* kk = (uint8_t*)base + keyk;
+    // every key the sort reads is written by the hash pass first: nothing to clear
     if ((e = launch_project(s, Q, K, W_sort, nullptr, kq, kk, nullptr, nullptr, stream)) != hipSuccess)
         return hip_fail(e, "hash");
     if ((e = launch_sort(s, kq, kk, perm_q, perm_k, stream)) != hipSuccess) return hip_fail(e, "sort");

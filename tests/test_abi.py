@@ -175,3 +175,15 @@ def test_token_rules_validation(kw, status):
         rc = lib.elsaa_token_rules_bwd(C.byref(c), C.byref(r), fake, None, None, fake, *([None] * 7),
                                        fake, 1 << 40, None)
         assert rc == -1
+
+
+def test_select_noalloc_rejects_on_the_host():
+    """The no-allocation selection checks pointers and its fixed scratch
+    limit (2 * B*H*N bytes of keys within 32 MiB) before any HIP call."""
+    lib = E.load()
+    fake = C.c_void_p(1 << 20)
+    c = _cfg().c()
+    assert lib.elsaa_select_noalloc(C.byref(c), None, fake, fake, fake, fake, None) == -1
+    big = _cfg(B=1, H=256, N=65600, causal=False).c()
+    assert lib.elsaa_select_noalloc(C.byref(big), fake, fake, fake, fake, fake, None) == -3
+    assert "scratch" in lib.elsaa_last_error().decode()
