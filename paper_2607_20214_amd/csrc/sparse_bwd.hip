@@ -99,6 +99,71 @@ __device__ __forceinline__ f32x4 lowrank_tile(const typename T::store_t* du_row,
     return acc;
 }
 
+// W' = W_hi' + W_lo' of one head staged in LDS for the low-rank parts of the
+// epilogues: each part [D][wk + 8] (the pad spreads a slice's 16 rows over
+// the banks).  Loaded into registers with the first tile's rows and written
+// to LDS before that tile's barrier, so the epilogue reads it without a
+// global round trip and every wave of the workgroup shares one copy.
+template <class T, int D>
+struct WtStage {
+    using S = typename T::store_t;
+    static constexpr int kMaxWk = 64;
+    static constexpr int EPC = 16 / T::bytes;                  // elements per 16-byte piece
+    static constexpr int PARTS = T::kSplit ? 2 : 1;
+    __host__ __device__ static constexpr size_t bytes(int wk) { return (size_t)PARTS * D * (wk + 8) * T::bytes; }
+    // global -> LDS directly (gfx950 global_load_lds_dwordx4: one wave
+    // instruction writes 64 consecutive 16-byte pieces of LDS, piece l from
+    // lane l; no registers hold the data).  The LDS bytes are cut into
+    // 16-byte pieces q = ((part * D + row) * CR + c); the pad piece of a row
+    // fetches the row's first piece again and is never read.  Issued before
+    // any other load of the workgroup, so the wait for the first tile's rows
+    // (the memory counter retires loads in order) also covers it.
+    __device__ __forceinline__ static void issue(const S* wth, const S* wtl, int wk, S* lds)
+    {
+        typedef __attribute__((address_space(3))) void lds_void_t;
+        const int CR = (wk + 8) * T::bytes / 16, CD = wk * T::bytes / 16;
+        const int pieces = PARTS * D * CR, per_part = D * CR;
+        const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6), lane = threadIdx.x & 63;
+        for (int j = w; 64 * j < pieces; j += kThreads / 64) {
+            const int q = 64 * j + lane;
+            if (q < pieces) {
+                const int part = q >= per_part, rem = q - part * per_part;
+                const int row = rem / CR, c = rem - row * CR;
+                const S* src = (part ? wtl : wth) + (size_t)row * wk + (c < CD ? c : 0) * EPC;
+                __builtin_amdgcn_global_load_lds(src, (lds_void_t*)(lds + (size_t)64 * j * EPC), 16, 0, 0);
+            }
+        }
+    }
+};
+
+// lowrank_tile with W' from the LDS copy (wt = WtStage layout) and the
+// token's du fragments already in registers (du_f[j]: elements 32 j + 8 g ..).
+template <class T, int D>
+__device__ __forceinline__ f32x4 lowrank_lds(const typename T::frag_t (&du_f)[2], const typename T::store_t* wt,
+                                             int wk, int g, int col, int dt)
+{
+    const int wkp = wk + 8;
+    f32x4 acc = {0, 0, 0, 0};
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+        if (32 * j < wk) {
+            const typename T::store_t* p = wt + (16 * dt + col) * wkp + 32 * j + 8 * g;
+            acc = T::mma(T::ld8(p), du_f[j], acc);
+            if (T::kSplit) acc = T::mma(T::ld8(p + D * wkp), du_f[j], acc);
+        }
+    return acc;
+}
+
+// du fragments of one token row (wk <= 64 values, zero k-steps past wk).
+template <class T>
+__device__ __forceinline__ void du_frags(const typename T::store_t* du_row, int wk, int g,
+                                         typename T::frag_t (&f)[2])
+{
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+        if (32 * j < wk) f[j] = T::ld8(du_row + 32 * j + 8 * g);
+}
+
 // ------------------------------------------------------------------------
 // dQ: query-centric.  One workgroup per 64 queries (16 per wave, one per
 // lane column); key tiles of 64 rows stream through LDS (tile.hpp) with the
@@ -106,16 +171,25 @@ __device__ __forceinline__ f32x4 lowrank_tile(const typename T::store_t* du_row,
 // and dP^T = V dO^T (key rows from LDS, this lane's query in registers),
 // dS^T in registers, dQ^T += K^T dS^T with K^T from the transposed LDS read.
 // ------------------------------------------------------------------------
+// LDS bytes of the query-centric pass (K and V tiles, W' for the epilogue).
 template <class T, int D, int MODE>
-__device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, int b)
+__host__ __device__ constexpr size_t dq_lds_bytes(int wk)
+{
+    return 2 * (size_t)tile::Tile<T, D, kThreads>::elems(kT) * T::bytes +
+           (MODE == kLevels ? 0 : WtStage<T, D>::bytes(wk));
+}
+
+template <class T, int D, int MODE>
+__device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, int b, char* smem)
 {
     using S = typename T::store_t;
     using F = typename T::frag_t;
     constexpr int KS = D / 32, DT = D / 16;
     using TD = tile::Tile<T, D, kThreads>;
     constexpr int PT = TD::PER_THREAD;
-    __shared__ __attribute__((aligned(16))) S sk[TD::elems(kT)];
-    __shared__ __attribute__((aligned(16))) S sv[TD::elems(kT)];
+    S* const sk = (S*)smem;
+    S* const sv = sk + TD::elems(kT);
+    S* const swt = sv + TD::elems(kT);          // W' (leaf, blocks)
     const size_t bh = (size_t)b * a.H + h;
     const int N = a.N;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -168,6 +242,10 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
     const int ntiles = (kend - kbeg + kT - 1) / kT;
     int tok[PT];
     uint4 rk[PT], rv[PT];
+    if (MODE != kLevels) {
+        const size_t wh = (bh % a.H) * D * a.wk;
+        WtStage<T, D>::issue((const S*)a.wt_hi + wh, (const S*)a.wt_lo + wh, a.wk, swt);
+    }
     tokens(kbeg, tok);
     TD::load(K, tok, rk);
     TD::load(V, tok, rv);
@@ -196,11 +274,16 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) acc[dt] = f32x4{0, 0, 0, 0};
 
+    if (MODE != kLevels && ntiles == 0) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+    }
     for (int t = 0; t < ntiles; ++t) {
         const int k0 = kbeg + t * kT;
         if (t > 0) __syncthreads();
         TD::store(sk, rk);
         TD::store(sv, rv);
+        if (MODE != kLevels && t == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // W' in LDS
         __syncthreads();
         if (t + 1 < ntiles) {
             TD::load(K, tok, rk);
@@ -242,21 +325,19 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
         for (int dt = 0; dt < DT; ++dt) store4<T>(out + 16 * dt + 4 * g, acc[dt] * a.tau);
         return;
     }
-    // dQ = this pass + the low-rank part + (leaf) the partials of the levels
-    // where the query was a future query, added in that order; the partial
-    // rows are fetched two at a time so their loads are in flight together.
-    // The low-rank part is a product across the wave's lanes, so every lane
-    // takes part (a lane without a query uses row 0 and discards the result).
+    // dQ = this pass + the low-rank part (W' from LDS) + (leaf) the partials
+    // of the levels where the query was a future query, added in that order;
+    // the partial rows are fetched two at a time so their loads are in
+    // flight together.  The low-rank part is a product across the wave's
+    // lanes, so every lane takes part (a lane without a query uses row 0 and
+    // discards the result).
+    const size_t row = bh * N + max(qtok, 0);
+    F duf[2];
+    du_frags<T>((const S*)a.du_q + row * a.wk, a.wk, g, duf);
     f32x4 tot[DT];
-    {
-        const S* du = (const S*)a.du_q + (bh * N + max(qtok, 0)) * a.wk;
-        const S* wth = (const S*)a.wt_hi + (bh % a.H) * D * a.wk;
-        const S* wtl = (const S*)a.wt_lo + (bh % a.H) * D * a.wk;
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) tot[dt] = acc[dt] * a.tau + lowrank_tile<T>(du, wth, wtl, a.wk, g, qq, dt);
-    }
+    for (int dt = 0; dt < DT; ++dt) tot[dt] = acc[dt] * a.tau + lowrank_lds<T, D>(duf, swt, a.wk, g, qq, dt);
     if (qtok < 0) return;
-    const size_t row = bh * N + qtok;
     unsigned lmask = MODE == kLeaf ? leaf_levels((tile / a.lt.per_leaf) * a.n_leaf, N, a.Lv, true) : 0u;
     while (lmask) {
         const S* src[2];
@@ -295,18 +376,30 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
 // S = Q K^T and dP = dO V^T (query rows from LDS), then dV^T += dO^T P and
 // dK^T += Q^T dS with the transposed operands read from the query tiles.
 // ------------------------------------------------------------------------
+// LDS bytes of the key-centric pass (Q and dO tiles, the tile's row
+// scalars, W' for the epilogue).
 template <class T, int D, int MODE>
-__device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h, int b)
+__host__ __device__ constexpr size_t dkv_lds_bytes(int wk)
+{
+    return 2 * (size_t)tile::Tile<T, D, kThreads>::elems(kT) * T::bytes + 4 * kT * 4 +
+           (MODE == kLevels ? 0 : WtStage<T, D>::bytes(wk));
+}
+
+template <class T, int D, int MODE>
+__device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h, int b, char* smem)
 {
     using S = typename T::store_t;
     using F = typename T::frag_t;
     constexpr int KS = D / 32, DT = D / 16;
     using TD = tile::Tile<T, D, kThreads>;
     constexpr int PT = TD::PER_THREAD;
-    __shared__ __attribute__((aligned(16))) S sq[TD::elems(kT)];
-    __shared__ __attribute__((aligned(16))) S so[TD::elems(kT)];
-    __shared__ float s_l2[kT], s_de[kT], s_sc[kT];
-    __shared__ int s_ok[kT];
+    S* const sq = (S*)smem;
+    S* const so = sq + TD::elems(kT);
+    float* const s_l2 = (float*)(so + TD::elems(kT));
+    float* const s_de = s_l2 + kT;
+    float* const s_sc = s_de + kT;
+    int* const s_ok = (int*)(s_sc + kT);
+    S* const swt = (S*)(s_ok + kT);              // W' (leaf, blocks)
     const size_t bh = (size_t)b * a.H + h;
     const int N = a.N;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -381,6 +474,10 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
     const int ntiles = (qend - qbeg + kT - 1) / kT;
     int tok[PT], qt_cur, qt_next = -1;
     uint4 rq[PT], ro[PT];
+    if (MODE != kLevels) {
+        const size_t wh = (bh % a.H) * D * a.wk;
+        WtStage<T, D>::issue((const S*)a.wt_hi + wh, (const S*)a.wt_lo + wh, a.wk, swt);
+    }
     tokens(qbeg, tok, qt_cur);
     TD::load(Q, tok, rq);
     TD::load(dO, tok, ro);
@@ -405,6 +502,10 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) { akT[dt] = f32x4{0, 0, 0, 0}; avT[dt] = f32x4{0, 0, 0, 0}; }
 
+    if (MODE != kLevels && ntiles == 0) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+    }
     for (int t = 0; t < ntiles; ++t) {
         const int q0 = qbeg + t * kT;
         if (t > 0) __syncthreads();
@@ -416,6 +517,7 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
             s_sc[threadIdx.x] = sc;
             s_ok[threadIdx.x] = qt_cur >= 0;
         }
+        if (MODE != kLevels && t == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // W' in LDS
         __syncthreads();
         if (t + 1 < ntiles) {
             TD::load(Q, tok, rq);
@@ -474,22 +576,25 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
         return;
     }
     // dK, dV = this pass + the low-rank parts + (leaf) the partials of the
-    // levels where the key was a past key, added in that order; the partial
-    // rows are fetched two (dK, dV) pairs at a time so their loads are in
-    // flight together.  The low-rank dK part is a product across the wave's
-    // lanes, so every lane takes part (a lane without a key uses row 0).
-    f32x4 tk[DT], tv[DT];
-    {
-        const S* du = (const S*)a.du_k + (bh * N + max(ktok, 0)) * a.wk;
-        const S* wth = (const S*)a.wt_hi + (bh % a.H) * D * a.wk;
-        const S* wtl = (const S*)a.wt_lo + (bh % a.H) * D * a.wk;
+    // levels where the key was a past key, added in that order.  The du and
+    // low-rank dV rows are requested together, before the low-rank product
+    // (W' from LDS); the partial rows follow two (dK, dV) pairs at a time so
+    // their loads are in flight together.  The low-rank dK part is a product
+    // across the wave's lanes, so every lane takes part (a lane without a
+    // key uses row 0).
+    const size_t row = bh * N + max(ktok, 0);
+    F duf[2];
+    du_frags<T>((const S*)a.du_k + row * a.wk, a.wk, g, duf);
+    f32x4 tv[DT];
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) tk[dt] = akT[dt] * a.tau + lowrank_tile<T>(du, wth, wtl, a.wk, g, col, dt);
+    for (int dt = 0; dt < DT; ++dt) tv[dt] = load4<T>((const S*)a.dv_lr + row * D + 16 * dt + 4 * g);
+    f32x4 tk[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+        tk[dt] = akT[dt] * a.tau + lowrank_lds<T, D>(duf, swt, a.wk, g, col, dt);
+        tv[dt] = avT[dt] + tv[dt];
     }
     if (ktok < 0) return;
-    const size_t row = bh * N + ktok;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) tv[dt] = avT[dt] + load4<T>((const S*)a.dv_lr + row * D + 16 * dt + 4 * g);
     unsigned lmask = MODE == kLeaf ? leaf_levels((tile / a.lt.per_leaf) * a.n_leaf, N, a.Lv, false) : 0u;
     while (lmask) {
         const S* sk_[2];
@@ -535,20 +640,34 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
     }
 }
 
+// float32 storage at d_h 128 holds twice the operand registers: one wave
+// per SIMD, so the accumulation registers can take what does not fit
+template <class T, int D>
+constexpr int two_pass_waves() { return T::bytes == 4 && D == 128 ? 1 : 2; }
+
+// LDS of the two passes: the tiles plus, outside the levels, W' sized for
+// the largest wk (64).
 template <class T, int D, int MODE>
-__global__ __launch_bounds__(kThreads, 2) void sparse_dq_kernel(BArgs a)
+constexpr size_t dq_lds() { return dq_lds_bytes<T, D, MODE>(WtStage<T, D>::kMaxWk); }
+template <class T, int D, int MODE>
+constexpr size_t dkv_lds() { return dkv_lds_bytes<T, D, MODE>(WtStage<T, D>::kMaxWk); }
+
+template <class T, int D, int MODE>
+__global__ __launch_bounds__(kThreads, (two_pass_waves<T, D>())) void sparse_dq_kernel(BArgs a)
 {
+    __shared__ __attribute__((aligned(16))) char smem[dq_lds<T, D, MODE>()];
     int tile, h, b;
     xcd_tile(tile, h, b);
-    sparse_dq_body<T, D, MODE>(a, tile, h, b);
+    sparse_dq_body<T, D, MODE>(a, tile, h, b, smem);
 }
 
 template <class T, int D, int MODE>
-__global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
+__global__ __launch_bounds__(kThreads, (two_pass_waves<T, D>())) void sparse_dkv_kernel(BArgs a)
 {
+    __shared__ __attribute__((aligned(16))) char smem[dkv_lds<T, D, MODE>()];
     int tile, h, b;
     xcd_tile(tile, h, b);
-    sparse_dkv_body<T, D, MODE>(a, tile, h, b);
+    sparse_dkv_body<T, D, MODE>(a, tile, h, b, smem);
 }
 
 // Both leaf passes in one launch: the workgroups of a leaf (its query tiles
@@ -556,13 +675,16 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_dkv_kernel(BArgs a)
 // XCD at about the same time and the leaf's Q, K, V, dO rows, read by both
 // passes, come from that XCD's L2 the second time.
 template <class T, int D>
-__global__ __launch_bounds__(kThreads, 2) void sparse_leaf_bwd_kernel(BArgs a)
+__global__ __launch_bounds__(kThreads, (two_pass_waves<T, D>())) void sparse_leaf_bwd_kernel(BArgs a)
 {
     int t2, h, b;
     xcd_tile(t2, h, b);
     const int per = a.lt.per_leaf, leaf = t2 / (2 * per), r = t2 - leaf * 2 * per;
-    if (r < per) sparse_dq_body<T, D, kLeaf>(a, leaf * per + r, h, b);
-    else sparse_dkv_body<T, D, kLeaf>(a, leaf * per + r - per, h, b);
+    // the two passes share one LDS region (a workgroup runs one of them)
+    constexpr size_t q = dq_lds<T, D, kLeaf>(), kv = dkv_lds<T, D, kLeaf>();
+    __shared__ __attribute__((aligned(16))) char smem[q > kv ? q : kv];
+    if (r < per) sparse_dq_body<T, D, kLeaf>(a, leaf * per + r, h, b, smem);
+    else sparse_dkv_body<T, D, kLeaf>(a, leaf * per + r - per, h, b, smem);
 }
 
 // ------------------------------------------------------------------------
@@ -588,8 +710,13 @@ __global__ __launch_bounds__(kThreads, 2) void sparse_leaf_bwd_kernel(BArgs a)
 // and stores there carry no per-row branch and the compiler can wait for
 // exactly the loads it needs (its memory counter retires in order).
 // ------------------------------------------------------------------------
+// waves per SIMD: three for 64-query blocks at d_h 64, two otherwise (a
+// 128-query block is 8 waves, two per SIMD)
+template <int D, int BQ>
+constexpr int block_waves() { return BQ == 64 && D == 64 ? 3 : 2; }
+
 template <class T, int D, int BQ, int MODE>
-__global__ __launch_bounds__(BQ * 4, BQ == 64 ? 3 : 1) void sparse_bwd_block_kernel(BArgs a)
+__global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_block_kernel(BArgs a)
 {
     using S = typename T::store_t;
     using F = typename T::frag_t;
@@ -727,19 +854,18 @@ __global__ __launch_bounds__(BQ * 4, BQ == 64 ? 3 : 1) void sparse_bwd_block_ker
         } else {
             // the low-rank dK part is a product across the wave's lanes: every
             // lane takes part (a lane without a key uses row 0), then stores
+            // (one 16-row slice at a time, so only one slice of it is live)
             const size_t wh = (bh % a.H) * D * a.wk;
             const S* du = (const S*)a.du_k + (bh * N + max(ktok, 0)) * a.wk;
-            f32x4 lrk[DT];
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt)
-                lrk[dt] = lowrank_tile<T>(du, (const S*)a.wt_hi + wh, (const S*)a.wt_lo + wh, a.wk, g, col, dt);
-            if (ktok < 0) return;
-            const size_t row = bh * N + ktok;
+            const size_t row = bh * N + max(ktok, 0);
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) {
-                const int d0 = 16 * dt + 4 * g;
-                store4<T>((S*)a.dK + row * D + d0, akT[dt] * a.tau + lrk[dt]);
-                store4<T>((S*)a.dV + row * D + d0, avT[dt] + load4<T>((const S*)a.dv_lr + row * D + d0));
+                const f32x4 lr = lowrank_tile<T>(du, (const S*)a.wt_hi + wh, (const S*)a.wt_lo + wh, a.wk, g, col, dt);
+                if (ktok >= 0) {
+                    const int d0 = 16 * dt + 4 * g;
+                    store4<T>((S*)a.dK + row * D + d0, akT[dt] * a.tau + lr);
+                    store4<T>((S*)a.dV + row * D + d0, avT[dt] + load4<T>((const S*)a.dv_lr + row * D + d0));
+                }
             }
         }
     };
@@ -934,15 +1060,20 @@ template <class T, int D>
 hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
 {
     hipError_t e;
-    // whole-block kernel: b in {64, 128}, blocks never straddle a segment
+    // whole-block kernel: b in {64, 128}, blocks never straddle a segment;
+    // b = 128 only where its registers fit without spilling (bf16 storage;
+    // non-causal blocks, which also form the low-rank parts, only at d_h 64)
     const int bq = s.k;
-    const bool whole = (bq == 64 || bq == 128) && s.neighbors == 0 && (s.causal ? (s.n_leaf % bq == 0) : true);
+    const bool fits128 = T::bytes == 2 && (s.causal || D == 64);
+    const bool whole = (bq == 64 || (bq == 128 && fits128)) && s.neighbors == 0 &&
+                       (s.causal ? (s.n_leaf % bq == 0) : true);
     if (!s.causal) {
         if (whole) {
             if (!(parts & kSparseFinalQ)) return hipSuccess;
             const int nbx = (s.N + bq - 1) / bq;
             if (bq == 64) launch_blocks<T, D, 64, kBlocks>("sparse_bwd_blocks", a, nbx, s.B * s.H, st);
-            else launch_blocks<T, D, 128, kBlocks>("sparse_bwd_blocks", a, nbx, s.B * s.H, st);
+            else if constexpr (T::bytes == 2 && D == 64)
+                launch_blocks<T, D, 128, kBlocks>("sparse_bwd_blocks", a, nbx, s.B * s.H, st);
             return hipGetLastError();
         }
         dim3 grid((s.N + kT - 1) / kT, s.H, s.B);
@@ -960,7 +1091,7 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
         if (whole) {
             const int nbx = s.Lv * (s.N / 2) / bq;
             if (bq == 64) launch_blocks<T, D, 64, kLevels>("sparse_bwd_levels", a, nbx, s.B * s.H, st);
-            else launch_blocks<T, D, 128, kLevels>("sparse_bwd_levels", a, nbx, s.B * s.H, st);
+            else if constexpr (T::bytes == 2) launch_blocks<T, D, 128, kLevels>("sparse_bwd_levels", a, nbx, s.B * s.H, st);
             if ((e = hipGetLastError()) != hipSuccess) return e;
         } else {
             dim3 grid(a.lt.first[s.Lv], s.H, s.B);

@@ -19,6 +19,9 @@ SMALL = [
     _w("nc-f32-512", 1, 1, 512, 64, 32, 32, False, "f32"),
     _w("nc-bf16-ragged-300", 1, 2, 300, 64, 64, 64, False, "bf16", recipe="clustered"),
     _w("nc-bf16-d128-k48-777", 1, 1, 777, 128, 48, 128, False, "bf16"),
+    _w("nc-bf16-d64-k128-1000", 1, 2, 1000, 64, 128, 64, False, "bf16"),
+    _w("nc-bf16-d128-k128-1000", 1, 1, 1000, 128, 128, 128, False, "bf16"),
+    _w("nc-f32-d128-k64-700", 1, 1, 700, 128, 64, 64, False, "f32"),
     _w("c-bf16-d128-1024", 1, 2, 1024, 128, 64, 128, True, "bf16"),
     _w("c-bf16-d64-2048-clustered", 1, 2, 2048, 64, 128, 64, True, "bf16", recipe="clustered"),
     _w("c-f32-d64-512", 1, 1, 512, 64, 32, 32, True, "f32"),
