@@ -89,11 +89,17 @@ typedef struct {
     int32_t m_one;          /* 1: m_sparse = 1, the Sort_Lsh_RACE ablation (Sec. 7); 0: ELSAA */
 } elsaa_config;
 
-/* Number of causal recursion levels Lv (0 for non-causal): the smallest Lv
- * with N / 2^Lv <= n0.  Returns a negative status if some segment longer
- * than n0 would have odd length (Alg. 5 would pad it with a zero token; the
- * GPU path does not implement that padding). */
+/* Number of causal recursion levels Lv (0 for non-causal).  Alg. 5 splits
+ * every list longer than n0 into halves, padding an odd list with one zero
+ * token first, so the lists at depth l all have L_l entries with L_0 = N,
+ * L_{l+1} = ceil(L_l / 2), and Lv is the smallest depth with L_Lv <= n0.
+ * Returns a negative status where a past half would have to hold a zero
+ * token (fewer real tokens than half its list; never for n0 >= 2 * Lv). */
 int elsaa_num_levels(const elsaa_config* cfg);
+
+/* Entries of perm_q / perm_k per (b, h): N non-causal; causal the sum over
+ * levels l < Lv of 2^l * L_{l+1} (= Lv * N / 2 when no list is padded). */
+int64_t elsaa_perm_length(const elsaa_config* cfg);
 
 /* Bytes of the `saved` buffer elsaa_fwd fills and elsaa_bwd reads, and of
  * the per-call scratch `workspace` (pass 0: elsaa_fwd / elsaa_select,
@@ -129,9 +135,15 @@ int elsaa_get_saved_layout(const elsaa_config* cfg, elsaa_saved_layout* out);
  * Output (int32 token indices within one (b,h)):
  *   non-causal: perm_q, perm_k [B,H,N]; sorted block t = positions
  *               [t*k, (t+1)*k) and query block t sees key block t;
- *   causal:     perm_q, perm_k [B,H,Lv,N/2]; level l lists its 2^l segments
- *               of length N/2^l in order, each giving its future half's
- *               queries (perm_q) and its past half's keys (perm_k) sorted. */
+ *   causal:     perm_q, perm_k [B,H,P] (P = elsaa_perm_length); level l
+ *               holds its 2^l segments in order, each giving its future
+ *               half's queries (perm_q) and its past half's keys (perm_k)
+ *               sorted, L_{l+1} entries each (elsaa_num_levels); a segment
+ *               spans the real tokens [a, a + r) of its list, the rest of the
+ *               list being Alg. 5's zero tokens, which trail future halves
+ *               only: they take the bucket of the zero vector (key 0), sort
+ *               after the real tokens of that bucket, and appear in perm_q
+ *               as -1.  Without padding this is [B,H,Lv,N/2]. */
 int elsaa_select(const elsaa_config* cfg, const void* Q, const void* K, const float* W_sort,
                  int32_t* perm_q, int32_t* perm_k, void* workspace, size_t workspace_bytes,
                  hipStream_t stream);

@@ -80,6 +80,8 @@ def _load():
         P = C.c_void_p
         lib.ora_hash.argtypes = [C.c_int, C.c_int, P, C.c_int, P, P]
         lib.ora_num_levels.argtypes = [P]
+        lib.ora_perm_length.argtypes = [P]
+        lib.ora_perm_length.restype = C.c_int64
         lib.ora_select.argtypes = [P, P, P, P, P, P]
         lib.ora_support_size.argtypes = [P, P, P, P]
         lib.ora_support_size.restype = C.c_int64
@@ -124,15 +126,24 @@ def num_levels(cfg: HeadCfg) -> int:
     return _load().ora_num_levels(C.byref(c))
 
 
+def perm_length(cfg: HeadCfg) -> int:
+    """Entries of one head's sorted lists (N; causal: all levels' lists)."""
+    c = cfg.c()
+    return _load().ora_perm_length(C.byref(c))
+
+
 def select(cfg: HeadCfg, Q, K, Wsort):
-    """Sorted index lists of one head (non-causal [N]; causal [Lv, N/2])."""
+    """Sorted index lists of one head: non-causal [N]; causal [Lv, N/2] when
+    no list is padded, else the levels' lists one after another [P] (zero
+    tokens of future halves as -1)."""
     Q, K, Wsort = _f32(Q), _f32(K), _f32(Wsort)
     c = cfg.c()
     if cfg.causal:
         lv = num_levels(cfg)
         if lv < 0:
-            raise ValueError("causal layout needs even segment lengths above n0")
-        shape = (lv, cfg.N // 2)
+            raise ValueError("a past half would hold a zero token: no sorted-list layout")
+        p = perm_length(cfg)
+        shape = (lv, cfg.N // 2) if (cfg.N % 2 == 0 and p == lv * (cfg.N // 2)) else (p,)
     else:
         shape = (cfg.N,)
     pq = np.empty(shape, np.int32)

@@ -132,28 +132,53 @@ static void sort_positions(int n, const uint32_t* keys, int32_t* order, kp_t* tm
     for (int i = 0; i < n; ++i) order[i] = tmp[i].pos;
 }
 
-/* Number of causal recursion levels for the regular layout: the smallest
- * Lv with N / 2^Lv <= n0 such that every split segment has even length;
- * -1 if some segment longer than n0 would be odd (zero padding needed). */
+/* Number of levels of the Alg. 5 recursion: every list longer than n0 is
+ * padded to even length with one zero token (Alg. 5) and halved, so all
+ * lists of depth l have L_l entries (L_0 = N, L_{l+1} = ceil(L_l / 2)) and
+ * Lv is the smallest depth with L_Lv <= n0.  Zero tokens only trail future
+ * halves; -1 if some past half would have to hold one (its list has fewer
+ * real tokens than half its length), a case the sorted-list layout below
+ * does not describe. */
 int ora_num_levels(const ora_cfg* c)
 {
     if (!cfg_ok(c)) return -1;
     if (!c->causal) return 0;
     int lv = 0;
-    int64_t n = c->N;
+    int64_t n = c->N, pads = 0;   /* pads: most zero tokens of a depth-lv list (all-future path) */
     while (n > c->n0) {
-        if (n & 1) return -1;
-        n >>= 1;
+        const int64_t m = (n + 1) / 2;
+        if (pads > n - m) return -1;
+        pads += n & 1;
+        n = m;
         ++lv;
     }
     return lv;
 }
 
+/* Entries per (b,h) of the causal sorted lists: level l has 2^l lists of
+ * L_{l+1} entries. */
+int64_t ora_perm_length(const ora_cfg* c)
+{
+    const int lv = ora_num_levels(c);
+    if (lv < 0) return -1;
+    if (!c->causal) return c->N;
+    int64_t n = c->N, total = 0;
+    for (int l = 0; l < lv; ++l) {
+        n = (n + 1) / 2;
+        total += n << l;
+    }
+    return total;
+}
+
 /* Sorted index lists in the layout the GPU library writes:
  *   non-causal: perm_q[N], perm_k[N] = token indices in sorted order;
- *   causal:     perm_q[Lv][N/2], perm_k[Lv][N/2]; level l holds its 2^l
- *               segments in order, each contributing its future half's
- *               queries (perm_q) and its past half's keys (perm_k) sorted. */
+ *   causal:     per level l, its 2^l segments in order, each contributing
+ *               its future half's queries (perm_q) and its past half's keys
+ *               (perm_k) sorted, L_{l+1} entries each.  A segment's list is
+ *               a run of real tokens [a, a + r) followed by zero tokens; the
+ *               zero tokens of a future half take the hash key of the zero
+ *               vector, sort by (key, list position) with the real tokens,
+ *               and are written as -1. */
 int ora_select(const ora_cfg* c, const float* Q, const float* K, const float* Wsort,
                int32_t* perm_q, int32_t* perm_k)
 {
@@ -164,6 +189,8 @@ int ora_select(const ora_cfg* c, const float* Q, const float* K, const float* Ws
     uint32_t* kb = (uint32_t*)malloc(sizeof(uint32_t) * (size_t)N);
     int32_t* ord = (int32_t*)malloc(sizeof(int32_t) * (size_t)N);
     kp_t* tmp = (kp_t*)malloc(sizeof(kp_t) * (size_t)N);
+    int64_t* sa = NULL;        /* real range [sa, sa + sr) of each segment of the current depth */
+    int64_t* sr = NULL;
     int rc = ORA_OK;
     if (!kq || !kk || !kb || !ord || !tmp) { rc = ORA_ENOMEM; goto done; }
     ora_hash(N, d, Q, c->sort_bits, Wsort, kq);
@@ -174,26 +201,47 @@ int ora_select(const ora_cfg* c, const float* Q, const float* K, const float* Ws
         for (int i = 0; i < N; ++i) kb[i] = kk[i];
         sort_positions(N, kb, perm_k, tmp);
     } else {
-        int lv = ora_num_levels(c);
+        const int lv = ora_num_levels(c);
         if (lv < 0) { rc = ORA_EINVAL; goto done; }
-        const int half_total = N / 2;
+        float* zero = (float*)calloc((size_t)d, sizeof(float));
+        uint8_t zk = 0;
+        if (!zero) { rc = ORA_ENOMEM; goto done; }
+        ora_hash(1, d, zero, c->sort_bits, Wsort, &zk);
+        free(zero);
+        sa = (int64_t*)malloc(sizeof(int64_t) << (lv > 0 ? lv : 1));
+        sr = (int64_t*)malloc(sizeof(int64_t) << (lv > 0 ? lv : 1));
+        if (!sa || !sr) { rc = ORA_ENOMEM; goto done; }
+        sa[0] = 0;
+        sr[0] = N;
+        int64_t len = N, out = 0;
         for (int l = 0; l < lv; ++l) {
-            const int seg = N >> l, h = seg >> 1;
-            for (int s = 0; s < (1 << l); ++s) {
-                const int a = s * seg;
-                int32_t* oq = perm_q + (size_t)l * half_total + (size_t)s * h;
-                int32_t* ok = perm_k + (size_t)l * half_total + (size_t)s * h;
-                for (int p = 0; p < h; ++p) kb[p] = kq[a + h + p];
-                sort_positions(h, kb, ord, tmp);
-                for (int p = 0; p < h; ++p) oq[p] = a + h + ord[p];
-                for (int p = 0; p < h; ++p) kb[p] = kk[a + p];
-                sort_positions(h, kb, ord, tmp);
-                for (int p = 0; p < h; ++p) ok[p] = a + ord[p];
+            const int64_t m = (len + 1) / 2;      /* halves after the zero-token padding of an odd list */
+            for (int64_t s = 0; s < ((int64_t)1 << l); ++s) {
+                const int64_t a = sa[s], r = sr[s];
+                const int64_t rf = r > m ? r - m : 0;  /* real tokens of the future half */
+                int32_t* oq = perm_q + out + s * m;
+                int32_t* ok = perm_k + out + s * m;
+                for (int64_t p = 0; p < m; ++p) kb[p] = p < rf ? kq[a + m + p] : zk;
+                sort_positions((int)m, kb, ord, tmp);
+                for (int64_t p = 0; p < m; ++p) oq[p] = ord[p] < rf ? (int32_t)(a + m + ord[p]) : -1;
+                for (int64_t p = 0; p < m; ++p) kb[p] = kk[a + p];
+                sort_positions((int)m, kb, ord, tmp);
+                for (int64_t p = 0; p < m; ++p) ok[p] = (int32_t)(a + ord[p]);
             }
+            /* the next depth: past child (a, m), future child (a + m, rf), in segment order */
+            for (int64_t s = ((int64_t)1 << l) - 1; s >= 0; --s) {
+                const int64_t a = sa[s], r = sr[s];
+                sa[2 * s] = a;
+                sr[2 * s] = m;
+                sa[2 * s + 1] = a + m;
+                sr[2 * s + 1] = r > m ? r - m : 0;
+            }
+            out += m << l;
+            len = m;
         }
     }
 done:
-    free(kq); free(kk); free(kb); free(ord); free(tmp);
+    free(kq); free(kk); free(kb); free(ord); free(tmp); free(sa); free(sr);
     return rc;
 }
 

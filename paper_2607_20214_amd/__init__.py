@@ -100,6 +100,8 @@ def load():
         lib = C.CDLL(LIB_PATH)
         P, S = C.c_void_p, C.c_size_t
         lib.elsaa_num_levels.argtypes = [P]
+        lib.elsaa_perm_length.argtypes = [P]
+        lib.elsaa_perm_length.restype = C.c_int64
         lib.elsaa_saved_bytes.argtypes = [P, C.POINTER(C.c_size_t)]
         lib.elsaa_workspace_bytes.argtypes = [P, C.c_int, C.POINTER(C.c_size_t)]
         lib.elsaa_get_saved_layout.argtypes = [P, P]
@@ -179,9 +181,23 @@ def saved_layout(cfg: Config) -> dict:
     return {f: getattr(L, f) for f, _ in _SavedLayout._fields_}
 
 
+def perm_length(cfg: Config) -> int:
+    """Entries of perm_q / perm_k per (b, h) (see elsaa_perm_length)."""
+    c = cfg.c()
+    n = load().elsaa_perm_length(C.byref(c))
+    if n < 0:
+        _check(int(n))
+    return n
+
+
 def _perm_shape(cfg: Config):
+    """[B, H, Lv, N/2] for causal lists without padding, [B, H, P] with it,
+    [B, H, N] non-causal."""
     if cfg.causal:
-        return (cfg.B, cfg.H, num_levels(cfg), cfg.N // 2)
+        lv, p = num_levels(cfg), perm_length(cfg)
+        if lv * (cfg.N // 2) == p and cfg.N % 2 == 0:
+            return (cfg.B, cfg.H, lv, cfg.N // 2)
+        return (cfg.B, cfg.H, p)
     return (cfg.B, cfg.H, cfg.N)
 
 

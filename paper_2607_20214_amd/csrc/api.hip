@@ -52,19 +52,6 @@ namespace {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Levels of the causal recursion (Alg. 5): smallest Lv with N / 2^Lv <= n0;
-// -1 when a segment longer than n0 would be odd.
-int levels_of(int64_t N, int64_t n0)
-{
-    int lv = 0;
-    while (N > n0) {
-        if (N & 1) return -1;
-        N >>= 1;
-        ++lv;
-    }
-    return lv;
-}
-
 int validate(const elsaa_config* c, Shape* s)
 {
     if (!c) return fail(ELSAA_ERR_INVALID_ARG, "cfg is NULL");
@@ -97,14 +84,16 @@ int validate(const elsaa_config* c, Shape* s)
         return fail(ELSAA_ERR_UNSUPPORTED, "N * d_h * element bytes must be < 2^32 (one head's rows)");
     const int n0 = c->n0 > 0 ? c->n0 : 2 * c->k;
     int lv = 0, n_leaf = c->N;
+    s->lt = LevelTiles{};
     if (c->causal) {
-        lv = levels_of(c->N, n0);
-        if (lv < 0)
+        // the recursion of Alg. 5 with its zero-token padding of odd lists
+        if (!level_tiles(c->N, n0, s->lt))
             return fail(ELSAA_ERR_UNSUPPORTED,
-                        "causal N = %d with n0 = %d needs zero-token padding of an odd segment (not on the GPU path)",
-                        c->N, n0);
-        n_leaf = c->N >> lv;
-        if (lv > kMaxLevels) return fail(ELSAA_ERR_UNSUPPORTED, "more than %d causal levels", kMaxLevels);
+                        "causal N = %d with n0 = %d: more than %d levels, or a past half that would hold "
+                        "a zero token",
+                        c->N, n0, kMaxLevels);
+        lv = s->lt.Lv;
+        n_leaf = s->lt.len[lv];
     }
     s->B = c->B; s->H = c->H; s->N = c->N; s->D = c->d_h;
     s->k = c->k;
@@ -164,7 +153,7 @@ FwdWorkspace fwd_workspace(const Shape& s)
     size_t off = 0;
     W.keyq = off; off = align256(off + bh * s.N);
     W.keyk = off; off = align256(off + bh * s.N);
-    const size_t npart = s.causal ? bh * s.Lv * (size_t)(s.N / 2) : 0;
+    const size_t npart = s.causal ? bh * (size_t)s.P() : 0;   // one entry per level list entry
     W.part_o = off; off = align256(off + npart * s.D * (s.bf16 ? 2 : 4));   // storage dtype
     W.part_lse = off; off = align256(off + npart * 4);
     W.total = off;
@@ -180,7 +169,7 @@ BwdWorkspace bwd_workspace(const Shape& s)
     BwdWorkspace W;
     const size_t bh = (size_t)s.B * s.H;
     const size_t bhn = bh * s.N;
-    const size_t npart = s.causal ? bh * s.Lv * (size_t)(s.N / 2) : 0;
+    const size_t npart = s.causal ? bh * (size_t)s.P() : 0;
     size_t off = 0;
     W.rs = off; off = align256(off + 5 * bhn * 4);
     W.states_b = off; off = align256(off + race_state_floats(s) * 4);
@@ -319,6 +308,14 @@ int elsaa_num_levels(const elsaa_config* cfg)
     int rc = validate(cfg, &s);
     if (rc) return rc;
     return s.Lv;
+}
+
+int64_t elsaa_perm_length(const elsaa_config* cfg)
+{
+    Shape s;
+    int rc = validate(cfg, &s);
+    if (rc) return rc;
+    return s.P();
 }
 
 int elsaa_saved_bytes(const elsaa_config* cfg, size_t* bytes)

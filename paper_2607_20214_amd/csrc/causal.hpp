@@ -1,12 +1,28 @@
-// causal.hpp -- workgroup numbering over the causal recursion (Alg. 5
-// unrolled): level l has 2^l segments whose future halves hold
-// half_l = N >> (l + 1) sorted queries (and whose past halves hold as many
-// sorted keys); the leaves are the N / n_leaf runs of n_leaf tokens.
-// Segment and leaf lengths need not be multiples of the 64-row tile: each
-// segment (leaf) gets ceil(length / 64) tiles, the last one ragged, so a
-// tile never straddles two segments (leaves).
+// causal.hpp -- geometry of the causal recursion (Alg. 5 unrolled) and the
+// workgroup numbering over it.
+//
+// A segment of the recursion is a list of L_l entries at depth l: a range
+// of real tokens [a, a + r) followed by L_l - r zero tokens.  A segment
+// longer than n0 is split (Alg. 5): an odd list is padded with one zero
+// token, then its first m = ceil(L_l / 2) entries form the past half and the
+// other m the future half, so L_{l+1} = m for every segment of the next
+// depth, and
+//   past child   = real [a, a + m), no zero tokens;
+//   future child = real [a + m, a + r), the rest zero tokens.
+// Zero tokens therefore only ever trail a future half, and the depth Lv is
+// the same for every segment (the smallest with L_Lv <= n0).  Level l's
+// SortLSH calls are the 2^l (future half, past half) pairs of depth-l
+// segments; its sorted lists take m_l = L_{l+1} entries each, stored segment
+// after segment, level after level (per (b,h): off[l] .. off[l] + 2^l m_l);
+// a zero token's entry in a query list is -1.  Without any padding
+// (N = n0' 2^Lv) this is L_l = N >> l and off[l] = l N / 2.
+//
+// Tiles: level l has 2^l segments x ceil(m_l / 64) tiles, each leaf
+// ceil(L_Lv / 64) tiles; a tile never straddles two segments (leaves), and
+// the last tile of each is ragged (masked).
 #pragma once
 #include <hip/hip_runtime.h>
+#include <stdint.h>
 
 namespace elsaa {
 
@@ -14,48 +30,111 @@ constexpr int kMaxLevels = 26;
 constexpr int kRowTile = 64;
 
 struct LevelTiles {
+    int Lv;                      // levels (0 non-causal or a single leaf)
+    int len[kMaxLevels + 1];     // list length L_l of a depth-l segment (len[0] = N)
+    int64_t off[kMaxLevels + 1]; // first entry of level l's lists within one (b,h); off[Lv] = all levels
     int first[kMaxLevels + 1];   // first tile of level l; first[Lv] = tiles of all levels
     int per_leaf;                // tiles per leaf
-    int leaves;                  // N / n_leaf
+    int leaves;                  // 2^Lv
+    int padded;                  // some segment carries zero tokens
     int leaf_tiles() const { return per_leaf * leaves; }
 };
 
-inline LevelTiles level_tiles(int N, int Lv, int n_leaf)
+// Geometry of the recursion for N tokens and base length n0; returns false
+// when some past half would have to hold a zero token (its real tokens fewer
+// than half the list), which the kernels do not implement, or when the depth
+// exceeds kMaxLevels.
+inline bool level_tiles(int N, int n0, LevelTiles& t)
 {
-    LevelTiles t = {};
+    t = LevelTiles{};
+    int L = N, lv = 0, pads = 0;                 // pads: the most zero tokens of any depth-lv segment
+    t.len[0] = N;
+    int64_t off = 0;
     int acc = 0;
-    for (int l = 0; l < Lv; ++l) {
-        t.first[l] = acc;
-        const int half = N >> (l + 1);
-        acc += (1 << l) * ((half + kRowTile - 1) / kRowTile);
+    while (L > n0) {
+        if (lv >= kMaxLevels) return false;
+        const int m = (L + 1) / 2;
+        if (pads > L - m) return false;          // the past half would reach a zero token
+        t.off[lv] = off;
+        t.first[lv] = acc;
+        off += (int64_t)m << lv;
+        acc += (1 << lv) * ((m + kRowTile - 1) / kRowTile);
+        pads += L & 1;                           // the all-future path collects every pad
+        L = m;
+        ++lv;
+        t.len[lv] = L;
+        if (pads) t.padded = 1;
     }
-    t.first[Lv] = acc;
-    t.per_leaf = (n_leaf + kRowTile - 1) / kRowTile;
-    t.leaves = N / n_leaf;
-    return t;
+    t.Lv = lv;
+    t.off[lv] = off;
+    t.first[lv] = acc;
+    t.per_leaf = (L + kRowTile - 1) / kRowTile;
+    t.leaves = 1 << lv;
+    return true;
 }
 
-// tile -> (level, half length, segment, first sorted position of the tile)
-__device__ __forceinline__ void level_tile(const LevelTiles& lt, int Lv, int N, int tile, int& level,
-                                           int& half, int& seg, int& p0)
+// Real token range [a, a + r) of segment s at depth l.
+__device__ __forceinline__ void seg_range(const LevelTiles& lt, int l, int s, int& a, int& r)
+{
+    a = 0;
+    r = lt.len[0];
+    for (int j = 0; j < l; ++j) {
+        const int m = lt.len[j + 1];
+        if ((s >> (l - 1 - j)) & 1) {
+            a += m;
+            r = r > m ? r - m : 0;
+        } else {
+            r = m;
+        }
+    }
+}
+
+// Entry of token t in the level-l lists of one (b,h): the entry of the same
+// rank within its segment's future half (future = true) or past half.
+__device__ __forceinline__ int64_t level_entry(const LevelTiles& lt, int l, int t, bool future)
+{
+    int a = 0, s = 0;
+    for (int j = 0; j < l; ++j) {
+        const int m = lt.len[j + 1];
+        const int f = t >= a + m;
+        s = 2 * s + f;
+        if (f) a += m;
+    }
+    const int m = lt.len[l + 1];
+    return lt.off[l] + (int64_t)s * m + (t - a - (future ? m : 0));
+}
+
+// Levels whose partials leaf s adds: bit l set when the leaf lies in the
+// future half (future = true) or in the past half of its level-l segment.
+__device__ __forceinline__ unsigned leaf_levels(const LevelTiles& lt, int leaf, bool future)
+{
+    unsigned mask = 0;
+    for (int l = 0; l < lt.Lv; ++l)
+        if ((((leaf >> (lt.Lv - 1 - l)) & 1) != 0) == future) mask |= 1u << l;
+    return mask;
+}
+
+// tile -> (level, half length m_l, segment, first list position of the tile)
+__device__ __forceinline__ void level_tile(const LevelTiles& lt, int tile, int& level, int& half, int& seg, int& p0)
 {
     level = 0;
-    while (level + 1 < Lv && tile >= lt.first[level + 1]) ++level;
+    while (level + 1 < lt.Lv && tile >= lt.first[level + 1]) ++level;
     const int t = tile - lt.first[level];
-    half = N >> (level + 1);
+    half = lt.len[level + 1];
     const int tps = (half + kRowTile - 1) / kRowTile;
     seg = t / tps;
     p0 = (t - seg * tps) * kRowTile;
 }
 
-// tile -> (first token of its leaf, first token of the tile, end of the leaf)
-__device__ __forceinline__ void leaf_tile(const LevelTiles& lt, int n_leaf, int tile, int& lbeg, int& t0,
-                                          int& lend)
+// tile -> (leaf, first token of its leaf, first token of the tile, end of
+// the leaf's real tokens); tiles past the real tokens have t0 >= lend.
+__device__ __forceinline__ void leaf_tile(const LevelTiles& lt, int tile, int& leaf, int& lbeg, int& t0, int& lend)
 {
-    const int leaf = tile / lt.per_leaf;
-    lbeg = leaf * n_leaf;
+    leaf = tile / lt.per_leaf;
+    int r;
+    seg_range(lt, lt.Lv, leaf, lbeg, r);
     t0 = lbeg + (tile - leaf * lt.per_leaf) * kRowTile;
-    lend = lbeg + n_leaf;
+    lend = lbeg + r;
 }
 
 // This workgroup's (tile, h, b) in a grid of (tiles, H, B), renumbered so

@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "causal.hpp"
+
 namespace elsaa {
 
 // Validated shape information of one operator call.
@@ -14,14 +16,15 @@ struct Shape {
     int r, L, Lp;         // RACE features, tables, tables padded to a multiple of 4
     int sort_bits;
     int Lv;               // causal recursion levels (0 non-causal)
-    int n_leaf;           // causal leaf length N / 2^Lv
+    int n_leaf;           // causal leaf list length (real tokens plus zero tokens)
+    LevelTiles lt;        // causal recursion geometry (causal.hpp)
     int causal;
     int bf16;             // storage dtype: 1 bf16, 0 float32
     float beta, lambda, eps, tau;
     int seg_len, nseg;    // RACE sequence segments (multiple of the 64-token chunk)
     int neighbors;        // r neighbouring sorted blocks on each side
     int m_one;            // m_sparse fixed to 1
-    int64_t P() const { return causal ? (int64_t)Lv * (N / 2) : (int64_t)N; }  // perm length per (b,h)
+    int64_t P() const { return causal ? lt.off[Lv] : (int64_t)N; }  // perm length per (b,h)
 };
 
 // Record an error message for elsaa_last_error() and return `code`.

@@ -12,6 +12,7 @@
 // at most 2^sort_bits buckets, one workgroup per sorted list.
 #include "common.hpp"
 #include "internal.hpp"
+#include "causal.hpp"
 
 namespace elsaa {
 
@@ -209,9 +210,12 @@ hipError_t launch_project(const Shape& s, const void* Q, const void* K, const fl
 // Stable counting sort, one workgroup per list.
 // Lists of one (b,h):
 //   non-causal: task 0 = all queries, task 1 = all keys;
-//   causal: level l has 2^l segments of length n = N >> l; task (l, s, q/k)
-//           sorts the future half [a + n/2, a + n) of the query keys or the
-//           past half [a, a + n/2) of the key keys, a = s * n.
+//   causal: level l has 2^l segments (causal.hpp); task (l, s, q/k) sorts
+//           the future half of segment s by the query keys or its past half
+//           by the key keys, m_l entries each.  A future half's trailing
+//           zero tokens (Alg. 5's padding of odd lists) take the key of the
+//           zero vector, 0 (no sign bit is set), and sort after every real
+//           token of that key; their entries are -1.
 // --------------------------------------------------------------------------
 
 constexpr int kSortThreads = 256;
@@ -229,7 +233,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint8_t* __res
                                                             const uint8_t* __restrict__ keyk,
                                                             int32_t* __restrict__ perm_q,
                                                             int32_t* __restrict__ perm_k, int H,
-                                                            int N, int causal, int Lv, int bits)
+                                                            int N, int causal, LevelTiles lt, int bits)
 {
     __shared__ int hist[kSortWaves][256];   // per quarter; then its running output positions
     __shared__ uint8_t kc[kKeyCache];
@@ -238,25 +242,26 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint8_t* __res
     const int nb = 1 << bits;
     const size_t bh = (size_t)b * H + h;
 
-    int start, len, is_k;
+    int start, len, nreal, is_k;             // list entries [0, len): tokens start + i for i < nreal
     size_t out_off;
     if (!causal) {
         is_k = task;
         start = 0;
-        len = N;
+        len = nreal = N;
         out_off = bh * N;
     } else {
         // level l owns tasks [2^(l+1) - 2, 2^(l+2) - 2)
-        int l = 31 - __clz(task + 2) - 1;
-        int t2 = task - ((1 << (l + 1)) - 2);
-        int seg = t2 >> 1;
+        const int l = 31 - __clz(task + 2) - 1;
+        const int t2 = task - ((1 << (l + 1)) - 2);
+        const int seg = t2 >> 1;
         is_k = t2 & 1;
-        int n = N >> l, half = n >> 1;
-        int a = seg * n;
+        int a, r;
+        seg_range(lt, l, seg, a, r);
+        const int half = lt.len[l + 1];
         start = is_k ? a : a + half;
         len = half;
-        // causal lists: [b,h][Lv][N/2]; level l, segment seg starts at seg * half
-        out_off = (bh * Lv + l) * (size_t)(N / 2) + (size_t)seg * half;
+        nreal = is_k ? half : (r > half ? r - half : 0);
+        out_off = bh * (size_t)lt.off[lt.Lv] + (size_t)lt.off[l] + (size_t)seg * half;
     }
     const uint8_t* key = (is_k ? keyk : keyq) + bh * N + start;
     int32_t* out = (is_k ? perm_k : perm_q) + out_off;
@@ -274,7 +279,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint8_t* __res
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const int i = i0 + j * kWave + lane;
-            v[j] = i < qend ? key[i] : 0;
+            v[j] = i < qend && i < nreal ? key[i] : 0;
         }
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
@@ -317,20 +322,20 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint8_t* __res
     __syncthreads();
     // rank the quarter, 64 keys per step; hist[wave][c] is the next output
     // position of bucket c in this quarter
-    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
     for (int i0 = qbeg; i0 < qend; i0 += kWave) {
         const int i = i0 + lane;
         const bool valid = i < qend;
-        const int kk = valid ? (i < kKeyCache ? kc[i] : key[i]) : 0;
+        const int kk = valid && i < nreal ? (i < kKeyCache ? kc[i] : key[i]) : 0;
         uint64_t same = __ballot(valid);
         for (int bit = 0; bit < bits; ++bit) {
             const uint64_t ones = __ballot(valid && ((kk >> bit) & 1));
             same &= ((kk >> bit) & 1) ? ones : ~ones;
         }
-        const int rank = __popcll(same & lt);
+        const int rank = __popcll(same & below);
         const int pos = valid ? hist[wave][kk] + rank : 0;
         __builtin_amdgcn_wave_barrier();                     // every lane has read before the leaders advance
-        if (valid) out[pos] = start + i;
+        if (valid) out[pos] = i < nreal ? start + i : -1;
         if (valid && rank == 0) hist[wave][kk] += __popcll(same);
     }
 }
@@ -342,7 +347,7 @@ hipError_t launch_sort(const Shape& s, const uint8_t* keyq, const uint8_t* keyk,
     if (tasks <= 0) return hipSuccess;
     dim3 grid(tasks, s.H, s.B);
     ELSAA_LAUNCH("sort", sort_kernel, grid, dim3(kSortThreads), 0, st, keyq, keyk, perm_q, perm_k,
-                       s.H, s.N, s.causal, s.Lv, s.sort_bits);
+                       s.H, s.N, s.causal, s.lt, s.sort_bits);
     return hipGetLastError();
 }
 

@@ -52,33 +52,19 @@ struct BArgs {
     void* dQ;
     void* dK;
     void* dV;
-    int H, N, k, Lv, n_leaf, wk;
-    LevelTiles lt;            // causal tile numbering
+    int H, N, k, Lv, wk;
+    LevelTiles lt;            // causal recursion geometry and tile numbering
     int nbr;                  // neighbouring sorted blocks on each side
     int nbx, nblk;            // whole-block kernel: blocks per head, blocks in all
     size_t BHN;
     float tau, tau2;
 };
 
-// Compact slot of token t in the level-l list of future (or past) halves.
-__device__ __forceinline__ size_t level_slot(size_t bh, int Lv, int l, int N, int t, int future)
+// Partial row of token t at level l: its entry among the level's future (or
+// past) halves, after the (b,h)s before it.
+__device__ __forceinline__ size_t level_slot(const LevelTiles& lt, size_t bh, int l, int t, bool future)
 {
-    const int hl = N >> (l + 1);
-    const int s2 = t / (2 * hl);
-    return (bh * Lv + l) * (size_t)(N / 2) + (size_t)s2 * hl + (t - s2 * 2 * hl - (future ? hl : 0));
-}
-
-// Causal levels whose partials the leaf starting at token lbeg adds: bit l
-// is set when the leaf lies in the future half (future = true) or in the
-// past half of its level-l segment.
-__device__ __forceinline__ unsigned leaf_levels(int lbeg, int N, int Lv, bool future)
-{
-    unsigned mask = 0;
-    for (int l = 0; l < Lv; ++l) {
-        const int hl = N >> (l + 1);
-        if ((((lbeg / hl) & 1) != 0) == future) mask |= 1u << l;
-    }
-    return mask;
+    return bh * (size_t)lt.off[lt.Lv] + (size_t)level_entry(lt, l, t, future);
 }
 
 // The low-rank part of dQ (dK) of one token for the 16-row slice dt of d:
@@ -212,21 +198,21 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
         klist = a.perm_k + bh * N;
     } else if (MODE == kLevels) {
         int seg, p0;
-        level_tile(a.lt, a.Lv, N, tile, level, half, seg, p0);
+        level_tile(a.lt, tile, level, half, seg, p0);
         bq = min(a.k, half);
         qpos = p0 + 16 * w + qq;
-        const size_t lbase = (bh * a.Lv + level) * (size_t)(N / 2) + (size_t)seg * half;
-        qtok = qpos < half ? a.perm_q[lbase + qpos] : -1;
+        const size_t lbase = bh * (size_t)a.lt.off[a.Lv] + (size_t)a.lt.off[level] + (size_t)seg * half;
+        qtok = qpos < half ? a.perm_q[lbase + qpos] : -1;      // -1 also for a zero token
         kbeg = max(0, (p0 / bq - a.nbr) * bq);
         kend = min(half, ((min(p0 + kT, half) - 1) / bq + 1 + a.nbr) * bq);
         klist = a.perm_k + lbase;
     } else {
-        int q0, lend;
-        leaf_tile(a.lt, a.n_leaf, tile, kbeg, q0, lend);
+        int q0, lend, leaf;
+        leaf_tile(a.lt, tile, leaf, kbeg, q0, lend);
         qtok = q0 + 16 * w + qq;
         qpos = qtok;
         if (qtok >= lend) qtok = -1;
-        kend = min(q0 + kT, lend);
+        kend = q0 < lend ? min(q0 + kT, lend) : kbeg;    // a tile past the leaf's real tokens has no work
     }
     const int blk_lo = (MODE == kLeaf) ? 0 : max(0, (qpos / bq - a.nbr) * bq);
     const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), (qpos / bq + 1 + a.nbr) * bq);
@@ -320,7 +306,7 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
     }
     if (MODE == kLevels) {
         if (qtok < 0) return;
-        S* out = (S*)a.part_dq + level_slot(bh, a.Lv, level, N, qtok, 1) * D;
+        S* out = (S*)a.part_dq + level_slot(a.lt, bh, level, qtok, true) * D;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) store4<T>(out + 16 * dt + 4 * g, acc[dt] * a.tau);
         return;
@@ -338,7 +324,7 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) tot[dt] = acc[dt] * a.tau + lowrank_lds<T, D>(duf, swt, a.wk, g, qq, dt);
     if (qtok < 0) return;
-    unsigned lmask = MODE == kLeaf ? leaf_levels((tile / a.lt.per_leaf) * a.n_leaf, N, a.Lv, true) : 0u;
+    unsigned lmask = MODE == kLeaf ? leaf_levels(a.lt, tile / a.lt.per_leaf, true) : 0u;
     while (lmask) {
         const S* src[2];
         bool use[2];
@@ -349,7 +335,7 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
             if (use[j]) {
                 const int l = __builtin_ctz(lmask);
                 lmask &= lmask - 1;
-                src[j] = (const S*)a.part_dq + level_slot(bh, a.Lv, l, N, qtok, 1) * D;
+                src[j] = (const S*)a.part_dq + level_slot(a.lt, bh, l, qtok, true) * D;
             }
         }
         f32x4 x[2][DT];
@@ -425,10 +411,10 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
         j0 = p0;
     } else if (MODE == kLevels) {
         int seg, p0;
-        level_tile(a.lt, a.Lv, N, tile, level, half, seg, p0);
+        level_tile(a.lt, tile, level, half, seg, p0);
         bq = min(a.k, half);
         kpos = p0 + 16 * w + col;
-        const size_t lbase = (bh * a.Lv + level) * (size_t)(N / 2) + (size_t)seg * half;
+        const size_t lbase = bh * (size_t)a.lt.off[a.Lv] + (size_t)a.lt.off[level] + (size_t)seg * half;
         klist = a.perm_k + lbase;
         ktok = kpos < half ? klist[kpos] : -1;
         qbeg = max(0, (p0 / bq - a.nbr) * bq);
@@ -436,13 +422,13 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
         qlist = a.perm_q + lbase;
         j0 = p0;
     } else {
-        int lbeg, lend;
-        leaf_tile(a.lt, a.n_leaf, tile, lbeg, j0, lend);
+        int lbeg, lend, leaf;
+        leaf_tile(a.lt, tile, leaf, lbeg, j0, lend);
         ktok = j0 + 16 * w + col;
         kpos = ktok;
         if (ktok >= lend) ktok = -1;
         qbeg = j0;
-        qend = lend;
+        qend = max(lend, j0);                            // a tile past the leaf's real tokens has no work
     }
     const int blk_lo = (MODE == kLeaf) ? 0 : max(0, (kpos / bq - a.nbr) * bq);
     const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), (kpos / bq + 1 + a.nbr) * bq);
@@ -567,7 +553,7 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
 
     if (MODE == kLevels) {
         if (ktok < 0) return;
-        const size_t slot = level_slot(bh, a.Lv, level, N, ktok, 0);
+        const size_t slot = level_slot(a.lt, bh, level, ktok, false);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
             store4<T>((S*)a.part_dk + slot * D + 16 * dt + 4 * g, akT[dt] * a.tau);
@@ -595,7 +581,7 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
         tv[dt] = avT[dt] + tv[dt];
     }
     if (ktok < 0) return;
-    unsigned lmask = MODE == kLeaf ? leaf_levels((tile / a.lt.per_leaf) * a.n_leaf, N, a.Lv, false) : 0u;
+    unsigned lmask = MODE == kLeaf ? leaf_levels(a.lt, tile / a.lt.per_leaf, false) : 0u;
     while (lmask) {
         const S* sk_[2];
         const S* sv_[2];
@@ -608,7 +594,7 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
             if (use[j]) {
                 const int l = __builtin_ctz(lmask);
                 lmask &= lmask - 1;
-                const size_t slot = level_slot(bh, a.Lv, l, N, ktok, 0);
+                const size_t slot = level_slot(a.lt, bh, l, ktok, false);
                 sk_[j] = (const S*)a.part_dk + slot * D;
                 sv_[j] = (const S*)a.part_dv + slot * D;
             }
@@ -762,10 +748,11 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
         const int x = id % a.nbx;
         k.bh = (size_t)(id / a.nbx);                     // b * H + h
         if (MODE == kLevels) {
+            // (whole-block levels are never padded: N / 2 entries per level)
             const int per_level = (N / 2) / BQ;
             k.level = x / per_level;
             const int t = x - k.level * per_level;
-            const size_t base = (k.bh * a.Lv + k.level) * (size_t)(N / 2) + (size_t)t * BQ;
+            const size_t base = k.bh * (size_t)a.lt.off[a.Lv] + (size_t)a.lt.off[k.level] + (size_t)t * BQ;
             k.ql = a.perm_q + base;
             k.kl = a.perm_k + base;
             k.nv = BQ;
@@ -847,7 +834,7 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) {
                 const int d0 = 16 * dt + 4 * g;
-                const size_t slot = level_slot(bh, a.Lv, level, N, ktok, 0);
+                const size_t slot = level_slot(a.lt, bh, level, ktok, false);
                 store4<T>((S*)a.part_dk + slot * D + d0, akT[dt] * a.tau);
                 store4<T>((S*)a.part_dv + slot * D + d0, avT[dt]);
             }
@@ -1006,7 +993,7 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
                 const int d0 = 16 * dt + 4 * g;
                 if (MODE == kLevels) {
                     if (!kFull && qtok < 0) continue;
-                    S* out = (S*)a.part_dq + level_slot(bh, a.Lv, level, N, qtok, 1) * D + d0;
+                    S* out = (S*)a.part_dq + level_slot(a.lt, bh, level, qtok, true) * D + d0;
                     store4<T>(out, dq[u] * a.tau);
                 } else {
                     // the low-rank part is a product across the wave's lanes:
@@ -1066,7 +1053,7 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
     const int bq = s.k;
     const bool fits128 = T::bytes == 2 && (s.causal || D == 64);
     const bool whole = (bq == 64 || (bq == 128 && fits128)) && s.neighbors == 0 &&
-                       (s.causal ? (s.n_leaf % bq == 0) : true);
+                       (s.causal ? (!s.lt.padded && s.n_leaf % bq == 0) : true);
     if (!s.causal) {
         if (whole) {
             if (!(parts & kSparseFinalQ)) return hipSuccess;
@@ -1133,8 +1120,8 @@ hipError_t launch_sparse_bwd(const Shape& s, const void* Q, const void* K, const
     a.wk = race_wk(s);
     a.part_dq = part_dq; a.part_dk = part_dk; a.part_dv = part_dv;
     a.dQ = dQ; a.dK = dK; a.dV = dV;
-    a.H = s.H; a.N = s.N; a.k = s.k; a.Lv = s.Lv; a.n_leaf = s.n_leaf;
-    if (s.causal) a.lt = level_tiles(s.N, s.Lv, s.n_leaf);
+    a.H = s.H; a.N = s.N; a.k = s.k; a.Lv = s.Lv;
+    a.lt = s.lt;
     a.nbr = s.neighbors;
     a.BHN = (size_t)s.B * s.H * s.N;
     a.tau = s.tau; a.tau2 = s.tau * kLog2e;

@@ -16,8 +16,8 @@
 //   kLevels  causal Alg. 5, every level at once: SortLSH(Q_future, K_past)
 //            of each segment; writes a normalised partial (O, log d) per
 //            query, stored by natural query index.
-//   kLeaf    causal Alg. 5 leaf (exact causal attention inside segments of
-//            N / 2^Lv tokens), then merges the level partials of the same
+//   kLeaf    causal Alg. 5 leaf (exact causal attention among the real
+//            tokens of each leaf segment), then merges the level partials of the same
 //            queries by log-sum-exp (MergeLSE) and applies the fusion.
 //
 // Fusion (Eq. m_sparse with the log-sum-exp form of Alg. 6, Eq. fusion):
@@ -55,8 +55,8 @@ struct Args {
     float* lse;
     float* m;
     float* O_s;
-    int H, N, k, Lv, n_leaf;
-    LevelTiles lt;   // causal tile numbering
+    int H, N, k, Lv;
+    LevelTiles lt;   // causal recursion geometry and tile numbering
     int nbr;         // neighbouring sorted blocks on each side
     int m_one;       // m_sparse fixed to 1
     float tau2;      // tau * log2(e)
@@ -104,22 +104,22 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
         klist = a.perm_k + bh * N;
     } else if (MODE == kLevels) {
         int p0;
-        level_tile(a.lt, a.Lv, N, tile, level, half, seg, p0);
+        level_tile(a.lt, tile, level, half, seg, p0);
         bq = min(a.k, half);
         qpos = p0 + 16 * w + qq;
-        const size_t lbase = (bh * a.Lv + level) * (size_t)(N / 2) + (size_t)seg * half;
-        qtok = qpos < half ? a.perm_q[lbase + qpos] : -1;
+        const size_t lbase = bh * (size_t)a.lt.off[a.Lv] + (size_t)a.lt.off[level] + (size_t)seg * half;
+        qtok = qpos < half ? a.perm_q[lbase + qpos] : -1;      // -1 also for a zero token
         const int plast = min(p0 + kQT, half) - 1;
         kbeg = max(0, (p0 / bq - a.nbr) * bq);
         kend = min(half, (plast / bq + 1 + a.nbr) * bq);
         klist = a.perm_k + lbase;
     } else {
-        int q0, lend;
-        leaf_tile(a.lt, a.n_leaf, tile, kbeg, q0, lend);
+        int q0, lend, leaf;
+        leaf_tile(a.lt, tile, leaf, kbeg, q0, lend);
         qtok = q0 + 16 * w + qq;
         qpos = qtok;
         if (qtok >= lend) qtok = -1;
-        kend = min(q0 + kQT, lend);
+        kend = q0 < lend ? min(q0 + kQT, lend) : kbeg;   // a tile past the leaf's real tokens has no work
     }
     const int blk_lo = (MODE == kLeaf) ? 0 : max(0, (qpos / bq - a.nbr) * bq);
     const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), (qpos / bq + 1 + a.nbr) * bq);
@@ -228,10 +228,8 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
 
     if (MODE == kLevels) {
         if (qtok < 0) return;
-        // compact slot of query qtok among the future halves of this level
-        const int s2 = qtok / (2 * half);
-        const size_t slot = (bh * a.Lv + level) * (size_t)(N / 2) + (size_t)s2 * half +
-                            (qtok - s2 * 2 * half - half);
+        // entry of query qtok among the future halves of this level
+        const size_t slot = bh * (size_t)a.lt.off[a.Lv] + (size_t)level_entry(a.lt, level, qtok, true);
         const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
         S* po = (S*)a.part_o + slot * D;
 #pragma unroll
@@ -244,10 +242,7 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
         // merge the partial of every level whose future half holds this leaf,
         // in level order; the partials are fetched two levels at a time so
         // their loads are in flight together
-        const int lbeg = (tile / a.lt.per_leaf) * a.n_leaf;
-        unsigned lmask = 0;
-        for (int l = 0; l < a.Lv; ++l)
-            if (((lbeg / (N >> (l + 1))) & 1) != 0) lmask |= 1u << l;
+        unsigned lmask = leaf_levels(a.lt, tile / a.lt.per_leaf, true);
         while (lmask) {
             size_t slot[2];
             bool use[2];
@@ -258,9 +253,7 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
                 if (use[j]) {
                     const int l = __builtin_ctz(lmask);
                     lmask &= lmask - 1;
-                    const int hl = N >> (l + 1);
-                    const int s2 = qtok / (2 * hl);
-                    slot[j] = (bh * a.Lv + l) * (size_t)(N / 2) + (size_t)s2 * hl + (qtok - s2 * 2 * hl - hl);
+                    slot[j] = bh * (size_t)a.lt.off[a.Lv] + (size_t)level_entry(a.lt, l, qtok, true);
                 }
             }
             float pl[2];
@@ -351,8 +344,8 @@ hipError_t launch_sparse_fwd(const Shape& s, const void* Q, const void* K, const
     a.nbr = s.neighbors; a.m_one = s.m_one;
     a.part_o = part_o; a.part_lse = part_lse;
     a.O = O; a.lse = lse; a.m = m; a.O_s = O_s;
-    a.H = s.H; a.N = s.N; a.k = s.k; a.Lv = s.Lv; a.n_leaf = s.n_leaf;
-    if (s.causal) a.lt = level_tiles(s.N, s.Lv, s.n_leaf);
+    a.H = s.H; a.N = s.N; a.k = s.k; a.Lv = s.Lv;
+    a.lt = s.lt;
     a.tau2 = s.tau * kLog2e;
     a.lambda = s.lambda; a.eps = s.eps;
     if (s.bf16) return s.D == 64 ? launch_t<BF16, 64>(s, a, st, parts) : launch_t<BF16, 128>(s, a, st, parts);

@@ -36,7 +36,7 @@ def _cfg(**kw):
     (dict(N=0), -1), (dict(k=0), -1), (dict(r=40), -1), (dict(sort_bits=9), -1),
     (dict(eps=0.0), -1), (dict(lam=-1.0), -1), (dict(beta=0.0), -1), (dict(dtype="f16"), None),
     (dict(d_h=96), -2), (dict(race_bits=3, r=64), -2), (dict(r=512), -2),
-    (dict(N=300, k=32), -2), (dict(N=98, k=16), -2),
+    (dict(N=5, k=1, n0=1), -2),     # a past half would hold one of Alg. 5's zero tokens
 ])
 def test_host_validation_rejects(kw, status):
     if status is None:
@@ -59,6 +59,21 @@ def test_head_rows_must_fit_32_bit_offsets():
         E.num_levels(_cfg(dtype="f32", **big))
     assert ei.value.status == -2
     assert E.num_levels(_cfg(dtype="bf16", **big)) == 0
+
+
+def test_padded_recursion_levels_and_list_length():
+    """Alg. 5 pads odd lists with a zero token: 300 -> 150 -> 75 (+1) -> 38."""
+    cfg = _cfg(N=300, k=32)
+    assert E.num_levels(cfg) == 3
+    assert E.perm_length(cfg) == 150 + 2 * 75 + 4 * 38
+    big = _cfg(N=16386, k=128, H=16, d_h=128, r=128)
+    assert E.num_levels(big) == 7
+    L, total = 16386, 0
+    for l in range(7):
+        L = (L + 1) // 2
+        total += L << l
+    assert E.perm_length(big) == total
+    assert E.perm_length(_cfg(N=16384, k=128, d_h=128, r=128)) == 6 * 8192
 
 
 def test_sizes_and_layout():

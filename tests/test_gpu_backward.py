@@ -29,6 +29,10 @@ SMALL = [
     _w("c-bf16-leaf-only-256", 2, 1, 256, 64, 128, 48, True, "bf16"),
     _w("c-bf16-r256-1024", 1, 1, 1024, 128, 128, 256, True, "bf16", recipe="mixed", centres=8),
     _w("c-bf16-n0-3x-768", 1, 1, 768, 64, 128, 64, True, "bf16"),
+    # Alg. 5's zero-token padding of odd lists
+    _w("c-bf16-d64-padded-1001", 1, 2, 1001, 64, 64, 64, True, "bf16"),
+    _w("c-bf16-d128-padded-777-k32", 1, 1, 777, 128, 32, 64, True, "bf16", recipe="clustered"),
+    _w("c-f32-d64-padded-300-k32", 1, 1, 300, 64, 32, 32, True, "f32"),
 ]
 
 
@@ -106,6 +110,16 @@ def test_backward_block_32k_attention_sampled_rows():
     qm[-64:] = 1
     km[:64] = 1
     _check(w, heads={(0, 4), (0, 9)}, q_mask=qm, k_mask=km)
+
+
+@pytest.mark.timeout(300)
+def test_backward_padded_16386():
+    """N = 16386 with n0 = 256 (seven levels, zero tokens from the second
+    level on) and with n0 = 4096 (three levels, leaves of 2049 entries), every
+    row of two heads."""
+    for n0, k in ((None, 128), (4096, 256)):
+        w = _w(f"c-bf16-padded-16386-n0-{n0}", 1, 2, 16386, 128, k, 128, True, "bf16", seed=64, n0=n0)
+        _check(w)
 
 
 def test_backward_is_deterministic():

@@ -128,7 +128,84 @@ def test_num_levels():
     assert oracle.num_levels(HeadCfg(N=65536, d=8, k=256, r=16, causal=True)) == 7
     assert oracle.num_levels(HeadCfg(N=768, d=8, k=128, r=16, causal=True)) == 2
     assert oracle.num_levels(HeadCfg(N=200, d=8, k=128, r=16, causal=True)) == 0
-    assert oracle.num_levels(HeadCfg(N=300, d=8, k=32, r=16, causal=True)) == -1   # 300, 150, 75 > 64 odd
+    # 300, 150, 75 (padded to 76), 38 <= 64: Alg. 5's zero token
+    assert oracle.num_levels(HeadCfg(N=300, d=8, k=32, r=16, causal=True)) == 3
+    assert oracle.num_levels(HeadCfg(N=16386, d=8, k=128, r=16, causal=True)) == 7
+    # 5 -> 3 + 3 (one zero token) -> the future half 2 real + 1 zero, padded to
+    # 4: its past half would be 2 entries with 1 real token -> no layout
+    assert oracle.num_levels(HeadCfg(N=5, d=8, k=1, r=16, causal=True, n0=1)) == -1
+
+
+def _padded_lists_support(N, n0, k, pq, pk):
+    """Support mask implied by sorted lists in the padded layout: level by
+    level, segment by segment (lists of ceil(L / 2) entries, L_0 = N), query
+    block t of a list sees key block t; every leaf segment's real tokens attend
+    causally.  Segment geometry written out here from the recursion itself:
+    an odd list gets one zero token at its end, the past half is the first
+    half of the (padded) list and the future half the rest."""
+    M = np.zeros((N, N), dtype=np.int64)
+    segs = [(0, N)]                       # (first real token, real tokens) per segment
+    L, off = N, 0
+    while L > n0:
+        m = (L + 1) // 2
+        b = min(k, m)
+        nxt = []
+        for s, (a, r) in enumerate(segs):
+            q = pq[off + s * m: off + (s + 1) * m]
+            kl = pk[off + s * m: off + (s + 1) * m]
+            assert sorted(kl.tolist()) == list(range(a, a + m)), "past half = first m real tokens"
+            fut = sorted(t for t in q.tolist() if t >= 0)
+            assert fut == list(range(a + m, a + r)), "future half = the remaining real tokens"
+            assert (q < 0).sum() == m - (r - m), "zero tokens fill the future list"
+            for p, tq in enumerate(q.tolist()):
+                if tq >= 0:
+                    t = p // b
+                    for tk in kl[t * b:(t + 1) * b].tolist():
+                        M[tq, tk] += 1
+            nxt += [(a, m), (a + m, r - m)]
+        off += m * len(segs)
+        segs, L = nxt, m
+    for a, r in segs:
+        for i in range(a, a + r):
+            M[i, a:i + 1] += 1
+    return M
+
+
+@pytest.mark.parametrize("N,n0,k", [(37, 8, 4), (45, 7, 3), (50, 6, 5), (101, 16, 8), (300, 64, 32),
+                                    (129, 32, 16), (64, 8, 4)])
+def test_select_lists_reproduce_the_literal_recursion(N, n0, k):
+    """The sorted lists (with Alg. 5's zero tokens, -1 in perm_q) define the
+    same supports as the literal recursion, padding included."""
+    cfg, Q, K, V, Ws, Wr = _tiny(10, N, 8, k, 16, True, n0=n0)
+    pq, pk = oracle.select(cfg, Q, K, Ws)
+    pq, pk = pq.reshape(-1), pk.reshape(-1)
+    assert pq.size == oracle.perm_length(cfg)
+    kq, _ = bf.keys64(Q, Ws)
+    kk, _ = bf.keys64(K, Ws)
+    want = bf.causal_support_mask(N, n0, k, kq, kk, pad_key=_pad_key(Ws))
+    assert np.array_equal(_padded_lists_support(N, n0, k, pq, pk), want)
+
+
+def test_zero_tokens_sort_after_the_real_tokens_of_their_bucket():
+    N, n0, k = 45, 7, 3
+    cfg, Q, K, V, Ws, Wr = _tiny(11, N, 8, k, 16, True, n0=n0)
+    pq, _ = oracle.select(cfg, Q, K, Ws)
+    kq, _ = bf.keys64(Q, Ws)
+    zk = _pad_key(Ws)
+    L, off, nseg, zeros = N, 0, 1, 0
+    while L > n0:
+        m = (L + 1) // 2
+        for s in range(nseg):
+            q = pq[off + s * m: off + (s + 1) * m].tolist()
+            keys = [zk if t < 0 else kq[t] for t in q]
+            assert keys == sorted(keys), "lists ascend by bucket"
+            for p in range(1, m):
+                if q[p - 1] < 0 and q[p] >= 0:
+                    assert keys[p] > keys[p - 1], "a zero token follows the real tokens of its bucket"
+            zeros += sum(t < 0 for t in q)
+        off += m * nseg
+        L, nseg = m, 2 * nseg
+    assert zeros > 0
 
 
 # --------------------------------------------------------------------------
