@@ -55,6 +55,31 @@ __device__ __forceinline__ typename T::frag_t col8_t(const typename T::store_t (
     }
 }
 
+// Phi^T operand fragment from a row-major feature tile ph[token][feature]:
+// lane (i, g) receives feature f0 + i at tokens kb + 8 g + j (transposed LDS
+// reads, so no transposed copy of the tile is kept).
+template <class T, int RP>
+__device__ __forceinline__ typename T::frag_t phi_t8(const typename T::store_t (*ph)[RP + kPad], int kb, int f0)
+{
+    return col8_t<T, RP + kPad>(ph, kb, f0);
+}
+
+// Weighted sums over the chunk's tokens on the matrix cores: the B operand of
+// Phi^T x [w | 0 ...] (tokens kb + 8 g + j of column 0 hold w, w = 1 when
+// null; the other columns 0), so column 0 of the product tile is
+// sum_k phi_f(k) w_k for the tile's 16 features.  w keeps float32 accuracy
+// (hi + lo parts, two products) when given.
+template <class T>
+__device__ __forceinline__ f32x4 token_sums(typename T::frag_t phit, const float* w, int kb, f32x4 acc)
+{
+    const int lane = threadIdx.x & 63, g = lane >> 4, col = lane & 15;
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = col == 0 ? (w ? w[kb + 8 * g + j] : 1.f) : 0.f;
+    if (!w) return T::mma(phit, T::pack(v), acc);
+    return mma_split<T>(phit, v, acc);
+}
+
 // a_state[f] += scale * sum over the chunk's tokens k of xt[f][k] (* wk[k] when
 // wk is not null), xt a transposed feature tile [RP][kC + kPad]; all threads,
 // 256 / RP per feature (16-byte LDS reads, then a lane reduction).

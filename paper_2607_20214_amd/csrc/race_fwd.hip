@@ -31,9 +31,8 @@ template <class T, int D, int RP>
 struct StateSmem {
     using S = typename T::store_t;
     S vt[D][kC + kPad];
-    S pht[RP][kC + kPad];
+    S ph[kC][RP + kPad];          // features, rows (their transpose is read with transposed LDS reads)
     float aw[kC];
-    float a_state[RP];
 };
 
 template <class T, int D, int RP>
@@ -41,8 +40,7 @@ struct OutSmem {
     using S = typename T::store_t;
     S vt[D][kC + kPad];           // V chunk, transposed
     S phq[kC][RP + kPad];         // Phi_Q chunk
-    S phk[kC][RP + kPad];         // Phi_K chunk
-    S phkt[RP][kC + kPad];        // Phi_K chunk, transposed
+    S phk[kC][RP + kPad];         // Phi_K chunk (its transpose is read with transposed LDS reads)
     S mm[kC][kC + kPad];          // tril(Phi_Q Phi_K') / L
     float a_state[RP];
     float den_a[kC];
@@ -71,15 +69,21 @@ __global__ __launch_bounds__(kThreads) void race_state_kernel(StateArgs a)
     const St* Vl = (const St*)a.Val + bh * a.N * D;
     const float* vs = a.vscale ? a.vscale + bh * a.N : nullptr;
     const float* aw = a.aw ? a.aw + bh * a.N : nullptr;
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    // w wave-uniform (scalar): MFMAs under a condition on w are then skipped by
+    // a scalar branch; matrix instructions ignore the EXEC mask
+    const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
     const int g = lane >> 4, col = lane & 15;
 
-    for (int f = threadIdx.x; f < RP; f += kThreads) sm.a_state[f] = 0.f;
     f32x4 S[RP / 16][DW];
 #pragma unroll
     for (int ft = 0; ft < RP / 16; ++ft)
 #pragma unroll
         for (int j = 0; j < DW; ++j) S[ft][j] = f32x4{0, 0, 0, 0};
+    // A on the matrix cores: wave w sums the feature tiles ft = w, w + 4, ...
+    constexpr int FT = RP / 16, NFA = (FT + 3) / 4;
+    f32x4 Aacc[NFA];
+#pragma unroll
+    for (int j = 0; j < NFA; ++j) Aacc[j] = f32x4{0, 0, 0, 0};
 
     const int t_beg = seg * a.seg_len, t_end = min(a.N, t_beg + a.seg_len);
     // projections, value rows and A weights of the chunk, loaded one chunk ahead
@@ -97,29 +101,24 @@ __global__ __launch_bounds__(kThreads) void race_state_kernel(StateArgs a)
         __syncthreads();
         vr.store(sm.vt, vs != nullptr);
         if (threadIdx.x < kC) sm.aw[threadIdx.x] = t0 + (int)threadIdx.x < a.N ? awv : 0.f;
-        features_from<T, RP>(ur, t0, a.N, a.L, a.two_beta, nullptr, sm.pht, nullptr);
+        features_from<T, RP>(ur, t0, a.N, a.L, a.two_beta, sm.ph, nullptr, nullptr);
         __syncthreads();
         load_chunk(t0 + kC < t_end ? t0 + kC : t0);   // the last chunk reloads its own (unconditional loads)
-        // S[f][cols of wave] += Phi'[f][rows] V[rows][cols]
+        // S[f][cols of wave] += Phi'[f][rows] V[rows][cols];  A[f] += Phi'[f][rows] aw[rows]
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
             typename T::frag_t bv[DW];
 #pragma unroll
             for (int j = 0; j < DW; ++j) bv[j] = T::ld8(&sm.vt[16 * (w * DW + j) + col][32 * kk + 8 * g]);
 #pragma unroll
-            for (int ft = 0; ft < RP / 16; ++ft) {
-                const auto af = T::ld8(&sm.pht[16 * ft + col][32 * kk + 8 * g]);
+            for (int ft = 0; ft < FT; ++ft) {
+                const auto af = phi_t8<T, RP>(sm.ph, 32 * kk, 16 * ft);
 #pragma unroll
                 for (int j = 0; j < DW; ++j) S[ft][j] = T::mma(af, bv[j], S[ft][j]);
+                if (ft % 4 == w) Aacc[ft / 4] = token_sums<T>(af, aw ? sm.aw : nullptr, 32 * kk, Aacc[ft / 4]);
             }
         }
-        for (int f = threadIdx.x; f < RP; f += kThreads) {
-            float s = 0.f;
-            for (int k = 0; k < kC; ++k) s += T::load(sm.pht[f][k]) * sm.aw[k];
-            sm.a_state[f] += s;
-        }
     }
-    __syncthreads();
     float* out = a.states + (bh * a.nseg + seg) * (size_t)(RP * D + RP);
 #pragma unroll
     for (int ft = 0; ft < RP / 16; ++ft)
@@ -128,7 +127,14 @@ __global__ __launch_bounds__(kThreads) void race_state_kernel(StateArgs a)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
                 out[(size_t)(16 * ft + 4 * g + i) * D + 16 * (w * DW + j) + col] = S[ft][j][i] * a.mul;
-    for (int f = threadIdx.x; f < RP; f += kThreads) out[RP * D + f] = sm.a_state[f] * a.mul;
+    // column 0 of the A tiles: lanes (g, 0) hold features 16 ft + 4 g + i
+#pragma unroll
+    for (int j = 0; j < NFA; ++j) {
+        const int ft = w + 4 * j;
+        if (ft < FT && col == 0)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) out[RP * D + 16 * ft + 4 * g + i] = Aacc[j][i] * a.mul;
+    }
 }
 
 // mode 0: total in every segment; 1: exclusive prefix; 2: exclusive suffix.
@@ -187,7 +193,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
     const St* V = (const St*)a.V + bh * a.N * D;
     float* Olr = a.O_lr + bh * a.N * D;
     float* dlr = a.d_lr + bh * a.N;
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);   // wave-uniform, as in race_state
     const int g = lane >> 4, col = lane & 15;
 
     const float* st_in = a.states + (bh * a.nseg + seg) * (size_t)(RP * D + RP);
@@ -200,6 +206,17 @@ __global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
             for (int i = 0; i < 4; ++i)
                 S[ft][j][i] = st_in[(size_t)(16 * ft + 4 * g + i) * D + 16 * (w * DW + j) + col];
     for (int f = threadIdx.x; f < RP; f += kThreads) sm.a_state[f] = st_in[RP * D + f];
+    // A runs on the matrix cores (causal): wave w keeps the feature tiles
+    // ft = w, w + 4, ... in column 0 of accumulator tiles, started from the
+    // segment's prefix state, and publishes them to a_state after each chunk
+    constexpr int FT = RP / 16, NFA = (FT + 3) / 4;
+    f32x4 Aacc[NFA];
+#pragma unroll
+    for (int j = 0; j < NFA; ++j) {
+        const int ft = w + 4 * j;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) Aacc[j][i] = ft < FT && col == 0 ? st_in[RP * D + 16 * ft + 4 * g + i] : 0.f;
+    }
 
     const int t_beg = seg * a.seg_len, t_end = min(a.N, t_beg + a.seg_len);
     URegs<RP> uq, uk;                    // projections and V rows of the chunk, loaded one chunk ahead
@@ -211,7 +228,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
         __syncthreads();
         vr.store(sm.vt, false);
         features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, sm.phq, nullptr, nullptr);
-        if (a.causal) features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, sm.phk, sm.phkt, nullptr);
+        if (a.causal) features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, sm.phk, nullptr, nullptr);
         __syncthreads();
         {
             // next chunk's rows (the last chunk reloads its own: unconditional loads)
@@ -265,8 +282,9 @@ __global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
         __syncthreads();
         // Num^T for the wave's d columns, all 64 queries (lane (g, col) holds
         // d = 16 (w DW + j) + 4 g + i of query 16 qt + col): inter-chunk part
-        // with S in float32 accuracy (hi / lo bf16 split made once per chunk),
-        // then the masked intra-chunk part
+        // with S rounded to the storage dtype once per chunk (the forward
+        // sums positive features against it, no cancellation), then the
+        // masked intra-chunk part
         f32x4 num[4][DW];
 #pragma unroll
         for (int qt = 0; qt < 4; ++qt)
@@ -274,7 +292,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
             for (int j = 0; j < DW; ++j) num[qt][j] = f32x4{0, 0, 0, 0};
 #pragma unroll
         for (int fs = 0; fs < FS; ++fs) {
-            F shi[DW], slo[DW];
+            F sf[DW];
 #pragma unroll
             for (int j = 0; j < DW; ++j) {
                 float sv[8];
@@ -283,17 +301,14 @@ __global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
                     sv[i] = S[2 * fs][j][i];
                     sv[4 + i] = S[2 * fs + 1][j][i];
                 }
-                T::split(sv, shi[j], slo[j]);
+                sf[j] = T::pack(sv);
             }
 #pragma unroll
             for (int qt = 0; qt < 4; ++qt) {
                 const F af = T::ld44(&sm.phq[16 * qt + col][32 * fs + 4 * g],
                                      &sm.phq[16 * qt + col][32 * fs + 16 + 4 * g]);
 #pragma unroll
-                for (int j = 0; j < DW; ++j) {
-                    num[qt][j] = T::mma(shi[j], af, num[qt][j]);
-                    if (T::kSplit) num[qt][j] = T::mma(slo[j], af, num[qt][j]);
-                }
+                for (int j = 0; j < DW; ++j) num[qt][j] = T::mma(sf[j], af, num[qt][j]);
             }
         }
 #pragma unroll
@@ -329,16 +344,20 @@ __global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
 #pragma unroll
                 for (int j = 0; j < DW; ++j) bv[j] = T::ld8(&sm.vt[16 * (w * DW + j) + col][32 * kk + 8 * g]);
 #pragma unroll
-                for (int ft = 0; ft < RP / 16; ++ft) {
-                    const F af = T::ld8(&sm.phkt[16 * ft + col][32 * kk + 8 * g]);
+                for (int ft = 0; ft < FT; ++ft) {
+                    const F af = phi_t8<T, RP>(sm.phk, 32 * kk, 16 * ft);
 #pragma unroll
                     for (int j = 0; j < DW; ++j) S[ft][j] = T::mma(af, bv[j], S[ft][j]);
+                    if (ft % 4 == w) Aacc[ft / 4] = token_sums<T>(af, nullptr, 32 * kk, Aacc[ft / 4]);
                 }
             }
-            for (int f = threadIdx.x; f < RP; f += kThreads) {
-                float s = 0.f;
-                for (int k = 0; k < kC; ++k) s += T::load(sm.phkt[f][k]);
-                sm.a_state[f] += s;
+            // the den of the next chunk reads a_state after its first barrier
+#pragma unroll
+            for (int j = 0; j < NFA; ++j) {
+                const int ft = w + 4 * j;
+                if (ft < FT && col == 0)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) sm.a_state[16 * ft + 4 * g + i] = Aacc[j][i];
             }
         }
     }
