@@ -110,8 +110,10 @@ def kernel_model(w, Lv: int) -> dict:
     """Bytes each sparse-branch kernel actually has to move as the path is
     split into kernels (name -> bytes per step): the survey accounting above
     plus the level partials (storage dtype), which the level kernels write and the
-    leaf kernels read back.  Reported beside the algorithmic figure so the
-    cost of the split is visible; not a roofline numerator."""
+    leaf kernels read back, with every tensor at the size the path stores it
+    (O_s float32; O_lr and the gradients in the storage dtype).  Reported beside the
+    algorithmic figure so the cost of the split is visible; not a roofline
+    numerator."""
     s = 2 if w.dtype == "bf16" else 4
     bh = w.B * w.H
     N, D = w.N, w.d
@@ -123,7 +125,7 @@ def kernel_model(w, Lv: int) -> dict:
     wk = max(32, 4 * w.L)
     return {
         "sparse_fwd_levels": lvl_pos * (3 * D * s + 8 + D * ps + 4),
-        "sparse_fwd_leaf": bh * N * (3 * D * s + 8 * D + 4 + D * s + 8) + lvl_pos * (D * ps + 4),
+        "sparse_fwd_leaf": bh * N * (3 * D * s + 4 * D + D * s + 4 + D * s + 8) + lvl_pos * (D * ps + 4),
         "sparse_bwd_levels": lvl_pos * (4 * D * s + 20 + 3 * D * ps),
         "sparse_leaf_bwd": bh * N * (4 * D * s + 12 + 2 * wk * s + D * s + 3 * D * s) + lvl_pos * 3 * D * ps,
     }

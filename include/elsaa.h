@@ -110,10 +110,12 @@ int elsaa_workspace_bytes(const elsaa_config* cfg, int pass, size_t* bytes);
 /* Byte offsets inside `saved` (each 256-byte aligned):
  *   perm_q, perm_k  int32 sorted index lists (layout as elsaa_select);
  *   m               float32 [B,H,N] denominator-aware multiplier;
- *   o_sparse        float32 [B,H,N,d_h] sparse-branch output O_s;
- *   o_lowrank       float32 [B,H,N,d_h] low-rank output O_lr (both kept in float32:
- *                   the backward's <dO, O_s> and <dO, O_lr> cancel against
- *                   <dO, V_j> terms);
+ *   o_sparse        float32 [B,H,N,d_h] sparse-branch output O_s (float32:
+ *                   the backward's <dO, O_s> cancels against <dO, V_j> of
+ *                   the dominant keys when attention is peaked);
+ *   o_lowrank       storage dtype [B,H,N,d_h] low-rank output O_lr (its
+ *                   weights are diffuse, so <dO, O_lr> has no such
+ *                   cancellation);
  *   u_q, u_k        float32 [B,H,N,P] RACE projections u = W_race x of the Q and K
  *                   rows (P = 4 L rounded up to 8, 16, 32 or 64; padded tables 0);
  *   race_states     float32 RACE segment states phi(k) V' and phi(k) of the key

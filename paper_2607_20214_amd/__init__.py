@@ -219,7 +219,7 @@ def saved_views(cfg: Config, saved: torch.Tensor) -> dict:
         "perm_k": view(L["perm_k"], npm, torch.int32, ps),
         "m": view(L["m"], B * H * N, torch.float32, (B, H, N)),
         "o_sparse": view(L["o_sparse"], B * H * N * d, torch.float32, (B, H, N, d)),
-        "o_lowrank": view(L["o_lowrank"], B * H * N * d, torch.float32, (B, H, N, d)),
+        "o_lowrank": view(L["o_lowrank"], B * H * N * d, cfg.torch_dtype, (B, H, N, d)),
     }
 
 

@@ -133,8 +133,9 @@ SavedLayout saved_layout(const Shape& s)
     L.perm_q = off; off = align256(off + bh * s.P() * 4);
     L.perm_k = off; off = align256(off + bh * s.P() * 4);
     L.m = off; off = align256(off + bh * s.N * 4);
-    L.o_s = off; off = align256(off + bh * s.N * s.D * 4);   // float32: the backward's Delta cancels against it
-    L.o_lr = off; off = align256(off + bh * s.N * s.D * 4);   // float32, same reason (dDen)
+    L.o_s = off; off = align256(off + bh * s.N * s.D * 4);   // float32: Delta = <dO, O_s> cancels against dP
+                                                              // of the dominant keys when attention is peaked
+    L.o_lr = off; off = align256(off + bh * s.N * s.D * (s.bf16 ? 2 : 4));   // storage dtype (diffuse weights)
     L.u_q = off; off = align256(off + bh * s.N * race_proj_stride(s) * 4);
     L.u_k = off; off = align256(off + bh * s.N * race_proj_stride(s) * 4);
     L.race_states = off; off = align256(off + race_state_floats(s) * 4);   // RACE segment prefix states
@@ -432,7 +433,7 @@ int elsaa_fwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     int32_t* pk = at<int32_t>(saved, SL.perm_k);
     float* m = at<float>(saved, SL.m);
     float* o_s = at<float>(saved, SL.o_s);
-    float* o_lr = at<float>(saved, SL.o_lr);
+    void* o_lr = at<char>(saved, SL.o_lr);
     float* uq = at<float>(saved, SL.u_q);
     float* uk = at<float>(saved, SL.u_k);
     hipError_t e;
@@ -483,7 +484,7 @@ int elsaa_bwd(const elsaa_config* cfg, const void* Q, const void* K, const void*
     const int32_t* pk = at<int32_t>(sv, SL.perm_k);
     const float* m = at<float>(sv, SL.m);
     const float* o_s = at<float>(sv, SL.o_s);
-    const float* o_lr = at<float>(sv, SL.o_lr);
+    const void* o_lr = at<char>(sv, SL.o_lr);
     const float* uq = at<float>(sv, SL.u_q);
     const float* uk = at<float>(sv, SL.u_k);
     float* rs = at<float>(workspace, W.rs);

@@ -10,7 +10,7 @@
 //   dg_s  = m <O_s, u>,  dg_lr = <O_lr, u>,  dlambda = -dm m Den / D
 // (lambda per token when given; with m fixed to 1 every dm term is zero).
 // Stored as rs[f][BHN] with f = 0: log2(d_s + eps), 1: Delta, 2: sc_s,
-// 3: sc_lr, 4: dDen.  16 lanes per row; O_s and O_lr are float32.
+// 3: sc_lr, 4: dDen.  16 lanes per row; O_s float32, O_lr in the storage dtype.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -21,7 +21,7 @@ namespace {
 template <class T, int D>
 __global__ __launch_bounds__(256) void bwd_rows_kernel(const typename T::store_t* __restrict__ dO,
                                                        const float* __restrict__ Os,
-                                                       const float* __restrict__ Olr,
+                                                       const typename T::store_t* __restrict__ Olr,
                                                        const float* __restrict__ m,
                                                        const float* __restrict__ lse,
                                                        const float* __restrict__ dlr,
@@ -38,10 +38,13 @@ __global__ __launch_bounds__(256) void bwd_rows_kernel(const typename T::store_t
     float uos = 0.f, uol = 0.f;
     const size_t base = row * D + sub * PL;
 #pragma unroll
-    for (int e = 0; e < PL; ++e) {
-        const float u = T::load(dO[base + e]);
-        uos += u * Os[base + e];
-        uol += u * Olr[base + e];
+    for (int e = 0; e < PL; e += 4) {
+        const f32x4 u = load4<T>(dO + base + e), xs = *(const f32x4*)(Os + base + e), xl = load4<T>(Olr + base + e);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            uos += u[i] * xs[i];
+            uol += u[i] * xl[i];
+        }
     }
     uos = row_sum16(uos);
     uol = row_sum16(uol);
@@ -71,7 +74,7 @@ __global__ __launch_bounds__(256) void bwd_rows_kernel(const typename T::store_t
 
 }  // namespace
 
-hipError_t launch_bwd_rows(const Shape& s, const void* dO, const float* Os, const float* Olr,
+hipError_t launch_bwd_rows(const Shape& s, const void* dO, const float* Os, const void* Olr,
                            const float* m, const float* lse, const float* dlr, const float* gates,
                            const float* lambda_rows, float* rs, float* dgates, float* dlambda,
                            hipStream_t st)
@@ -80,7 +83,7 @@ hipError_t launch_bwd_rows(const Shape& s, const void* dO, const float* Os, cons
     dim3 grid((unsigned)((BHN + 15) / 16));
 #define ELSAA_ROWS(T_, D_)                                                                       \
     ELSAA_LAUNCH("bwd_rows", (bwd_rows_kernel<T_, D_>), grid, dim3(256), 0, st,                          \
-                       (const T_::store_t*)dO, Os, Olr, m, \
+                       (const T_::store_t*)dO, Os, (const T_::store_t*)Olr, m, \
                        lse, dlr, gates, lambda_rows, rs, dgates, dlambda, BHN, s.lambda, s.eps, s.m_one)
     if (s.bf16) {
         if (s.D == 64) ELSAA_ROWS(BF16, 64);

@@ -72,7 +72,7 @@ bool race_bwd_fits(const Shape& s);
 hipError_t launch_race_states(const Shape& s, const float* U, const void* Val, const float* vscale,
                               const float* aw, float mul, float* states, int scan_mode, hipStream_t st);
 hipError_t launch_race_fwd(const Shape& s, const float* Uq, const float* Uk, const void* V,
-                           float* states, float* O_lr, float* d_lr, hipStream_t st);
+                           float* states, void* O_lr, float* d_lr, hipStream_t st);
 size_t race_wt_bytes(const Shape& s);       // one of the W' hi / lo buffers
 int race_wk(const Shape& s);                // columns of W' and of a du row (4 L padded to 32)
 // states_f: the forward's segment prefix states (elsaa_fwd keeps them in saved);
@@ -100,12 +100,12 @@ enum SparsePart {
 hipError_t launch_sparse_fwd(const Shape& s, const void* Q, const void* K, const void* V,
                              const int32_t* perm_q, const int32_t* perm_k, const float* gates,
                              const float* lambda_rows,
-                             const float* O_lr, const float* d_lr, void* part_o, float* part_lse,
+                             const void* O_lr, const float* d_lr, void* part_o, float* part_lse,
                              void* O, float* lse, float* m, float* O_s, hipStream_t st,
                              int parts = kSparseAll);
 
 // backward: per-row scalars rs[5][BHN] (log2(d_s+eps), Delta, sc_s, sc_lr, dDen)
-hipError_t launch_bwd_rows(const Shape& s, const void* dO, const float* Os, const float* Olr,
+hipError_t launch_bwd_rows(const Shape& s, const void* dO, const float* Os, const void* Olr,
                            const float* m, const float* lse, const float* dlr, const float* gates,
                            const float* lambda_rows, float* rs, float* dgates, float* dlambda,
                            hipStream_t st);

@@ -172,7 +172,7 @@ struct OutArgs {
     const float* Uk;      // projections of K rows
     const void* V;
     const float* states;
-    float* O_lr;          // float32 [BH][N][D]
+    void* O_lr;           // storage dtype [BH][N][D]
     float* d_lr;
     int H, N, L, seg_len, nseg, causal;
     float two_beta, inv_L, eps;
@@ -191,7 +191,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
     const float* Uq = a.Uq + bh * a.N * (RP / 4);
     const float* Uk = a.Uk + bh * a.N * (RP / 4);
     const St* V = (const St*)a.V + bh * a.N * D;
-    float* Olr = a.O_lr + bh * a.N * D;
+    St* Olr = (St*)a.O_lr + bh * a.N * D;
     float* dlr = a.d_lr + bh * a.N;
     const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);   // wave-uniform, as in race_state
     const int g = lane >> 4, col = lane & 15;
@@ -331,7 +331,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
                 const float inv = 1.f / (den + a.eps);
 #pragma unroll
                 for (int j = 0; j < DW; ++j)
-                    *(f32x4*)(Olr + (size_t)tok * D + 16 * (w * DW + j) + 4 * g) = num[qt][j] * inv;
+                    store4<T>(Olr + (size_t)tok * D + 16 * (w * DW + j) + 4 * g, num[qt][j] * inv);
             }
         }
         if (threadIdx.x < kC && t0 + threadIdx.x < a.N)
@@ -465,7 +465,7 @@ hipError_t launch_race_states(const Shape& s, const float* U, const void* Val, c
 }
 
 hipError_t launch_race_fwd(const Shape& s, const float* Uq, const float* Uk, const void* V,
-                           float* states, float* O_lr, float* d_lr, hipStream_t st)
+                           float* states, void* O_lr, float* d_lr, hipStream_t st)
 {
     hipError_t e = launch_race_states(s, Uk, V, nullptr, nullptr, 1.f, states, s.causal ? 1 : 0, st);
     if (e != hipSuccess) return e;

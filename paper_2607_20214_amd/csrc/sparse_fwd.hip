@@ -47,14 +47,14 @@ struct Args {
     const int32_t* perm_k;
     const float* gates;
     const float* lam_rows;    // per-token lambda_i or null (scalar lambda)
-    const float* O_lr;
+    const void* O_lr;         // storage dtype [BH][N][D]
     const float* d_lr;
     void* part_o;             // [BH][Lv][N/2][D] normalised level outputs, storage dtype
     float* part_lse;          // [BH][Lv][N/2] log of each level's denominator
     void* O;
     float* lse;
     float* m;
-    float* O_s;
+    float* O_s;               // float32 [BH][N][D]
     int H, N, k, Lv;
     LevelTiles lt;   // causal recursion geometry and tile numbering
     int nbr;         // neighbouring sorted blocks on each side
@@ -292,7 +292,7 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
         gs = a.gates[row * 2 + 0];
         gl = a.gates[row * 2 + 1];
     }
-    const float* olr = a.O_lr + row * D;
+    const S* olr = (const S*)a.O_lr + row * D;
     S* out = (S*)a.O + row * D;
     float* os = a.O_s + row * D;
 #pragma unroll
@@ -300,7 +300,7 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
         const int c0 = 16 * dt + 4 * g;
         const f32x4 o_s = acc[dt] * inv_den;
         *(f32x4*)(os + c0) = o_s;
-        const f32x4 o_l = *(const f32x4*)(olr + c0);
+        const f32x4 o_l = load4<T>(olr + c0);
         store4<T>(out + c0, o_s * (gs * mf) + o_l * gl);
     }
     if (g == 0) {
@@ -334,7 +334,7 @@ hipError_t launch_t(const Shape& s, const Args& a, hipStream_t st, int parts)
 
 hipError_t launch_sparse_fwd(const Shape& s, const void* Q, const void* K, const void* V,
                              const int32_t* perm_q, const int32_t* perm_k, const float* gates,
-                             const float* lambda_rows, const float* O_lr, const float* d_lr, void* part_o, float* part_lse,
+                             const float* lambda_rows, const void* O_lr, const float* d_lr, void* part_o, float* part_lse,
                              void* O, float* lse, float* m, float* O_s, hipStream_t st, int parts)
 {
     Args a;
