@@ -47,13 +47,12 @@ struct Lb1Smem {
     using S = typename T::store_t;
     S vt[D][kC + kPad];            // V chunk transposed
     S dn[kC][D + kPad];            // dO chunk, rows (dNum_i = sc_lr,i dO_i: the products apply sc_lr)
-    S pkt[RP][kC + kPad];          // Phi_K transposed
+    S pk[kC][RP + kPad];           // Phi_K chunk, rows (Phi_K^T operands: transposed LDS reads)
     S gg[kC][kC + kPad];           // G[i][j] = <dNum_i, V_j> + dDen_i, j <= i
     float ts[kC][RP / 4];          // tanh(W q) of the chunk's queries
     S du[kC][w_kdim<RP>() + kPad];
     float dden[kC];
     float sc[kC];                  // sc_lr of the chunk's queries
-    float a_state[RP];             // A = sum phi(k) of the keys before the chunk
 };
 
 template <class T, int D, int RP>
@@ -61,12 +60,13 @@ struct Lb2Smem {
     using S = typename T::store_t;
     S vr[kC][D + kPad];            // V chunk, rows
     S dnt[D][kC + kPad];           // dNum / L chunk, transposed
-    S pqt[RP][kC + kPad];          // Phi_Q transposed
+    S pq[kC][RP + kPad];           // Phi_Q chunk, rows (Phi_Q^T operands: transposed LDS reads)
     S ggt[kC][kC + kPad];          // G'[j][i] / L, i >= j
     float ts[kC][RP / 4];          // tanh(W k) of the chunk's keys
     S du[kC][w_kdim<RP>() + kPad];
-    float dden[kC];
+    float dden[kC];                // dDen / L of the chunk's queries
     float a_state[RP];             // dA = (1/L) sum phi(q) dDen of the queries after the chunk
+                                   // (rows of feature tile ft are read and written by wave ft % 4 only)
 };
 
 template <class T, int D, int RP>
@@ -74,8 +74,7 @@ struct Lb3Smem {
     using S = typename T::store_t;
     S dnt[D][kC + kPad];           // dNum / L chunk, transposed
     S pk[kC][RP + kPad];           // Phi_K rows
-    S pq[kC][RP + kPad];           // Phi_Q rows
-    S pqt[RP][kC + kPad];          // Phi_Q transposed
+    S pq[kC][RP + kPad];           // Phi_Q rows (Phi_Q^T operands: transposed LDS reads)
     S mt[kC][kC + kPad];           // M'[j][i] = <phi(k_j), phi(q_i)>, i >= j
 };
 
@@ -132,15 +131,16 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
     const float* sclr = a.rs + 3 * a.BHN + bh * a.N;
     const float* dden = a.rs + 4 * a.BHN + bh * a.N;
     St* du_out = (St*)a.out + bh * a.N * w_kdim<RP>();
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
     const int g = lane >> 4, col = lane & 15;
 
     for (int it = threadIdx.x; it < kC * (w_kdim<RP>() + kPad); it += kThreads)
         (&sm.du[0][0])[it] = T::store(0.f);
-    // state S'[d][f] for the wave's features f = 16 (w + 4j) + col; A[f] in LDS
-    f32x4 St_[NFT][DT];
+    // state S'[d][f] for the wave's features f = 16 (w + 4j) + col, and
+    // A[f] of the same feature tiles (lane (g, col) register i: feature
+    // 16 (w + 4j) + 4 g + i, every column alike; token_sums keeps it so)
+    f32x4 St_[NFT][DT], Aacc[NFT];
     const float* st_in = a.states + (bh * a.nseg + seg) * (size_t)(RP * D + RP);
-    for (int f = threadIdx.x; f < RP; f += kThreads) sm.a_state[f] = st_in[RP * D + f];
 #pragma unroll
     for (int j = 0; j < NFT; ++j) {
         const int ft = w + 4 * j;
@@ -149,6 +149,8 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
                 St_[j][dt][i] = ft < FT ? st_in[(size_t)(16 * ft + col) * D + 16 * dt + 4 * g + i] : 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) Aacc[j][i] = ft < FT ? st_in[RP * D + 16 * ft + 4 * g + i] : 0.f;
     }
 
     const int t_beg = seg * a.seg_len, t_end = min(a.N, t_beg + a.seg_len);
@@ -166,7 +168,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
         const bool in = threadIdx.x < kC && t0 + (int)threadIdx.x < a.N;
         const float ddv = in ? dden[t0 + threadIdx.x] : 0.f, scv = in ? sclr[t0 + threadIdx.x] : 0.f;
         features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, nullptr, nullptr, sm.ts);
-        if (a.causal) features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, nullptr, sm.pkt, nullptr);
+        if (a.causal) features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, sm.pk, nullptr, nullptr);
         sdn.store(sm.dn, false);
         if (a.causal) svt.store(sm.vt, false);
         if (threadIdx.x < kC) {
@@ -233,11 +235,11 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
             for (int qt = 0; qt < 4; ++qt) {
                 const float ddq = sm.dden[16 * qt + col], scq = sm.sc[16 * qt + col];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) acc[qt][i] = acc[qt][i] * scq + sm.a_state[16 * ft + 4 * g + i] * ddq;
+                for (int i = 0; i < 4; ++i) acc[qt][i] = acc[qt][i] * scq + Aacc[j][i] * ddq;
                 if (a.causal) {
 #pragma unroll
                     for (int kk = 0; kk < 2; ++kk)
-                        acc[qt] = T::mma(T::ld8(&sm.pkt[16 * ft + col][32 * kk + 8 * g]),
+                        acc[qt] = T::mma(phi_t8<T, RP>(sm.pk, 32 * kk, 16 * ft),
                                          T::ld8(&sm.gg[16 * qt + col][32 * kk + 8 * g]), acc[qt]);
                 }
                 acc[qt] *= a.inv_L;
@@ -247,20 +249,20 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
         __syncthreads();
         store_du<T, RP>(sm.du, du_out, t0, a.N);
         if (a.causal) {
-            // S' += V' Phi_K (chunk), A += Phi_K' 1
+            // S' += V' Phi_K (chunk), A += Phi_K' 1 (one Phi_K^T fragment each)
 #pragma unroll
             for (int j = 0; j < NFT; ++j) {
                 const int ft = w + 4 * j;
                 if (ft >= FT) break;
 #pragma unroll
                 for (int kk = 0; kk < 2; ++kk) {
-                    const F bf = T::ld8(&sm.pkt[16 * ft + col][32 * kk + 8 * g]);
+                    const F bf = phi_t8<T, RP>(sm.pk, 32 * kk, 16 * ft);
 #pragma unroll
                     for (int dt = 0; dt < DT; ++dt)
                         St_[j][dt] = T::mma(T::ld8(&sm.vt[16 * dt + col][32 * kk + 8 * g]), bf, St_[j][dt]);
+                    Aacc[j] = token_sums<T>(bf, nullptr, 32 * kk, Aacc[j]);
                 }
             }
-            add_chunk_sums<T, RP>(sm.pkt, nullptr, 1.f, sm.a_state);
         }
     }
 }
@@ -282,11 +284,12 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
     const float* sclr = a.rs + 3 * a.BHN + bh * a.N;
     const float* dden = a.rs + 4 * a.BHN + bh * a.N;
     St* du_out = (St*)a.out + bh * a.N * w_kdim<RP>();
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
     const int g = lane >> 4, col = lane & 15;
 
     for (int it = threadIdx.x; it < kC * (w_kdim<RP>() + kPad); it += kThreads)
         (&sm.du[0][0])[it] = T::store(0.f);
+    // dS'[d][f] of the wave's feature tiles, laid out as in LB1; dA in LDS
     f32x4 St_[NFT][DT];
     const float* st_in = a.states + (bh * a.nseg + seg) * (size_t)(RP * D + RP);
     for (int f = threadIdx.x; f < RP; f += kThreads) sm.a_state[f] = st_in[RP * D + f];
@@ -316,10 +319,10 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
         const bool in = threadIdx.x < kC && t0 + (int)threadIdx.x < a.N;
         const float ddv = in ? dden[t0 + threadIdx.x] : 0.f;
         features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, nullptr, nullptr, sm.ts);
-        if (a.causal) features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, nullptr, sm.pqt, nullptr);
+        if (a.causal) features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, sm.pq, nullptr, nullptr);
         svr.store(sm.vr, false);
         if (a.causal) sdn.store(sm.dnt, true);
-        if (threadIdx.x < kC) sm.dden[threadIdx.x] = ddv;
+        if (threadIdx.x < kC) sm.dden[threadIdx.x] = ddv * a.inv_L;
         __syncthreads();
         {
             // previous chunk's projections (unconditional: chunk 0 reloads its own)
@@ -344,7 +347,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
                 const f32x4 dd = *(const f32x4*)&sm.dden[16 * it + 4 * g];
                 f32x4 v;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) v[i] = 16 * it + 4 * g + i >= kj ? acc[i] + dd[i] * a.inv_L : 0.f;
+                for (int i = 0; i < 4; ++i) v[i] = 16 * it + 4 * g + i >= kj ? acc[i] + dd[i] : 0.f;
                 store4<T>(&sm.ggt[kj][16 * it + 4 * g], v);
             }
         }
@@ -382,7 +385,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
                 if (a.causal) {
 #pragma unroll
                     for (int kk = 0; kk < 2; ++kk)
-                        acc[kt] = T::mma(T::ld8(&sm.pqt[16 * ft + col][32 * kk + 8 * g]),
+                        acc[kt] = T::mma(phi_t8<T, RP>(sm.pq, 32 * kk, 16 * ft),
                                          T::ld8(&sm.ggt[16 * kt + col][32 * kk + 8 * g]), acc[kt]);
                 }
                 chain_rule_t<T, RP>(acc[kt], kt, ft, a.L, a.beta, sm.ts, sm.du);
@@ -391,20 +394,27 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
         __syncthreads();
         store_du<T, RP>(sm.du, du_out, t0, a.N);
         if (a.causal) {
-            // dS' += (dNum / L)' Phi_Q (chunk), dA += (1/L) Phi_Q' dDen
+            // dS' += (dNum / L)' Phi_Q (chunk), dA += Phi_Q' (dDen / L) (one
+            // Phi_Q^T fragment each; the weights keep float32 accuracy)
 #pragma unroll
             for (int j = 0; j < NFT; ++j) {
                 const int ft = w + 4 * j;
                 if (ft >= FT) break;
+                f32x4 asum = {0, 0, 0, 0};
 #pragma unroll
                 for (int kk = 0; kk < 2; ++kk) {
-                    const F bf = T::ld8(&sm.pqt[16 * ft + col][32 * kk + 8 * g]);
+                    const F bf = phi_t8<T, RP>(sm.pq, 32 * kk, 16 * ft);
 #pragma unroll
                     for (int dt = 0; dt < DT; ++dt)
                         St_[j][dt] = T::mma(T::ld8(&sm.dnt[16 * dt + col][32 * kk + 8 * g]), bf, St_[j][dt]);
+                    asum = token_sums<T>(bf, sm.dden, 32 * kk, asum);
                 }
+                // every column holds the sums; column 0 adds them (this
+                // wave's rows; read again after the next chunk's barriers)
+                if (col == 0)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) sm.a_state[16 * ft + 4 * g + i] += asum[i];
             }
-            add_chunk_sums<T, RP>(sm.pqt, sm.dden, a.inv_L, sm.a_state);
         }
     }
 }
@@ -424,7 +434,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dv_kernel(LbArgs a)
     const St* dO = (const St*)a.dO + bh * a.N * D;
     const float* sclr = a.rs + 3 * a.BHN + bh * a.N;
     St* out = (St*)a.out + bh * a.N * D;
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
     const int g = lane >> 4, col = lane & 15;
 
     const float* st_in = a.states + (bh * a.nseg + seg) * (size_t)(RP * D + RP);
@@ -450,7 +460,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dv_kernel(LbArgs a)
         if (a.causal) sdn.load(dO, t0, a.N, sclr, a.inv_L);
         features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, sm.pk, nullptr, nullptr);
         if (a.causal) {
-            features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, sm.pq, sm.pqt, nullptr);
+            features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, sm.pq, nullptr, nullptr);
             sdn.store(sm.dnt, true);
         }
         __syncthreads();
@@ -535,7 +545,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dv_kernel(LbArgs a)
                 for (int j = 0; j < DW; ++j) bv[j] = T::ld8(&sm.dnt[16 * (w * DW + j) + col][32 * kk + 8 * g]);
 #pragma unroll
                 for (int ft = 0; ft < RP / 16; ++ft) {
-                    const F af = T::ld8(&sm.pqt[16 * ft + col][32 * kk + 8 * g]);
+                    const F af = phi_t8<T, RP>(sm.pq, 32 * kk, 16 * ft);
 #pragma unroll
                     for (int j = 0; j < DW; ++j) S[ft][j] = T::mma(af, bv[j], S[ft][j]);
                 }

@@ -64,46 +64,21 @@ __device__ __forceinline__ typename T::frag_t phi_t8(const typename T::store_t (
     return col8_t<T, RP + kPad>(ph, kb, f0);
 }
 
-// Weighted sums over the chunk's tokens on the matrix cores: the B operand of
-// Phi^T x [w | 0 ...] (tokens kb + 8 g + j of column 0 hold w, w = 1 when
-// null; the other columns 0), so column 0 of the product tile is
-// sum_k phi_f(k) w_k for the tile's 16 features.  w keeps float32 accuracy
-// (hi + lo parts, two products) when given.
+// Weighted sums over 32 of the chunk's tokens on the matrix cores: Phi^T x W
+// with every column of W holding the weights of tokens kb .. kb + 31 (w, or 1
+// when null), so every lane of the product tile holds the sums of its rows'
+// features: lane (g, col) register i += sum_k phi_{f0 + 4g + i}(k) w_k (phit
+// from phi_t8 at feature f0).  w keeps float32 accuracy (hi + lo parts, two
+// products) when given.
 template <class T>
 __device__ __forceinline__ f32x4 token_sums(typename T::frag_t phit, const float* w, int kb, f32x4 acc)
 {
-    const int lane = threadIdx.x & 63, g = lane >> 4, col = lane & 15;
+    const int g = (threadIdx.x & 63) >> 4;
     float v[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) v[j] = col == 0 ? (w ? w[kb + 8 * g + j] : 1.f) : 0.f;
+    for (int j = 0; j < 8; ++j) v[j] = w ? w[kb + 8 * g + j] : 1.f;
     if (!w) return T::mma(phit, T::pack(v), acc);
     return mma_split<T>(phit, v, acc);
-}
-
-// a_state[f] += scale * sum over the chunk's tokens k of xt[f][k] (* wk[k] when
-// wk is not null), xt a transposed feature tile [RP][kC + kPad]; all threads,
-// 256 / RP per feature (16-byte LDS reads, then a lane reduction).
-template <class T, int RP>
-__device__ __forceinline__ void add_chunk_sums(const typename T::store_t (*xt)[kC + kPad], const float* wk,
-                                               float scale, float* a_state)
-{
-    constexpr int TPF = RP >= kThreads ? 1 : kThreads / RP;   // threads per feature
-    constexpr int PER = kC / TPF;                               // tokens per thread
-    static_assert(PER % 8 == 0, "chunk split");
-    for (int f0 = 0; f0 < RP; f0 += kThreads / TPF) {
-        const int f = f0 + (int)threadIdx.x / TPF, part = threadIdx.x % TPF;
-        float s = 0.f;
-#pragma unroll
-        for (int k8 = 0; k8 < PER; k8 += 8) {
-            const int k = part * PER + k8;
-            const auto v = T::ld8(&xt[f][k]);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) s += wk ? (float)v[j] * wk[k + j] : (float)v[j];
-        }
-#pragma unroll
-        for (int m = 1; m < TPF; m <<= 1) s += __shfl_xor(s, m);
-        if (part == 0) a_state[f] += s * scale;
-    }
 }
 
 // projection count padded to whole 32-wide k-steps (backward du x W)

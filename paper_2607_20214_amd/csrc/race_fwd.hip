@@ -207,8 +207,9 @@ __global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
                 S[ft][j][i] = st_in[(size_t)(16 * ft + 4 * g + i) * D + 16 * (w * DW + j) + col];
     for (int f = threadIdx.x; f < RP; f += kThreads) sm.a_state[f] = st_in[RP * D + f];
     // A runs on the matrix cores (causal): wave w keeps the feature tiles
-    // ft = w, w + 4, ... in column 0 of accumulator tiles, started from the
-    // segment's prefix state, and publishes them to a_state after each chunk
+    // ft = w, w + 4, ... in accumulator tiles (every column holds the sums;
+    // column 0 starts from the segment's prefix state and is published to
+    // a_state after each chunk)
     constexpr int FT = RP / 16, NFA = (FT + 3) / 4;
     f32x4 Aacc[NFA];
 #pragma unroll
