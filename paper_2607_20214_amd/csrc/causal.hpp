@@ -104,6 +104,21 @@ __device__ __forceinline__ int64_t level_entry(const LevelTiles& lt, int l, int 
     return lt.off[l] + (int64_t)s * m + (t - a - (future ? m : 0));
 }
 
+// Per-level rows (the causal levels' partial results, one row per list
+// entry) of segment seg at level l: token t of that segment has its row at
+// base + t, i.e. the entry of the same rank within the segment's future half
+// (future = true) or past half, after the (b,h)s before it.  Every token of a
+// sorted block, a level tile or a leaf lies in one segment per level, so
+// callers form the base once from uniform values (scalar work) and add the
+// token.
+__device__ __forceinline__ int64_t seg_slot_base(const LevelTiles& lt, size_t bh, int l, int seg, bool future)
+{
+    int a, r;
+    seg_range(lt, l, seg, a, r);
+    const int m = lt.len[l + 1];
+    return (int64_t)(bh * (size_t)lt.off[lt.Lv] + (size_t)lt.off[l]) + (int64_t)seg * m - a - (future ? m : 0);
+}
+
 // Levels whose partials leaf s adds: bit l set when the leaf lies in the
 // future half (future = true) or in the past half of its level-l segment.
 __device__ __forceinline__ unsigned leaf_levels(const LevelTiles& lt, int leaf, bool future)

@@ -60,12 +60,6 @@ struct BArgs {
     float tau, tau2;
 };
 
-// Partial row of token t at level l: its entry among the level's future (or
-// past) halves, after the (b,h)s before it.
-__device__ __forceinline__ size_t level_slot(const LevelTiles& lt, size_t bh, int l, int t, bool future)
-{
-    return bh * (size_t)lt.off[lt.Lv] + (size_t)level_entry(lt, l, t, future);
-}
 
 // The low-rank part of dQ (dK) of one token for the 16-row slice dt of d:
 // (du W')^T, rows d = 16 dt + 4 g + i, the token in the lane's column (du_row
@@ -186,6 +180,7 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
     const S* dO = (const S*)a.dO + bh * N * D;
 
     int level = 0, half = N, qpos, qtok, kbeg, kend, bq = 1;
+    int64_t slot0 = 0;                           // levels: partial row of token t at slot0 + t
     const int32_t* klist = nullptr;
     if (MODE == kBlocks) {
         bq = min(a.k, N);
@@ -203,6 +198,7 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
         qpos = p0 + 16 * w + qq;
         const size_t lbase = bh * (size_t)a.lt.off[a.Lv] + (size_t)a.lt.off[level] + (size_t)seg * half;
         qtok = qpos < half ? a.perm_q[lbase + qpos] : -1;      // -1 also for a zero token
+        slot0 = seg_slot_base(a.lt, bh, level, seg, true);
         kbeg = max(0, (p0 / bq - a.nbr) * bq);
         kend = min(half, ((min(p0 + kT, half) - 1) / bq + 1 + a.nbr) * bq);
         klist = a.perm_k + lbase;
@@ -306,7 +302,7 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
     }
     if (MODE == kLevels) {
         if (qtok < 0) return;
-        S* out = (S*)a.part_dq + level_slot(a.lt, bh, level, qtok, true) * D;
+        S* out = (S*)a.part_dq + (size_t)(slot0 + qtok) * D;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) store4<T>(out + 16 * dt + 4 * g, acc[dt] * a.tau);
         return;
@@ -324,7 +320,8 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) tot[dt] = acc[dt] * a.tau + lowrank_lds<T, D>(duf, swt, a.wk, g, qq, dt);
     if (qtok < 0) return;
-    unsigned lmask = MODE == kLeaf ? leaf_levels(a.lt, tile / a.lt.per_leaf, true) : 0u;
+    const int leaf = tile / a.lt.per_leaf;
+    unsigned lmask = MODE == kLeaf ? leaf_levels(a.lt, leaf, true) : 0u;
     while (lmask) {
         const S* src[2];
         bool use[2];
@@ -335,7 +332,8 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
             if (use[j]) {
                 const int l = __builtin_ctz(lmask);
                 lmask &= lmask - 1;
-                src[j] = (const S*)a.part_dq + level_slot(a.lt, bh, l, qtok, true) * D;
+                const int64_t base = seg_slot_base(a.lt, bh, l, leaf >> (a.Lv - l), true);
+                src[j] = (const S*)a.part_dq + (size_t)(base + qtok) * D;
             }
         }
         f32x4 x[2][DT];
@@ -396,6 +394,7 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
     const S* dO = (const S*)a.dO + bh * N * D;
 
     int level = 0, half = N, kpos, ktok, qbeg, qend, bq = 1, j0 = 0;
+    int64_t slot0 = 0;                           // levels: partial row of token t at slot0 + t
     const int32_t* qlist = nullptr;
     const int32_t* klist = nullptr;
     if (MODE == kBlocks) {
@@ -417,6 +416,7 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
         const size_t lbase = bh * (size_t)a.lt.off[a.Lv] + (size_t)a.lt.off[level] + (size_t)seg * half;
         klist = a.perm_k + lbase;
         ktok = kpos < half ? klist[kpos] : -1;
+        slot0 = seg_slot_base(a.lt, bh, level, seg, false);
         qbeg = max(0, (p0 / bq - a.nbr) * bq);
         qend = min(half, ((min(p0 + kT, half) - 1) / bq + 1 + a.nbr) * bq);
         qlist = a.perm_q + lbase;
@@ -553,7 +553,7 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
 
     if (MODE == kLevels) {
         if (ktok < 0) return;
-        const size_t slot = level_slot(a.lt, bh, level, ktok, false);
+        const size_t slot = (size_t)(slot0 + ktok);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
             store4<T>((S*)a.part_dk + slot * D + 16 * dt + 4 * g, akT[dt] * a.tau);
@@ -581,7 +581,8 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
         tv[dt] = avT[dt] + tv[dt];
     }
     if (ktok < 0) return;
-    unsigned lmask = MODE == kLeaf ? leaf_levels(a.lt, tile / a.lt.per_leaf, false) : 0u;
+    const int leaf = tile / a.lt.per_leaf;
+    unsigned lmask = MODE == kLeaf ? leaf_levels(a.lt, leaf, false) : 0u;
     while (lmask) {
         const S* sk_[2];
         const S* sv_[2];
@@ -594,7 +595,7 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
             if (use[j]) {
                 const int l = __builtin_ctz(lmask);
                 lmask &= lmask - 1;
-                const size_t slot = level_slot(a.lt, bh, l, ktok, false);
+                const size_t slot = (size_t)(seg_slot_base(a.lt, bh, l, leaf >> (a.Lv - l), false) + ktok);
                 sk_[j] = (const S*)a.part_dk + slot * D;
                 sv_[j] = (const S*)a.part_dv + slot * D;
             }
@@ -739,7 +740,9 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
     // ---- block id -> head and the sorted positions [p0, p0 + nv) of its lists
     struct Blk {
         size_t bh;
-        int level, nv;
+        int nv;
+        int64_t qslot, kslot;                        // levels: partial rows of token t at qslot + t (as a
+                                                     // query) and kslot + t (as a key)
         const int32_t* ql;
         const int32_t* kl;
     };
@@ -750,15 +753,19 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
         if (MODE == kLevels) {
             // (whole-block levels are never padded: N / 2 entries per level)
             const int per_level = (N / 2) / BQ;
-            k.level = x / per_level;
-            const int t = x - k.level * per_level;
-            const size_t base = k.bh * (size_t)a.lt.off[a.Lv] + (size_t)a.lt.off[k.level] + (size_t)t * BQ;
+            const int level = x / per_level;
+            const int t = x - level * per_level;
+            const size_t base = k.bh * (size_t)a.lt.off[a.Lv] + (size_t)a.lt.off[level] + (size_t)t * BQ;
             k.ql = a.perm_q + base;
             k.kl = a.perm_k + base;
             k.nv = BQ;
+            // a block never straddles a segment (the half length is a multiple of BQ)
+            const int seg = t * BQ / a.lt.len[level + 1];
+            k.qslot = seg_slot_base(a.lt, k.bh, level, seg, true);
+            k.kslot = seg_slot_base(a.lt, k.bh, level, seg, false);
         } else {
             const int p0 = x * BQ;
-            k.level = 0;
+            k.qslot = k.kslot = 0;
             k.ql = a.perm_q + k.bh * N + p0;
             k.kl = a.perm_k + k.bh * N + p0;
             k.nv = min(BQ, N - p0);
@@ -828,13 +835,13 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
 
     // dK, dV of a lane's key: rows d = 16 dt + 4 g + i of the accumulators
     f32x4 akT[DT], avT[DT];
-    auto store_dkv = [&](size_t bh, int level, int ktok) {
+    auto store_dkv = [&](size_t bh, int64_t kslot, int ktok) {
         if (MODE == kLevels) {
             if (!(kFull || ktok >= 0)) return;
+            const size_t slot = (size_t)(kslot + ktok);
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) {
                 const int d0 = 16 * dt + 4 * g;
-                const size_t slot = level_slot(a.lt, bh, level, ktok, false);
                 store4<T>((S*)a.part_dk + slot * D + d0, akT[dt] * a.tau);
                 store4<T>((S*)a.part_dv + slot * D + d0, avT[dt]);
             }
@@ -869,12 +876,13 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
     // a block's dK, dV leave once the next block's rows are in LDS (so no
     // wait for those rows also waits for the stores): the previous block
     size_t prev_bh = 0;
-    int prev_level = 0, prev_ktok = -1;
+    int64_t prev_kslot = 0;
+    int prev_ktok = -1;
     bool first = true;
     for (;;) {
         lanes();
         const size_t bh = blk.bh;
-        const int level = blk.level;
+        const int64_t qslot = blk.qslot, kslot = blk.kslot;
         const int ktok = ix.ktok;
         if (!first) __syncthreads();                     // the previous block's dQ phase is done with LDS
 #pragma unroll
@@ -900,7 +908,7 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
             }
             __syncthreads();
             if (qt == 0) {                               // the previous block's dK, dV leave now
-                if (!first) store_dkv(prev_bh, prev_level, prev_ktok);
+                if (!first) store_dkv(prev_bh, prev_kslot, prev_ktok);
                 first = false;
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt) { akT[dt] = f32x4{0, 0, 0, 0}; avT[dt] = f32x4{0, 0, 0, 0}; }
@@ -993,7 +1001,7 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
                 const int d0 = 16 * dt + 4 * g;
                 if (MODE == kLevels) {
                     if (!kFull && qtok < 0) continue;
-                    S* out = (S*)a.part_dq + level_slot(a.lt, bh, level, qtok, true) * D + d0;
+                    S* out = (S*)a.part_dq + (size_t)(qslot + qtok) * D + d0;
                     store4<T>(out, dq[u] * a.tau);
                 } else {
                     // the low-rank part is a product across the wave's lanes:
@@ -1009,7 +1017,7 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
         }
 
         prev_bh = bh;
-        prev_level = level;
+        prev_kslot = kslot;
         prev_ktok = ktok;
         if (!has_next) break;
         qload(nblk.bh, nix, 0);                          // the next block's first Q / dO tile
@@ -1017,7 +1025,7 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
         blk = nblk;
         ix = nix;
     }
-    store_dkv(prev_bh, prev_level, prev_ktok);
+    store_dkv(prev_bh, prev_kslot, prev_ktok);
 }
 
 // Whole-block launch: as many workgroups as the device runs at once (cached
