@@ -140,7 +140,7 @@ def source_digest(names) -> str:
 
 
 KERNEL_SOURCES = {
-    "project": ["select.hip", "common.hpp"], "sort": ["select.hip"],
+    "project": ["select.hip", "common.hpp"], "sort": ["select.hip", "causal.hpp"],
     "race_state_fwd": ["race_fwd.hip", "race_common.hpp", "common.hpp"],
     "race_state_bwd": ["race_fwd.hip", "race_common.hpp", "common.hpp"],
     "race_scan_fwd": ["race_fwd.hip"], "race_scan_bwd": ["race_fwd.hip"],
@@ -160,8 +160,8 @@ def sources_of(kernel: str):
     if kernel in KERNEL_SOURCES:
         return KERNEL_SOURCES[kernel]
     if kernel.startswith("sparse_fwd"):
-        return ["sparse_fwd.hip", "tile.hpp", "common.hpp"]
-    return ["sparse_bwd.hip", "tile.hpp", "common.hpp"]
+        return ["sparse_fwd.hip", "tile.hpp", "causal.hpp", "internal.hpp", "common.hpp"]
+    return ["sparse_bwd.hip", "tile.hpp", "causal.hpp", "internal.hpp", "common.hpp"]
 
 
 def read_traffic(kernel: str, workload: str):
