@@ -60,13 +60,12 @@ struct Lb2Smem {
     using S = typename T::store_t;
     S vr[kC][D + kPad];            // V chunk, rows
     S dnt[D][kC + kPad];           // dNum / L chunk, transposed
-    S pq[kC][RP + kPad];           // Phi_Q chunk, rows (Phi_Q^T operands: transposed LDS reads)
+    S pqt[RP][kC + kPad];          // Phi_Q transposed
     S ggt[kC][kC + kPad];          // G'[j][i] / L, i >= j
     float ts[kC][RP / 4];          // tanh(W k) of the chunk's keys
     S du[kC][w_kdim<RP>() + kPad];
-    float dden[kC];                // dDen / L of the chunk's queries
+    float dden[kC];
     float a_state[RP];             // dA = (1/L) sum phi(q) dDen of the queries after the chunk
-                                   // (rows of feature tile ft are read and written by wave ft % 4 only)
 };
 
 template <class T, int D, int RP>
@@ -289,7 +288,6 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
 
     for (int it = threadIdx.x; it < kC * (w_kdim<RP>() + kPad); it += kThreads)
         (&sm.du[0][0])[it] = T::store(0.f);
-    // dS'[d][f] of the wave's feature tiles, laid out as in LB1; dA in LDS
     f32x4 St_[NFT][DT];
     const float* st_in = a.states + (bh * a.nseg + seg) * (size_t)(RP * D + RP);
     for (int f = threadIdx.x; f < RP; f += kThreads) sm.a_state[f] = st_in[RP * D + f];
@@ -319,10 +317,10 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
         const bool in = threadIdx.x < kC && t0 + (int)threadIdx.x < a.N;
         const float ddv = in ? dden[t0 + threadIdx.x] : 0.f;
         features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, nullptr, nullptr, sm.ts);
-        if (a.causal) features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, sm.pq, nullptr, nullptr);
+        if (a.causal) features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, nullptr, sm.pqt, nullptr);
         svr.store(sm.vr, false);
         if (a.causal) sdn.store(sm.dnt, true);
-        if (threadIdx.x < kC) sm.dden[threadIdx.x] = ddv * a.inv_L;
+        if (threadIdx.x < kC) sm.dden[threadIdx.x] = ddv;
         __syncthreads();
         {
             // previous chunk's projections (unconditional: chunk 0 reloads its own)
@@ -347,7 +345,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
                 const f32x4 dd = *(const f32x4*)&sm.dden[16 * it + 4 * g];
                 f32x4 v;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) v[i] = 16 * it + 4 * g + i >= kj ? acc[i] + dd[i] : 0.f;
+                for (int i = 0; i < 4; ++i) v[i] = 16 * it + 4 * g + i >= kj ? acc[i] + dd[i] * a.inv_L : 0.f;
                 store4<T>(&sm.ggt[kj][16 * it + 4 * g], v);
             }
         }
@@ -385,7 +383,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
                 if (a.causal) {
 #pragma unroll
                     for (int kk = 0; kk < 2; ++kk)
-                        acc[kt] = T::mma(phi_t8<T, RP>(sm.pq, 32 * kk, 16 * ft),
+                        acc[kt] = T::mma(T::ld8(&sm.pqt[16 * ft + col][32 * kk + 8 * g]),
                                          T::ld8(&sm.ggt[16 * kt + col][32 * kk + 8 * g]), acc[kt]);
                 }
                 chain_rule_t<T, RP>(acc[kt], kt, ft, a.L, a.beta, sm.ts, sm.du);
@@ -394,27 +392,20 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
         __syncthreads();
         store_du<T, RP>(sm.du, du_out, t0, a.N);
         if (a.causal) {
-            // dS' += (dNum / L)' Phi_Q (chunk), dA += Phi_Q' (dDen / L) (one
-            // Phi_Q^T fragment each; the weights keep float32 accuracy)
+            // dS' += (dNum / L)' Phi_Q (chunk), dA += (1/L) Phi_Q' dDen
 #pragma unroll
             for (int j = 0; j < NFT; ++j) {
                 const int ft = w + 4 * j;
                 if (ft >= FT) break;
-                f32x4 asum = {0, 0, 0, 0};
 #pragma unroll
                 for (int kk = 0; kk < 2; ++kk) {
-                    const F bf = phi_t8<T, RP>(sm.pq, 32 * kk, 16 * ft);
+                    const F bf = T::ld8(&sm.pqt[16 * ft + col][32 * kk + 8 * g]);
 #pragma unroll
                     for (int dt = 0; dt < DT; ++dt)
                         St_[j][dt] = T::mma(T::ld8(&sm.dnt[16 * dt + col][32 * kk + 8 * g]), bf, St_[j][dt]);
-                    asum = token_sums<T>(bf, sm.dden, 32 * kk, asum);
                 }
-                // every column holds the sums; column 0 adds them (this
-                // wave's rows; read again after the next chunk's barriers)
-                if (col == 0)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) sm.a_state[16 * ft + 4 * g + i] += asum[i];
             }
+            add_chunk_sums<T, RP>(sm.pqt, sm.dden, a.inv_L, sm.a_state);
         }
     }
 }

@@ -81,6 +81,32 @@ __device__ __forceinline__ f32x4 token_sums(typename T::frag_t phit, const float
     return mma_split<T>(phit, v, acc);
 }
 
+// a_state[f] += scale * sum over the chunk's tokens k of xt[f][k] (* wk[k] when
+// wk is not null), xt a transposed feature tile [RP][kC + kPad]; all threads,
+// 256 / RP per feature (16-byte LDS reads, then a lane reduction).
+template <class T, int RP>
+__device__ __forceinline__ void add_chunk_sums(const typename T::store_t (*xt)[kC + kPad], const float* wk,
+                                               float scale, float* a_state)
+{
+    constexpr int TPF = RP >= kThreads ? 1 : kThreads / RP;   // threads per feature
+    constexpr int PER = kC / TPF;                               // tokens per thread
+    static_assert(PER % 8 == 0, "chunk split");
+    for (int f0 = 0; f0 < RP; f0 += kThreads / TPF) {
+        const int f = f0 + (int)threadIdx.x / TPF, part = threadIdx.x % TPF;
+        float s = 0.f;
+#pragma unroll
+        for (int k8 = 0; k8 < PER; k8 += 8) {
+            const int k = part * PER + k8;
+            const auto v = T::ld8(&xt[f][k]);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) s += wk ? (float)v[j] * wk[k + j] : (float)v[j];
+        }
+#pragma unroll
+        for (int m = 1; m < TPF; m <<= 1) s += __shfl_xor(s, m);
+        if (part == 0) a_state[f] += s * scale;
+    }
+}
+
 // projection count padded to whole 32-wide k-steps (backward du x W)
 template <int RP> constexpr int w_kdim() { return RP / 4 < 32 ? 32 : RP / 4; }
 

@@ -31,8 +31,9 @@ template <class T, int D, int RP>
 struct StateSmem {
     using S = typename T::store_t;
     S vt[D][kC + kPad];
-    S ph[kC][RP + kPad];          // features, rows (their transpose is read with transposed LDS reads)
+    S pht[RP][kC + kPad];
     float aw[kC];
+    float a_state[RP];
 };
 
 template <class T, int D, int RP>
@@ -69,21 +70,15 @@ __global__ __launch_bounds__(kThreads) void race_state_kernel(StateArgs a)
     const St* Vl = (const St*)a.Val + bh * a.N * D;
     const float* vs = a.vscale ? a.vscale + bh * a.N : nullptr;
     const float* aw = a.aw ? a.aw + bh * a.N : nullptr;
-    // w wave-uniform (scalar): MFMAs under a condition on w are then skipped by
-    // a scalar branch; matrix instructions ignore the EXEC mask
     const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
     const int g = lane >> 4, col = lane & 15;
 
+    for (int f = threadIdx.x; f < RP; f += kThreads) sm.a_state[f] = 0.f;
     f32x4 S[RP / 16][DW];
 #pragma unroll
     for (int ft = 0; ft < RP / 16; ++ft)
 #pragma unroll
         for (int j = 0; j < DW; ++j) S[ft][j] = f32x4{0, 0, 0, 0};
-    // A on the matrix cores: wave w sums the feature tiles ft = w, w + 4, ...
-    constexpr int FT = RP / 16, NFA = (FT + 3) / 4;
-    f32x4 Aacc[NFA];
-#pragma unroll
-    for (int j = 0; j < NFA; ++j) Aacc[j] = f32x4{0, 0, 0, 0};
 
     const int t_beg = seg * a.seg_len, t_end = min(a.N, t_beg + a.seg_len);
     // projections, value rows and A weights of the chunk, loaded one chunk ahead
@@ -101,24 +96,29 @@ __global__ __launch_bounds__(kThreads) void race_state_kernel(StateArgs a)
         __syncthreads();
         vr.store(sm.vt, vs != nullptr);
         if (threadIdx.x < kC) sm.aw[threadIdx.x] = t0 + (int)threadIdx.x < a.N ? awv : 0.f;
-        features_from<T, RP>(ur, t0, a.N, a.L, a.two_beta, sm.ph, nullptr, nullptr);
+        features_from<T, RP>(ur, t0, a.N, a.L, a.two_beta, nullptr, sm.pht, nullptr);
         __syncthreads();
         load_chunk(t0 + kC < t_end ? t0 + kC : t0);   // the last chunk reloads its own (unconditional loads)
-        // S[f][cols of wave] += Phi'[f][rows] V[rows][cols];  A[f] += Phi'[f][rows] aw[rows]
+        // S[f][cols of wave] += Phi'[f][rows] V[rows][cols]
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
             typename T::frag_t bv[DW];
 #pragma unroll
             for (int j = 0; j < DW; ++j) bv[j] = T::ld8(&sm.vt[16 * (w * DW + j) + col][32 * kk + 8 * g]);
 #pragma unroll
-            for (int ft = 0; ft < FT; ++ft) {
-                const auto af = phi_t8<T, RP>(sm.ph, 32 * kk, 16 * ft);
+            for (int ft = 0; ft < RP / 16; ++ft) {
+                const auto af = T::ld8(&sm.pht[16 * ft + col][32 * kk + 8 * g]);
 #pragma unroll
                 for (int j = 0; j < DW; ++j) S[ft][j] = T::mma(af, bv[j], S[ft][j]);
-                if (ft % 4 == w) Aacc[ft / 4] = token_sums<T>(af, aw ? sm.aw : nullptr, 32 * kk, Aacc[ft / 4]);
             }
         }
+        for (int f = threadIdx.x; f < RP; f += kThreads) {
+            float s = 0.f;
+            for (int k = 0; k < kC; ++k) s += T::load(sm.pht[f][k]) * sm.aw[k];
+            sm.a_state[f] += s;
+        }
     }
+    __syncthreads();
     float* out = a.states + (bh * a.nseg + seg) * (size_t)(RP * D + RP);
 #pragma unroll
     for (int ft = 0; ft < RP / 16; ++ft)
@@ -127,14 +127,7 @@ __global__ __launch_bounds__(kThreads) void race_state_kernel(StateArgs a)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
                 out[(size_t)(16 * ft + 4 * g + i) * D + 16 * (w * DW + j) + col] = S[ft][j][i] * a.mul;
-    // column 0 of the A tiles: lanes (g, 0) hold features 16 ft + 4 g + i
-#pragma unroll
-    for (int j = 0; j < NFA; ++j) {
-        const int ft = w + 4 * j;
-        if (ft < FT && col == 0)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) out[RP * D + 16 * ft + 4 * g + i] = Aacc[j][i] * a.mul;
-    }
+    for (int f = threadIdx.x; f < RP; f += kThreads) out[RP * D + f] = sm.a_state[f] * a.mul;
 }
 
 // mode 0: total in every segment; 1: exclusive prefix; 2: exclusive suffix.
