@@ -272,6 +272,9 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
             TD::load(V, tok, rv);
             if (t + 2 < ntiles) tokens(k0 + 2 * kT, tok);
         }
+        // a key tile every lane sees whole skips the mask (one wave vote)
+        const bool full = __all(qtok >= 0 && k0 + kT <= kend &&
+                                (MODE == kLeaf ? k0 + kT - 1 <= qtok : (k0 >= blk_lo && k0 + kT <= blk_hi)));
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
             float v8[8];
@@ -285,14 +288,20 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
                     st = T::mma(TD::row8(sk, kr, 32 * ks + 8 * g), qf[ks], st);
                     dp = T::mma(TD::row8(sv, kr, 32 * ks + 8 * g), df[ks], dp);
                 }
+                if (full) {
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int p = k0 + key_of(s, g, i);
-                    bool ok = p < kend && qtok >= 0;
-                    if (MODE == kLeaf) ok = ok && p <= qtok;
-                    else ok = ok && p >= blk_lo && p < blk_hi;
-                    const float P = ok ? fast_exp2(st[i] * a.tau2 - lse2) : 0.f;
-                    v8[4 * h2 + i] = P * (scs * dp[i] - delta);
+                    for (int i = 0; i < 4; ++i)
+                        v8[4 * h2 + i] = fast_exp2(fmaf(st[i], a.tau2, -lse2)) * fmaf(scs, dp[i], -delta);
+                } else {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int p = k0 + key_of(s, g, i);
+                        bool ok = p < kend && qtok >= 0;
+                        if (MODE == kLeaf) ok = ok && p <= qtok;
+                        else ok = ok && p >= blk_lo && p < blk_hi;
+                        const float P = ok ? fast_exp2(fmaf(st[i], a.tau2, -lse2)) : 0.f;
+                        v8[4 * h2 + i] = P * fmaf(scs, dp[i], -delta);
+                    }
                 }
             }
             const F bf = T::pack(v8);
@@ -512,6 +521,10 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
             qt_cur = qt_next;
             if (t + 2 < ntiles) tokens(q0 + 2 * kT, tok, qt_next);
         }
+        // a query tile every lane's key sees whole skips the mask (one wave
+        // vote; the query lists of a padded recursion may hold zero tokens)
+        const bool full = __all(ktok >= 0 && q0 + kT <= qend && !(MODE == kLevels && a.lt.padded) &&
+                                (MODE == kLeaf ? q0 >= ktok : (q0 >= blk_lo && q0 + kT <= blk_hi)));
         F pf[2], zf[2];
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
@@ -529,14 +542,17 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int ql = key_of(s, g, i);
-                    const int p = q0 + ql;
-                    bool ok = ktok >= 0 && s_ok[ql];
-                    if (MODE == kLeaf) ok = ok && p >= ktok;
-                    else ok = ok && p >= blk_lo && p < blk_hi;
-                    const float P = ok ? fast_exp2(st[i] * a.tau2 - s_l2[ql]) : 0.f;
+                    float P = fast_exp2(fmaf(st[i], a.tau2, -s_l2[ql]));
+                    if (!full) {
+                        const int p = q0 + ql;
+                        bool ok = ktok >= 0 && s_ok[ql];
+                        if (MODE == kLeaf) ok = ok && p >= ktok;
+                        else ok = ok && p >= blk_lo && p < blk_hi;
+                        P = ok ? P : 0.f;
+                    }
                     const float c = s_sc[ql];
                     p8[4 * h2 + i] = P * c;
-                    z8[4 * h2 + i] = P * (c * dp[i] - s_de[ql]);
+                    z8[4 * h2 + i] = P * fmaf(c, dp[i], -s_de[ql]);
                 }
             }
             pf[kk] = T::pack(p8);

@@ -178,21 +178,32 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
             for (int ks = 0; ks < KS; ++ks)
                 st[s] = T::mma(Tl::row8(sk, kr, 32 * ks + 8 * g), qf[ks], st[s]);
         }
-        // scale to log2 units and mask
+        // mask (masked scores -> -inf), running max in log2 units.  A tile
+        // that every lane of the wave sees whole (all but the diagonal tile
+        // of a causal leaf and ragged ends) skips the mask: one wave vote.
+        const bool lane_full = qtok >= 0 && k0 + kKT <= kend &&
+                               (MODE == kLeaf ? k0 + kKT - 1 <= qtok : (k0 >= blk_lo && k0 + kKT <= blk_hi));
         float tmax = -INFINITY;
+        if (__all(lane_full)) {
 #pragma unroll
-        for (int s = 0; s < 4; ++s)
+            for (int s = 0; s < 4; ++s)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int p = k0 + key_of(s, g, i);
-                bool ok = p < kend && qtok >= 0;
-                if (MODE == kLeaf) ok = ok && p <= qtok;
-                else ok = ok && p >= blk_lo && p < blk_hi;
-                const float v = ok ? st[s][i] * a.tau2 : -INFINITY;
-                st[s][i] = v;
-                tmax = fmaxf(tmax, v);
-            }
-        tmax = wave_max16(tmax);
+                for (int i = 0; i < 4; ++i) tmax = fmaxf(tmax, st[s][i]);
+        } else {
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int p = k0 + key_of(s, g, i);
+                    bool ok = p < kend && qtok >= 0;
+                    if (MODE == kLeaf) ok = ok && p <= qtok;
+                    else ok = ok && p >= blk_lo && p < blk_hi;
+                    const float v = ok ? st[s][i] : -INFINITY;
+                    st[s][i] = v;
+                    tmax = fmaxf(tmax, v);
+                }
+        }
+        tmax = wave_max16(tmax) * a.tau2;            // tau2 > 0: the max of the scaled scores
         const float m_new = fmaxf(m_run, tmax);
         const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
         const float corr = fast_exp2(m_run - m_use);
@@ -201,15 +212,19 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
         for (int s = 0; s < 4; ++s)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const float p = fast_exp2(st[s][i] - m_use);
+                const float p = fast_exp2(fmaf(st[s][i], a.tau2, -m_use));
                 st[s][i] = p;
                 psum += p;
             }
         psum = wave_sum16(psum);
         l_run = l_run * corr + psum;
-        m_run = m_new;
+        // the output is rescaled only when some lane's running max moved
+        // (corr = 1 otherwise; a lane still at -inf has a zero accumulator)
+        if (__any(m_new != m_run)) {
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) acc[dt] *= corr;
+            for (int dt = 0; dt < DT; ++dt) acc[dt] *= corr;
+        }
+        m_run = m_new;
         // O^T += V^T P^T over two 32-key k-steps
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
