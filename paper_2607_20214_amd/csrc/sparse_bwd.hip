@@ -388,6 +388,7 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
     constexpr int PT = TD::PER_THREAD;
     S* const sq = (S*)smem;
     S* const so = sq + TD::elems(kT);
+    static_assert(TD::elems(kT) * T::bytes % 16 == 0, "row scalars 16-byte aligned");
     float* const s_l2 = (float*)(so + TD::elems(kT));
     float* const s_de = s_l2 + kT;
     float* const s_sc = s_de + kT;
@@ -539,20 +540,22 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
                     st = T::mma(TD::row8(sq, qr, 32 * ks + 8 * g), kf[ks], st);
                     dp = T::mma(TD::row8(so, qr, 32 * ks + 8 * g), vf[ks], dp);
                 }
+                // this lane's four queries are consecutive: one 16-byte read per scalar
+                const int q4 = key_of(s, g, 0);
+                const f32x4 l2v = *(const f32x4*)&s_l2[q4], scv = *(const f32x4*)&s_sc[q4],
+                            dev = *(const f32x4*)&s_de[q4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int ql = key_of(s, g, i);
-                    float P = fast_exp2(fmaf(st[i], a.tau2, -s_l2[ql]));
+                    float P = fast_exp2(fmaf(st[i], a.tau2, -l2v[i]));
                     if (!full) {
-                        const int p = q0 + ql;
-                        bool ok = ktok >= 0 && s_ok[ql];
+                        const int p = q0 + q4 + i;
+                        bool ok = ktok >= 0 && s_ok[q4 + i];
                         if (MODE == kLeaf) ok = ok && p >= ktok;
                         else ok = ok && p >= blk_lo && p < blk_hi;
                         P = ok ? P : 0.f;
                     }
-                    const float c = s_sc[ql];
-                    p8[4 * h2 + i] = P * c;
-                    z8[4 * h2 + i] = P * fmaf(c, dp[i], -s_de[ql]);
+                    p8[4 * h2 + i] = P * scv[i];
+                    z8[4 * h2 + i] = P * fmaf(scv[i], dp[i], -dev[i]);
                 }
             }
             pf[kk] = T::pack(p8);
@@ -732,8 +735,8 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
     static_assert(TS::elems(BQ) <= 2 * TD::elems(64), "dS^T fits in the query tiles");
     __shared__ __attribute__((aligned(16))) S sk[TD::elems(BQ)];
     __shared__ __attribute__((aligned(16))) S sqo[2 * TD::elems(64)];   // Q tile, dO tile; later dS^T
-    __shared__ float s_l2[64], s_de[64], s_sc[64];
-    __shared__ int s_qt[64];
+    __shared__ __attribute__((aligned(16))) float s_l2[64], s_de[64], s_sc[64];
+    __shared__ __attribute__((aligned(16))) int s_qt[64];
     S* const sq = sqo;
     S* const so = sqo + TD::elems(64);
     S* const sds = sqo;
@@ -952,14 +955,16 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
                         st = T::mma(TD::row8(sq, qr, 32 * ks + 8 * g), TD::row8(sk, kloc, 32 * ks + 8 * g), st);
                         dp = T::mma(TD::row8(so, qr, 32 * ks + 8 * g), vf[ks], dp);
                     }
+                    // this lane's four queries are consecutive: 16-byte scalar reads
+                    const int q4 = key_of(s, g, 0);
+                    const f32x4 l2v = *(const f32x4*)&s_l2[q4], scv = *(const f32x4*)&s_sc[q4],
+                                dev = *(const f32x4*)&s_de[q4];
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        const int q = key_of(s, g, i);
-                        const bool ok = kFull || (ktok >= 0 && s_qt[q] >= 0);
-                        const float P = ok ? fast_exp2(st[i] * a.tau2 - s_l2[q]) : 0.f;
-                        const float c = s_sc[q];
-                        p8[4 * h2 + i] = P * c;
-                        z8[4 * h2 + i] = P * (c * dp[i] - s_de[q]);
+                        const bool ok = kFull || (ktok >= 0 && s_qt[q4 + i] >= 0);
+                        const float P = ok ? fast_exp2(fmaf(st[i], a.tau2, -l2v[i])) : 0.f;
+                        p8[4 * h2 + i] = P * scv[i];
+                        z8[4 * h2 + i] = P * fmaf(scv[i], dp[i], -dev[i]);
                     }
                 }
                 pf[kk] = T::pack(p8);
