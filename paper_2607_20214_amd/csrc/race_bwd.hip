@@ -80,18 +80,22 @@ struct Lb3Smem {
 template <class T, int D, int RP>
 constexpr bool bwd_fits()
 {
-    return sizeof(Lb1Smem<T, D, RP>) <= kMaxLds && sizeof(Lb2Smem<T, D, RP>) <= kMaxLds &&
+    return sizeof(Lb1Smem<T, D, RP / table_split<RP>()>) <= kMaxLds &&
+           sizeof(Lb2Smem<T, D, RP / table_split<RP>()>) <= kMaxLds &&
            sizeof(Lb3Smem<T, D, RP>) <= kMaxLds;
 }
 
 // du rows [t0, t0 + 64) of the chunk (LDS, storage dtype) -> rows of out
 // [N][WK], 16 bytes per thread and store.
-template <class T, int RP>
-__device__ __forceinline__ void store_du(const typename T::store_t (*du)[w_kdim<RP>() + kPad],
+template <class T, int RPW, int RP>
+__device__ __forceinline__ void store_du(const typename T::store_t (*du)[w_kdim<RPW>() + kPad],
                                          typename T::store_t* out, int t0, int N)
 {
-    constexpr int WK = w_kdim<RP>(), PER = 16 / T::bytes, CH = WK / PER;
-    static_assert(WK % PER == 0, "du row of whole 16-byte pieces");
+    // a workgroup holding all the features writes whole (padded) rows,
+    // one holding some of the tables their RPW / 4 columns
+    constexpr int WK = w_kdim<RP>(), COLS = RPW == RP ? WK : RPW / 4;
+    constexpr int PER = 16 / T::bytes, CH = COLS / PER;
+    static_assert(COLS % PER == 0, "du row of whole 16-byte pieces");
     for (int it = threadIdx.x; it < kC * CH; it += kThreads) {
         const int r = it / CH, c = it % CH;
         if (t0 + r < N) stg16(out + (size_t)(t0 + r) * WK + c * PER, *(const uint4*)&du[r][c * PER]);
@@ -119,21 +123,23 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
 {
     using St = typename T::store_t;
     using F = typename T::frag_t;
-    constexpr int DT = D / 16, KS = D / 32, FT = RP / 16, NFT = (FT + 3) / 4;
-    __shared__ Lb1Smem<T, D, RP> sm;
-    const int seg = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+    constexpr int SPLIT = table_split<RP>(), RPW = RP / SPLIT;   // features of this workgroup
+    constexpr int DT = D / 16, KS = D / 32, FT = RPW / 16, NFT = (FT + 3) / 4;
+    __shared__ Lb1Smem<T, D, RPW> sm;
+    const int seg = blockIdx.x / SPLIT, part = blockIdx.x % SPLIT, h = blockIdx.y, b = blockIdx.z;
+    const int F0 = part * RPW, L = a.L - F0 / 16;                  // first feature; tables from here on
     const size_t bh = (size_t)b * a.H + h;
-    const float* Uq = a.Uq + bh * a.N * (RP / 4);
-    const float* Uk = a.Uk + bh * a.N * (RP / 4);
+    const float* Uq = a.Uq + bh * a.N * (RP / 4) + F0 / 4;
+    const float* Uk = a.Uk + bh * a.N * (RP / 4) + F0 / 4;
     const St* V = (const St*)a.V + bh * a.N * D;
     const St* dO = (const St*)a.dO + bh * a.N * D;
     const float* sclr = a.rs + 3 * a.BHN + bh * a.N;
     const float* dden = a.rs + 4 * a.BHN + bh * a.N;
-    St* du_out = (St*)a.out + bh * a.N * w_kdim<RP>();
+    St* du_out = (St*)a.out + bh * a.N * w_kdim<RP>() + F0 / 4;
     const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
     const int g = lane >> 4, col = lane & 15;
 
-    for (int it = threadIdx.x; it < kC * (w_kdim<RP>() + kPad); it += kThreads)
+    for (int it = threadIdx.x; it < kC * (w_kdim<RPW>() + kPad); it += kThreads)
         (&sm.du[0][0])[it] = T::store(0.f);
     // state S'[d][f] for the wave's features f = 16 (w + 4j) + col, and
     // A[f] of the same feature tiles (lane (g, col) register i: feature
@@ -147,15 +153,15 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
         for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                St_[j][dt][i] = ft < FT ? st_in[(size_t)(16 * ft + col) * D + 16 * dt + 4 * g + i] : 0.f;
+                St_[j][dt][i] = ft < FT ? st_in[(size_t)(F0 + 16 * ft + col) * D + 16 * dt + 4 * g + i] : 0.f;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) Aacc[j][i] = ft < FT ? st_in[RP * D + 16 * ft + 4 * g + i] : 0.f;
+        for (int i = 0; i < 4; ++i) Aacc[j][i] = ft < FT ? st_in[RP * D + F0 + 16 * ft + 4 * g + i] : 0.f;
     }
 
     const int t_beg = seg * a.seg_len, t_end = min(a.N, t_beg + a.seg_len);
-    URegs<RP> uq, uk;                    // projections of the chunk, loaded one chunk ahead
-    uq.load(Uq, t_beg, a.N);
-    if (a.causal) uk.load(Uk, t_beg, a.N);
+    URegs<RPW> uq, uk;                    // projections of the chunk, loaded one chunk ahead
+    uq.load(Uq, t_beg, a.N, RP / 4);
+    if (a.causal) uk.load(Uk, t_beg, a.N, RP / 4);
     for (int t0 = t_beg; t0 < t_end; t0 += kC) {
         __syncthreads();
         // every global load of the chunk is issued first; the features (vector
@@ -166,8 +172,8 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
         if (a.causal) svt.load(V, t0, a.N, nullptr, 1.f);
         const bool in = threadIdx.x < kC && t0 + (int)threadIdx.x < a.N;
         const float ddv = in ? dden[t0 + threadIdx.x] : 0.f, scv = in ? sclr[t0 + threadIdx.x] : 0.f;
-        features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, nullptr, nullptr, sm.ts);
-        if (a.causal) features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, sm.pk, nullptr, nullptr);
+        features_from<T, RPW>(uq, t0, a.N, L, a.two_beta, nullptr, nullptr, sm.ts);
+        if (a.causal) features_from<T, RPW>(uk, t0, a.N, L, a.two_beta, sm.pk, nullptr, nullptr);
         sdn.store(sm.dn, false);
         if (a.causal) svt.store(sm.vt, false);
         if (threadIdx.x < kC) {
@@ -179,8 +185,8 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
             // next chunk's projections (the last chunk reloads its own, so
             // the loads are unconditional)
             const int tn = t0 + kC < t_end ? t0 + kC : t0;
-            uq.load(Uq, tn, a.N);
-            if (a.causal) uk.load(Uk, tn, a.N);
+            uq.load(Uq, tn, a.N, RP / 4);
+            if (a.causal) uk.load(Uk, tn, a.N, RP / 4);
         }
         if (a.causal) {
             // G rows [16w, 16w + 16): sc_lr,i <dO_i, V_j> + dDen_i for j <= i,
@@ -238,15 +244,15 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
                 if (a.causal) {
 #pragma unroll
                     for (int kk = 0; kk < 2; ++kk)
-                        acc[qt] = T::mma(phi_t8<T, RP>(sm.pk, 32 * kk, 16 * ft),
+                        acc[qt] = T::mma(phi_t8<T, RPW>(sm.pk, 32 * kk, 16 * ft),
                                          T::ld8(&sm.gg[16 * qt + col][32 * kk + 8 * g]), acc[qt]);
                 }
                 acc[qt] *= a.inv_L;
-                chain_rule_t<T, RP>(acc[qt], qt, ft, a.L, a.beta, sm.ts, sm.du);
+                chain_rule_t<T, RPW>(acc[qt], qt, ft, L, a.beta, sm.ts, sm.du);
             }
         }
         __syncthreads();
-        store_du<T, RP>(sm.du, du_out, t0, a.N);
+        store_du<T, RPW, RP>(sm.du, du_out, t0, a.N);
         if (a.causal) {
             // S' += V' Phi_K (chunk), A += Phi_K' 1 (one Phi_K^T fragment each)
 #pragma unroll
@@ -255,7 +261,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
                 if (ft >= FT) break;
 #pragma unroll
                 for (int kk = 0; kk < 2; ++kk) {
-                    const F bf = phi_t8<T, RP>(sm.pk, 32 * kk, 16 * ft);
+                    const F bf = phi_t8<T, RPW>(sm.pk, 32 * kk, 16 * ft);
 #pragma unroll
                     for (int dt = 0; dt < DT; ++dt)
                         St_[j][dt] = T::mma(T::ld8(&sm.vt[16 * dt + col][32 * kk + 8 * g]), bf, St_[j][dt]);
@@ -272,25 +278,27 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
 {
     using St = typename T::store_t;
     using F = typename T::frag_t;
-    constexpr int DT = D / 16, KS = D / 32, FT = RP / 16, NFT = (FT + 3) / 4;
-    __shared__ Lb2Smem<T, D, RP> sm;
-    const int seg = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+    constexpr int SPLIT = table_split<RP>(), RPW = RP / SPLIT;   // features of this workgroup
+    constexpr int DT = D / 16, KS = D / 32, FT = RPW / 16, NFT = (FT + 3) / 4;
+    __shared__ Lb2Smem<T, D, RPW> sm;
+    const int seg = blockIdx.x / SPLIT, part = blockIdx.x % SPLIT, h = blockIdx.y, b = blockIdx.z;
+    const int F0 = part * RPW, L = a.L - F0 / 16;                  // first feature; tables from here on
     const size_t bh = (size_t)b * a.H + h;
-    const float* Uq = a.Uq + bh * a.N * (RP / 4);
-    const float* Uk = a.Uk + bh * a.N * (RP / 4);
+    const float* Uq = a.Uq + bh * a.N * (RP / 4) + F0 / 4;
+    const float* Uk = a.Uk + bh * a.N * (RP / 4) + F0 / 4;
     const St* V = (const St*)a.V + bh * a.N * D;
     const St* dO = (const St*)a.dO + bh * a.N * D;
     const float* sclr = a.rs + 3 * a.BHN + bh * a.N;
     const float* dden = a.rs + 4 * a.BHN + bh * a.N;
-    St* du_out = (St*)a.out + bh * a.N * w_kdim<RP>();
+    St* du_out = (St*)a.out + bh * a.N * w_kdim<RP>() + F0 / 4;
     const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
     const int g = lane >> 4, col = lane & 15;
 
-    for (int it = threadIdx.x; it < kC * (w_kdim<RP>() + kPad); it += kThreads)
+    for (int it = threadIdx.x; it < kC * (w_kdim<RPW>() + kPad); it += kThreads)
         (&sm.du[0][0])[it] = T::store(0.f);
     f32x4 St_[NFT][DT];
     const float* st_in = a.states + (bh * a.nseg + seg) * (size_t)(RP * D + RP);
-    for (int f = threadIdx.x; f < RP; f += kThreads) sm.a_state[f] = st_in[RP * D + f];
+    for (int f = threadIdx.x; f < RPW; f += kThreads) sm.a_state[f] = st_in[RP * D + F0 + f];
 #pragma unroll
     for (int j = 0; j < NFT; ++j) {
         const int ft = w + 4 * j;
@@ -298,14 +306,14 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
         for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                St_[j][dt][i] = ft < FT ? st_in[(size_t)(16 * ft + col) * D + 16 * dt + 4 * g + i] : 0.f;
+                St_[j][dt][i] = ft < FT ? st_in[(size_t)(F0 + 16 * ft + col) * D + 16 * dt + 4 * g + i] : 0.f;
     }
 
     const int t_beg = seg * a.seg_len, t_end = min(a.N, t_beg + a.seg_len);
     const int nch = (t_end - t_beg + kC - 1) / kC;
-    URegs<RP> uq, uk;                    // projections of the chunk, loaded one chunk ahead
-    uk.load(Uk, t_beg + (nch - 1) * kC, a.N);
-    if (a.causal) uq.load(Uq, t_beg + (nch - 1) * kC, a.N);
+    URegs<RPW> uq, uk;                    // projections of the chunk, loaded one chunk ahead
+    uk.load(Uk, t_beg + (nch - 1) * kC, a.N, RP / 4);
+    if (a.causal) uq.load(Uq, t_beg + (nch - 1) * kC, a.N, RP / 4);
     for (int c = nch - 1; c >= 0; --c) {
         const int t0 = t_beg + c * kC;
         __syncthreads();
@@ -316,8 +324,8 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
         if (a.causal) sdn.load(dO, t0, a.N, sclr, a.inv_L);
         const bool in = threadIdx.x < kC && t0 + (int)threadIdx.x < a.N;
         const float ddv = in ? dden[t0 + threadIdx.x] : 0.f;
-        features_from<T, RP>(uk, t0, a.N, a.L, a.two_beta, nullptr, nullptr, sm.ts);
-        if (a.causal) features_from<T, RP>(uq, t0, a.N, a.L, a.two_beta, nullptr, sm.pqt, nullptr);
+        features_from<T, RPW>(uk, t0, a.N, L, a.two_beta, nullptr, nullptr, sm.ts);
+        if (a.causal) features_from<T, RPW>(uq, t0, a.N, L, a.two_beta, nullptr, sm.pqt, nullptr);
         svr.store(sm.vr, false);
         if (a.causal) sdn.store(sm.dnt, true);
         if (threadIdx.x < kC) sm.dden[threadIdx.x] = ddv;
@@ -325,8 +333,8 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
         {
             // previous chunk's projections (unconditional: chunk 0 reloads its own)
             const int tn = c > 0 ? t0 - kC : t0;
-            uk.load(Uk, tn, a.N);
-            if (a.causal) uq.load(Uq, tn, a.N);
+            uk.load(Uk, tn, a.N, RP / 4);
+            if (a.causal) uq.load(Uq, tn, a.N, RP / 4);
         }
         if (a.causal) {
             // G' rows j in [16w, 16w + 16): (<V_j, dNum_i> + dDen_i) / L for
@@ -386,11 +394,11 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
                         acc[kt] = T::mma(T::ld8(&sm.pqt[16 * ft + col][32 * kk + 8 * g]),
                                          T::ld8(&sm.ggt[16 * kt + col][32 * kk + 8 * g]), acc[kt]);
                 }
-                chain_rule_t<T, RP>(acc[kt], kt, ft, a.L, a.beta, sm.ts, sm.du);
+                chain_rule_t<T, RPW>(acc[kt], kt, ft, L, a.beta, sm.ts, sm.du);
             }
         }
         __syncthreads();
-        store_du<T, RP>(sm.du, du_out, t0, a.N);
+        store_du<T, RPW, RP>(sm.du, du_out, t0, a.N);
         if (a.causal) {
             // dS' += (dNum / L)' Phi_Q (chunk), dA += (1/L) Phi_Q' dDen
 #pragma unroll
@@ -405,7 +413,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dk_kernel(LbArgs a)
                         St_[j][dt] = T::mma(T::ld8(&sm.dnt[16 * dt + col][32 * kk + 8 * g]), bf, St_[j][dt]);
                 }
             }
-            add_chunk_sums<T, RP>(sm.pqt, sm.dden, a.inv_L, sm.a_state);
+            add_chunk_sums<T, RPW>(sm.pqt, sm.dden, a.inv_L, sm.a_state);
         }
     }
 }
@@ -441,8 +449,8 @@ __global__ __launch_bounds__(kThreads, 2) void race_dv_kernel(LbArgs a)
     const int t_beg = seg * a.seg_len, t_end = min(a.N, t_beg + a.seg_len);
     const int nch = (t_end - t_beg + kC - 1) / kC;
     URegs<RP> uq, uk;                    // projections of the chunk, loaded one chunk ahead
-    uk.load(Uk, t_beg + (nch - 1) * kC, a.N);
-    if (a.causal) uq.load(Uq, t_beg + (nch - 1) * kC, a.N);
+    uk.load(Uk, t_beg + (nch - 1) * kC, a.N, RP / 4);
+    if (a.causal) uq.load(Uq, t_beg + (nch - 1) * kC, a.N, RP / 4);
     for (int c = nch - 1; c >= 0; --c) {
         const int t0 = t_beg + c * kC;
         __syncthreads();
@@ -458,8 +466,8 @@ __global__ __launch_bounds__(kThreads, 2) void race_dv_kernel(LbArgs a)
         {
             // previous chunk's projections (unconditional: chunk 0 reloads its own)
             const int tn = c > 0 ? t0 - kC : t0;
-            uk.load(Uk, tn, a.N);
-            if (a.causal) uq.load(Uq, tn, a.N);
+            uk.load(Uk, tn, a.N, RP / 4);
+            if (a.causal) uq.load(Uq, tn, a.N, RP / 4);
         }
         if (a.causal) {
             // M' rows j in [16w, 16w + 16): <phi(k_j), phi(q_i)> for i >= j,
@@ -552,11 +560,11 @@ struct BwdFn {
         if constexpr (!bwd_fits<T, D, RP>()) {
             return hipErrorInvalidConfiguration;
         } else {
-            dim3 grid(s.nseg, s.H, s.B);
-            ELSAA_LAUNCH("race_dq", (race_dq_kernel<T, D, RP>), grid, dim3(kThreads), 0, st, a1);
+            dim3 grid(s.nseg, s.H, s.B), grid_t(s.nseg * table_split<RP>(), s.H, s.B);
+            ELSAA_LAUNCH("race_dq", (race_dq_kernel<T, D, RP>), grid_t, dim3(kThreads), 0, st, a1);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
-            ELSAA_LAUNCH("race_dk", (race_dk_kernel<T, D, RP>), grid, dim3(kThreads), 0, st, a2);
+            ELSAA_LAUNCH("race_dk", (race_dk_kernel<T, D, RP>), grid_t, dim3(kThreads), 0, st, a2);
             if ((e = hipGetLastError()) != hipSuccess) return e;
             ELSAA_LAUNCH("race_dv", (race_dv_kernel<T, D, RP>), grid, dim3(kThreads), 0, st, a3);
             return hipGetLastError();

@@ -110,6 +110,13 @@ __device__ __forceinline__ void add_chunk_sums(const typename T::store_t (*xt)[k
 // projection count padded to whole 32-wide k-steps (backward du x W)
 template <int RP> constexpr int w_kdim() { return RP / 4 < 32 ? 32 : RP / 4; }
 
+// Workgroups per sequence segment in the passes whose feature tables are
+// independent (the state sums and the dQ / dK chain rules): each holds
+// RP / split consecutive features (whole tables), reads the same chunk rows
+// and writes its own state rows or du columns.  256 features split in two,
+// so a workgroup's registers and LDS are those of the 128-feature passes.
+template <int RP> constexpr int table_split() { return RP == 256 ? 2 : 1; }
+
 // Rows [t0, t0 + 64) of X (zero past N), each multiplied by scale[row] * mul
 // when scale != nullptr (by mul otherwise), into a transposed tile
 // xt[d][token].  load() issues every global load of the thread into
@@ -243,7 +250,9 @@ struct URegs {
     // Rows past N and tables past RP / 16 load clamped in-range values
     // (features_from zeroes those rows' features and skips those tables), so
     // the loads carry no per-lane branches.
-    __device__ __forceinline__ void load(const float* U, int t0, int N)
+    // stride: floats per projection row (RP / 4 unless this workgroup holds
+    // only some of the row's tables, U then pointing at its first table)
+    __device__ __forceinline__ void load(const float* U, int t0, int N, int stride = RP / 4)
     {
         const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
         const int g = lane >> 4, col = lane & 15;
@@ -251,7 +260,7 @@ struct URegs {
 #pragma unroll
         for (int m = 0; m < NU; ++m) {
             const int tb = min(g + 4 * m, RP / 16 - 1);
-            u[m] = *(const f32x4*)(U + (size_t)tok * (RP / 4) + 4 * tb);
+            u[m] = *(const f32x4*)(U + (size_t)tok * stride + 4 * tb);
         }
     }
 };

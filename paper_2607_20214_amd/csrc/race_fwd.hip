@@ -63,30 +63,32 @@ __global__ __launch_bounds__(kThreads) void race_state_kernel(StateArgs a)
 {
     using St = typename T::store_t;
     constexpr int DW = D / 64;
-    __shared__ StateSmem<T, D, RP> sm;
-    const int seg = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+    constexpr int SPLIT = table_split<RP>(), RPW = RP / SPLIT;   // features of this workgroup
+    __shared__ StateSmem<T, D, RPW> sm;
+    const int seg = blockIdx.x / SPLIT, part = blockIdx.x % SPLIT, h = blockIdx.y, b = blockIdx.z;
+    const int F0 = part * RPW, L = a.L - F0 / 16;                  // first feature; tables from here on
     const size_t bh = (size_t)b * a.H + h;
-    const float* U = a.U + bh * a.N * (RP / 4);
+    const float* U = a.U + bh * a.N * (RP / 4) + F0 / 4;
     const St* Vl = (const St*)a.Val + bh * a.N * D;
     const float* vs = a.vscale ? a.vscale + bh * a.N : nullptr;
     const float* aw = a.aw ? a.aw + bh * a.N : nullptr;
     const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
     const int g = lane >> 4, col = lane & 15;
 
-    for (int f = threadIdx.x; f < RP; f += kThreads) sm.a_state[f] = 0.f;
-    f32x4 S[RP / 16][DW];
+    for (int f = threadIdx.x; f < RPW; f += kThreads) sm.a_state[f] = 0.f;
+    f32x4 S[RPW / 16][DW];
 #pragma unroll
-    for (int ft = 0; ft < RP / 16; ++ft)
+    for (int ft = 0; ft < RPW / 16; ++ft)
 #pragma unroll
         for (int j = 0; j < DW; ++j) S[ft][j] = f32x4{0, 0, 0, 0};
 
     const int t_beg = seg * a.seg_len, t_end = min(a.N, t_beg + a.seg_len);
     // projections, value rows and A weights of the chunk, loaded one chunk ahead
-    URegs<RP> ur;
+    URegs<RPW> ur;
     StageT<T, D> vr;
     float awv = 0.f;
     auto load_chunk = [&](int c0) {
-        ur.load(U, c0, a.N);
+        ur.load(U, c0, a.N, RP / 4);
         vr.load(Vl, c0, a.N, vs, 1.f);
         const int r = min(c0 + (int)threadIdx.x, a.N - 1);
         awv = aw ? aw[r] : 1.f;   // masked to the chunk's rows where stored
@@ -96,7 +98,7 @@ __global__ __launch_bounds__(kThreads) void race_state_kernel(StateArgs a)
         __syncthreads();
         vr.store(sm.vt, vs != nullptr);
         if (threadIdx.x < kC) sm.aw[threadIdx.x] = t0 + (int)threadIdx.x < a.N ? awv : 0.f;
-        features_from<T, RP>(ur, t0, a.N, a.L, a.two_beta, nullptr, sm.pht, nullptr);
+        features_from<T, RPW>(ur, t0, a.N, L, a.two_beta, nullptr, sm.pht, nullptr);
         __syncthreads();
         load_chunk(t0 + kC < t_end ? t0 + kC : t0);   // the last chunk reloads its own (unconditional loads)
         // S[f][cols of wave] += Phi'[f][rows] V[rows][cols]
@@ -106,13 +108,13 @@ __global__ __launch_bounds__(kThreads) void race_state_kernel(StateArgs a)
 #pragma unroll
             for (int j = 0; j < DW; ++j) bv[j] = T::ld8(&sm.vt[16 * (w * DW + j) + col][32 * kk + 8 * g]);
 #pragma unroll
-            for (int ft = 0; ft < RP / 16; ++ft) {
+            for (int ft = 0; ft < RPW / 16; ++ft) {
                 const auto af = T::ld8(&sm.pht[16 * ft + col][32 * kk + 8 * g]);
 #pragma unroll
                 for (int j = 0; j < DW; ++j) S[ft][j] = T::mma(af, bv[j], S[ft][j]);
             }
         }
-        for (int f = threadIdx.x; f < RP; f += kThreads) {
+        for (int f = threadIdx.x; f < RPW; f += kThreads) {
             float s = 0.f;
             for (int k = 0; k < kC; ++k) s += T::load(sm.pht[f][k]) * sm.aw[k];
             sm.a_state[f] += s;
@@ -121,13 +123,13 @@ __global__ __launch_bounds__(kThreads) void race_state_kernel(StateArgs a)
     __syncthreads();
     float* out = a.states + (bh * a.nseg + seg) * (size_t)(RP * D + RP);
 #pragma unroll
-    for (int ft = 0; ft < RP / 16; ++ft)
+    for (int ft = 0; ft < RPW / 16; ++ft)
 #pragma unroll
         for (int j = 0; j < DW; ++j)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                out[(size_t)(16 * ft + 4 * g + i) * D + 16 * (w * DW + j) + col] = S[ft][j][i] * a.mul;
-    for (int f = threadIdx.x; f < RP; f += kThreads) out[RP * D + f] = sm.a_state[f] * a.mul;
+                out[(size_t)(F0 + 16 * ft + 4 * g + i) * D + 16 * (w * DW + j) + col] = S[ft][j][i] * a.mul;
+    for (int f = threadIdx.x; f < RPW; f += kThreads) out[RP * D + F0 + f] = sm.a_state[f] * a.mul;
 }
 
 // mode 0: total in every segment; 1: exclusive prefix; 2: exclusive suffix.
@@ -360,7 +362,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
 template <class T, int D, int RP>
 constexpr bool fits()
 {
-    return sizeof(StateSmem<T, D, RP>) <= kMaxLds && sizeof(OutSmem<T, D, RP>) <= kMaxLds;
+    return sizeof(StateSmem<T, D, RP / table_split<RP>()>) <= kMaxLds && sizeof(OutSmem<T, D, RP>) <= kMaxLds;
 }
 
 template <class T, int D, int RP>
@@ -369,7 +371,7 @@ hipError_t launch_states_t(const Shape& s, const StateArgs& a, int scan_mode, hi
     if constexpr (!fits<T, D, RP>()) {
         return hipErrorInvalidConfiguration;
     } else {
-        dim3 grid(s.nseg, s.H, s.B);
+        dim3 grid(s.nseg * table_split<RP>(), s.H, s.B);
         // the forward sums key rows, the backward (vscale set) query rows
         const bool bwd = a.vscale != nullptr;
         ELSAA_LAUNCH(bwd ? "race_state_bwd" : "race_state_fwd", (race_state_kernel<T, D, RP>), grid, dim3(kThreads),

@@ -27,6 +27,11 @@ SMALL = [
     _w("c-f32-d128-512", 1, 1, 512, 128, 32, 64, True, "f32"),
     _w("c-bf16-leaf-only-256", 2, 1, 256, 64, 128, 48, True, "bf16"),
     _w("c-bf16-r256-1024", 1, 1, 1024, 128, 128, 256, True, "bf16", recipe="mixed", centres=8),
+    # 256 features: the state, dQ and dK passes split the tables over two
+    # workgroups; r = 192 leaves the second one 4 live tables of 8
+    _w("nc-bf16-d64-r256-700", 1, 2, 700, 64, 64, 256, False, "bf16"),
+    _w("c-bf16-d64-r256-ragged-900", 1, 1, 900, 64, 128, 256, True, "bf16"),
+    _w("c-bf16-d128-r192-ragged-1300", 1, 1, 1300, 128, 128, 192, True, "bf16", recipe="clustered"),
     _w("c-bf16-n0-3x-768", 1, 1, 768, 64, 128, 64, True, "bf16"),
     # Alg. 5's zero-token padding of odd lists: 1001 -> 501 -> 251 -> 126
     _w("c-bf16-d64-padded-1001", 1, 2, 1001, 64, 64, 64, True, "bf16"),
