@@ -426,9 +426,11 @@ def main():
             continue
         ms = sum(per_step[kn] for kn in ran)
         unit_rows[name] = (ms, nb, nf, ran)
-    # the dominant unit (largest time per step); for a unit of one kernel the
-    # figures are per launch over that kernel's average launch duration
-    dom = max(unit_rows, key=lambda n: unit_rows[n][0])
+    # the dominant kernel (largest time per step) and its unit; for a unit of
+    # one kernel the figures are per launch over that kernel's average launch
+    # duration, for a unit of several the unit's per step
+    unit_of = {kn: name for name, row in unit_rows.items() for kn in row[3]}
+    dom = unit_of[max(unit_of, key=lambda kn: per_step[kn])]
     ms, nb, nf, ran = unit_rows[dom]
     if len(ran) == 1:
         tot_ms, n = prof[ran[0]]
