@@ -297,6 +297,13 @@ def roofline_entry(nbytes, nflops, seconds, peak_tf):
             "frac": round(a / peak_tf, 4)}
 
 
+def dominant_unit(unit_rows: dict, per_step: dict) -> str:
+    """The unit of the kernel with the largest time per step.  unit_rows:
+    {unit: (ms, bytes, flops, kernels that ran)}; per_step: {kernel: ms}."""
+    unit_of = {kn: name for name, row in unit_rows.items() for kn in row[3]}
+    return unit_of[max(unit_of, key=lambda kn: per_step[kn])]
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -429,8 +436,7 @@ def main():
     # the dominant kernel (largest time per step) and its unit; for a unit of
     # one kernel the figures are per launch over that kernel's average launch
     # duration, for a unit of several the unit's per step
-    unit_of = {kn: name for name, row in unit_rows.items() for kn in row[3]}
-    dom = unit_of[max(unit_of, key=lambda kn: per_step[kn])]
+    dom = dominant_unit(unit_rows, per_step)
     ms, nb, nf, ran = unit_rows[dom]
     if len(ran) == 1:
         tot_ms, n = prof[ran[0]]
