@@ -27,6 +27,12 @@ SMALL = [
     _w("c-f32-d128-512", 1, 1, 512, 128, 32, 64, True, "f32"),
     _w("c-bf16-leaf-only-256", 2, 1, 256, 64, 128, 48, True, "bf16"),
     _w("c-bf16-r256-1024", 1, 1, 1024, 128, 128, 256, True, "bf16", recipe="mixed", centres=8),
+    # degenerate lengths: one token, two, three; 65 = one padded level
+    _w("nc-f32-n1", 1, 1, 1, 64, 32, 32, False, "f32"),
+    _w("c-bf16-n1-d128", 1, 2, 1, 128, 64, 128, True, "bf16"),
+    _w("c-bf16-n2-d64", 2, 1, 2, 64, 64, 64, True, "bf16"),
+    _w("nc-bf16-n3-d128", 1, 1, 3, 128, 128, 128, False, "bf16"),
+    _w("c-bf16-n65-k32-padded", 1, 2, 65, 64, 32, 64, True, "bf16"),
     # 256 features: the state, dQ and dK passes split the tables over two
     # workgroups; r = 192 leaves the second one 4 live tables of 8
     _w("nc-bf16-d64-r256-700", 1, 2, 700, 64, 64, 256, False, "bf16"),
