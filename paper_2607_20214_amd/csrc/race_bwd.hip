@@ -265,7 +265,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_dq_kernel(LbArgs a)
 #pragma unroll
                     for (int dt = 0; dt < DT; ++dt)
                         St_[j][dt] = T::mma(T::ld8(&sm.vt[16 * dt + col][32 * kk + 8 * g]), bf, St_[j][dt]);
-                    Aacc[j] = token_sums<T>(bf, nullptr, 32 * kk, Aacc[j]);
+                    Aacc[j] = token_sums<T>(bf, Aacc[j]);
                 }
             }
         }

@@ -64,21 +64,15 @@ __device__ __forceinline__ typename T::frag_t phi_t8(const typename T::store_t (
     return col8_t<T, RP + kPad>(ph, kb, f0);
 }
 
-// Weighted sums over 32 of the chunk's tokens on the matrix cores: Phi^T x W
-// with every column of W holding the weights of tokens kb .. kb + 31 (w, or 1
-// when null), so every lane of the product tile holds the sums of its rows'
-// features: lane (g, col) register i += sum_k phi_{f0 + 4g + i}(k) w_k (phit
-// from phi_t8 at feature f0).  w keeps float32 accuracy (hi + lo parts, two
-// products) when given.
+// Sums over 32 of the chunk's tokens on the matrix cores: Phi^T x 1 (every
+// entry of the B operand 1), so every lane of the product tile holds the
+// sums of its rows' features: lane (g, col) register i += sum over tokens
+// kb .. kb + 31 of phi_{f0 + 4g + i} (phit from phi_t8 at feature f0).
 template <class T>
-__device__ __forceinline__ f32x4 token_sums(typename T::frag_t phit, const float* w, int kb, f32x4 acc)
+__device__ __forceinline__ f32x4 token_sums(typename T::frag_t phit, f32x4 acc)
 {
-    const int g = (threadIdx.x & 63) >> 4;
-    float v[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) v[j] = w ? w[kb + 8 * g + j] : 1.f;
-    if (!w) return T::mma(phit, T::pack(v), acc);
-    return mma_split<T>(phit, v, acc);
+    float one[8] = {1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f};
+    return T::mma(phit, T::pack(one), acc);
 }
 
 // a_state[f] += scale * sum over the chunk's tokens k of xt[f][k] (* wk[k] when

@@ -344,7 +344,7 @@ __global__ __launch_bounds__(kThreads, 2) void race_out_kernel(OutArgs a)
                     const F af = phi_t8<T, RP>(sm.phk, 32 * kk, 16 * ft);
 #pragma unroll
                     for (int j = 0; j < DW; ++j) S[ft][j] = T::mma(af, bv[j], S[ft][j]);
-                    if (ft % 4 == w) Aacc[ft / 4] = token_sums<T>(af, nullptr, 32 * kk, Aacc[ft / 4]);
+                    if (ft % 4 == w) Aacc[ft / 4] = token_sums<T>(af, Aacc[ft / 4]);
                 }
             }
             // the den of the next chunk reads a_state after its first barrier
