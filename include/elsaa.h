@@ -116,8 +116,9 @@ int elsaa_workspace_bytes(const elsaa_config* cfg, int pass, size_t* bytes);
  *   o_lowrank       storage dtype [B,H,N,d_h] low-rank output O_lr (its
  *                   weights are diffuse, so <dO, O_lr> has no such
  *                   cancellation);
- *   u_q, u_k        float32 [B,H,N,P] RACE projections u = W_race x of the Q and K
- *                   rows (P = 4 L rounded up to 8, 16, 32 or 64; padded tables 0);
+ *   u_q, u_k        float32 [B,H,N,P] tanh of the RACE projections, t = tanh(W_race x),
+ *                   of the Q and K rows (P = 4 L rounded up to 8, 16, 32 or 64;
+ *                   padded tables 0);
  *   race_states     float32 RACE segment states phi(k) V' and phi(k) of the key
  *                   rows before each sequence segment (causal; the totals when
  *                   non-causal), [B*H][segments][r_p * d_h + r_p] with r_p = r

@@ -3,8 +3,9 @@
 // Features (Alg. 2): for table l, u = W_l x (4 projections), t = tanh(u), and
 // for bucket c of the hypercube {+-1}^4 (bit b of c set <-> v_cb = +1)
 //   phi_c = exp(beta t.v_c) / sum_c' exp(beta t.v_c') = prod_b sigmoid(2 beta v_cb t_b).
-// The projections u = W x are computed once per row by the projection kernel
-// and stored in float32; chunks are 64 tokens; each workgroup is 4 waves,
+// The projection kernel forms u = W x once per row and stores t = tanh(u)
+// in float32 (every pass uses u only through t); chunks are 64 tokens; each
+// workgroup is 4 waves,
 // wave w handles tokens 16w .. 16w+15 of a chunk when computing features.
 #pragma once
 #include "common.hpp"
@@ -234,7 +235,7 @@ __device__ void stage_r(typename T::store_t (*x)[D + kPad], const typename T::st
     st.store(x, scale != nullptr);
 }
 
-// Projections u of the tables this lane handles for chunk tokens
+// Projections t = tanh(u) of the tables this lane handles for chunk tokens
 // [t0 + 16w, t0 + 16w + 16) (table tb = g + 4 m of token 16w + col), loaded
 // ahead of features_from so that the next chunk's loads overlap this one.
 template <int RP>
@@ -260,9 +261,9 @@ struct URegs {
 };
 
 // Features of chunk tokens [t0 + 16w, t0 + 16w + 16) for every table, from
-// the projections in ur (URegs::load of the same chunk).
+// the projections t = tanh(u) in ur (URegs::load of the same chunk).
 // Writes phi (as T) row-major into ph[token][feature] and/or transposed into
-// pht[feature][token], and t = tanh(u) into ts[token][4 * table + bit].
+// pht[feature][token], and t into ts[token][4 * table + bit].
 template <class T, int RP>
 __device__ void features_from(const URegs<RP>& ur, int t0, int N, int L, float two_beta,
                               typename T::store_t (*ph)[RP + kPad], typename T::store_t (*pht)[kC + kPad],
@@ -276,14 +277,11 @@ __device__ void features_from(const URegs<RP>& ur, int t0, int N, int L, float t
     for (int m = 0; m < URegs<RP>::NU; ++m) {   // this lane: table tb of token tl
         const int tb = g + 4 * m;
         if (tb >= RP / 16) break;
-        const f32x4 u = ur.u[m];
+        const f32x4 t = ur.u[m];                 // t = tanh(W x), formed by the projection pass
         const bool live = tb < L && tok < N;
-        float t[4], sp[4], sn[4];
+        float sp[4], sn[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            t[i] = tanh_abs(u[i]);
-            sigmoid_pair(two_beta * t[i], sp[i], sn[i]);
-        }
+        for (int i = 0; i < 4; ++i) sigmoid_pair(two_beta * t[i], sp[i], sn[i]);
         if (ts) *(f32x4*)&ts[tl][4 * tb] = f32x4{t[0], t[1], t[2], t[3]};
         float phi[16];
 #pragma unroll

@@ -5,7 +5,7 @@
 // A^l = Phi_K^l' 1, B^l = Phi_K^l' V; the causal form restricts both sums to
 // keys j <= i.  O_lr = Num / (Den + eps), d_lr = Den.
 //
-// Features come from the projections u = W x stored by the projection kernel.
+// Features come from t = tanh(W x), stored by the projection kernel.
 // The sequence of each (b,h) is cut into segments of whole 64-token chunks:
 //   state  one workgroup per segment: S = sum_j phi(x_j) v_j' (r x d) and
 //          A = sum_j a_j phi(x_j) over the segment (forward: x = k, v = V,

@@ -5,14 +5,15 @@
 // multiply-add chain over e = 0..d-1 of W_sort[h][t][e] * x[e] is > 0; the key
 // is the rank of the bit code in the reflected Gray sequence so neighbouring
 // buckets differ in one bit (sorted Hamming LSH, Sec. 3).  The same pass over
-// Q or K also computes the RACE projections u = W_race x (Alg. 2), so each
-// input row is read once for both branches' hashing.
+// Q or K also computes the RACE projections u = W_race x (Alg. 2) and stores
+// t = tanh(u), so each input row is read once for both branches' hashing.
 // Sort (Alg. 4, step "Sort"; one call per half-segment of each level of
 // Alg. 5): ascending by (key, token index), i.e. a stable counting sort over
 // at most 2^sort_bits buckets, one workgroup per sorted list.
 #include "common.hpp"
 #include "internal.hpp"
 #include "causal.hpp"
+#include "race_common.hpp"
 
 namespace elsaa {
 
@@ -26,7 +27,7 @@ constexpr int kProjTarget = 1024;      // workgroups per launch (about four per 
 // every row it writes the sortLSH bucket key and, when W_race is given, the
 // RACE projections u = W_race x in float32 accuracy: W = W_hi + W_lo split
 // into two bf16 parts for the bf16 MFMA path (the residual is below 2^-16
-// relative), plain float32 MFMA for float32 storage.  u is stored
+// relative), plain float32 MFMA for float32 storage.  t = tanh(u) is stored
 // [BH][N][UP] (UP = padded projections).  W is staged once per workgroup;
 // the next tile's rows are loaded into registers while the current one is
 // hashed and projected.
@@ -153,7 +154,12 @@ __global__ __launch_bounds__(kProjThreads) void proj_kernel(ProjIO io, const flo
                     if (T::bytes == 2) acc = T::mma(T::ld8(&sm.wlo[16 * pt + col][32 * ks + 8 * g]), xf[ks], acc);
                 }
                 const int p0 = 16 * pt + 4 * g;
-                if (tl < rows && p0 < UP) *(f32x4*)(U + (bh * N + row0 + tl) * UP + p0) = acc;
+                if (tl < rows && p0 < UP) {
+                    // the RACE passes use u only through t = tanh(u): store t
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) acc[i] = race::tanh_abs(acc[i]);
+                    *(f32x4*)(U + (bh * N + row0 + tl) * UP + p0) = acc;
+                }
             }
         }
         __syncthreads();
