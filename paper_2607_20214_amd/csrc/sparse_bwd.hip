@@ -213,12 +213,15 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
     const int blk_lo = (MODE == kLeaf) ? 0 : max(0, (qpos / bq - a.nbr) * bq);
     const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), (qpos / bq + 1 + a.nbr) * bq);
 
-    // key rows of the tile at k0 that this thread stages (-1 = none)
+    // key rows of the tile at k0 that this thread stages: positions past the
+    // scanned range repeat its last key (a real row: key lists hold no zero
+    // tokens), whose scores the mask drops, so the loads need no per-row
+    // branch
     auto tokens = [&](int k0, int (&tok)[PT]) {
 #pragma unroll
         for (int j = 0; j < PT; ++j) {
-            const int p = k0 + TD::row_of(j);
-            tok[j] = p < kend ? ((MODE == kLeaf) ? p : klist[p]) : -1;
+            const int p = min(k0 + TD::row_of(j), kend - 1);
+            tok[j] = (MODE == kLeaf) ? p : klist[p];
         }
     };
     const int ntiles = (kend - kbeg + kT - 1) / kT;
@@ -228,9 +231,11 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
         const size_t wh = (bh % a.H) * D * a.wk;
         WtStage<T, D>::issue((const S*)a.wt_hi + wh, (const S*)a.wt_lo + wh, a.wk, swt);
     }
-    tokens(kbeg, tok);
-    TD::load(K, tok, rk);
-    TD::load(V, tok, rv);
+    if (ntiles > 0) {
+        tokens(kbeg, tok);
+        TD::load_all(K, tok, rk);
+        TD::load_all(V, tok, rv);
+    }
     if (ntiles > 1) tokens(kbeg + kT, tok);
 
     float lse2 = 0.f, delta = 0.f, scs = 0.f;
@@ -268,8 +273,8 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
         if (MODE != kLevels && t == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // W' in LDS
         __syncthreads();
         if (t + 1 < ntiles) {
-            TD::load(K, tok, rk);
-            TD::load(V, tok, rv);
+            TD::load_all(K, tok, rk);
+            TD::load_all(V, tok, rv);
             if (t + 2 < ntiles) tokens(k0 + 2 * kT, tok);
         }
         // a key tile every lane sees whole skips the mask (one wave vote)
@@ -288,20 +293,17 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
                     st = T::mma(TD::row8(sk, kr, 32 * ks + 8 * g), qf[ks], st);
                     dp = T::mma(TD::row8(sv, kr, 32 * ks + 8 * g), df[ks], dp);
                 }
-                if (full) {
 #pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        v8[4 * h2 + i] = fast_exp2(fmaf(st[i], a.tau2, -lse2)) * fmaf(scs, dp[i], -delta);
-                } else {
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
+                for (int i = 0; i < 4; ++i) {
+                    float P = fast_exp2(fmaf(st[i], a.tau2, -lse2));
+                    if (!full) {
                         const int p = k0 + key_of(s, g, i);
                         bool ok = p < kend && qtok >= 0;
                         if (MODE == kLeaf) ok = ok && p <= qtok;
                         else ok = ok && p >= blk_lo && p < blk_hi;
-                        const float P = ok ? fast_exp2(fmaf(st[i], a.tau2, -lse2)) : 0.f;
-                        v8[4 * h2 + i] = P * fmaf(scs, dp[i], -delta);
+                        P = ok ? P : 0.f;
                     }
+                    v8[4 * h2 + i] = P * fmaf(scs, dp[i], -delta);
                 }
             }
             const F bf = T::pack(v8);
@@ -444,12 +446,15 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
     const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), (kpos / bq + 1 + a.nbr) * bq);
 
     // query rows of the tile at q0 that this thread stages, and the scalars
-    // of query q0 + threadIdx.x (threads < 64)
+    // of query q0 + threadIdx.x (threads < 64).  Staged rows past the
+    // scanned range repeat its last entry and a zero token's entry (-1)
+    // reads row 0: real rows whose scores the mask drops (the scalars mark
+    // them), so the loads need no per-row branch.
     auto tokens = [&](int q0, int (&tok)[PT], int& qt) {
 #pragma unroll
         for (int j = 0; j < PT; ++j) {
-            const int p = q0 + TD::row_of(j);
-            tok[j] = p < qend ? ((MODE == kLeaf) ? p : qlist[p]) : -1;
+            const int p = min(q0 + TD::row_of(j), qend - 1);
+            tok[j] = (MODE == kLeaf) ? p : max(qlist[p], 0);
         }
         qt = -1;
         if (threadIdx.x < kT) {
@@ -474,9 +479,12 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
         const size_t wh = (bh % a.H) * D * a.wk;
         WtStage<T, D>::issue((const S*)a.wt_hi + wh, (const S*)a.wt_lo + wh, a.wk, swt);
     }
-    tokens(qbeg, tok, qt_cur);
-    TD::load(Q, tok, rq);
-    TD::load(dO, tok, ro);
+    qt_cur = -1;
+    if (ntiles > 0) {
+        tokens(qbeg, tok, qt_cur);
+        TD::load_all(Q, tok, rq);
+        TD::load_all(dO, tok, ro);
+    }
     scalars(qt_cur);
     if (ntiles > 1) tokens(qbeg + kT, tok, qt_next);
 
@@ -516,8 +524,8 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
         if (MODE != kLevels && t == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // W' in LDS
         __syncthreads();
         if (t + 1 < ntiles) {
-            TD::load(Q, tok, rq);
-            TD::load(dO, tok, ro);
+            TD::load_all(Q, tok, rq);
+            TD::load_all(dO, tok, ro);
             scalars(qt_next);
             qt_cur = qt_next;
             if (t + 2 < ntiles) tokens(q0 + 2 * kT, tok, qt_next);

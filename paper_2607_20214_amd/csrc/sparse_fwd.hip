@@ -147,20 +147,25 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) acc[dt] = f32x4{0, 0, 0, 0};
 
-    // rows of the key tile at k0 that this thread stages (-1 = none)
+    // rows of the key tile at k0 that this thread stages: positions past
+    // the scanned range repeat its last key (a real row: key lists hold no
+    // zero tokens), whose scores the mask drops, so the loads need no
+    // per-row branch
     auto tokens = [&](int k0, int (&tok)[PT]) {
 #pragma unroll
         for (int j = 0; j < PT; ++j) {
-            const int p = k0 + Tl::row_of(j);
-            tok[j] = p < kend ? ((MODE == kLeaf) ? p : klist[p]) : -1;
+            const int p = min(k0 + Tl::row_of(j), kend - 1);
+            tok[j] = (MODE == kLeaf) ? p : klist[p];
         }
     };
     const int ntiles = (kend - kbeg + kKT - 1) / kKT;
     int tok[PT];
     uint4 rk[PT], rv[PT];
-    tokens(kbeg, tok);
-    Tl::load(K, tok, rk);
-    Tl::load(V, tok, rv);
+    if (ntiles > 0) {
+        tokens(kbeg, tok);
+        Tl::load_all(K, tok, rk);
+        Tl::load_all(V, tok, rv);
+    }
     if (ntiles > 1) tokens(kbeg + kKT, tok);
 
     for (int t = 0; t < ntiles; ++t) {
@@ -170,8 +175,8 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
         Tl::store(sv, rv);
         __syncthreads();
         if (t + 1 < ntiles) {                // next tile's rows in flight during this one
-            Tl::load(K, tok, rk);
-            Tl::load(V, tok, rv);
+            Tl::load_all(K, tok, rk);
+            Tl::load_all(V, tok, rv);
             if (t + 2 < ntiles) tokens(k0 + 2 * kKT, tok);
         }
 
@@ -190,13 +195,7 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
         // of a causal leaf and ragged ends) skips the mask: one wave vote.
         const bool lane_full = qtok >= 0 && k0 + kKT <= kend &&
                                (MODE == kLeaf ? k0 + kKT - 1 <= qtok : (k0 >= blk_lo && k0 + kKT <= blk_hi));
-        float tmax = -INFINITY;
-        if (__all(lane_full)) {
-#pragma unroll
-            for (int s = 0; s < 4; ++s)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) tmax = fmaxf(tmax, st[s][i]);
-        } else {
+        if (!__all(lane_full)) {
 #pragma unroll
             for (int s = 0; s < 4; ++s)
 #pragma unroll
@@ -205,11 +204,14 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
                     bool ok = p < kend && qtok >= 0;
                     if (MODE == kLeaf) ok = ok && p <= qtok;
                     else ok = ok && p >= blk_lo && p < blk_hi;
-                    const float v = ok ? st[s][i] : -INFINITY;
-                    st[s][i] = v;
-                    tmax = fmaxf(tmax, v);
+                    st[s][i] = ok ? st[s][i] : -INFINITY;
                 }
         }
+        float tmax = -INFINITY;
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) tmax = fmaxf(tmax, st[s][i]);
         tmax = wave_max16(tmax) * a.tau2;            // tau2 > 0: the max of the scaled scores
         const float m_new = fmaxf(m_run, tmax);
         const float m_use = (m_new == -INFINITY) ? 0.f : m_new;

@@ -28,6 +28,8 @@ CASES = [
     _w("c-bf16-d128-800-leaf50", 2, 1, 800, 128, 32, 64, "bf16", 60),
     # the text setting's block and base length, scaled: levels 4000 / 2000 / 1000, leaves 1000
     _w("c-bf16-text-8000-b256-leaf1000", 1, 1, 8000, 128, 256, 64, "bf16", 1000),
+    # leaves of 9 tiles (odd: the last workgroup of a long leaf holds one query tile), d_h 64
+    _w("c-bf16-d64-2080-leaf520", 1, 2, 2080, 64, 64, 64, "bf16", 520),
     # the text setting's own leaf of 4096 tokens
     _w("c-bf16-text-8192-b256-n04096", 1, 1, 8192, 128, 256, 64, "bf16", 4096),
 ]
