@@ -8,8 +8,10 @@ already resident in HBM).  After W warm-up steps, K steps are timed as a user
 runs them (value, ms_per_step); then K more steps are timed with the library's
 per-kernel HIP events on (each launch bracketed on its own stream), which give
 the kernel durations behind the roofline of the dominant kernel and of every
-kernel (their step time is reported as profiled_ms_per_step).  Prints one JSON
-line, with the CPU oracle timed on a bounded sample.
+kernel (their step time is reported as profiled_ms_per_step).  Last, K calls
+of the forward and of the backward are timed on their own (medians, in
+fwd_bwd_split).  Prints one JSON line, with the CPU oracle timed on a bounded
+sample.
 """
 from __future__ import annotations
 
@@ -236,6 +238,10 @@ def cpu_baseline(w, inp, min_seconds: float = 10.0) -> dict:
     if w.backward:
         nb, tb = _oracle_heads(w, inp, hc, True, min_seconds)
         out["value"] = w.B * w.N * nb / (tb * total)
+        # the backward alone: a head's forward + backward less its forward
+        t_bwd = tb / nb - tf / nf
+        if t_bwd > 0:
+            out["bwd_value"] = w.B * w.N / (t_bwd * total)
         out["sample"] = (f"forward alone on {nf} of {total} heads ({tf:.1f} s); forward + backward (one "
                          f"oracle backward call per head) on {nb} of {total} heads ({tb:.1f} s); all "
                          f"{w.N} tokens of each head; {threads} threads; scaled to {total} heads")
@@ -416,6 +422,26 @@ def main():
     t3 = time.perf_counter()
     prof = E.profile_read()
     E.profile_enable(False)
+    # timed region 3: forward and backward each on their own, every call
+    # bracketed by events on torch's current stream (the library's side
+    # stream joins that stream before each call returns); medians over the
+    # calls
+    split = None
+    if w.backward and blk is None and not args.rules:
+        cur = torch.cuda.current_stream()
+        tf, tb = [], []
+        for _ in range(args.steps):
+            e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+            e0.record(cur)
+            o_, lse_, dlr_, saved_ = E.fwd(cfg, q, k, v, ws, wr, buffers=bufs)
+            e1.record(cur)
+            E.bwd(cfg, q, k, v, wr, do, lse_, dlr_, saved_, buffers=bufs)
+            e2.record(cur)
+            e2.synchronize()
+            tf.append(e0.elapsed_time(e1))
+            tb.append(e1.elapsed_time(e2))
+        split = {"fwd_ms_median": round(float(np.median(tf)), 4), "bwd_ms_median": round(float(np.median(tb)), 4),
+                 "calls": args.steps}
 
     elapsed = t1 - t0
     ms_step = elapsed / args.steps * 1e3
@@ -503,6 +529,8 @@ def main():
         "roofline_kernel_model": kmodel,
         "kernel_ms_per_step": {n: round(t, 4) for n, t in sorted(per_step.items(), key=lambda x: -x[1])},
     }
+    if split is not None:
+        result["fwd_bwd_split"] = split
     if args.rules:
         result["config"]["rules"] = {"gate_hidden": rules_G, "lambda_rule": True}
     if not args.no_cpu_baseline:
