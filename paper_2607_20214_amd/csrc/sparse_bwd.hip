@@ -806,19 +806,27 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
         int qtk[NQT][PT];
         int qt1[NQT];                                    // query 64 qt + (tx % 64) (scalars, dQ rows)
     };
-    auto indices = [&](const Blk& k, Idx& ix) {
+    // the key lists of a block, and the query list entries of its tile t
+    // (a block's later query tiles are indexed while its first is consumed,
+    // so their entries are not held in registers across the block change)
+    auto indices_k = [&](const Blk& k, Idx& ix) {
 #pragma unroll
-        for (int t = 0; t < NQT; ++t) {
+        for (int t = 0; t < NQT; ++t)
 #pragma unroll
             for (int j = 0; j < PT; ++j) {
                 const int r = 64 * t + TD::row_of(j, tx);
                 ix.ktk[t][j] = (kFull || r < k.nv) ? k.kl[(uint32_t)r] : -1;
-                ix.qtk[t][j] = (kFull || r < k.nv) ? k.ql[(uint32_t)r] : -1;
             }
-            const int r = 64 * t + (tx & 63);
-            ix.qt1[t] = (kFull || r < k.nv) ? k.ql[(uint32_t)r] : -1;
-        }
         ix.ktok = (kFull || kloc < k.nv) ? k.kl[(uint32_t)kloc] : -1;
+    };
+    auto indices_q = [&](const Blk& k, Idx& ix, int t) {
+#pragma unroll
+        for (int j = 0; j < PT; ++j) {
+            const int r = 64 * t + TD::row_of(j, tx);
+            ix.qtk[t][j] = (kFull || r < k.nv) ? k.ql[(uint32_t)r] : -1;
+        }
+        const int r = 64 * t + (tx & 63);
+        ix.qt1[t] = (kFull || r < k.nv) ? k.ql[(uint32_t)r] : -1;
     };
     auto kload = [&](size_t bh, const Idx& ix, uint4 (&rk)[NQT][PT]) {
         const S* K = (const S*)a.K + bh * N * D;
@@ -894,7 +902,8 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
     int id = blockIdx.x;
     Blk blk = block_of(id);
     Idx ix;
-    indices(blk, ix);
+    indices_k(blk, ix);
+    indices_q(blk, ix, 0);
     uint4 rk[NQT][PT];
     F vf[KS];
     kload(blk.bh, ix, rk);
@@ -941,10 +950,12 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
                 for (int dt = 0; dt < DT; ++dt) { akT[dt] = f32x4{0, 0, 0, 0}; avT[dt] = f32x4{0, 0, 0, 0}; }
             }
             if (!last) {
+                indices_q(blk, ix, qt + 1);
                 qload(bh, ix, qt + 1);                   // next tile in flight
             } else if (has_next) {
                 nblk = block_of(nid);                    // the next block's index lists
-                indices(nblk, nix);
+                indices_k(nblk, nix);
+                indices_q(nblk, nix, 0);
             }
 
             // S and dP for the 64 queries x this wave's 16 keys (rows: queries);
@@ -990,6 +1001,7 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
                     avT[dt] = T::mma(TD::col8(so, 32 * kk, 16 * dt, tx), pf[kk], avT[dt]);
                     akT[dt] = T::mma(TD::col8(sq, 32 * kk, 16 * dt, tx), zf[kk], akT[dt]);
                 }
+            if (last && has_next) qload(nblk.bh, nix, 0);  // the next block's first Q / dO tile, under the dQ phase
             __syncthreads();                             // query tiles no longer read
             // dS^T [key][query] into the query-tile space: slots 8g + j of k-step kk
             // hold queries 32 kk + 8 g + j, eight consecutive queries per write
@@ -1049,7 +1061,6 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
         prev_kslot = kslot;
         prev_ktok = ktok;
         if (!has_next) break;
-        qload(nblk.bh, nix, 0);                          // the next block's first Q / dO tile
         id = nid;
         blk = nblk;
         ix = nix;
