@@ -39,6 +39,9 @@ static_assert(kQT == kRowTile, "causal tiles are numbered in 64-query tiles");
 
 enum Mode { kBlocks = 0, kLevels = 1, kLeaf = 2 };
 
+// headroom (log2 units) of the online softmax's lazy reference max
+constexpr float kLazy = 8.f;
+
 struct Args {
     const void* Q;
     const void* K;
@@ -213,9 +216,22 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
 #pragma unroll
             for (int i = 0; i < 4; ++i) tmax = fmaxf(tmax, st[s][i]);
         tmax = wave_max16(tmax) * a.tau2;            // tau2 > 0: the max of the scaled scores
-        const float m_new = fmaxf(m_run, tmax);
-        const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-        const float corr = fast_exp2(m_run - m_use);
+        // The reference m_run of the exponentials is raised (and the
+        // accumulators rescaled) only when some lane's tile max exceeds it by
+        // more than kLazy (log2 units); otherwise the tile's P stay below
+        // 2^kLazy, which float32 and the bf16 operands hold.  Any reference
+        // gives the same O and log d: the denominator is kept relative to
+        // the same m_run.  A lane still at -inf (no key seen) takes its first
+        // finite max at once.
+        if (__any(tmax > m_run + kLazy)) {
+            const float m_new = fmaxf(m_run, tmax);
+            const float corr = fast_exp2(m_run - ((m_new == -INFINITY) ? 0.f : m_new));
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) acc[dt] *= corr;
+            l_run *= corr;
+            m_run = m_new;
+        }
+        const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
         float psum = 0.f;
 #pragma unroll
         for (int s = 0; s < 4; ++s)
@@ -225,15 +241,7 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
                 st[s][i] = p;
                 psum += p;
             }
-        psum = wave_sum16(psum);
-        l_run = l_run * corr + psum;
-        // the output is rescaled only when some lane's running max moved
-        // (corr = 1 otherwise; a lane still at -inf has a zero accumulator)
-        if (__any(m_new != m_run)) {
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) acc[dt] *= corr;
-        }
-        m_run = m_new;
+        l_run += wave_sum16(psum);
         // O^T += V^T P^T over two 32-key k-steps
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
