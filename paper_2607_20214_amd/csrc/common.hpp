@@ -152,6 +152,24 @@ __device__ __forceinline__ f32x4 load4(const typename T::store_t* p)
     }
 }
 
+// Four consecutive storage-dtype elements loaded as they are (no conversion,
+// so a load issued early is not waited for until its value is used), and
+// their float32 values.
+template <class T> struct Raw4 {
+    using type = f32x4;
+    __device__ static __forceinline__ type ld(const typename T::store_t* p) { return *(const f32x4*)p; }
+    __device__ static __forceinline__ f32x4 val(type v) { return v; }
+};
+template <> struct Raw4<BF16> {
+    using type = uint2;
+    __device__ static __forceinline__ type ld(const uint16_t* p) { return *(const uint2*)p; }
+    __device__ static __forceinline__ f32x4 val(type v)
+    {
+        return f32x4{bf16_to_f32(v.x & 0xffffu), bf16_to_f32(v.x >> 16), bf16_to_f32(v.y & 0xffffu),
+                     bf16_to_f32(v.y >> 16)};
+    }
+};
+
 // 16-byte global load / store of raw bytes.
 __device__ __forceinline__ uint4 ldg16(const void* p) { return *(const uint4*)p; }
 __device__ __forceinline__ void stg16(void* p, uint4 v) { *(uint4*)p = v; }

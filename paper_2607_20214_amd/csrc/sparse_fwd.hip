@@ -270,6 +270,24 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
         return;
     }
 
+    // the fusion's row inputs are requested before the level partials are
+    // merged, so their loads share the first round trip
+    const size_t row = bh * N + max(qtok, 0);
+    using R4 = Raw4<T>;
+    typename R4::type olr_raw[DT];
+    float dl = 0.f, lam = a.lambda, gs = 1.f, gl = 1.f;
+    if (qtok >= 0) {
+        const S* olr = (const S*)a.O_lr + row * D;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) olr_raw[dt] = R4::ld(olr + 16 * dt + 4 * g);
+        dl = a.d_lr[row];
+        if (a.lam_rows) lam = a.lam_rows[row];
+        if (a.gates) {
+            gs = a.gates[row * 2 + 0];
+            gl = a.gates[row * 2 + 1];
+        }
+    }
+
     if (MODE == kLeaf && qtok >= 0) {
         // merge the partial of every level whose future half holds this leaf,
         // in level order; the partials are fetched two levels at a time so
@@ -313,18 +331,9 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
 
     // ---- fusion epilogue (kBlocks, kLeaf) --------------------------------
     if (qtok < 0) return;
-    const size_t row = bh * N + qtok;
     const float lse_nat = (m_run + __log2f(l_run)) * kLn2;       // log d_s
     const float inv_den = 1.f / (l_run + a.eps * fast_exp2(-m_run)); // 1 / (d_s + eps), rescaled
-    const float dl = a.d_lr[row];
-    const float lam = a.lam_rows ? a.lam_rows[row] : a.lambda;
     const float mf = a.m_one ? 1.f : 1.f / (1.f + __expf(__logf(lam * dl + a.eps) - lse_nat));
-    float gs = 1.f, gl = 1.f;
-    if (a.gates) {
-        gs = a.gates[row * 2 + 0];
-        gl = a.gates[row * 2 + 1];
-    }
-    const S* olr = (const S*)a.O_lr + row * D;
     S* out = (S*)a.O + row * D;
     float* os = a.O_s + row * D;
 #pragma unroll
@@ -332,8 +341,7 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
         const int c0 = 16 * dt + 4 * g;
         const f32x4 o_s = acc[dt] * inv_den;
         *(f32x4*)(os + c0) = o_s;
-        const f32x4 o_l = load4<T>(olr + c0);
-        store4<T>(out + c0, o_s * (gs * mf) + o_l * gl);
+        store4<T>(out + c0, o_s * (gs * mf) + R4::val(olr_raw[dt]) * gl);
     }
     if (g == 0) {
         a.lse[row] = lse_nat;
