@@ -100,7 +100,10 @@ def test_backward_causal_16k_workload_all_heads():
     _check(W.CAUSAL_16K)
 
 
+@pytest.mark.timeout(900)
 def test_backward_causal_64k_mixed_workload_sampled_rows():
+    """All 8 heads of the 64K mixed workload (heads 0-3 peaked, 4-7
+    diffuse) on 264 sampled query rows and 264 sampled key rows each."""
     w = W.CAUSAL_64K_MIXED
     rng = np.random.default_rng(6)
     qm = np.zeros(w.N, np.uint8)
@@ -109,7 +112,7 @@ def test_backward_causal_64k_mixed_workload_sampled_rows():
     km[rng.choice(w.N, 200, replace=False)] = 1
     qm[-64:] = 1
     km[:64] = 1
-    _check(w, heads={(0, 1), (0, 6)}, q_mask=qm, k_mask=km)
+    _check(w, q_mask=qm, k_mask=km)
 
 
 def test_backward_block_32k_attention_sampled_rows():

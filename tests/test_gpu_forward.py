@@ -104,14 +104,17 @@ def test_forward_causal_16k_workload_all_heads():
     _check_case(W.CAUSAL_16K)
 
 
+@pytest.mark.timeout(600)
 def test_forward_causal_64k_mixed_workload_sampled_rows():
+    """All 8 heads of the 64K mixed workload (heads 0-3 peaked, 4-7
+    diffuse) on 428 sampled rows each."""
     w = W.CAUSAL_64K_MIXED
     mask = np.zeros(w.N, np.uint8)
     rng = np.random.default_rng(5)
     mask[rng.choice(w.N, 300, replace=False)] = 1
     mask[:64] = 1
     mask[-64:] = 1
-    _check_case(w, heads={(0, 0), (0, 7)}, row_mask=mask)
+    _check_case(w, row_mask=mask)
 
 
 def test_forward_block_32k_attention_sampled_rows():
