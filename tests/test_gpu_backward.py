@@ -115,9 +115,10 @@ def test_backward_causal_64k_mixed_workload_sampled_rows():
     _check(w, q_mask=qm, k_mask=km)
 
 
+@pytest.mark.timeout(900)
 def test_backward_block_32k_attention_sampled_rows():
     """Backward of the 32768-token, d_model 1024 block's attention (16 heads
-    of 64, seven levels) at full size, on sampled rows of two heads."""
+    of 64, seven levels) at full size, on sampled rows of every head."""
     w = W.BLOCK_32K
     rng = np.random.default_rng(8)
     qm = np.zeros(w.N, np.uint8)
@@ -126,7 +127,7 @@ def test_backward_block_32k_attention_sampled_rows():
     km[rng.choice(w.N, 200, replace=False)] = 1
     qm[-64:] = 1
     km[:64] = 1
-    _check(w, heads={(0, 4), (0, 9)}, q_mask=qm, k_mask=km)
+    _check(w, q_mask=qm, k_mask=km)
 
 
 @pytest.mark.timeout(300)

@@ -117,16 +117,17 @@ def test_forward_causal_64k_mixed_workload_sampled_rows():
     _check_case(w, row_mask=mask)
 
 
+@pytest.mark.timeout(600)
 def test_forward_block_32k_attention_sampled_rows():
     """The attention of the 32768-token, d_model 1024 block (16 heads of 64,
-    seven levels) at full size, on sampled rows of two heads."""
+    seven levels) at full size, on sampled rows of every head."""
     w = W.BLOCK_32K
     mask = np.zeros(w.N, np.uint8)
     rng = np.random.default_rng(7)
     mask[rng.choice(w.N, 300, replace=False)] = 1
     mask[:64] = 1
     mask[-64:] = 1
-    _check_case(w, heads={(0, 2), (0, 13)}, row_mask=mask)
+    _check_case(w, row_mask=mask)
 
 
 def test_forward_padded_16386_sampled_rows():

@@ -74,7 +74,9 @@ def test_ragged_causal_with_neighbours():
     _check(_w("c-bf16-d128-2000-leaf250-nbr1", 1, 1, 2000, 128, 64, 128, "bf16", 300, seed=81), neighbors=1)
 
 
+@pytest.mark.timeout(900)
 def test_text_setting_full_size_sampled_rows():
+    """All 16 heads of the text setting at N = 32000 on 368 sampled rows each."""
     # N = 32000 (the ArXiv length): the oracle computes sampled rows only
     w = W.TEXT_32K
     mask = np.zeros(w.N, np.uint8)
@@ -84,4 +86,4 @@ def test_text_setting_full_size_sampled_rows():
     mask[-64:] = 1
     mask[3990:4010] = 1        # across the first leaf boundary
     mask[15990:16010] = 1      # across the top-level halves
-    _check(w, heads={(0, 0), (0, 9)}, q_mask=mask)
+    _check(w, q_mask=mask)
