@@ -144,6 +144,44 @@ __device__ __forceinline__ void du_frags(const typename T::store_t* du_row, int 
         if (32 * j < wk) f[j] = T::ld8(du_row + 32 * j + 8 * g);
 }
 
+// x[e] += the 8 storage-dtype elements at p (16-byte aligned in bf16).
+template <class T>
+__device__ __forceinline__ void add8(const typename T::store_t* p, float (&x)[8])
+{
+    if constexpr (T::bytes == 2) {
+        const uint4 v = *(const uint4*)p;
+        const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            x[2 * i] += bf16_to_f32(u[i] & 0xffffu);
+            x[2 * i + 1] += bf16_to_f32(u[i] >> 16);
+        }
+    } else {
+        const f32x4 a = *(const f32x4*)p, b = *(const f32x4*)(p + 4);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            x[i] += a[i];
+            x[4 + i] += b[i];
+        }
+    }
+}
+
+// 8 consecutive elements of the storage dtype from float32, one 16-byte
+// store in bf16.
+template <class T>
+__device__ __forceinline__ void store8(typename T::store_t* p, const float (&x)[8])
+{
+    if constexpr (T::bytes == 2) {
+        uint32_t u[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) u[i] = (uint32_t)T::store(x[2 * i]) | ((uint32_t)T::store(x[2 * i + 1]) << 16);
+        *(uint4*)p = make_uint4(u[0], u[1], u[2], u[3]);
+    } else {
+        *(f32x4*)p = f32x4{x[0], x[1], x[2], x[3]};
+        *(f32x4*)(p + 4) = f32x4{x[4], x[5], x[6], x[7]};
+    }
+}
+
 // ------------------------------------------------------------------------
 // dQ: query-centric.  One workgroup per 64 queries (16 per wave, one per
 // lane column); key tiles of 64 rows stream through LDS (tile.hpp) with the
@@ -598,60 +636,84 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
     const size_t row = bh * N + max(ktok, 0);
     F duf[2];
     du_frags<T>((const S*)a.du_k + row * a.wk, a.wk, g, duf);
-    f32x4 tv[DT];
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) tv[dt] = load4<T>((const S*)a.dv_lr + row * D + 16 * dt + 4 * g);
     f32x4 tk[DT];
 #pragma unroll
+    for (int dt = 0; dt < DT; ++dt) tk[dt] = akT[dt] * a.tau + lowrank_lds<T, D>(duf, swt, a.wk, g, col, dt);
+
+    // The rest runs on whole rows: the two float32 sums go to LDS (the tile,
+    // scalar and W' space is free now) as rows [key][d], and each thread
+    // then takes 8 consecutive elements of a row, so the low-rank dV rows,
+    // the partial rows and the results move as 16-byte pieces with 16 (d_h
+    // 128) or 8 lanes covering a row, instead of 8-byte pieces of 16 rows
+    // per instruction.
+    constexpr int RS = D + 4;                     // LDS row stride (floats)
+    static_assert(MODE == kLevels || 2 * 64 * RS * 4 <= dkv_lds_bytes<T, D, MODE>(WtStage<T, D>::kMaxWk),
+                  "row sums fit in the pass's LDS");
+    float* const ek = (float*)smem;               // dK rows
+    float* const ev = ek + 64 * RS;               // dV rows
+    __syncthreads();                              // every wave is done with the tiles and W'
+#pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
-        tk[dt] = akT[dt] * a.tau + lowrank_lds<T, D>(duf, swt, a.wk, g, col, dt);
-        tv[dt] = avT[dt] + tv[dt];
+        const int r = 16 * w + col, c = 16 * dt + 4 * g;
+        *(f32x4*)&ek[r * RS + c] = tk[dt];
+        *(f32x4*)&ev[r * RS + c] = avT[dt];
     }
-    if (ktok < 0) return;
+    __syncthreads();
+    constexpr int PPR = D / 8, RPP = kThreads / PPR, NPASS = 64 / RPP;
+    const int piece = threadIdx.x % PPR, c8 = 8 * piece;
+    // rows past the keys of the list (or leaf) read the tile's first key's
+    // rows (loads without a branch) and store nothing
+    const int nrow = MODE == kLeaf ? qend - j0 : min(64, N - j0);
+    if (nrow <= 0) return;
+    const int tok0 = MODE == kLeaf ? j0 : klist[j0];
+    int tokr[NPASS], tokl[NPASS];
+    float sk8[NPASS][8], sv8[NPASS][8];
+#pragma unroll
+    for (int ps = 0; ps < NPASS; ++ps) {
+        const int r = ps * RPP + (int)threadIdx.x / PPR;
+        tokr[ps] = r < nrow ? (MODE == kLeaf ? j0 + r : klist[j0 + r]) : -1;
+        tokl[ps] = tokr[ps] >= 0 ? tokr[ps] : tok0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            sk8[ps][e] = ek[r * RS + c8 + e];
+            sv8[ps][e] = ev[r * RS + c8 + e];
+        }
+    }
+#pragma unroll
+    for (int ps = 0; ps < NPASS; ++ps) add8<T>((const S*)a.dv_lr + (bh * N + tokl[ps]) * D + c8, sv8[ps]);
     const int leaf = tile / a.lt.per_leaf;
     unsigned lmask = MODE == kLeaf ? leaf_levels(a.lt, leaf, false) : 0u;
     while (lmask) {
-        const S* sk_[2];
-        const S* sv_[2];
+        // two levels at a time, for every row of the thread
+        int64_t base[2];
         bool use[2];
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-            sk_[j] = (const S*)a.part_dk;
-            sv_[j] = (const S*)a.part_dv;
             use[j] = lmask != 0;
+            base[j] = 0;
             if (use[j]) {
                 const int l = __builtin_ctz(lmask);
                 lmask &= lmask - 1;
-                const size_t slot = (size_t)(seg_slot_base(a.lt, bh, l, leaf >> (a.Lv - l), false) + ktok);
-                sk_[j] = (const S*)a.part_dk + slot * D;
-                sv_[j] = (const S*)a.part_dv + slot * D;
+                base[j] = seg_slot_base(a.lt, bh, l, leaf >> (a.Lv - l), false);
             }
         }
-        f32x4 xk[2][DT], xv[2][DT];
 #pragma unroll
         for (int j = 0; j < 2; ++j)
             if (use[j])
 #pragma unroll
-                for (int dt = 0; dt < DT; ++dt) {
-                    xk[j][dt] = load4<T>(sk_[j] + 16 * dt + 4 * g);
-                    xv[j][dt] = load4<T>(sv_[j] + 16 * dt + 4 * g);
-                }
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-            if (use[j])
-#pragma unroll
-                for (int dt = 0; dt < DT; ++dt) {
-                    tk[dt] += xk[j][dt];
-                    tv[dt] += xv[j][dt];
+                for (int ps = 0; ps < NPASS; ++ps) {
+                    const size_t slot = (size_t)(base[j] + tokl[ps]);
+                    add8<T>((const S*)a.part_dk + slot * D + c8, sk8[ps]);
+                    add8<T>((const S*)a.part_dv + slot * D + c8, sv8[ps]);
                 }
     }
-    S* ok_ = (S*)a.dK + row * D;
-    S* ov = (S*)a.dV + row * D;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-        store4<T>(ok_ + 16 * dt + 4 * g, tk[dt]);
-        store4<T>(ov + 16 * dt + 4 * g, tv[dt]);
-    }
+    for (int ps = 0; ps < NPASS; ++ps)
+        if (tokr[ps] >= 0) {
+            const size_t o = (bh * N + tokr[ps]) * D + c8;
+            store8<T>((S*)a.dK + o, sk8[ps]);
+            store8<T>((S*)a.dV + o, sv8[ps]);
+        }
 }
 
 // float32 storage at d_h 128 holds twice the operand registers: one wave
