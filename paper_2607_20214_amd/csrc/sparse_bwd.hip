@@ -218,11 +218,14 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
     const S* dO = (const S*)a.dO + bh * N * D;
 
     int level = 0, half = N, qpos, qtok, kbeg, kend, bq = 1;
+    int qrow0 = 0, nq = 0;                       // blocks, leaf: first query position of the tile, its queries
     int64_t slot0 = 0;                           // levels: partial row of token t at slot0 + t
     const int32_t* klist = nullptr;
     if (MODE == kBlocks) {
         bq = min(a.k, N);
         const int p0 = tile * kT;
+        qrow0 = p0;
+        nq = min(kT, N - p0);
         qpos = p0 + 16 * w + qq;
         qtok = qpos < N ? a.perm_q[bh * N + qpos] : -1;
         const int plast = min(p0 + kT, N) - 1;
@@ -247,6 +250,8 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
         qpos = qtok;
         if (qtok >= lend) qtok = -1;
         kend = q0 < lend ? min(q0 + kT, lend) : kbeg;    // a tile past the leaf's real tokens has no work
+        qrow0 = q0;
+        nq = max(0, min(kT, lend - q0));
     }
     const int blk_lo = (MODE == kLeaf) ? 0 : max(0, (qpos / bq - a.nbr) * bq);
     const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), (qpos / bq + 1 + a.nbr) * bq);
@@ -357,49 +362,68 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
         return;
     }
     // dQ = this pass + the low-rank part (W' from LDS) + (leaf) the partials
-    // of the levels where the query was a future query, added in that order;
-    // the partial rows are fetched two at a time so their loads are in
-    // flight together.  The low-rank part is a product across the wave's
-    // lanes, so every lane takes part (a lane without a query uses row 0 and
-    // discards the result).
+    // of the levels where the query was a future query, added in that order.
+    // The low-rank part is a product across the wave's lanes, so every lane
+    // takes part (a lane without a query uses row 0 and discards the
+    // result).  The rest runs on whole rows: the float32 sums go to LDS (the
+    // tile and W' space is free now) as rows [query][d], and each thread
+    // then adds 8 consecutive elements of the partial rows (two levels at a
+    // time) and stores them, so a row moves as 16-byte pieces.
     const size_t row = bh * N + max(qtok, 0);
     F duf[2];
     du_frags<T>((const S*)a.du_q + row * a.wk, a.wk, g, duf);
     f32x4 tot[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) tot[dt] = acc[dt] * a.tau + lowrank_lds<T, D>(duf, swt, a.wk, g, qq, dt);
-    if (qtok < 0) return;
+    constexpr int RS = D + 4;                     // LDS row stride (floats)
+    static_assert(MODE == kLevels || 64 * RS * 4 <= dq_lds_bytes<T, D, MODE>(WtStage<T, D>::kMaxWk),
+                  "row sums fit in the pass's LDS");
+    float* const eq = (float*)smem;
+    __syncthreads();                              // every wave is done with the tiles and W'
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) *(f32x4*)&eq[(16 * w + qq) * RS + 16 * dt + 4 * g] = tot[dt];
+    __syncthreads();
+    if (nq <= 0) return;
+    constexpr int PPR = D / 8, RPP = kThreads / PPR, NPASS = 64 / RPP;
+    const int c8 = 8 * ((int)threadIdx.x % PPR);
+    // rows past the tile's queries read the first query's rows (loads
+    // without a branch) and store nothing
+    const int tok0 = MODE == kLeaf ? qrow0 : a.perm_q[bh * N + qrow0];
+    int tokr[NPASS], tokl[NPASS];
+    float s8[NPASS][8];
+#pragma unroll
+    for (int ps = 0; ps < NPASS; ++ps) {
+        const int r = ps * RPP + (int)threadIdx.x / PPR;
+        tokr[ps] = r < nq ? (MODE == kLeaf ? qrow0 + r : a.perm_q[bh * N + qrow0 + r]) : -1;
+        tokl[ps] = tokr[ps] >= 0 ? tokr[ps] : tok0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s8[ps][e] = eq[r * RS + c8 + e];
+    }
     const int leaf = tile / a.lt.per_leaf;
     unsigned lmask = MODE == kLeaf ? leaf_levels(a.lt, leaf, true) : 0u;
     while (lmask) {
-        const S* src[2];
+        int64_t base[2];
         bool use[2];
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-            src[j] = (const S*)a.part_dq;
             use[j] = lmask != 0;
+            base[j] = 0;
             if (use[j]) {
                 const int l = __builtin_ctz(lmask);
                 lmask &= lmask - 1;
-                const int64_t base = seg_slot_base(a.lt, bh, l, leaf >> (a.Lv - l), true);
-                src[j] = (const S*)a.part_dq + (size_t)(base + qtok) * D;
+                base[j] = seg_slot_base(a.lt, bh, l, leaf >> (a.Lv - l), true);
             }
         }
-        f32x4 x[2][DT];
 #pragma unroll
         for (int j = 0; j < 2; ++j)
             if (use[j])
 #pragma unroll
-                for (int dt = 0; dt < DT; ++dt) x[j][dt] = load4<T>(src[j] + 16 * dt + 4 * g);
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-            if (use[j])
-#pragma unroll
-                for (int dt = 0; dt < DT; ++dt) tot[dt] += x[j][dt];
+                for (int ps = 0; ps < NPASS; ++ps)
+                    add8<T>((const S*)a.part_dq + (size_t)(base[j] + tokl[ps]) * D + c8, s8[ps]);
     }
-    S* out = (S*)a.dQ + row * D;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) store4<T>(out + 16 * dt + 4 * g, tot[dt]);
+    for (int ps = 0; ps < NPASS; ++ps)
+        if (tokr[ps] >= 0) store8<T>((S*)a.dQ + (bh * N + tokr[ps]) * D + c8, s8[ps]);
 }
 
 // ------------------------------------------------------------------------
