@@ -170,6 +170,75 @@ template <> struct Raw4<BF16> {
     }
 };
 
+// x[e] += the 8 storage-dtype elements at p (16-byte aligned in bf16).
+template <class T>
+__device__ __forceinline__ void add8(const typename T::store_t* p, float (&x)[8])
+{
+    if constexpr (T::bytes == 2) {
+        const uint4 v = *(const uint4*)p;
+        const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            x[2 * i] += bf16_to_f32(u[i] & 0xffffu);
+            x[2 * i + 1] += bf16_to_f32(u[i] >> 16);
+        }
+    } else {
+        const f32x4 a = *(const f32x4*)p, b = *(const f32x4*)(p + 4);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            x[i] += a[i];
+            x[4 + i] += b[i];
+        }
+    }
+}
+
+// 8 consecutive elements of the storage dtype from float32, one 16-byte
+// store in bf16.
+template <class T>
+__device__ __forceinline__ void store8(typename T::store_t* p, const float (&x)[8])
+{
+    if constexpr (T::bytes == 2) {
+        uint32_t u[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) u[i] = (uint32_t)T::store(x[2 * i]) | ((uint32_t)T::store(x[2 * i + 1]) << 16);
+        *(uint4*)p = make_uint4(u[0], u[1], u[2], u[3]);
+    } else {
+        *(f32x4*)p = f32x4{x[0], x[1], x[2], x[3]};
+        *(f32x4*)(p + 4) = f32x4{x[4], x[5], x[6], x[7]};
+    }
+}
+
+// Eight consecutive storage-dtype elements loaded as they are (16 bytes in
+// bf16), and their float32 values.
+template <class T> struct Raw8 {
+    struct type { f32x4 a, b; };
+    __device__ static __forceinline__ type ld(const typename T::store_t* p)
+    {
+        return type{*(const f32x4*)p, *(const f32x4*)(p + 4)};
+    }
+    __device__ static __forceinline__ void val(type v, float (&x)[8])
+    {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            x[i] = v.a[i];
+            x[4 + i] = v.b[i];
+        }
+    }
+};
+template <> struct Raw8<BF16> {
+    using type = uint4;
+    __device__ static __forceinline__ type ld(const uint16_t* p) { return *(const uint4*)p; }
+    __device__ static __forceinline__ void val(type v, float (&x)[8])
+    {
+        const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            x[2 * i] = bf16_to_f32(u[i] & 0xffffu);
+            x[2 * i + 1] = bf16_to_f32(u[i] >> 16);
+        }
+    }
+};
+
 // 16-byte global load / store of raw bytes.
 __device__ __forceinline__ uint4 ldg16(const void* p) { return *(const uint4*)p; }
 __device__ __forceinline__ void stg16(void* p, uint4 v) { *(uint4*)p = v; }

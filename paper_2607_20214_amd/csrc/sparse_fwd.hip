@@ -75,8 +75,10 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
     constexpr int DT = D / 16;   // 16-wide tiles of the head dim
     using Tl = tile::Tile<T, D>;
     constexpr int PT = Tl::PER_THREAD;
-    __shared__ __attribute__((aligned(16))) S sk[Tl::elems(kKT)];
-    __shared__ __attribute__((aligned(16))) S sv[Tl::elems(kKT)];
+    // the K and V tiles, one array (the epilogue reuses it whole for rows)
+    __shared__ __attribute__((aligned(16))) S skv[2 * Tl::elems(kKT)];
+    S* const sk = skv;
+    S* const sv = skv + Tl::elems(kKT);
 
     int tile, h, b;
     xcd_tile(tile, h, b);
@@ -101,11 +103,14 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
     int qtok;                           // token index of this lane's query (-1 = none)
     int kbeg, kend;                     // key positions [kbeg, kend) scanned by the tile
     int bq = 1;                         // block size b' (kBlocks / kLevels)
+    int qrow0 = 0, nq = 0;              // kBlocks / kLeaf: first query position of the tile, its queries
     const int32_t* klist = nullptr;     // sorted key list (kBlocks / kLevels)
     // sorted query block t sees the sorted key blocks t - nbr .. t + nbr
     if (MODE == kBlocks) {
         bq = min(a.k, N);
         const int p0 = tile * kQT;
+        qrow0 = p0;
+        nq = min(kQT, N - p0);
         qpos = p0 + 16 * w + qq;
         qtok = qpos < N ? a.perm_q[bh * N + qpos] : -1;
         const int plast = min(p0 + kQT, N) - 1;
@@ -130,6 +135,8 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
         qpos = qtok;
         if (qtok >= lend) qtok = -1;
         kend = q0 < lend ? min(q0 + kQT, lend) : kbeg;   // a tile past the leaf's real tokens has no work
+        qrow0 = q0;
+        nq = max(0, min(kQT, lend - q0));
     }
     const int blk_lo = (MODE == kLeaf) ? 0 : max(0, (qpos / bq - a.nbr) * bq);
     const int blk_hi = (MODE == kLeaf) ? 0 : min((MODE == kBlocks ? N : half), (qpos / bq + 1 + a.nbr) * bq);
@@ -270,82 +277,127 @@ __global__ __launch_bounds__(kThreads, 3) void sparse_fwd_kernel(Args a)
         return;
     }
 
-    // the fusion's row inputs are requested before the level partials are
-    // merged, so their loads share the first round trip
-    const size_t row = bh * N + max(qtok, 0);
-    using R4 = Raw4<T>;
-    typename R4::type olr_raw[DT];
-    float dl = 0.f, lam = a.lambda, gs = 1.f, gl = 1.f;
-    if (qtok >= 0) {
-        const S* olr = (const S*)a.O_lr + row * D;
+    // The rest runs on whole rows: the unnormalised output (relative to the
+    // running max) goes to LDS as rows [query][d] (the tile space is free
+    // now) with the row's running max and denominator, and each thread then
+    // takes 8 consecutive elements of a row, so the level partials, O_lr and
+    // the outputs move as 16-byte pieces with 16 (d_h 128) or 8 lanes
+    // covering a row.
+    constexpr int RS = D + 4;                       // LDS row stride (floats)
+    static_assert(64 * RS * 4 + 2 * 64 * 4 <= sizeof(skv), "row sums fit in the tiles' LDS");
+    float* const eo = (float*)skv;
+    float* const em = eo + 64 * RS;                 // running max (log2 units)
+    float* const el = em + 64;                      // running denominator
+    __syncthreads();                                // every wave is done with the tiles
+    {
+        const int r = 16 * w + qq;
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) olr_raw[dt] = R4::ld(olr + 16 * dt + 4 * g);
-        dl = a.d_lr[row];
-        if (a.lam_rows) lam = a.lam_rows[row];
-        if (a.gates) {
-            gs = a.gates[row * 2 + 0];
-            gl = a.gates[row * 2 + 1];
+        for (int dt = 0; dt < DT; ++dt) *(f32x4*)&eo[r * RS + 16 * dt + 4 * g] = acc[dt];
+        if (g == 0) {
+            em[r] = m_run;
+            el[r] = l_run;
         }
     }
-
-    if (MODE == kLeaf && qtok >= 0) {
+    __syncthreads();
+    if (nq <= 0) return;
+    constexpr int PPR = D / 8, RPP = kThreads / PPR, NPASS = 64 / RPP;
+    const int c8 = 8 * ((int)threadIdx.x % PPR);
+    using R8 = Raw8<T>;
+    // rows past the tile's queries read the first query's rows (loads
+    // without a branch) and store nothing; the fusion's row inputs are
+    // requested before the level partials are merged
+    const int tok0 = MODE == kLeaf ? qrow0 : a.perm_q[bh * N + qrow0];
+    int tokr[NPASS], tokl[NPASS];
+    float o8[NPASS][8], mr[NPASS], lr[NPASS], dl[NPASS], lam[NPASS], gs[NPASS], gl[NPASS];
+    typename R8::type olr[NPASS];
+#pragma unroll
+    for (int ps = 0; ps < NPASS; ++ps) {
+        const int r = ps * RPP + (int)threadIdx.x / PPR;
+        tokr[ps] = r < nq ? (MODE == kLeaf ? qrow0 + r : a.perm_q[bh * N + qrow0 + r]) : -1;
+        tokl[ps] = tokr[ps] >= 0 ? tokr[ps] : tok0;
+        const size_t row = bh * N + tokl[ps];
+        olr[ps] = R8::ld((const S*)a.O_lr + row * D + c8);
+        dl[ps] = a.d_lr[row];
+        lam[ps] = a.lam_rows ? a.lam_rows[row] : a.lambda;
+        gs[ps] = 1.f;
+        gl[ps] = 1.f;
+        if (a.gates) {
+            gs[ps] = a.gates[row * 2 + 0];
+            gl[ps] = a.gates[row * 2 + 1];
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o8[ps][e] = eo[r * RS + c8 + e];
+        mr[ps] = em[r];
+        lr[ps] = el[r];
+    }
+    if (MODE == kLeaf) {
         // merge the partial of every level whose future half holds this leaf,
-        // in level order; the partials are fetched two levels at a time so
-        // their loads are in flight together
+        // in level order, two levels at a time so their loads are in flight
+        // together
         unsigned lmask = leaf_levels(a.lt, tile / a.lt.per_leaf, true);
         while (lmask) {
-            size_t slot[2];
+            int lv[2];
             bool use[2];
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
                 use[j] = lmask != 0;
-                slot[j] = 0;
+                lv[j] = 0;
                 if (use[j]) {
-                    const int l = __builtin_ctz(lmask);
+                    lv[j] = __builtin_ctz(lmask);
                     lmask &= lmask - 1;
-                    slot[j] = bh * (size_t)a.lt.off[a.Lv] + (size_t)level_entry(a.lt, l, qtok, true);
                 }
             }
-            float pl[2];
-            f32x4 v[2][DT];
+            float pl[2][NPASS];
+            typename R8::type v[2][NPASS];
 #pragma unroll
             for (int j = 0; j < 2; ++j)
-                if (use[j]) {
-                    pl[j] = a.part_lse[slot[j]] * kLog2e;
-                    const S* po = (const S*)a.part_o + slot[j] * D;
+                if (use[j])
 #pragma unroll
-                    for (int dt = 0; dt < DT; ++dt) v[j][dt] = load4<T>(po + 16 * dt + 4 * g);
-                }
+                    for (int ps = 0; ps < NPASS; ++ps) {
+                        const size_t slot = bh * (size_t)a.lt.off[a.Lv] + (size_t)level_entry(a.lt, lv[j], tokl[ps], true);
+                        pl[j][ps] = a.part_lse[slot] * kLog2e;
+                        v[j][ps] = R8::ld((const S*)a.part_o + slot * D + c8);
+                    }
 #pragma unroll
             for (int j = 0; j < 2; ++j)
-                if (use[j]) {
-                    const float m_new = fmaxf(m_run, pl[j]);
-                    const float c_old = fast_exp2(m_run - m_new), c_new = fast_exp2(pl[j] - m_new);
+                if (use[j])
 #pragma unroll
-                    for (int dt = 0; dt < DT; ++dt) acc[dt] = acc[dt] * c_old + v[j][dt] * c_new;
-                    l_run = l_run * c_old + c_new;
-                    m_run = m_new;
-                }
+                    for (int ps = 0; ps < NPASS; ++ps) {
+                        const float m_new = fmaxf(mr[ps], pl[j][ps]);
+                        const float c_old = fast_exp2(mr[ps] - m_new), c_new = fast_exp2(pl[j][ps] - m_new);
+                        float x[8];
+                        R8::val(v[j][ps], x);
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) o8[ps][e] = o8[ps][e] * c_old + x[e] * c_new;
+                        lr[ps] = lr[ps] * c_old + c_new;
+                        mr[ps] = m_new;
+                    }
         }
     }
 
     // ---- fusion epilogue (kBlocks, kLeaf) --------------------------------
-    if (qtok < 0) return;
-    const float lse_nat = (m_run + __log2f(l_run)) * kLn2;       // log d_s
-    const float inv_den = 1.f / (l_run + a.eps * fast_exp2(-m_run)); // 1 / (d_s + eps), rescaled
-    const float mf = a.m_one ? 1.f : 1.f / (1.f + __expf(__logf(lam * dl + a.eps) - lse_nat));
-    S* out = (S*)a.O + row * D;
-    float* os = a.O_s + row * D;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-        const int c0 = 16 * dt + 4 * g;
-        const f32x4 o_s = acc[dt] * inv_den;
-        *(f32x4*)(os + c0) = o_s;
-        store4<T>(out + c0, o_s * (gs * mf) + R4::val(olr_raw[dt]) * gl);
-    }
-    if (g == 0) {
-        a.lse[row] = lse_nat;
-        a.m[row] = mf;
+    for (int ps = 0; ps < NPASS; ++ps) {
+        if (tokr[ps] < 0) continue;
+        const size_t row = bh * N + tokr[ps];
+        const float lse_nat = (mr[ps] + __log2f(lr[ps])) * kLn2;          // log d_s
+        const float inv_den = 1.f / (lr[ps] + a.eps * fast_exp2(-mr[ps])); // 1 / (d_s + eps), rescaled
+        const float mf = a.m_one ? 1.f : 1.f / (1.f + __expf(__logf(lam[ps] * dl[ps] + a.eps) - lse_nat));
+        float os[8], ol[8], out[8];
+        R8::val(olr[ps], ol);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            os[e] = o8[ps][e] * inv_den;
+            out[e] = os[e] * (gs[ps] * mf) + ol[e] * gl[ps];
+        }
+        float* po = a.O_s + row * D + c8;
+        *(f32x4*)po = f32x4{os[0], os[1], os[2], os[3]};
+        *(f32x4*)(po + 4) = f32x4{os[4], os[5], os[6], os[7]};
+        store8<T>((S*)a.O + row * D + c8, out);
+        if (c8 == 0) {
+            a.lse[row] = lse_nat;
+            a.m[row] = mf;
+        }
     }
 }
 
