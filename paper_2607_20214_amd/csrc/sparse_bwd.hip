@@ -317,10 +317,30 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
         }
     }
     if (MODE == kLevels) {
-        if (qtok < 0) return;
-        S* out = (S*)a.part_dq + (size_t)(slot0 + qtok) * D;
+        // partial rows through LDS as rows, stored as 16-byte pieces of whole
+        // rows (16 or 8 lanes a row)
+        constexpr int RS = D + 4;
+        static_assert(64 * RS * 4 + 64 * 4 <= dq_lds_bytes<T, D, MODE>(WtStage<T, D>::kMaxWk), "rows fit in LDS");
+        float* const eo = (float*)smem;
+        int* const eq = (int*)(eo + 64 * RS);     // query of each row (-1 = none)
+        __syncthreads();                          // every wave is done with the tiles
+        const int r0 = 16 * w + qq;
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) store4<T>(out + 16 * dt + 4 * g, acc[dt] * a.tau);
+        for (int dt = 0; dt < DT; ++dt) *(f32x4*)&eo[r0 * RS + 16 * dt + 4 * g] = acc[dt] * a.tau;
+        if (g == 0) eq[r0] = qtok;
+        __syncthreads();
+        constexpr int PPR = D / 8, RPP = kThreads / PPR, NPASS = 64 / RPP;
+        const int c8 = 8 * ((int)threadIdx.x % PPR);
+#pragma unroll
+        for (int ps = 0; ps < NPASS; ++ps) {
+            const int r = ps * RPP + (int)threadIdx.x / PPR;
+            const int q = eq[r];
+            if (q < 0) continue;
+            float x[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) x[e] = eo[r * RS + c8 + e];
+            store8<T>((S*)a.part_dq + (size_t)(slot0 + q) * D + c8, x);
+        }
         return;
     }
     // dQ = this pass + the low-rank part (W' from LDS) + (leaf) the partials
@@ -603,12 +623,36 @@ __device__ __forceinline__ void sparse_dkv_body(const BArgs& a, int tile, int h,
     }
 
     if (MODE == kLevels) {
-        if (ktok < 0) return;
-        const size_t slot = (size_t)(slot0 + ktok);
+        // partial rows through LDS as rows, stored as 16-byte pieces of whole
+        // rows (16 or 8 lanes a row)
+        constexpr int RS = D + 4;
+        static_assert(2 * 64 * RS * 4 + 64 * 4 <= dkv_lds_bytes<T, D, MODE>(WtStage<T, D>::kMaxWk) ||
+                      64 * RS * 4 + 64 * 4 <= dkv_lds_bytes<T, D, MODE>(WtStage<T, D>::kMaxWk), "rows fit in LDS");
+        float* const eo = (float*)smem;
+        int* const ek = (int*)(eo + 64 * RS);     // key of each row (-1 = none)
+        const int r0 = 16 * w + col;
+        constexpr int PPR = D / 8, RPP = kThreads / PPR, NPASS = 64 / RPP;
+        const int c8 = 8 * ((int)threadIdx.x % PPR);
+        // dK, then dV through the same rows
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-            store4<T>((S*)a.part_dk + slot * D + 16 * dt + 4 * g, akT[dt] * a.tau);
-            store4<T>((S*)a.part_dv + slot * D + 16 * dt + 4 * g, avT[dt]);
+        for (int part = 0; part < 2; ++part) {
+            __syncthreads();                      // the tiles (or the previous part's rows) are done with
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+                *(f32x4*)&eo[r0 * RS + 16 * dt + 4 * g] = part == 0 ? akT[dt] * a.tau : avT[dt];
+            if (g == 0) ek[r0] = ktok;
+            __syncthreads();
+            S* dst = (S*)(part == 0 ? a.part_dk : a.part_dv);
+#pragma unroll
+            for (int ps = 0; ps < NPASS; ++ps) {
+                const int r = ps * RPP + (int)threadIdx.x / PPR;
+                const int k = ek[r];
+                if (k < 0) continue;
+                float x[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) x[e] = eo[r * RS + c8 + e];
+                store8<T>(dst + (size_t)(slot0 + k) * D + c8, x);
+            }
         }
         return;
     }
