@@ -46,13 +46,14 @@ struct BArgs {
     const void* wt_hi;        // W' = W_hi' + W_lo' per head, storage dtype [H][D][wk]
     const void* wt_lo;
     const void* dv_lr;        // storage dtype [BHN][D] low-rank dV
-    void* part_dq;            // [BH][Lv][N/2][D] per-level partials, storage dtype
+    void* part_dq;            // [BH][Lv][N/2][dq_halves][D] per-level partials, storage dtype
     void* part_dk;
     void* part_dv;
     void* dQ;
     void* dK;
     void* dV;
     int H, N, k, Lv, wk;
+    int dq_halves;            // 2: 256-key blocks as two 128-key halves, one dQ partial row each
     LevelTiles lt;            // causal recursion geometry and tile numbering
     int nbr;                  // neighbouring sorted blocks on each side
     int nbx, nblk;            // whole-block kernel: blocks per head, blocks in all
@@ -400,8 +401,11 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
         for (int j = 0; j < 2; ++j)
             if (use[j])
 #pragma unroll
-                for (int ps = 0; ps < NPASS; ++ps)
-                    add8<T>((const S*)a.part_dq + (size_t)(base[j] + tokl[ps]) * D + c8, s8[ps]);
+                for (int ps = 0; ps < NPASS; ++ps) {
+                    const S* pr = (const S*)a.part_dq + (size_t)(base[j] + tokl[ps]) * a.dq_halves * D + c8;
+                    add8<T>(pr, s8[ps]);
+                    if (a.dq_halves == 2) add8<T>(pr + D, s8[ps]);   // second key half of a 256-key block
+                }
     }
 #pragma unroll
     for (int ps = 0; ps < NPASS; ++ps)
@@ -816,18 +820,29 @@ __global__ __launch_bounds__(kThreads, (two_pass_waves<T, D>())) void sparse_lea
 // and stores there carry no per-row branch and the compiler can wait for
 // exactly the loads it needs (its memory counter retires in order).
 // ------------------------------------------------------------------------
-// waves per SIMD: three for 64-query blocks at d_h 64, two otherwise (a
-// 128-query block is 8 waves, two per SIMD)
+//
+// Blocks of QB = 256 (the levels only) are two work items of 128 keys each:
+// the workgroup of key half c streams all 256 queries of the block, so dK and
+// dV of its keys are complete, and its dQ partial (from its 128 keys) goes to
+// row c of the query's pair of dQ partial rows, which the leaf adds.  The
+// two halves of a block are items id and id + 8: on workgroups of one XCD
+// (workgroups are dealt to the 8 XCDs in turn), whose L2 serves the block's
+// query rows to the second.
+//
+// waves per SIMD: three for 64-key blocks at d_h 64, two otherwise (a
+// 128-key block is 8 waves, two per SIMD)
 template <int D, int BQ>
 constexpr int block_waves() { return BQ == 64 && D == 64 ? 3 : 2; }
 
-template <class T, int D, int BQ, int MODE>
+template <class T, int D, int BQ, int MODE, int QB = BQ>
 __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_block_kernel(BArgs a)
 {
     using S = typename T::store_t;
     using F = typename T::frag_t;
     constexpr int NW = BQ / 16, NT = 64 * NW;
-    constexpr int KS = D / 32, DT = D / 16, NQT = BQ / 64;
+    constexpr int KS = D / 32, DT = D / 16, NQT = QB / 64, NKT = BQ / 64;
+    constexpr int HALVES = QB / BQ;                       // work items per block
+    static_assert(HALVES == 1 || (HALVES == 2 && MODE == kLevels), "key halves: levels only");
     using TD = tile::Tile<T, D, NT>;        // Q, dO, K tiles (rows of D)
     using TS = tile::Tile<T, 64, NT>;       // dS^T tile (BQ rows of 64 queries)
     constexpr int PT = TD::PER_THREAD;
@@ -860,6 +875,7 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
     struct Blk {
         size_t bh;
         int nv;
+        int half;                                    // key half of a 256-key block (0 otherwise)
         int64_t qslot, kslot;                        // levels: partial rows of token t at qslot + t (as a
                                                      // query) and kslot + t (as a key)
         const int32_t* ql;
@@ -867,19 +883,34 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
     };
     auto block_of = [&](int id) {
         Blk k;
-        const int x = id % a.nbx;
-        k.bh = (size_t)(id / a.nbx);                     // b * H + h
+        // key halves: items 16 j + i and 16 j + 8 + i (i < 8) are the two
+        // halves of block 8 j + i; past the last whole group of 8 blocks,
+        // items 2 m and 2 m + 1 are the halves of the next block m
+        int item = id;
+        k.half = 0;
+        if (HALVES == 2) {
+            const int whole = (a.nblk >> 4) << 4;
+            if (id < whole) {
+                item = (id >> 4) * 8 + (id & 7);
+                k.half = (id >> 3) & 1;
+            } else {
+                item = (whole >> 1) + ((id - whole) >> 1);
+                k.half = (id - whole) & 1;
+            }
+        }
+        const int x = item % a.nbx;
+        k.bh = (size_t)(item / a.nbx);                   // b * H + h
         if (MODE == kLevels) {
             // (whole-block levels are never padded: N / 2 entries per level)
-            const int per_level = (N / 2) / BQ;
+            const int per_level = (N / 2) / QB;
             const int level = x / per_level;
             const int t = x - level * per_level;
-            const size_t base = k.bh * (size_t)a.lt.off[a.Lv] + (size_t)a.lt.off[level] + (size_t)t * BQ;
+            const size_t base = k.bh * (size_t)a.lt.off[a.Lv] + (size_t)a.lt.off[level] + (size_t)t * QB;
             k.ql = a.perm_q + base;
-            k.kl = a.perm_k + base;
+            k.kl = a.perm_k + base + k.half * BQ;
             k.nv = BQ;
-            // a block never straddles a segment (the half length is a multiple of BQ)
-            const int seg = t * BQ / a.lt.len[level + 1];
+            // a block never straddles a segment (the half length is a multiple of QB)
+            const int seg = t * QB / a.lt.len[level + 1];
             k.qslot = seg_slot_base(a.lt, k.bh, level, seg, true);
             k.kslot = seg_slot_base(a.lt, k.bh, level, seg, false);
         } else {
@@ -893,7 +924,7 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
     };
     // index lists of a block: K tile rows, this lane's key, every query tile
     struct Idx {
-        int ktk[NQT][PT];
+        int ktk[NKT][PT];
         int ktok;
         int qtk[NQT][PT];
         int qt1[NQT];                                    // query 64 qt + (tx % 64) (scalars, dQ rows)
@@ -903,7 +934,7 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
     // so their entries are not held in registers across the block change)
     auto indices_k = [&](const Blk& k, Idx& ix) {
 #pragma unroll
-        for (int t = 0; t < NQT; ++t)
+        for (int t = 0; t < NKT; ++t)
 #pragma unroll
             for (int j = 0; j < PT; ++j) {
                 const int r = 64 * t + TD::row_of(j, tx);
@@ -920,10 +951,10 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
         const int r = 64 * t + (tx & 63);
         ix.qt1[t] = (kFull || r < k.nv) ? k.ql[(uint32_t)r] : -1;
     };
-    auto kload = [&](size_t bh, const Idx& ix, uint4 (&rk)[NQT][PT]) {
+    auto kload = [&](size_t bh, const Idx& ix, uint4 (&rk)[NKT][PT]) {
         const S* K = (const S*)a.K + bh * N * D;
 #pragma unroll
-        for (int t = 0; t < NQT; ++t) {
+        for (int t = 0; t < NKT; ++t) {
             if constexpr (kFull) TD::load_all(K, ix.ktk[t], rk[t], tx);
             else TD::load(K, ix.ktk[t], rk[t], tx);
         }
@@ -996,7 +1027,7 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
     Idx ix;
     indices_k(blk, ix);
     indices_q(blk, ix, 0);
-    uint4 rk[NQT][PT];
+    uint4 rk[NKT][PT];
     F vf[KS];
     kload(blk.bh, ix, rk);
     vload(blk.bh, ix.ktok, vf);
@@ -1011,10 +1042,11 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
         lanes();
         const size_t bh = blk.bh;
         const int64_t qslot = blk.qslot, kslot = blk.kslot;
+        const int half = blk.half;
         const int ktok = ix.ktok;
         if (!first) __syncthreads();                     // the previous block's dQ phase is done with LDS
 #pragma unroll
-        for (int t = 0; t < NQT; ++t) TD::store(sk, rk[t], 64 * t, tx);
+        for (int t = 0; t < NKT; ++t) TD::store(sk, rk[t], 64 * t, tx);
         // (this lane's K row is read from the block's K tile when needed)
 
         const int nid = id + gridDim.x;
@@ -1134,7 +1166,7 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
                 const int d0 = 16 * dt + 4 * g;
                 if (MODE == kLevels) {
                     if (!kFull && qtok < 0) continue;
-                    S* out = (S*)a.part_dq + (size_t)(qslot + qtok) * D + d0;
+                    S* out = (S*)a.part_dq + ((size_t)(qslot + qtok) * HALVES + half) * D + d0;
                     store4<T>(out, dq[u] * a.tau);
                 } else {
                     // the low-rank part is a product across the wave's lanes:
@@ -1162,11 +1194,11 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
 
 // Whole-block launch: as many workgroups as the device runs at once (cached
 // per instantiation and device), each walking its share of the blocks.
-template <class T, int D, int BQ, int MODE>
+template <class T, int D, int BQ, int MODE, int QB = BQ>
 void launch_blocks(const char* name, BArgs a, int nbx, int BH, hipStream_t st)
 {
     static int resident[64] = {0};
-    auto kern = sparse_bwd_block_kernel<T, D, BQ, MODE>;
+    auto kern = sparse_bwd_block_kernel<T, D, BQ, MODE, QB>;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = 0;
     int& res = resident[dev & 63];
@@ -1178,10 +1210,20 @@ void launch_blocks(const char* name, BArgs a, int nbx, int BH, hipStream_t st)
         res = cus * per;
     }
     a.nbx = nbx;
-    a.nblk = nbx * BH;
+    a.nblk = nbx * BH * (QB / BQ);                       // work items (key halves of QB = 256)
     const int grid = a.nblk < res ? a.nblk : res;
     ELSAA_LAUNCH(name, kern, dim3(grid), dim3(BQ * 4), 0, st, a);
 }
+
+}  // namespace
+
+bool sparse_bwd_split_dq(const Shape& s)
+{
+    return s.causal && s.bf16 && s.Lv > 0 && s.k == 256 && s.neighbors == 0 && !s.lt.padded &&
+           s.n_leaf % 256 == 0;
+}
+
+namespace {
 
 template <class T, int D>
 hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
@@ -1219,6 +1261,12 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
             const int nbx = s.Lv * (s.N / 2) / bq;
             if (bq == 64) launch_blocks<T, D, 64, kLevels>("sparse_bwd_levels", a, nbx, s.B * s.H, st);
             else if constexpr (T::bytes == 2) launch_blocks<T, D, 128, kLevels>("sparse_bwd_levels", a, nbx, s.B * s.H, st);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        } else if (sparse_bwd_split_dq(s)) {
+            // 256-key blocks as two 128-key halves, dQ partials in two parts
+            const int nbx = s.Lv * (s.N / 2) / 256;
+            if constexpr (T::bytes == 2)
+                launch_blocks<T, D, 128, kLevels, 256>("sparse_bwd_levels", a, nbx, s.B * s.H, st);
             if ((e = hipGetLastError()) != hipSuccess) return e;
         } else {
             dim3 grid(a.lt.first[s.Lv], s.H, s.B);
@@ -1259,6 +1307,7 @@ hipError_t launch_sparse_bwd(const Shape& s, const void* Q, const void* K, const
     a.du_q = du_q; a.du_k = du_k; a.wt_hi = wt_hi; a.wt_lo = wt_lo; a.dv_lr = dv_lr;
     a.wk = race_wk(s);
     a.part_dq = part_dq; a.part_dk = part_dk; a.part_dv = part_dv;
+    a.dq_halves = sparse_bwd_split_dq(s) ? 2 : 1;
     a.dQ = dQ; a.dK = dK; a.dV = dV;
     a.H = s.H; a.N = s.N; a.k = s.k; a.Lv = s.Lv;
     a.lt = s.lt;

@@ -47,6 +47,11 @@ SMALL = [
     _w("c-bf16-d64-padded-1001", 1, 2, 1001, 64, 64, 64, True, "bf16"),
     _w("c-bf16-d128-padded-777-k32", 1, 1, 777, 128, 32, 64, True, "bf16", recipe="clustered"),
     _w("c-f32-d64-padded-300-k32", 1, 1, 300, 64, 32, 32, True, "f32"),
+    # b = 256 levels as two 128-key halves (two dQ partials per level): whole
+    # groups of 8 blocks, d_h 64, and the tail of the item order (10 blocks)
+    _w("c-bf16-d128-k256-4096", 1, 2, 4096, 128, 256, 128, True, "bf16"),
+    _w("c-bf16-d64-k256-2048-clustered", 1, 2, 2048, 64, 256, 64, True, "bf16", recipe="clustered"),
+    _w("c-bf16-d128-k256-1024-h5", 1, 5, 1024, 128, 256, 64, True, "bf16"),
 ]
 
 
