@@ -125,22 +125,13 @@ def kernel_model(w, Lv: int) -> dict:
     ps = s                          # level partials are kept in the storage dtype
     lvl_pos = Lv * bh * half        # (level, position) slots of the partials
     wk = max(32, 4 * w.L)
-    # 256-key blocks run as two 128-key halves, each with its own dQ partial
-    nq = 2 if split_dq(w, Lv) else 1
     return {
         "sparse_fwd_levels": lvl_pos * (3 * D * s + 8 + D * ps + 4),
         "sparse_fwd_leaf": bh * N * (3 * D * s + 4 * D + D * s + 4 + D * s + 8) + lvl_pos * (D * ps + 4),
-        "sparse_bwd_levels": lvl_pos * (4 * D * s + 20 + (2 + nq) * D * ps),
-        "sparse_leaf_bwd": bh * N * (4 * D * s + 12 + 2 * wk * s + D * s + 3 * D * s) + lvl_pos * (2 + nq) * D * ps,
+        "sparse_bwd_levels": lvl_pos * (4 * D * s + 20 + 3 * D * ps),
+        "sparse_leaf_bwd": bh * N * (4 * D * s + 12 + 2 * wk * s + D * s + 3 * D * s) + lvl_pos * 3 * D * ps,
     }
 
-
-def split_dq(w, Lv: int) -> bool:
-    """Whether the level backward runs 256-key blocks as two 128-key halves
-    (causal bf16, b = 256, no neighbours, no padded level: the library's own
-    rule), which doubles the dQ level partials."""
-    return (w.causal and w.dtype == "bf16" and w.k == 256 and getattr(w, "neighbors", 0) == 0 and Lv > 0
-            and w.N % (1 << Lv) == 0 and (w.N >> Lv) % 256 == 0)
 
 
 def source_digest(names) -> str:

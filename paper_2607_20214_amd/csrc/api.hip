@@ -179,8 +179,7 @@ BwdWorkspace bwd_workspace(const Shape& s)
     W.du_q = off; off = align256(off + bhn * race_wk(s) * (s.bf16 ? 2 : 4));
     W.du_k = off; off = align256(off + bhn * race_wk(s) * (s.bf16 ? 2 : 4));
     W.dv_lr = off; off = align256(off + bhn * s.D * (s.bf16 ? 2 : 4));   // storage dtype
-    // storage dtype; two dQ rows per entry where 256-key blocks run as two halves
-    W.part_dq = off; off = align256(off + npart * (sparse_bwd_split_dq(s) ? 2 : 1) * s.D * (s.bf16 ? 2 : 4));
+    W.part_dq = off; off = align256(off + npart * s.D * (s.bf16 ? 2 : 4));   // storage dtype
     W.part_dk = off; off = align256(off + npart * s.D * (s.bf16 ? 2 : 4));
     W.part_dv = off; off = align256(off + npart * s.D * (s.bf16 ? 2 : 4));
     W.total = off;

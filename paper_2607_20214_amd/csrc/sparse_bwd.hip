@@ -46,14 +46,13 @@ struct BArgs {
     const void* wt_hi;        // W' = W_hi' + W_lo' per head, storage dtype [H][D][wk]
     const void* wt_lo;
     const void* dv_lr;        // storage dtype [BHN][D] low-rank dV
-    void* part_dq;            // [BH][Lv][N/2][dq_halves][D] per-level partials, storage dtype
+    void* part_dq;            // [BH][Lv][N/2][D] per-level partials, storage dtype
     void* part_dk;
     void* part_dv;
     void* dQ;
     void* dK;
     void* dV;
     int H, N, k, Lv, wk;
-    int dq_halves;            // 2: 256-key blocks as two 128-key halves, one dQ partial row each
     LevelTiles lt;            // causal recursion geometry and tile numbering
     int nbr;                  // neighbouring sorted blocks on each side
     int nbx, nblk;            // whole-block kernel: blocks per head, blocks in all
@@ -402,9 +401,7 @@ __device__ __forceinline__ void sparse_dq_body(const BArgs& a, int tile, int h, 
             if (use[j])
 #pragma unroll
                 for (int ps = 0; ps < NPASS; ++ps) {
-                    const S* pr = (const S*)a.part_dq + (size_t)(base[j] + tokl[ps]) * a.dq_halves * D + c8;
-                    add8<T>(pr, s8[ps]);
-                    if (a.dq_halves == 2) add8<T>(pr + D, s8[ps]);   // second key half of a 256-key block
+                    add8<T>((const S*)a.part_dq + (size_t)(base[j] + tokl[ps]) * D + c8, s8[ps]);
                 }
     }
 #pragma unroll
@@ -821,13 +818,13 @@ __global__ __launch_bounds__(kThreads, (two_pass_waves<T, D>())) void sparse_lea
 // exactly the loads it needs (its memory counter retires in order).
 // ------------------------------------------------------------------------
 //
-// Blocks of QB = 256 (the levels only) are two work items of 128 keys each:
-// the workgroup of key half c streams all 256 queries of the block, so dK and
-// dV of its keys are complete, and its dQ partial (from its 128 keys) goes to
-// row c of the query's pair of dQ partial rows, which the leaf adds.  The
-// two halves of a block are items id and id + 8: on workgroups of one XCD
-// (workgroups are dealt to the 8 XCDs in turn), whose L2 serves the block's
-// query rows to the second.
+// Blocks of QB = 256 (the levels only) are two consecutive work items of one
+// workgroup, one per 128-key half: each streams all 256 queries of the block
+// (the second time from the compute unit's caches), so dK and dV of the
+// half's keys are complete.  The first half's dQ tiles wait in LDS (bf16,
+// each thread keeps the values it will add itself) and the second half adds
+// them before storing the block's dQ partials, so each level entry still has
+// one dQ partial row.
 //
 // waves per SIMD: three for 64-key blocks at d_h 64, two otherwise (a
 // 128-key block is 8 waves, two per SIMD)
@@ -843,6 +840,9 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
     constexpr int KS = D / 32, DT = D / 16, NQT = QB / 64, NKT = BQ / 64;
     constexpr int HALVES = QB / BQ;                       // work items per block
     static_assert(HALVES == 1 || (HALVES == 2 && MODE == kLevels), "key halves: levels only");
+    constexpr int PER_WQ = DT * 4 / NW;                   // dQ output tiles per wave and query tile
+    // the first key half's dQ tiles, thread by thread (bf16, 4 values per tile)
+    __shared__ __attribute__((aligned(16))) S sdq[HALVES == 2 ? NQT * PER_WQ * NT * 4 : 1];
     using TD = tile::Tile<T, D, NT>;        // Q, dO, K tiles (rows of D)
     using TS = tile::Tile<T, 64, NT>;       // dS^T tile (BQ rows of 64 queries)
     constexpr int PT = TD::PER_THREAD;
@@ -883,21 +883,9 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
     };
     auto block_of = [&](int id) {
         Blk k;
-        // key halves: items 16 j + i and 16 j + 8 + i (i < 8) are the two
-        // halves of block 8 j + i; past the last whole group of 8 blocks,
-        // items 2 m and 2 m + 1 are the halves of the next block m
-        int item = id;
-        k.half = 0;
-        if (HALVES == 2) {
-            const int whole = (a.nblk >> 4) << 4;
-            if (id < whole) {
-                item = (id >> 4) * 8 + (id & 7);
-                k.half = (id >> 3) & 1;
-            } else {
-                item = (whole >> 1) + ((id - whole) >> 1);
-                k.half = (id - whole) & 1;
-            }
-        }
+        // key halves: items 2 m and 2 m + 1 are the halves of block m
+        const int item = HALVES == 1 ? id : id >> 1;
+        k.half = HALVES == 1 ? 0 : id & 1;
         const int x = item % a.nbx;
         k.bh = (size_t)(item / a.nbx);                   // b * H + h
         if (MODE == kLevels) {
@@ -1022,7 +1010,9 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
         }
     };
 
-    int id = blockIdx.x;
+    // items of this workgroup: id, id + gridDim.x, ... (key halves: the two
+    // halves of blocks blockIdx.x, blockIdx.x + gridDim.x, ... in turn)
+    int id = HALVES == 1 ? (int)blockIdx.x : 2 * (int)blockIdx.x;
     Blk blk = block_of(id);
     Idx ix;
     indices_k(blk, ix);
@@ -1049,7 +1039,7 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
         for (int t = 0; t < NKT; ++t) TD::store(sk, rk[t], 64 * t, tx);
         // (this lane's K row is read from the block's K tile when needed)
 
-        const int nid = id + gridDim.x;
+        const int nid = HALVES == 1 ? id + (int)gridDim.x : ((id & 1) ? id - 1 + 2 * (int)gridDim.x : id + 1);
         const bool has_next = nid < a.nblk;
         Blk nblk = blk;
         Idx nix;
@@ -1166,8 +1156,17 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
                 const int d0 = 16 * dt + 4 * g;
                 if (MODE == kLevels) {
                     if (!kFull && qtok < 0) continue;
-                    S* out = (S*)a.part_dq + ((size_t)(qslot + qtok) * HALVES + half) * D + d0;
-                    store4<T>(out, dq[u] * a.tau);
+                    f32x4 v = dq[u] * a.tau;
+                    if constexpr (HALVES == 2) {
+                        S* keep = sdq + (((qt * PER_WQ + u) * NT) + tx) * 4;
+                        if (half == 0) {                 // first key half: kept for the second
+                            store4<T>(keep, v);
+                            continue;
+                        }
+                        v += load4<T>(keep);
+                    }
+                    S* out = (S*)a.part_dq + (size_t)(qslot + qtok) * D + d0;
+                    store4<T>(out, v);
                 } else {
                     // the low-rank part is a product across the wave's lanes:
                     // every lane takes part (a lane without a query uses row 0)
@@ -1211,7 +1210,8 @@ void launch_blocks(const char* name, BArgs a, int nbx, int BH, hipStream_t st)
     }
     a.nbx = nbx;
     a.nblk = nbx * BH * (QB / BQ);                       // work items (key halves of QB = 256)
-    const int grid = a.nblk < res ? a.nblk : res;
+    const int blocks = nbx * BH;                         // a workgroup starts at a block's first item
+    const int grid = blocks < res ? blocks : res;
     ELSAA_LAUNCH(name, kern, dim3(grid), dim3(BQ * 4), 0, st, a);
 }
 
@@ -1307,7 +1307,6 @@ hipError_t launch_sparse_bwd(const Shape& s, const void* Q, const void* K, const
     a.du_q = du_q; a.du_k = du_k; a.wt_hi = wt_hi; a.wt_lo = wt_lo; a.dv_lr = dv_lr;
     a.wk = race_wk(s);
     a.part_dq = part_dq; a.part_dk = part_dk; a.part_dv = part_dv;
-    a.dq_halves = sparse_bwd_split_dq(s) ? 2 : 1;
     a.dQ = dQ; a.dK = dK; a.dV = dV;
     a.H = s.H; a.N = s.N; a.k = s.k; a.Lv = s.Lv;
     a.lt = s.lt;
