@@ -831,7 +831,7 @@ __global__ __launch_bounds__(kThreads, (two_pass_waves<T, D>())) void sparse_lea
 template <int D, int BQ>
 constexpr int block_waves() { return BQ == 64 && D == 64 ? 3 : 2; }
 
-template <class T, int D, int BQ, int MODE, int QB = BQ>
+template <class T, int D, int BQ, int MODE, int QB = BQ, bool FULL = MODE == kLevels>
 __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_block_kernel(BArgs a)
 {
     using S = typename T::store_t;
@@ -846,7 +846,13 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
     using TD = tile::Tile<T, D, NT>;        // Q, dO, K tiles (rows of D)
     using TS = tile::Tile<T, 64, NT>;       // dS^T tile (BQ rows of 64 queries)
     constexpr int PT = TD::PER_THREAD;
-    constexpr bool kFull = MODE == kLevels;  // every block holds BQ valid queries and keys
+    // every block holds QB valid queries and BQ valid keys (the levels, unless
+    // a level's half length is not a multiple of QB: then its last block is short)
+    constexpr bool kFull = FULL;
+    static_assert(!FULL || MODE == kLevels, "full blocks: levels only");
+    // levels: rows past a short block's entries are loaded from its last
+    // entry (a real row, masked out), so the row loads carry no branch
+    constexpr bool kClamp = MODE == kLevels;
     static_assert(TS::elems(BQ) <= 2 * TD::elems(64), "dS^T fits in the query tiles");
     __shared__ __attribute__((aligned(16))) S sk[TD::elems(BQ)];
     __shared__ __attribute__((aligned(16))) S sqo[2 * TD::elems(64)];   // Q tile, dO tile; later dS^T
@@ -874,7 +880,7 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
     // ---- block id -> head and the sorted positions [p0, p0 + nv) of its lists
     struct Blk {
         size_t bh;
-        int nv;
+        int nv, nvk;                                 // valid queries, valid keys of the item
         int half;                                    // key half of a 256-key block (0 otherwise)
         int64_t qslot, kslot;                        // levels: partial rows of token t at qslot + t (as a
                                                      // query) and kslot + t (as a key)
@@ -888,7 +894,26 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
         k.half = HALVES == 1 ? 0 : id & 1;
         const int x = item % a.nbx;
         k.bh = (size_t)(item / a.nbx);                   // b * H + h
-        if (MODE == kLevels) {
+        if (MODE == kLevels && !FULL) {
+            // level lists of any even length: ceil(h / QB) blocks per list of
+            // h entries, the last one short (no zero tokens: unpadded levels)
+            int level = 0, first = 0;
+            for (;;) {
+                const int cnt = ((a.lt.len[level + 1] + QB - 1) / QB) << level;
+                if (x < first + cnt || level + 1 >= a.Lv) break;
+                first += cnt;
+                ++level;
+            }
+            const int h = a.lt.len[level + 1], nbs = (h + QB - 1) / QB;
+            const int j = x - first, seg = j / nbs, p0 = (j - seg * nbs) * QB;
+            const size_t base = k.bh * (size_t)a.lt.off[a.Lv] + (size_t)a.lt.off[level] + (size_t)seg * h + p0;
+            k.nv = min(QB, h - p0);
+            k.nvk = max(0, min(BQ, k.nv - k.half * BQ));
+            k.ql = a.perm_q + base;
+            k.kl = a.perm_k + base + (k.nvk > 0 ? k.half * BQ : 0);   // (no keys: rows of half 0, masked)
+            k.qslot = seg_slot_base(a.lt, k.bh, level, seg, true);
+            k.kslot = seg_slot_base(a.lt, k.bh, level, seg, false);
+        } else if (MODE == kLevels) {
             // (whole-block levels are never padded: N / 2 entries per level)
             const int per_level = (N / 2) / QB;
             const int level = x / per_level;
@@ -896,7 +921,8 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
             const size_t base = k.bh * (size_t)a.lt.off[a.Lv] + (size_t)a.lt.off[level] + (size_t)t * QB;
             k.ql = a.perm_q + base;
             k.kl = a.perm_k + base + k.half * BQ;
-            k.nv = BQ;
+            k.nv = QB;
+            k.nvk = BQ;
             // a block never straddles a segment (the half length is a multiple of QB)
             const int seg = t * QB / a.lt.len[level + 1];
             k.qslot = seg_slot_base(a.lt, k.bh, level, seg, true);
@@ -907,6 +933,7 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
             k.ql = a.perm_q + k.bh * N + p0;
             k.kl = a.perm_k + k.bh * N + p0;
             k.nv = min(BQ, N - p0);
+            k.nvk = k.nv;
         }
         return k;
     };
@@ -926,15 +953,19 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
 #pragma unroll
             for (int j = 0; j < PT; ++j) {
                 const int r = 64 * t + TD::row_of(j, tx);
-                ix.ktk[t][j] = (kFull || r < k.nv) ? k.kl[(uint32_t)r] : -1;
+                if constexpr (kFull) ix.ktk[t][j] = k.kl[(uint32_t)r];
+                else if constexpr (kClamp) ix.ktk[t][j] = k.kl[(uint32_t)min(r, max(k.nvk, 1) - 1)];
+                else ix.ktk[t][j] = r < k.nvk ? k.kl[(uint32_t)r] : -1;
             }
-        ix.ktok = (kFull || kloc < k.nv) ? k.kl[(uint32_t)kloc] : -1;
+        ix.ktok = (kFull || kloc < k.nvk) ? k.kl[(uint32_t)kloc] : -1;
     };
     auto indices_q = [&](const Blk& k, Idx& ix, int t) {
 #pragma unroll
         for (int j = 0; j < PT; ++j) {
             const int r = 64 * t + TD::row_of(j, tx);
-            ix.qtk[t][j] = (kFull || r < k.nv) ? k.ql[(uint32_t)r] : -1;
+            if constexpr (kFull) ix.qtk[t][j] = k.ql[(uint32_t)r];
+            else if constexpr (kClamp) ix.qtk[t][j] = k.ql[(uint32_t)min(r, k.nv - 1)];
+            else ix.qtk[t][j] = r < k.nv ? k.ql[(uint32_t)r] : -1;
         }
         const int r = 64 * t + (tx & 63);
         ix.qt1[t] = (kFull || r < k.nv) ? k.ql[(uint32_t)r] : -1;
@@ -943,7 +974,7 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
         const S* K = (const S*)a.K + bh * N * D;
 #pragma unroll
         for (int t = 0; t < NKT; ++t) {
-            if constexpr (kFull) TD::load_all(K, ix.ktk[t], rk[t], tx);
+            if constexpr (kFull || kClamp) TD::load_all(K, ix.ktk[t], rk[t], tx);
             else TD::load(K, ix.ktk[t], rk[t], tx);
         }
     };
@@ -965,7 +996,7 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
     auto qload = [&](size_t bh, const Idx& ix, int qt) {
         const S* Q = (const S*)a.Q + bh * N * D;
         const S* dO = (const S*)a.dO + bh * N * D;
-        if constexpr (kFull) {
+        if constexpr (kFull || kClamp) {
             TD::load_all(Q, ix.qtk[qt], rq, tx);
             TD::load_all(dO, ix.qtk[qt], ro, tx);
         } else {
@@ -1051,7 +1082,8 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
             TD::store(sq, rq, 0, tx);
             TD::store(so, ro, 0, tx);
             if (threadIdx.x < 64) {
-                s_l2[tx] = (kFull || ix.qt1[qt] >= 0) ? l2 : 0.f;
+                // (a short block's missing query: an infinite log denominator, P = 0)
+                s_l2[tx] = (kFull || ix.qt1[qt] >= 0) ? l2 : (kClamp ? INFINITY : 0.f);
                 s_de[tx] = de;
                 s_sc[tx] = sc;
                 s_qt[tx] = ix.qt1[qt];
@@ -1094,7 +1126,7 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
                                 dev = *(const f32x4*)&s_de[q4];
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        const bool ok = kFull || (ktok >= 0 && s_qt[q4 + i] >= 0);
+                        const bool ok = kFull || (kClamp ? ktok >= 0 : (ktok >= 0 && s_qt[q4 + i] >= 0));
                         const float P = ok ? fast_exp2(fmaf(st[i], a.tau2, -l2v[i])) : 0.f;
                         p8[4 * h2 + i] = P * scv[i];
                         z8[4 * h2 + i] = P * fmaf(scv[i], dp[i], -dev[i]);
@@ -1193,11 +1225,11 @@ __global__ __launch_bounds__(BQ * 4, (block_waves<D, BQ>())) void sparse_bwd_blo
 
 // Whole-block launch: as many workgroups as the device runs at once (cached
 // per instantiation and device), each walking its share of the blocks.
-template <class T, int D, int BQ, int MODE, int QB = BQ>
+template <class T, int D, int BQ, int MODE, int QB = BQ, bool FULL = MODE == kLevels>
 void launch_blocks(const char* name, BArgs a, int nbx, int BH, hipStream_t st)
 {
     static int resident[64] = {0};
-    auto kern = sparse_bwd_block_kernel<T, D, BQ, MODE, QB>;
+    auto kern = sparse_bwd_block_kernel<T, D, BQ, MODE, QB, FULL>;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = 0;
     int& res = resident[dev & 63];
@@ -1219,8 +1251,7 @@ void launch_blocks(const char* name, BArgs a, int nbx, int BH, hipStream_t st)
 
 bool sparse_bwd_split_dq(const Shape& s)
 {
-    return s.causal && s.bf16 && s.Lv > 0 && s.k == 256 && s.neighbors == 0 && !s.lt.padded &&
-           s.n_leaf % 256 == 0;
+    return s.causal && s.bf16 && s.Lv > 0 && s.k == 256 && s.neighbors == 0 && !s.lt.padded;
 }
 
 namespace {
@@ -1263,10 +1294,18 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
             else if constexpr (T::bytes == 2) launch_blocks<T, D, 128, kLevels>("sparse_bwd_levels", a, nbx, s.B * s.H, st);
             if ((e = hipGetLastError()) != hipSuccess) return e;
         } else if (sparse_bwd_split_dq(s)) {
-            // 256-key blocks as two 128-key halves, dQ partials in two parts
-            const int nbx = s.Lv * (s.N / 2) / 256;
-            if constexpr (T::bytes == 2)
-                launch_blocks<T, D, 128, kLevels, 256>("sparse_bwd_levels", a, nbx, s.B * s.H, st);
+            // 256-key blocks as two 128-key halves in turn; a level whose
+            // half length is not a multiple of 256 ends its lists with a short block
+            if (s.n_leaf % 256 == 0) {
+                const int nbx = s.Lv * (s.N / 2) / 256;
+                if constexpr (T::bytes == 2)
+                    launch_blocks<T, D, 128, kLevels, 256>("sparse_bwd_levels", a, nbx, s.B * s.H, st);
+            } else {
+                int nbx = 0;
+                for (int l = 0; l < s.Lv; ++l) nbx += ((s.lt.len[l + 1] + 255) / 256) << l;
+                if constexpr (T::bytes == 2)
+                    launch_blocks<T, D, 128, kLevels, 256, false>("sparse_bwd_levels", a, nbx, s.B * s.H, st);
+            }
             if ((e = hipGetLastError()) != hipSuccess) return e;
         } else {
             dim3 grid(a.lt.first[s.Lv], s.H, s.B);

@@ -52,6 +52,10 @@ SMALL = [
     _w("c-bf16-d128-k256-4096", 1, 2, 4096, 128, 256, 128, True, "bf16"),
     _w("c-bf16-d64-k256-2048-clustered", 1, 2, 2048, 64, 256, 64, True, "bf16", recipe="clustered"),
     _w("c-bf16-d128-k256-1024-h5", 1, 5, 1024, 128, 256, 64, True, "bf16"),
+    # level halves of 1500, 750 and 375 entries: every list ends in a short
+    # block (375: 119 entries, so its second key half holds no key)
+    _w("c-bf16-d128-k256-3000-short", 1, 2, 3000, 128, 256, 64, True, "bf16"),
+    _w("c-bf16-d64-k256-1500-short", 1, 2, 1500, 64, 256, 64, True, "bf16", recipe="clustered"),
 ]
 
 
