@@ -813,9 +813,10 @@ __global__ __launch_bounds__(kThreads, (two_pass_waves<T, D>())) void sparse_lea
 // the current block's last tile: its index lists at the start of the tile,
 // its V rows (into the V registers) and K rows once dP is formed, and its
 // first Q / dO tile at the end; the current block's dK, dV are stored once
-// the next block's rows are in LDS.  At the levels every block is full, so loads
-// and stores there carry no per-row branch and the compiler can wait for
-// exactly the loads it needs (its memory counter retires in order).
+// the next block's rows are in LDS.  At the levels every row load reads a
+// real row (a short block's missing rows repeat its last entry and are
+// masked), so loads there carry no per-row branch and the compiler can wait
+// for exactly the loads it needs (its memory counter retires in order).
 // ------------------------------------------------------------------------
 //
 // Blocks of QB = 256 (the levels only) are two consecutive work items of one
@@ -1262,7 +1263,8 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
     hipError_t e;
     // whole-block kernel: b in {64, 128}, blocks never straddle a segment;
     // b = 128 only where its registers fit without spilling (bf16 storage;
-    // non-causal blocks, which also form the low-rank parts, only at d_h 64)
+    // non-causal blocks, which also form the low-rank parts, only at d_h 64);
+    // causal b = 256 (sparse_bwd_split_dq) as two 128-key halves per block
     const int bq = s.k;
     const bool fits128 = T::bytes == 2 && (s.causal || D == 64);
     const bool whole = (bq == 64 || (bq == 128 && fits128)) && s.neighbors == 0 &&
