@@ -149,12 +149,15 @@ def test_backward_padded_16386():
         _check(w)
 
 
-def test_backward_is_deterministic():
-    w = _w("c-bf16-det", 1, 2, 2048, 128, 128, 128, True, "bf16", seed=63)
+@pytest.mark.parametrize("k", [128, 256], ids=["k128", "k256-halves"])
+def test_backward_is_deterministic(k):
+    """Two runs give the same bits (b = 256: the two key halves of each
+    block in turn, the first half's dQ kept in LDS)."""
+    w = _w(f"c-bf16-det-k{k}", 1, 2, 2048, 128, k, 128, True, "bf16", seed=63)
     cfg = cfg_of(w)
     inp = W.make_inputs(w, with_grad=True)
     say(f"[bwd-det] {w.name}")
     _, a = run_gpu_fwd_bwd(cfg, inp)
     _, b = run_gpu_fwd_bwd(cfg, inp)
-    for k in a:
-        assert np.array_equal(a[k], b[k]), k
+    for name in a:
+        assert np.array_equal(a[name], b[name]), name
