@@ -111,9 +111,7 @@ hipError_t launch_bwd_rows(const Shape& s, const void* dO, const float* Os, cons
                            hipStream_t st);
 // sparse backward; adds the low-rank parts (du W' for dQ and dK, the dV rows)
 // and writes dQ, dK, dV; the causal level partials part_dq / part_dk / part_dv
-// ([BH][Lv][N/2][D]) are kept in the storage dtype.  sparse_bwd_split_dq(s):
-// the level backward runs 256-key blocks as two 128-key halves in turn
-bool sparse_bwd_split_dq(const Shape& s);
+// ([BH][Lv][N/2][D]) are kept in the storage dtype
 hipError_t launch_sparse_bwd(const Shape& s, const void* Q, const void* K, const void* V,
                              const void* dO, const int32_t* perm_q, const int32_t* perm_k,
                              const float* rs, const void* du_q, const void* du_k, const void* wt_hi,

@@ -1248,14 +1248,12 @@ void launch_blocks(const char* name, BArgs a, int nbx, int BH, hipStream_t st)
     ELSAA_LAUNCH(name, kern, dim3(grid), dim3(BQ * 4), 0, st, a);
 }
 
-}  // namespace
-
-bool sparse_bwd_split_dq(const Shape& s)
+// causal b = 256 levels run as two 128-key halves per block (bf16, no
+// neighbouring blocks, no padded level)
+bool block_halves(const Shape& s)
 {
     return s.causal && s.bf16 && s.Lv > 0 && s.k == 256 && s.neighbors == 0 && !s.lt.padded;
 }
-
-namespace {
 
 template <class T, int D>
 hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
@@ -1264,7 +1262,7 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
     // whole-block kernel: b in {64, 128}, blocks never straddle a segment;
     // b = 128 only where its registers fit without spilling (bf16 storage;
     // non-causal blocks, which also form the low-rank parts, only at d_h 64);
-    // causal b = 256 (sparse_bwd_split_dq) as two 128-key halves per block
+    // causal b = 256 (block_halves) as two 128-key halves per block
     const int bq = s.k;
     const bool fits128 = T::bytes == 2 && (s.causal || D == 64);
     const bool whole = (bq == 64 || (bq == 128 && fits128)) && s.neighbors == 0 &&
@@ -1295,7 +1293,7 @@ hipError_t launch_t(const Shape& s, const BArgs& a, hipStream_t st, int parts)
             if (bq == 64) launch_blocks<T, D, 64, kLevels>("sparse_bwd_levels", a, nbx, s.B * s.H, st);
             else if constexpr (T::bytes == 2) launch_blocks<T, D, 128, kLevels>("sparse_bwd_levels", a, nbx, s.B * s.H, st);
             if ((e = hipGetLastError()) != hipSuccess) return e;
-        } else if (sparse_bwd_split_dq(s)) {
+        } else if (block_halves(s)) {
             // 256-key blocks as two 128-key halves in turn; a level whose
             // half length is not a multiple of 256 ends its lists with a short block
             if (s.n_leaf % 256 == 0) {
