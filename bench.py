@@ -10,8 +10,9 @@ per-kernel HIP events on (each launch bracketed on its own stream), which give
 the kernel durations behind the roofline of the dominant kernel and of every
 kernel (their step time is reported as profiled_ms_per_step).  Last, K calls
 of the forward and of the backward are timed on their own (medians, in
-fwd_bwd_split).  Prints one JSON line, with the CPU oracle timed on a bounded
-sample.
+fwd_bwd_split), and K replays of one step captured as a HIP graph (graph_replay:
+the same kernels without per-launch host overhead).  Prints one JSON line, with
+the CPU oracle timed on a bounded sample.
 """
 from __future__ import annotations
 
@@ -444,6 +445,30 @@ def main():
         split = {"fwd_ms_median": round(float(np.median(tf)), 4), "bwd_ms_median": round(float(np.median(tb)), 4),
                  "calls": args.steps}
 
+    # timed region 4: one step captured as a HIP graph (the library enqueues
+    # only kernels and event record / wait pairs), replayed K times
+    graph = None
+    if blk is None and not args.rules:
+        cap = torch.cuda.Stream()
+        cap.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(cap):
+            step()
+        torch.cuda.current_stream().wait_stream(cap)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step()
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        t4 = time.perf_counter()
+        for _ in range(args.steps):
+            g.replay()
+        torch.cuda.synchronize()
+        t5 = time.perf_counter()
+        graph = {"ms_per_step": round((t5 - t4) / args.steps * 1e3, 4), "steps": args.steps}
+        del g
+
     elapsed = t1 - t0
     ms_step = elapsed / args.steps * 1e3
     tokens = w.B * w.N * args.steps
@@ -532,6 +557,8 @@ def main():
     }
     if split is not None:
         result["fwd_bwd_split"] = split
+    if graph is not None:
+        result["graph_replay"] = graph
     if args.rules:
         result["config"]["rules"] = {"gate_hidden": rules_G, "lambda_rule": True}
     if not args.no_cpu_baseline:
