@@ -312,6 +312,36 @@ def dominant_unit(unit_rows: dict, per_step: dict) -> str:
     return unit_of[max(unit_of, key=lambda kn: per_step[kn])]
 
 
+def graph_replay(step, steps: int, warmup: int) -> dict:
+    """Capture one step as a HIP graph (after a warm-up call on a side stream,
+    as capture needs) and time `steps` replays; a refused capture is
+    reported instead of ending the run."""
+    import torch
+    try:
+        cap = torch.cuda.Stream()
+        cap.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(cap):
+            step()
+        torch.cuda.current_stream().wait_stream(cap)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step()
+        for _ in range(warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            g.replay()
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        del g
+        return {"ms_per_step": round((t1 - t0) / steps * 1e3, 4), "steps": steps}
+    except RuntimeError as exc:
+        torch.cuda.synchronize()
+        return {"error": str(exc)[:200]}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -447,27 +477,7 @@ def main():
 
     # timed region 4: one step captured as a HIP graph (the library enqueues
     # only kernels and event record / wait pairs), replayed K times
-    graph = None
-    if blk is None and not args.rules:
-        cap = torch.cuda.Stream()
-        cap.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(cap):
-            step()
-        torch.cuda.current_stream().wait_stream(cap)
-        torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            step()
-        for _ in range(args.warmup):
-            g.replay()
-        torch.cuda.synchronize()
-        t4 = time.perf_counter()
-        for _ in range(args.steps):
-            g.replay()
-        torch.cuda.synchronize()
-        t5 = time.perf_counter()
-        graph = {"ms_per_step": round((t5 - t4) / args.steps * 1e3, 4), "steps": args.steps}
-        del g
+    graph = graph_replay(step, args.steps, args.warmup) if blk is None and not args.rules else None
 
     elapsed = t1 - t0
     ms_step = elapsed / args.steps * 1e3
