@@ -124,7 +124,7 @@ __global__ __launch_bounds__(kProjThreads) void proj_kernel(ProjIO io, const flo
             const float* w0 = ws_h + (size_t)w * D;
             const float* w1 = ws_h + (size_t)b1 * D;
             float p0 = 0.0f, p1 = 0.0f;
-#pragma unroll 4
+#pragma unroll
             for (int e0 = 0; e0 < D; e0 += PER) {
                 const uint4 v = *(const uint4*)&sm.x[lane][e0];
                 const S* xs = (const S*)&v;
