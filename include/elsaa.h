@@ -44,6 +44,12 @@
  * everything ran on the given stream.  Concurrent elsaa_fwd calls on one
  * device share the second stream, so their sorts run one after another.
  *
+ * Graph capture: elsaa_fwd and elsaa_bwd enqueue only kernels and event
+ * record / wait pairs, so both can be captured into a HIP graph on the given
+ * stream (the second stream joins the capture through the fork event) and
+ * replayed; make one uncaptured call on the device first, which creates the
+ * second stream and caches launch geometry.
+ *
  * Errors: every entry point validates all arguments on the host before any
  * launch, so a rejected call writes nothing and leaves the stream untouched.
  * It returns a negative elsaa_status; elsaa_last_error() gives a message
